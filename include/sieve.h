@@ -1,0 +1,179 @@
+/*
+ * sieve.h -- C ABI of the MI355X (gfx950) threshold-aware IVF search library.
+ *
+ * The operation (SieveIVF, arXiv 2608.03199):
+ *   Given an IVF index over a corpus X and a query batch Q, each query q ranks
+ *   the IVF centroids by inner product (Sec. 2.3, Sec. 4.1) and probes the
+ *   partitions in that order.  A probe is a hit when the partition holds a
+ *   candidate x with <q, x> >= tau (the threshold candidate set R(q, tau),
+ *   Sec. 2.2); the query stops after W consecutive threshold-empty probes or
+ *   after nprobe_max probes (Sec. 3.5, Sec. 4.1, Algorithm 1).  The result is
+ *   the top-k of all qualifying candidates met on the way (the final MergeTopK
+ *   of Algorithm 1).  Lookahead (Sec. 4.3, Algorithm 2) dispatches, ahead of
+ *   time, every probe that the stop rule has already committed; it changes no
+ *   output (the equivalence argument of Sec. 4.3).  sieve_search_fixed is the
+ *   fixed-probe IVF baseline (Sec. 2.3): every query probes min(nprobe, nlist)
+ *   partitions.
+ *
+ * Conventions shared by every entry point:
+ *   - Return value: SIEVE_OK (0) or a negative sieve_status.  On error no
+ *     output buffer is written and sieve_last_error() describes the cause.
+ *     Argument checks run before any HIP call.
+ *   - Residency: every array argument is a DEVICE pointer on the current HIP
+ *     device (for example torch.Tensor.data_ptr() of a CUDA tensor), laid out
+ *     row-major and contiguous.  "stream" is a hipStream_t (NULL = the null
+ *     stream); all work is ordered on it.
+ *   - Similarity is the raw inner product of the stored values; the library
+ *     never renormalises.  With unit-normalised data it is the cosine.
+ *   - Centroid order: score descending, ties to the lower centroid index,
+ *     decided in double precision (an fp32 screen whose near-ties are
+ *     re-scored in fp64, so the order is that of exact-product fp64 sums).
+ *   - Result order: score descending, ties to the lower id.  Fewer than k
+ *     qualifying candidates are padded with id -1 and score -INFINITY.
+ *   - Thread safety: one search at a time per index handle (the handle caches
+ *     its device workspace).  Different handles are independent.
+ */
+#ifndef SIEVE_H
+#define SIEVE_H
+
+#include <stdint.h>
+
+#if defined(__GNUC__)
+#define SIEVE_API __attribute__((visibility("default")))
+#else
+#define SIEVE_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum sieve_status {
+  SIEVE_OK = 0,
+  SIEVE_EINVAL = -1,       /* a null required pointer, an out-of-range size or flag, bad offsets */
+  SIEVE_ENOMEM = -2,       /* device memory could not be allocated                               */
+  SIEVE_EDEVICE = -3,      /* a HIP runtime call failed (the message names it)                   */
+  SIEVE_EUNSUPPORTED = -4, /* valid, but outside this build's limits (see each function)         */
+  SIEVE_EINTERNAL = -5     /* an internal consistency check failed                               */
+} sieve_status;
+
+typedef enum sieve_dtype {
+  SIEVE_F32 = 0, /* IEEE binary32 storage, fp32 MFMA accumulate                 */
+  SIEVE_F16 = 1  /* IEEE binary16 storage, exact products, fp32 MFMA accumulate */
+} sieve_dtype;
+
+/* Any W >= min(nprobe_max, nlist) disables early stopping; this value is the
+ * conventional "infinite window". */
+#define SIEVE_W_INF 0x7fffffff
+/* Largest k accepted (the paper's k sweep reaches 50, Sec. 6.4). */
+#define SIEVE_K_MAX 64
+
+typedef struct sieve_index sieve_index; /* opaque, owned by the library */
+
+/* Counters of one search call (filled when a non-NULL pointer is passed). */
+typedef struct sieve_stats {
+  int32_t rounds;           /* bulk-synchronous scheduling rounds                          */
+  int32_t nprobe_eff;       /* min(nprobe_max, nlist)                                      */
+  int32_t scan_launches;    /* partition-scan kernel launches                              */
+  int32_t pool_retries;     /* re-runs after the candidate pool overflowed (results equal) */
+  int64_t items;            /* (query, rank) searches executed                             */
+  int64_t probes_total;     /* sum over queries of out_probes                              */
+  int64_t vectors_scanned;  /* sum over items of the probed list's length                  */
+  int64_t list_loads;       /* sum over rounds of distinct non-empty lists probed          */
+  int64_t hits;             /* qualifying (query, row) pairs found                         */
+  double scan_bytes;        /* algorithmic bytes of the scan: list rows + per-item query
+                               rows and item records + candidate records written          */
+  double scan_flops;        /* 2 * d * vectors_scanned                                     */
+  double rank_flops;        /* 2 * d * nq * nlist (the centroid screen)                    */
+  float ms_rank, ms_sched, ms_scan, ms_update, ms_finalize, ms_total; /* device time, ms */
+} sieve_stats;
+
+/*
+ * sieve_load_index -- copy an IVF index (Sec. 2.3) into a library-owned
+ * device layout.
+ *   vectors      [n * d] of dtype, partition-major: the rows of list l are
+ *                rows list_offsets[l] .. list_offsets[l+1]-1.
+ *   dtype        SIEVE_F32 or SIEVE_F16 (queries and centroids share it).
+ *   n            number of rows (>= 0); d: dimension, 8 <= d <= 4096 and a
+ *                multiple of 8 (else SIEVE_EUNSUPPORTED).
+ *   list_offsets [nlist + 1] int64: non-decreasing, list_offsets[0] == 0,
+ *                list_offsets[nlist] == n (checked on a host copy; else
+ *                SIEVE_EINVAL).  Empty lists are allowed.
+ *   nlist        1 <= nlist <= 16384 (else SIEVE_EUNSUPPORTED).
+ *   ids          [n] int64 row ids (the ids returned by searches; each id is
+ *                expected once).
+ *   centroids    [nlist * d] of dtype.
+ *   out          receives the handle; the caller's buffers may be freed on
+ *                return.  Free with sieve_free_index.
+ * Synchronous: returns once the copies are complete.
+ */
+SIEVE_API int sieve_load_index(const void* vectors, int32_t dtype, int64_t n, int32_t d,
+                               const int64_t* list_offsets, int32_t nlist, const int64_t* ids,
+                               const void* centroids, void* stream, sieve_index** out);
+
+/*
+ * sieve_search -- threshold-aware search with the consecutive-empty stop rule
+ * (Sec. 4.1), partition-major continuous batching (Sec. 4.2, Algorithm 1) and,
+ * when lookahead = 1, committed-prefix lookahead (Sec. 4.3, Algorithm 2).
+ *   queries      [nq * d] of the index dtype; nq >= 0 (0 returns at once).
+ *   exclude_ids  [nq] int64 or NULL: row id to skip for each query (a
+ *                self-join passes each query's own id); the skipped row is
+ *                neither a hit nor a result.
+ *   k            1 <= k <= SIEVE_K_MAX.
+ *   tau          similarity threshold, a candidate qualifies when its fp32
+ *                score >= tau; NaN is SIEVE_EINVAL.
+ *   W            consecutive-empty window, W >= 1 (SIEVE_W_INF: never stop).
+ *   nprobe_max   >= 1; clamped to nlist; the clamped value must be <= 2048
+ *                (else SIEVE_EUNSUPPORTED).
+ *   lookahead    0 (Algorithm 1) or 1 (Algorithm 2); outputs are identical.
+ *   out_ids      [nq * k] int64, out_scores [nq * k] float: per query the
+ *                top-k qualifying candidates, score descending then id
+ *                ascending, padded with (-1, -INFINITY).
+ *   out_probes   [nq] int32: partitions searched, including the W trailing
+ *                empty ones (min(L + W, n) with L the last hit rank).
+ *   stats        NULL or a struct to fill.
+ * Synchronous: returns once the outputs are complete on the stream.
+ */
+SIEVE_API int sieve_search(const sieve_index* idx, const void* queries, int64_t nq,
+                           const int64_t* exclude_ids, int32_t k, float tau, int32_t W,
+                           int32_t nprobe_max, int32_t lookahead, int64_t* out_ids,
+                           float* out_scores, int32_t* out_probes, sieve_stats* stats,
+                           void* stream);
+
+/*
+ * sieve_search_fixed -- fixed-probe IVF baseline (Sec. 2.3): every query
+ * probes its first min(nprobe, nlist) ranked partitions and returns the top-k
+ * of the qualifying candidates found there.  Arguments as for sieve_search;
+ * out_probes[i] = min(nprobe, nlist).  Queries are processed in chunks so
+ * that the materialised (query, rank) items fit the workspace.
+ */
+SIEVE_API int sieve_search_fixed(const sieve_index* idx, const void* queries, int64_t nq,
+                                 const int64_t* exclude_ids, int32_t k, float tau, int32_t nprobe,
+                                 int64_t* out_ids, float* out_scores, int32_t* out_probes,
+                                 sieve_stats* stats, void* stream);
+
+/*
+ * sieve_rank -- the probe order alone (Sec. 4.1): for each query, the first
+ * min(nprobe, nlist) centroid indices by inner product, descending, ties to
+ * the lower index, decided in fp64 (see the conventions above).
+ *   out_order    [nq * min(nprobe, nlist)] int32, row-major.
+ * Other arguments and limits as for sieve_search.
+ */
+SIEVE_API int sieve_rank(const sieve_index* idx, const void* queries, int64_t nq, int32_t nprobe,
+                         int32_t* out_order, void* stream);
+
+/* Release an index and its cached workspace.  NULL is a no-op. */
+SIEVE_API void sieve_free_index(sieve_index* idx);
+
+/* Message of the last failed call on this thread ("" if none).  Valid until
+ * the next call on the same thread. */
+SIEVE_API const char* sieve_last_error(void);
+
+/* Library version string. */
+SIEVE_API const char* sieve_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SIEVE_H */

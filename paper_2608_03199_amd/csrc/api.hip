@@ -1,0 +1,641 @@
+// api.hip -- the C ABI of libsieve: argument checks, the library-owned index
+// layout, the workspace, and the host side of the round loop.
+//
+// A search is:
+//   rank      fp32 MFMA centroid screen + exact fp64 order (rank.hip)
+//   admit     initial ready items: ranks 1..min(W, n) with lookahead
+//             (Algorithm 2), rank 1 without (Algorithm 1), 1..n for fixed
+//   rounds    offsets -> scatter -> tiles -> scan -> update, then one
+//             8-byte-class readback of the round counters decides whether
+//             another round is needed (the only data-dependent host sync)
+//   finalize  counting sort of the candidate pool by query, per-query top-k
+// Fixed probing runs the same kernels with every rank admitted up front, in
+// query chunks, without updates and without per-chunk syncs.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "sieve_internal.h"
+
+namespace sieve {
+size_t rank_select_lds(int32_t nlist, int32_t cap);
+}
+
+using namespace sieve;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIP_TRY(expr)                                                                  \
+  do {                                                                                 \
+    hipError_t e_ = (expr);                                                            \
+    if (e_ != hipSuccess)                                                              \
+      return fail(e_ == hipErrorOutOfMemory ? SIEVE_ENOMEM : SIEVE_EDEVICE, "%s: %s (%s)", \
+                  #expr, hipGetErrorString(e_), __func__);                             \
+  } while (0)
+
+struct Buf {
+  void* p = nullptr;
+  size_t bytes = 0;
+};
+
+int ensure(Buf& b, size_t bytes) {
+  if (bytes == 0) bytes = 16;
+  if (b.bytes >= bytes) return SIEVE_OK;
+  if (b.p) (void)hipFree(b.p);
+  b.p = nullptr;
+  b.bytes = 0;
+  hipError_t e = hipMalloc(&b.p, bytes);
+  if (e != hipSuccess) {
+    b.p = nullptr;
+    (void)hipGetLastError();
+    return fail(SIEVE_ENOMEM, "hipMalloc of %zu bytes failed: %s", bytes, hipGetErrorString(e));
+  }
+  b.bytes = bytes;
+  return SIEVE_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+constexpr int kEvents = 6;
+
+}  // namespace
+
+struct sieve_index {
+  int dtype = 0;
+  int64_t n = 0;
+  int d = 0;
+  int nlist = 0;
+  int device = 0;
+  int cus = 256;
+  void* vectors = nullptr;
+  int64_t* offsets = nullptr;
+  int64_t* ids = nullptr;
+  void* centroids = nullptr;
+  std::vector<int64_t> h_offsets;
+  int64_t max_list = 0;
+  double cmax = 0.0;
+  // workspace, grown on demand
+  Buf scores, P, items, bucket, tiles, cnt, item_off, cursor, tile_off, rc, state_a, state_b,
+      lmax, hcount, hoff, hcur, scan_tmp, pool, pool_sorted;
+  int64_t pool_cap = 0;
+  RoundCounters* rc_host = nullptr;
+  hipEvent_t ev[kEvents] = {};
+  bool events = false;
+};
+
+namespace {
+
+int elem_bytes(int dtype) { return dtype == SIEVE_F32 ? 4 : 2; }
+
+double host_elem(const void* base, int dtype, int64_t i) {
+  if (dtype == SIEVE_F32) return (double)((const float*)base)[i];
+  return (double)((const _Float16*)base)[i];
+}
+
+int alloc_events(sieve_index* ix) {
+  if (ix->events) return SIEVE_OK;
+  for (int i = 0; i < kEvents; ++i) HIP_TRY(hipEventCreate(&ix->ev[i]));
+  ix->events = true;
+  return SIEVE_OK;
+}
+
+float elapsed(sieve_index* ix, int a, int b) {
+  float ms = 0.f;
+  if (hipEventElapsedTime(&ms, ix->ev[a], ix->ev[b]) != hipSuccess) {
+    (void)hipGetLastError();
+    return 0.f;
+  }
+  return ms;
+}
+
+// Tunables of the scan decomposition (they never change results).
+int row_chunk_for(const sieve_index* ix) {
+  (void)ix;
+  return 512;
+}
+
+int scan_grid(const sieve_index* ix, int tile_q) {
+  const size_t lds = scan_lds_bytes(ix->dtype, ix->d, tile_q) + 4096;
+  int per_cu = (int)((160 * 1024) / lds);
+  per_cu = per_cu < 1 ? 1 : (per_cu > 4 ? 4 : per_cu);
+  return ix->cus * per_cu;
+}
+
+struct SearchPlan {
+  int n;            // effective probes limit
+  int mode;         // 0 lookahead, 1 basic, 2 fixed
+  int W;
+  int k;
+  float tau;
+  int64_t nq;
+  int tile_q;
+  int row_chunk;
+  int64_t rank_chunk;  // queries per centroid-screen chunk
+  int64_t fix_chunk;   // queries per fixed-probe chunk
+  int64_t item_cap;
+};
+
+int check_common(const sieve_index* ix, const void* queries, int64_t nq, int32_t k, float tau,
+                 int64_t* out_ids, float* out_scores, int32_t* out_probes) {
+  if (!ix) return fail(SIEVE_EINVAL, "index handle is NULL");
+  if (nq < 0) return fail(SIEVE_EINVAL, "nq = %lld is negative", (long long)nq);
+  if (k < 1 || k > SIEVE_K_MAX) return fail(SIEVE_EINVAL, "k = %d outside [1, %d]", k, SIEVE_K_MAX);
+  if (isnan(tau)) return fail(SIEVE_EINVAL, "tau is NaN");
+  if (nq > 0 && (!queries || !out_ids || !out_scores || !out_probes))
+    return fail(SIEVE_EINVAL, "queries and every output pointer must be non-NULL when nq > 0");
+  if (nq > 0 && !aligned16(queries)) return fail(SIEVE_EINVAL, "queries must be 16-byte aligned");
+  if (nq > (int64_t)INT32_MAX / 2) return fail(SIEVE_EUNSUPPORTED, "nq = %lld too large", (long long)nq);
+  return SIEVE_OK;
+}
+
+int grow_workspace(sieve_index* ix, const SearchPlan& pl) {
+  const int64_t nq = pl.nq;
+  const int n = pl.n;
+  const int64_t rank_rows = pl.mode == 2 ? pl.fix_chunk : nq;
+  int st;
+  if ((st = ensure(ix->scores, (size_t)pl.rank_chunk * ix->nlist * sizeof(float)))) return st;
+  if ((st = ensure(ix->P, (size_t)rank_rows * n * sizeof(int32_t)))) return st;
+  if ((st = ensure(ix->items, (size_t)pl.item_cap * sizeof(Item)))) return st;
+  if ((st = ensure(ix->bucket, (size_t)pl.item_cap * sizeof(Item)))) return st;
+  // tiles: sum_p ceil(c_p / tq) * ceil(len_p / rc) <= items * max_chunks / tq + lists + rows / rc
+  const int64_t max_ch = (ix->max_list + pl.row_chunk - 1) / pl.row_chunk;
+  const int64_t tile_cap = pl.item_cap / pl.tile_q * (max_ch > 0 ? max_ch : 1) + ix->nlist +
+                           ix->n / pl.row_chunk + 16;
+  if (tile_cap > INT32_MAX) return fail(SIEVE_EUNSUPPORTED, "tile count bound overflows int32");
+  if ((st = ensure(ix->tiles, (size_t)tile_cap * sizeof(Tile)))) return st;
+  const size_t nl = (size_t)ix->nlist;
+  if ((st = ensure(ix->cnt, nl * 4)) || (st = ensure(ix->item_off, nl * 4)) ||
+      (st = ensure(ix->cursor, nl * 4)) || (st = ensure(ix->tile_off, nl * 4)))
+    return st;
+  if ((st = ensure(ix->rc, sizeof(RoundCounters)))) return st;
+  const size_t qn = (size_t)nq * 4;
+  if ((st = ensure(ix->state_a, qn)) || (st = ensure(ix->state_b, qn)) ||
+      (st = ensure(ix->lmax, qn)) || (st = ensure(ix->hcount, qn)) ||
+      (st = ensure(ix->hoff, qn)) || (st = ensure(ix->hcur, qn)))
+    return st;
+  if ((st = ensure(ix->scan_tmp, exclusive_scan_tmp_elems(nq) * 4))) return st;
+  if (ix->pool_cap == 0) {
+    int64_t cap = nq * 16;
+    if (cap < (1 << 20)) cap = 1 << 20;
+    ix->pool_cap = cap;
+  }
+  if ((st = ensure(ix->pool, (size_t)ix->pool_cap * sizeof(Hit)))) return st;
+  if ((st = ensure(ix->pool_sorted, (size_t)ix->pool_cap * sizeof(Hit)))) return st;
+  if (!ix->rc_host) HIP_TRY(hipHostMalloc((void**)&ix->rc_host, sizeof(RoundCounters), 0));
+  return SIEVE_OK;
+}
+
+// Centroid order of queries [q0, q0 + cnt) into P (row-major [cnt][n]).
+int rank_queries(sieve_index* ix, const void* queries, int64_t q0, int64_t cnt,
+                 const SearchPlan& pl, int32_t* P, hipStream_t s) {
+  RoundCounters* rc = (RoundCounters*)ix->rc.p;
+  for (int64_t a = 0; a < cnt; a += pl.rank_chunk) {
+    const int32_t c = (int32_t)((cnt - a) < pl.rank_chunk ? (cnt - a) : pl.rank_chunk);
+    HIP_TRY(launch_rank_scores(ix->dtype, queries, q0 + a, c, ix->centroids, ix->nlist, ix->d,
+                               (float*)ix->scores.p, s));
+    HIP_TRY(launch_rank_select(ix->dtype, queries, q0 + a, c, ix->centroids, ix->nlist, ix->d,
+                               (const float*)ix->scores.p, pl.n, ix->cmax, P + a * pl.n, rc, s));
+  }
+  return SIEVE_OK;
+}
+
+ScanArgs make_scan_args(sieve_index* ix, const void* queries, const int64_t* exclude,
+                        const SearchPlan& pl) {
+  ScanArgs a;
+  RoundCounters* rc = (RoundCounters*)ix->rc.p;
+  a.vectors = ix->vectors;
+  a.list_offsets = ix->offsets;
+  a.ids = ix->ids;
+  a.queries = queries;
+  a.exclude = exclude;
+  a.bucket = (const Item*)ix->bucket.p;
+  a.tiles = (const Tile*)ix->tiles.p;
+  a.rc = rc;
+  a.lmax = (int32_t*)ix->lmax.p;
+  a.hcount = (int32_t*)ix->hcount.p;
+  a.pool = (Hit*)ix->pool.p;
+  a.pool_count = &rc->hits;
+  a.pool_cap = ix->pool_cap;
+  a.d = ix->d;
+  a.row_chunk = pl.row_chunk;
+  a.tile_q = pl.tile_q;
+  a.tau = pl.tau;
+  return a;
+}
+
+// One scheduling round over n_items ready items (already histogrammed).
+int run_round(sieve_index* ix, const ScanArgs& sa, int n_items, int64_t q0, const int32_t* P,
+              const SearchPlan& pl, hipStream_t s, bool timed, float* ms_sched, float* ms_scan) {
+  RoundCounters* rc = (RoundCounters*)ix->rc.p;
+  if (timed) HIP_TRY(hipEventRecord(ix->ev[0], s));
+  HIP_TRY(launch_sched_offsets((const int32_t*)ix->cnt.p, ix->offsets, ix->nlist, pl.row_chunk,
+                               pl.tile_q, (int32_t*)ix->item_off.p, (int32_t*)ix->cursor.p,
+                               (int32_t*)ix->tile_off.p, rc, s));
+  HIP_TRY(launch_sched_scatter((const Item*)ix->items.p, n_items, P, pl.n, (int32_t)q0,
+                               (int32_t*)ix->cursor.p, (Item*)ix->bucket.p, s));
+  HIP_TRY(launch_sched_tiles((int32_t*)ix->cnt.p, (const int32_t*)ix->item_off.p,
+                             (const int32_t*)ix->tile_off.p, ix->offsets, ix->nlist, pl.row_chunk,
+                             pl.tile_q, (Tile*)ix->tiles.p, s));
+  if (timed) HIP_TRY(hipEventRecord(ix->ev[1], s));
+  HIP_TRY(launch_scan(ix->dtype, sa, scan_grid(ix, pl.tile_q), s));
+  if (timed) HIP_TRY(hipEventRecord(ix->ev[2], s));
+  (void)ms_sched;
+  (void)ms_scan;
+  return SIEVE_OK;
+}
+
+int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t* exclude,
+                SearchPlan pl, int64_t* out_ids, float* out_scores, int32_t* out_probes,
+                sieve_stats* stats, hipStream_t s) {
+  int st;
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev != ix->device)
+    return fail(SIEVE_EINVAL, "current device %d differs from the index's device %d", dev,
+                ix->device);
+  const bool timed = stats != nullptr;
+  if (timed && (st = alloc_events(ix))) return st;
+  if ((st = grow_workspace(ix, pl))) return st;
+
+  RoundCounters* rc = (RoundCounters*)ix->rc.p;
+  const int e = elem_bytes(ix->dtype);
+  const ScanArgs sa0 = make_scan_args(ix, queries, exclude, pl);
+
+  for (int attempt = 0;; ++attempt) {
+    float ms_rank = 0, ms_sched = 0, ms_scan = 0, ms_update = 0, ms_fin = 0;
+    int rounds = 0, scan_launches = 0;
+    int64_t items_total = 0;
+    ScanArgs sa = sa0;
+    sa.pool = (Hit*)ix->pool.p;
+    sa.pool_cap = ix->pool_cap;
+
+    if (timed) HIP_TRY(hipEventRecord(ix->ev[4], s));
+    HIP_TRY(launch_zero_bytes(rc, sizeof(RoundCounters), s));
+    HIP_TRY(launch_fill_i32((int32_t*)ix->cnt.p, ix->nlist, 0, s));
+    HIP_TRY(launch_fill_i32((int32_t*)ix->hcount.p, nq, 0, s));
+    int32_t* P = (int32_t*)ix->P.p;
+
+    if (pl.mode != 2) {
+      if (timed) HIP_TRY(hipEventRecord(ix->ev[0], s));
+      if ((st = rank_queries(ix, queries, 0, nq, pl, P, s))) return st;
+      const int s0 = pl.mode == 0 ? (pl.W < pl.n ? pl.W : pl.n) : 1;
+      HIP_TRY(launch_emit_initial(P, pl.n, nq, 0, s0, pl.mode, (Item*)ix->items.p,
+                                  (int32_t*)ix->cnt.p, (int32_t*)ix->state_a.p,
+                                  (int32_t*)ix->state_b.p, (int32_t*)ix->lmax.p, s));
+      if (timed) {
+        HIP_TRY(hipEventRecord(ix->ev[1], s));
+        HIP_TRY(hipEventSynchronize(ix->ev[1]));
+        ms_rank += elapsed(ix, 0, 1);
+      }
+      int64_t n_items = nq * s0;
+      while (n_items > 0) {
+        if ((st = run_round(ix, sa, (int)n_items, 0, P, pl, s, timed, &ms_sched, &ms_scan)))
+          return st;
+        if (pl.mode == 0)
+          HIP_TRY(launch_update_lookahead(nq, P, pl.n, pl.W, (int32_t*)ix->state_a.p,
+                                          (int32_t*)ix->lmax.p, (Item*)ix->items.p,
+                                          (int32_t*)ix->cnt.p, rc, s));
+        else
+          HIP_TRY(launch_update_basic(nq, P, pl.n, pl.W, (int32_t*)ix->state_a.p,
+                                      (int32_t*)ix->state_b.p, (int32_t*)ix->lmax.p,
+                                      (Item*)ix->items.p, (int32_t*)ix->cnt.p, rc, s));
+        if (timed) HIP_TRY(hipEventRecord(ix->ev[3], s));
+        HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipStreamSynchronize(s));
+        if (timed) {
+          ms_sched += elapsed(ix, 0, 1);
+          ms_scan += elapsed(ix, 1, 2);
+          ms_update += elapsed(ix, 2, 3);
+        }
+        items_total += n_items;
+        ++rounds;
+        ++scan_launches;
+        if (ix->rc_host->rank_error)
+          return fail(SIEVE_EUNSUPPORTED,
+                      "more than %d centroids tie within the fp32 screening bound at a rank "
+                      "boundary", kMaxCand);
+        n_items = ix->rc_host->new_items;
+        if (n_items > pl.item_cap)
+          return fail(SIEVE_EINTERNAL, "round emitted %lld items, capacity %lld",
+                      (long long)n_items, (long long)pl.item_cap);
+      }
+    } else {
+      for (int64_t q0 = 0; q0 < nq; q0 += pl.fix_chunk) {
+        const int64_t c = (nq - q0) < pl.fix_chunk ? (nq - q0) : pl.fix_chunk;
+        if (timed) HIP_TRY(hipEventRecord(ix->ev[0], s));
+        if ((st = rank_queries(ix, queries, q0, c, pl, P, s))) return st;
+        HIP_TRY(launch_emit_initial(P, pl.n, c, (int32_t)q0, pl.n, 2, (Item*)ix->items.p,
+                                    (int32_t*)ix->cnt.p, nullptr, nullptr, nullptr, s));
+        if (timed) HIP_TRY(hipEventRecord(ix->ev[1], s));
+        if (timed) HIP_TRY(hipEventSynchronize(ix->ev[1]));
+        if (timed) ms_rank += elapsed(ix, 0, 1);
+        if ((st = run_round(ix, sa, (int)(c * pl.n), q0, P, pl, s, timed, &ms_sched, &ms_scan)))
+          return st;
+        if (timed) {
+          HIP_TRY(hipEventSynchronize(ix->ev[2]));
+          ms_sched += elapsed(ix, 0, 1);
+          ms_scan += elapsed(ix, 1, 2);
+        }
+        items_total += c * pl.n;
+        ++rounds;
+        ++scan_launches;
+      }
+      HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
+      HIP_TRY(hipStreamSynchronize(s));
+      if (ix->rc_host->rank_error)
+        return fail(SIEVE_EUNSUPPORTED,
+                    "more than %d centroids tie within the fp32 screening bound at a rank "
+                    "boundary", kMaxCand);
+    }
+
+    const int64_t hits = (int64_t)ix->rc_host->hits;
+    if (hits > ix->pool_cap) {
+      // the pool overflowed: grow it and run again (the search is deterministic)
+      ix->pool_cap = hits + hits / 8 + 1024;
+      if ((st = ensure(ix->pool, (size_t)ix->pool_cap * sizeof(Hit)))) return st;
+      if ((st = ensure(ix->pool_sorted, (size_t)ix->pool_cap * sizeof(Hit)))) return st;
+      if (attempt >= 2) return fail(SIEVE_EINTERNAL, "candidate pool kept overflowing");
+      if (stats) stats->pool_retries = attempt + 1;
+      continue;
+    }
+
+    // finalize: group the pool by query, then per-query top-k
+    if (timed) HIP_TRY(hipEventRecord(ix->ev[0], s));
+    HIP_TRY(launch_exclusive_scan((const int32_t*)ix->hcount.p, (int32_t*)ix->hoff.p,
+                                  (int32_t*)ix->hcur.p, nq, (int32_t*)ix->scan_tmp.p, s));
+    HIP_TRY(launch_pool_scatter((const Hit*)ix->pool.p, hits, (int32_t*)ix->hcur.p,
+                                (Hit*)ix->pool_sorted.p, s));
+    const int32_t* probes_src = pl.mode == 0   ? (const int32_t*)ix->state_a.p
+                                : pl.mode == 1 ? (const int32_t*)ix->state_b.p
+                                               : nullptr;
+    HIP_TRY(launch_topk(nq, pl.k, (const Hit*)ix->pool_sorted.p, (const int32_t*)ix->hoff.p,
+                        (const int32_t*)ix->hcount.p, probes_src, pl.n, out_ids, out_scores,
+                        out_probes, rc, s));
+    if (timed) HIP_TRY(hipEventRecord(ix->ev[1], s));
+    if (timed) HIP_TRY(hipEventRecord(ix->ev[5], s));
+    HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    if (timed) {
+      ms_fin = elapsed(ix, 0, 1);
+      const RoundCounters& h = *ix->rc_host;
+      const double eb = (double)ix->d * e;
+      stats->rounds = rounds;
+      stats->nprobe_eff = pl.n;
+      stats->scan_launches = scan_launches;
+      stats->items = items_total;
+      stats->probes_total = (int64_t)h.probes;
+      stats->vectors_scanned = (int64_t)h.item_rows;
+      stats->list_loads = (int64_t)h.list_loads;
+      stats->hits = (int64_t)h.hits;
+      stats->scan_bytes = (double)h.list_rows * eb + (double)items_total * (eb + sizeof(Item)) +
+                          (double)h.hits * sizeof(Hit);
+      stats->scan_flops = 2.0 * (double)ix->d * (double)h.item_rows;
+      stats->rank_flops = 2.0 * (double)ix->d * (double)nq * (double)ix->nlist;
+      stats->ms_rank = ms_rank;
+      stats->ms_sched = ms_sched;
+      stats->ms_scan = ms_scan;
+      stats->ms_update = ms_update;
+      stats->ms_finalize = ms_fin;
+      stats->ms_total = elapsed(ix, 4, 5);
+    }
+    return SIEVE_OK;
+  }
+}
+
+int plan_search(const sieve_index* ix, int64_t nq, int32_t k, float tau, int32_t W,
+                int32_t nprobe, int mode, SearchPlan* pl) {
+  pl->n = nprobe < ix->nlist ? nprobe : ix->nlist;
+  if (pl->n > kMaxRanks)
+    return fail(SIEVE_EUNSUPPORTED, "min(nprobe, nlist) = %d exceeds %d", pl->n, kMaxRanks);
+  pl->mode = mode;
+  pl->W = W;
+  pl->k = k;
+  pl->tau = tau;
+  pl->nq = nq;
+  pl->tile_q = tile_rows(ix->dtype, ix->d);
+  pl->row_chunk = row_chunk_for(ix);
+  int64_t rc = (int64_t)(256ll << 20) / ((int64_t)ix->nlist * 4);
+  if (rc < 64) rc = 64;
+  pl->rank_chunk = nq < rc ? nq : rc;
+  if (pl->rank_chunk < 1) pl->rank_chunk = 1;
+  if (mode == 2) {
+    int64_t fc = (int64_t)(64ll << 20) / pl->n;  // <= 64M items per chunk
+    if (fc < 1) fc = 1;
+    pl->fix_chunk = nq < fc ? nq : fc;
+    if (pl->fix_chunk < 1) pl->fix_chunk = 1;
+    pl->item_cap = pl->fix_chunk * pl->n;
+    if (pl->rank_chunk > pl->fix_chunk) pl->rank_chunk = pl->fix_chunk;
+  } else {
+    pl->fix_chunk = 0;
+    const int s0 = mode == 0 ? (W < pl->n ? W : pl->n) : 1;
+    pl->item_cap = nq * (int64_t)s0;
+    if (pl->item_cap > INT32_MAX)
+      return fail(SIEVE_EUNSUPPORTED, "nq * min(W, n) = %lld exceeds int32", (long long)pl->item_cap);
+  }
+  if (pl->item_cap < 1) pl->item_cap = 1;
+  return SIEVE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+SIEVE_API const char* sieve_last_error(void) { return g_err.c_str(); }
+
+SIEVE_API const char* sieve_version(void) { return "sieve-mi355x 0.1 (gfx950)"; }
+
+SIEVE_API int sieve_load_index(const void* vectors, int32_t dtype, int64_t n, int32_t d,
+                               const int64_t* list_offsets, int32_t nlist, const int64_t* ids,
+                               const void* centroids, void* stream, sieve_index** out) {
+  g_err.clear();
+  if (!out) return fail(SIEVE_EINVAL, "out is NULL");
+  if (dtype != SIEVE_F32 && dtype != SIEVE_F16) return fail(SIEVE_EINVAL, "bad dtype %d", dtype);
+  if (n < 0) return fail(SIEVE_EINVAL, "n = %lld is negative", (long long)n);
+  if (d < 1 || nlist < 1) return fail(SIEVE_EINVAL, "d and nlist must be >= 1");
+  if (!list_offsets || !centroids || (n > 0 && (!vectors || !ids)))
+    return fail(SIEVE_EINVAL, "a required pointer is NULL");
+  if (d % 8 != 0 || d > kMaxD)
+    return fail(SIEVE_EUNSUPPORTED, "d = %d: must be a multiple of 8 and <= %d", d, kMaxD);
+  if (nlist > kMaxNlist) return fail(SIEVE_EUNSUPPORTED, "nlist = %d exceeds %d", nlist, kMaxNlist);
+  if ((n > 0 && !aligned16(vectors)) || !aligned16(centroids) || !aligned16(list_offsets) ||
+      (n > 0 && !aligned16(ids)))
+    return fail(SIEVE_EINVAL, "arrays must be 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  std::vector<int64_t> off(nlist + 1);
+  HIP_TRY(hipMemcpyAsync(off.data(), list_offsets, sizeof(int64_t) * (nlist + 1),
+                         hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  if (off[0] != 0 || off[nlist] != n)
+    return fail(SIEVE_EINVAL, "list_offsets must start at 0 and end at n");
+  int64_t max_list = 0;
+  for (int c = 0; c < nlist; ++c) {
+    const int64_t len = off[c + 1] - off[c];
+    if (len < 0) return fail(SIEVE_EINVAL, "list_offsets decrease at list %d", c);
+    if (len > INT32_MAX / 2) return fail(SIEVE_EUNSUPPORTED, "list %d is too long", c);
+    if (len > max_list) max_list = len;
+  }
+  const int e = elem_bytes(dtype);
+  sieve_index* ix = new sieve_index();
+  ix->dtype = dtype;
+  ix->n = n;
+  ix->d = d;
+  ix->nlist = nlist;
+  ix->device = dev;
+  ix->h_offsets = off;
+  ix->max_list = max_list;
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, dev) == hipSuccess && prop.multiProcessorCount > 0)
+    ix->cus = prop.multiProcessorCount;
+  auto bail = [&](int code) {
+    sieve_free_index(ix);
+    return code;
+  };
+  const size_t vbytes = (size_t)n * d * e, cbytes = (size_t)nlist * d * e;
+  hipError_t err;
+  if ((err = hipMalloc(&ix->vectors, vbytes ? vbytes : 16)) != hipSuccess ||
+      (err = hipMalloc((void**)&ix->offsets, sizeof(int64_t) * (nlist + 1))) != hipSuccess ||
+      (err = hipMalloc((void**)&ix->ids, n > 0 ? sizeof(int64_t) * n : 16)) != hipSuccess ||
+      (err = hipMalloc(&ix->centroids, cbytes)) != hipSuccess) {
+    (void)hipGetLastError();
+    return bail(fail(SIEVE_ENOMEM, "index allocation failed: %s", hipGetErrorString(err)));
+  }
+  if ((vbytes && (err = hipMemcpyAsync(ix->vectors, vectors, vbytes, hipMemcpyDeviceToDevice, s)) != hipSuccess) ||
+      (err = hipMemcpyAsync(ix->offsets, list_offsets, sizeof(int64_t) * (nlist + 1), hipMemcpyDeviceToDevice, s)) != hipSuccess ||
+      (n > 0 && (err = hipMemcpyAsync(ix->ids, ids, sizeof(int64_t) * n, hipMemcpyDeviceToDevice, s)) != hipSuccess) ||
+      (err = hipMemcpyAsync(ix->centroids, centroids, cbytes, hipMemcpyDeviceToDevice, s)) != hipSuccess)
+    return bail(fail(SIEVE_EDEVICE, "index copy failed: %s", hipGetErrorString(err)));
+  std::vector<uint8_t> hc(cbytes);
+  if ((err = hipMemcpyAsync(hc.data(), centroids, cbytes, hipMemcpyDeviceToHost, s)) != hipSuccess ||
+      (err = hipStreamSynchronize(s)) != hipSuccess)
+    return bail(fail(SIEVE_EDEVICE, "index copy failed: %s", hipGetErrorString(err)));
+  double cmax = 0.0;
+  for (int c = 0; c < nlist; ++c) {
+    double ss = 0.0;
+    for (int t = 0; t < d; ++t) {
+      const double v = host_elem(hc.data(), dtype, (int64_t)c * d + t);
+      ss += v * v;
+    }
+    if (ss > cmax) cmax = ss;
+  }
+  ix->cmax = sqrt(cmax) * (1.0 + 1e-12);
+  if (!isfinite(ix->cmax)) return bail(fail(SIEVE_EINVAL, "centroids contain inf or NaN"));
+  *out = ix;
+  return SIEVE_OK;
+}
+
+SIEVE_API void sieve_free_index(sieve_index* ix) {
+  if (!ix) return;
+  Buf* bufs[] = {&ix->scores, &ix->P, &ix->items, &ix->bucket, &ix->tiles, &ix->cnt,
+                 &ix->item_off, &ix->cursor, &ix->tile_off, &ix->rc, &ix->state_a,
+                 &ix->state_b, &ix->lmax, &ix->hcount, &ix->hoff, &ix->hcur, &ix->scan_tmp,
+                 &ix->pool, &ix->pool_sorted};
+  for (Buf* b : bufs)
+    if (b->p) (void)hipFree(b->p);
+  if (ix->vectors) (void)hipFree(ix->vectors);
+  if (ix->offsets) (void)hipFree(ix->offsets);
+  if (ix->ids) (void)hipFree(ix->ids);
+  if (ix->centroids) (void)hipFree(ix->centroids);
+  if (ix->rc_host) (void)hipHostFree(ix->rc_host);
+  if (ix->events)
+    for (int i = 0; i < kEvents; ++i) (void)hipEventDestroy(ix->ev[i]);
+  delete ix;
+}
+
+SIEVE_API int sieve_search(const sieve_index* idx, const void* queries, int64_t nq,
+                           const int64_t* exclude_ids, int32_t k, float tau, int32_t W,
+                           int32_t nprobe_max, int32_t lookahead, int64_t* out_ids,
+                           float* out_scores, int32_t* out_probes, sieve_stats* stats,
+                           void* stream) {
+  g_err.clear();
+  int st = check_common(idx, queries, nq, k, tau, out_ids, out_scores, out_probes);
+  if (st) return st;
+  if (W < 1) return fail(SIEVE_EINVAL, "W = %d must be >= 1", W);
+  if (nprobe_max < 1) return fail(SIEVE_EINVAL, "nprobe_max = %d must be >= 1", nprobe_max);
+  if (lookahead != 0 && lookahead != 1) return fail(SIEVE_EINVAL, "lookahead must be 0 or 1");
+  sieve_index* ix = const_cast<sieve_index*>(idx);
+  SearchPlan pl;
+  if ((st = plan_search(ix, nq, k, tau, W, nprobe_max, lookahead ? 0 : 1, &pl))) return st;
+  if (stats) memset(stats, 0, sizeof(*stats));
+  if (nq == 0) {
+    if (stats) stats->nprobe_eff = pl.n;
+    return SIEVE_OK;
+  }
+  return search_impl(ix, queries, nq, exclude_ids, pl, out_ids, out_scores, out_probes, stats,
+                     (hipStream_t)stream);
+}
+
+SIEVE_API int sieve_rank(const sieve_index* idx, const void* queries, int64_t nq, int32_t nprobe,
+                         int32_t* out_order, void* stream) {
+  g_err.clear();
+  if (!idx) return fail(SIEVE_EINVAL, "index handle is NULL");
+  if (nq < 0) return fail(SIEVE_EINVAL, "nq is negative");
+  if (nprobe < 1) return fail(SIEVE_EINVAL, "nprobe = %d must be >= 1", nprobe);
+  if (nq > 0 && (!queries || !out_order))
+    return fail(SIEVE_EINVAL, "queries and out_order must be non-NULL when nq > 0");
+  if (nq > 0 && !aligned16(queries)) return fail(SIEVE_EINVAL, "queries must be 16-byte aligned");
+  if (nq > (int64_t)INT32_MAX / 2) return fail(SIEVE_EUNSUPPORTED, "nq too large");
+  sieve_index* ix = const_cast<sieve_index*>(idx);
+  SearchPlan pl;
+  int st;
+  if ((st = plan_search(ix, nq, 1, 0.f, 1, nprobe, 1, &pl))) return st;
+  if (nq == 0) return SIEVE_OK;
+  if ((int64_t)nq * pl.n > (int64_t)INT32_MAX * 8)
+    return fail(SIEVE_EUNSUPPORTED, "nq * nprobe too large");
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev != ix->device) return fail(SIEVE_EINVAL, "current device differs from the index's");
+  hipStream_t s = (hipStream_t)stream;
+  if ((st = ensure(ix->scores, (size_t)pl.rank_chunk * ix->nlist * sizeof(float)))) return st;
+  if ((st = ensure(ix->rc, sizeof(RoundCounters)))) return st;
+  if (!ix->rc_host) HIP_TRY(hipHostMalloc((void**)&ix->rc_host, sizeof(RoundCounters), 0));
+  RoundCounters* rc = (RoundCounters*)ix->rc.p;
+  HIP_TRY(launch_zero_bytes(rc, sizeof(RoundCounters), s));
+  if ((st = rank_queries(ix, queries, 0, nq, pl, out_order, s))) return st;
+  HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  if (ix->rc_host->rank_error)
+    return fail(SIEVE_EUNSUPPORTED,
+                "more than %d centroids tie within the fp32 screening bound at a rank boundary",
+                kMaxCand);
+  return SIEVE_OK;
+}
+
+SIEVE_API int sieve_search_fixed(const sieve_index* idx, const void* queries, int64_t nq,
+                                 const int64_t* exclude_ids, int32_t k, float tau, int32_t nprobe,
+                                 int64_t* out_ids, float* out_scores, int32_t* out_probes,
+                                 sieve_stats* stats, void* stream) {
+  g_err.clear();
+  int st = check_common(idx, queries, nq, k, tau, out_ids, out_scores, out_probes);
+  if (st) return st;
+  if (nprobe < 1) return fail(SIEVE_EINVAL, "nprobe = %d must be >= 1", nprobe);
+  sieve_index* ix = const_cast<sieve_index*>(idx);
+  SearchPlan pl;
+  if ((st = plan_search(ix, nq, k, tau, SIEVE_W_INF, nprobe, 2, &pl))) return st;
+  if (stats) memset(stats, 0, sizeof(*stats));
+  if (nq == 0) {
+    if (stats) stats->nprobe_eff = pl.n;
+    return SIEVE_OK;
+  }
+  return search_impl(ix, queries, nq, exclude_ids, pl, out_ids, out_scores, out_probes, stats,
+                     (hipStream_t)stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,148 @@
+// mfma_tile.h -- the query-tile x row-block inner product engine on gfx950 MFMA.
+//
+// A work-group of 4 wave64 scores up to 16*QB query rows (staged once in LDS)
+// against a run of stored rows (list vectors or centroids) streamed straight
+// from HBM into registers, 16 rows per wave at a time.  Each output block is
+// 16 queries x 16 rows, accumulated in fp32 by
+//   fp32 data: v_mfma_f32_16x16x4_f32   (4 MFMAs per 16-dimension chunk)
+//   fp16 data: v_mfma_f32_16x16x32_f16  (1 MFMA per 32-dimension chunk)
+// The MFMA operand layout gives lane l the (row l%16, k-group l/16) element;
+// the k index is remapped so that every lane reads one contiguous 16-byte
+// segment per chunk from both operands (the dot product is a sum over k, so
+// any bijection applied to both operands leaves it unchanged, and the fixed
+// order of the chunk loop makes every score independent of tiling).  The
+// 16x16 accumulator puts output (row 4*(l/16)+r, column l%16) in element r of
+// lane l.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "sieve_internal.h"
+
+namespace sieve {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <int DT>
+struct DTraits;
+template <>
+struct DTraits<SIEVE_F32> {
+  static constexpr int kElem = 4;
+  static constexpr int kSegDims = 4;     // dims per 16-byte segment
+  static constexpr int kChunkDims = 16;  // dims consumed by the 4 lane groups per chunk
+};
+template <>
+struct DTraits<SIEVE_F16> {
+  static constexpr int kElem = 2;
+  static constexpr int kSegDims = 8;
+  static constexpr int kChunkDims = 32;
+};
+
+__device__ __forceinline__ f32x4 mma_chunk_f32(u32x4 a, u32x4 b, f32x4 acc) {
+  // whole-vector casts: element-wise casts of vector lanes are not reliable here
+  const f32x4 af = __builtin_bit_cast(f32x4, a);
+  const f32x4 bf = __builtin_bit_cast(f32x4, b);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(af[0], bf[0], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(af[1], bf[1], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(af[2], bf[2], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(af[3], bf[3], acc, 0, 0, 0);
+  return acc;
+}
+
+__device__ __forceinline__ f32x4 mma_chunk_f16(u32x4 a, u32x4 b, f32x4 acc) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                __builtin_bit_cast(f16x8, b), acc, 0, 0, 0);
+}
+
+template <int DT>
+__device__ __forceinline__ f32x4 mma_chunk(u32x4 a, u32x4 b, f32x4 acc) {
+  if constexpr (DT == SIEVE_F32)
+    return mma_chunk_f32(a, b, acc);
+  else
+    return mma_chunk_f16(a, b, acc);
+}
+
+// Geometry of one query row in LDS, in 16-byte segments: 4 segments per chunk
+// plus one pad segment that staggers rows across LDS banks.
+template <int DT>
+struct RowGeom {
+  int nchunks;   // ceil(d / kChunkDims)
+  int segs;      // 16-byte segments per LDS row (4*nchunks + 1)
+  int dsegs;     // real 16-byte segments of a stored row (d / kSegDims)
+  __device__ __host__ static RowGeom make(int d) {
+    RowGeom g;
+    g.nchunks = (d + DTraits<DT>::kChunkDims - 1) / DTraits<DT>::kChunkDims;
+    g.segs = 4 * g.nchunks + 1;
+    g.dsegs = d / DTraits<DT>::kSegDims;
+    return g;
+  }
+};
+
+template <int DT>
+__host__ __device__ inline int lds_row_bytes(int d) {
+  return RowGeom<DT>::make(d).segs * 16;
+}
+
+// Stage rows of the query tile into LDS: row i (< nrows_pad) <- src(i) or 0.
+// src_row(i) returns a pointer to the stored row, or nullptr for padding.
+template <int DT, typename SrcRow>
+__device__ __forceinline__ void stage_queries(u32x4* lds, const RowGeom<DT>& g, int nrows_pad,
+                                              SrcRow src_row) {
+  const int total = nrows_pad * g.segs;
+  for (int e = threadIdx.x; e < total; e += blockDim.x) {
+    const int i = e / g.segs, s = e - i * g.segs;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    const u32x4* row = src_row(i);
+    if (row != nullptr && s < g.dsegs) v = row[s];
+    lds[e] = v;
+  }
+}
+
+// Score one 16-row block against QB query blocks.  vrow points at the
+// stored row this lane feeds (already clamped into bounds).  lane group h
+// reads segment 4*c + h of chunk c.
+template <int DT, int D, int QBMAX>
+__device__ __forceinline__ void score_block(const u32x4* __restrict__ lds, const RowGeom<DT>& g,
+                                            const u32x4* __restrict__ vrow, int qb_n,
+                                            f32x4 (&acc)[QBMAX]) {
+  const int lane = threadIdx.x & 63;
+  const int h = lane >> 4, r16 = lane & 15;
+#pragma unroll
+  for (int qb = 0; qb < QBMAX; ++qb) acc[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  constexpr int kNC = D / DTraits<DT>::kChunkDims;  // compile-time chunk count (0: runtime)
+  if constexpr (kNC > 0) {
+    u32x4 b[kNC];
+#pragma unroll
+    for (int c = 0; c < kNC; ++c) b[c] = vrow[4 * c + h];
+#pragma unroll
+    for (int c = 0; c < kNC; ++c) {
+#pragma unroll
+      for (int qb = 0; qb < QBMAX; ++qb) {
+        if (qb < qb_n) {
+          const u32x4 a = lds[(qb * 16 + r16) * g.segs + 4 * c + h];
+          acc[qb] = mma_chunk<DT>(a, b[c], acc[qb]);
+        }
+      }
+    }
+  } else {
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    u32x4 bn = (h < g.dsegs) ? vrow[h] : zero;
+    for (int c = 0; c < g.nchunks; ++c) {
+      const u32x4 bc = bn;
+      const int sn = 4 * (c + 1) + h;
+      bn = (sn < g.dsegs) ? vrow[sn] : zero;
+#pragma unroll
+      for (int qb = 0; qb < QBMAX; ++qb) {
+        if (qb < qb_n) {
+          const u32x4 a = lds[(qb * 16 + r16) * g.segs + 4 * c + h];
+          acc[qb] = mma_chunk<DT>(a, bc, acc[qb]);
+        }
+      }
+    }
+  }
+}
+
+}  // namespace sieve

@@ -1,0 +1,244 @@
+// scan.hip -- partition scan (within-partition search, Sec. 2.3 and Sec. 5)
+// fused with the tau test, and the centroid-screen GEMM of the ranking step
+// (Sec. 4.1).  Both use the MFMA tile engine of mfma_tile.h.
+//
+// Partition scan: each tile holds up to 16*QB ready items (q_i, j) of one
+// partition (Sec. 4.2's partition group) and one chunk of that partition's
+// rows.  The queries are staged once in LDS; every wave streams 16 rows at a
+// time from HBM into registers and scores them against all staged queries.
+// A score that reaches tau (inclusive, Sec. 2.2) for a row whose id is not
+// the query's exclusion id makes the probe a hit (Sec. 4.1): the candidate is
+// appended to the hit pool and the query's highest hit rank of the round is
+// raised with an atomic max.  The hit test depends only on the pair's own
+// score, never on other candidates, so it is the same whatever the dispatch
+// order (the property the lookahead equivalence of Sec. 4.3 needs).
+//
+// Work distribution: a persistent grid pulls tiles from 8 contiguous ranges,
+// one per XCD (a block starts on the range of blockIdx % 8, the XCD it is
+// dispatched to, so tiles of the same list share that XCD's L2), and steals
+// from the other ranges once its own is drained.  Every block exits after at
+// most (tiles + 8) queue pops.
+#include "mfma_tile.h"
+
+namespace sieve {
+namespace {
+
+template <int DT, int D>
+__global__ __launch_bounds__(kScanThreads) void scan_kernel(ScanArgs a, int qb_max) {
+  extern __shared__ u32x4 lds[];
+  __shared__ int s_tile;
+  __shared__ int32_t s_q[kTileQ];
+  __shared__ int32_t s_rank[kTileQ];
+  __shared__ int64_t s_ex[kTileQ];
+
+  const int d = D > 0 ? D : a.d;
+  const RowGeom<DT> g = RowGeom<DT>::make(d);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int h = lane >> 4, r16 = lane & 15;
+  const size_t row_bytes = (size_t)d * DTraits<DT>::kElem;
+  const int ntiles = a.rc->ntiles;
+  const int home = blockIdx.x & 7;
+
+  for (int xi = 0; xi < 8; ++xi) {
+    const int x = (home + xi) & 7;
+    const int t_begin = (int)(((int64_t)ntiles * x) / 8);
+    const int t_end = (int)(((int64_t)ntiles * (x + 1)) / 8);
+    for (;;) {
+      if (threadIdx.x == 0) s_tile = t_begin + atomicAdd(&a.rc->queue[x], 1);
+      __syncthreads();
+      const int t = s_tile;
+      __syncthreads();
+      if (t >= t_end) break;
+      const Tile tile = a.tiles[t];
+      const int nq = tile.nq;
+      const int qb_n = (nq + 15) >> 4;
+      const int64_t list_begin = a.list_offsets[tile.list];
+      const int64_t list_end = a.list_offsets[tile.list + 1];
+      const int64_t r0 = list_begin + (int64_t)tile.chunk * a.row_chunk;
+      const int64_t r1 = min(list_end, r0 + a.row_chunk);
+
+      if (threadIdx.x < nq) {
+        const Item it = a.bucket[tile.item_begin + threadIdx.x];
+        s_q[threadIdx.x] = it.q;
+        s_rank[threadIdx.x] = it.rank;
+        s_ex[threadIdx.x] = a.exclude ? a.exclude[it.q] : INT64_MIN;
+      }
+      __syncthreads();
+      const char* qbase = (const char*)a.queries;
+      stage_queries<DT>(lds, g, qb_n * 16, [&](int i) -> const u32x4* {
+        return i < nq ? (const u32x4*)(qbase + (size_t)s_q[i] * row_bytes) : nullptr;
+      });
+      __syncthreads();
+
+      const int nrows = (int)(r1 - r0);
+      const char* vbase = (const char*)a.vectors;
+      for (int rb = wave; rb * 16 < nrows; rb += kScanThreads / 64) {
+        const int64_t row = r0 + rb * 16 + r16;
+        const int64_t rowc = row < r1 ? row : r1 - 1;
+        const u32x4* vrow = (const u32x4*)(vbase + (size_t)rowc * row_bytes);
+        f32x4 acc[kQB];
+        score_block<DT, D, kQB>(lds, g, vrow, qb_n, acc);
+
+        // tau test: one wave-wide vote in the common (no candidate) case
+        bool any = false;
+#pragma unroll
+        for (int qb = 0; qb < kQB; ++qb) {
+          if (qb < qb_n) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int i = qb * 16 + 4 * h + r;
+              any |= (row < r1) && (i < nq) && (acc[qb][r] >= a.tau);
+            }
+          }
+        }
+        if (__ballot(any) == 0) continue;
+        if (any) {
+          const int64_t rid = a.ids[rowc];
+#pragma unroll
+          for (int qb = 0; qb < kQB; ++qb) {
+            if (qb < qb_n) {
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                const int i = qb * 16 + 4 * h + r;
+                const float sc = acc[qb][r];
+                if ((row < r1) && (i < nq) && (sc >= a.tau) && rid != s_ex[i]) {
+                  const int q = s_q[i];
+                  const unsigned long long slot = atomicAdd(a.pool_count, 1ull);
+                  if ((int64_t)slot < a.pool_cap) {
+                    Hit hv;
+                    hv.score = sc;
+                    hv.q = q;
+                    hv.id = rid;
+                    a.pool[slot] = hv;
+                  }
+                  atomicAdd(&a.hcount[q], 1);
+                  atomicMax(&a.lmax[q], s_rank[i] + 1);
+                }
+              }
+            }
+          }
+        }
+      }
+      __syncthreads();  // LDS is restaged by the next tile
+    }
+  }
+}
+
+// Centroid screen: scores[qi - q0][c] = fp32 <query qi, centroid c> for a
+// chunk of queries.  Grid: (ceil(nqc / kTileQ), ceil(nlist / 64)).
+template <int DT, int D>
+__global__ __launch_bounds__(kScanThreads) void rank_scores_kernel(const void* queries, int64_t q0,
+                                                                   int32_t nqc,
+                                                                   const void* centroids,
+                                                                   int32_t nlist, int32_t dd,
+                                                                   int32_t rows, float* scores) {
+  extern __shared__ u32x4 lds[];
+  const int d = D > 0 ? D : dd;
+  const RowGeom<DT> g = RowGeom<DT>::make(d);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int h = lane >> 4, r16 = lane & 15;
+  const size_t row_bytes = (size_t)d * DTraits<DT>::kElem;
+  const int qt0 = blockIdx.x * rows;
+  const int nq = min(rows, nqc - qt0);
+  const int qb_n = (nq + 15) >> 4;
+  const char* qbase = (const char*)queries + (size_t)(q0 + qt0) * row_bytes;
+  stage_queries<DT>(lds, g, qb_n * 16, [&](int i) -> const u32x4* {
+    return i < nq ? (const u32x4*)(qbase + (size_t)i * row_bytes) : nullptr;
+  });
+  __syncthreads();
+  const int c = blockIdx.y * 64 + wave * 16 + r16;
+  const int cc = c < nlist ? c : nlist - 1;
+  const u32x4* vrow = (const u32x4*)((const char*)centroids + (size_t)cc * row_bytes);
+  f32x4 acc[kQB];
+  score_block<DT, D, kQB>(lds, g, vrow, qb_n, acc);
+  if (c >= nlist) return;
+#pragma unroll
+  for (int qb = 0; qb < kQB; ++qb) {
+    if (qb < qb_n) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = qb * 16 + 4 * h + r;
+        if (i < nq) scores[(size_t)(qt0 + i) * nlist + c] = acc[qb][r];
+      }
+    }
+  }
+}
+
+// Dynamic LDS above 64 KB must be opted into once per kernel.
+constexpr int kMaxDynLds = 150 * 1024;
+
+template <int DT, int D>
+hipError_t launch_scan_t(const ScanArgs& a, int32_t grid, hipStream_t s) {
+  static const hipError_t attr = hipFuncSetAttribute(
+      (const void*)scan_kernel<DT, D>, hipFuncAttributeMaxDynamicSharedMemorySize, kMaxDynLds);
+  if (attr != hipSuccess) return attr;
+  const size_t lds = (size_t)a.tile_q * lds_row_bytes<DT>(D > 0 ? D : a.d);
+  if (lds > (size_t)kMaxDynLds) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((scan_kernel<DT, D>), dim3(grid), dim3(kScanThreads), lds, s, a, kQB);
+  return hipGetLastError();
+}
+
+template <int DT, int D>
+hipError_t launch_rank_scores_t(const void* queries, int64_t q0, int32_t nqc,
+                                const void* centroids, int32_t nlist, int32_t d, float* scores,
+                                hipStream_t s) {
+  static const hipError_t attr =
+      hipFuncSetAttribute((const void*)rank_scores_kernel<DT, D>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, kMaxDynLds);
+  if (attr != hipSuccess) return attr;
+  const int rows = tile_rows(DT, d);
+  const size_t lds = (size_t)rows * lds_row_bytes<DT>(d);
+  if (lds > (size_t)kMaxDynLds) return hipErrorInvalidValue;
+  dim3 grid((nqc + rows - 1) / rows, (nlist + 63) / 64);
+  hipLaunchKernelGGL((rank_scores_kernel<DT, D>), grid, dim3(kScanThreads), lds, s, queries, q0,
+                     nqc, centroids, nlist, d, rows, scores);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t scan_lds_bytes(int dtype, int d, int rows) {
+  return (size_t)rows * (dtype == SIEVE_F32 ? lds_row_bytes<SIEVE_F32>(d)
+                                            : lds_row_bytes<SIEVE_F16>(d));
+}
+
+int tile_rows(int dtype, int d) {
+  const int rb = dtype == SIEVE_F32 ? lds_row_bytes<SIEVE_F32>(d) : lds_row_bytes<SIEVE_F16>(d);
+  int qb = (80 * 1024) / (16 * rb);
+  qb = qb < 1 ? 1 : (qb > kQB ? kQB : qb);
+  return 16 * qb;
+}
+
+hipError_t launch_scan(int dtype, const ScanArgs& a, int32_t grid, hipStream_t s) {
+  if (dtype == SIEVE_F32) {
+    switch (a.d) {
+      case 64: return launch_scan_t<SIEVE_F32, 64>(a, grid, s);
+      case 128: return launch_scan_t<SIEVE_F32, 128>(a, grid, s);
+      default: return launch_scan_t<SIEVE_F32, 0>(a, grid, s);
+    }
+  }
+  switch (a.d) {
+    case 128: return launch_scan_t<SIEVE_F16, 128>(a, grid, s);
+    case 768: return launch_scan_t<SIEVE_F16, 768>(a, grid, s);
+    default: return launch_scan_t<SIEVE_F16, 0>(a, grid, s);
+  }
+}
+
+hipError_t launch_rank_scores(int dtype, const void* queries, int64_t q0, int32_t nqc,
+                              const void* centroids, int32_t nlist, int32_t d, float* scores,
+                              hipStream_t s) {
+  if (dtype == SIEVE_F32) {
+    switch (d) {
+      case 64: return launch_rank_scores_t<SIEVE_F32, 64>(queries, q0, nqc, centroids, nlist, d, scores, s);
+      case 128: return launch_rank_scores_t<SIEVE_F32, 128>(queries, q0, nqc, centroids, nlist, d, scores, s);
+      default: return launch_rank_scores_t<SIEVE_F32, 0>(queries, q0, nqc, centroids, nlist, d, scores, s);
+    }
+  }
+  switch (d) {
+    case 128: return launch_rank_scores_t<SIEVE_F16, 128>(queries, q0, nqc, centroids, nlist, d, scores, s);
+    case 768: return launch_rank_scores_t<SIEVE_F16, 768>(queries, q0, nqc, centroids, nlist, d, scores, s);
+    default: return launch_rank_scores_t<SIEVE_F16, 0>(queries, q0, nqc, centroids, nlist, d, scores, s);
+  }
+}
+
+}  // namespace sieve

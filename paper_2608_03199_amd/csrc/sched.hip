@@ -1,0 +1,293 @@
+// sched.hip -- device-side partition-major scheduling and the stop-rule
+// update.
+//
+// Continuous batching (Sec. 4.2, Algorithm 1) regroups ready items (q_i, j)
+// by partition p_{i,j}.  On the GPU this runs as bulk-synchronous rounds: all
+// items ready at the start of a round are histogrammed by partition (the
+// histogram is taken when the items are emitted), turned into partition-major
+// buckets by an exclusive scan and a scatter, and cut into scan tiles.  The
+// FIFO order and the 16K microbatch cap of the paper only decide timing, so
+// a round simply dispatches every ready group at once.
+//
+// After a round's scan, the update applies the stop rule to every query:
+//   lookahead (Sec. 4.3, Algorithm 2): a hit at rank j extends the stop line
+//     s <- max(s, min(j + W, n)); the newly committed ranks are emitted at
+//     once.  Only the largest hit rank of the round matters, because the
+//     updates combine through max.
+//   basic (Algorithm 1): one rank per round; stale resets on a hit and grows
+//     on an empty probe; the next rank is emitted while stale < W and
+//     next <= n.
+#include "sieve_internal.h"
+
+namespace sieve {
+namespace {
+
+constexpr int kThreads = 256;
+
+inline int blocks_for(int64_t n, int per = kThreads) {
+  int64_t b = (n + per - 1) / per;
+  return (int)(b < 1 ? 1 : b);
+}
+
+// Initial admission: ranks [0, s0) of every query of the chunk [q0, q0+nqc).
+// mode 0: lookahead (stop line s0), 1: basic (next = 0, stale = 0), 2: fixed.
+__global__ void emit_initial_kernel(const int32_t* __restrict__ P, int32_t n, int64_t nqc,
+                                    int32_t q0, int32_t s0, int32_t mode, Item* __restrict__ items,
+                                    int32_t* __restrict__ cnt, int32_t* __restrict__ state_a,
+                                    int32_t* __restrict__ state_b, int32_t* __restrict__ lmax) {
+  const int64_t ql = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (ql >= nqc) return;
+  const int32_t q = q0 + (int32_t)ql;
+  for (int j = 0; j < s0; ++j) {
+    Item it;
+    it.q = q;
+    it.rank = j;
+    items[ql * s0 + j] = it;
+    atomicAdd(&cnt[P[ql * n + j]], 1);
+  }
+  if (mode == 0) {
+    state_a[q] = s0;
+    lmax[q] = 0;
+  } else if (mode == 1) {
+    state_a[q] = 0;  // next (0-based rank in flight)
+    state_b[q] = 0;  // stale
+    lmax[q] = 0;
+  }
+}
+
+// One work-group: exclusive scans over the lists of the item histogram and
+// of the per-list tile counts; resets the round's counters.
+constexpr int kOffThreads = 1024;
+
+__global__ __launch_bounds__(kOffThreads) void sched_offsets_kernel(
+    const int32_t* __restrict__ cnt, const int64_t* __restrict__ list_offsets, int32_t nlist,
+    int32_t row_chunk, int32_t tile_q, int32_t* __restrict__ item_off,
+    int32_t* __restrict__ cursor, int32_t* __restrict__ tile_off, RoundCounters* rc) {
+  __shared__ int64_t s_items[kOffThreads];
+  __shared__ int64_t s_tiles[kOffThreads];
+  __shared__ unsigned long long s_stat[3];
+  const int t = threadIdx.x;
+  const int per = (nlist + kOffThreads - 1) / kOffThreads;
+  const int b = t * per, e = min(nlist, b + per);
+  int64_t si = 0, st = 0;
+  unsigned long long list_rows = 0, item_rows = 0, loads = 0;
+  for (int p = b; p < e; ++p) {
+    const int64_t len = list_offsets[p + 1] - list_offsets[p];
+    const int c = cnt[p];
+    si += c;
+    if (c > 0 && len > 0) {
+      st += (int64_t)((c + tile_q - 1) / tile_q) * ((len + row_chunk - 1) / row_chunk);
+      list_rows += (unsigned long long)len;
+      item_rows += (unsigned long long)len * (unsigned long long)c;
+      loads += 1;
+    }
+  }
+  if (t < 3) s_stat[t] = 0;
+  s_items[t] = si;
+  s_tiles[t] = st;
+  __syncthreads();
+  // inclusive Hillis-Steele scan over the 1024 partial sums
+  for (int off = 1; off < kOffThreads; off <<= 1) {
+    int64_t vi = t >= off ? s_items[t - off] : 0;
+    int64_t vt = t >= off ? s_tiles[t - off] : 0;
+    __syncthreads();
+    s_items[t] += vi;
+    s_tiles[t] += vt;
+    __syncthreads();
+  }
+  int64_t ri = s_items[t] - si, rt = s_tiles[t] - st;  // exclusive prefixes
+  for (int p = b; p < e; ++p) {
+    const int64_t len = list_offsets[p + 1] - list_offsets[p];
+    const int c = cnt[p];
+    item_off[p] = (int32_t)ri;
+    cursor[p] = (int32_t)ri;
+    tile_off[p] = (int32_t)rt;
+    ri += c;
+    if (c > 0 && len > 0)
+      rt += (int64_t)((c + tile_q - 1) / tile_q) * ((len + row_chunk - 1) / row_chunk);
+  }
+  atomicAdd(&s_stat[0], list_rows);
+  atomicAdd(&s_stat[1], item_rows);
+  atomicAdd(&s_stat[2], loads);
+  __syncthreads();
+  if (t == 0) {
+    rc->ntiles = (int32_t)s_tiles[kOffThreads - 1];
+    rc->new_items = 0;
+    for (int x = 0; x < 8; ++x) rc->queue[x] = 0;
+    rc->list_rows += s_stat[0];
+    rc->item_rows += s_stat[1];
+    rc->list_loads += s_stat[2];
+  }
+}
+
+__global__ void sched_scatter_kernel(const Item* __restrict__ items, int32_t n_items,
+                                     const int32_t* __restrict__ P, int32_t n, int32_t q0,
+                                     int32_t* __restrict__ cursor, Item* __restrict__ bucket) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_items) return;
+  const Item it = items[i];
+  const int p = P[(int64_t)(it.q - q0) * n + it.rank];
+  const int pos = atomicAdd(&cursor[p], 1);
+  bucket[pos] = it;
+}
+
+// One thread per list: write its tiles (query tiles x row chunks), tiles that
+// share a row chunk adjacent, and clear the list's histogram entry for the
+// next round.
+__global__ void sched_tiles_kernel(int32_t* __restrict__ cnt, const int32_t* __restrict__ item_off,
+                                   const int32_t* __restrict__ tile_off,
+                                   const int64_t* __restrict__ list_offsets, int32_t nlist,
+                                   int32_t row_chunk, int32_t tile_q, Tile* __restrict__ tiles) {
+  const int p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= nlist) return;
+  const int c = cnt[p];
+  cnt[p] = 0;
+  const int64_t len = list_offsets[p + 1] - list_offsets[p];
+  if (c == 0 || len == 0) return;
+  const int ntq = (c + tile_q - 1) / tile_q;
+  const int nch = (int)((len + row_chunk - 1) / row_chunk);
+  int32_t o = tile_off[p];
+  for (int ch = 0; ch < nch; ++ch) {
+    for (int tq = 0; tq < ntq; ++tq) {
+      Tile t;
+      t.list = p;
+      t.item_begin = item_off[p] + tq * tile_q;
+      t.nq = min(tile_q, c - tq * tile_q);
+      t.chunk = ch;
+      tiles[o++] = t;
+    }
+  }
+}
+
+__global__ void update_lookahead_kernel(int64_t nq, const int32_t* __restrict__ P, int32_t n,
+                                        int32_t W, int32_t* __restrict__ stop,
+                                        int32_t* __restrict__ lmax, Item* __restrict__ items,
+                                        int32_t* __restrict__ cnt, RoundCounters* rc) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= nq) return;
+  const int L = lmax[q];  // 1-based highest hit rank of this round, 0 = none
+  if (L == 0) return;
+  lmax[q] = 0;
+  const int s = stop[q];
+  const int reach = (W > n - L) ? n : L + W;  // min(L + W, n) without overflow
+  if (reach <= s) return;
+  const int base = atomicAdd(&rc->new_items, reach - s);
+  for (int j = s; j < reach; ++j) {
+    Item it;
+    it.q = (int32_t)q;
+    it.rank = j;
+    items[base + (j - s)] = it;
+    atomicAdd(&cnt[P[q * n + j]], 1);
+  }
+  stop[q] = reach;
+}
+
+// next[q]: rank in flight (0-based) or -1 once stopped; on stopping,
+// stale[q] is overwritten with the probe count.
+__global__ void update_basic_kernel(int64_t nq, const int32_t* __restrict__ P, int32_t n,
+                                    int32_t W, int32_t* __restrict__ next,
+                                    int32_t* __restrict__ stale, int32_t* __restrict__ lmax,
+                                    Item* __restrict__ items, int32_t* __restrict__ cnt,
+                                    RoundCounters* rc) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= nq) return;
+  const int cur = next[q];
+  if (cur < 0) return;
+  const bool hit = lmax[q] == cur + 1;
+  lmax[q] = 0;
+  const int st = hit ? 0 : stale[q] + 1;
+  const int nx = cur + 1;
+  if (st < W && nx < n) {
+    stale[q] = st;
+    next[q] = nx;
+    const int pos = atomicAdd(&rc->new_items, 1);
+    Item it;
+    it.q = (int32_t)q;
+    it.rank = nx;
+    items[pos] = it;
+    atomicAdd(&cnt[P[q * n + nx]], 1);
+  } else {
+    next[q] = -1;
+    stale[q] = nx;  // probes
+  }
+}
+
+__global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
+__global__ void zero_bytes_kernel(uint8_t* p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0;
+}
+
+}  // namespace
+
+hipError_t launch_emit_initial(const int32_t* P, int32_t n, int64_t nqc, int32_t q0, int32_t s0,
+                               int32_t mode, Item* items, int32_t* cnt, int32_t* state_a,
+                               int32_t* state_b, int32_t* lmax, hipStream_t s) {
+  hipLaunchKernelGGL(emit_initial_kernel, dim3(blocks_for(nqc)), dim3(kThreads), 0, s, P, n, nqc,
+                     q0, s0, mode, items, cnt, state_a, state_b, lmax);
+  return hipGetLastError();
+}
+
+hipError_t launch_sched_offsets(const int32_t* cnt, const int64_t* list_offsets, int32_t nlist,
+                                int32_t row_chunk, int32_t tile_q, int32_t* item_off,
+                                int32_t* cursor, int32_t* tile_off, RoundCounters* rc,
+                                hipStream_t s) {
+  hipLaunchKernelGGL(sched_offsets_kernel, dim3(1), dim3(kOffThreads), 0, s, cnt, list_offsets,
+                     nlist, row_chunk, tile_q, item_off, cursor, tile_off, rc);
+  return hipGetLastError();
+}
+
+hipError_t launch_sched_scatter(const Item* items, int32_t n_items, const int32_t* P, int32_t n,
+                                int32_t q0, int32_t* cursor, Item* bucket, hipStream_t s) {
+  if (n_items <= 0) return hipSuccess;
+  hipLaunchKernelGGL(sched_scatter_kernel, dim3(blocks_for(n_items)), dim3(kThreads), 0, s, items,
+                     n_items, P, n, q0, cursor, bucket);
+  return hipGetLastError();
+}
+
+hipError_t launch_sched_tiles(int32_t* cnt, const int32_t* item_off, const int32_t* tile_off,
+                              const int64_t* list_offsets, int32_t nlist, int32_t row_chunk,
+                              int32_t tile_q, Tile* tiles, hipStream_t s) {
+  hipLaunchKernelGGL(sched_tiles_kernel, dim3(blocks_for(nlist)), dim3(kThreads), 0, s, cnt,
+                     item_off, tile_off, list_offsets, nlist, row_chunk, tile_q, tiles);
+  return hipGetLastError();
+}
+
+hipError_t launch_update_lookahead(int64_t nq, const int32_t* P, int32_t n, int32_t W,
+                                   int32_t* stop, int32_t* lmax, Item* items, int32_t* cnt,
+                                   RoundCounters* rc, hipStream_t s) {
+  hipLaunchKernelGGL(update_lookahead_kernel, dim3(blocks_for(nq)), dim3(kThreads), 0, s, nq, P, n,
+                     W, stop, lmax, items, cnt, rc);
+  return hipGetLastError();
+}
+
+hipError_t launch_update_basic(int64_t nq, const int32_t* P, int32_t n, int32_t W, int32_t* next,
+                               int32_t* stale, int32_t* lmax, Item* items, int32_t* cnt,
+                               RoundCounters* rc, hipStream_t s) {
+  hipLaunchKernelGGL(update_basic_kernel, dim3(blocks_for(nq)), dim3(kThreads), 0, s, nq, P, n, W,
+                     next, stale, lmax, items, cnt, rc);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  int b = blocks_for(n);
+  hipLaunchKernelGGL(fill_i32_kernel, dim3(b > 4096 ? 4096 : b), dim3(kThreads), 0, s, p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_bytes(void* p, int64_t bytes, hipStream_t s) {
+  if (bytes <= 0) return hipSuccess;
+  int b = blocks_for(bytes);
+  hipLaunchKernelGGL(zero_bytes_kernel, dim3(b > 4096 ? 4096 : b), dim3(kThreads), 0, s,
+                     (uint8_t*)p, bytes);
+  return hipGetLastError();
+}
+
+}  // namespace sieve

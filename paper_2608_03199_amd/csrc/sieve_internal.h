@@ -1,0 +1,123 @@
+// sieve_internal.h -- device data layout and kernel launchers of the gfx950
+// threshold-aware IVF search.  Everything here is internal to libsieve.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/sieve.h"
+
+namespace sieve {
+
+// One ready item (q_i, j) of Sec. 4.2: query index and 0-based probe rank.
+struct Item {
+  int32_t q;
+  int32_t rank;
+};
+
+// One unit of partition-scan work: up to kTileQ items of one list, scored
+// against one chunk of that list's rows.
+struct Tile {
+  int32_t list;       // partition id
+  int32_t item_begin; // first item of the tile in the partition-major bucket
+  int32_t nq;         // items in the tile (1..kTileQ)
+  int32_t chunk;      // row chunk: rows [chunk*row_chunk, min(len, (chunk+1)*row_chunk))
+};
+
+// One qualifying candidate found by the scan (score >= tau, not excluded).
+struct Hit {
+  float score;
+  int32_t q;
+  int64_t id;
+};
+
+// Query-tile width of the scan: 8 blocks of 16 queries (MFMA M = 16).
+constexpr int kQB = 8;
+constexpr int kTileQ = 16 * kQB;
+constexpr int kScanThreads = 256;  // 4 wave64
+constexpr int kMaxRanks = 2048;    // largest n = min(nprobe_max, nlist)
+constexpr int kMaxNlist = 16384;   // centroid scores of one query fit in LDS
+constexpr int kMaxCand = 4096;     // rank-boundary candidates kept for the exact sort
+constexpr int kMaxD = 4096;
+
+// Per-round scheduling counters (device).
+struct RoundCounters {
+  int32_t ntiles;          // tiles built this round
+  int32_t new_items;       // items emitted by the update for the next round
+  int32_t queue[8];        // per-XCD tile cursors of the scan's work queue
+  int32_t rank_error;      // set when a rank boundary has more than kMaxCand candidates
+  int32_t pad;
+  unsigned long long list_rows;   // sum over active lists of their length (this round)
+  unsigned long long item_rows;   // sum over items of their list's length (this round)
+  unsigned long long list_loads;  // active non-empty lists (this round)
+  unsigned long long hits;        // pool appends (whole search)
+  unsigned long long probes;      // sum of out_probes (whole search)
+};
+
+struct ScanArgs {
+  const void* vectors;         // [n, d] partition-major
+  const int64_t* list_offsets; // [nlist + 1]
+  const int64_t* ids;          // [n]
+  const void* queries;         // [nq, d]
+  const int64_t* exclude;      // [nq] or null
+  const Item* bucket;          // partition-major items of this round
+  const Tile* tiles;
+  RoundCounters* rc;
+  int32_t* lmax;               // [nq] max 1-based hit rank this round (0 = none)
+  int32_t* hcount;             // [nq] pool entries per query
+  Hit* pool;
+  unsigned long long* pool_count;
+  int64_t pool_cap;
+  int32_t d;
+  int32_t row_chunk;
+  int32_t tile_q;              // query rows per tile (multiple of 16, <= kTileQ)
+  float tau;
+};
+
+// Query rows per tile for a dtype and dimension: as many 16-row blocks (<= 8)
+// as fit an 80 KB LDS budget, so that two work-groups share a CU.
+int tile_rows(int dtype, int d);
+
+// ---- launchers (each returns the hipError_t of its launch) ----
+hipError_t launch_rank_scores(int dtype, const void* queries, int64_t q0, int32_t nqc,
+                              const void* centroids, int32_t nlist, int32_t d, float* scores,
+                              hipStream_t s);
+size_t scan_lds_bytes(int dtype, int d, int rows);
+hipError_t launch_rank_select(int dtype, const void* queries, int64_t q0, int32_t nqc,
+                              const void* centroids, int32_t nlist, int32_t d, const float* scores,
+                              int32_t n, double cmax, int32_t* P, RoundCounters* rc,
+                              hipStream_t s);
+
+hipError_t launch_emit_initial(const int32_t* P, int32_t n, int64_t nqc, int32_t q0, int32_t s0,
+                               int32_t mode, Item* items, int32_t* cnt, int32_t* state_a,
+                               int32_t* state_b, int32_t* lmax, hipStream_t s);
+hipError_t launch_sched_offsets(const int32_t* cnt, const int64_t* list_offsets, int32_t nlist,
+                                int32_t row_chunk, int32_t tile_q, int32_t* item_off,
+                                int32_t* cursor, int32_t* tile_off, RoundCounters* rc,
+                                hipStream_t s);
+hipError_t launch_sched_scatter(const Item* items, int32_t n_items, const int32_t* P, int32_t n,
+                                int32_t q0, int32_t* cursor, Item* bucket, hipStream_t s);
+hipError_t launch_sched_tiles(int32_t* cnt, const int32_t* item_off, const int32_t* tile_off,
+                              const int64_t* list_offsets, int32_t nlist, int32_t row_chunk,
+                              int32_t tile_q, Tile* tiles, hipStream_t s);
+hipError_t launch_scan(int dtype, const ScanArgs& a, int32_t grid, hipStream_t s);
+hipError_t launch_update_lookahead(int64_t nq, const int32_t* P, int32_t n, int32_t W,
+                                   int32_t* stop, int32_t* lmax, Item* items, int32_t* cnt,
+                                   RoundCounters* rc, hipStream_t s);
+hipError_t launch_update_basic(int64_t nq, const int32_t* P, int32_t n, int32_t W, int32_t* next,
+                               int32_t* stale, int32_t* lmax, Item* items, int32_t* cnt,
+                               RoundCounters* rc, hipStream_t s);
+
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
+hipError_t launch_zero_bytes(void* p, int64_t bytes, hipStream_t s);
+hipError_t launch_exclusive_scan(const int32_t* in, int32_t* out, int32_t* out_copy, int64_t n,
+                                 int32_t* block_tmp, hipStream_t s);
+size_t exclusive_scan_tmp_elems(int64_t n);
+hipError_t launch_pool_scatter(const Hit* pool, int64_t n, int32_t* cursor, Hit* sorted,
+                               hipStream_t s);
+hipError_t launch_topk(int64_t nq, int32_t k, const Hit* sorted, const int32_t* hoff,
+                       const int32_t* hcount, const int32_t* probes_src, int32_t probes_const,
+                       int64_t* out_ids, float* out_scores, int32_t* out_probes,
+                       RoundCounters* rc, hipStream_t s);
+
+}  // namespace sieve

@@ -1,0 +1,226 @@
+// topk.hip -- the final MergeTopK of Algorithm 1: every qualifying candidate
+// a query met during the search is merged into its top-k, score descending
+// then id ascending.  As in the paper, local results only accumulate during
+// the search and are merged once at the end; the stop rule never looks at
+// them.
+//
+// The candidate pool is unordered (appends from many tiles).  It is grouped
+// by query with a counting sort (the per-query counts come from the scan's
+// appends, then an exclusive scan and a scatter), and each query's segment is
+// reduced by one wave64 that keeps its running top-64 in registers, one
+// candidate per lane, merging 64 new candidates at a time with bitonic
+// sorting networks over lane shuffles.  The total order makes the result
+// independent of the pool's order.
+#include "sieve_internal.h"
+
+namespace sieve {
+namespace {
+
+constexpr int kScanBlock = 1024;
+constexpr int kScanPer = 4;
+constexpr int kScanTile = kScanBlock * kScanPer;
+
+// In-block exclusive scan of kScanTile int32 values starting at base; returns
+// the block total through *total.
+__device__ void block_scan_tile(const int32_t* in, int32_t* out, int32_t* out2, int64_t n,
+                                int64_t base, int32_t add, int32_t* total) {
+  __shared__ int32_t s[kScanBlock];
+  const int t = threadIdx.x;
+  int32_t v[kScanPer];
+  int32_t sum = 0;
+  for (int e = 0; e < kScanPer; ++e) {
+    const int64_t i = base + (int64_t)t * kScanPer + e;
+    v[e] = i < n ? in[i] : 0;
+    sum += v[e];
+  }
+  s[t] = sum;
+  __syncthreads();
+  for (int off = 1; off < kScanBlock; off <<= 1) {
+    const int32_t x = t >= off ? s[t - off] : 0;
+    __syncthreads();
+    s[t] += x;
+    __syncthreads();
+  }
+  int32_t run = s[t] - sum + add;
+  if (out) {
+    for (int e = 0; e < kScanPer; ++e) {
+      const int64_t i = base + (int64_t)t * kScanPer + e;
+      if (i < n) {
+        out[i] = run;
+        if (out2) out2[i] = run;
+      }
+      run += v[e];
+    }
+  }
+  if (total && t == kScanBlock - 1) *total = s[t];
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(kScanBlock) void scan_partials_kernel(const int32_t* in, int64_t n,
+                                                                  int32_t* partial) {
+  block_scan_tile(in, nullptr, nullptr, n, (int64_t)blockIdx.x * kScanTile, 0,
+                  &partial[blockIdx.x]);
+}
+
+__global__ __launch_bounds__(kScanBlock) void scan_partials_top_kernel(int32_t* partial,
+                                                                      int32_t nparts) {
+  // nparts <= kScanTile: exclusive scan in place
+  __shared__ int32_t tot;
+  block_scan_tile(partial, partial, nullptr, nparts, 0, 0, &tot);
+}
+
+__global__ __launch_bounds__(kScanBlock) void scan_apply_kernel(const int32_t* in, int64_t n,
+                                                               const int32_t* partial,
+                                                               int32_t* out, int32_t* out2) {
+  block_scan_tile(in, out, out2, n, (int64_t)blockIdx.x * kScanTile, partial[blockIdx.x],
+                  nullptr);
+}
+
+__global__ void pool_scatter_kernel(const Hit* __restrict__ pool, int64_t n,
+                                    int32_t* __restrict__ cursor, Hit* __restrict__ sorted) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const Hit h = pool[i];
+  const int pos = atomicAdd(&cursor[h.q], 1);
+  sorted[pos] = h;
+}
+
+struct Cand {
+  float s;
+  long long id;
+};
+
+__device__ __forceinline__ bool better(const Cand& a, const Cand& b) {
+  return a.s > b.s || (a.s == b.s && a.id < b.id);
+}
+
+__device__ __forceinline__ Cand shfl_xor_cand(const Cand& c, int m) {
+  Cand o;
+  o.s = __shfl_xor(c.s, m);
+  const int lo = __shfl_xor((int)(c.id & 0xffffffffll), m);
+  const int hi = __shfl_xor((int)(c.id >> 32), m);
+  o.id = ((long long)hi << 32) | (unsigned int)lo;
+  return o;
+}
+
+__device__ __forceinline__ Cand shfl_cand(const Cand& c, int src) {
+  Cand o;
+  o.s = __shfl(c.s, src);
+  const int lo = __shfl((int)(c.id & 0xffffffffll), src);
+  const int hi = __shfl((int)(c.id >> 32), src);
+  o.id = ((long long)hi << 32) | (unsigned int)lo;
+  return o;
+}
+
+// Sort 64 lane-held candidates, best first.
+__device__ __forceinline__ Cand wave_sort_desc(Cand v, int lane) {
+#pragma unroll
+  for (int k = 2; k <= 64; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const Cand o = shfl_xor_cand(v, j);
+      const bool lower = (lane & j) == 0;
+      const bool desc = (lane & k) == 0;  // final stage: whole wave descending
+      const bool keep_better = (lower == desc);
+      const bool ob = better(o, v);
+      if (keep_better ? ob : !ob) v = o;
+    }
+  }
+  return v;
+}
+
+// Sort a bitonic 64-sequence, best first.
+__device__ __forceinline__ Cand wave_merge_desc(Cand v, int lane) {
+#pragma unroll
+  for (int j = 32; j > 0; j >>= 1) {
+    const Cand o = shfl_xor_cand(v, j);
+    const bool lower = (lane & j) == 0;
+    const bool ob = better(o, v);
+    if (lower ? ob : !ob) v = o;
+  }
+  return v;
+}
+
+// One wave per query.
+__global__ __launch_bounds__(256) void topk_kernel(int64_t nq, int32_t k,
+                                                   const Hit* __restrict__ sorted,
+                                                   const int32_t* __restrict__ hoff,
+                                                   const int32_t* __restrict__ hcount,
+                                                   const int32_t* __restrict__ probes_src,
+                                                   int32_t probes_const,
+                                                   int64_t* __restrict__ out_ids,
+                                                   float* __restrict__ out_scores,
+                                                   int32_t* __restrict__ out_probes,
+                                                   RoundCounters* rc) {
+  const int lane = threadIdx.x & 63;
+  const int64_t q = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (q >= nq) return;
+  const int m = hcount[q];
+  const int beg = m > 0 ? hoff[q] : 0;
+  const Cand none = {-INFINITY, 0x7fffffffffffffffll};
+  Cand top = none;
+  for (int b = 0; b < m; b += 64) {
+    Cand c = none;
+    if (b + lane < m) {
+      const Hit h = sorted[beg + b + lane];
+      c.s = h.score;
+      c.id = h.id;
+    }
+    c = wave_sort_desc(c, lane);
+    if (b == 0) {
+      top = c;
+    } else {
+      const Cand r = shfl_cand(c, 63 - lane);  // reversed: top ++ reverse(c) is bitonic
+      top = better(top, r) ? top : r;
+      top = wave_merge_desc(top, lane);
+    }
+  }
+  if (lane < k) {
+    const bool real = top.id != none.id;
+    out_ids[q * k + lane] = real ? (int64_t)top.id : -1;
+    out_scores[q * k + lane] = real ? top.s : -INFINITY;
+  }
+  if (lane == 0) {
+    const int32_t p = probes_src ? probes_src[q] : probes_const;
+    out_probes[q] = p;
+    atomicAdd(&rc->probes, (unsigned long long)p);
+  }
+}
+
+}  // namespace
+
+size_t exclusive_scan_tmp_elems(int64_t n) { return (size_t)((n + kScanTile - 1) / kScanTile) + 1; }
+
+hipError_t launch_exclusive_scan(const int32_t* in, int32_t* out, int32_t* out_copy, int64_t n,
+                                 int32_t* block_tmp, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t nb = (n + kScanTile - 1) / kScanTile;
+  if (nb > kScanTile) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(scan_partials_kernel, dim3((unsigned)nb), dim3(kScanBlock), 0, s, in, n,
+                     block_tmp);
+  hipLaunchKernelGGL(scan_partials_top_kernel, dim3(1), dim3(kScanBlock), 0, s, block_tmp,
+                     (int32_t)nb);
+  hipLaunchKernelGGL(scan_apply_kernel, dim3((unsigned)nb), dim3(kScanBlock), 0, s, in, n,
+                     block_tmp, out, out_copy);
+  return hipGetLastError();
+}
+
+hipError_t launch_pool_scatter(const Hit* pool, int64_t n, int32_t* cursor, Hit* sorted,
+                               hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(pool_scatter_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, pool,
+                     n, cursor, sorted);
+  return hipGetLastError();
+}
+
+hipError_t launch_topk(int64_t nq, int32_t k, const Hit* sorted, const int32_t* hoff,
+                       const int32_t* hcount, const int32_t* probes_src, int32_t probes_const,
+                       int64_t* out_ids, float* out_scores, int32_t* out_probes,
+                       RoundCounters* rc, hipStream_t s) {
+  if (nq <= 0) return hipSuccess;
+  hipLaunchKernelGGL(topk_kernel, dim3((unsigned)((nq + 3) / 4)), dim3(256), 0, s, nq, k, sorted,
+                     hoff, hcount, probes_src, probes_const, out_ids, out_scores, out_probes, rc);
+  return hipGetLastError();
+}
+
+}  // namespace sieve

@@ -1,0 +1,89 @@
+"""CPU-side checks of the C ABI: the library builds for gfx950, loads, exports
+every symbol include/sieve.h declares, mirrors sieve_stats exactly, and
+rejects bad arguments before any HIP call."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sieve.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2608_03199_amd as ps
+    if not os.path.exists(ps.LIB_PATH):
+        from paper_2608_03199_amd import build
+        build.build()
+    return ps.load_library()
+
+
+def declared_symbols():
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"SIEVE_API\s+[\w\s\*]+?\b(sieve_\w+)\s*\(", txt)))
+
+
+def test_header_declares_the_boundary():
+    syms = declared_symbols()
+    for s in ("sieve_load_index", "sieve_search", "sieve_search_fixed", "sieve_free_index",
+              "sieve_last_error"):
+        assert s in syms
+
+
+def test_library_exports_every_declared_symbol(lib):
+    import paper_2608_03199_amd as ps
+    out = subprocess.run(["nm", "-D", "--defined-only", ps.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (sieve_\w+)", out))
+    assert set(declared_symbols()) <= exported
+    for s in declared_symbols():
+        assert hasattr(lib, s)
+    # nothing else with C linkage leaks out
+    assert all(s.startswith("sieve_") for s in exported)
+
+
+def test_stats_struct_layout_matches_c(tmp_path):
+    import paper_2608_03199_amd as ps
+    fields = [f for f, _ in ps.Stats._fields_]
+    src = tmp_path / "layout.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "sieve.h"\nint main(void){'
+                   'printf("%zu", sizeof(sieve_stats));' +
+                   "".join(f'printf(" %zu", offsetof(sieve_stats, {f}));' for f in fields) +
+                   "return 0;}\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)], check=True)
+    vals = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True,
+                                           check=True).stdout.split()]
+    assert vals[0] == ctypes.sizeof(ps.Stats)
+    assert vals[1:] == [getattr(ps.Stats, f).offset for f in fields]
+
+
+def test_argument_errors_without_a_gpu(lib):
+    # no handle: rejected before any HIP call
+    rc = lib.sieve_search(None, None, 0, None, 10, 0.9, 8, 32, 1, None, None, None, None, None)
+    assert rc == -1 and b"NULL" in lib.sieve_last_error()
+    rc = lib.sieve_search_fixed(None, None, 0, None, 10, 0.9, 32, None, None, None, None, None)
+    assert rc == -1
+    h = ctypes.c_void_p()
+    rc = lib.sieve_load_index(None, 0, 10, 64, None, 4, None, None, None, ctypes.byref(h))
+    assert rc == -1 and h.value is None
+    rc = lib.sieve_load_index(None, 7, 0, 64, None, 4, None, None, None, ctypes.byref(h))
+    assert rc == -1 and b"dtype" in lib.sieve_last_error()
+    fake = ctypes.c_void_p(0x1000)
+    rc = lib.sieve_load_index(fake, 0, 0, 12, fake, 4, fake, fake, None, ctypes.byref(h))
+    assert rc == -4  # d not a multiple of 8
+    rc = lib.sieve_load_index(fake, 0, 0, 64, fake, 20000, fake, fake, None, ctypes.byref(h))
+    assert rc == -4  # nlist above the supported maximum
+    lib.sieve_free_index(None)
+    assert b"gfx950" in lib.sieve_version()
+
+
+def test_no_cpu_fallback_in_binding():
+    """The binding holds marshalling only: no oracle import, no torch compute on the path."""
+    src = open(os.path.join(ROOT, "paper_2608_03199_amd", "__init__.py")).read()
+    assert "oracle" not in src.replace("no oracle", "")
+    for bad in ("torch.topk", "torch.matmul", "@", "torch.sort", ".mm("):
+        assert bad not in src.split('"""', 2)[2]

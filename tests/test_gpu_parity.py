@@ -1,0 +1,230 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Every case runs the library on seeded synthetic inputs and the oracle on the
+same arrays, and compares ids and probe counts exactly and scores to 1e-4
+(tests/parity.py states the flagged exceptions).  Sizes span many tiles,
+ragged query tiles and ragged row blocks; edge cases cover empty input,
+k = 1 and k = 64, nprobe = 1 and nprobe > nlist, W = 1 and W = infinity,
+empty lists, dimensions that are not a multiple of the MFMA chunk, and a
+threshold low enough to overflow the candidate pool.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import sieve_workloads as sw
+from parity import assert_parity, compare
+
+pytestmark = pytest.mark.gpu
+
+NTHREADS = min(16, os.cpu_count() or 1)
+
+
+def _lib():
+    import paper_2608_03199_amd as ps
+    return ps
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _require_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    _lib().load_library()
+
+
+class Case:
+    """A workload on the GPU, its library index and host copies for the oracle."""
+
+    def __init__(self, w: sw.Workload):
+        ps = _lib()
+        self.w = w
+        self.h = w.numpy()
+        self.ix = ps.Index(w.vectors, w.list_offsets, w.ids, w.centroids)
+
+    def gpu(self, k, tau, W, nprobe, lookahead=True, queries=None, exclude=True, fixed=False,
+            stats=False):
+        q = self.w.queries if queries is None else queries
+        ex = self.w.exclude_ids[: q.shape[0]] if exclude else None
+        if fixed:
+            r = self.ix.search_fixed(q, ex, k, tau, nprobe, with_stats=stats)
+        else:
+            r = self.ix.search(q, ex, k, tau, W, nprobe, lookahead=lookahead, with_stats=stats)
+        torch.cuda.synchronize()
+        out = [r[0].cpu().numpy(), r[1].cpu().numpy(), r[2].cpu().numpy()]
+        if stats:
+            out.append(r[3])
+        return out
+
+    def oracle(self, k, tau, W, nprobe, nq=None, exclude=True):
+        h = self.h
+        qs = h["queries"] if nq is None else h["queries"][:nq]
+        ex = (h["exclude_ids"][: qs.shape[0]]) if exclude else None
+        return oracle.search(h["vectors"], h["list_offsets"], h["ids"], h["centroids"], qs, ex, k,
+                             tau, W, nprobe, oracle.MODE_A, NTHREADS)
+
+
+_cases = {}
+
+
+def case(name, **kw) -> Case:
+    key = (name, tuple(sorted(kw.items())))
+    if key not in _cases:
+        print(f"[gpu-test] generating workload {name} {kw}", flush=True)
+        _cases[key] = Case(sw.make(name, device="cuda", **kw))
+    return _cases[key]
+
+
+def _check(c: Case, k, tau, W, nprobe, lookahead=True, fixed=False, nq=None, exclude=True):
+    q = c.w.queries if nq is None else c.w.queries[:nq]
+    g_ids, g_sc, g_pr = c.gpu(k, tau, W, nprobe, lookahead, queries=q, exclude=exclude,
+                              fixed=fixed)
+    o = c.oracle(k, tau, oracle.W_INF if fixed else W, nprobe, nq=q.shape[0], exclude=exclude)
+    rep = compare(g_ids, g_sc, g_pr, o)
+    print(f"[gpu-test] k={k} tau={tau} W={W} nprobe={nprobe} la={lookahead} fixed={fixed} "
+          f"-> {rep}", flush=True)
+    assert_parity(rep)
+    return g_ids, g_sc, g_pr, o
+
+
+@pytest.mark.parametrize("name", ["tiny", "tiny16", "c1"])
+@pytest.mark.parametrize("lookahead", [True, False])
+def test_sieve_matches_oracle(name, lookahead):
+    c = case(name)
+    s = c.w.spec
+    _check(c, s.k, s.tau, s.W, s.nprobe_max, lookahead)
+
+
+@pytest.mark.parametrize("name", ["tiny", "tiny16", "c1"])
+def test_fixed_matches_oracle(name):
+    c = case(name)
+    s = c.w.spec
+    _check(c, s.k, s.tau, oracle.W_INF, s.fixed_nprobe, fixed=True)
+
+
+@pytest.mark.parametrize("name", ["tiny16", "c1"])
+@pytest.mark.parametrize("W", [1, 2, 4, 16])
+def test_lookahead_invariance_and_window_sweep(name, W):
+    c = case(name)
+    s = c.w.spec
+    a = c.gpu(s.k, s.tau, W, s.nprobe_max, lookahead=True, stats=True)
+    b = c.gpu(s.k, s.tau, W, s.nprobe_max, lookahead=False, stats=True)
+    for x, y in zip(a[:3], b[:3]):
+        assert np.array_equal(x, y)
+    # the same query-partition searches: same items, probes and scanned rows
+    assert a[3].items == b[3].items and a[3].vectors_scanned == b[3].vectors_scanned
+    assert a[3].probes_total == b[3].probes_total == int(a[2].sum())
+    _check(c, s.k, s.tau, W, s.nprobe_max, lookahead=True)
+
+
+def test_infinite_window_equals_fixed():
+    c = case("c1")
+    s = c.w.spec
+    a = c.gpu(s.k, s.tau, 0x7FFFFFFF, s.nprobe_max)
+    f = c.gpu(s.k, s.tau, 0, s.nprobe_max, fixed=True)
+    for x, y in zip(a, f):
+        assert np.array_equal(x, y)
+
+
+def test_repeatable():
+    c = case("c1")
+    s = c.w.spec
+    a = c.gpu(s.k, s.tau, s.W, s.nprobe_max)
+    b = c.gpu(s.k, s.tau, s.W, s.nprobe_max)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+@pytest.mark.parametrize("k", [1, 7, 64])
+def test_k_edges(k):
+    c = case("tiny")
+    _check(c, k, 0.85, 3, 12)
+    _check(c, k, 0.85, 3, 12, fixed=True)
+
+
+@pytest.mark.parametrize("nprobe", [1, 5, 16, 1000])
+def test_nprobe_edges(nprobe):
+    c = case("tiny")
+    _check(c, 10, 0.9, 2, nprobe)
+    _check(c, 10, 0.9, 2, nprobe, fixed=True)
+
+
+def test_ragged_and_small_batches():
+    c = case("c1")
+    for nq in (1, 15, 17, 129, 333):
+        _check(c, 10, 0.9, 8, 32, nq=nq)
+    # no exclusion: every query finds itself at rank 1
+    g_ids, g_sc, g_pr, o = _check(c, 10, 0.9, 8, 32, nq=64, exclude=False)
+    assert np.array_equal(g_ids[:, 0], c.h["exclude_ids"][:64])
+
+
+def test_empty_query_batch():
+    c = case("tiny")
+    ids, sc, pr = c.gpu(10, 0.9, 3, 12, queries=c.w.queries[:0])
+    assert ids.shape == (0, 10) and pr.shape == (0,)
+
+
+@pytest.mark.parametrize("d,dtype", [(40, torch.float32), (72, torch.float16),
+                                     (96, torch.float32), (256, torch.float16)])
+def test_uncommon_dimensions(d, dtype):
+    """Dimensions off the compiled fast paths, including partial MFMA chunks."""
+    spec = sw.SPECS["tiny"]
+    import dataclasses
+    sp = dataclasses.replace(spec, name=f"d{d}", d=d, dtype="f16" if dtype == torch.float16
+                             else "f32", n=4000, nlist=24, nq=200)
+    c = Case(sw.make(sp, device="cuda"))
+    _check(c, 10, 0.9, 3, 12)
+    _check(c, 10, 0.9, 3, 24, fixed=True)
+
+
+def test_empty_lists_and_unbalanced_index():
+    """Lists of length zero are threshold-empty probes; one list holds most rows."""
+    rng = np.random.default_rng(5)
+    d, nlist, n = 32, 12, 2500
+    X = rng.standard_normal((n, d)).astype(np.float32)
+    X /= np.linalg.norm(X, axis=1, keepdims=True)
+    X[1::5] = X[0::5][: len(X[1::5])] + 0.03 * rng.standard_normal((len(X[1::5]), d))
+    X /= np.linalg.norm(X, axis=1, keepdims=True)
+    C = rng.standard_normal((nlist, d)).astype(np.float32)
+    C /= np.linalg.norm(C, axis=1, keepdims=True)
+    sizes = np.array([0, 2000, 0, 0, 100, 100, 0, 100, 100, 50, 50, 0])
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    ids = rng.permutation(n).astype(np.int64)
+    qrows = rng.choice(n, 300, replace=False)
+    ps = _lib()
+    dev = "cuda"
+    ix = ps.Index(torch.from_numpy(X).to(dev), torch.from_numpy(off).to(dev),
+                  torch.from_numpy(ids).to(dev), torch.from_numpy(C).to(dev))
+    Q = X[qrows].copy()
+    ex = ids[qrows]
+    for W in (1, 3, 0x7FFFFFFF):
+        g = ix.search(torch.from_numpy(Q).to(dev), torch.from_numpy(ex).to(dev), 10, 0.9, W, 12)
+        o = oracle.search(X, off, ids, C, Q, ex, 10, 0.9, W, 12)
+        rep = compare(g[0].cpu().numpy(), g[1].cpu().numpy(), g[2].cpu().numpy(), o)
+        assert_parity(rep)
+
+
+def test_low_threshold_overflows_pool_and_retries():
+    """tau = -1: every scanned row qualifies; the pool overflows and the search re-runs."""
+    c = case("c1")
+    g_ids, g_sc, g_pr, st = c.gpu(10, -1.0, 4, 8, queries=c.w.queries[:600], stats=True)
+    assert st.pool_retries >= 1 and st.hits > (1 << 20)
+    o = c.oracle(10, -1.0, 4, 8, nq=600)
+    rep = compare(g_ids, g_sc, g_pr, o)
+    print(f"[gpu-test] low tau -> {rep}", flush=True)
+    assert_parity(rep)
+
+
+def test_invalid_arguments_leave_outputs_untouched():
+    ps = _lib()
+    c = case("tiny")
+    q = c.w.queries
+    for kw in (dict(k=0), dict(k=65), dict(W=0), dict(nprobe_max=0), dict(tau=float("nan"))):
+        args = dict(k=10, tau=0.9, W=3, nprobe_max=12)
+        args.update(kw)
+        with pytest.raises(ps.SieveError) as e:
+            c.ix.search(q, c.w.exclude_ids, args["k"], args["tau"], args["W"],
+                        args["nprobe_max"])
+        assert e.value.code == -1
