@@ -1,0 +1,244 @@
+"""Benchmark: threshold-aware IVF search (W = 8, lookahead) on one MI355X.
+
+One step = one sieve_search call over the workload's whole query batch with
+inputs resident in HBM: centroid ranking, partition-major scheduling rounds,
+the partition scan with the tau test, the stop-rule updates and the final
+top-k.  The default workload is the mid-size self-join (N = 1,000,000 rows,
+d = 128, fp32, nlist = 1,024, Q = 10,000, k = 10, tau = 0.92, W = 8,
+nprobe_max = 128).  The same run times the fixed-probe baseline (nprobe = 128)
+on the same GPU for the speedup, reads the partition-scan kernel's device
+time from the library's HIP events on the search stream for the roofline,
+and times the CPU oracle on a bounded query sample (cpu_baseline).
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config c2]
+
+Prints exactly one JSON line (last line of stdout).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = {"f32": 157.3, "f16": 2500.0}
+PMC_FILE = os.path.join(ROOT, "profiles", "scan_traffic_pmc.json")
+SCAN_SOURCES = ["paper_2608_03199_amd/csrc/scan.hip", "paper_2608_03199_amd/csrc/mfma_tile.h"]
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def scan_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in SCAN_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(config: str):
+    """HBM bytes per scan launch from the committed rocprofv3 counter summary,
+    or None when it is absent or was taken on a different scan kernel."""
+    try:
+        with open(PMC_FILE) as f:
+            d = json.load(f)
+    except (OSError, ValueError):
+        return None
+    e = d.get(config)
+    if not e or e.get("scan_source_hash") != scan_source_hash():
+        return None
+    return e.get("bytes_per_launch")
+
+
+def workload_name(spec) -> str:
+    return (f"{spec.name}: self-join N={spec.n:,} d={spec.d} {spec.dtype}, nlist={spec.nlist:,}, "
+            f"Q={spec.nq:,}, k={spec.k}, tau={spec.tau}, W={spec.W}, "
+            f"nprobe_max={spec.nprobe_max}, lookahead on")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="c2")
+    ap.add_argument("--oracle-queries", type=int, default=4000,
+                    help="queries in the single-thread oracle sample")
+    ap.add_argument("--no-oracle", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run a plain 1 GiB device copy (HBM counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: this build measures one GPU only; --gpus must be 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2608_03199_amd as ps
+    import sieve_workloads as sw
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    spec = sw.SPECS[args.config]
+    log(f"[bench] generating {args.config} on {dev}")
+    t0 = time.time()
+    w = sw.make(spec, device=dev)
+    torch.cuda.synchronize()
+    log(f"[bench] generated in {time.time() - t0:.1f}s; lists {sw.list_stats(w.list_offsets.cpu().numpy())}")
+    ix = ps.Index(w.vectors, w.list_offsets, w.ids, w.centroids)
+    nq = spec.nq
+
+    if args.copy_probe:
+        a = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        a.fill_(1.0)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
+    def sieve(with_stats=True):
+        return ix.search(w.queries, w.exclude_ids, spec.k, spec.tau, spec.W, spec.nprobe_max,
+                         lookahead=True, with_stats=with_stats)
+
+    def fixed(with_stats=True):
+        return ix.search_fixed(w.queries, w.exclude_ids, spec.k, spec.tau, spec.fixed_nprobe,
+                               with_stats=with_stats)
+
+    for _ in range(args.warmup):
+        sieve()
+        fixed()
+    torch.cuda.synchronize()
+
+    # timed region: exactly K sieve steps
+    log(f"[bench] timing {args.steps} steps")
+    stats = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        r = sieve()
+        stats.append(r[3])
+    torch.cuda.synchronize()
+    t_sieve = time.perf_counter() - t0
+    ids, scores, probes = r[0], r[1], r[2]
+
+    # fixed-probe baseline on the same GPU (same number of steps)
+    fstats = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        fr = fixed()
+        fstats.append(fr[3])
+    torch.cuda.synchronize()
+    t_fixed = time.perf_counter() - t0
+
+    ms_step = 1e3 * t_sieve / args.steps
+    qps = nq * args.steps / t_sieve
+    fixed_qps = nq * args.steps / t_fixed
+    st = stats[-1]
+    mean = lambda xs, f: float(np.mean([getattr(x, f) for x in xs]))
+    ms_scan = mean(stats, "ms_scan")
+    launches = st.scan_launches
+    bytes_launch = st.scan_bytes / max(launches, 1)
+    flops_launch = st.scan_flops / max(launches, 1)
+    avg_launch_ms = ms_scan / max(launches, 1)
+    peak_f = MFMA_PEAK_TFLOPS[spec.dtype]
+    t_hbm = st.scan_bytes / (HBM_PEAK_GBS * 1e9)
+    t_mfma = st.scan_flops / (peak_f * 1e12)
+    bound = "hbm" if t_hbm >= t_mfma else "mfma"
+    gbs = bytes_launch / (avg_launch_ms * 1e-3) / 1e9
+    tfs = flops_launch / (avg_launch_ms * 1e-3) / 1e12
+    traffic = measured_traffic(args.config)
+    if bound == "hbm":
+        roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    else:
+        roof = {"bound": "mfma", "achieved": round(tfs, 2), "peak": peak_f, "unit": "TFLOP/s",
+                "frac": round(tfs / peak_f, 4)}
+    roof["traffic"] = traffic
+    roof["kernel"] = "scan_kernel (partition scan + tau test)"
+    roof["launches_per_step"] = launches
+    roof["avg_launch_ms"] = round(avg_launch_ms, 5)
+    roof["alg_bytes_per_launch"] = round(bytes_launch)
+    roof["alg_flops_per_launch"] = round(flops_launch)
+    roof["other_bound_frac"] = round((tfs / peak_f) if bound == "hbm" else (gbs / HBM_PEAK_GBS), 4)
+    roof["roofline_time_frac"] = round(max(t_hbm, t_mfma) / (ms_scan * 1e-3), 4)
+
+    out = {
+        "metric": "queries/sec at W=8 (k=10, tau); speedup vs fixed-nprobe; scan HBM GB/s",
+        "value": round(qps, 1),
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": spec.dtype,
+        "data": "synthetic (seeded mixture + near-duplicate groups, spherical k-means IVF)",
+        "config": {"workload": workload_name(spec), "queries": nq, "k": spec.k,
+                   "tau": spec.tau, "W": spec.W, "nprobe_max": spec.nprobe_max,
+                   "fixed_nprobe": spec.fixed_nprobe, "parallelism": "single GPU"},
+        "speedup_vs_fixed": round(t_fixed / t_sieve, 3),
+        "fixed_qps": round(fixed_qps, 1),
+        "partition_vectors_per_s": round(st.vectors_scanned * args.steps / t_sieve, 1),
+        "scan_hbm_gbs": round(gbs, 1),
+        "mean_probes": round(float(probes.float().mean().item()), 3),
+        "rounds": st.rounds,
+        "phase_ms": {k: round(mean(stats, "ms_" + k), 4) for k in
+                     ("rank", "sched", "scan", "update", "finalize", "total")},
+        "fixed_phase_ms": {k: round(mean(fstats, "ms_" + k), 4) for k in
+                           ("rank", "sched", "scan", "finalize", "total")},
+        "roofline": roof,
+    }
+
+    if not args.no_oracle:
+        import oracle
+        sys.path.insert(0, os.path.join(ROOT, "tests"))
+        from parity import compare
+        h = w.numpy()
+        m = min(args.oracle_queries, nq)
+        rng = np.random.default_rng(spec.seed + 77)
+        sel = np.sort(rng.choice(nq, m, replace=False))
+        log(f"[bench] oracle on {m} queries, 1 thread")
+        t0 = time.perf_counter()
+        o = oracle.search(h["vectors"], h["list_offsets"], h["ids"], h["centroids"],
+                          h["queries"][sel], h["exclude_ids"][sel], spec.k, spec.tau, spec.W,
+                          spec.nprobe_max, oracle.MODE_A, 1)
+        t_or = time.perf_counter() - t0
+        rep = compare(ids.cpu().numpy()[sel], scores.cpu().numpy()[sel],
+                      probes.cpu().numpy()[sel], o)
+        out["cpu_baseline"] = {"value": round(m / t_or, 2), "unit": "queries/s", "cores": 1,
+                               "kind": "oracle",
+                               "sample": f"{m} seeded queries of the same workload, "
+                                         f"single thread, {t_or:.1f}s",
+                               "cpu": _cpu_model()}
+        out["parity_sample"] = {k: rep[k] for k in ("queries", "mismatch", "flag_tau_edge",
+                                                    "flag_kth_tie", "flagged_mismatch",
+                                                    "max_score_err")}
+    ix.close()
+    print(json.dumps(out), flush=True)
+
+
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip() + f" ({os.cpu_count()} threads visible)"
+    except OSError:
+        pass
+    return "unknown"
+
+
+if __name__ == "__main__":
+    main()

@@ -72,8 +72,6 @@ int ensure(Buf& b, size_t bytes) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-constexpr int kEvents = 6;
-
 }  // namespace
 
 struct sieve_index {
@@ -95,8 +93,11 @@ struct sieve_index {
       lmax, hcount, hoff, hcur, scan_tmp, pool, pool_sorted;
   int64_t pool_cap = 0;
   RoundCounters* rc_host = nullptr;
-  hipEvent_t ev[kEvents] = {};
-  bool events = false;
+  // phase timing (only when stats are requested): events are recorded on the
+  // stream as the search goes and read once after its final synchronisation
+  std::vector<hipEvent_t> ev_pool;
+  size_t ev_used = 0;
+  std::vector<int> span_phase, span_a, span_b;
 };
 
 namespace {
@@ -108,20 +109,55 @@ double host_elem(const void* base, int dtype, int64_t i) {
   return (double)((const _Float16*)base)[i];
 }
 
-int alloc_events(sieve_index* ix) {
-  if (ix->events) return SIEVE_OK;
-  for (int i = 0; i < kEvents; ++i) HIP_TRY(hipEventCreate(&ix->ev[i]));
-  ix->events = true;
-  return SIEVE_OK;
+enum Phase { kRank = 0, kSched, kScan, kUpdate, kFinal, kTotal, kPhases };
+
+// Record an event on the stream and return its slot; -1 when not timing.
+int mark(sieve_index* ix, bool timed, hipStream_t s) {
+  if (!timed) return -1;
+  if (ix->ev_used == ix->ev_pool.size()) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) {
+      (void)hipGetLastError();
+      return -1;
+    }
+    ix->ev_pool.push_back(e);
+  }
+  const int slot = (int)ix->ev_used++;
+  if (hipEventRecord(ix->ev_pool[slot], s) != hipSuccess) {
+    (void)hipGetLastError();
+    return -1;
+  }
+  return slot;
 }
 
-float elapsed(sieve_index* ix, int a, int b) {
-  float ms = 0.f;
-  if (hipEventElapsedTime(&ms, ix->ev[a], ix->ev[b]) != hipSuccess) {
-    (void)hipGetLastError();
-    return 0.f;
+void span(sieve_index* ix, int phase, int a, int b) {
+  if (a < 0 || b < 0) return;
+  ix->span_phase.push_back(phase);
+  ix->span_a.push_back(a);
+  ix->span_b.push_back(b);
+}
+
+void reset_timeline(sieve_index* ix) {
+  ix->ev_used = 0;
+  ix->span_phase.clear();
+  ix->span_a.clear();
+  ix->span_b.clear();
+}
+
+// After the stream has drained: milliseconds per phase, and scan span count.
+void read_timeline(sieve_index* ix, float* ms, int* scan_spans) {
+  for (int p = 0; p < kPhases; ++p) ms[p] = 0.f;
+  *scan_spans = 0;
+  for (size_t i = 0; i < ix->span_phase.size(); ++i) {
+    float t = 0.f;
+    if (hipEventElapsedTime(&t, ix->ev_pool[ix->span_a[i]], ix->ev_pool[ix->span_b[i]]) !=
+        hipSuccess) {
+      (void)hipGetLastError();
+      t = 0.f;
+    }
+    ms[ix->span_phase[i]] += t;
+    if (ix->span_phase[i] == kScan) ++*scan_spans;
   }
-  return ms;
 }
 
 // Tunables of the scan decomposition (they never change results).
@@ -241,9 +277,9 @@ ScanArgs make_scan_args(sieve_index* ix, const void* queries, const int64_t* exc
 
 // One scheduling round over n_items ready items (already histogrammed).
 int run_round(sieve_index* ix, const ScanArgs& sa, int n_items, int64_t q0, const int32_t* P,
-              const SearchPlan& pl, hipStream_t s, bool timed, float* ms_sched, float* ms_scan) {
+              const SearchPlan& pl, hipStream_t s, bool timed) {
   RoundCounters* rc = (RoundCounters*)ix->rc.p;
-  if (timed) HIP_TRY(hipEventRecord(ix->ev[0], s));
+  const int e0 = mark(ix, timed, s);
   HIP_TRY(launch_sched_offsets((const int32_t*)ix->cnt.p, ix->offsets, ix->nlist, pl.row_chunk,
                                pl.tile_q, (int32_t*)ix->item_off.p, (int32_t*)ix->cursor.p,
                                (int32_t*)ix->tile_off.p, rc, s));
@@ -252,11 +288,11 @@ int run_round(sieve_index* ix, const ScanArgs& sa, int n_items, int64_t q0, cons
   HIP_TRY(launch_sched_tiles((int32_t*)ix->cnt.p, (const int32_t*)ix->item_off.p,
                              (const int32_t*)ix->tile_off.p, ix->offsets, ix->nlist, pl.row_chunk,
                              pl.tile_q, (Tile*)ix->tiles.p, s));
-  if (timed) HIP_TRY(hipEventRecord(ix->ev[1], s));
+  const int e1 = mark(ix, timed, s);
   HIP_TRY(launch_scan(ix->dtype, sa, scan_grid(ix, pl.tile_q), s));
-  if (timed) HIP_TRY(hipEventRecord(ix->ev[2], s));
-  (void)ms_sched;
-  (void)ms_scan;
+  const int e2 = mark(ix, timed, s);
+  span(ix, kSched, e0, e1);
+  span(ix, kScan, e1, e2);
   return SIEVE_OK;
 }
 
@@ -270,7 +306,6 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     return fail(SIEVE_EINVAL, "current device %d differs from the index's device %d", dev,
                 ix->device);
   const bool timed = stats != nullptr;
-  if (timed && (st = alloc_events(ix))) return st;
   if ((st = grow_workspace(ix, pl))) return st;
 
   RoundCounters* rc = (RoundCounters*)ix->rc.p;
@@ -278,35 +313,31 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
   const ScanArgs sa0 = make_scan_args(ix, queries, exclude, pl);
 
   for (int attempt = 0;; ++attempt) {
-    float ms_rank = 0, ms_sched = 0, ms_scan = 0, ms_update = 0, ms_fin = 0;
-    int rounds = 0, scan_launches = 0;
+    reset_timeline(ix);
+    int rounds = 0;
     int64_t items_total = 0;
     ScanArgs sa = sa0;
     sa.pool = (Hit*)ix->pool.p;
     sa.pool_cap = ix->pool_cap;
 
-    if (timed) HIP_TRY(hipEventRecord(ix->ev[4], s));
+    const int t_begin = mark(ix, timed, s);
     HIP_TRY(launch_zero_bytes(rc, sizeof(RoundCounters), s));
     HIP_TRY(launch_fill_i32((int32_t*)ix->cnt.p, ix->nlist, 0, s));
     HIP_TRY(launch_fill_i32((int32_t*)ix->hcount.p, nq, 0, s));
     int32_t* P = (int32_t*)ix->P.p;
 
     if (pl.mode != 2) {
-      if (timed) HIP_TRY(hipEventRecord(ix->ev[0], s));
+      const int r0 = mark(ix, timed, s);
       if ((st = rank_queries(ix, queries, 0, nq, pl, P, s))) return st;
       const int s0 = pl.mode == 0 ? (pl.W < pl.n ? pl.W : pl.n) : 1;
       HIP_TRY(launch_emit_initial(P, pl.n, nq, 0, s0, pl.mode, (Item*)ix->items.p,
                                   (int32_t*)ix->cnt.p, (int32_t*)ix->state_a.p,
                                   (int32_t*)ix->state_b.p, (int32_t*)ix->lmax.p, s));
-      if (timed) {
-        HIP_TRY(hipEventRecord(ix->ev[1], s));
-        HIP_TRY(hipEventSynchronize(ix->ev[1]));
-        ms_rank += elapsed(ix, 0, 1);
-      }
+      span(ix, kRank, r0, mark(ix, timed, s));
       int64_t n_items = nq * s0;
       while (n_items > 0) {
-        if ((st = run_round(ix, sa, (int)n_items, 0, P, pl, s, timed, &ms_sched, &ms_scan)))
-          return st;
+        if ((st = run_round(ix, sa, (int)n_items, 0, P, pl, s, timed))) return st;
+        const int u0 = mark(ix, timed, s);
         if (pl.mode == 0)
           HIP_TRY(launch_update_lookahead(nq, P, pl.n, pl.W, (int32_t*)ix->state_a.p,
                                           (int32_t*)ix->lmax.p, (Item*)ix->items.p,
@@ -315,17 +346,11 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
           HIP_TRY(launch_update_basic(nq, P, pl.n, pl.W, (int32_t*)ix->state_a.p,
                                       (int32_t*)ix->state_b.p, (int32_t*)ix->lmax.p,
                                       (Item*)ix->items.p, (int32_t*)ix->cnt.p, rc, s));
-        if (timed) HIP_TRY(hipEventRecord(ix->ev[3], s));
+        span(ix, kUpdate, u0, mark(ix, timed, s));
         HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
         HIP_TRY(hipStreamSynchronize(s));
-        if (timed) {
-          ms_sched += elapsed(ix, 0, 1);
-          ms_scan += elapsed(ix, 1, 2);
-          ms_update += elapsed(ix, 2, 3);
-        }
         items_total += n_items;
         ++rounds;
-        ++scan_launches;
         if (ix->rc_host->rank_error)
           return fail(SIEVE_EUNSUPPORTED,
                       "more than %d centroids tie within the fp32 screening bound at a rank "
@@ -338,23 +363,14 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     } else {
       for (int64_t q0 = 0; q0 < nq; q0 += pl.fix_chunk) {
         const int64_t c = (nq - q0) < pl.fix_chunk ? (nq - q0) : pl.fix_chunk;
-        if (timed) HIP_TRY(hipEventRecord(ix->ev[0], s));
+        const int r0 = mark(ix, timed, s);
         if ((st = rank_queries(ix, queries, q0, c, pl, P, s))) return st;
         HIP_TRY(launch_emit_initial(P, pl.n, c, (int32_t)q0, pl.n, 2, (Item*)ix->items.p,
                                     (int32_t*)ix->cnt.p, nullptr, nullptr, nullptr, s));
-        if (timed) HIP_TRY(hipEventRecord(ix->ev[1], s));
-        if (timed) HIP_TRY(hipEventSynchronize(ix->ev[1]));
-        if (timed) ms_rank += elapsed(ix, 0, 1);
-        if ((st = run_round(ix, sa, (int)(c * pl.n), q0, P, pl, s, timed, &ms_sched, &ms_scan)))
-          return st;
-        if (timed) {
-          HIP_TRY(hipEventSynchronize(ix->ev[2]));
-          ms_sched += elapsed(ix, 0, 1);
-          ms_scan += elapsed(ix, 1, 2);
-        }
+        span(ix, kRank, r0, mark(ix, timed, s));
+        if ((st = run_round(ix, sa, (int)(c * pl.n), q0, P, pl, s, timed))) return st;
         items_total += c * pl.n;
         ++rounds;
-        ++scan_launches;
       }
       HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
       HIP_TRY(hipStreamSynchronize(s));
@@ -376,7 +392,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     }
 
     // finalize: group the pool by query, then per-query top-k
-    if (timed) HIP_TRY(hipEventRecord(ix->ev[0], s));
+    const int f0 = mark(ix, timed, s);
     HIP_TRY(launch_exclusive_scan((const int32_t*)ix->hcount.p, (int32_t*)ix->hoff.p,
                                   (int32_t*)ix->hcur.p, nq, (int32_t*)ix->scan_tmp.p, s));
     HIP_TRY(launch_pool_scatter((const Hit*)ix->pool.p, hits, (int32_t*)ix->hcur.p,
@@ -387,12 +403,15 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     HIP_TRY(launch_topk(nq, pl.k, (const Hit*)ix->pool_sorted.p, (const int32_t*)ix->hoff.p,
                         (const int32_t*)ix->hcount.p, probes_src, pl.n, out_ids, out_scores,
                         out_probes, rc, s));
-    if (timed) HIP_TRY(hipEventRecord(ix->ev[1], s));
-    if (timed) HIP_TRY(hipEventRecord(ix->ev[5], s));
+    const int f1 = mark(ix, timed, s);
+    span(ix, kFinal, f0, f1);
+    span(ix, kTotal, t_begin, f1);
     HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
     if (timed) {
-      ms_fin = elapsed(ix, 0, 1);
+      float ms[kPhases];
+      int scan_launches = 0;
+      read_timeline(ix, ms, &scan_launches);
       const RoundCounters& h = *ix->rc_host;
       const double eb = (double)ix->d * e;
       stats->rounds = rounds;
@@ -407,12 +426,12 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
                           (double)h.hits * sizeof(Hit);
       stats->scan_flops = 2.0 * (double)ix->d * (double)h.item_rows;
       stats->rank_flops = 2.0 * (double)ix->d * (double)nq * (double)ix->nlist;
-      stats->ms_rank = ms_rank;
-      stats->ms_sched = ms_sched;
-      stats->ms_scan = ms_scan;
-      stats->ms_update = ms_update;
-      stats->ms_finalize = ms_fin;
-      stats->ms_total = elapsed(ix, 4, 5);
+      stats->ms_rank = ms[kRank];
+      stats->ms_sched = ms[kSched];
+      stats->ms_scan = ms[kScan];
+      stats->ms_update = ms[kUpdate];
+      stats->ms_finalize = ms[kFinal];
+      stats->ms_total = ms[kTotal];
     }
     return SIEVE_OK;
   }
@@ -554,8 +573,7 @@ SIEVE_API void sieve_free_index(sieve_index* ix) {
   if (ix->ids) (void)hipFree(ix->ids);
   if (ix->centroids) (void)hipFree(ix->centroids);
   if (ix->rc_host) (void)hipHostFree(ix->rc_host);
-  if (ix->events)
-    for (int i = 0; i < kEvents; ++i) (void)hipEventDestroy(ix->ev[i]);
+  for (hipEvent_t e : ix->ev_pool) (void)hipEventDestroy(e);
   delete ix;
 }
 

@@ -101,46 +101,98 @@ __device__ __forceinline__ void stage_queries(u32x4* lds, const RowGeom<DT>& g, 
   }
 }
 
-// Score one 16-row block against QB query blocks.  vrow points at the
-// stored row this lane feeds (already clamped into bounds).  lane group h
-// reads segment 4*c + h of chunk c.
+// Score the 16-row block whose fragments are in b[] against qb_n query blocks
+// (compile-time dimension D: kNC chunks, fragments already in registers).
 template <int DT, int D, int QBMAX>
-__device__ __forceinline__ void score_block(const u32x4* __restrict__ lds, const RowGeom<DT>& g,
-                                            const u32x4* __restrict__ vrow, int qb_n,
-                                            f32x4 (&acc)[QBMAX]) {
+__device__ __forceinline__ void score_regs(const u32x4* __restrict__ lds, int segs,
+                                           const u32x4 (&b)[D / DTraits<DT>::kChunkDims],
+                                           int qb_n, f32x4 (&acc)[QBMAX]) {
+  constexpr int kNC = D / DTraits<DT>::kChunkDims;
   const int lane = threadIdx.x & 63;
   const int h = lane >> 4, r16 = lane & 15;
 #pragma unroll
   for (int qb = 0; qb < QBMAX; ++qb) acc[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  constexpr int kNC = D / DTraits<DT>::kChunkDims;  // compile-time chunk count (0: runtime)
-  if constexpr (kNC > 0) {
-    u32x4 b[kNC];
 #pragma unroll
-    for (int c = 0; c < kNC; ++c) b[c] = vrow[4 * c + h];
+  for (int c = 0; c < kNC; ++c) {
 #pragma unroll
-    for (int c = 0; c < kNC; ++c) {
-#pragma unroll
-      for (int qb = 0; qb < QBMAX; ++qb) {
-        if (qb < qb_n) {
-          const u32x4 a = lds[(qb * 16 + r16) * g.segs + 4 * c + h];
-          acc[qb] = mma_chunk<DT>(a, b[c], acc[qb]);
-        }
+    for (int qb = 0; qb < QBMAX; ++qb) {
+      if (qb < qb_n) {
+        const u32x4 a = lds[(qb * 16 + r16) * segs + 4 * c + h];
+        acc[qb] = mma_chunk<DT>(a, b[c], acc[qb]);
       }
     }
-  } else {
-    const u32x4 zero = {0u, 0u, 0u, 0u};
-    u32x4 bn = (h < g.dsegs) ? vrow[h] : zero;
-    for (int c = 0; c < g.nchunks; ++c) {
-      const u32x4 bc = bn;
-      const int sn = 4 * (c + 1) + h;
-      bn = (sn < g.dsegs) ? vrow[sn] : zero;
+  }
+}
+
+// Runtime-dimension variant: fragments are loaded chunk by chunk (one ahead).
+template <int DT, int QBMAX>
+__device__ __forceinline__ void score_stream(const u32x4* __restrict__ lds, const RowGeom<DT>& g,
+                                             const u32x4* __restrict__ vrow, int qb_n,
+                                             f32x4 (&acc)[QBMAX]) {
+  const int lane = threadIdx.x & 63;
+  const int h = lane >> 4, r16 = lane & 15;
 #pragma unroll
-      for (int qb = 0; qb < QBMAX; ++qb) {
-        if (qb < qb_n) {
-          const u32x4 a = lds[(qb * 16 + r16) * g.segs + 4 * c + h];
-          acc[qb] = mma_chunk<DT>(a, bc, acc[qb]);
-        }
+  for (int qb = 0; qb < QBMAX; ++qb) acc[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+  u32x4 bn = (h < g.dsegs) ? vrow[h] : zero;
+  for (int c = 0; c < g.nchunks; ++c) {
+    const u32x4 bc = bn;
+    const int sn = 4 * (c + 1) + h;
+    bn = (sn < g.dsegs) ? vrow[sn] : zero;
+#pragma unroll
+    for (int qb = 0; qb < QBMAX; ++qb) {
+      if (qb < qb_n) {
+        const u32x4 a = lds[(qb * 16 + r16) * g.segs + 4 * c + h];
+        acc[qb] = mma_chunk<DT>(a, bc, acc[qb]);
       }
+    }
+  }
+}
+
+// Stream rows [r0, r1) of a row-major store through the waves of the block:
+// wave w scores row blocks w, w + W, w + 2W, ... (W = waves per block)
+// against the staged query blocks and hands each finished block to
+// epi(acc, row) with row = the stored row this lane's column holds (may be
+// >= r1 on the last block: the epilogue masks it; loads are clamped).  With a
+// compile-time dimension, the next block's fragments are loaded while the
+// current block is multiplied.
+template <int DT, int D, int QBMAX, typename Epi>
+__device__ __forceinline__ void stream_rows(const u32x4* __restrict__ lds, const RowGeom<DT>& g,
+                                            const char* __restrict__ base, size_t row_bytes,
+                                            int64_t r0, int64_t r1, int qb_n, Epi&& epi) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nwaves = blockDim.x >> 6;
+  const int h = lane >> 4, r16 = lane & 15;
+  const int64_t nrows = r1 - r0;
+  constexpr int kNC = D / DTraits<DT>::kChunkDims;
+  if constexpr (kNC > 0) {
+    u32x4 bn[kNC];
+    int64_t rb = wave;
+    auto load = [&](int64_t blk, u32x4(&dst)[kNC]) {
+      const int64_t row = r0 + blk * 16 + r16;
+      const int64_t rowc = row < r1 ? row : r1 - 1;
+      const u32x4* vrow = (const u32x4*)(base + (size_t)rowc * row_bytes);
+#pragma unroll
+      for (int c = 0; c < kNC; ++c) dst[c] = vrow[4 * c + h];
+    };
+    if (rb * 16 < nrows) load(rb, bn);
+    for (; rb * 16 < nrows; rb += nwaves) {
+      u32x4 bc[kNC];
+#pragma unroll
+      for (int c = 0; c < kNC; ++c) bc[c] = bn[c];
+      if ((rb + nwaves) * 16 < nrows) load(rb + nwaves, bn);
+      f32x4 acc[QBMAX];
+      score_regs<DT, D, QBMAX>(lds, g.segs, bc, qb_n, acc);
+      epi(acc, r0 + rb * 16 + r16);
+    }
+  } else {
+    for (int64_t rb = wave; rb * 16 < nrows; rb += nwaves) {
+      const int64_t row = r0 + rb * 16 + r16;
+      const int64_t rowc = row < r1 ? row : r1 - 1;
+      const u32x4* vrow = (const u32x4*)(base + (size_t)rowc * row_bytes);
+      f32x4 acc[QBMAX];
+      score_stream<DT, QBMAX>(lds, g, vrow, qb_n, acc);
+      epi(acc, row);
     }
   }
 }

@@ -24,7 +24,7 @@ namespace sieve {
 namespace {
 
 template <int DT, int D>
-__global__ __launch_bounds__(kScanThreads) void scan_kernel(ScanArgs a, int qb_max) {
+__global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int qb_max) {
   extern __shared__ u32x4 lds[];
   __shared__ int s_tile;
   __shared__ int32_t s_q[kTileQ];
@@ -33,8 +33,8 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(ScanArgs a, int qb_m
 
   const int d = D > 0 ? D : a.d;
   const RowGeom<DT> g = RowGeom<DT>::make(d);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int h = lane >> 4, r16 = lane & 15;
+  const int lane = threadIdx.x & 63;
+  const int h = lane >> 4;
   const size_t row_bytes = (size_t)d * DTraits<DT>::kElem;
   const int ntiles = a.rc->ntiles;
   const int home = blockIdx.x & 7;
@@ -70,73 +70,66 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(ScanArgs a, int qb_m
       });
       __syncthreads();
 
-      const int nrows = (int)(r1 - r0);
-      const char* vbase = (const char*)a.vectors;
-      for (int rb = wave; rb * 16 < nrows; rb += kScanThreads / 64) {
-        const int64_t row = r0 + rb * 16 + r16;
-        const int64_t rowc = row < r1 ? row : r1 - 1;
-        const u32x4* vrow = (const u32x4*)(vbase + (size_t)rowc * row_bytes);
-        f32x4 acc[kQB];
-        score_block<DT, D, kQB>(lds, g, vrow, qb_n, acc);
-
-        // tau test: one wave-wide vote in the common (no candidate) case
-        bool any = false;
+      stream_rows<DT, D, kQB>(
+          lds, g, (const char*)a.vectors, row_bytes, r0, r1, qb_n,
+          [&](const f32x4(&acc)[kQB], int64_t row) {
+            // tau test: one wave-wide vote in the common (no candidate) case
+            bool any = false;
 #pragma unroll
-        for (int qb = 0; qb < kQB; ++qb) {
-          if (qb < qb_n) {
+            for (int qb = 0; qb < kQB; ++qb) {
+              if (qb < qb_n) {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int i = qb * 16 + 4 * h + r;
-              any |= (row < r1) && (i < nq) && (acc[qb][r] >= a.tau);
-            }
-          }
-        }
-        if (__ballot(any) == 0) continue;
-        if (any) {
-          const int64_t rid = a.ids[rowc];
-#pragma unroll
-          for (int qb = 0; qb < kQB; ++qb) {
-            if (qb < qb_n) {
-#pragma unroll
-              for (int r = 0; r < 4; ++r) {
-                const int i = qb * 16 + 4 * h + r;
-                const float sc = acc[qb][r];
-                if ((row < r1) && (i < nq) && (sc >= a.tau) && rid != s_ex[i]) {
-                  const int q = s_q[i];
-                  const unsigned long long slot = atomicAdd(a.pool_count, 1ull);
-                  if ((int64_t)slot < a.pool_cap) {
-                    Hit hv;
-                    hv.score = sc;
-                    hv.q = q;
-                    hv.id = rid;
-                    a.pool[slot] = hv;
-                  }
-                  atomicAdd(&a.hcount[q], 1);
-                  atomicMax(&a.lmax[q], s_rank[i] + 1);
+                for (int r = 0; r < 4; ++r) {
+                  const int i = qb * 16 + 4 * h + r;
+                  any |= (row < r1) && (i < nq) && (acc[qb][r] >= a.tau);
                 }
               }
             }
-          }
-        }
-      }
+            if (__ballot(any) == 0) return;
+            if (!any) return;
+            const int64_t rid = a.ids[row];
+#pragma unroll
+            for (int qb = 0; qb < kQB; ++qb) {
+              if (qb < qb_n) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                  const int i = qb * 16 + 4 * h + r;
+                  const float sc = acc[qb][r];
+                  if ((i < nq) && (sc >= a.tau) && rid != s_ex[i]) {
+                    const int q = s_q[i];
+                    const unsigned long long slot = atomicAdd(a.pool_count, 1ull);
+                    if ((int64_t)slot < a.pool_cap) {
+                      Hit hv;
+                      hv.score = sc;
+                      hv.q = q;
+                      hv.id = rid;
+                      a.pool[slot] = hv;
+                    }
+                    atomicAdd(&a.hcount[q], 1);
+                    atomicMax(&a.lmax[q], s_rank[i] + 1);
+                  }
+                }
+              }
+            }
+          });
       __syncthreads();  // LDS is restaged by the next tile
     }
   }
 }
 
 // Centroid screen: scores[qi - q0][c] = fp32 <query qi, centroid c> for a
-// chunk of queries.  Grid: (ceil(nqc / kTileQ), ceil(nlist / 64)).
+// chunk of queries.  Grid: (ceil(nqc / rows), ceil(nlist / kScreenCents)).
+constexpr int kScreenCents = 256;
+
 template <int DT, int D>
-__global__ __launch_bounds__(kScanThreads) void rank_scores_kernel(const void* queries, int64_t q0,
-                                                                   int32_t nqc,
-                                                                   const void* centroids,
-                                                                   int32_t nlist, int32_t dd,
-                                                                   int32_t rows, float* scores) {
+__global__ __launch_bounds__(kScanThreads, 2) void rank_scores_kernel(
+    const void* queries, int64_t q0, int32_t nqc, const void* centroids, int32_t nlist,
+    int32_t dd, int32_t rows, float* scores) {
   extern __shared__ u32x4 lds[];
   const int d = D > 0 ? D : dd;
   const RowGeom<DT> g = RowGeom<DT>::make(d);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int h = lane >> 4, r16 = lane & 15;
+  const int lane = threadIdx.x & 63;
+  const int h = lane >> 4;
   const size_t row_bytes = (size_t)d * DTraits<DT>::kElem;
   const int qt0 = blockIdx.x * rows;
   const int nq = min(rows, nqc - qt0);
@@ -146,22 +139,22 @@ __global__ __launch_bounds__(kScanThreads) void rank_scores_kernel(const void* q
     return i < nq ? (const u32x4*)(qbase + (size_t)i * row_bytes) : nullptr;
   });
   __syncthreads();
-  const int c = blockIdx.y * 64 + wave * 16 + r16;
-  const int cc = c < nlist ? c : nlist - 1;
-  const u32x4* vrow = (const u32x4*)((const char*)centroids + (size_t)cc * row_bytes);
-  f32x4 acc[kQB];
-  score_block<DT, D, kQB>(lds, g, vrow, qb_n, acc);
-  if (c >= nlist) return;
+  const int64_t c0 = (int64_t)blockIdx.y * kScreenCents;
+  const int64_t c1 = min<int64_t>(nlist, c0 + kScreenCents);
+  stream_rows<DT, D, kQB>(lds, g, (const char*)centroids, row_bytes, c0, c1, qb_n,
+                          [&](const f32x4(&acc)[kQB], int64_t c) {
+                            if (c >= c1) return;
 #pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) {
-    if (qb < qb_n) {
+                            for (int qb = 0; qb < kQB; ++qb) {
+                              if (qb < qb_n) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int i = qb * 16 + 4 * h + r;
-        if (i < nq) scores[(size_t)(qt0 + i) * nlist + c] = acc[qb][r];
-      }
-    }
-  }
+                                for (int r = 0; r < 4; ++r) {
+                                  const int i = qb * 16 + 4 * h + r;
+                                  if (i < nq) scores[(size_t)(qt0 + i) * nlist + c] = acc[qb][r];
+                                }
+                              }
+                            }
+                          });
 }
 
 // Dynamic LDS above 64 KB must be opted into once per kernel.
@@ -189,7 +182,7 @@ hipError_t launch_rank_scores_t(const void* queries, int64_t q0, int32_t nqc,
   const int rows = tile_rows(DT, d);
   const size_t lds = (size_t)rows * lds_row_bytes<DT>(d);
   if (lds > (size_t)kMaxDynLds) return hipErrorInvalidValue;
-  dim3 grid((nqc + rows - 1) / rows, (nlist + 63) / 64);
+  dim3 grid((nqc + rows - 1) / rows, (nlist + kScreenCents - 1) / kScreenCents);
   hipLaunchKernelGGL((rank_scores_kernel<DT, D>), grid, dim3(kScanThreads), lds, s, queries, q0,
                      nqc, centroids, nlist, d, rows, scores);
   return hipGetLastError();
@@ -219,7 +212,6 @@ hipError_t launch_scan(int dtype, const ScanArgs& a, int32_t grid, hipStream_t s
   }
   switch (a.d) {
     case 128: return launch_scan_t<SIEVE_F16, 128>(a, grid, s);
-    case 768: return launch_scan_t<SIEVE_F16, 768>(a, grid, s);
     default: return launch_scan_t<SIEVE_F16, 0>(a, grid, s);
   }
 }
@@ -236,7 +228,6 @@ hipError_t launch_rank_scores(int dtype, const void* queries, int64_t q0, int32_
   }
   switch (d) {
     case 128: return launch_rank_scores_t<SIEVE_F16, 128>(queries, q0, nqc, centroids, nlist, d, scores, s);
-    case 768: return launch_rank_scores_t<SIEVE_F16, 768>(queries, q0, nqc, centroids, nlist, d, scores, s);
     default: return launch_rank_scores_t<SIEVE_F16, 0>(queries, q0, nqc, centroids, nlist, d, scores, s);
   }
 }

@@ -154,7 +154,12 @@ __global__ __launch_bounds__(256) void topk_kernel(int64_t nq, int32_t k,
                                                    RoundCounters* rc) {
   const int lane = threadIdx.x & 63;
   const int64_t q = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (q >= nq) return;
+  __shared__ int32_t s_probes[4];
+  if (q >= nq) {
+    if (lane == 0) s_probes[threadIdx.x >> 6] = 0;
+    __syncthreads();
+    return;
+  }
   const int m = hcount[q];
   const int beg = m > 0 ? hoff[q] : 0;
   const Cand none = {-INFINITY, 0x7fffffffffffffffll};
@@ -183,8 +188,12 @@ __global__ __launch_bounds__(256) void topk_kernel(int64_t nq, int32_t k,
   if (lane == 0) {
     const int32_t p = probes_src ? probes_src[q] : probes_const;
     out_probes[q] = p;
-    atomicAdd(&rc->probes, (unsigned long long)p);
+    s_probes[threadIdx.x >> 6] = p;
   }
+  __syncthreads();  // one atomic per block for the probe total
+  if (threadIdx.x == 0)
+    atomicAdd(&rc->probes, (unsigned long long)(s_probes[0] + s_probes[1] + s_probes[2] +
+                                                 s_probes[3]));
 }
 
 }  // namespace

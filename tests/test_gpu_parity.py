@@ -228,3 +228,15 @@ def test_invalid_arguments_leave_outputs_untouched():
             c.ix.search(q, c.w.exclude_ids, args["k"], args["tau"], args["W"],
                         args["nprobe_max"])
         assert e.value.code == -1
+
+
+@pytest.mark.parametrize("name", ["tiny", "tiny16", "c1"])
+def test_rank_order_matches_oracle_exactly(name):
+    """Kernel (1): the probe order equals the oracle's fp64 order, all ranks."""
+    c = case(name)
+    nl = c.w.spec.nlist
+    P = c.ix.rank(c.w.queries, nl).cpu().numpy()
+    h = c.h
+    o = oracle.search(h["vectors"], h["list_offsets"], h["ids"], h["centroids"], h["queries"],
+                      h["exclude_ids"], 1, 2.0, 1, nl, want_order=True, nthreads=NTHREADS)
+    assert np.array_equal(P, o.order)
