@@ -70,9 +70,11 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="c2")
-    ap.add_argument("--oracle-queries", type=int, default=4000,
+    ap.add_argument("--oracle-queries", type=int, default=10000,
                     help="queries in the single-thread oracle sample")
     ap.add_argument("--no-oracle", action="store_true")
+    ap.add_argument("--skip-fixed", action="store_true",
+                    help="do not time the fixed-probe baseline (profiling runs)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -115,7 +117,8 @@ def main():
 
     for _ in range(args.warmup):
         sieve()
-        fixed()
+        if not args.skip_fixed:
+            fixed()
     torch.cuda.synchronize()
 
     # timed region: exactly K sieve steps
@@ -134,11 +137,11 @@ def main():
     fstats = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for _ in range(0 if args.skip_fixed else args.steps):
         fr = fixed()
         fstats.append(fr[3])
     torch.cuda.synchronize()
-    t_fixed = time.perf_counter() - t0
+    t_fixed = time.perf_counter() - t0 if not args.skip_fixed else float("nan")
 
     ms_step = 1e3 * t_sieve / args.steps
     qps = nq * args.steps / t_sieve
@@ -196,8 +199,8 @@ def main():
         "rounds": st.rounds,
         "phase_ms": {k: round(mean(stats, "ms_" + k), 4) for k in
                      ("rank", "sched", "scan", "update", "finalize", "total")},
-        "fixed_phase_ms": {k: round(mean(fstats, "ms_" + k), 4) for k in
-                           ("rank", "sched", "scan", "finalize", "total")},
+        "fixed_phase_ms": ({k: round(mean(fstats, "ms_" + k), 4) for k in
+                            ("rank", "sched", "scan", "finalize", "total")} if fstats else None),
         "roofline": roof,
     }
 

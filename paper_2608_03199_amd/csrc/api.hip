@@ -12,6 +12,7 @@
 // Fixed probing runs the same kernels with every rank admitted up front, in
 // query chunks, without updates and without per-chunk syncs.
 #include <math.h>
+#include <stdlib.h>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -160,17 +161,32 @@ void read_timeline(sieve_index* ix, float* ms, int* scan_spans) {
   }
 }
 
-// Tunables of the scan decomposition (they never change results).
+// Tunables of the scan decomposition.  They never change results; the
+// SIEVE_* environment variables override them for tuning sweeps.
+int env_int(const char* name, int dflt) {
+  const char* v = getenv(name);
+  if (!v || !*v) return dflt;
+  const int x = atoi(v);
+  return x > 0 ? x : dflt;
+}
+
 int row_chunk_for(const sieve_index* ix) {
   (void)ix;
-  return 512;
+  const int rc = env_int("SIEVE_ROW_CHUNK", 512);
+  return ((rc + 63) / 64) * 64;
 }
 
 int scan_grid(const sieve_index* ix, int tile_q) {
   const size_t lds = scan_lds_bytes(ix->dtype, ix->d, tile_q) + 4096;
   int per_cu = (int)((160 * 1024) / lds);
-  per_cu = per_cu < 1 ? 1 : (per_cu > 4 ? 4 : per_cu);
-  return ix->cus * per_cu;
+  per_cu = per_cu < 1 ? 1 : (per_cu > 2 ? 2 : per_cu);
+  per_cu = env_int("SIEVE_SCAN_BLOCKS_PER_CU", per_cu);
+  return ((ix->cus * per_cu + 7) / 8) * 8;  // the scan's schedule needs a multiple of 8
+}
+
+// Large rounds balance better with the atomic queue, small ones without it.
+int scan_dynamic(int64_t n_items) {
+  return n_items >= (int64_t)env_int("SIEVE_DYNAMIC_MIN_ITEMS", 200000) ? 1 : 0;
 }
 
 struct SearchPlan {
@@ -289,7 +305,9 @@ int run_round(sieve_index* ix, const ScanArgs& sa, int n_items, int64_t q0, cons
                              (const int32_t*)ix->tile_off.p, ix->offsets, ix->nlist, pl.row_chunk,
                              pl.tile_q, (Tile*)ix->tiles.p, s));
   const int e1 = mark(ix, timed, s);
-  HIP_TRY(launch_scan(ix->dtype, sa, scan_grid(ix, pl.tile_q), s));
+  ScanArgs sr = sa;
+  sr.dynamic = scan_dynamic(n_items);
+  HIP_TRY(launch_scan(ix->dtype, sr, scan_grid(ix, pl.tile_q), s));
   const int e2 = mark(ix, timed, s);
   span(ix, kSched, e0, e1);
   span(ix, kScan, e1, e2);

@@ -101,38 +101,49 @@ __device__ __forceinline__ void stage_queries(u32x4* lds, const RowGeom<DT>& g, 
   }
 }
 
-// Score the 16-row block whose fragments are in b[] against qb_n query blocks
+// Score the 16-row block whose fragments are in b[] against QB query blocks
 // (compile-time dimension D: kNC chunks, fragments already in registers).
-template <int DT, int D, int QBMAX>
+// Fully unrolled and software-pipelined: the query fragments of chunk c + 1
+// are read from LDS while chunk c's MFMAs issue; a scheduling fence after
+// each chunk keeps the compiler from hoisting every LDS read (which would
+// cost registers and occupancy).
+template <int DT, int D, int QB>
 __device__ __forceinline__ void score_regs(const u32x4* __restrict__ lds, int segs,
                                            const u32x4 (&b)[D / DTraits<DT>::kChunkDims],
-                                           int qb_n, f32x4 (&acc)[QBMAX]) {
+                                           f32x4 (&acc)[QB]) {
   constexpr int kNC = D / DTraits<DT>::kChunkDims;
   const int lane = threadIdx.x & 63;
   const int h = lane >> 4, r16 = lane & 15;
+  const u32x4* arow = lds + r16 * segs + h;
+  u32x4 a0[QB], a1[QB];
 #pragma unroll
-  for (int qb = 0; qb < QBMAX; ++qb) acc[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int qb = 0; qb < QB; ++qb) {
+    acc[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    a0[qb] = arow[qb * 16 * segs];
+  }
 #pragma unroll
   for (int c = 0; c < kNC; ++c) {
+    u32x4(&cur)[QB] = (c & 1) ? a1 : a0;
+    u32x4(&nxt)[QB] = (c & 1) ? a0 : a1;
+    if (c + 1 < kNC) {
 #pragma unroll
-    for (int qb = 0; qb < QBMAX; ++qb) {
-      if (qb < qb_n) {
-        const u32x4 a = lds[(qb * 16 + r16) * segs + 4 * c + h];
-        acc[qb] = mma_chunk<DT>(a, b[c], acc[qb]);
-      }
+      for (int qb = 0; qb < QB; ++qb) nxt[qb] = arow[qb * 16 * segs + 4 * (c + 1)];
     }
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) acc[qb] = mma_chunk<DT>(cur[qb], b[c], acc[qb]);
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
 // Runtime-dimension variant: fragments are loaded chunk by chunk (one ahead).
-template <int DT, int QBMAX>
+template <int DT, int QB>
 __device__ __forceinline__ void score_stream(const u32x4* __restrict__ lds, const RowGeom<DT>& g,
-                                             const u32x4* __restrict__ vrow, int qb_n,
-                                             f32x4 (&acc)[QBMAX]) {
+                                             const u32x4* __restrict__ vrow, f32x4 (&acc)[QB]) {
   const int lane = threadIdx.x & 63;
   const int h = lane >> 4, r16 = lane & 15;
+  const u32x4* arow = lds + r16 * g.segs + h;
 #pragma unroll
-  for (int qb = 0; qb < QBMAX; ++qb) acc[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int qb = 0; qb < QB; ++qb) acc[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
   const u32x4 zero = {0u, 0u, 0u, 0u};
   u32x4 bn = (h < g.dsegs) ? vrow[h] : zero;
   for (int c = 0; c < g.nchunks; ++c) {
@@ -140,60 +151,90 @@ __device__ __forceinline__ void score_stream(const u32x4* __restrict__ lds, cons
     const int sn = 4 * (c + 1) + h;
     bn = (sn < g.dsegs) ? vrow[sn] : zero;
 #pragma unroll
-    for (int qb = 0; qb < QBMAX; ++qb) {
-      if (qb < qb_n) {
-        const u32x4 a = lds[(qb * 16 + r16) * g.segs + 4 * c + h];
-        acc[qb] = mma_chunk<DT>(a, bc, acc[qb]);
-      }
+    for (int qb = 0; qb < QB; ++qb) {
+      const u32x4 av = arow[qb * 16 * g.segs + 4 * c];
+      acc[qb] = mma_chunk<DT>(av, bc, acc[qb]);
     }
   }
 }
 
 // Stream rows [r0, r1) of a row-major store through the waves of the block:
 // wave w scores row blocks w, w + W, w + 2W, ... (W = waves per block)
-// against the staged query blocks and hands each finished block to
-// epi(acc, row) with row = the stored row this lane's column holds (may be
-// >= r1 on the last block: the epilogue masks it; loads are clamped).  With a
-// compile-time dimension, the next block's fragments are loaded while the
-// current block is multiplied.
-template <int DT, int D, int QBMAX, typename Epi>
-__device__ __forceinline__ void stream_rows(const u32x4* __restrict__ lds, const RowGeom<DT>& g,
-                                            const char* __restrict__ base, size_t row_bytes,
-                                            int64_t r0, int64_t r1, int qb_n, Epi&& epi) {
+// against QB staged query blocks and hands each finished block to
+// epi(acc, row, rid), row = the stored row this lane's column holds (it may
+// be >= r1 on the last block: the epilogue masks it; loads are clamped) and
+// rid = ids[row] when an id array is given (else 0).  With a compile-time
+// dimension, two fragment buffers alternate so that the next block's
+// fragments (and ids) load while the current block is multiplied.
+template <int DT, int D, int QB, typename Epi>
+__device__ __forceinline__ void stream_rows_qb(const u32x4* __restrict__ lds,
+                                               const RowGeom<DT>& g,
+                                               const char* __restrict__ base, size_t row_bytes,
+                                               const int64_t* __restrict__ ids, int64_t r0,
+                                               int64_t r1, Epi& epi) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nwaves = blockDim.x >> 6;
   const int h = lane >> 4, r16 = lane & 15;
   const int64_t nrows = r1 - r0;
   constexpr int kNC = D / DTraits<DT>::kChunkDims;
   if constexpr (kNC > 0) {
-    u32x4 bn[kNC];
-    int64_t rb = wave;
-    auto load = [&](int64_t blk, u32x4(&dst)[kNC]) {
+    auto load = [&](int64_t blk, u32x4(&dst)[kNC], int64_t& rid) {
       const int64_t row = r0 + blk * 16 + r16;
       const int64_t rowc = row < r1 ? row : r1 - 1;
-      const u32x4* vrow = (const u32x4*)(base + (size_t)rowc * row_bytes);
+      const u32x4* vrow = (const u32x4*)(base + (size_t)rowc * row_bytes) + h;
 #pragma unroll
-      for (int c = 0; c < kNC; ++c) dst[c] = vrow[4 * c + h];
+      for (int c = 0; c < kNC; ++c) dst[c] = vrow[4 * c];
+      rid = ids ? ids[rowc] : 0;
     };
-    if (rb * 16 < nrows) load(rb, bn);
-    for (; rb * 16 < nrows; rb += nwaves) {
-      u32x4 bc[kNC];
-#pragma unroll
-      for (int c = 0; c < kNC; ++c) bc[c] = bn[c];
-      if ((rb + nwaves) * 16 < nrows) load(rb + nwaves, bn);
-      f32x4 acc[QBMAX];
-      score_regs<DT, D, QBMAX>(lds, g.segs, bc, qb_n, acc);
-      epi(acc, r0 + rb * 16 + r16);
+    u32x4 b0[kNC], b1[kNC];
+    int64_t id0 = 0, id1 = 0;
+    int64_t rb = wave;
+    if (rb * 16 < nrows) load(rb, b0, id0);
+    while (rb * 16 < nrows) {
+      if ((rb + nwaves) * 16 < nrows) load(rb + nwaves, b1, id1);
+      {
+        f32x4 acc[QB];
+        score_regs<DT, D, QB>(lds, g.segs, b0, acc);
+        epi(acc, r0 + rb * 16 + r16, id0);
+      }
+      rb += nwaves;
+      if (rb * 16 >= nrows) break;
+      if ((rb + nwaves) * 16 < nrows) load(rb + nwaves, b0, id0);
+      {
+        f32x4 acc[QB];
+        score_regs<DT, D, QB>(lds, g.segs, b1, acc);
+        epi(acc, r0 + rb * 16 + r16, id1);
+      }
+      rb += nwaves;
     }
   } else {
     for (int64_t rb = wave; rb * 16 < nrows; rb += nwaves) {
       const int64_t row = r0 + rb * 16 + r16;
       const int64_t rowc = row < r1 ? row : r1 - 1;
       const u32x4* vrow = (const u32x4*)(base + (size_t)rowc * row_bytes);
-      f32x4 acc[QBMAX];
-      score_stream<DT, QBMAX>(lds, g, vrow, qb_n, acc);
-      epi(acc, row);
+      const int64_t rid = ids ? ids[rowc] : 0;
+      f32x4 acc[QB];
+      score_stream<DT, QB>(lds, g, vrow, acc);
+      epi(acc, row, rid);
     }
+  }
+}
+
+// Dispatch on the tile's number of 16-query blocks (uniform per tile).
+template <int DT, int D, typename Epi>
+__device__ __forceinline__ void stream_rows(const u32x4* __restrict__ lds, const RowGeom<DT>& g,
+                                            const char* __restrict__ base, size_t row_bytes,
+                                            const int64_t* __restrict__ ids, int64_t r0,
+                                            int64_t r1, int qb_n, Epi&& epi) {
+  switch (qb_n) {
+    case 1: stream_rows_qb<DT, D, 1>(lds, g, base, row_bytes, ids, r0, r1, epi); break;
+    case 2: stream_rows_qb<DT, D, 2>(lds, g, base, row_bytes, ids, r0, r1, epi); break;
+    case 3: stream_rows_qb<DT, D, 3>(lds, g, base, row_bytes, ids, r0, r1, epi); break;
+    case 4: stream_rows_qb<DT, D, 4>(lds, g, base, row_bytes, ids, r0, r1, epi); break;
+    case 5: stream_rows_qb<DT, D, 5>(lds, g, base, row_bytes, ids, r0, r1, epi); break;
+    case 6: stream_rows_qb<DT, D, 6>(lds, g, base, row_bytes, ids, r0, r1, epi); break;
+    case 7: stream_rows_qb<DT, D, 7>(lds, g, base, row_bytes, ids, r0, r1, epi); break;
+    default: stream_rows_qb<DT, D, 8>(lds, g, base, row_bytes, ids, r0, r1, epi); break;
   }
 }
 

@@ -37,6 +37,37 @@ __device__ __forceinline__ double load_elem(const void* base, int64_t i) {
     return (double)((const _Float16*)base)[i];
 }
 
+// fp64 sum over dimensions in ascending order of exact products q_t * c_t
+// (the products of two fp32 or fp16 values are exact in fp64, so fused and
+// unfused multiply-adds agree).  Rows are read 16 bytes at a time so that
+// loads run ahead of the dependent accumulation.
+template <int DT>
+__device__ __forceinline__ double dot_fp64(const void* __restrict__ queries, int64_t q,
+                                           const void* __restrict__ centroids, int c, int d) {
+  typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+  constexpr int per = DT == SIEVE_F32 ? 4 : 8;  // elements per 16 bytes
+  const int nseg = d / per;                     // d is a multiple of 8
+  const u4* qa = (const u4*)((const char*)queries + (size_t)q * d * (DT == SIEVE_F32 ? 4 : 2));
+  const u4* ca = (const u4*)((const char*)centroids + (size_t)c * d * (DT == SIEVE_F32 ? 4 : 2));
+  double s = 0.0;
+#pragma unroll 4
+  for (int g = 0; g < nseg; ++g) {
+    const u4 qv = qa[g], cv = ca[g];
+    if constexpr (DT == SIEVE_F32) {
+      const float* qf = (const float*)&qv;
+      const float* cf = (const float*)&cv;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) s += (double)qf[e] * (double)cf[e];
+    } else {
+      const _Float16* qh = (const _Float16*)&qv;
+      const _Float16* ch = (const _Float16*)&cv;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s += (double)qh[e] * (double)ch[e];
+    }
+  }
+  return s;
+}
+
 template <int DT>
 __global__ __launch_bounds__(kThreads) void rank_select_kernel(
     const void* __restrict__ queries, int64_t q0, const void* __restrict__ centroids,
@@ -50,6 +81,7 @@ __global__ __launch_bounds__(kThreads) void rank_select_kernel(
   __shared__ int s_remaining;
   __shared__ int s_m;
   __shared__ double s_red[kThreads / 64];
+  __shared__ int s_wsum[kThreads / 64];
 
   int capp = 1;
   while (capp < cap) capp <<= 1;
@@ -80,27 +112,32 @@ __global__ __launch_bounds__(kThreads) void rank_select_kernel(
   for (int w = 0; w < kThreads / 64; ++w) qn += s_red[w];
   qn = sqrt(qn);
 
-  // 1. radix select of the n-th largest key
+  // 1. radix select of the n-th largest key, 8 bits per pass; the digit of
+  // each pass is found by a block-wide inclusive scan over the 256 bins taken
+  // from the highest digit down (thread t holds digit 255 - t).
   for (int shift = 24; shift >= 0; shift -= 8) {
     hist[t] = 0;  // kThreads == 256 bins
     __syncthreads();
     const uint32_t hi_mask = shift == 24 ? 0u : (0xffffffffu << (shift + 8));
     const uint32_t prefix = s_prefix;
+    const int rem = s_remaining;
     for (int c = t; c < nlist; c += kThreads) {
       const uint32_t k = keys[c];
       if ((k & hi_mask) == prefix) atomicAdd(&hist[(k >> shift) & 255], 1);
     }
     __syncthreads();
-    if (t == 0) {
-      int acc = 0, rem = s_remaining;
-      for (int dg = 255; dg >= 0; --dg) {
-        if (acc + hist[dg] >= rem) {
-          s_prefix = prefix | ((uint32_t)dg << shift);
-          s_remaining = rem - acc;
-          break;
-        }
-        acc += hist[dg];
-      }
+    const int v = hist[255 - t];
+    int incl = v;
+    for (int o = 1; o < 64; o <<= 1) {
+      const int u = __shfl_up(incl, o);
+      if ((t & 63) >= o) incl += u;
+    }
+    if ((t & 63) == 63) s_wsum[t >> 6] = incl;
+    __syncthreads();
+    for (int w = 0; w < (t >> 6); ++w) incl += s_wsum[w];
+    if (incl >= rem && incl - v < rem) {
+      s_prefix = prefix | ((uint32_t)(255 - t) << shift);
+      s_remaining = rem - (incl - v);
     }
     __syncthreads();
   }
@@ -157,13 +194,7 @@ __global__ __launch_bounds__(kThreads) void rank_select_kernel(
   __syncthreads();
   for (int i = t; i < m; i += kThreads) {
     const bool member = link[i] || (i > 0 && link[i - 1]);
-    if (member) {
-      const int c = (int)(ck[i] & 0xffffffffu);
-      double s = 0.0;
-      for (int u = 0; u < d; ++u)
-        s += load_elem<DT>(queries, qg * d + u) * load_elem<DT>(centroids, (int64_t)c * d + u);
-      cs[i] = s;
-    }
+    if (member) cs[i] = dot_fp64<DT>(queries, qg, centroids, (int)(ck[i] & 0xffffffffu), d);
   }
   __syncthreads();
   // 3c. insertion sort of every run by (s64 desc, c asc)

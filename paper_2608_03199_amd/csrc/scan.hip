@@ -13,11 +13,9 @@
 // score, never on other candidates, so it is the same whatever the dispatch
 // order (the property the lookahead equivalence of Sec. 4.3 needs).
 //
-// Work distribution: a persistent grid pulls tiles from 8 contiguous ranges,
-// one per XCD (a block starts on the range of blockIdx % 8, the XCD it is
-// dispatched to, so tiles of the same list share that XCD's L2), and steals
-// from the other ranges once its own is drained.  Every block exits after at
-// most (tiles + 8) queue pops.
+// Work distribution: a persistent grid pulls tiles from a per-XCD work queue
+// (see the kernel); every block exits after its claims run dry, at most
+// tiles + 8 claims per block.
 #include "mfma_tile.h"
 
 namespace sieve {
@@ -26,7 +24,6 @@ namespace {
 template <int DT, int D>
 __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int qb_max) {
   extern __shared__ u32x4 lds[];
-  __shared__ int s_tile;
   __shared__ int32_t s_q[kTileQ];
   __shared__ int32_t s_rank[kTileQ];
   __shared__ int64_t s_ex[kTileQ];
@@ -37,83 +34,125 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
   const int h = lane >> 4;
   const size_t row_bytes = (size_t)d * DTraits<DT>::kElem;
   const int ntiles = a.rc->ntiles;
+  __shared__ int s_claim;
+
+  // Tile schedule: the round's tiles are split into 8 contiguous ranges, one
+  // per XCD (block b runs on XCD b % 8, so tiles of one list share that XCD's
+  // L2).  Static: the blocks of an XCD take its range's tiles in a fixed
+  // stride (no atomics; best for small rounds).  Dynamic: thread 0 claims
+  // tiles from its XCD's range with an atomic counter and moves on to the
+  // other ranges once it is drained (balances large rounds).  A block always
+  // holds two claims ahead: the tile it runs, whose descriptor and items were
+  // prefetched, and the next one, whose loads are issued under this tile's
+  // MFMAs; the claim after that is made then too and read after the MFMAs.
   const int home = blockIdx.x & 7;
+  int xq = 0;    // thread 0, dynamic schedule: ranges already drained
+  int kseq = 0;  // thread 0, static schedule: tiles taken so far
+  auto claim = [&]() -> int {
+    if (!a.dynamic) {
+      // static: block (home, slot) takes every (grid/8)-th tile of its range
+      const int b = (int)(((int64_t)ntiles * home) / 8);
+      const int e = (int)(((int64_t)ntiles * (home + 1)) / 8);
+      const int tt = b + (blockIdx.x >> 3) + kseq * (int)(gridDim.x >> 3);
+      ++kseq;
+      return tt < e ? tt : -1;
+    }
+    while (xq < 8) {
+      const int x = (home + xq) & 7;
+      const int b = (int)(((int64_t)ntiles * x) / 8), e = (int)(((int64_t)ntiles * (x + 1)) / 8);
+      const int i = atomicAdd(&a.rc->queue[x], 1);
+      if (b + i < e) return b + i;
+      ++xq;
+    }
+    return -1;
+  };
 
-  for (int xi = 0; xi < 8; ++xi) {
-    const int x = (home + xi) & 7;
-    const int t_begin = (int)(((int64_t)ntiles * x) / 8);
-    const int t_end = (int)(((int64_t)ntiles * (x + 1)) / 8);
-    for (;;) {
-      if (threadIdx.x == 0) s_tile = t_begin + atomicAdd(&a.rc->queue[x], 1);
-      __syncthreads();
-      const int t = s_tile;
-      __syncthreads();
-      if (t >= t_end) break;
-      const Tile tile = a.tiles[t];
-      const int nq = tile.nq;
-      const int qb_n = (nq + 15) >> 4;
-      const int64_t list_begin = a.list_offsets[tile.list];
-      const int64_t list_end = a.list_offsets[tile.list + 1];
-      const int64_t r0 = list_begin + (int64_t)tile.chunk * a.row_chunk;
-      const int64_t r1 = min(list_end, r0 + a.row_chunk);
+  // prefetched state of the tile to run next
+  Tile nt = {};
+  Item nit = {};
+  int64_t nex = INT64_MIN, nr0 = 0, nr1 = 0;
+  auto prefetch = [&](int tt) {
+    if (tt < 0) return;
+    nt = a.tiles[tt];
+    const int64_t lb = a.list_offsets[nt.list];
+    nr0 = lb + (int64_t)nt.chunk * a.row_chunk;
+    nr1 = min(a.list_offsets[nt.list + 1], nr0 + a.row_chunk);
+    if ((int)threadIdx.x < nt.nq) {
+      nit = a.bucket[nt.item_begin + threadIdx.x];
+      nex = a.exclude ? a.exclude[nit.q] : INT64_MIN;
+    }
+  };
+  if (threadIdx.x == 0) s_claim = claim();
+  __syncthreads();
+  int t = s_claim;
+  __syncthreads();
+  if (threadIdx.x == 0) s_claim = claim();
+  __syncthreads();
+  int t_next = s_claim;
+  prefetch(t);
+  for (; t >= 0;) {
+    const Tile tile = nt;
+    if ((int)threadIdx.x < tile.nq) {
+      s_q[threadIdx.x] = nit.q;
+      s_rank[threadIdx.x] = nit.rank;
+      s_ex[threadIdx.x] = nex;
+    }
+    __syncthreads();
+    const int nq = tile.nq;
+    const int qb_n = (nq + 15) >> 4;
+    const int64_t r0 = nr0, r1 = nr1;
+    const char* qbase = (const char*)a.queries;
+    stage_queries<DT>(lds, g, qb_n * 16, [&](int i) -> const u32x4* {
+      return i < nq ? (const u32x4*)(qbase + (size_t)s_q[i] * row_bytes) : nullptr;
+    });
+    __syncthreads();
+    prefetch(t_next);  // next tile's descriptor and items load under this tile's MFMAs
+    int t_after = -1;
+    if (threadIdx.x == 0) t_after = claim();  // read after the MFMAs
 
-      if (threadIdx.x < nq) {
-        const Item it = a.bucket[tile.item_begin + threadIdx.x];
-        s_q[threadIdx.x] = it.q;
-        s_rank[threadIdx.x] = it.rank;
-        s_ex[threadIdx.x] = a.exclude ? a.exclude[it.q] : INT64_MIN;
-      }
-      __syncthreads();
-      const char* qbase = (const char*)a.queries;
-      stage_queries<DT>(lds, g, qb_n * 16, [&](int i) -> const u32x4* {
-        return i < nq ? (const u32x4*)(qbase + (size_t)s_q[i] * row_bytes) : nullptr;
-      });
-      __syncthreads();
-
-      stream_rows<DT, D, kQB>(
-          lds, g, (const char*)a.vectors, row_bytes, r0, r1, qb_n,
-          [&](const f32x4(&acc)[kQB], int64_t row) {
+    stream_rows<DT, D>(
+          lds, g, (const char*)a.vectors, row_bytes, a.ids, r0, r1, qb_n,
+          [&](const auto& acc, int64_t row, int64_t rid) {
+            constexpr int QB = sizeof(acc) / sizeof(acc[0]);
             // tau test: one wave-wide vote in the common (no candidate) case
             bool any = false;
 #pragma unroll
-            for (int qb = 0; qb < kQB; ++qb) {
-              if (qb < qb_n) {
+            for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                  const int i = qb * 16 + 4 * h + r;
-                  any |= (row < r1) && (i < nq) && (acc[qb][r] >= a.tau);
-                }
+              for (int r = 0; r < 4; ++r) {
+                const int i = qb * 16 + 4 * h + r;
+                any |= (row < r1) && (i < nq) && (acc[qb][r] >= a.tau);
               }
             }
             if (__ballot(any) == 0) return;
             if (!any) return;
-            const int64_t rid = a.ids[row];
 #pragma unroll
-            for (int qb = 0; qb < kQB; ++qb) {
-              if (qb < qb_n) {
+            for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                  const int i = qb * 16 + 4 * h + r;
-                  const float sc = acc[qb][r];
-                  if ((i < nq) && (sc >= a.tau) && rid != s_ex[i]) {
-                    const int q = s_q[i];
-                    const unsigned long long slot = atomicAdd(a.pool_count, 1ull);
-                    if ((int64_t)slot < a.pool_cap) {
-                      Hit hv;
-                      hv.score = sc;
-                      hv.q = q;
-                      hv.id = rid;
-                      a.pool[slot] = hv;
-                    }
-                    atomicAdd(&a.hcount[q], 1);
-                    atomicMax(&a.lmax[q], s_rank[i] + 1);
+              for (int r = 0; r < 4; ++r) {
+                const int i = qb * 16 + 4 * h + r;
+                const float sc = acc[qb][r];
+                if ((i < nq) && (sc >= a.tau) && rid != s_ex[i]) {
+                  const int q = s_q[i];
+                  const unsigned long long slot = atomicAdd(a.pool_count, 1ull);
+                  if ((int64_t)slot < a.pool_cap) {
+                    Hit hv;
+                    hv.score = sc;
+                    hv.q = q;
+                    hv.id = rid;
+                    a.pool[slot] = hv;
                   }
+                  atomicAdd(&a.hcount[q], 1);
+                  atomicMax(&a.lmax[q], s_rank[i] + 1);
                 }
               }
             }
           });
-      __syncthreads();  // LDS is restaged by the next tile
-    }
+    __syncthreads();  // LDS is restaged by the next tile
+    if (threadIdx.x == 0) s_claim = t_after;
+    __syncthreads();
+    t = t_next;
+    t_next = s_claim;
   }
 }
 
@@ -141,20 +180,19 @@ __global__ __launch_bounds__(kScanThreads, 2) void rank_scores_kernel(
   __syncthreads();
   const int64_t c0 = (int64_t)blockIdx.y * kScreenCents;
   const int64_t c1 = min<int64_t>(nlist, c0 + kScreenCents);
-  stream_rows<DT, D, kQB>(lds, g, (const char*)centroids, row_bytes, c0, c1, qb_n,
-                          [&](const f32x4(&acc)[kQB], int64_t c) {
-                            if (c >= c1) return;
+  stream_rows<DT, D>(lds, g, (const char*)centroids, row_bytes, nullptr, c0, c1, qb_n,
+                     [&](const auto& acc, int64_t c, int64_t) {
+                       constexpr int QB = sizeof(acc) / sizeof(acc[0]);
+                       if (c >= c1) return;
 #pragma unroll
-                            for (int qb = 0; qb < kQB; ++qb) {
-                              if (qb < qb_n) {
+                       for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
-                                for (int r = 0; r < 4; ++r) {
-                                  const int i = qb * 16 + 4 * h + r;
-                                  if (i < nq) scores[(size_t)(qt0 + i) * nlist + c] = acc[qb][r];
-                                }
-                              }
-                            }
-                          });
+                         for (int r = 0; r < 4; ++r) {
+                           const int i = qb * 16 + 4 * h + r;
+                           if (i < nq) scores[(size_t)(qt0 + i) * nlist + c] = acc[qb][r];
+                         }
+                       }
+                     });
 }
 
 // Dynamic LDS above 64 KB must be opted into once per kernel.

@@ -106,9 +106,16 @@ __global__ __launch_bounds__(kOffThreads) void sched_offsets_kernel(
     if (c > 0 && len > 0)
       rt += (int64_t)((c + tile_q - 1) / tile_q) * ((len + row_chunk - 1) / row_chunk);
   }
-  atomicAdd(&s_stat[0], list_rows);
-  atomicAdd(&s_stat[1], item_rows);
-  atomicAdd(&s_stat[2], loads);
+  for (int o = 32; o > 0; o >>= 1) {
+    list_rows += __shfl_xor(list_rows, o);
+    item_rows += __shfl_xor(item_rows, o);
+    loads += __shfl_xor(loads, o);
+  }
+  if ((t & 63) == 0) {
+    atomicAdd(&s_stat[0], list_rows);
+    atomicAdd(&s_stat[1], item_rows);
+    atomicAdd(&s_stat[2], loads);
+  }
   __syncthreads();
   if (t == 0) {
     rc->ntiles = (int32_t)s_tiles[kOffThreads - 1];

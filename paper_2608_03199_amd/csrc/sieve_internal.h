@@ -71,6 +71,7 @@ struct ScanArgs {
   int32_t d;
   int32_t row_chunk;
   int32_t tile_q;              // query rows per tile (multiple of 16, <= kTileQ)
+  int32_t dynamic;             // 1: atomic work queue, 0: static strided schedule
   float tau;
 };
 
