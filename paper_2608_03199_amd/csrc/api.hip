@@ -23,7 +23,6 @@
 #include "sieve_internal.h"
 
 namespace sieve {
-size_t rank_select_lds(int32_t nlist, int32_t cap);
 }
 
 using namespace sieve;
@@ -201,6 +200,7 @@ struct SearchPlan {
   int64_t rank_chunk;  // queries per centroid-screen chunk
   int64_t fix_chunk;   // queries per fixed-probe chunk
   int64_t item_cap;
+  bool wide_rank;      // rank with room for every boundary near-tie (retry path)
 };
 
 int check_common(const sieve_index* ix, const void* queries, int64_t nq, int32_t k, float tau,
@@ -262,7 +262,8 @@ int rank_queries(sieve_index* ix, const void* queries, int64_t q0, int64_t cnt,
     HIP_TRY(launch_rank_scores(ix->dtype, queries, q0 + a, c, ix->centroids, ix->nlist, ix->d,
                                (float*)ix->scores.p, s));
     HIP_TRY(launch_rank_select(ix->dtype, queries, q0 + a, c, ix->centroids, ix->nlist, ix->d,
-                               (const float*)ix->scores.p, pl.n, ix->cmax, P + a * pl.n, rc, s));
+                               (const float*)ix->scores.p, pl.n, ix->cmax, P + a * pl.n, rc,
+                               pl.wide_rank, s));
   }
   return SIEVE_OK;
 }
@@ -330,7 +331,8 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
   const int e = elem_bytes(ix->dtype);
   const ScanArgs sa0 = make_scan_args(ix, queries, exclude, pl);
 
-  for (int attempt = 0;; ++attempt) {
+  int pool_retries = 0;
+  for (;;) {
     reset_timeline(ix);
     int rounds = 0;
     int64_t items_total = 0;
@@ -369,10 +371,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
         HIP_TRY(hipStreamSynchronize(s));
         items_total += n_items;
         ++rounds;
-        if (ix->rc_host->rank_error)
-          return fail(SIEVE_EUNSUPPORTED,
-                      "more than %d centroids tie within the fp32 screening bound at a rank "
-                      "boundary", kMaxCand);
+        if (ix->rc_host->rank_error) break;  // handled below: re-rank wide or fail
         n_items = ix->rc_host->new_items;
         if (n_items > pl.item_cap)
           return fail(SIEVE_EINTERNAL, "round emitted %lld items, capacity %lld",
@@ -392,10 +391,14 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
       }
       HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
       HIP_TRY(hipStreamSynchronize(s));
-      if (ix->rc_host->rank_error)
+    }
+    if (ix->rc_host->rank_error) {
+      if (pl.wide_rank)
         return fail(SIEVE_EUNSUPPORTED,
                     "more than %d centroids tie within the fp32 screening bound at a rank "
                     "boundary", kMaxCand);
+      pl.wide_rank = true;  // a rank boundary overflowed the narrow buffer: run again
+      continue;
     }
 
     const int64_t hits = (int64_t)ix->rc_host->hits;
@@ -404,8 +407,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
       ix->pool_cap = hits + hits / 8 + 1024;
       if ((st = ensure(ix->pool, (size_t)ix->pool_cap * sizeof(Hit)))) return st;
       if ((st = ensure(ix->pool_sorted, (size_t)ix->pool_cap * sizeof(Hit)))) return st;
-      if (attempt >= 2) return fail(SIEVE_EINTERNAL, "candidate pool kept overflowing");
-      if (stats) stats->pool_retries = attempt + 1;
+      if (++pool_retries > 2) return fail(SIEVE_EINTERNAL, "candidate pool kept overflowing");
       continue;
     }
 
@@ -435,6 +437,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
       stats->rounds = rounds;
       stats->nprobe_eff = pl.n;
       stats->scan_launches = scan_launches;
+      stats->pool_retries = pool_retries;
       stats->items = items_total;
       stats->probes_total = (int64_t)h.probes;
       stats->vectors_scanned = (int64_t)h.item_rows;
@@ -466,6 +469,7 @@ int plan_search(const sieve_index* ix, int64_t nq, int32_t k, float tau, int32_t
   pl->tau = tau;
   pl->nq = nq;
   pl->tile_q = tile_rows(ix->dtype, ix->d);
+  pl->wide_rank = false;
   pl->row_chunk = row_chunk_for(ix);
   int64_t rc = (int64_t)(256ll << 20) / ((int64_t)ix->nlist * 4);
   if (rc < 64) rc = 64;
@@ -643,15 +647,17 @@ SIEVE_API int sieve_rank(const sieve_index* idx, const void* queries, int64_t nq
   if ((st = ensure(ix->rc, sizeof(RoundCounters)))) return st;
   if (!ix->rc_host) HIP_TRY(hipHostMalloc((void**)&ix->rc_host, sizeof(RoundCounters), 0));
   RoundCounters* rc = (RoundCounters*)ix->rc.p;
-  HIP_TRY(launch_zero_bytes(rc, sizeof(RoundCounters), s));
-  if ((st = rank_queries(ix, queries, 0, nq, pl, out_order, s))) return st;
-  HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipStreamSynchronize(s));
-  if (ix->rc_host->rank_error)
-    return fail(SIEVE_EUNSUPPORTED,
-                "more than %d centroids tie within the fp32 screening bound at a rank boundary",
-                kMaxCand);
-  return SIEVE_OK;
+  for (int attempt = 0; attempt < 2; ++attempt) {
+    pl.wide_rank = attempt > 0;
+    HIP_TRY(launch_zero_bytes(rc, sizeof(RoundCounters), s));
+    if ((st = rank_queries(ix, queries, 0, nq, pl, out_order, s))) return st;
+    HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    if (!ix->rc_host->rank_error) return SIEVE_OK;
+  }
+  return fail(SIEVE_EUNSUPPORTED,
+              "more than %d centroids tie within the fp32 screening bound at a rank boundary",
+              kMaxCand);
 }
 
 SIEVE_API int sieve_search_fixed(const sieve_index* idx, const void* queries, int64_t nq,

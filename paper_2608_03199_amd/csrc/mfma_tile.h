@@ -87,17 +87,33 @@ __host__ __device__ inline int lds_row_bytes(int d) {
 }
 
 // Stage rows of the query tile into LDS: row i (< nrows_pad) <- src(i) or 0.
-// src_row(i) returns a pointer to the stored row, or nullptr for padding.
+// src_row(i) returns a pointer to the stored row, or nullptr for padding;
+// src_row(0) must be a real row (it stands in as a safe address).  Eight
+// segments per thread are loaded per step from always-valid addresses and
+// masked afterwards, so their loads are in flight together.
 template <int DT, typename SrcRow>
 __device__ __forceinline__ void stage_queries(u32x4* lds, const RowGeom<DT>& g, int nrows_pad,
                                               SrcRow src_row) {
   const int total = nrows_pad * g.segs;
-  for (int e = threadIdx.x; e < total; e += blockDim.x) {
-    const int i = e / g.segs, s = e - i * g.segs;
-    u32x4 v = {0u, 0u, 0u, 0u};
-    const u32x4* row = src_row(i);
-    if (row != nullptr && s < g.dsegs) v = row[s];
-    lds[e] = v;
+  const u32x4* safe = src_row(0);
+  constexpr int kBatch = 8;
+  for (int e0 = threadIdx.x; e0 < total; e0 += kBatch * blockDim.x) {
+    u32x4 v[kBatch];
+    bool ok[kBatch];
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const int e = e0 + k * (int)blockDim.x;
+      const int i = e / g.segs, s = e - i * g.segs;
+      const u32x4* row = e < total ? src_row(i) : nullptr;
+      ok[k] = row != nullptr && s < g.dsegs;
+      const u32x4* src = ok[k] ? row + s : safe;  // select the address, load unconditionally
+      v[k] = *src;
+    }
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const int e = e0 + k * (int)blockDim.x;
+      if (e < total) lds[e] = ok[k] ? v[k] : u32x4{0u, 0u, 0u, 0u};
+    }
   }
 }
 
@@ -145,11 +161,15 @@ __device__ __forceinline__ void score_stream(const u32x4* __restrict__ lds, cons
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) acc[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
   const u32x4 zero = {0u, 0u, 0u, 0u};
-  u32x4 bn = (h < g.dsegs) ? vrow[h] : zero;
+  // segment indices past the row are clamped to segment 0 (a valid address)
+  // and masked to zero, so no branch separates the loads
+  u32x4 bn = vrow[h < g.dsegs ? h : 0];
+  if (h >= g.dsegs) bn = zero;
   for (int c = 0; c < g.nchunks; ++c) {
     const u32x4 bc = bn;
     const int sn = 4 * (c + 1) + h;
-    bn = (sn < g.dsegs) ? vrow[sn] : zero;
+    bn = vrow[sn < g.dsegs ? sn : 0];
+    if (sn >= g.dsegs) bn = zero;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       const u32x4 av = arow[qb * 16 * g.segs + 4 * c];

@@ -18,8 +18,6 @@
 namespace sieve {
 namespace {
 
-constexpr int kThreads = 256;
-
 __device__ __forceinline__ uint32_t f2key(float f) {
   const uint32_t u = __float_as_uint(f);
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
@@ -37,22 +35,32 @@ __device__ __forceinline__ double load_elem(const void* base, int64_t i) {
     return (double)((const _Float16*)base)[i];
 }
 
-// fp64 sum over dimensions in ascending order of exact products q_t * c_t
-// (the products of two fp32 or fp16 values are exact in fp64, so fused and
-// unfused multiply-adds agree).  Rows are read 16 bytes at a time so that
-// loads run ahead of the dependent accumulation.
+// Near-tie members whose centroid rows are staged per batch.
+constexpr int kMaxMembers = 64;
+
+// Bytes of the region holding the score keys and, later, the staged rows:
+// at least the query row plus one centroid row.
+__host__ __device__ inline int stage_bytes(int nlist, int d, int elem) {
+  const int keys = (nlist * 4 + 15) & ~15;
+  const int rows = 2 * d * elem;
+  return keys > rows ? keys : rows;
+}
+
+// fp64 sum in dimension order of exact products; the centroid row is in LDS,
+// the query row is read from global memory 16 bytes at a time.
 template <int DT>
-__device__ __forceinline__ double dot_fp64(const void* __restrict__ queries, int64_t q,
-                                           const void* __restrict__ centroids, int c, int d) {
+__device__ __forceinline__ double dot_fp64_lds(const uint32_t __attribute__((ext_vector_type(4)))*
+                                                   __restrict__ qrow,
+                                               const uint32_t __attribute__((ext_vector_type(4)))*
+                                                   __restrict__ crow,
+                                               int d) {
   typedef uint32_t u4 __attribute__((ext_vector_type(4)));
-  constexpr int per = DT == SIEVE_F32 ? 4 : 8;  // elements per 16 bytes
-  const int nseg = d / per;                     // d is a multiple of 8
-  const u4* qa = (const u4*)((const char*)queries + (size_t)q * d * (DT == SIEVE_F32 ? 4 : 2));
-  const u4* ca = (const u4*)((const char*)centroids + (size_t)c * d * (DT == SIEVE_F32 ? 4 : 2));
+  constexpr int per = DT == SIEVE_F32 ? 4 : 8;
+  const int nseg = d / per;
   double s = 0.0;
-#pragma unroll 4
+#pragma unroll 8
   for (int g = 0; g < nseg; ++g) {
-    const u4 qv = qa[g], cv = ca[g];
+    const u4 qv = qrow[g], cv = crow[g];
     if constexpr (DT == SIEVE_F32) {
       const float* qf = (const float*)&qv;
       const float* cf = (const float*)&cv;
@@ -68,24 +76,34 @@ __device__ __forceinline__ double dot_fp64(const void* __restrict__ queries, int
   return s;
 }
 
-template <int DT>
-__global__ __launch_bounds__(kThreads) void rank_select_kernel(
+// Candidate counts up to this use the counting sort (O(m^2 / NT) compares,
+// no barriers); larger ones a bitonic network.
+constexpr int kRankSortMax = 1024;
+
+// One query per block of NT threads.
+template <int DT, int NT>
+__global__ __launch_bounds__(NT) void rank_select_kernel(
     const void* __restrict__ queries, int64_t q0, const void* __restrict__ centroids,
     int32_t nlist, int32_t d, const float* __restrict__ scores, int32_t n, int32_t cap,
     double cmax, int32_t* __restrict__ P, RoundCounters* rc) {
+  typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+  constexpr int kWaves = NT / 64;
+  constexpr int kBins = 256;
+  constexpr int kBPT = kBins / NT > 0 ? kBins / NT : 1;  // bins per thread
+  const int elem = DT == SIEVE_F32 ? 4 : 2;
   extern __shared__ uint8_t smem[];
-  uint32_t* keys = (uint32_t*)smem;                                    // [nlist]
-  unsigned long long* ck = (unsigned long long*)(smem + ((nlist * 4 + 15) & ~15));  // [capp]
-  __shared__ int hist[256];
-  __shared__ uint32_t s_prefix;
-  __shared__ int s_remaining;
-  __shared__ int s_m;
-  __shared__ double s_red[kThreads / 64];
-  __shared__ int s_wsum[kThreads / 64];
+  float* sv = (float*)smem;  // [nlist] fp32 scores, later the staged rows
+  unsigned long long* ck = (unsigned long long*)(smem + stage_bytes(nlist, d, elem));  // [capp]
+  __shared__ int hist[kBins];
+  __shared__ float s_min[kWaves], s_max[kWaves];
+  __shared__ double s_red[kWaves];
+  __shared__ int s_wsum[kWaves];
+  __shared__ int s_bin, s_m, s_nmem;
+  __shared__ int s_members[NT];
 
   int capp = 1;
-  while (capp < cap) capp <<= 1;
-  double* cs = (double*)(ck + capp);  // [cap] fp64 scores of run members
+  while (capp < 2 * cap) capp <<= 1;
+  double* cs = (double*)(ck + capp);     // [cap] fp64 scores of run members
   uint8_t* link = (uint8_t*)(cs + cap);  // [cap]
 
   const int t = threadIdx.x;
@@ -93,41 +111,78 @@ __global__ __launch_bounds__(kThreads) void rank_select_kernel(
   const int64_t qg = q0 + ql;
   const float* row = scores + ql * nlist;
 
-  // |q| in fp64
+  // scores, their range, |q| in fp64
+  float lo_v = INFINITY, hi_v = -INFINITY;
+  for (int c0 = t; c0 < nlist; c0 += 8 * NT) {
+    float v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int c = c0 + k * NT;
+      v[k] = row[c < nlist ? c : nlist - 1];  // clamped: the loads issue together
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int c = c0 + k * NT;
+      if (c < nlist) {
+        sv[c] = v[k];
+        lo_v = fminf(lo_v, v[k]);
+        hi_v = fmaxf(hi_v, v[k]);
+      }
+    }
+  }
   double ss = 0.0;
-  for (int i = t; i < d; i += kThreads) {
+  for (int i = t; i < d; i += NT) {
     const double v = load_elem<DT>(queries, qg * d + i);
     ss += v * v;
   }
-  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
-  if ((t & 63) == 0) s_red[t >> 6] = ss;
-  for (int c = t; c < nlist; c += kThreads) keys[c] = f2key(row[c]);
+  for (int o = 32; o > 0; o >>= 1) {
+    ss += __shfl_xor(ss, o);
+    lo_v = fminf(lo_v, __shfl_xor(lo_v, o));
+    hi_v = fmaxf(hi_v, __shfl_xor(hi_v, o));
+  }
+  if ((t & 63) == 0) {
+    s_red[t >> 6] = ss;
+    s_min[t >> 6] = lo_v;
+    s_max[t >> 6] = hi_v;
+  }
+  for (int b = t; b < kBins; b += NT) hist[b] = 0;
   if (t == 0) {
-    s_prefix = 0;
-    s_remaining = n;
     s_m = 0;
+    s_nmem = 0;
   }
   __syncthreads();
   double qn = 0.0;
-  for (int w = 0; w < kThreads / 64; ++w) qn += s_red[w];
+  float smin = s_min[0], smax = s_max[0];
+  for (int w = 0; w < kWaves; ++w) {
+    qn += s_red[w];
+    smin = fminf(smin, s_min[w]);
+    smax = fmaxf(smax, s_max[w]);
+  }
   qn = sqrt(qn);
+  const double delta = 2.0 * (double)(d + 2) * 5.9604644775390625e-08 * qn * cmax + 1e-30;
+  const double gap = 2.0 * delta;
 
-  // 1. radix select of the n-th largest key, 8 bits per pass; the digit of
-  // each pass is found by a block-wide inclusive scan over the 256 bins taken
-  // from the highest digit down (thread t holds digit 255 - t).
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    hist[t] = 0;  // kThreads == 256 bins
-    __syncthreads();
-    const uint32_t hi_mask = shift == 24 ? 0u : (0xffffffffu << (shift + 8));
-    const uint32_t prefix = s_prefix;
-    const int rem = s_remaining;
-    for (int c = t; c < nlist; c += kThreads) {
-      const uint32_t k = keys[c];
-      if ((k & hi_mask) == prefix) atomicAdd(&hist[(k >> shift) & 255], 1);
+  // 1. one histogram of the scores over [smin, smax] in 256 equal bins (bin
+  // index non-decreasing in the score); the bin holding the n-th largest
+  // score is found by a block-wide scan from the top bin down
+  const float span = smax - smin;
+  const float scale = span > 0.f ? (float)kBins / span : 0.f;
+  auto bin_of = [&](float v) {
+    int b = (int)((v - smin) * scale);
+    return b < 0 ? 0 : (b > kBins - 1 ? kBins - 1 : b);
+  };
+  for (int c = t; c < nlist; c += NT) atomicAdd(&hist[bin_of(sv[c])], 1);
+  __syncthreads();
+  {
+    int v[kBPT];
+    int own = 0;
+#pragma unroll
+    for (int e = 0; e < kBPT; ++e) {
+      const int b = kBins - 1 - (t * kBPT + e);
+      v[e] = (t * kBPT + e) < kBins ? hist[b] : 0;
+      own += v[e];
     }
-    __syncthreads();
-    const int v = hist[255 - t];
-    int incl = v;
+    int incl = own;
     for (int o = 1; o < 64; o <<= 1) {
       const int u = __shfl_up(incl, o);
       if ((t & 63) >= o) incl += u;
@@ -135,126 +190,397 @@ __global__ __launch_bounds__(kThreads) void rank_select_kernel(
     if ((t & 63) == 63) s_wsum[t >> 6] = incl;
     __syncthreads();
     for (int w = 0; w < (t >> 6); ++w) incl += s_wsum[w];
-    if (incl >= rem && incl - v < rem) {
-      s_prefix = prefix | ((uint32_t)(255 - t) << shift);
-      s_remaining = rem - (incl - v);
+    int before = incl - own;
+#pragma unroll
+    for (int e = 0; e < kBPT; ++e) {
+      if (before < n && before + v[e] >= n) s_bin = kBins - 1 - (t * kBPT + e);
+      before += v[e];
+    }
+  }
+  __syncthreads();
+
+  // 2. candidates: every score in the boundary bin or above, and any score
+  // within 2 delta below it; the n-th largest fp32 score v lies in the bin,
+  // so this contains { c : s32[c] >= v - 2 delta }, which holds the fp64
+  // top-n.  Keys sort as (s32 desc, c asc).
+  const int bstar = s_bin;
+  // lower edge of the boundary bin, less the fp32 rounding of bin_of and of
+  // the edge itself (a few ulps of the score range; a wider margin only adds
+  // candidates)
+  const double edge = (double)(smin + (float)bstar / (scale > 0.f ? scale : 1.f));
+  const double lo = edge - gap - 1e-6 * ((double)fabsf(smin) + (double)fabsf(smax) + 1e-30);
+  for (int c = t; c < nlist; c += NT) {
+    const float v = sv[c];
+    const bool take = bin_of(v) >= bstar || (double)v >= lo;
+    if (take) {
+      const int slot = atomicAdd(&s_m, 1);
+      if (slot < cap) ck[slot] = ((unsigned long long)(~f2key(v)) << 32) | (unsigned)c;
+    }
+  }
+  __syncthreads();
+  const int m = s_m;
+  if (m > cap || m < n) {
+    // too many near-ties for this launch's buffer (m > cap), or a candidate
+    // set that cannot be right (m < n): the caller discards this search and
+    // re-ranks with the wide buffer.  The row still gets valid list ids so
+    // that every kernel that runs before the check stays in bounds.
+    if (t == 0) atomicExch(&rc->rank_error, 1);
+    for (int r = t; r < n; r += NT) P[ql * n + r] = r;
+    return;
+  }
+
+  // 3a. sort by key ascending == (s32 desc, c asc)
+  if (m <= kRankSortMax) {
+    // rank by counting: keys are distinct (the centroid index is in the low
+    // bits), so a key's position is the number of smaller keys
+    unsigned long long* out = ck + cap;
+    for (int i = t; i < m; i += NT) {
+      const unsigned long long ki = ck[i];
+      int pos = 0;
+      for (int j = 0; j < m; ++j) pos += ck[j] < ki ? 1 : 0;
+      out[pos] = ki;
     }
     __syncthreads();
-  }
-  const float vth = key2f(s_prefix);
-  const double delta = 2.0 * (double)(d + 2) * 5.9604644775390625e-08 * qn * cmax + 1e-30;
-  const double gap = 2.0 * delta;
-  const double lo = (double)vth - gap;
-
-  // 2. gather candidates
-  for (int c = t; c < nlist; c += kThreads) {
-    const float v = key2f(keys[c]);
-    if ((double)v >= lo) {
-      const int slot = atomicAdd(&s_m, 1);
-      if (slot < cap) ck[slot] = ((unsigned long long)(~keys[c]) << 32) | (unsigned)c;
-    }
-  }
-  __syncthreads();
-  const int m_all = s_m;
-  if (m_all > cap && t == 0) atomicExch(&rc->rank_error, 1);
-  const int m = m_all < cap ? m_all : cap;
-  int mp = 1;
-  while (mp < m) mp <<= 1;
-  for (int i = m + t; i < mp; i += kThreads) ck[i] = ~0ull;
-  __syncthreads();
-
-  // 3a. bitonic sort by (s32 desc, c asc) == key ascending
-  for (int kk = 2; kk <= mp; kk <<= 1) {
-    for (int j = kk >> 1; j > 0; j >>= 1) {
-      for (int i = t; i < mp; i += kThreads) {
-        const int ij = i ^ j;
-        if (ij > i) {
-          const unsigned long long a = ck[i], b = ck[ij];
-          const bool up = (i & kk) == 0;
-          if ((a > b) == up) {
-            ck[i] = b;
-            ck[ij] = a;
+    for (int i = t; i < m; i += NT) ck[i] = out[i];
+    __syncthreads();
+  } else {
+    int mp = 1;
+    while (mp < m) mp <<= 1;
+    for (int i = m + t; i < mp; i += NT) ck[i] = ~0ull;
+    __syncthreads();
+    for (int kk = 2; kk <= mp; kk <<= 1) {
+      for (int j = kk >> 1; j > 0; j >>= 1) {
+        for (int i = t; i < mp; i += NT) {
+          const int ij = i ^ j;
+          if (ij > i) {
+            const unsigned long long x = ck[i], y = ck[ij];
+            const bool up = (i & kk) == 0;
+            if ((x > y) == up) {
+              ck[i] = y;
+              ck[ij] = x;
+            }
           }
         }
+        __syncthreads();
       }
-      __syncthreads();
     }
   }
 
-  // 3b. runs of near-ties, fp64 scores of their members
-  for (int i = t; i < m; i += kThreads) {
+  // 3b. runs of near-ties (successive fp32 gaps <= 2 delta)
+  for (int i = t; i < m; i += NT) {
     bool l = false;
     if (i + 1 < m) {
-      const double a = (double)key2f(~(uint32_t)(ck[i] >> 32));
-      const double b = (double)key2f(~(uint32_t)(ck[i + 1] >> 32));
-      l = (a - b) <= gap;
+      const double x = (double)key2f(~(uint32_t)(ck[i] >> 32));
+      const double y = (double)key2f(~(uint32_t)(ck[i + 1] >> 32));
+      l = (x - y) <= gap;
     }
     link[i] = l ? 1 : 0;
   }
   __syncthreads();
-  for (int i = t; i < m; i += kThreads) {
-    const bool member = link[i] || (i > 0 && link[i - 1]);
-    if (member) cs[i] = dot_fp64<DT>(queries, qg, centroids, (int)(ck[i] & 0xffffffffu), d);
+  // 3c. fp64 scores of run members: positions are collected in parallel, the
+  // query row and the members' centroid rows are staged in LDS (the score
+  // space is free now), then each member's sum runs in dimension order
+  {
+    const int rowb = d * elem;
+    const int segs = rowb / 16;
+    u4* stage = (u4*)smem;
+    int per_batch = stage_bytes(nlist, d, elem) / rowb - 1;
+    if (per_batch > NT) per_batch = NT;
+    const u4* qsrc = (const u4*)((const char*)queries + (size_t)qg * rowb);
+    for (int g = t; g < segs; g += NT) stage[g] = qsrc[g];
+    for (int base = 0; base < m; base += NT) {
+      const int i = base + t;
+      if (i < m && (link[i] || (i > 0 && link[i - 1]))) s_members[atomicAdd(&s_nmem, 1)] = i;
+      __syncthreads();
+      const int nm = s_nmem;
+      for (int b0 = 0; b0 < nm; b0 += per_batch) {
+        const int nb = nm - b0 < per_batch ? nm - b0 : per_batch;
+        for (int e = t; e < nb * segs; e += NT) {
+          const int j = e / segs, g = e - j * segs;
+          const int c = (int)(ck[s_members[b0 + j]] & 0xffffffffu);
+          stage[(j + 1) * segs + g] = ((const u4*)((const char*)centroids + (size_t)c * rowb))[g];
+        }
+        __syncthreads();
+        if (t < nb) cs[s_members[b0 + t]] = dot_fp64_lds<DT>(stage, stage + (t + 1) * segs, d);
+        __syncthreads();
+      }
+      if (t == 0) s_nmem = 0;
+      __syncthreads();
+    }
   }
-  __syncthreads();
-  // 3c. insertion sort of every run by (s64 desc, c asc)
-  for (int i = t; i < m; i += kThreads) {
+  // 3d. insertion sort of every run by (s64 desc, c asc)
+  for (int i = t; i < m; i += NT) {
     if (link[i] && (i == 0 || !link[i - 1])) {
       int e = i;
       while (link[e]) ++e;  // run is [i, e]
-      for (int a = i + 1; a <= e; ++a) {
-        const unsigned long long kv = ck[a];
-        const double sv = cs[a];
-        const unsigned cv = (unsigned)(kv & 0xffffffffu);
-        int b = a - 1;
-        while (b >= i) {
-          const unsigned cb = (unsigned)(ck[b] & 0xffffffffu);
-          const bool before = (sv > cs[b]) || (sv == cs[b] && cv < cb);
+      for (int x = i + 1; x <= e; ++x) {
+        const unsigned long long kv = ck[x];
+        const double sx = cs[x];
+        const unsigned cx = (unsigned)(kv & 0xffffffffu);
+        int y = x - 1;
+        while (y >= i) {
+          const unsigned cy = (unsigned)(ck[y] & 0xffffffffu);
+          const bool before = (sx > cs[y]) || (sx == cs[y] && cx < cy);
           if (!before) break;
-          ck[b + 1] = ck[b];
-          cs[b + 1] = cs[b];
-          --b;
+          ck[y + 1] = ck[y];
+          cs[y + 1] = cs[y];
+          --y;
         }
-        ck[b + 1] = kv;
-        cs[b + 1] = sv;
+        ck[y + 1] = kv;
+        cs[y + 1] = sx;
       }
     }
   }
   __syncthreads();
   // 4. the first n
-  for (int r = t; r < n; r += kThreads) P[ql * n + r] = (int32_t)(ck[r] & 0xffffffffu);
+  for (int r = t; r < n; r += NT) P[ql * n + r] = (int32_t)(ck[r] & 0xffffffffu);
+}
+
+// Boundary candidates per lane in the wave kernel (capw <= 64 * this).
+constexpr int kKeysPerLane = 8;
+
+// Wave-level fence: orders this wave's LDS writes before its later LDS reads
+// (other lanes read what a lane wrote; no other wave shares the region).
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Bytes of one wave's LDS region in the wave-per-query kernel.
+__host__ __device__ inline int wave_region_bytes(int capw, int d, int elem) {
+  return capw * 8 * 2 + capw * 8 + ((capw + 15) & ~15) + 5 * d * elem;
+}
+
+// One query per wave, four per block; KPL = keys per lane (nlist <= 64*KPL).
+// 1. the scores of the query are held in registers, KPL per lane;
+// 2. the n-th largest key (the order-preserving integer image of the fp32
+//    score) is found bit by bit from the top: a bit is kept when at least n
+//    keys are >= the prefix with that bit set (32 counting steps, each
+//    register compares and ballot popcounts);
+// 3. candidates (score >= v - 2 delta) are compacted with ballots;
+// 4. they are sorted exactly by counting; near-tie runs get fp64 scores and
+//    an insertion sort, as in the block kernel.
+// A query with more than capw candidates sets rank_error (the caller then
+// re-ranks with the block kernel) and writes a valid placeholder row.
+template <int DT, int KPL>
+__global__ __launch_bounds__(256) void rank_select_wave_kernel(
+    const void* __restrict__ queries, int64_t q0, int32_t nqc, const void* __restrict__ centroids,
+    int32_t nlist, int32_t d, const float* __restrict__ scores, int32_t n, int32_t capw,
+    double cmax, int32_t* __restrict__ P, RoundCounters* rc) {
+  typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+  extern __shared__ uint8_t smem[];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t ql = (int64_t)blockIdx.x * 4 + wave;
+  if (ql >= nqc) return;  // whole wave; no block barrier follows
+  const int elem = DT == SIEVE_F32 ? 4 : 2;
+  uint8_t* region = smem + (size_t)wave * wave_region_bytes(capw, d, elem);
+  unsigned long long* ck = (unsigned long long*)region;  // [capw]
+  unsigned long long* out = ck + capw;                   // [capw]
+  double* cs = (double*)(out + capw);                    // [capw]
+  uint8_t* link = (uint8_t*)(cs + capw);                 // [capw]
+  u4* stage = (u4*)(link + ((capw + 15) & ~15));         // query row + 4 centroid rows
+  const int64_t qg = q0 + ql;
+  const float* row = scores + ql * nlist;
+
+  // all loads are issued before any is used: clamped addresses, no branches
+  float raw[KPL];
+#pragma unroll
+  for (int j = 0; j < KPL; ++j) {
+    const int c = lane + 64 * j;
+    raw[j] = row[c < nlist ? c : nlist - 1];
+  }
+  uint32_t key[KPL];
+#pragma unroll
+  for (int j = 0; j < KPL; ++j)
+    key[j] = (lane + 64 * j) < nlist ? f2key(raw[j]) : 0u;  // 0 sorts below every score
+  double ss = 0.0;
+  for (int i = lane; i < d; i += 64) {
+    const double v = load_elem<DT>(queries, qg * d + i);
+    ss += v * v;
+  }
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+  const double qn = sqrt(ss);
+  const double delta = 2.0 * (double)(d + 2) * 5.9604644775390625e-08 * qn * cmax + 1e-30;
+  const double gap = 2.0 * delta;
+
+  // 2. exact n-th largest key; each count is a sum of ballot popcounts, so
+  // it stays in scalar registers (no cross-lane shuffles)
+  uint32_t prefix = 0;
+  for (int bit = 31; bit >= 0; --bit) {
+    const uint32_t cand = prefix | (1u << bit);
+    int cnt = 0;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) cnt += __popcll(__ballot(key[j] >= cand));
+    if (cnt >= n) prefix = cand;
+  }
+  const double lo = (double)key2f(prefix) - gap;
+
+  // 3. candidates, compacted with ballots
+  int m = 0;
+#pragma unroll
+  for (int j = 0; j < KPL; ++j) {
+    const int c = lane + 64 * j;
+    const bool take = c < nlist && (double)key2f(key[j]) >= lo;
+    const unsigned long long mask = __ballot(take);
+    const int pos = m + __popcll(mask & ((1ull << lane) - 1ull));
+    if (take && pos < capw) ck[pos] = ((unsigned long long)(~key[j]) << 32) | (unsigned)c;
+    m += __popcll(mask);
+  }
+  if (m > capw || m < n) {
+    if (lane == 0) atomicExch(&rc->rank_error, 1);
+    for (int r = lane; r < n; r += 64) P[ql * n + r] = r;
+    return;
+  }
+  wave_sync();
+
+  // 4a. rank by counting (keys are distinct): position = number of smaller keys
+  for (int i = lane; i < m; i += 64) {
+    const unsigned long long ki = ck[i];
+    int pos = 0;
+#pragma unroll 8
+    for (int j = 0; j < m; ++j) pos += ck[j] < ki ? 1 : 0;
+    out[pos] = ki;
+  }
+  wave_sync();
+  // 4b. runs of near-ties
+  for (int i = lane; i < m; i += 64) {
+    bool l = false;
+    if (i + 1 < m) {
+      const double x = (double)key2f(~(uint32_t)(out[i] >> 32));
+      const double y = (double)key2f(~(uint32_t)(out[i + 1] >> 32));
+      l = (x - y) <= gap;
+    }
+    link[i] = l ? 1 : 0;
+  }
+  wave_sync();
+  // 4c. fp64 scores of run members, staged four rows at a time
+  {
+    const int rowb = d * elem, segs = rowb / 16;
+    const u4* qsrc = (const u4*)((const char*)queries + (size_t)qg * rowb);
+    for (int g = lane; g < segs; g += 64) stage[g] = qsrc[g];
+    for (int base = 0; base < m; base += 64) {
+      const int i = base + lane;
+      const bool member = i < m && (link[i] || (i > 0 && link[i - 1]));
+      unsigned long long mask = __ballot(member);
+      while (mask) {
+        // up to four members per batch: stage their rows, then one lane each
+        int who[4], nb = 0;
+        while (mask && nb < 4) {
+          const int b = __ffsll((long long)mask) - 1;
+          mask &= mask - 1;
+          who[nb++] = base + b;
+        }
+        wave_sync();
+        for (int e = lane; e < nb * segs; e += 64) {
+          const int j = e / segs, g = e - j * segs;
+          const int c = (int)(out[who[j]] & 0xffffffffu);
+          stage[(j + 1) * segs + g] = ((const u4*)((const char*)centroids + (size_t)c * rowb))[g];
+        }
+        wave_sync();
+        if (lane < nb) cs[who[lane]] = dot_fp64_lds<DT>(stage, stage + (lane + 1) * segs, d);
+        wave_sync();
+      }
+    }
+  }
+  // 4d. insertion sort of every run by (s64 desc, c asc)
+  for (int i = lane; i < m; i += 64) {
+    if (link[i] && (i == 0 || !link[i - 1])) {
+      int e = i;
+      while (link[e]) ++e;
+      for (int x = i + 1; x <= e; ++x) {
+        const unsigned long long kv = out[x];
+        const double sx = cs[x];
+        const unsigned cx = (unsigned)(kv & 0xffffffffu);
+        int y = x - 1;
+        while (y >= i) {
+          const unsigned cy = (unsigned)(out[y] & 0xffffffffu);
+          const bool before = (sx > cs[y]) || (sx == cs[y] && cx < cy);
+          if (!before) break;
+          out[y + 1] = out[y];
+          cs[y + 1] = cs[y];
+          --y;
+        }
+        out[y + 1] = kv;
+        cs[y + 1] = sx;
+      }
+    }
+  }
+  wave_sync();
+  for (int r = lane; r < n; r += 64) P[ql * n + r] = (int32_t)(out[r] & 0xffffffffu);
 }
 
 }  // namespace
 
-size_t rank_select_lds(int32_t nlist, int32_t cap) {
+size_t rank_select_lds(int32_t nlist, int32_t cap, int32_t d, int dtype) {
   int capp = 1;
-  while (capp < cap) capp <<= 1;
-  return (size_t)((nlist * 4 + 15) & ~15) + (size_t)capp * 8 + (size_t)cap * 8 + (size_t)cap;
+  while (capp < 2 * cap) capp <<= 1;
+  return (size_t)stage_bytes(nlist, d, dtype == SIEVE_F32 ? 4 : 2) + (size_t)capp * 8 +
+         (size_t)cap * 8 + (size_t)cap;
+}
+
+// `wide` (set after a launch reported more near-ties at a rank boundary than
+// its buffer holds) sizes the candidate buffer for every centroid.
+template <int DT, int KPL>
+hipError_t launch_wave_t(const void* queries, int64_t q0, int32_t nqc, const void* centroids,
+                         int32_t nlist, int32_t d, const float* scores, int32_t n, int32_t capw,
+                         double cmax, int32_t* P, RoundCounters* rc, hipStream_t s) {
+  const int elem = DT == SIEVE_F32 ? 4 : 2;
+  const size_t lds = (size_t)4 * wave_region_bytes(capw, d, elem);
+  static const hipError_t attr =
+      hipFuncSetAttribute((const void*)rank_select_wave_kernel<DT, KPL>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, 150 * 1024);
+  if (attr != hipSuccess) return attr;
+  if (lds > 150 * 1024) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((rank_select_wave_kernel<DT, KPL>), dim3((unsigned)((nqc + 3) / 4)),
+                     dim3(256), lds, s, queries, q0, nqc, centroids, nlist, d, scores, n, capw,
+                     cmax, P, rc);
+  return hipGetLastError();
+}
+
+template <int DT>
+hipError_t launch_wave(const void* queries, int64_t q0, int32_t nqc, const void* centroids,
+                       int32_t nlist, int32_t d, const float* scores, int32_t n, int32_t capw,
+                       double cmax, int32_t* P, RoundCounters* rc, hipStream_t s) {
+  if (nlist <= 256)
+    return launch_wave_t<DT, 4>(queries, q0, nqc, centroids, nlist, d, scores, n, capw, cmax, P,
+                                rc, s);
+  if (nlist <= 1024)
+    return launch_wave_t<DT, 16>(queries, q0, nqc, centroids, nlist, d, scores, n, capw, cmax, P,
+                                 rc, s);
+  return launch_wave_t<DT, 64>(queries, q0, nqc, centroids, nlist, d, scores, n, capw, cmax, P,
+                               rc, s);
 }
 
 hipError_t launch_rank_select(int dtype, const void* queries, int64_t q0, int32_t nqc,
                               const void* centroids, int32_t nlist, int32_t d, const float* scores,
-                              int32_t n, double cmax, int32_t* P, RoundCounters* rc,
+                              int32_t n, double cmax, int32_t* P, RoundCounters* rc, bool wide,
                               hipStream_t s) {
   if (nqc <= 0) return hipSuccess;
-  const int32_t cap = nlist < kMaxCand ? nlist : kMaxCand;
-  const size_t lds = rank_select_lds(nlist, cap);
-  static const hipError_t a32 = hipFuncSetAttribute(
-      (const void*)rank_select_kernel<SIEVE_F32>, hipFuncAttributeMaxDynamicSharedMemorySize,
-      150 * 1024);
-  static const hipError_t a16 = hipFuncSetAttribute(
-      (const void*)rank_select_kernel<SIEVE_F16>, hipFuncAttributeMaxDynamicSharedMemorySize,
-      150 * 1024);
-  if (a32 != hipSuccess) return a32;
-  if (a16 != hipSuccess) return a16;
+  // one wave per query while the boundary buffer stays small
+  const int elem = dtype == SIEVE_F32 ? 4 : 2;
+  int capw = n + 128 < nlist ? n + 128 : nlist;
+  if (!wide && nlist <= 4096 && capw <= 64 * kKeysPerLane &&
+      4 * wave_region_bytes(capw, d, elem) <= 96 * 1024) {
+    return dtype == SIEVE_F32
+               ? launch_wave<SIEVE_F32>(queries, q0, nqc, centroids, nlist, d, scores, n, capw,
+                                        cmax, P, rc, s)
+               : launch_wave<SIEVE_F16>(queries, q0, nqc, centroids, nlist, d, scores, n, capw,
+                                        cmax, P, rc, s);
+  }
+  // block kernel: narrow (n + 512 boundary candidates) or wide (every
+  // centroid, up to kMaxCand)
+  int32_t cap = nlist < kMaxCand ? nlist : kMaxCand;
+  if (!wide && n + 512 < cap) cap = n + 512;
+  while (cap > n && rank_select_lds(nlist, cap, d, dtype) > 150 * 1024) cap = (cap + n) / 2;
+  const size_t lds = rank_select_lds(nlist, cap, d, dtype);
   if (lds > 150 * 1024) return hipErrorInvalidValue;
   if (dtype == SIEVE_F32)
-    hipLaunchKernelGGL(rank_select_kernel<SIEVE_F32>, dim3(nqc), dim3(kThreads), lds, s, queries,
-                       q0, centroids, nlist, d, scores, n, cap, cmax, P, rc);
+    hipLaunchKernelGGL((rank_select_kernel<SIEVE_F32, 256>), dim3(nqc), dim3(256), lds, s,
+                       queries, q0, centroids, nlist, d, scores, n, cap, cmax, P, rc);
   else
-    hipLaunchKernelGGL(rank_select_kernel<SIEVE_F16>, dim3(nqc), dim3(kThreads), lds, s, queries,
-                       q0, centroids, nlist, d, scores, n, cap, cmax, P, rc);
+    hipLaunchKernelGGL((rank_select_kernel<SIEVE_F16, 256>), dim3(nqc), dim3(256), lds, s,
+                       queries, q0, centroids, nlist, d, scores, n, cap, cmax, P, rc);
   return hipGetLastError();
 }
 

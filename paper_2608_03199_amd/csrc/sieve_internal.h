@@ -86,7 +86,7 @@ hipError_t launch_rank_scores(int dtype, const void* queries, int64_t q0, int32_
 size_t scan_lds_bytes(int dtype, int d, int rows);
 hipError_t launch_rank_select(int dtype, const void* queries, int64_t q0, int32_t nqc,
                               const void* centroids, int32_t nlist, int32_t d, const float* scores,
-                              int32_t n, double cmax, int32_t* P, RoundCounters* rc,
+                              int32_t n, double cmax, int32_t* P, RoundCounters* rc, bool wide,
                               hipStream_t s);
 
 hipError_t launch_emit_initial(const int32_t* P, int32_t n, int64_t nqc, int32_t q0, int32_t s0,

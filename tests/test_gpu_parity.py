@@ -240,3 +240,31 @@ def test_rank_order_matches_oracle_exactly(name):
     o = oracle.search(h["vectors"], h["list_offsets"], h["ids"], h["centroids"], h["queries"],
                       h["exclude_ids"], 1, 2.0, 1, nl, want_order=True, nthreads=NTHREADS)
     assert np.array_equal(P, o.order)
+
+
+def test_rank_with_many_exact_ties_takes_the_wide_path():
+    """800 identical centroids tie at the top: the one-wave selection runs out of
+    boundary room, the search re-ranks with the wide kernel, and the order is
+    still the oracle's (ties to the lower centroid index)."""
+    rng = np.random.default_rng(11)
+    d, nlist, n = 32, 1024, 3000
+    C = rng.standard_normal((nlist, d)).astype(np.float32)
+    C /= np.linalg.norm(C, axis=1, keepdims=True)
+    C[100:900] = C[100]
+    X = rng.standard_normal((n, d)).astype(np.float32)
+    X /= np.linalg.norm(X, axis=1, keepdims=True)
+    sizes = rng.multinomial(n, np.ones(nlist) / nlist)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    ids = np.arange(n, dtype=np.int64)
+    Q = (C[100] + 0.01 * rng.standard_normal((64, d))).astype(np.float32)
+    Q /= np.linalg.norm(Q, axis=1, keepdims=True)
+    ps = _lib()
+    dev = "cuda"
+    ix = ps.Index(torch.from_numpy(X).to(dev), torch.from_numpy(off).to(dev),
+                  torch.from_numpy(ids).to(dev), torch.from_numpy(C).to(dev))
+    P = ix.rank(torch.from_numpy(Q).to(dev), 16).cpu().numpy()
+    o = oracle.search(X, off, ids, C, Q, None, 1, 2.0, 1, 16, want_order=True)
+    assert np.array_equal(P, o.order)
+    g = ix.search(torch.from_numpy(Q).to(dev), None, 10, 0.5, 3, 16)
+    o = oracle.search(X, off, ids, C, Q, None, 10, 0.5, 3, 16)
+    assert_parity(compare(g[0].cpu().numpy(), g[1].cpu().numpy(), g[2].cpu().numpy(), o))
