@@ -35,46 +35,108 @@ __device__ __forceinline__ double load_elem(const void* base, int64_t i) {
     return (double)((const _Float16*)base)[i];
 }
 
-// Near-tie members whose centroid rows are staged per batch.
-constexpr int kMaxMembers = 64;
-
-// Bytes of the region holding the score keys and, later, the staged rows:
-// at least the query row plus one centroid row.
-__host__ __device__ inline int stage_bytes(int nlist, int d, int elem) {
-  const int keys = (nlist * 4 + 15) & ~15;
-  const int rows = 2 * d * elem;
-  return keys > rows ? keys : rows;
-}
-
-// fp64 sum in dimension order of exact products; the centroid row is in LDS,
-// the query row is read from global memory 16 bytes at a time.
+// fp64 inner product of query row q and centroid row c (global memory) by
+// one wave: lane l sums dimensions l, l+64, ... in order, then the 64
+// partial sums are added as a tree.  Its distance to the dimension-ordered
+// sequential fp64 sum is at most (d + ceil(d/64) + 6) 2^-53 sum_t |q_t c_t|.
 template <int DT>
-__device__ __forceinline__ double dot_fp64_lds(const uint32_t __attribute__((ext_vector_type(4)))*
-                                                   __restrict__ qrow,
-                                               const uint32_t __attribute__((ext_vector_type(4)))*
-                                                   __restrict__ crow,
-                                               int d) {
-  typedef uint32_t u4 __attribute__((ext_vector_type(4)));
-  constexpr int per = DT == SIEVE_F32 ? 4 : 8;
-  const int nseg = d / per;
+__device__ __forceinline__ double wave_dot_fp64(const void* __restrict__ queries, int64_t q,
+                                                const void* __restrict__ centroids, int c, int d) {
+  const int lane = threadIdx.x & 63;
   double s = 0.0;
-#pragma unroll 8
-  for (int g = 0; g < nseg; ++g) {
-    const u4 qv = qrow[g], cv = crow[g];
-    if constexpr (DT == SIEVE_F32) {
-      const float* qf = (const float*)&qv;
-      const float* cf = (const float*)&cv;
+  for (int t0 = 0; t0 < d; t0 += 256) {
+    double qv[4], cv[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) s += (double)qf[e] * (double)cf[e];
-    } else {
-      const _Float16* qh = (const _Float16*)&qv;
-      const _Float16* ch = (const _Float16*)&cv;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) s += (double)qh[e] * (double)ch[e];
+    for (int k = 0; k < 4; ++k) {
+      const int t = t0 + lane + 64 * k;
+      const int tc = t < d ? t : d - 1;  // clamped: the loads issue together
+      qv[k] = load_elem<DT>(queries, q * d + tc);
+      cv[k] = load_elem<DT>(centroids, (int64_t)c * d + tc);
     }
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (t0 + lane + 64 * k < d) s += qv[k] * cv[k];
   }
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
   return s;
 }
+
+// The dimension-ordered sequential fp64 sum (what the order is defined by).
+template <int DT>
+__device__ __noinline__ double seq_dot_fp64(const void* __restrict__ queries, int64_t q,
+                                            const void* __restrict__ centroids, int c, int d) {
+  double s = 0.0;
+  for (int t = 0; t < d; ++t)
+    s += load_elem<DT>(queries, q * d + t) * load_elem<DT>(centroids, (int64_t)c * d + t);
+  return s;
+}
+
+// Order candidates [0, m) already sorted by fp32 screen key: inside each run
+// of near-ties (link[i]: the gap to i+1 is within the screen bound) sort by
+// fp64 score desc, centroid asc.  Tier 1 scores come from wave_dot_fp64;
+// a run whose tier-1 neighbours are within 2 * bound64 is re-scored with the
+// exact sequential sum before its final sort.  NW waves of the calling block
+// (waves w0..w0+NW-1) share the work; the caller synchronises between calls
+// of the three steps.
+template <int DT>
+__device__ __forceinline__ void refine_members(unsigned long long* ck, double* cs,
+                                               const uint8_t* link, int m,
+                                               const void* queries, int64_t qg,
+                                               const void* centroids, int d, int wave, int nwaves) {
+  for (int i = wave; i < m; i += nwaves) {
+    const bool member = link[i] || (i > 0 && link[i - 1]);  // wave-uniform
+    if (member) {
+      const double v = wave_dot_fp64<DT>(queries, qg, centroids, (int)(ck[i] & 0xffffffffu), d);
+      if ((threadIdx.x & 63) == 0) cs[i] = v;
+    }
+  }
+}
+
+__device__ __forceinline__ void sort_run(unsigned long long* ck, double* cs, int i, int e) {
+  for (int x = i + 1; x <= e; ++x) {
+    const unsigned long long kv = ck[x];
+    const double sx = cs[x];
+    const unsigned cx = (unsigned)(kv & 0xffffffffu);
+    int y = x - 1;
+    while (y >= i) {
+      const unsigned cy = (unsigned)(ck[y] & 0xffffffffu);
+      const bool before = (sx > cs[y]) || (sx == cs[y] && cx < cy);
+      if (!before) break;
+      ck[y + 1] = ck[y];
+      cs[y + 1] = cs[y];
+      --y;
+    }
+    ck[y + 1] = kv;
+    cs[y + 1] = sx;
+  }
+}
+
+// One thread per run start: sort by tier-1 score; if two neighbours are
+// within gap64, re-score the whole run exactly and sort again.
+template <int DT>
+__device__ __forceinline__ void order_runs(unsigned long long* ck, double* cs, const uint8_t* link,
+                                           int m, const void* queries, int64_t qg,
+                                           const void* centroids, int d, double gap64, int tid,
+                                           int nthreads) {
+  for (int i = tid; i < m; i += nthreads) {
+    if (link[i] && (i == 0 || !link[i - 1])) {
+      int e = i;
+      while (link[e]) ++e;  // run is [i, e]
+      sort_run(ck, cs, i, e);
+      bool close = false;
+      for (int x = i; x < e; ++x) close |= (cs[x] - cs[x + 1]) <= gap64;
+      if (close) {
+        for (int x = i; x <= e; ++x)
+          cs[x] = seq_dot_fp64<DT>(queries, qg, centroids, (int)(ck[x] & 0xffffffffu), d);
+        sort_run(ck, cs, i, e);
+      }
+    }
+  }
+}
+
+
+// Bytes of the region holding one query's fp32 scores.
+__host__ __device__ inline int keys_bytes(int nlist) { return (nlist * 4 + 15) & ~15; }
 
 // Candidate counts up to this use the counting sort (O(m^2 / NT) compares,
 // no barriers); larger ones a bitonic network.
@@ -86,20 +148,17 @@ __global__ __launch_bounds__(NT) void rank_select_kernel(
     const void* __restrict__ queries, int64_t q0, const void* __restrict__ centroids,
     int32_t nlist, int32_t d, const float* __restrict__ scores, int32_t n, int32_t cap,
     double cmax, int32_t* __restrict__ P, RoundCounters* rc) {
-  typedef uint32_t u4 __attribute__((ext_vector_type(4)));
   constexpr int kWaves = NT / 64;
   constexpr int kBins = 256;
   constexpr int kBPT = kBins / NT > 0 ? kBins / NT : 1;  // bins per thread
-  const int elem = DT == SIEVE_F32 ? 4 : 2;
   extern __shared__ uint8_t smem[];
-  float* sv = (float*)smem;  // [nlist] fp32 scores, later the staged rows
-  unsigned long long* ck = (unsigned long long*)(smem + stage_bytes(nlist, d, elem));  // [capp]
+  float* sv = (float*)smem;  // [nlist] fp32 scores
+  unsigned long long* ck = (unsigned long long*)(smem + keys_bytes(nlist));  // [capp]
   __shared__ int hist[kBins];
   __shared__ float s_min[kWaves], s_max[kWaves];
   __shared__ double s_red[kWaves];
   __shared__ int s_wsum[kWaves];
-  __shared__ int s_bin, s_m, s_nmem;
-  __shared__ int s_members[NT];
+  __shared__ int s_bin, s_m;
 
   int capp = 1;
   while (capp < 2 * cap) capp <<= 1;
@@ -146,10 +205,7 @@ __global__ __launch_bounds__(NT) void rank_select_kernel(
     s_max[t >> 6] = hi_v;
   }
   for (int b = t; b < kBins; b += NT) hist[b] = 0;
-  if (t == 0) {
-    s_m = 0;
-    s_nmem = 0;
-  }
+  if (t == 0) s_m = 0;
   __syncthreads();
   double qn = 0.0;
   float smin = s_min[0], smax = s_max[0];
@@ -237,6 +293,7 @@ __global__ __launch_bounds__(NT) void rank_select_kernel(
     for (int i = t; i < m; i += NT) {
       const unsigned long long ki = ck[i];
       int pos = 0;
+#pragma unroll 8
       for (int j = 0; j < m; ++j) pos += ck[j] < ki ? 1 : 0;
       out[pos] = ki;
     }
@@ -277,59 +334,14 @@ __global__ __launch_bounds__(NT) void rank_select_kernel(
     link[i] = l ? 1 : 0;
   }
   __syncthreads();
-  // 3c. fp64 scores of run members: positions are collected in parallel, the
-  // query row and the members' centroid rows are staged in LDS (the score
-  // space is free now), then each member's sum runs in dimension order
+  // 3c. fp64 scores of run members, one wave per member
+  refine_members<DT>(ck, cs, link, m, queries, qg, centroids, d, t >> 6, NT / 64);
+  __syncthreads();
+  // 3d. order inside each run (exact sequential sums where tier 1 is too close)
   {
-    const int rowb = d * elem;
-    const int segs = rowb / 16;
-    u4* stage = (u4*)smem;
-    int per_batch = stage_bytes(nlist, d, elem) / rowb - 1;
-    if (per_batch > NT) per_batch = NT;
-    const u4* qsrc = (const u4*)((const char*)queries + (size_t)qg * rowb);
-    for (int g = t; g < segs; g += NT) stage[g] = qsrc[g];
-    for (int base = 0; base < m; base += NT) {
-      const int i = base + t;
-      if (i < m && (link[i] || (i > 0 && link[i - 1]))) s_members[atomicAdd(&s_nmem, 1)] = i;
-      __syncthreads();
-      const int nm = s_nmem;
-      for (int b0 = 0; b0 < nm; b0 += per_batch) {
-        const int nb = nm - b0 < per_batch ? nm - b0 : per_batch;
-        for (int e = t; e < nb * segs; e += NT) {
-          const int j = e / segs, g = e - j * segs;
-          const int c = (int)(ck[s_members[b0 + j]] & 0xffffffffu);
-          stage[(j + 1) * segs + g] = ((const u4*)((const char*)centroids + (size_t)c * rowb))[g];
-        }
-        __syncthreads();
-        if (t < nb) cs[s_members[b0 + t]] = dot_fp64_lds<DT>(stage, stage + (t + 1) * segs, d);
-        __syncthreads();
-      }
-      if (t == 0) s_nmem = 0;
-      __syncthreads();
-    }
-  }
-  // 3d. insertion sort of every run by (s64 desc, c asc)
-  for (int i = t; i < m; i += NT) {
-    if (link[i] && (i == 0 || !link[i - 1])) {
-      int e = i;
-      while (link[e]) ++e;  // run is [i, e]
-      for (int x = i + 1; x <= e; ++x) {
-        const unsigned long long kv = ck[x];
-        const double sx = cs[x];
-        const unsigned cx = (unsigned)(kv & 0xffffffffu);
-        int y = x - 1;
-        while (y >= i) {
-          const unsigned cy = (unsigned)(ck[y] & 0xffffffffu);
-          const bool before = (sx > cs[y]) || (sx == cs[y] && cx < cy);
-          if (!before) break;
-          ck[y + 1] = ck[y];
-          cs[y + 1] = cs[y];
-          --y;
-        }
-        ck[y + 1] = kv;
-        cs[y + 1] = sx;
-      }
-    }
+    const double gap64 =
+        2.0 * 2.0 * (double)(d + (d + 63) / 64 + 6) * 1.1102230246251565e-16 * qn * cmax + 1e-300;
+    order_runs<DT>(ck, cs, link, m, queries, qg, centroids, d, gap64, t, NT);
   }
   __syncthreads();
   // 4. the first n
@@ -348,8 +360,8 @@ __device__ __forceinline__ void wave_sync() {
 }
 
 // Bytes of one wave's LDS region in the wave-per-query kernel.
-__host__ __device__ inline int wave_region_bytes(int capw, int d, int elem) {
-  return capw * 8 * 2 + capw * 8 + ((capw + 15) & ~15) + 5 * d * elem;
+__host__ __device__ inline int wave_region_bytes(int capw) {
+  return capw * 8 * 2 + capw * 8 + ((capw + 15) & ~15);
 }
 
 // One query per wave, four per block; KPL = keys per lane (nlist <= 64*KPL).
@@ -368,18 +380,15 @@ __global__ __launch_bounds__(256) void rank_select_wave_kernel(
     const void* __restrict__ queries, int64_t q0, int32_t nqc, const void* __restrict__ centroids,
     int32_t nlist, int32_t d, const float* __restrict__ scores, int32_t n, int32_t capw,
     double cmax, int32_t* __restrict__ P, RoundCounters* rc) {
-  typedef uint32_t u4 __attribute__((ext_vector_type(4)));
   extern __shared__ uint8_t smem[];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t ql = (int64_t)blockIdx.x * 4 + wave;
   if (ql >= nqc) return;  // whole wave; no block barrier follows
-  const int elem = DT == SIEVE_F32 ? 4 : 2;
-  uint8_t* region = smem + (size_t)wave * wave_region_bytes(capw, d, elem);
+  uint8_t* region = smem + (size_t)wave * wave_region_bytes(capw);
   unsigned long long* ck = (unsigned long long*)region;  // [capw]
   unsigned long long* out = ck + capw;                   // [capw]
   double* cs = (double*)(out + capw);                    // [capw]
   uint8_t* link = (uint8_t*)(cs + capw);                 // [capw]
-  u4* stage = (u4*)(link + ((capw + 15) & ~15));         // query row + 4 centroid rows
   const int64_t qg = q0 + ql;
   const float* row = scores + ql * nlist;
 
@@ -454,57 +463,14 @@ __global__ __launch_bounds__(256) void rank_select_wave_kernel(
     link[i] = l ? 1 : 0;
   }
   wave_sync();
-  // 4c. fp64 scores of run members, staged four rows at a time
+  // 4c. fp64 scores of run members (this wave alone)
+  refine_members<DT>(out, cs, link, m, queries, qg, centroids, d, 0, 1);
+  wave_sync();
+  // 4d. order inside each run (exact sequential sums where tier 1 is too close)
   {
-    const int rowb = d * elem, segs = rowb / 16;
-    const u4* qsrc = (const u4*)((const char*)queries + (size_t)qg * rowb);
-    for (int g = lane; g < segs; g += 64) stage[g] = qsrc[g];
-    for (int base = 0; base < m; base += 64) {
-      const int i = base + lane;
-      const bool member = i < m && (link[i] || (i > 0 && link[i - 1]));
-      unsigned long long mask = __ballot(member);
-      while (mask) {
-        // up to four members per batch: stage their rows, then one lane each
-        int who[4], nb = 0;
-        while (mask && nb < 4) {
-          const int b = __ffsll((long long)mask) - 1;
-          mask &= mask - 1;
-          who[nb++] = base + b;
-        }
-        wave_sync();
-        for (int e = lane; e < nb * segs; e += 64) {
-          const int j = e / segs, g = e - j * segs;
-          const int c = (int)(out[who[j]] & 0xffffffffu);
-          stage[(j + 1) * segs + g] = ((const u4*)((const char*)centroids + (size_t)c * rowb))[g];
-        }
-        wave_sync();
-        if (lane < nb) cs[who[lane]] = dot_fp64_lds<DT>(stage, stage + (lane + 1) * segs, d);
-        wave_sync();
-      }
-    }
-  }
-  // 4d. insertion sort of every run by (s64 desc, c asc)
-  for (int i = lane; i < m; i += 64) {
-    if (link[i] && (i == 0 || !link[i - 1])) {
-      int e = i;
-      while (link[e]) ++e;
-      for (int x = i + 1; x <= e; ++x) {
-        const unsigned long long kv = out[x];
-        const double sx = cs[x];
-        const unsigned cx = (unsigned)(kv & 0xffffffffu);
-        int y = x - 1;
-        while (y >= i) {
-          const unsigned cy = (unsigned)(out[y] & 0xffffffffu);
-          const bool before = (sx > cs[y]) || (sx == cs[y] && cx < cy);
-          if (!before) break;
-          out[y + 1] = out[y];
-          cs[y + 1] = cs[y];
-          --y;
-        }
-        out[y + 1] = kv;
-        cs[y + 1] = sx;
-      }
-    }
+    const double gap64 =
+        2.0 * 2.0 * (double)(d + (d + 63) / 64 + 6) * 1.1102230246251565e-16 * qn * cmax + 1e-300;
+    order_runs<DT>(out, cs, link, m, queries, qg, centroids, d, gap64, lane, 64);
   }
   wave_sync();
   for (int r = lane; r < n; r += 64) P[ql * n + r] = (int32_t)(out[r] & 0xffffffffu);
@@ -512,11 +478,10 @@ __global__ __launch_bounds__(256) void rank_select_wave_kernel(
 
 }  // namespace
 
-size_t rank_select_lds(int32_t nlist, int32_t cap, int32_t d, int dtype) {
+size_t rank_select_lds(int32_t nlist, int32_t cap) {
   int capp = 1;
   while (capp < 2 * cap) capp <<= 1;
-  return (size_t)stage_bytes(nlist, d, dtype == SIEVE_F32 ? 4 : 2) + (size_t)capp * 8 +
-         (size_t)cap * 8 + (size_t)cap;
+  return (size_t)keys_bytes(nlist) + (size_t)capp * 8 + (size_t)cap * 8 + (size_t)cap;
 }
 
 // `wide` (set after a launch reported more near-ties at a rank boundary than
@@ -525,8 +490,7 @@ template <int DT, int KPL>
 hipError_t launch_wave_t(const void* queries, int64_t q0, int32_t nqc, const void* centroids,
                          int32_t nlist, int32_t d, const float* scores, int32_t n, int32_t capw,
                          double cmax, int32_t* P, RoundCounters* rc, hipStream_t s) {
-  const int elem = DT == SIEVE_F32 ? 4 : 2;
-  const size_t lds = (size_t)4 * wave_region_bytes(capw, d, elem);
+  const size_t lds = (size_t)4 * wave_region_bytes(capw);
   static const hipError_t attr =
       hipFuncSetAttribute((const void*)rank_select_wave_kernel<DT, KPL>,
                           hipFuncAttributeMaxDynamicSharedMemorySize, 150 * 1024);
@@ -560,8 +524,8 @@ hipError_t launch_rank_select(int dtype, const void* queries, int64_t q0, int32_
   // one wave per query while the boundary buffer stays small
   const int elem = dtype == SIEVE_F32 ? 4 : 2;
   int capw = n + 128 < nlist ? n + 128 : nlist;
-  if (!wide && nlist <= 4096 && capw <= 64 * kKeysPerLane &&
-      4 * wave_region_bytes(capw, d, elem) <= 96 * 1024) {
+  if (!wide && nlist <= 1024 && capw <= 64 * kKeysPerLane &&
+      4 * wave_region_bytes(capw) <= 96 * 1024) {
     return dtype == SIEVE_F32
                ? launch_wave<SIEVE_F32>(queries, q0, nqc, centroids, nlist, d, scores, n, capw,
                                         cmax, P, rc, s)
@@ -572,8 +536,8 @@ hipError_t launch_rank_select(int dtype, const void* queries, int64_t q0, int32_
   // centroid, up to kMaxCand)
   int32_t cap = nlist < kMaxCand ? nlist : kMaxCand;
   if (!wide && n + 512 < cap) cap = n + 512;
-  while (cap > n && rank_select_lds(nlist, cap, d, dtype) > 150 * 1024) cap = (cap + n) / 2;
-  const size_t lds = rank_select_lds(nlist, cap, d, dtype);
+  while (cap > n && rank_select_lds(nlist, cap) > 150 * 1024) cap = (cap + n) / 2;
+  const size_t lds = rank_select_lds(nlist, cap);
   if (lds > 150 * 1024) return hipErrorInvalidValue;
   if (dtype == SIEVE_F32)
     hipLaunchKernelGGL((rank_select_kernel<SIEVE_F32, 256>), dim3(nqc), dim3(256), lds, s,
