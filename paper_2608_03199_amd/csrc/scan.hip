@@ -27,6 +27,7 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
   __shared__ int32_t s_q[kTileQ];
   __shared__ int32_t s_rank[kTileQ];
   __shared__ int64_t s_ex[kTileQ];
+  __shared__ int32_t s_hits[kTileQ];  // candidates per staged query in this tile
 
   const int d = D > 0 ? D : a.d;
   const RowGeom<DT> g = RowGeom<DT>::make(d);
@@ -90,6 +91,7 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
   __syncthreads();
   int t_next = s_claim;
   prefetch(t);
+  if (threadIdx.x < kTileQ) s_hits[threadIdx.x] = 0;
   for (; t >= 0;) {
     const Tile tile = nt;
     if ((int)threadIdx.x < tile.nq) {
@@ -125,30 +127,45 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
               }
             }
             if (__ballot(any) == 0) return;
-            if (!any) return;
+            // Candidates: pool slots are claimed once per ballot group; the
+            // per-query count and hit flag go to LDS and reach global memory
+            // once per tile (after the tile's last row block).
 #pragma unroll
             for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
               for (int r = 0; r < 4; ++r) {
                 const int i = qb * 16 + 4 * h + r;
                 const float sc = acc[qb][r];
-                if ((i < nq) && (sc >= a.tau) && rid != s_ex[i]) {
-                  const int q = s_q[i];
-                  const unsigned long long slot = atomicAdd(a.pool_count, 1ull);
+                const bool hit = any && (row < r1) && (i < nq) && (sc >= a.tau) && rid != s_ex[i];
+                const unsigned long long mask = __ballot(hit);
+                if (mask == 0) continue;
+                unsigned long long base = 0;
+                if (lane == __ffsll((long long)mask) - 1)
+                  base = atomicAdd(a.pool_count, (unsigned long long)__popcll(mask));
+                base = __shfl(base, __ffsll((long long)mask) - 1);
+                if (hit) {
+                  const unsigned long long slot =
+                      base + (unsigned long long)__popcll(mask & ((1ull << lane) - 1ull));
                   if ((int64_t)slot < a.pool_cap) {
                     Hit hv;
                     hv.score = sc;
-                    hv.q = q;
+                    hv.q = s_q[i];
                     hv.id = rid;
                     a.pool[slot] = hv;
                   }
-                  atomicAdd(&a.hcount[q], 1);
-                  atomicMax(&a.lmax[q], s_rank[i] + 1);
+                  atomicAdd(&s_hits[i], 1);
                 }
               }
             }
           });
     __syncthreads();  // LDS is restaged by the next tile
+    if ((int)threadIdx.x < nq && s_hits[threadIdx.x] > 0) {
+      // this tile's candidates of one query: one count update, one hit flag
+      const int q = s_q[threadIdx.x];
+      atomicAdd(&a.hcount[q], s_hits[threadIdx.x]);
+      atomicMax(&a.lmax[q], s_rank[threadIdx.x] + 1);
+      s_hits[threadIdx.x] = 0;
+    }
     if (threadIdx.x == 0) s_claim = t_after;
     __syncthreads();
     t = t_next;

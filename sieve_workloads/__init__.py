@@ -207,7 +207,8 @@ def make(spec: WorkloadSpec | str, device: Optional[str] = None, seed: Optional[
     dev = torch.device(device)
     N, d, s = spec.n, spec.d, spec.seed
     sdt = _torch_dtype(spec.dtype)
-    chunk = max(1, (1 << 26) // d)
+    chunk = max(1, (1 << 26) // d)              # rows per elementwise chunk
+    mchunk = max(1, (1 << 28) // spec.nlist)    # rows per (rows x nlist) score block
 
     # mixture corpus
     g_c = _gen(s, "centres", dev)
@@ -256,7 +257,7 @@ def make(spec: WorkloadSpec | str, device: Optional[str] = None, seed: Optional[
     cent = xsamp[: spec.nlist].clone()
     for _ in range(spec.kmeans_iters):
         assign = torch.empty(ns, dtype=torch.int64, device=dev)
-        for a, b in _rows(ns, chunk):
+        for a, b in _rows(ns, mchunk):
             assign[a:b] = (xsamp[a:b] @ cent.T).argmax(dim=1)
         sums = torch.zeros_like(cent).index_add_(0, assign, xsamp)
         cnt = torch.bincount(assign, minlength=spec.nlist)
@@ -268,7 +269,7 @@ def make(spec: WorkloadSpec | str, device: Optional[str] = None, seed: Optional[
 
     # exact assignment, partition-major layout
     margin = 4.0 * d * 2.0 ** -24 + 1e-7
-    assign, refined = _argmax_ip(xs_store, c_store, margin, chunk)
+    assign, refined = _argmax_ip(xs_store, c_store, margin, mchunk)
     order = torch.sort(assign, stable=True).indices
     counts = torch.bincount(assign, minlength=spec.nlist)
     offsets = torch.zeros(spec.nlist + 1, dtype=torch.int64, device=dev)
