@@ -17,6 +17,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <string>
 #include <vector>
 
@@ -90,7 +91,7 @@ struct sieve_index {
   double cmax = 0.0;
   // workspace, grown on demand
   Buf scores, P, items, bucket, tiles, cnt, item_off, cursor, tile_off, rc, state_a, state_b,
-      lmax, hcount, hoff, hcur, scan_tmp, pool, pool_sorted;
+      lmax, hcount, hoff, hcur, scan_tmp, pool, pool_sorted, arenas, have, ext, qext, Pext;
   int64_t pool_cap = 0;
   RoundCounters* rc_host = nullptr;
   // phase timing (only when stats are requested): events are recorded on the
@@ -200,6 +201,8 @@ struct SearchPlan {
   int64_t rank_chunk;  // queries per centroid-screen chunk
   int64_t fix_chunk;   // queries per fixed-probe chunk
   int64_t item_cap;
+  int r0;              // ranks ordered up front (the rest on demand)
+  int scan_grid;       // scan work-groups (fixed for the whole search)
   bool wide_rank;      // rank with room for every boundary near-tie (retry path)
 };
 
@@ -237,15 +240,19 @@ int grow_workspace(sieve_index* ix, const SearchPlan& pl) {
     return st;
   if ((st = ensure(ix->rc, sizeof(RoundCounters)))) return st;
   const size_t qn = (size_t)nq * 4;
+  if ((st = ensure(ix->have, qn)) || (st = ensure(ix->ext, qn))) return st;
   if ((st = ensure(ix->state_a, qn)) || (st = ensure(ix->state_b, qn)) ||
       (st = ensure(ix->lmax, qn)) || (st = ensure(ix->hcount, qn)) ||
       (st = ensure(ix->hoff, qn)) || (st = ensure(ix->hcur, qn)))
     return st;
   if ((st = ensure(ix->scan_tmp, exclusive_scan_tmp_elems(nq) * 4))) return st;
-  if (ix->pool_cap == 0) {
+  if ((st = ensure(ix->arenas, (size_t)pl.scan_grid * sizeof(ArenaRec)))) return st;
+  // arena runs can leave up to kArenaMax unused slots per scan work-group
+  const int64_t slack = (int64_t)pl.scan_grid * kArenaMax;
+  if (ix->pool_cap < slack + (1 << 20)) {
     int64_t cap = nq * 16;
     if (cap < (1 << 20)) cap = 1 << 20;
-    ix->pool_cap = cap;
+    ix->pool_cap = cap + slack;
   }
   if ((st = ensure(ix->pool, (size_t)ix->pool_cap * sizeof(Hit)))) return st;
   if ((st = ensure(ix->pool_sorted, (size_t)ix->pool_cap * sizeof(Hit)))) return st;
@@ -254,15 +261,17 @@ int grow_workspace(sieve_index* ix, const SearchPlan& pl) {
 }
 
 // Centroid order of queries [q0, q0 + cnt) into P (row-major [cnt][n]).
-int rank_queries(sieve_index* ix, const void* queries, int64_t q0, int64_t cnt,
-                 const SearchPlan& pl, int32_t* P, hipStream_t s) {
+// Order the first nsel centroids of queries [q0, q0 + cnt) into rows of P
+// (row stride ldp), in chunks whose screen scores fit the score buffer.
+int rank_queries(sieve_index* ix, const void* queries, int64_t q0, int64_t cnt, int nsel,
+                 int64_t ldp, const SearchPlan& pl, int32_t* P, hipStream_t s) {
   RoundCounters* rc = (RoundCounters*)ix->rc.p;
   for (int64_t a = 0; a < cnt; a += pl.rank_chunk) {
     const int32_t c = (int32_t)((cnt - a) < pl.rank_chunk ? (cnt - a) : pl.rank_chunk);
     HIP_TRY(launch_rank_scores(ix->dtype, queries, q0 + a, c, ix->centroids, ix->nlist, ix->d,
                                (float*)ix->scores.p, s));
     HIP_TRY(launch_rank_select(ix->dtype, queries, q0 + a, c, ix->centroids, ix->nlist, ix->d,
-                               (const float*)ix->scores.p, pl.n, ix->cmax, P + a * pl.n, rc,
+                               (const float*)ix->scores.p, nsel, ix->cmax, P + a * ldp, ldp, rc,
                                pl.wide_rank, s));
   }
   return SIEVE_OK;
@@ -283,6 +292,7 @@ ScanArgs make_scan_args(sieve_index* ix, const void* queries, const int64_t* exc
   a.lmax = (int32_t*)ix->lmax.p;
   a.hcount = (int32_t*)ix->hcount.p;
   a.pool = (Hit*)ix->pool.p;
+  a.arenas = (ArenaRec*)ix->arenas.p;
   a.pool_count = &rc->hits;
   a.pool_cap = ix->pool_cap;
   a.d = ix->d;
@@ -308,7 +318,7 @@ int run_round(sieve_index* ix, const ScanArgs& sa, int n_items, int64_t q0, cons
   const int e1 = mark(ix, timed, s);
   ScanArgs sr = sa;
   sr.dynamic = scan_dynamic(n_items);
-  HIP_TRY(launch_scan(ix->dtype, sr, scan_grid(ix, pl.tile_q), s));
+  HIP_TRY(launch_scan(ix->dtype, sr, pl.scan_grid, s));
   const int e2 = mark(ix, timed, s);
   span(ix, kSched, e0, e1);
   span(ix, kScan, e1, e2);
@@ -336,19 +346,22 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     reset_timeline(ix);
     int rounds = 0;
     int64_t items_total = 0;
+    int64_t ext_total = 0;
     ScanArgs sa = sa0;
     sa.pool = (Hit*)ix->pool.p;
     sa.pool_cap = ix->pool_cap;
 
     const int t_begin = mark(ix, timed, s);
     HIP_TRY(launch_zero_bytes(rc, sizeof(RoundCounters), s));
+    HIP_TRY(launch_zero_bytes(ix->arenas.p, (size_t)pl.scan_grid * sizeof(ArenaRec), s));
     HIP_TRY(launch_fill_i32((int32_t*)ix->cnt.p, ix->nlist, 0, s));
     HIP_TRY(launch_fill_i32((int32_t*)ix->hcount.p, nq, 0, s));
     int32_t* P = (int32_t*)ix->P.p;
 
     if (pl.mode != 2) {
       const int r0 = mark(ix, timed, s);
-      if ((st = rank_queries(ix, queries, 0, nq, pl, P, s))) return st;
+      if ((st = rank_queries(ix, queries, 0, nq, pl.r0, pl.n, pl, P, s))) return st;
+      HIP_TRY(launch_fill_i32((int32_t*)ix->have.p, nq, pl.r0, s));
       const int s0 = pl.mode == 0 ? (pl.W < pl.n ? pl.W : pl.n) : 1;
       HIP_TRY(launch_emit_initial(P, pl.n, nq, 0, s0, pl.mode, (Item*)ix->items.p,
                                   (int32_t*)ix->cnt.p, (int32_t*)ix->state_a.p,
@@ -358,13 +371,15 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
       while (n_items > 0) {
         if ((st = run_round(ix, sa, (int)n_items, 0, P, pl, s, timed))) return st;
         const int u0 = mark(ix, timed, s);
+        int32_t* have = (int32_t*)ix->have.p;
+        int32_t* ext = (int32_t*)ix->ext.p;
         if (pl.mode == 0)
           HIP_TRY(launch_update_lookahead(nq, P, pl.n, pl.W, (int32_t*)ix->state_a.p,
-                                          (int32_t*)ix->lmax.p, (Item*)ix->items.p,
+                                          (int32_t*)ix->lmax.p, have, ext, (Item*)ix->items.p,
                                           (int32_t*)ix->cnt.p, rc, s));
         else
           HIP_TRY(launch_update_basic(nq, P, pl.n, pl.W, (int32_t*)ix->state_a.p,
-                                      (int32_t*)ix->state_b.p, (int32_t*)ix->lmax.p,
+                                      (int32_t*)ix->state_b.p, (int32_t*)ix->lmax.p, have, ext,
                                       (Item*)ix->items.p, (int32_t*)ix->cnt.p, rc, s));
         span(ix, kUpdate, u0, mark(ix, timed, s));
         HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
@@ -372,6 +387,28 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
         items_total += n_items;
         ++rounds;
         if (ix->rc_host->rank_error) break;  // handled below: re-rank wide or fail
+        if (const int32_t n_ext = ix->rc_host->n_ext) {
+          // stop lines passed the ordered prefix: order every rank of those queries
+          const int x0 = mark(ix, timed, s);
+          const int64_t rb = (int64_t)ix->d * e;
+          if ((st = ensure(ix->qext, (size_t)n_ext * rb)) ||
+              (st = ensure(ix->Pext, (size_t)n_ext * pl.n * sizeof(int32_t))))
+            return st;
+          HIP_TRY(launch_gather_rows(ext, n_ext, queries, rb, ix->qext.p, s));
+          if ((st = rank_queries(ix, ix->qext.p, 0, n_ext, pl.n, pl.n, pl, (int32_t*)ix->Pext.p,
+                                 s)))
+            return st;
+          HIP_TRY(launch_scatter_ranks(ext, n_ext, (const int32_t*)ix->Pext.p, pl.n, P, s));
+          HIP_TRY(launch_emit_pending(ext, n_ext, pl.mode, P, pl.n, (const int32_t*)ix->state_a.p,
+                                      have, pl.n, (Item*)ix->items.p, (int32_t*)ix->cnt.p, rc,
+                                      s));
+          span(ix, kRank, x0, mark(ix, timed, s));
+          HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost,
+                                 s));
+          HIP_TRY(hipStreamSynchronize(s));
+          ext_total += n_ext;
+          if (ix->rc_host->rank_error) break;
+        }
         n_items = ix->rc_host->new_items;
         if (n_items > pl.item_cap)
           return fail(SIEVE_EINTERNAL, "round emitted %lld items, capacity %lld",
@@ -381,7 +418,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
       for (int64_t q0 = 0; q0 < nq; q0 += pl.fix_chunk) {
         const int64_t c = (nq - q0) < pl.fix_chunk ? (nq - q0) : pl.fix_chunk;
         const int r0 = mark(ix, timed, s);
-        if ((st = rank_queries(ix, queries, q0, c, pl, P, s))) return st;
+        if ((st = rank_queries(ix, queries, q0, c, pl.n, pl.n, pl, P, s))) return st;
         HIP_TRY(launch_emit_initial(P, pl.n, c, (int32_t)q0, pl.n, 2, (Item*)ix->items.p,
                                     (int32_t*)ix->cnt.p, nullptr, nullptr, nullptr, s));
         span(ix, kRank, r0, mark(ix, timed, s));
@@ -404,7 +441,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     const int64_t hits = (int64_t)ix->rc_host->hits;
     if (hits > ix->pool_cap) {
       // the pool overflowed: grow it and run again (the search is deterministic)
-      ix->pool_cap = hits + hits / 8 + 1024;
+      ix->pool_cap = hits + hits / 8 + (int64_t)pl.scan_grid * kArenaMax;
       if ((st = ensure(ix->pool, (size_t)ix->pool_cap * sizeof(Hit)))) return st;
       if ((st = ensure(ix->pool_sorted, (size_t)ix->pool_cap * sizeof(Hit)))) return st;
       if (++pool_retries > 2) return fail(SIEVE_EINTERNAL, "candidate pool kept overflowing");
@@ -413,6 +450,8 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
 
     // finalize: group the pool by query, then per-query top-k
     const int f0 = mark(ix, timed, s);
+    HIP_TRY(launch_retire_arenas((const ArenaRec*)ix->arenas.p, pl.scan_grid, (Hit*)ix->pool.p,
+                                 ix->pool_cap, s));
     HIP_TRY(launch_exclusive_scan((const int32_t*)ix->hcount.p, (int32_t*)ix->hoff.p,
                                   (int32_t*)ix->hcur.p, nq, (int32_t*)ix->scan_tmp.p, s));
     HIP_TRY(launch_pool_scatter((const Hit*)ix->pool.p, hits, (int32_t*)ix->hcur.p,
@@ -442,9 +481,9 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
       stats->probes_total = (int64_t)h.probes;
       stats->vectors_scanned = (int64_t)h.item_rows;
       stats->list_loads = (int64_t)h.list_loads;
-      stats->hits = (int64_t)h.hits;
+      stats->hits = (int64_t)h.candidates;
       stats->scan_bytes = (double)h.list_rows * eb + (double)items_total * (eb + sizeof(Item)) +
-                          (double)h.hits * sizeof(Hit);
+                          (double)h.candidates * sizeof(Hit);
       stats->scan_flops = 2.0 * (double)ix->d * (double)h.item_rows;
       stats->rank_flops = 2.0 * (double)ix->d * (double)nq * (double)ix->nlist;
       stats->ms_rank = ms[kRank];
@@ -471,6 +510,14 @@ int plan_search(const sieve_index* ix, int64_t nq, int32_t k, float tau, int32_t
   pl->tile_q = tile_rows(ix->dtype, ix->d);
   pl->wide_rank = false;
   pl->row_chunk = row_chunk_for(ix);
+  pl->scan_grid = scan_grid(ix, pl->tile_q);
+  // Lazy ranking: a stop line starts at min(W, n) and mostly stays near it,
+  // so only the first r0 ranks are ordered up front (queries whose stop line
+  // passes r0 get all n later).
+  const int64_t r0 = env_int("SIEVE_RANK_PREFIX", 32);
+  const int64_t w2 = 2 * (int64_t)W;
+  pl->r0 = mode == 2 || (int64_t)W >= pl->n ? pl->n
+                                           : (int)std::min<int64_t>(pl->n, std::max(r0, w2));
   int64_t rc = (int64_t)(256ll << 20) / ((int64_t)ix->nlist * 4);
   if (rc < 64) rc = 64;
   pl->rank_chunk = nq < rc ? nq : rc;
@@ -587,7 +634,8 @@ SIEVE_API void sieve_free_index(sieve_index* ix) {
   Buf* bufs[] = {&ix->scores, &ix->P, &ix->items, &ix->bucket, &ix->tiles, &ix->cnt,
                  &ix->item_off, &ix->cursor, &ix->tile_off, &ix->rc, &ix->state_a,
                  &ix->state_b, &ix->lmax, &ix->hcount, &ix->hoff, &ix->hcur, &ix->scan_tmp,
-                 &ix->pool, &ix->pool_sorted};
+                 &ix->pool, &ix->pool_sorted, &ix->arenas, &ix->have, &ix->ext, &ix->qext,
+                 &ix->Pext};
   for (Buf* b : bufs)
     if (b->p) (void)hipFree(b->p);
   if (ix->vectors) (void)hipFree(ix->vectors);
@@ -650,7 +698,7 @@ SIEVE_API int sieve_rank(const sieve_index* idx, const void* queries, int64_t nq
   for (int attempt = 0; attempt < 2; ++attempt) {
     pl.wide_rank = attempt > 0;
     HIP_TRY(launch_zero_bytes(rc, sizeof(RoundCounters), s));
-    if ((st = rank_queries(ix, queries, 0, nq, pl, out_order, s))) return st;
+    if ((st = rank_queries(ix, queries, 0, nq, pl.n, pl.n, pl, out_order, s))) return st;
     HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
     if (!ix->rc_host->rank_error) return SIEVE_OK;

@@ -147,7 +147,7 @@ template <int DT, int NT>
 __global__ __launch_bounds__(NT) void rank_select_kernel(
     const void* __restrict__ queries, int64_t q0, const void* __restrict__ centroids,
     int32_t nlist, int32_t d, const float* __restrict__ scores, int32_t n, int32_t cap,
-    double cmax, int32_t* __restrict__ P, RoundCounters* rc) {
+    double cmax, int32_t* __restrict__ P, int64_t ldp, RoundCounters* rc) {
   constexpr int kWaves = NT / 64;
   constexpr int kBins = 256;
   constexpr int kBPT = kBins / NT > 0 ? kBins / NT : 1;  // bins per thread
@@ -281,7 +281,7 @@ __global__ __launch_bounds__(NT) void rank_select_kernel(
     // re-ranks with the wide buffer.  The row still gets valid list ids so
     // that every kernel that runs before the check stays in bounds.
     if (t == 0) atomicExch(&rc->rank_error, 1);
-    for (int r = t; r < n; r += NT) P[ql * n + r] = r;
+    for (int r = t; r < n; r += NT) P[ql * ldp + r] = r;
     return;
   }
 
@@ -345,7 +345,7 @@ __global__ __launch_bounds__(NT) void rank_select_kernel(
   }
   __syncthreads();
   // 4. the first n
-  for (int r = t; r < n; r += NT) P[ql * n + r] = (int32_t)(ck[r] & 0xffffffffu);
+  for (int r = t; r < n; r += NT) P[ql * ldp + r] = (int32_t)(ck[r] & 0xffffffffu);
 }
 
 // Boundary candidates per lane in the wave kernel (capw <= 64 * this).
@@ -379,7 +379,7 @@ template <int DT, int KPL>
 __global__ __launch_bounds__(256) void rank_select_wave_kernel(
     const void* __restrict__ queries, int64_t q0, int32_t nqc, const void* __restrict__ centroids,
     int32_t nlist, int32_t d, const float* __restrict__ scores, int32_t n, int32_t capw,
-    double cmax, int32_t* __restrict__ P, RoundCounters* rc) {
+    double cmax, int32_t* __restrict__ P, int64_t ldp, RoundCounters* rc) {
   extern __shared__ uint8_t smem[];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t ql = (int64_t)blockIdx.x * 4 + wave;
@@ -438,7 +438,7 @@ __global__ __launch_bounds__(256) void rank_select_wave_kernel(
   }
   if (m > capw || m < n) {
     if (lane == 0) atomicExch(&rc->rank_error, 1);
-    for (int r = lane; r < n; r += 64) P[ql * n + r] = r;
+    for (int r = lane; r < n; r += 64) P[ql * ldp + r] = r;
     return;
   }
   wave_sync();
@@ -473,7 +473,7 @@ __global__ __launch_bounds__(256) void rank_select_wave_kernel(
     order_runs<DT>(out, cs, link, m, queries, qg, centroids, d, gap64, lane, 64);
   }
   wave_sync();
-  for (int r = lane; r < n; r += 64) P[ql * n + r] = (int32_t)(out[r] & 0xffffffffu);
+  for (int r = lane; r < n; r += 64) P[ql * ldp + r] = (int32_t)(out[r] & 0xffffffffu);
 }
 
 }  // namespace
@@ -489,7 +489,8 @@ size_t rank_select_lds(int32_t nlist, int32_t cap) {
 template <int DT, int KPL>
 hipError_t launch_wave_t(const void* queries, int64_t q0, int32_t nqc, const void* centroids,
                          int32_t nlist, int32_t d, const float* scores, int32_t n, int32_t capw,
-                         double cmax, int32_t* P, RoundCounters* rc, hipStream_t s) {
+                         double cmax, int32_t* P, int64_t ldp, RoundCounters* rc,
+                         hipStream_t s) {
   const size_t lds = (size_t)4 * wave_region_bytes(capw);
   static const hipError_t attr =
       hipFuncSetAttribute((const void*)rank_select_wave_kernel<DT, KPL>,
@@ -498,28 +499,29 @@ hipError_t launch_wave_t(const void* queries, int64_t q0, int32_t nqc, const voi
   if (lds > 150 * 1024) return hipErrorInvalidValue;
   hipLaunchKernelGGL((rank_select_wave_kernel<DT, KPL>), dim3((unsigned)((nqc + 3) / 4)),
                      dim3(256), lds, s, queries, q0, nqc, centroids, nlist, d, scores, n, capw,
-                     cmax, P, rc);
+                     cmax, P, ldp, rc);
   return hipGetLastError();
 }
 
 template <int DT>
 hipError_t launch_wave(const void* queries, int64_t q0, int32_t nqc, const void* centroids,
                        int32_t nlist, int32_t d, const float* scores, int32_t n, int32_t capw,
-                       double cmax, int32_t* P, RoundCounters* rc, hipStream_t s) {
+                       double cmax, int32_t* P, int64_t ldp, RoundCounters* rc,
+                       hipStream_t s) {
   if (nlist <= 256)
-    return launch_wave_t<DT, 4>(queries, q0, nqc, centroids, nlist, d, scores, n, capw, cmax, P,
-                                rc, s);
+    return launch_wave_t<DT, 4>(queries, q0, nqc, centroids, nlist, d, scores, n, capw, cmax,
+                                  P, ldp, rc, s);
   if (nlist <= 1024)
-    return launch_wave_t<DT, 16>(queries, q0, nqc, centroids, nlist, d, scores, n, capw, cmax, P,
-                                 rc, s);
-  return launch_wave_t<DT, 64>(queries, q0, nqc, centroids, nlist, d, scores, n, capw, cmax, P,
-                               rc, s);
+    return launch_wave_t<DT, 16>(queries, q0, nqc, centroids, nlist, d, scores, n, capw, cmax,
+                                  P, ldp, rc, s);
+  return launch_wave_t<DT, 64>(queries, q0, nqc, centroids, nlist, d, scores, n, capw, cmax,
+                                 P, ldp, rc, s);
 }
 
 hipError_t launch_rank_select(int dtype, const void* queries, int64_t q0, int32_t nqc,
                               const void* centroids, int32_t nlist, int32_t d, const float* scores,
-                              int32_t n, double cmax, int32_t* P, RoundCounters* rc, bool wide,
-                              hipStream_t s) {
+                              int32_t n, double cmax, int32_t* P, int64_t ldp, RoundCounters* rc,
+                              bool wide, hipStream_t s) {
   if (nqc <= 0) return hipSuccess;
   // one wave per query while the boundary buffer stays small
   const int elem = dtype == SIEVE_F32 ? 4 : 2;
@@ -528,9 +530,9 @@ hipError_t launch_rank_select(int dtype, const void* queries, int64_t q0, int32_
       4 * wave_region_bytes(capw) <= 96 * 1024) {
     return dtype == SIEVE_F32
                ? launch_wave<SIEVE_F32>(queries, q0, nqc, centroids, nlist, d, scores, n, capw,
-                                        cmax, P, rc, s)
+                                        cmax, P, ldp, rc, s)
                : launch_wave<SIEVE_F16>(queries, q0, nqc, centroids, nlist, d, scores, n, capw,
-                                        cmax, P, rc, s);
+                                        cmax, P, ldp, rc, s);
   }
   // block kernel: narrow (n + 512 boundary candidates) or wide (every
   // centroid, up to kMaxCand)
@@ -541,10 +543,10 @@ hipError_t launch_rank_select(int dtype, const void* queries, int64_t q0, int32_
   if (lds > 150 * 1024) return hipErrorInvalidValue;
   if (dtype == SIEVE_F32)
     hipLaunchKernelGGL((rank_select_kernel<SIEVE_F32, 256>), dim3(nqc), dim3(256), lds, s,
-                       queries, q0, centroids, nlist, d, scores, n, cap, cmax, P, rc);
+                       queries, q0, centroids, nlist, d, scores, n, cap, cmax, P, ldp, rc);
   else
     hipLaunchKernelGGL((rank_select_kernel<SIEVE_F16, 256>), dim3(nqc), dim3(256), lds, s,
-                       queries, q0, centroids, nlist, d, scores, n, cap, cmax, P, rc);
+                       queries, q0, centroids, nlist, d, scores, n, cap, cmax, P, ldp, rc);
   return hipGetLastError();
 }
 

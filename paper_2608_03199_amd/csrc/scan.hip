@@ -16,6 +16,14 @@
 // Work distribution: a persistent grid pulls tiles from a per-XCD work queue
 // (see the kernel); every block exits after its claims run dry, at most
 // tiles + 8 claims per block.
+//
+// Candidate pool: a block appends into a run of pool slots (its arena) that
+// it claimed with one global atomic, handing out slots with one LDS atomic
+// per ballot group of candidates.  A group that does not fit the arena claims
+// its slots from the global counter directly, and at the end of that tile the
+// block gives the arena's unused tail sentinel entries and claims a run twice
+// as long (up to kArenaMax).  The arena carries over to the block's next
+// launch in the same search; blocks that never meet a candidate claim nothing.
 #include "mfma_tile.h"
 
 namespace sieve {
@@ -28,6 +36,11 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
   __shared__ int32_t s_rank[kTileQ];
   __shared__ int64_t s_ex[kTileQ];
   __shared__ int32_t s_hits[kTileQ];  // candidates per staged query in this tile
+  __shared__ unsigned long long s_abase;  // first pool slot of the block's arena
+  __shared__ int32_t s_asize;  // arena slots (0: no arena)
+  __shared__ int32_t s_aused;  // arena slots handed out (may run past s_asize)
+  __shared__ int32_t s_afill;  // arena slots actually used (a prefix of the arena)
+  __shared__ int32_t s_afall;  // a group fell back to the global counter this tile
 
   const int d = D > 0 ? D : a.d;
   const RowGeom<DT> g = RowGeom<DT>::make(d);
@@ -92,6 +105,14 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
   int t_next = s_claim;
   prefetch(t);
   if (threadIdx.x < kTileQ) s_hits[threadIdx.x] = 0;
+  if (threadIdx.x == 0) {
+    const ArenaRec ar = a.arenas[blockIdx.x];  // the run left by the previous launch
+    s_abase = ar.base;
+    s_asize = ar.size;
+    s_aused = ar.fill;  // no run (size 0): every group takes the global path
+    s_afill = ar.fill;
+    s_afall = 0;
+  }
   for (; t >= 0;) {
     const Tile tile = nt;
     if ((int)threadIdx.x < tile.nq) {
@@ -127,22 +148,38 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
               }
             }
             if (__ballot(any) == 0) return;
-            // Candidates: pool slots are claimed once per ballot group; the
-            // per-query count and hit flag go to LDS and reach global memory
-            // once per tile (after the tile's last row block).
+            // Candidates: one ballot group (16 rows x 4 queries) takes its
+            // pool slots with one LDS atomic on the block's arena; the
+            // per-query counts go to LDS (one add per query of the group)
+            // and reach global memory once per tile.
+            const int r16 = lane & 15;
 #pragma unroll
             for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
               for (int r = 0; r < 4; ++r) {
                 const int i = qb * 16 + 4 * h + r;
                 const float sc = acc[qb][r];
-                const bool hit = any && (row < r1) && (i < nq) && (sc >= a.tau) && rid != s_ex[i];
+                bool hit = any && (row < r1) && (i < nq) && (sc >= a.tau);
+                if (__ballot(hit) == 0) continue;
+                hit = hit && rid != s_ex[i];  // self-exclusion, read only for qualifying pairs
                 const unsigned long long mask = __ballot(hit);
                 if (mask == 0) continue;
+                const int leader = __ffsll((long long)mask) - 1;  // wave-uniform
                 unsigned long long base = 0;
-                if (lane == __ffsll((long long)mask) - 1)
-                  base = atomicAdd(a.pool_count, (unsigned long long)__popcll(mask));
-                base = __shfl(base, __ffsll((long long)mask) - 1);
+                if (lane == leader) {
+                  const int cnt = __popcll(mask);
+                  const int o = atomicAdd(&s_aused, cnt);
+                  if (o + cnt <= s_asize) {
+                    base = s_abase + (unsigned long long)o;
+                    atomicAdd(&s_afill, cnt);
+                  } else {
+                    base = atomicAdd(a.pool_count, (unsigned long long)cnt);
+                    s_afall = 1;
+                  }
+                }
+                base = ((unsigned long long)(uint32_t)__builtin_amdgcn_readlane(
+                            (int)(base >> 32), leader) << 32) |
+                       (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)base, leader);
                 if (hit) {
                   const unsigned long long slot =
                       base + (unsigned long long)__popcll(mask & ((1ull << lane) - 1ull));
@@ -153,7 +190,10 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
                     hv.id = rid;
                     a.pool[slot] = hv;
                   }
-                  atomicAdd(&s_hits[i], 1);
+                }
+                if (r16 == 0) {
+                  const int c = __popcll((mask >> (16 * h)) & 0xffffull);
+                  if (c) atomicAdd(&s_hits[i], c);
                 }
               }
             }
@@ -166,10 +206,38 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
       atomicMax(&a.lmax[q], s_rank[threadIdx.x] + 1);
       s_hits[threadIdx.x] = 0;
     }
-    if (threadIdx.x == 0) s_claim = t_after;
+    const bool refill = s_afall != 0;  // block-uniform: written before the barrier
+    if (refill) {
+      // sentinels over the unused tail of the arena being replaced
+      const unsigned long long ab = s_abase;
+      const Hit none = {-INFINITY, -1, -1};
+      for (int i = s_afill + (int)threadIdx.x; i < s_asize; i += blockDim.x) {
+        const unsigned long long slot = ab + (unsigned long long)i;
+        if ((int64_t)slot < a.pool_cap) a.pool[slot] = none;
+      }
+      __syncthreads();  // everyone has read the old arena before it is replaced
+    }
+    if (threadIdx.x == 0) {
+      s_claim = t_after;
+      if (refill) {
+        const int sz = s_asize == 0 ? kArenaMin : min(2 * s_asize, kArenaMax);
+        s_abase = atomicAdd(a.pool_count, (unsigned long long)sz);
+        s_asize = sz;
+        s_aused = 0;
+        s_afill = 0;
+        s_afall = 0;
+      }
+    }
     __syncthreads();
     t = t_next;
     t_next = s_claim;
+  }
+  if (threadIdx.x == 0) {
+    ArenaRec ar;
+    ar.base = s_abase;
+    ar.size = s_asize;
+    ar.fill = s_afill;
+    a.arenas[blockIdx.x] = ar;
   }
 }
 

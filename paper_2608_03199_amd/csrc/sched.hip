@@ -17,6 +17,11 @@
 //   basic (Algorithm 1): one rank per round; stale resets on a hit and grows
 //     on an empty probe; the next rank is emitted while stale < W and
 //     next <= n.
+// Ranks are ordered lazily: P holds the first have[q] ranks of query q.  An
+// update that commits a rank at or beyond have[q] emits what it can, lists
+// the query, and the host extends the listed queries' rank prefix before the
+// next round (emit_pending then emits the rest).  Only the round in which an
+// item is dispatched changes, which the result does not depend on (Sec. 4.3).
 #include "sieve_internal.h"
 
 namespace sieve {
@@ -120,6 +125,7 @@ __global__ __launch_bounds__(kOffThreads) void sched_offsets_kernel(
   if (t == 0) {
     rc->ntiles = (int32_t)s_tiles[kOffThreads - 1];
     rc->new_items = 0;
+    rc->n_ext = 0;
     for (int x = 0; x < 8; ++x) rc->queue[x] = 0;
     rc->list_rows += s_stat[0];
     rc->item_rows += s_stat[1];
@@ -168,7 +174,9 @@ __global__ void sched_tiles_kernel(int32_t* __restrict__ cnt, const int32_t* __r
 
 __global__ void update_lookahead_kernel(int64_t nq, const int32_t* __restrict__ P, int32_t n,
                                         int32_t W, int32_t* __restrict__ stop,
-                                        int32_t* __restrict__ lmax, Item* __restrict__ items,
+                                        int32_t* __restrict__ lmax,
+                                        const int32_t* __restrict__ have,
+                                        int32_t* __restrict__ ext, Item* __restrict__ items,
                                         int32_t* __restrict__ cnt, RoundCounters* rc) {
   const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (q >= nq) return;
@@ -178,14 +186,19 @@ __global__ void update_lookahead_kernel(int64_t nq, const int32_t* __restrict__ 
   const int s = stop[q];
   const int reach = (W > n - L) ? n : L + W;  // min(L + W, n) without overflow
   if (reach <= s) return;
-  const int base = atomicAdd(&rc->new_items, reach - s);
-  for (int j = s; j < reach; ++j) {
-    Item it;
-    it.q = (int32_t)q;
-    it.rank = j;
-    items[base + (j - s)] = it;
-    atomicAdd(&cnt[P[q * n + j]], 1);
+  const int hv = have[q];
+  const int e0 = min(s, hv), e1 = min(reach, hv);  // emitted so far / after this update
+  if (e1 > e0) {
+    const int base = atomicAdd(&rc->new_items, e1 - e0);
+    for (int j = e0; j < e1; ++j) {
+      Item it;
+      it.q = (int32_t)q;
+      it.rank = j;
+      items[base + (j - e0)] = it;
+      atomicAdd(&cnt[P[q * n + j]], 1);
+    }
   }
+  if (reach > hv) ext[atomicAdd(&rc->n_ext, 1)] = (int32_t)q;
   stop[q] = reach;
 }
 
@@ -194,6 +207,7 @@ __global__ void update_lookahead_kernel(int64_t nq, const int32_t* __restrict__ 
 __global__ void update_basic_kernel(int64_t nq, const int32_t* __restrict__ P, int32_t n,
                                     int32_t W, int32_t* __restrict__ next,
                                     int32_t* __restrict__ stale, int32_t* __restrict__ lmax,
+                                    const int32_t* __restrict__ have, int32_t* __restrict__ ext,
                                     Item* __restrict__ items, int32_t* __restrict__ cnt,
                                     RoundCounters* rc) {
   const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -207,16 +221,79 @@ __global__ void update_basic_kernel(int64_t nq, const int32_t* __restrict__ P, i
   if (st < W && nx < n) {
     stale[q] = st;
     next[q] = nx;
-    const int pos = atomicAdd(&rc->new_items, 1);
-    Item it;
-    it.q = (int32_t)q;
-    it.rank = nx;
-    items[pos] = it;
-    atomicAdd(&cnt[P[q * n + nx]], 1);
+    if (nx < have[q]) {
+      const int pos = atomicAdd(&rc->new_items, 1);
+      Item it;
+      it.q = (int32_t)q;
+      it.rank = nx;
+      items[pos] = it;
+      atomicAdd(&cnt[P[q * n + nx]], 1);
+    } else {
+      ext[atomicAdd(&rc->n_ext, 1)] = (int32_t)q;
+    }
   } else {
     next[q] = -1;
     stale[q] = nx;  // probes
   }
+}
+
+// Row copy in 16-byte units: dst row i <- src row ext[i].
+__global__ void gather_rows_kernel(const int32_t* __restrict__ ext, int32_t n_ext,
+                                   const uint4* __restrict__ src, int64_t row_u4,
+                                   uint4* __restrict__ dst) {
+  const int64_t total = (int64_t)n_ext * row_u4;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = e / row_u4, c = e - i * row_u4;
+    dst[e] = src[(int64_t)ext[i] * row_u4 + c];
+  }
+}
+
+__global__ void scatter_ranks_kernel(const int32_t* __restrict__ ext, int32_t n_ext,
+                                     const int32_t* __restrict__ Pext, int32_t n,
+                                     int32_t* __restrict__ P) {
+  const int64_t total = (int64_t)n_ext * n;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = e / n, j = e - i * n;
+    P[(int64_t)ext[i] * n + j] = Pext[e];
+  }
+}
+
+// After the listed queries' prefixes grew to new_have: lookahead (mode 0)
+// emits ranks [min(stop, have), min(stop, new_have)); basic (mode 1) emits
+// the rank in flight.
+__global__ void emit_pending_kernel(const int32_t* __restrict__ ext, int32_t n_ext, int32_t mode,
+                                    const int32_t* __restrict__ P, int32_t n,
+                                    const int32_t* __restrict__ state_a,
+                                    int32_t* __restrict__ have, int32_t new_have,
+                                    Item* __restrict__ items, int32_t* __restrict__ cnt,
+                                    RoundCounters* rc) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_ext) return;
+  const int64_t q = ext[i];
+  const int hv = have[q];
+  int e0, e1;
+  if (mode == 0) {
+    const int s = state_a[q];
+    e0 = min(s, hv);
+    e1 = min(s, new_have);
+  } else {
+    const int nx = state_a[q];
+    e0 = nx >= hv ? nx : 0;
+    e1 = nx >= hv && nx < new_have ? nx + 1 : 0;
+  }
+  if (e1 > e0) {
+    const int base = atomicAdd(&rc->new_items, e1 - e0);
+    for (int j = e0; j < e1; ++j) {
+      Item it;
+      it.q = (int32_t)q;
+      it.rank = j;
+      items[base + (j - e0)] = it;
+      atomicAdd(&cnt[P[q * n + j]], 1);
+    }
+  }
+  have[q] = new_have > hv ? new_have : hv;
 }
 
 __global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
@@ -267,18 +344,50 @@ hipError_t launch_sched_tiles(int32_t* cnt, const int32_t* item_off, const int32
 }
 
 hipError_t launch_update_lookahead(int64_t nq, const int32_t* P, int32_t n, int32_t W,
-                                   int32_t* stop, int32_t* lmax, Item* items, int32_t* cnt,
-                                   RoundCounters* rc, hipStream_t s) {
+                                   int32_t* stop, int32_t* lmax, const int32_t* have,
+                                   int32_t* ext, Item* items, int32_t* cnt, RoundCounters* rc,
+                                   hipStream_t s) {
   hipLaunchKernelGGL(update_lookahead_kernel, dim3(blocks_for(nq)), dim3(kThreads), 0, s, nq, P, n,
-                     W, stop, lmax, items, cnt, rc);
+                     W, stop, lmax, have, ext, items, cnt, rc);
   return hipGetLastError();
 }
 
 hipError_t launch_update_basic(int64_t nq, const int32_t* P, int32_t n, int32_t W, int32_t* next,
-                               int32_t* stale, int32_t* lmax, Item* items, int32_t* cnt,
-                               RoundCounters* rc, hipStream_t s) {
+                               int32_t* stale, int32_t* lmax, const int32_t* have, int32_t* ext,
+                               Item* items, int32_t* cnt, RoundCounters* rc, hipStream_t s) {
   hipLaunchKernelGGL(update_basic_kernel, dim3(blocks_for(nq)), dim3(kThreads), 0, s, nq, P, n, W,
-                     next, stale, lmax, items, cnt, rc);
+                     next, stale, lmax, have, ext, items, cnt, rc);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_rows(const int32_t* ext, int32_t n_ext, const void* src,
+                              int64_t row_bytes, void* dst, hipStream_t s) {
+  if (n_ext <= 0) return hipSuccess;
+  const int64_t row_u4 = row_bytes / 16;
+  const int64_t total = (int64_t)n_ext * row_u4;
+  const int64_t b = (total + kThreads - 1) / kThreads;
+  hipLaunchKernelGGL(gather_rows_kernel, dim3((unsigned)(b < 8192 ? b : 8192)), dim3(kThreads), 0,
+                     s, ext, n_ext, (const uint4*)src, row_u4, (uint4*)dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter_ranks(const int32_t* ext, int32_t n_ext, const int32_t* Pext,
+                                int32_t n, int32_t* P, hipStream_t s) {
+  if (n_ext <= 0) return hipSuccess;
+  const int64_t total = (int64_t)n_ext * n;
+  const int64_t b = (total + kThreads - 1) / kThreads;
+  hipLaunchKernelGGL(scatter_ranks_kernel, dim3((unsigned)(b < 8192 ? b : 8192)), dim3(kThreads),
+                     0, s, ext, n_ext, Pext, n, P);
+  return hipGetLastError();
+}
+
+hipError_t launch_emit_pending(const int32_t* ext, int32_t n_ext, int32_t mode, const int32_t* P,
+                               int32_t n, const int32_t* state_a, int32_t* have,
+                               int32_t new_have, Item* items, int32_t* cnt, RoundCounters* rc,
+                               hipStream_t s) {
+  if (n_ext <= 0) return hipSuccess;
+  hipLaunchKernelGGL(emit_pending_kernel, dim3(blocks_for(n_ext)), dim3(kThreads), 0, s, ext,
+                     n_ext, mode, P, n, state_a, have, new_have, items, cnt, rc);
   return hipGetLastError();
 }
 

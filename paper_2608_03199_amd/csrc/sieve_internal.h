@@ -46,12 +46,26 @@ struct RoundCounters {
   int32_t new_items;       // items emitted by the update for the next round
   int32_t queue[8];        // per-XCD tile cursors of the scan's work queue
   int32_t rank_error;      // set when a rank boundary has more than kMaxCand candidates
-  int32_t pad;
+  int32_t n_ext;           // queries whose stop line passed their ranked prefix (this round)
   unsigned long long list_rows;   // sum over active lists of their length (this round)
   unsigned long long item_rows;   // sum over items of their list's length (this round)
   unsigned long long list_loads;  // active non-empty lists (this round)
-  unsigned long long hits;        // pool appends (whole search)
+  unsigned long long hits;        // pool slots claimed (whole search; includes arena tails)
   unsigned long long probes;      // sum of out_probes (whole search)
+  unsigned long long candidates;  // qualifying candidates merged by the final top-k
+};
+
+// Candidate-pool arenas: a scan work-group claims pool slots in runs (first
+// kArenaMin, doubling per refill up to kArenaMax) and keeps its current run
+// across the launches of one search in an ArenaRec indexed by block.  The
+// slots of a run it never fills are given a sentinel entry (q = -1) that the
+// final merge skips, once per search.
+constexpr int kArenaMin = 256;
+constexpr int kArenaMax = 4096;
+struct ArenaRec {
+  unsigned long long base;  // first pool slot of the run
+  int32_t size;             // slots in the run, 0 = no run
+  int32_t fill;             // slots used (a prefix of the run)
 };
 
 struct ScanArgs {
@@ -66,6 +80,7 @@ struct ScanArgs {
   int32_t* lmax;               // [nq] max 1-based hit rank this round (0 = none)
   int32_t* hcount;             // [nq] pool entries per query
   Hit* pool;
+  ArenaRec* arenas;            // [scan grid] per-block pool runs
   unsigned long long* pool_count;
   int64_t pool_cap;
   int32_t d;
@@ -86,8 +101,8 @@ hipError_t launch_rank_scores(int dtype, const void* queries, int64_t q0, int32_
 size_t scan_lds_bytes(int dtype, int d, int rows);
 hipError_t launch_rank_select(int dtype, const void* queries, int64_t q0, int32_t nqc,
                               const void* centroids, int32_t nlist, int32_t d, const float* scores,
-                              int32_t n, double cmax, int32_t* P, RoundCounters* rc, bool wide,
-                              hipStream_t s);
+                              int32_t n, double cmax, int32_t* P, int64_t ldp, RoundCounters* rc,
+                              bool wide, hipStream_t s);
 
 hipError_t launch_emit_initial(const int32_t* P, int32_t n, int64_t nqc, int32_t q0, int32_t s0,
                                int32_t mode, Item* items, int32_t* cnt, int32_t* state_a,
@@ -102,18 +117,33 @@ hipError_t launch_sched_tiles(int32_t* cnt, const int32_t* item_off, const int32
                               const int64_t* list_offsets, int32_t nlist, int32_t row_chunk,
                               int32_t tile_q, Tile* tiles, hipStream_t s);
 hipError_t launch_scan(int dtype, const ScanArgs& a, int32_t grid, hipStream_t s);
+// The updates emit ranks below have[q] (ranks already ordered in P) and
+// list the queries that need more in ext[] (count in rc->n_ext).
 hipError_t launch_update_lookahead(int64_t nq, const int32_t* P, int32_t n, int32_t W,
-                                   int32_t* stop, int32_t* lmax, Item* items, int32_t* cnt,
-                                   RoundCounters* rc, hipStream_t s);
+                                   int32_t* stop, int32_t* lmax, const int32_t* have,
+                                   int32_t* ext, Item* items, int32_t* cnt, RoundCounters* rc,
+                                   hipStream_t s);
 hipError_t launch_update_basic(int64_t nq, const int32_t* P, int32_t n, int32_t W, int32_t* next,
-                               int32_t* stale, int32_t* lmax, Item* items, int32_t* cnt,
-                               RoundCounters* rc, hipStream_t s);
+                               int32_t* stale, int32_t* lmax, const int32_t* have, int32_t* ext,
+                               Item* items, int32_t* cnt, RoundCounters* rc, hipStream_t s);
+// Lazy ranking: copy the listed queries' rows together, copy their new rank
+// rows into P, and emit the items the extension unblocked.
+hipError_t launch_gather_rows(const int32_t* ext, int32_t n_ext, const void* src,
+                              int64_t row_bytes, void* dst, hipStream_t s);
+hipError_t launch_scatter_ranks(const int32_t* ext, int32_t n_ext, const int32_t* Pext,
+                                int32_t n, int32_t* P, hipStream_t s);
+hipError_t launch_emit_pending(const int32_t* ext, int32_t n_ext, int32_t mode, const int32_t* P,
+                               int32_t n, const int32_t* state_a, int32_t* have,
+                               int32_t new_have, Item* items, int32_t* cnt, RoundCounters* rc,
+                               hipStream_t s);
 
 hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
 hipError_t launch_zero_bytes(void* p, int64_t bytes, hipStream_t s);
 hipError_t launch_exclusive_scan(const int32_t* in, int32_t* out, int32_t* out_copy, int64_t n,
                                  int32_t* block_tmp, hipStream_t s);
 size_t exclusive_scan_tmp_elems(int64_t n);
+hipError_t launch_retire_arenas(const ArenaRec* arenas, int32_t n, Hit* pool, int64_t pool_cap,
+                                hipStream_t s);
 hipError_t launch_pool_scatter(const Hit* pool, int64_t n, int32_t* cursor, Hit* sorted,
                                hipStream_t s);
 hipError_t launch_topk(int64_t nq, int32_t k, const Hit* sorted, const int32_t* hoff,

@@ -81,8 +81,22 @@ __global__ void pool_scatter_kernel(const Hit* __restrict__ pool, int64_t n,
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const Hit h = pool[i];
+  if (h.q < 0) return;  // unused arena slot
   const int pos = atomicAdd(&cursor[h.q], 1);
   sorted[pos] = h;
+}
+
+// Sentinels over the unused tail of every block's last arena (one block per
+// arena record).
+__global__ __launch_bounds__(256) void retire_arenas_kernel(const ArenaRec* __restrict__ arenas,
+                                                            Hit* __restrict__ pool,
+                                                            int64_t pool_cap) {
+  const ArenaRec ar = arenas[blockIdx.x];
+  const Hit none = {-INFINITY, -1, -1};
+  for (int i = ar.fill + (int)threadIdx.x; i < ar.size; i += blockDim.x) {
+    const unsigned long long slot = ar.base + (unsigned long long)i;
+    if ((int64_t)slot < pool_cap) pool[slot] = none;
+  }
 }
 
 struct Cand {
@@ -141,7 +155,8 @@ __device__ __forceinline__ Cand wave_merge_desc(Cand v, int lane) {
   return v;
 }
 
-// One wave per query.
+// One wave per query, grid-stride over the queries; each block adds its
+// probe and candidate totals to the round counters once.
 __global__ __launch_bounds__(256) void topk_kernel(int64_t nq, int32_t k,
                                                    const Hit* __restrict__ sorted,
                                                    const int32_t* __restrict__ hoff,
@@ -152,48 +167,49 @@ __global__ __launch_bounds__(256) void topk_kernel(int64_t nq, int32_t k,
                                                    float* __restrict__ out_scores,
                                                    int32_t* __restrict__ out_probes,
                                                    RoundCounters* rc) {
-  const int lane = threadIdx.x & 63;
-  const int64_t q = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  __shared__ int32_t s_probes[4];
-  if (q >= nq) {
-    if (lane == 0) s_probes[threadIdx.x >> 6] = 0;
-    __syncthreads();
-    return;
-  }
-  const int m = hcount[q];
-  const int beg = m > 0 ? hoff[q] : 0;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __shared__ unsigned long long s_probes[4], s_cands[4];
+  unsigned long long probes = 0, cands = 0;
   const Cand none = {-INFINITY, 0x7fffffffffffffffll};
-  Cand top = none;
-  for (int b = 0; b < m; b += 64) {
-    Cand c = none;
-    if (b + lane < m) {
-      const Hit h = sorted[beg + b + lane];
-      c.s = h.score;
-      c.id = h.id;
+  for (int64_t q = (int64_t)blockIdx.x * 4 + wave; q < nq; q += (int64_t)gridDim.x * 4) {
+    const int m = hcount[q];
+    const int beg = m > 0 ? hoff[q] : 0;
+    Cand top = none;
+    for (int b = 0; b < m; b += 64) {
+      Cand c = none;
+      if (b + lane < m) {
+        const Hit h = sorted[beg + b + lane];
+        c.s = h.score;
+        c.id = h.id;
+      }
+      c = wave_sort_desc(c, lane);
+      if (b == 0) {
+        top = c;
+      } else {
+        const Cand r = shfl_cand(c, 63 - lane);  // reversed: top ++ reverse(c) is bitonic
+        top = better(top, r) ? top : r;
+        top = wave_merge_desc(top, lane);
+      }
     }
-    c = wave_sort_desc(c, lane);
-    if (b == 0) {
-      top = c;
-    } else {
-      const Cand r = shfl_cand(c, 63 - lane);  // reversed: top ++ reverse(c) is bitonic
-      top = better(top, r) ? top : r;
-      top = wave_merge_desc(top, lane);
+    if (lane < k) {
+      const bool real = top.id != none.id;
+      out_ids[q * k + lane] = real ? (int64_t)top.id : -1;
+      out_scores[q * k + lane] = real ? top.s : -INFINITY;
     }
-  }
-  if (lane < k) {
-    const bool real = top.id != none.id;
-    out_ids[q * k + lane] = real ? (int64_t)top.id : -1;
-    out_scores[q * k + lane] = real ? top.s : -INFINITY;
+    const int32_t p = probes_src ? probes_src[q] : probes_const;
+    if (lane == 0) out_probes[q] = p;
+    probes += (unsigned long long)p;
+    cands += (unsigned long long)m;
   }
   if (lane == 0) {
-    const int32_t p = probes_src ? probes_src[q] : probes_const;
-    out_probes[q] = p;
-    s_probes[threadIdx.x >> 6] = p;
+    s_probes[wave] = probes;
+    s_cands[wave] = cands;
   }
-  __syncthreads();  // one atomic per block for the probe total
-  if (threadIdx.x == 0)
-    atomicAdd(&rc->probes, (unsigned long long)(s_probes[0] + s_probes[1] + s_probes[2] +
-                                                 s_probes[3]));
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    atomicAdd(&rc->probes, s_probes[0] + s_probes[1] + s_probes[2] + s_probes[3]);
+    atomicAdd(&rc->candidates, s_cands[0] + s_cands[1] + s_cands[2] + s_cands[3]);
+  }
 }
 
 }  // namespace
@@ -214,6 +230,14 @@ hipError_t launch_exclusive_scan(const int32_t* in, int32_t* out, int32_t* out_c
   return hipGetLastError();
 }
 
+hipError_t launch_retire_arenas(const ArenaRec* arenas, int32_t n, Hit* pool, int64_t pool_cap,
+                                hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(retire_arenas_kernel, dim3((unsigned)n), dim3(256), 0, s, arenas, pool,
+                     pool_cap);
+  return hipGetLastError();
+}
+
 hipError_t launch_pool_scatter(const Hit* pool, int64_t n, int32_t* cursor, Hit* sorted,
                                hipStream_t s) {
   if (n <= 0) return hipSuccess;
@@ -227,7 +251,9 @@ hipError_t launch_topk(int64_t nq, int32_t k, const Hit* sorted, const int32_t* 
                        int64_t* out_ids, float* out_scores, int32_t* out_probes,
                        RoundCounters* rc, hipStream_t s) {
   if (nq <= 0) return hipSuccess;
-  hipLaunchKernelGGL(topk_kernel, dim3((unsigned)((nq + 3) / 4)), dim3(256), 0, s, nq, k, sorted,
+  const int64_t want = (nq + 3) / 4;
+  const unsigned blocks = (unsigned)(want < 4096 ? want : 4096);
+  hipLaunchKernelGGL(topk_kernel, dim3(blocks), dim3(256), 0, s, nq, k, sorted,
                      hoff, hcount, probes_src, probes_const, out_ids, out_scores, out_probes, rc);
   return hipGetLastError();
 }

@@ -119,6 +119,37 @@ def test_lookahead_invariance_and_window_sweep(name, W):
     _check(c, s.k, s.tau, W, s.nprobe_max, lookahead=True)
 
 
+@pytest.fixture
+def short_rank_prefix():
+    """Order only max(1, 2W) ranks up front, so that stop lines pass the ordered prefix and
+    the on-demand extension runs."""
+    old = os.environ.get("SIEVE_RANK_PREFIX")
+    os.environ["SIEVE_RANK_PREFIX"] = "1"
+    yield
+    if old is None:
+        del os.environ["SIEVE_RANK_PREFIX"]
+    else:
+        os.environ["SIEVE_RANK_PREFIX"] = old
+
+
+@pytest.mark.parametrize("name", ["tiny", "c1"])
+@pytest.mark.parametrize("W", [1, 2, 4])
+def test_lazy_rank_extension(name, W, short_rank_prefix):
+    # tau = 0.5 makes cluster mates qualify in some queries, so stop lines go deep
+    c = case(name)
+    s = c.w.spec
+    tau = 0.5
+    a = c.gpu(s.k, tau, W, s.nprobe_max, lookahead=True, stats=True)
+    b = c.gpu(s.k, tau, W, s.nprobe_max, lookahead=False, stats=True)
+    # some stop line must have passed the 2W-rank prefix for the test to mean anything
+    assert int(a[2].max()) > 2 * W
+    for x, y in zip(a[:3], b[:3]):
+        assert np.array_equal(x, y)
+    assert a[3].items == b[3].items and a[3].vectors_scanned == b[3].vectors_scanned
+    _check(c, s.k, tau, W, s.nprobe_max, lookahead=True)
+    _check(c, s.k, tau, W, s.nprobe_max, lookahead=False)
+
+
 def test_infinite_window_equals_fixed():
     c = case("c1")
     s = c.w.spec
@@ -207,11 +238,24 @@ def test_empty_lists_and_unbalanced_index():
 
 
 def test_low_threshold_overflows_pool_and_retries():
-    """tau = -1: every scanned row qualifies; the pool overflows and the search re-runs."""
+    """tau = -1: every scanned row qualifies (about 5M candidates for 1,000 queries x 16
+    probes of ~312 rows), more than a fresh index's first candidate pool holds (1M slots
+    plus 4,096 per scan work-group), so the pool grows and the search re-runs."""
+    ps = _lib()
     c = case("c1")
-    g_ids, g_sc, g_pr, st = c.gpu(10, -1.0, 4, 8, queries=c.w.queries[:600], stats=True)
-    assert st.pool_retries >= 1 and st.hits > (1 << 20)
-    o = c.oracle(10, -1.0, 4, 8, nq=600)
+    ix = ps.Index(c.w.vectors, c.w.list_offsets, c.w.ids, c.w.centroids)
+    try:
+        g_ids, g_sc, g_pr, st = (t.cpu().numpy() if hasattr(t, "cpu") else t for t in
+                                 ix.search(c.w.queries, c.w.exclude_ids, 10, -1.0, 4, 16,
+                                           with_stats=True))
+        assert st.pool_retries >= 1 and st.hits > 4_000_000
+        # a second search on the grown pool needs no retry and gives the same result
+        g2 = ix.search(c.w.queries, c.w.exclude_ids, 10, -1.0, 4, 16, with_stats=True)
+        assert g2[3].pool_retries == 0 and g2[3].hits == st.hits
+        assert np.array_equal(g2[0].cpu().numpy(), g_ids)
+    finally:
+        ix.close()
+    o = c.oracle(10, -1.0, 4, 16)
     rep = compare(g_ids, g_sc, g_pr, o)
     print(f"[gpu-test] low tau -> {rep}", flush=True)
     assert_parity(rep)
