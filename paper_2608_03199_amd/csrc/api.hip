@@ -91,7 +91,8 @@ struct sieve_index {
   double cmax = 0.0;
   // workspace, grown on demand
   Buf scores, P, items, bucket, tiles, cnt, item_off, cursor, tile_off, rc, state_a, state_b,
-      lmax, hcount, hoff, hcur, scan_tmp, pool, pool_sorted, arenas, have, ext, qext, Pext;
+      lmax, hcount, hoff, hcur, scan_tmp, pool, pool_sorted, arenas, have, ext, qext, Pext,
+      cand, ccount;
   int64_t pool_cap = 0;
   RoundCounters* rc_host = nullptr;
   // phase timing (only when stats are requested): events are recorded on the
@@ -261,11 +262,37 @@ int grow_workspace(sieve_index* ix, const SearchPlan& pl) {
 }
 
 // Centroid order of queries [q0, q0 + cnt) into P (row-major [cnt][n]).
+// Ranking path: 1 materialised screen scores + selection, 2 fused screen +
+// selection (short prefixes only); SIEVE_RANK_PATH forces one for tests.
+bool use_prefix_path(const sieve_index* ix, int nsel, bool wide) {
+  if (wide || nsel > kRankPrefixMax || nsel > ix->nlist) return false;
+  const int forced = env_int("SIEVE_RANK_PATH", 0);
+  if (forced == 1) return false;
+  if (forced == 2) return true;
+  return ix->nlist > 1024;
+}
+
 // Order the first nsel centroids of queries [q0, q0 + cnt) into rows of P
-// (row stride ldp), in chunks whose screen scores fit the score buffer.
+// (row stride ldp), in chunks whose screen scores (or candidate lists) fit
+// their buffers.
 int rank_queries(sieve_index* ix, const void* queries, int64_t q0, int64_t cnt, int nsel,
                  int64_t ldp, const SearchPlan& pl, int32_t* P, hipStream_t s) {
   RoundCounters* rc = (RoundCounters*)ix->rc.p;
+  if (use_prefix_path(ix, nsel, pl.wide_rank)) {
+    const int64_t cap = rank_prefix_cap(nsel, ix->nlist);
+    const int64_t chunk = cnt < (1 << 18) ? cnt : (1 << 18);
+    int st;
+    if ((st = ensure(ix->cand, (size_t)chunk * cap * sizeof(unsigned long long))) ||
+        (st = ensure(ix->ccount, (size_t)chunk * sizeof(int32_t))))
+      return st;
+    for (int64_t a = 0; a < cnt; a += chunk) {
+      const int32_t c = (int32_t)((cnt - a) < chunk ? (cnt - a) : chunk);
+      HIP_TRY(launch_rank_prefix(ix->dtype, queries, q0 + a, c, ix->centroids, ix->nlist, ix->d,
+                                 nsel, ix->cmax, (unsigned long long*)ix->cand.p,
+                                 (int32_t*)ix->ccount.p, P + a * ldp, ldp, rc, s));
+    }
+    return SIEVE_OK;
+  }
   for (int64_t a = 0; a < cnt; a += pl.rank_chunk) {
     const int32_t c = (int32_t)((cnt - a) < pl.rank_chunk ? (cnt - a) : pl.rank_chunk);
     HIP_TRY(launch_rank_scores(ix->dtype, queries, q0 + a, c, ix->centroids, ix->nlist, ix->d,
@@ -635,7 +662,7 @@ SIEVE_API void sieve_free_index(sieve_index* ix) {
                  &ix->item_off, &ix->cursor, &ix->tile_off, &ix->rc, &ix->state_a,
                  &ix->state_b, &ix->lmax, &ix->hcount, &ix->hoff, &ix->hcur, &ix->scan_tmp,
                  &ix->pool, &ix->pool_sorted, &ix->arenas, &ix->have, &ix->ext, &ix->qext,
-                 &ix->Pext};
+                 &ix->Pext, &ix->cand, &ix->ccount};
   for (Buf* b : bufs)
     if (b->p) (void)hipFree(b->p);
   if (ix->vectors) (void)hipFree(ix->vectors);

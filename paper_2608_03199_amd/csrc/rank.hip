@@ -1,9 +1,6 @@
-// rank.hip -- per-query centroid order P_i (Sec. 4.1), exact in fp64.
-//
-// The MFMA screen (scan.hip) gives fp32 scores s32[c].  For unit-scale data
-// |s32[c] - s64[c]| <= delta, with s64 the fp64 sum of exact products in
-// dimension order and delta = 2 (d + 2) 2^-24 |q| max_c |c| (twice the
-// standard bound on a length-d fp32 accumulation).  Hence:
+// rank.hip -- per-query centroid order P_i (Sec. 4.1), exact in fp64, from
+// materialised fp32 screen scores (scan.hip writes them).  See rank_common.h
+// for the bound delta that makes the order exact.  Steps:
 //   1. the n-th largest fp32 score v is found by an 8-bit radix select;
 //   2. every centroid of the true fp64 top-n has s32 >= v - 2 delta, so the
 //      candidates are all c with s32[c] >= v - 2 delta;
@@ -13,127 +10,10 @@
 //      scores, which are then ordered by (s64 desc, c asc) inside each run;
 //   4. the first n candidates are P_i.
 // The result equals sorting all centroids by (fp64 score desc, index asc).
-#include "sieve_internal.h"
+#include "rank_common.h"
 
 namespace sieve {
 namespace {
-
-__device__ __forceinline__ uint32_t f2key(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-__device__ __forceinline__ float key2f(uint32_t k) {
-  const uint32_t u = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
-  return __uint_as_float(u);
-}
-
-template <int DT>
-__device__ __forceinline__ double load_elem(const void* base, int64_t i) {
-  if constexpr (DT == SIEVE_F32)
-    return (double)((const float*)base)[i];
-  else
-    return (double)((const _Float16*)base)[i];
-}
-
-// fp64 inner product of query row q and centroid row c (global memory) by
-// one wave: lane l sums dimensions l, l+64, ... in order, then the 64
-// partial sums are added as a tree.  Its distance to the dimension-ordered
-// sequential fp64 sum is at most (d + ceil(d/64) + 6) 2^-53 sum_t |q_t c_t|.
-template <int DT>
-__device__ __forceinline__ double wave_dot_fp64(const void* __restrict__ queries, int64_t q,
-                                                const void* __restrict__ centroids, int c, int d) {
-  const int lane = threadIdx.x & 63;
-  double s = 0.0;
-  for (int t0 = 0; t0 < d; t0 += 256) {
-    double qv[4], cv[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int t = t0 + lane + 64 * k;
-      const int tc = t < d ? t : d - 1;  // clamped: the loads issue together
-      qv[k] = load_elem<DT>(queries, q * d + tc);
-      cv[k] = load_elem<DT>(centroids, (int64_t)c * d + tc);
-    }
-#pragma unroll
-    for (int k = 0; k < 4; ++k)
-      if (t0 + lane + 64 * k < d) s += qv[k] * cv[k];
-  }
-  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
-  return s;
-}
-
-// The dimension-ordered sequential fp64 sum (what the order is defined by).
-template <int DT>
-__device__ __noinline__ double seq_dot_fp64(const void* __restrict__ queries, int64_t q,
-                                            const void* __restrict__ centroids, int c, int d) {
-  double s = 0.0;
-  for (int t = 0; t < d; ++t)
-    s += load_elem<DT>(queries, q * d + t) * load_elem<DT>(centroids, (int64_t)c * d + t);
-  return s;
-}
-
-// Order candidates [0, m) already sorted by fp32 screen key: inside each run
-// of near-ties (link[i]: the gap to i+1 is within the screen bound) sort by
-// fp64 score desc, centroid asc.  Tier 1 scores come from wave_dot_fp64;
-// a run whose tier-1 neighbours are within 2 * bound64 is re-scored with the
-// exact sequential sum before its final sort.  NW waves of the calling block
-// (waves w0..w0+NW-1) share the work; the caller synchronises between calls
-// of the three steps.
-template <int DT>
-__device__ __forceinline__ void refine_members(unsigned long long* ck, double* cs,
-                                               const uint8_t* link, int m,
-                                               const void* queries, int64_t qg,
-                                               const void* centroids, int d, int wave, int nwaves) {
-  for (int i = wave; i < m; i += nwaves) {
-    const bool member = link[i] || (i > 0 && link[i - 1]);  // wave-uniform
-    if (member) {
-      const double v = wave_dot_fp64<DT>(queries, qg, centroids, (int)(ck[i] & 0xffffffffu), d);
-      if ((threadIdx.x & 63) == 0) cs[i] = v;
-    }
-  }
-}
-
-__device__ __forceinline__ void sort_run(unsigned long long* ck, double* cs, int i, int e) {
-  for (int x = i + 1; x <= e; ++x) {
-    const unsigned long long kv = ck[x];
-    const double sx = cs[x];
-    const unsigned cx = (unsigned)(kv & 0xffffffffu);
-    int y = x - 1;
-    while (y >= i) {
-      const unsigned cy = (unsigned)(ck[y] & 0xffffffffu);
-      const bool before = (sx > cs[y]) || (sx == cs[y] && cx < cy);
-      if (!before) break;
-      ck[y + 1] = ck[y];
-      cs[y + 1] = cs[y];
-      --y;
-    }
-    ck[y + 1] = kv;
-    cs[y + 1] = sx;
-  }
-}
-
-// One thread per run start: sort by tier-1 score; if two neighbours are
-// within gap64, re-score the whole run exactly and sort again.
-template <int DT>
-__device__ __forceinline__ void order_runs(unsigned long long* ck, double* cs, const uint8_t* link,
-                                           int m, const void* queries, int64_t qg,
-                                           const void* centroids, int d, double gap64, int tid,
-                                           int nthreads) {
-  for (int i = tid; i < m; i += nthreads) {
-    if (link[i] && (i == 0 || !link[i - 1])) {
-      int e = i;
-      while (link[e]) ++e;  // run is [i, e]
-      sort_run(ck, cs, i, e);
-      bool close = false;
-      for (int x = i; x < e; ++x) close |= (cs[x] - cs[x + 1]) <= gap64;
-      if (close) {
-        for (int x = i; x <= e; ++x)
-          cs[x] = seq_dot_fp64<DT>(queries, qg, centroids, (int)(ck[x] & 0xffffffffu), d);
-        sort_run(ck, cs, i, e);
-      }
-    }
-  }
-}
-
 
 // Bytes of the region holding one query's fp32 scores.
 __host__ __device__ inline int keys_bytes(int nlist) { return (nlist * 4 + 15) & ~15; }
@@ -351,19 +231,6 @@ __global__ __launch_bounds__(NT) void rank_select_kernel(
 // Boundary candidates per lane in the wave kernel (capw <= 64 * this).
 constexpr int kKeysPerLane = 8;
 
-// Wave-level fence: orders this wave's LDS writes before its later LDS reads
-// (other lanes read what a lane wrote; no other wave shares the region).
-__device__ __forceinline__ void wave_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-// Bytes of one wave's LDS region in the wave-per-query kernel.
-__host__ __device__ inline int wave_region_bytes(int capw) {
-  return capw * 8 * 2 + capw * 8 + ((capw + 15) & ~15);
-}
-
 // One query per wave, four per block; KPL = keys per lane (nlist <= 64*KPL).
 // 1. the scores of the query are held in registers, KPL per lane;
 // 2. the n-th largest key (the order-preserving integer image of the fp32
@@ -443,37 +310,8 @@ __global__ __launch_bounds__(256) void rank_select_wave_kernel(
   }
   wave_sync();
 
-  // 4a. rank by counting (keys are distinct): position = number of smaller keys
-  for (int i = lane; i < m; i += 64) {
-    const unsigned long long ki = ck[i];
-    int pos = 0;
-#pragma unroll 8
-    for (int j = 0; j < m; ++j) pos += ck[j] < ki ? 1 : 0;
-    out[pos] = ki;
-  }
-  wave_sync();
-  // 4b. runs of near-ties
-  for (int i = lane; i < m; i += 64) {
-    bool l = false;
-    if (i + 1 < m) {
-      const double x = (double)key2f(~(uint32_t)(out[i] >> 32));
-      const double y = (double)key2f(~(uint32_t)(out[i + 1] >> 32));
-      l = (x - y) <= gap;
-    }
-    link[i] = l ? 1 : 0;
-  }
-  wave_sync();
-  // 4c. fp64 scores of run members (this wave alone)
-  refine_members<DT>(out, cs, link, m, queries, qg, centroids, d, 0, 1);
-  wave_sync();
-  // 4d. order inside each run (exact sequential sums where tier 1 is too close)
-  {
-    const double gap64 =
-        2.0 * 2.0 * (double)(d + (d + 63) / 64 + 6) * 1.1102230246251565e-16 * qn * cmax + 1e-300;
-    order_runs<DT>(out, cs, link, m, queries, qg, centroids, d, gap64, lane, 64);
-  }
-  wave_sync();
-  for (int r = lane; r < n; r += 64) P[ql * ldp + r] = (int32_t)(out[r] & 0xffffffffu);
+  finish_candidates_wave<DT>(ck, out, cs, link, m, n, gap, queries, qg, centroids, d, qn, cmax,
+                             P + ql * ldp);
 }
 
 }  // namespace

@@ -1,0 +1,304 @@
+// rank_prefix.hip -- the first R entries of many queries' centroid orders
+// (Sec. 4.1's P_i prefix), exact in fp64, without materialising the query x
+// centroid score matrix.
+//
+// A work-group stages up to 64 queries in LDS and streams every centroid
+// through the MFMA engine of mfma_tile.h twice:
+//   pass 1: each lane keeps, for each of its query rows, the two largest
+//     screen scores of the centroids it sees (64 lanes see disjoint centroid
+//     sets per query).  The R-th largest of these 128 values belongs to R
+//     distinct centroids, so it is at most the R-th largest screen score v;
+//     lo = that value - 2 delta is then a valid lower limit for the
+//     candidates (rank_common.h);
+//   pass 2: recomputes the same scores (same instruction sequence, so the
+//     same bits) and appends every centroid with s32 >= lo to the query's
+//     candidate list in global memory.
+// A second kernel (one wave per query) sorts each list, re-scores near-tie
+// runs in fp64 and writes the first R centroids.  A query with more than
+// `cap` candidates (or fewer than R) sets rank_error: the caller re-ranks
+// from materialised scores with a wide buffer.
+#include "mfma_tile.h"
+#include "rank_common.h"
+
+namespace sieve {
+namespace {
+
+constexpr int kPrefixQB = 4;           // 16-query blocks per work-group, at most
+constexpr int kPrefixRows = 16 * kPrefixQB;
+constexpr int kPrefixKeep = 128;       // values kept per query: 2 x 16 columns x 4 waves
+
+template <int DT, int D, int QB>
+__device__ __forceinline__ void prefix_body(
+    u32x4* lds, const RowGeom<DT>& g, const void* __restrict__ queries, int64_t q0, int qt0,
+    int nq, const void* __restrict__ centroids, int32_t nlist, int d, int32_t R, double cmax,
+    int32_t cap, unsigned long long* __restrict__ cand, float* s_lo, int32_t* s_cnt) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int h = lane >> 4, r16 = lane & 15;
+  const size_t row_bytes = (size_t)d * DTraits<DT>::kElem;
+  const char* qbase = (const char*)queries + (size_t)(q0 + qt0) * row_bytes;
+  auto stage = [&]() {
+    stage_queries<DT>(lds, g, QB * 16, [&](int i) -> const u32x4* {
+      return i < nq ? (const u32x4*)(qbase + (size_t)i * row_bytes) : nullptr;
+    });
+  };
+
+  // pass 1: two largest screen scores per (query row, lane)
+  float m1[QB * 4], m2[QB * 4];
+#pragma unroll
+  for (int x = 0; x < QB * 4; ++x) m1[x] = m2[x] = -INFINITY;
+  auto top2 = [&](const auto& acc, int64_t c, int64_t) {
+    const bool ok = c < nlist;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int x = qb * 4 + r;
+        const float s = ok ? acc[qb][r] : -INFINITY;
+        const float lower = fminf(m1[x], s);
+        m1[x] = fmaxf(m1[x], s);
+        m2[x] = fmaxf(m2[x], lower);
+      }
+    }
+  };
+  stream_rows_qb<DT, D, QB>(lds, g, (const char*)centroids, row_bytes, nullptr, 0, nlist, top2);
+  __syncthreads();  // the staged queries are dead until re-staged below
+
+  float* keep = (float*)lds;  // [QB * 16][kPrefixKeep]
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = qb * 16 + 4 * h + r;
+      float* dst = keep + i * kPrefixKeep + (wave * 16 + r16) * 2;
+      dst[0] = m1[qb * 4 + r];
+      dst[1] = m2[qb * 4 + r];
+    }
+  }
+  __syncthreads();
+
+  // lower limit per query: R-th largest kept value (bitwise search over the
+  // order-preserving keys), less 2 delta, rounded down to fp32
+  for (int i = wave; i < nq; i += 4) {
+    const uint32_t ka = f2key(keep[i * kPrefixKeep + 2 * lane]);
+    const uint32_t kb = f2key(keep[i * kPrefixKeep + 2 * lane + 1]);
+    uint32_t prefix = 0;
+    for (int bit = 31; bit >= 0; --bit) {
+      const uint32_t c = prefix | (1u << bit);
+      const int cnt = __popcll(__ballot(ka >= c)) + __popcll(__ballot(kb >= c));
+      if (cnt >= R) prefix = c;
+    }
+    double ss = 0.0;
+    for (int t = lane; t < d; t += 64) {
+      const double v = load_elem<DT>(queries, (q0 + qt0 + i) * d + t);
+      ss += v * v;
+    }
+    for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+    const double delta =
+        2.0 * (double)(d + 2) * 5.9604644775390625e-08 * sqrt(ss) * cmax + 1e-30;
+    const double lo = (double)key2f(prefix) - 2.0 * delta;
+    float lof = (float)lo;
+    if ((double)lof > lo) lof = nextafterf(lof, -INFINITY);
+    if (lane == 0) s_lo[i] = lof;
+  }
+  __syncthreads();
+  stage();
+  __syncthreads();
+
+  // pass 2: append every centroid at or above the limit
+  float lim[QB * 4];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = qb * 16 + 4 * h + r;
+      lim[qb * 4 + r] = i < nq ? s_lo[i] : INFINITY;
+    }
+  }
+  auto collect = [&](const auto& acc, int64_t c, int64_t) {
+    const bool ok = c < nlist;
+    bool any = false;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) any |= ok && acc[qb][r] >= lim[qb * 4 + r];
+    }
+    if (__ballot(any) == 0) return;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float s = acc[qb][r];
+        if (ok && s >= lim[qb * 4 + r]) {
+          const int i = qb * 16 + 4 * h + r;
+          const int slot = atomicAdd(&s_cnt[i], 1);
+          if (slot < cap)
+            cand[(int64_t)(qt0 + i) * cap + slot] =
+                ((unsigned long long)(~f2key(s)) << 32) | (unsigned)c;
+        }
+      }
+    }
+  };
+  stream_rows_qb<DT, D, QB>(lds, g, (const char*)centroids, row_bytes, nullptr, 0, nlist,
+                            collect);
+}
+
+template <int DT, int D>
+__global__ __launch_bounds__(256, 2) void rank_prefix_kernel(
+    const void* __restrict__ queries, int64_t q0, int32_t nqc, const void* __restrict__ centroids,
+    int32_t nlist, int32_t dd, int32_t R, int32_t rows, double cmax, int32_t cap,
+    unsigned long long* __restrict__ cand, int32_t* __restrict__ ccount) {
+  extern __shared__ u32x4 lds[];
+  __shared__ float s_lo[kPrefixRows];
+  __shared__ int32_t s_cnt[kPrefixRows];
+  const int d = D > 0 ? D : dd;
+  const RowGeom<DT> g = RowGeom<DT>::make(d);
+  const int qt0 = blockIdx.x * rows;
+  const int nq = min(rows, nqc - qt0);
+  const int qb_n = (nq + 15) >> 4;
+  if (threadIdx.x < kPrefixRows) s_cnt[threadIdx.x] = 0;
+  // stage once here; the body re-stages after pass 1
+  const size_t row_bytes = (size_t)d * DTraits<DT>::kElem;
+  const char* qbase = (const char*)queries + (size_t)(q0 + qt0) * row_bytes;
+  stage_queries<DT>(lds, g, qb_n * 16, [&](int i) -> const u32x4* {
+    return i < nq ? (const u32x4*)(qbase + (size_t)i * row_bytes) : nullptr;
+  });
+  __syncthreads();
+  switch (qb_n) {
+    case 1:
+      prefix_body<DT, D, 1>(lds, g, queries, q0, qt0, nq, centroids, nlist, d, R, cmax, cap, cand,
+                            s_lo, s_cnt);
+      break;
+    case 2:
+      prefix_body<DT, D, 2>(lds, g, queries, q0, qt0, nq, centroids, nlist, d, R, cmax, cap, cand,
+                            s_lo, s_cnt);
+      break;
+    case 3:
+      prefix_body<DT, D, 3>(lds, g, queries, q0, qt0, nq, centroids, nlist, d, R, cmax, cap, cand,
+                            s_lo, s_cnt);
+      break;
+    default:
+      prefix_body<DT, D, 4>(lds, g, queries, q0, qt0, nq, centroids, nlist, d, R, cmax, cap, cand,
+                            s_lo, s_cnt);
+      break;
+  }
+  __syncthreads();
+  if ((int)threadIdx.x < nq) ccount[qt0 + threadIdx.x] = s_cnt[threadIdx.x];
+}
+
+// One wave per query: sort the candidate list, order near-tie runs in fp64,
+// write the first R centroids.
+template <int DT>
+__global__ __launch_bounds__(256) void rank_prefix_finish_kernel(
+    const void* __restrict__ queries, int64_t q0, int32_t nqc, const void* __restrict__ centroids,
+    int32_t d, int32_t R, int32_t cap, double cmax,
+    const unsigned long long* __restrict__ cand, const int32_t* __restrict__ ccount,
+    int32_t* __restrict__ P, int64_t ldp, RoundCounters* rc) {
+  extern __shared__ uint8_t smem[];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t ql = (int64_t)blockIdx.x * 4 + wave;
+  if (ql >= nqc) return;  // whole wave; no block barrier follows
+  uint8_t* region = smem + (size_t)wave * wave_region_bytes(cap);
+  unsigned long long* ck = (unsigned long long*)region;  // [cap]
+  unsigned long long* out = ck + cap;                    // [cap]
+  double* cs = (double*)(out + cap);                     // [cap]
+  uint8_t* link = (uint8_t*)(cs + cap);                  // [cap]
+  const int64_t qg = q0 + ql;
+  const int m = ccount[ql];
+  if (m > cap || m < R) {
+    if (lane == 0) atomicExch(&rc->rank_error, 1);
+    for (int r = lane; r < R; r += 64) P[ql * ldp + r] = r;  // valid placeholder
+    return;
+  }
+  for (int i = lane; i < m; i += 64) ck[i] = cand[ql * cap + i];
+  double ss = 0.0;
+  for (int t = lane; t < d; t += 64) {
+    const double v = load_elem<DT>(queries, qg * d + t);
+    ss += v * v;
+  }
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+  const double qn = sqrt(ss);
+  const double delta = 2.0 * (double)(d + 2) * 5.9604644775390625e-08 * qn * cmax + 1e-30;
+  wave_sync();
+  finish_candidates_wave<DT>(ck, out, cs, link, m, R, 2.0 * delta, queries, qg, centroids, d, qn,
+                             cmax, P + ql * ldp);
+}
+
+constexpr int kMaxDynLds = 150 * 1024;
+
+template <int DT>
+int prefix_rows(int d) {
+  const int rb = lds_row_bytes<DT>(d);
+  int qb = (80 * 1024) / (16 * rb);
+  qb = qb < 1 ? 1 : (qb > kPrefixQB ? kPrefixQB : qb);
+  return 16 * qb;
+}
+
+template <int DT, int D>
+hipError_t launch_prefix_t(const void* queries, int64_t q0, int32_t nqc, const void* centroids,
+                           int32_t nlist, int32_t d, int32_t R, double cmax, int32_t cap,
+                           unsigned long long* cand, int32_t* ccount, hipStream_t s) {
+  static const hipError_t attr =
+      hipFuncSetAttribute((const void*)rank_prefix_kernel<DT, D>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, kMaxDynLds);
+  if (attr != hipSuccess) return attr;
+  const int rows = prefix_rows<DT>(d);
+  size_t lds = (size_t)rows * lds_row_bytes<DT>(d);
+  const size_t keep = (size_t)rows * kPrefixKeep * sizeof(float);
+  if (keep > lds) lds = keep;
+  if (lds > (size_t)kMaxDynLds) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((rank_prefix_kernel<DT, D>), dim3((unsigned)((nqc + rows - 1) / rows)),
+                     dim3(256), lds, s, queries, q0, nqc, centroids, nlist, d, R, rows, cmax, cap,
+                     cand, ccount);
+  return hipGetLastError();
+}
+
+template <int DT>
+hipError_t launch_finish_t(const void* queries, int64_t q0, int32_t nqc, const void* centroids,
+                           int32_t d, int32_t R, int32_t cap, double cmax,
+                           const unsigned long long* cand, const int32_t* ccount, int32_t* P,
+                           int64_t ldp, RoundCounters* rc, hipStream_t s) {
+  static const hipError_t attr =
+      hipFuncSetAttribute((const void*)rank_prefix_finish_kernel<DT>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, kMaxDynLds);
+  if (attr != hipSuccess) return attr;
+  const size_t lds = (size_t)4 * wave_region_bytes(cap);
+  if (lds > (size_t)kMaxDynLds) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((rank_prefix_finish_kernel<DT>), dim3((unsigned)((nqc + 3) / 4)), dim3(256),
+                     lds, s, queries, q0, nqc, centroids, d, R, cap, cmax, cand, ccount, P, ldp,
+                     rc);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int rank_prefix_cap(int32_t R, int32_t nlist) {
+  const int cap = R + 128;
+  return cap < nlist ? cap : nlist;
+}
+
+hipError_t launch_rank_prefix(int dtype, const void* queries, int64_t q0, int32_t nqc,
+                              const void* centroids, int32_t nlist, int32_t d, int32_t R,
+                              double cmax, unsigned long long* cand, int32_t* ccount, int32_t* P,
+                              int64_t ldp, RoundCounters* rc, hipStream_t s) {
+  if (nqc <= 0) return hipSuccess;
+  if (R < 1 || R > kRankPrefixMax || R > nlist) return hipErrorInvalidValue;
+  const int cap = rank_prefix_cap(R, nlist);
+  hipError_t e;
+#define SIEVE_PREFIX(DT, D)                                                                  \
+  launch_prefix_t<DT, D>(queries, q0, nqc, centroids, nlist, d, R, cmax, cap, cand, ccount, s)
+  if (dtype == SIEVE_F32) {
+    e = d == 64 ? SIEVE_PREFIX(SIEVE_F32, 64)
+                : d == 128 ? SIEVE_PREFIX(SIEVE_F32, 128) : SIEVE_PREFIX(SIEVE_F32, 0);
+  } else {
+    e = d == 128 ? SIEVE_PREFIX(SIEVE_F16, 128) : SIEVE_PREFIX(SIEVE_F16, 0);
+  }
+#undef SIEVE_PREFIX
+  if (e != hipSuccess) return e;
+  return dtype == SIEVE_F32
+             ? launch_finish_t<SIEVE_F32>(queries, q0, nqc, centroids, d, R, cap, cmax, cand,
+                                          ccount, P, ldp, rc, s)
+             : launch_finish_t<SIEVE_F16>(queries, q0, nqc, centroids, d, R, cap, cmax, cand,
+                                          ccount, P, ldp, rc, s);
+}
+
+}  // namespace sieve

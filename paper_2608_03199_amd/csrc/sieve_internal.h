@@ -99,6 +99,15 @@ hipError_t launch_rank_scores(int dtype, const void* queries, int64_t q0, int32_
                               const void* centroids, int32_t nlist, int32_t d, float* scores,
                               hipStream_t s);
 size_t scan_lds_bytes(int dtype, int d, int rows);
+// Fused screen + selection of the first R (<= kRankPrefixMax) ranks of
+// queries [q0, q0 + nqc) into P (row stride ldp); cand holds
+// nqc * rank_prefix_cap(R, nlist) keys and ccount nqc counts.
+constexpr int kRankPrefixMax = 64;
+int rank_prefix_cap(int32_t R, int32_t nlist);
+hipError_t launch_rank_prefix(int dtype, const void* queries, int64_t q0, int32_t nqc,
+                              const void* centroids, int32_t nlist, int32_t d, int32_t R,
+                              double cmax, unsigned long long* cand, int32_t* ccount, int32_t* P,
+                              int64_t ldp, RoundCounters* rc, hipStream_t s);
 hipError_t launch_rank_select(int dtype, const void* queries, int64_t q0, int32_t nqc,
                               const void* centroids, int32_t nlist, int32_t d, const float* scores,
                               int32_t n, double cmax, int32_t* P, int64_t ldp, RoundCounters* rc,

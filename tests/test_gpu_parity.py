@@ -119,6 +119,19 @@ def test_lookahead_invariance_and_window_sweep(name, W):
     _check(c, s.k, s.tau, W, s.nprobe_max, lookahead=True)
 
 
+@pytest.fixture(params=["materialised", "fused"])
+def rank_path(request):
+    """Run a test under each ranking path: materialised screen scores + selection, and the
+    fused screen + selection that short prefixes use on large centroid sets (forced here)."""
+    old = os.environ.get("SIEVE_RANK_PATH")
+    os.environ["SIEVE_RANK_PATH"] = "1" if request.param == "materialised" else "2"
+    yield request.param
+    if old is None:
+        del os.environ["SIEVE_RANK_PATH"]
+    else:
+        os.environ["SIEVE_RANK_PATH"] = old
+
+
 @pytest.fixture
 def short_rank_prefix():
     """Order only max(1, 2W) ranks up front, so that stop lines pass the ordered prefix and
@@ -134,7 +147,7 @@ def short_rank_prefix():
 
 @pytest.mark.parametrize("name", ["tiny", "c1"])
 @pytest.mark.parametrize("W", [1, 2, 4])
-def test_lazy_rank_extension(name, W, short_rank_prefix):
+def test_lazy_rank_extension(name, W, short_rank_prefix, rank_path):
     # tau = 0.5 makes cluster mates qualify in some queries, so stop lines go deep
     c = case(name)
     s = c.w.spec
@@ -286,7 +299,28 @@ def test_rank_order_matches_oracle_exactly(name):
     assert np.array_equal(P, o.order)
 
 
-def test_rank_with_many_exact_ties_takes_the_wide_path():
+@pytest.mark.parametrize("name", ["tiny", "tiny16", "c1"])
+def test_rank_prefix_matches_oracle_exactly(name, rank_path):
+    """Short prefixes of the probe order (the lazily ranked part) equal the oracle's."""
+    c = case(name)
+    nl = c.w.spec.nlist
+    h = c.h
+    o = oracle.search(h["vectors"], h["list_offsets"], h["ids"], h["centroids"], h["queries"],
+                      h["exclude_ids"], 1, 2.0, 1, nl, want_order=True, nthreads=NTHREADS)
+    for R in sorted({1, 8, min(nl, 32), min(nl, 64)}):
+        P = c.ix.rank(c.w.queries, R).cpu().numpy()
+        assert np.array_equal(P, o.order[:, :R]), R
+
+
+@pytest.mark.parametrize("name", ["tiny", "tiny16", "c1"])
+@pytest.mark.parametrize("lookahead", [True, False])
+def test_sieve_matches_oracle_on_each_rank_path(name, lookahead, rank_path):
+    c = case(name)
+    s = c.w.spec
+    _check(c, s.k, s.tau, s.W, s.nprobe_max, lookahead)
+
+
+def test_rank_with_many_exact_ties_takes_the_wide_path(rank_path):
     """800 identical centroids tie at the top: the one-wave selection runs out of
     boundary room, the search re-ranks with the wide kernel, and the order is
     still the oracle's (ties to the lower centroid index)."""
