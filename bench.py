@@ -29,6 +29,8 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"f32": 157.3, "f16": 2500.0}
 PMC_FILE = os.path.join(ROOT, "profiles", "scan_traffic_pmc.json")
+# oracle sample per workload: roughly 10-30 s of single-thread fp64 work
+ORACLE_SAMPLE = {"tiny": 150, "tiny16": 150, "c1": 1000, "c2": 10000, "c3": 200, "c5": 300}
 SCAN_SOURCES = ["paper_2608_03199_amd/csrc/scan.hip", "paper_2608_03199_amd/csrc/mfma_tile.h"]
 
 
@@ -70,8 +72,9 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="c2")
-    ap.add_argument("--oracle-queries", type=int, default=10000,
-                    help="queries in the single-thread oracle sample")
+    ap.add_argument("--oracle-queries", type=int, default=None,
+                    help="queries in the single-thread oracle sample (default: about 10-30 s "
+                         "of oracle work for the workload)")
     ap.add_argument("--no-oracle", action="store_true")
     ap.add_argument("--skip-fixed", action="store_true",
                     help="do not time the fixed-probe baseline (profiling runs)")
@@ -212,7 +215,7 @@ def main():
         sys.path.insert(0, os.path.join(ROOT, "tests"))
         from parity import compare
         h = w.numpy()
-        m = min(args.oracle_queries, nq)
+        m = min(args.oracle_queries or ORACLE_SAMPLE.get(args.config, 1000), nq)
         rng = np.random.default_rng(spec.seed + 77)
         sel = np.sort(rng.choice(nq, m, replace=False))
         log(f"[bench] oracle on {m} queries, 1 thread")

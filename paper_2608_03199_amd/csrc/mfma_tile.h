@@ -178,6 +178,104 @@ __device__ __forceinline__ void score_stream(const u32x4* __restrict__ lds, cons
   }
 }
 
+// Rows longer than kSliceChunks MFMA chunks stream in slices of that many
+// chunks, one slice ahead: two slices occupy registers instead of two rows,
+// and each wave still keeps a slice of loads in flight under its MFMAs.
+constexpr int kSliceChunks = 8;
+
+// Multiply slice s (chunks [s*kSliceChunks, ...)) of a row block, whose
+// fragments are in b[], into acc; the query fragments of the next chunk are
+// read from LDS while the current chunk's MFMAs issue.
+template <int DT, int D, int QB>
+__device__ __forceinline__ void mma_slice(const u32x4* __restrict__ arow, int segs, int s,
+                                          const u32x4 (&b)[kSliceChunks], f32x4 (&acc)[QB]) {
+  constexpr int kNC = D / DTraits<DT>::kChunkDims;
+  const int c0 = s * kSliceChunks;
+  u32x4 a0[QB], a1[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) a0[qb] = arow[qb * 16 * segs + 4 * c0];
+#pragma unroll
+  for (int c = 0; c < kSliceChunks; ++c) {
+    if (c0 + c < kNC) {
+      u32x4(&cur)[QB] = (c & 1) ? a1 : a0;
+      u32x4(&nxt)[QB] = (c & 1) ? a0 : a1;
+      if (c + 1 < kSliceChunks && c0 + c + 1 < kNC) {
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) nxt[qb] = arow[qb * 16 * segs + 4 * (c0 + c + 1)];
+      }
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) acc[qb] = mma_chunk<DT>(cur[qb], b[c], acc[qb]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+}
+
+// Sliced variant of stream_rows_qb (see there) for kNC > kSliceChunks.  Two
+// row blocks (rb and rb + W) are processed per iteration so that the slice
+// buffers alternate at compile-time indices; chunks are accumulated in the
+// same order as in the unsliced variant, so scores are bit-identical.
+template <int DT, int D, int QB, typename Epi>
+__device__ __forceinline__ void stream_rows_sliced(const u32x4* __restrict__ lds,
+                                                   const RowGeom<DT>& g,
+                                                   const char* __restrict__ base,
+                                                   size_t row_bytes,
+                                                   const int64_t* __restrict__ ids, int64_t r0,
+                                                   int64_t r1, Epi& epi) {
+  constexpr int kNC = D / DTraits<DT>::kChunkDims;
+  constexpr int kNS = (kNC + kSliceChunks - 1) / kSliceChunks;  // slices per row block
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nwaves = blockDim.x >> 6;
+  const int h = lane >> 4, r16 = lane & 15;
+  const int64_t nrows = r1 - r0;
+  const u32x4* arow = lds + r16 * g.segs + h;
+  auto rowc_of = [&](int64_t blk) {
+    const int64_t row = r0 + blk * 16 + r16;
+    return row < r1 ? row : r1 - 1;  // clamped: loads stay unconditional
+  };
+  auto load = [&](int64_t rowc, int s, u32x4(&dst)[kSliceChunks]) {
+    const u32x4* vrow = (const u32x4*)(base + (size_t)rowc * row_bytes) + h;
+#pragma unroll
+    for (int c = 0; c < kSliceChunks; ++c)
+      if (s * kSliceChunks + c < kNC) dst[c] = vrow[4 * (s * kSliceChunks + c)];
+  };
+  int64_t rb = wave;
+  if (rb * 16 >= nrows) return;
+  u32x4 bufA[kSliceChunks], bufB[kSliceChunks];
+  load(rowc_of(rb), 0, bufA);
+  for (;;) {
+    const int64_t rb2 = rb + nwaves, rb3 = rb2 + nwaves;
+    const bool has2 = rb2 * 16 < nrows, has3 = rb3 * 16 < nrows;
+    const int64_t rc1 = rowc_of(rb), rc2 = rowc_of(rb2), rc3 = rowc_of(rb3);
+    const int64_t id1 = ids ? ids[rc1] : 0;
+    const int64_t id2 = ids ? ids[rc2] : 0;
+    f32x4 acc[QB];
+#pragma unroll
+    for (int gs = 0; gs < 2 * kNS; ++gs) {
+      const int s = gs % kNS;
+      const bool second = gs >= kNS;
+      if (second && !has2) break;
+      if (s == 0) {
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) acc[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+      // issue the next slice's loads before this slice's MFMAs
+      const int ng = gs + 1;
+      if (ng < 2 * kNS) {
+        if (ng < kNS)
+          load(rc1, ng % kNS, (ng & 1) ? bufB : bufA);
+        else if (has2)
+          load(rc2, ng % kNS, (ng & 1) ? bufB : bufA);
+      } else if (has3) {
+        load(rc3, 0, bufA);  // 2 * kNS is even: the next pair starts in bufA
+      }
+      mma_slice<DT, D, QB>(arow, g.segs, s, (gs & 1) ? bufB : bufA, acc);
+      if (s == kNS - 1) epi(acc, r0 + (second ? rb2 : rb) * 16 + r16, second ? id2 : id1);
+    }
+    if (!has3) break;
+    rb = rb3;
+  }
+}
+
 // Stream rows [r0, r1) of a row-major store through the waves of the block:
 // wave w scores row blocks w, w + W, w + 2W, ... (W = waves per block)
 // against QB staged query blocks and hands each finished block to
@@ -197,7 +295,9 @@ __device__ __forceinline__ void stream_rows_qb(const u32x4* __restrict__ lds,
   const int h = lane >> 4, r16 = lane & 15;
   const int64_t nrows = r1 - r0;
   constexpr int kNC = D / DTraits<DT>::kChunkDims;
-  if constexpr (kNC > 0) {
+  if constexpr (kNC > kSliceChunks) {
+    stream_rows_sliced<DT, D, QB>(lds, g, base, row_bytes, ids, r0, r1, epi);
+  } else if constexpr (kNC > 0) {
     auto load = [&](int64_t blk, u32x4(&dst)[kNC], int64_t& rid) {
       const int64_t row = r0 + blk * 16 + r16;
       const int64_t rowc = row < r1 ? row : r1 - 1;
@@ -240,22 +340,41 @@ __device__ __forceinline__ void stream_rows_qb(const u32x4* __restrict__ lds,
   }
 }
 
+// Largest number of 16-query blocks a tile of compile-time dimension D can
+// stage (the 80 KB LDS budget that keeps two work-groups per CU; the host's
+// tile size follows the same rule).  D = 0: runtime dimension, up to 8.
+template <int DT, int D>
+constexpr int qb_cap() {
+  if (D == 0) return 8;
+  const int segs = 4 * ((D + DTraits<DT>::kChunkDims - 1) / DTraits<DT>::kChunkDims) + 1;
+  const int qb = (80 * 1024) / (16 * segs * 16);
+  return qb < 1 ? 1 : (qb > 8 ? 8 : qb);
+}
+
+template <int DT, int D, int QB, typename Epi>
+__device__ __forceinline__ void stream_rows_from(const u32x4* __restrict__ lds,
+                                                 const RowGeom<DT>& g,
+                                                 const char* __restrict__ base, size_t row_bytes,
+                                                 const int64_t* __restrict__ ids, int64_t r0,
+                                                 int64_t r1, int qb_n, Epi& epi) {
+  constexpr int kMax = qb_cap<DT, D>();
+  if constexpr (QB >= kMax) {
+    stream_rows_qb<DT, D, kMax>(lds, g, base, row_bytes, ids, r0, r1, epi);
+  } else {
+    if (qb_n <= QB)
+      stream_rows_qb<DT, D, QB>(lds, g, base, row_bytes, ids, r0, r1, epi);
+    else
+      stream_rows_from<DT, D, QB + 1>(lds, g, base, row_bytes, ids, r0, r1, qb_n, epi);
+  }
+}
+
 // Dispatch on the tile's number of 16-query blocks (uniform per tile).
 template <int DT, int D, typename Epi>
 __device__ __forceinline__ void stream_rows(const u32x4* __restrict__ lds, const RowGeom<DT>& g,
                                             const char* __restrict__ base, size_t row_bytes,
                                             const int64_t* __restrict__ ids, int64_t r0,
                                             int64_t r1, int qb_n, Epi&& epi) {
-  switch (qb_n) {
-    case 1: stream_rows_qb<DT, D, 1>(lds, g, base, row_bytes, ids, r0, r1, epi); break;
-    case 2: stream_rows_qb<DT, D, 2>(lds, g, base, row_bytes, ids, r0, r1, epi); break;
-    case 3: stream_rows_qb<DT, D, 3>(lds, g, base, row_bytes, ids, r0, r1, epi); break;
-    case 4: stream_rows_qb<DT, D, 4>(lds, g, base, row_bytes, ids, r0, r1, epi); break;
-    case 5: stream_rows_qb<DT, D, 5>(lds, g, base, row_bytes, ids, r0, r1, epi); break;
-    case 6: stream_rows_qb<DT, D, 6>(lds, g, base, row_bytes, ids, r0, r1, epi); break;
-    case 7: stream_rows_qb<DT, D, 7>(lds, g, base, row_bytes, ids, r0, r1, epi); break;
-    default: stream_rows_qb<DT, D, 8>(lds, g, base, row_bytes, ids, r0, r1, epi); break;
-  }
+  stream_rows_from<DT, D, 1>(lds, g, base, row_bytes, ids, r0, r1, qb_n, epi);
 }
 
 }  // namespace sieve

@@ -163,24 +163,18 @@ __global__ __launch_bounds__(256, 2) void rank_prefix_kernel(
     return i < nq ? (const u32x4*)(qbase + (size_t)i * row_bytes) : nullptr;
   });
   __syncthreads();
+  // the host sizes rows by the same LDS rule, so qb_n <= kQBMax
+  constexpr int kQBMax = qb_cap<DT, D>() < kPrefixQB ? qb_cap<DT, D>() : kPrefixQB;
+#define SIEVE_BODY(QB)                                                                        \
+  prefix_body<DT, D, QB>(lds, g, queries, q0, qt0, nq, centroids, nlist, d, R, cmax, cap, cand, \
+                         s_lo, s_cnt)
   switch (qb_n) {
-    case 1:
-      prefix_body<DT, D, 1>(lds, g, queries, q0, qt0, nq, centroids, nlist, d, R, cmax, cap, cand,
-                            s_lo, s_cnt);
-      break;
-    case 2:
-      prefix_body<DT, D, 2>(lds, g, queries, q0, qt0, nq, centroids, nlist, d, R, cmax, cap, cand,
-                            s_lo, s_cnt);
-      break;
-    case 3:
-      prefix_body<DT, D, 3>(lds, g, queries, q0, qt0, nq, centroids, nlist, d, R, cmax, cap, cand,
-                            s_lo, s_cnt);
-      break;
-    default:
-      prefix_body<DT, D, 4>(lds, g, queries, q0, qt0, nq, centroids, nlist, d, R, cmax, cap, cand,
-                            s_lo, s_cnt);
-      break;
+    case 1: SIEVE_BODY(1); break;
+    case 2: if constexpr (kQBMax >= 2) SIEVE_BODY(2); break;
+    case 3: if constexpr (kQBMax >= 3) SIEVE_BODY(3); break;
+    default: if constexpr (kQBMax >= 4) SIEVE_BODY(4); break;
   }
+#undef SIEVE_BODY
   __syncthreads();
   if ((int)threadIdx.x < nq) ccount[qt0 + threadIdx.x] = s_cnt[threadIdx.x];
 }
@@ -290,7 +284,9 @@ hipError_t launch_rank_prefix(int dtype, const void* queries, int64_t q0, int32_
     e = d == 64 ? SIEVE_PREFIX(SIEVE_F32, 64)
                 : d == 128 ? SIEVE_PREFIX(SIEVE_F32, 128) : SIEVE_PREFIX(SIEVE_F32, 0);
   } else {
-    e = d == 128 ? SIEVE_PREFIX(SIEVE_F16, 128) : SIEVE_PREFIX(SIEVE_F16, 0);
+    e = d == 128   ? SIEVE_PREFIX(SIEVE_F16, 128)
+        : d == 768 ? SIEVE_PREFIX(SIEVE_F16, 768)
+                   : SIEVE_PREFIX(SIEVE_F16, 0);
   }
 #undef SIEVE_PREFIX
   if (e != hipSuccess) return e;

@@ -335,6 +335,7 @@ hipError_t launch_scan(int dtype, const ScanArgs& a, int32_t grid, hipStream_t s
   }
   switch (a.d) {
     case 128: return launch_scan_t<SIEVE_F16, 128>(a, grid, s);
+    case 768: return launch_scan_t<SIEVE_F16, 768>(a, grid, s);
     default: return launch_scan_t<SIEVE_F16, 0>(a, grid, s);
   }
 }

@@ -211,9 +211,11 @@ def test_empty_query_batch():
 
 
 @pytest.mark.parametrize("d,dtype", [(40, torch.float32), (72, torch.float16),
-                                     (96, torch.float32), (256, torch.float16)])
-def test_uncommon_dimensions(d, dtype):
-    """Dimensions off the compiled fast paths, including partial MFMA chunks."""
+                                     (96, torch.float32), (256, torch.float16),
+                                     (768, torch.float16)])
+def test_uncommon_dimensions(d, dtype, rank_path):
+    """Dimensions off the compiled fast paths, including partial MFMA chunks, and d = 768
+    fp16 (rows streamed in slices of 8 MFMA chunks)."""
     spec = sw.SPECS["tiny"]
     import dataclasses
     sp = dataclasses.replace(spec, name=f"d{d}", d=d, dtype="f16" if dtype == torch.float16
