@@ -151,6 +151,40 @@ __device__ __forceinline__ void score_regs(const u32x4* __restrict__ lds, int se
   }
 }
 
+// Two row blocks against the same staged queries: every query fragment read
+// from LDS feeds two MFMAs, which halves the LDS traffic per flop (the limit
+// of the fp16 path with many query blocks).  Same chunk order per output as
+// score_regs, so the same bits.
+template <int DT, int D, int QB>
+__device__ __forceinline__ void score_regs2(const u32x4* __restrict__ lds, int segs,
+                                            const u32x4 (&b0)[D / DTraits<DT>::kChunkDims],
+                                            const u32x4 (&b1)[D / DTraits<DT>::kChunkDims],
+                                            f32x4 (&acc0)[QB], f32x4 (&acc1)[QB]) {
+  constexpr int kNC = D / DTraits<DT>::kChunkDims;
+  constexpr int kN = kNC * QB;  // (chunk, query block) steps, chunk-major
+  constexpr int kAhead = 3;     // query fragments in flight from LDS
+  const int lane = threadIdx.x & 63;
+  const int h = lane >> 4, r16 = lane & 15;
+  const u32x4* arow = lds + r16 * segs + h;
+  auto frag = [&](int t) { return arow[(t % QB) * 16 * segs + 4 * (t / QB)]; };
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    acc0[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    acc1[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  u32x4 a[kAhead + 1];
+#pragma unroll
+  for (int t = 0; t < kAhead && t < kN; ++t) a[t] = frag(t);
+#pragma unroll
+  for (int t = 0; t < kN; ++t) {
+    if (t + kAhead < kN) a[(t + kAhead) % (kAhead + 1)] = frag(t + kAhead);
+    const int qb = t % QB, c = t / QB;
+    acc0[qb] = mma_chunk<DT>(a[t % (kAhead + 1)], b0[c], acc0[qb]);
+    acc1[qb] = mma_chunk<DT>(a[t % (kAhead + 1)], b1[c], acc1[qb]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
 // Runtime-dimension variant: fragments are loaded chunk by chunk (one ahead).
 template <int DT, int QB>
 __device__ __forceinline__ void score_stream(const u32x4* __restrict__ lds, const RowGeom<DT>& g,
@@ -210,11 +244,36 @@ __device__ __forceinline__ void mma_slice(const u32x4* __restrict__ arow, int se
   }
 }
 
-// Sliced variant of stream_rows_qb (see there) for kNC > kSliceChunks.  Two
-// row blocks (rb and rb + W) are processed per iteration so that the slice
-// buffers alternate at compile-time indices; chunks are accumulated in the
-// same order as in the unsliced variant, so scores are bit-identical.
-template <int DT, int D, int QB, typename Epi>
+// Fragment buffers in flight per wave: a wave keeps (buffers - 1) row blocks
+// (or slices) loading while it multiplies one, so that its loads cover the
+// memory latency.  Tiles with few query blocks have few MFMAs per row and
+// spare registers, so they buffer deeper.
+// Reserve: VGPRs the caller's epilogue keeps live across the stream.
+template <int DT, int D, int QB, int Reserve>
+constexpr int ring_depth() {
+  constexpr int kNC = D / DTraits<DT>::kChunkDims;
+  if (kNC > kSliceChunks) return Reserve > 0 ? 2 : 3;  // slices of kSliceChunks chunks
+  const int per = 4 * kNC;                             // VGPRs per buffered row block
+  const int budget = (QB <= 2 ? 96 : (QB <= 4 ? 64 : 40)) - Reserve;
+  const int nb = budget / per;
+  return nb < 2 ? 2 : (nb > 6 ? 6 : nb);
+}
+
+// Pairs of row blocks (score_regs2) where the LDS reads of query fragments
+// would bound the MFMA rate: fp16 rows of at most 8 chunks, 3+ query blocks.
+template <int DT, int D, int QB>
+constexpr bool pair_mode() {
+  constexpr int kNC = D / DTraits<DT>::kChunkDims;
+  return DT == SIEVE_F16 && kNC > 0 && kNC <= kSliceChunks && QB >= 3;
+}
+
+// Sliced variant of stream_rows_qb (see there) for kNC > kSliceChunks.  The
+// wave's row blocks form a stream of slices (block k, slice s); slice t loads
+// into buffer t % NB while slice t - NB + 1 is multiplied.  NB row blocks are
+// unrolled per iteration so that buffer indices are compile-time constants.
+// Chunks are accumulated in the same order as in the unsliced variant, so
+// scores are bit-identical.
+template <int DT, int D, int QB, int Reserve, bool kIds, typename Epi>
 __device__ __forceinline__ void stream_rows_sliced(const u32x4* __restrict__ lds,
                                                    const RowGeom<DT>& g,
                                                    const char* __restrict__ base,
@@ -223,6 +282,7 @@ __device__ __forceinline__ void stream_rows_sliced(const u32x4* __restrict__ lds
                                                    int64_t r1, Epi& epi) {
   constexpr int kNC = D / DTraits<DT>::kChunkDims;
   constexpr int kNS = (kNC + kSliceChunks - 1) / kSliceChunks;  // slices per row block
+  constexpr int NB = ring_depth<DT, D, QB, Reserve>();
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nwaves = blockDim.x >> 6;
   const int h = lane >> 4, r16 = lane & 15;
@@ -232,47 +292,42 @@ __device__ __forceinline__ void stream_rows_sliced(const u32x4* __restrict__ lds
     const int64_t row = r0 + blk * 16 + r16;
     return row < r1 ? row : r1 - 1;  // clamped: loads stay unconditional
   };
-  auto load = [&](int64_t rowc, int s, u32x4(&dst)[kSliceChunks]) {
-    const u32x4* vrow = (const u32x4*)(base + (size_t)rowc * row_bytes) + h;
+  auto load = [&](int64_t blk, int s, u32x4(&dst)[kSliceChunks]) {
+    const u32x4* vrow = (const u32x4*)(base + (size_t)rowc_of(blk) * row_bytes) + h;
 #pragma unroll
     for (int c = 0; c < kSliceChunks; ++c)
       if (s * kSliceChunks + c < kNC) dst[c] = vrow[4 * (s * kSliceChunks + c)];
   };
+  u32x4 buf[NB][kSliceChunks];
   int64_t rb = wave;
-  if (rb * 16 >= nrows) return;
-  u32x4 bufA[kSliceChunks], bufB[kSliceChunks];
-  load(rowc_of(rb), 0, bufA);
-  for (;;) {
-    const int64_t rb2 = rb + nwaves, rb3 = rb2 + nwaves;
-    const bool has2 = rb2 * 16 < nrows, has3 = rb3 * 16 < nrows;
-    const int64_t rc1 = rowc_of(rb), rc2 = rowc_of(rb2), rc3 = rowc_of(rb3);
-    const int64_t id1 = ids ? ids[rc1] : 0;
-    const int64_t id2 = ids ? ids[rc2] : 0;
-    f32x4 acc[QB];
+  if (nrows <= 0) return;
+  // Prefetches are issued unconditionally (past the end they re-read the
+  // clamped last row): the load sequence then never depends on control
+  // flow, and the compiler's wait counts stay exact.
 #pragma unroll
-    for (int gs = 0; gs < 2 * kNS; ++gs) {
-      const int s = gs % kNS;
-      const bool second = gs >= kNS;
-      if (second && !has2) break;
+  for (int u = 0; u < NB - 1; ++u) load(rb + (u / kNS) * nwaves, u % kNS, buf[u]);
+  f32x4 acc[QB];
+  int64_t rid = 0;
+  for (;;) {
+#pragma unroll
+    for (int u = 0; u < NB * kNS; ++u) {
+      const int s = u % kNS;
+      const int64_t blk = rb + (u / kNS) * nwaves;
+      if (blk * 16 >= nrows) return;
       if (s == 0) {
+        if constexpr (kIds) rid = ids[rowc_of(blk)];
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) acc[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
       }
-      // issue the next slice's loads before this slice's MFMAs
-      const int ng = gs + 1;
-      if (ng < 2 * kNS) {
-        if (ng < kNS)
-          load(rc1, ng % kNS, (ng & 1) ? bufB : bufA);
-        else if (has2)
-          load(rc2, ng % kNS, (ng & 1) ? bufB : bufA);
-      } else if (has3) {
-        load(rc3, 0, bufA);  // 2 * kNS is even: the next pair starts in bufA
-      }
-      mma_slice<DT, D, QB>(arow, g.segs, s, (gs & 1) ? bufB : bufA, acc);
-      if (s == kNS - 1) epi(acc, r0 + (second ? rb2 : rb) * 16 + r16, second ? id2 : id1);
+      const int un = u + NB - 1;  // issue the slice NB - 1 ahead before these MFMAs
+      load(rb + (un / kNS) * nwaves, un % kNS, buf[un % NB]);
+      // keep the prefetch above the MFMAs (the scheduler would otherwise sink
+      // loads towards their use to save registers, serialising the stream)
+      __builtin_amdgcn_sched_barrier(0);
+      mma_slice<DT, D, QB>(arow, g.segs, s, buf[u % NB], acc);
+      if (s == kNS - 1) epi(acc, r0 + blk * 16 + r16, rid);
     }
-    if (!has3) break;
-    rb = rb3;
+    rb += NB * nwaves;
   }
 }
 
@@ -284,7 +339,7 @@ __device__ __forceinline__ void stream_rows_sliced(const u32x4* __restrict__ lds
 // rid = ids[row] when an id array is given (else 0).  With a compile-time
 // dimension, two fragment buffers alternate so that the next block's
 // fragments (and ids) load while the current block is multiplied.
-template <int DT, int D, int QB, typename Epi>
+template <int DT, int D, int QB, typename Epi, int Reserve = 0, bool kIds = true>
 __device__ __forceinline__ void stream_rows_qb(const u32x4* __restrict__ lds,
                                                const RowGeom<DT>& g,
                                                const char* __restrict__ base, size_t row_bytes,
@@ -296,43 +351,90 @@ __device__ __forceinline__ void stream_rows_qb(const u32x4* __restrict__ lds,
   const int64_t nrows = r1 - r0;
   constexpr int kNC = D / DTraits<DT>::kChunkDims;
   if constexpr (kNC > kSliceChunks) {
-    stream_rows_sliced<DT, D, QB>(lds, g, base, row_bytes, ids, r0, r1, epi);
-  } else if constexpr (kNC > 0) {
+    stream_rows_sliced<DT, D, QB, Reserve, kIds>(lds, g, base, row_bytes, ids, r0, r1, epi);
+  } else if constexpr (pair_mode<DT, D, QB>()) {
+    // super-block sb = row blocks 2 sb and 2 sb + 1; super-block sb + W loads
+    // while sb is multiplied
     auto load = [&](int64_t blk, u32x4(&dst)[kNC], int64_t& rid) {
       const int64_t row = r0 + blk * 16 + r16;
       const int64_t rowc = row < r1 ? row : r1 - 1;
       const u32x4* vrow = (const u32x4*)(base + (size_t)rowc * row_bytes) + h;
 #pragma unroll
       for (int c = 0; c < kNC; ++c) dst[c] = vrow[4 * c];
-      rid = ids ? ids[rowc] : 0;
+      if constexpr (kIds) rid = ids[rowc];
     };
-    u32x4 b0[kNC], b1[kNC];
-    int64_t id0 = 0, id1 = 0;
+    u32x4 p0[kNC], p1[kNC], q0[kNC], q1[kNC];
+    int64_t ip0 = 0, ip1 = 0, iq0 = 0, iq1 = 0;
+    int64_t sb = wave;
+    if (nrows <= 0) return;
+    // unconditional prefetches (clamped rows past the end): a fixed load
+    // sequence keeps the compiler's wait counts exact
+    load(2 * sb, p0, ip0);
+    load(2 * sb + 1, p1, ip1);
+    while (sb * 32 < nrows) {
+      int64_t nsb = sb + nwaves;
+      load(2 * nsb, q0, iq0);
+      load(2 * nsb + 1, q1, iq1);
+      __builtin_amdgcn_sched_barrier(0);  // prefetch stays above the MFMAs
+      {
+        f32x4 acc0[QB], acc1[QB];
+        score_regs2<DT, D, QB>(lds, g.segs, p0, p1, acc0, acc1);
+        epi(acc0, r0 + 2 * sb * 16 + r16, ip0);
+        if ((2 * sb + 1) * 16 < nrows) epi(acc1, r0 + (2 * sb + 1) * 16 + r16, ip1);
+      }
+      sb = nsb;
+      if (sb * 32 >= nrows) break;
+      nsb = sb + nwaves;
+      load(2 * nsb, p0, ip0);
+      load(2 * nsb + 1, p1, ip1);
+      __builtin_amdgcn_sched_barrier(0);
+      {
+        f32x4 acc0[QB], acc1[QB];
+        score_regs2<DT, D, QB>(lds, g.segs, q0, q1, acc0, acc1);
+        epi(acc0, r0 + 2 * sb * 16 + r16, iq0);
+        if ((2 * sb + 1) * 16 < nrows) epi(acc1, r0 + (2 * sb + 1) * 16 + r16, iq1);
+      }
+      sb = nsb;
+    }
+  } else if constexpr (kNC > 0) {
+    // NB fragment buffers: block rb + (NB - 1) W loads while block rb is
+    // multiplied; NB blocks are unrolled per iteration (compile-time indices)
+    constexpr int NB = ring_depth<DT, D, QB, Reserve>();
+    auto load = [&](int64_t blk, u32x4(&dst)[kNC], int64_t& rid) {
+      const int64_t row = r0 + blk * 16 + r16;
+      const int64_t rowc = row < r1 ? row : r1 - 1;
+      const u32x4* vrow = (const u32x4*)(base + (size_t)rowc * row_bytes) + h;
+#pragma unroll
+      for (int c = 0; c < kNC; ++c) dst[c] = vrow[4 * c];
+      if constexpr (kIds) rid = ids[rowc];
+    };
+    u32x4 buf[NB][kNC];
+    int64_t rid[NB];
+    if (nrows <= 0) return;
+    // unconditional prefetches (clamped rows past the end): a fixed load
+    // sequence keeps the compiler's wait counts exact
+#pragma unroll
+    for (int j = 0; j < NB - 1; ++j) load(wave + j * nwaves, buf[j], rid[j]);
     int64_t rb = wave;
-    if (rb * 16 < nrows) load(rb, b0, id0);
-    while (rb * 16 < nrows) {
-      if ((rb + nwaves) * 16 < nrows) load(rb + nwaves, b1, id1);
-      {
+    for (;;) {
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        if (rb * 16 >= nrows) return;
+        load(rb + (NB - 1) * nwaves, buf[(j + NB - 1) % NB], rid[(j + NB - 1) % NB]);
+        __builtin_amdgcn_sched_barrier(0);  // prefetch stays above the MFMAs
         f32x4 acc[QB];
-        score_regs<DT, D, QB>(lds, g.segs, b0, acc);
-        epi(acc, r0 + rb * 16 + r16, id0);
+        score_regs<DT, D, QB>(lds, g.segs, buf[j], acc);
+        epi(acc, r0 + rb * 16 + r16, rid[j]);
+        rb += nwaves;
       }
-      rb += nwaves;
-      if (rb * 16 >= nrows) break;
-      if ((rb + nwaves) * 16 < nrows) load(rb + nwaves, b0, id0);
-      {
-        f32x4 acc[QB];
-        score_regs<DT, D, QB>(lds, g.segs, b1, acc);
-        epi(acc, r0 + rb * 16 + r16, id1);
-      }
-      rb += nwaves;
     }
   } else {
     for (int64_t rb = wave; rb * 16 < nrows; rb += nwaves) {
       const int64_t row = r0 + rb * 16 + r16;
       const int64_t rowc = row < r1 ? row : r1 - 1;
       const u32x4* vrow = (const u32x4*)(base + (size_t)rowc * row_bytes);
-      const int64_t rid = ids ? ids[rowc] : 0;
+      int64_t rid = 0;
+      if constexpr (kIds) rid = ids[rowc];
       f32x4 acc[QB];
       score_stream<DT, QB>(lds, g, vrow, acc);
       epi(acc, row, rid);
@@ -351,30 +453,33 @@ constexpr int qb_cap() {
   return qb < 1 ? 1 : (qb > 8 ? 8 : qb);
 }
 
-template <int DT, int D, int QB, typename Epi>
+template <int DT, int D, int QB, bool kIds, int kMax, typename Epi>
 __device__ __forceinline__ void stream_rows_from(const u32x4* __restrict__ lds,
                                                  const RowGeom<DT>& g,
                                                  const char* __restrict__ base, size_t row_bytes,
                                                  const int64_t* __restrict__ ids, int64_t r0,
                                                  int64_t r1, int qb_n, Epi& epi) {
-  constexpr int kMax = qb_cap<DT, D>();
   if constexpr (QB >= kMax) {
-    stream_rows_qb<DT, D, kMax>(lds, g, base, row_bytes, ids, r0, r1, epi);
+    stream_rows_qb<DT, D, kMax, Epi, 0, kIds>(lds, g, base, row_bytes, ids, r0, r1, epi);
   } else {
     if (qb_n <= QB)
-      stream_rows_qb<DT, D, QB>(lds, g, base, row_bytes, ids, r0, r1, epi);
+      stream_rows_qb<DT, D, QB, Epi, 0, kIds>(lds, g, base, row_bytes, ids, r0, r1, epi);
     else
-      stream_rows_from<DT, D, QB + 1>(lds, g, base, row_bytes, ids, r0, r1, qb_n, epi);
+      stream_rows_from<DT, D, QB + 1, kIds, kMax>(lds, g, base, row_bytes, ids, r0, r1, qb_n,
+                                                  epi);
   }
 }
 
 // Dispatch on the tile's number of 16-query blocks (uniform per tile).
-template <int DT, int D, typename Epi>
+// kIds: hand each row block's ids[row] to the epilogue (else 0).  QBLimit:
+// the caller's largest tile, in 16-query blocks.
+template <int DT, int D, bool kIds = true, int QBLimit = 8, typename Epi>
 __device__ __forceinline__ void stream_rows(const u32x4* __restrict__ lds, const RowGeom<DT>& g,
                                             const char* __restrict__ base, size_t row_bytes,
                                             const int64_t* __restrict__ ids, int64_t r0,
                                             int64_t r1, int qb_n, Epi&& epi) {
-  stream_rows_from<DT, D, 1>(lds, g, base, row_bytes, ids, r0, r1, qb_n, epi);
+  constexpr int kMax = qb_cap<DT, D>() < QBLimit ? qb_cap<DT, D>() : QBLimit;
+  stream_rows_from<DT, D, 1, kIds, kMax>(lds, g, base, row_bytes, ids, r0, r1, qb_n, epi);
 }
 
 }  // namespace sieve

@@ -60,7 +60,8 @@ __device__ __forceinline__ void prefix_body(
       }
     }
   };
-  stream_rows_qb<DT, D, QB>(lds, g, (const char*)centroids, row_bytes, nullptr, 0, nlist, top2);
+  stream_rows_qb<DT, D, QB, decltype(top2), 8 * QB, false>(lds, g, (const char*)centroids, row_bytes,
+                                                     nullptr, 0, nlist, top2);
   __syncthreads();  // the staged queries are dead until re-staged below
 
   float* keep = (float*)lds;  // [QB * 16][kPrefixKeep]
@@ -138,8 +139,8 @@ __device__ __forceinline__ void prefix_body(
       }
     }
   };
-  stream_rows_qb<DT, D, QB>(lds, g, (const char*)centroids, row_bytes, nullptr, 0, nlist,
-                            collect);
+  stream_rows_qb<DT, D, QB, decltype(collect), 4 * QB, false>(lds, g, (const char*)centroids,
+                                                      row_bytes, nullptr, 0, nlist, collect);
 }
 
 template <int DT, int D>

@@ -133,20 +133,30 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
     int t_after = -1;
     if (threadIdx.x == 0) t_after = claim();  // read after the MFMAs
 
+    // Only the tile's last 16-query block can hold padding rows (qb_n =
+    // ceil(nq / 16)); its four rows of this lane get threshold +inf when they
+    // are padding, so the test below needs no per-row index compares.
+    const float tau = a.tau;
+    float thr_last[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      thr_last[r] = ((qb_n - 1) * 16 + 4 * h + r) < nq ? tau : INFINITY;
     stream_rows<DT, D>(
           lds, g, (const char*)a.vectors, row_bytes, a.ids, r0, r1, qb_n,
           [&](const auto& acc, int64_t row, int64_t rid) {
             constexpr int QB = sizeof(acc) / sizeof(acc[0]);
-            // tau test: one wave-wide vote in the common (no candidate) case
-            bool any = false;
+            // tau test: one wave-wide vote in the common (no candidate) case;
+            // full query blocks through a max tree, the last one per row
+            float mx = -INFINITY;
 #pragma unroll
-            for (int qb = 0; qb < QB; ++qb) {
+            for (int qb = 0; qb + 1 < QB; ++qb) {
 #pragma unroll
-              for (int r = 0; r < 4; ++r) {
-                const int i = qb * 16 + 4 * h + r;
-                any |= (row < r1) && (i < nq) && (acc[qb][r] >= a.tau);
-              }
+              for (int r = 0; r < 4; ++r) mx = fmaxf(mx, acc[qb][r]);
             }
+            bool any = mx >= tau;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) any |= acc[QB - 1][r] >= thr_last[r];
+            any = any && (row < r1);
             if (__ballot(any) == 0) return;
             // Candidates: one ballot group (16 rows x 4 queries) takes its
             // pool slots with one LDS atomic on the block's arena; the
@@ -159,27 +169,35 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
               for (int r = 0; r < 4; ++r) {
                 const int i = qb * 16 + 4 * h + r;
                 const float sc = acc[qb][r];
-                bool hit = any && (row < r1) && (i < nq) && (sc >= a.tau);
+                bool hit = any && (sc >= (qb + 1 < QB ? tau : thr_last[r]));
                 if (__ballot(hit) == 0) continue;
                 hit = hit && rid != s_ex[i];  // self-exclusion, read only for qualifying pairs
                 const unsigned long long mask = __ballot(hit);
                 if (mask == 0) continue;
                 const int leader = __ffsll((long long)mask) - 1;  // wave-uniform
-                unsigned long long base = 0;
+                const int cnt = __popcll(mask);
+                int o = 0;
                 if (lane == leader) {
-                  const int cnt = __popcll(mask);
-                  const int o = atomicAdd(&s_aused, cnt);
-                  if (o + cnt <= s_asize) {
-                    base = s_abase + (unsigned long long)o;
-                    atomicAdd(&s_afill, cnt);
-                  } else {
-                    base = atomicAdd(a.pool_count, (unsigned long long)cnt);
+                  o = atomicAdd(&s_aused, cnt);
+                  if (o + cnt <= s_asize) atomicAdd(&s_afill, cnt);
+                }
+                o = __builtin_amdgcn_readlane(o, leader);
+                unsigned long long base;
+                if (o + cnt <= s_asize) {  // wave-uniform; the common case
+                  base = s_abase + (unsigned long long)o;
+                } else {
+                  // The global claim sits in its own branch: waiting for its
+                  // result also waits for every load in flight (the prefetched
+                  // rows), which must not happen on the common path.
+                  unsigned long long gb = 0;
+                  if (lane == leader) {
+                    gb = atomicAdd(a.pool_count, (unsigned long long)cnt);
                     s_afall = 1;
                   }
+                  base = ((unsigned long long)(uint32_t)__builtin_amdgcn_readlane(
+                              (int)(gb >> 32), leader) << 32) |
+                         (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)gb, leader);
                 }
-                base = ((unsigned long long)(uint32_t)__builtin_amdgcn_readlane(
-                            (int)(base >> 32), leader) << 32) |
-                       (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)base, leader);
                 if (hit) {
                   const unsigned long long slot =
                       base + (unsigned long long)__popcll(mask & ((1ull << lane) - 1ull));
@@ -242,8 +260,10 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
 }
 
 // Centroid screen: scores[qi - q0][c] = fp32 <query qi, centroid c> for a
-// chunk of queries.  Grid: (ceil(nqc / rows), ceil(nlist / kScreenCents)).
+// chunk of queries.  Grid: (ceil(nqc / rows), ceil(nlist / kScreenCents)),
+// rows <= 16 * kScreenQB queries per work-group.
 constexpr int kScreenCents = 256;
+constexpr int kScreenQB = 4;
 
 template <int DT, int D>
 __global__ __launch_bounds__(kScanThreads, 2) void rank_scores_kernel(
@@ -265,7 +285,8 @@ __global__ __launch_bounds__(kScanThreads, 2) void rank_scores_kernel(
   __syncthreads();
   const int64_t c0 = (int64_t)blockIdx.y * kScreenCents;
   const int64_t c1 = min<int64_t>(nlist, c0 + kScreenCents);
-  stream_rows<DT, D>(lds, g, (const char*)centroids, row_bytes, nullptr, c0, c1, qb_n,
+  stream_rows<DT, D, false, kScreenQB>(lds, g, (const char*)centroids, row_bytes, nullptr, c0, c1,
+                                       qb_n,
                      [&](const auto& acc, int64_t c, int64_t) {
                        constexpr int QB = sizeof(acc) / sizeof(acc[0]);
                        if (c >= c1) return;
@@ -302,7 +323,7 @@ hipError_t launch_rank_scores_t(const void* queries, int64_t q0, int32_t nqc,
       hipFuncSetAttribute((const void*)rank_scores_kernel<DT, D>,
                           hipFuncAttributeMaxDynamicSharedMemorySize, kMaxDynLds);
   if (attr != hipSuccess) return attr;
-  const int rows = tile_rows(DT, d);
+  const int rows = tile_rows(DT, d) < 16 * kScreenQB ? tile_rows(DT, d) : 16 * kScreenQB;
   const size_t lds = (size_t)rows * lds_row_bytes<DT>(d);
   if (lds > (size_t)kMaxDynLds) return hipErrorInvalidValue;
   dim3 grid((nqc + rows - 1) / rows, (nlist + kScreenCents - 1) / kScreenCents);
