@@ -228,7 +228,7 @@ int grow_workspace(sieve_index* ix, const SearchPlan& pl) {
   if ((st = ensure(ix->scores, (size_t)pl.rank_chunk * ix->nlist * sizeof(float)))) return st;
   if ((st = ensure(ix->P, (size_t)rank_rows * n * sizeof(int32_t)))) return st;
   if ((st = ensure(ix->items, (size_t)pl.item_cap * sizeof(Item)))) return st;
-  if ((st = ensure(ix->bucket, (size_t)pl.item_cap * sizeof(Item)))) return st;
+  if ((st = ensure(ix->bucket, (size_t)pl.item_cap * sizeof(BItem)))) return st;
   // tiles: sum_p ceil(c_p / tq) * ceil(len_p / rc) <= items * max_chunks / tq + lists + rows / rc
   const int64_t max_ch = (ix->max_list + pl.row_chunk - 1) / pl.row_chunk;
   const int64_t tile_cap = pl.item_cap / pl.tile_q * (max_ch > 0 ? max_ch : 1) + ix->nlist +
@@ -313,7 +313,7 @@ ScanArgs make_scan_args(sieve_index* ix, const void* queries, const int64_t* exc
   a.ids = ix->ids;
   a.queries = queries;
   a.exclude = exclude;
-  a.bucket = (const Item*)ix->bucket.p;
+  a.bucket = (const BItem*)ix->bucket.p;
   a.tiles = (const Tile*)ix->tiles.p;
   a.rc = rc;
   a.lmax = (int32_t*)ix->lmax.p;
@@ -337,8 +337,8 @@ int run_round(sieve_index* ix, const ScanArgs& sa, int n_items, int64_t q0, cons
   HIP_TRY(launch_sched_offsets((const int32_t*)ix->cnt.p, ix->offsets, ix->nlist, pl.row_chunk,
                                pl.tile_q, (int32_t*)ix->item_off.p, (int32_t*)ix->cursor.p,
                                (int32_t*)ix->tile_off.p, rc, s));
-  HIP_TRY(launch_sched_scatter((const Item*)ix->items.p, n_items, P, pl.n, (int32_t)q0,
-                               (int32_t*)ix->cursor.p, (Item*)ix->bucket.p, s));
+  HIP_TRY(launch_sched_scatter((const Item*)ix->items.p, n_items, P, pl.n, (int32_t)q0, sa.exclude,
+                               (int32_t*)ix->cursor.p, (BItem*)ix->bucket.p, s));
   HIP_TRY(launch_sched_tiles((int32_t*)ix->cnt.p, (const int32_t*)ix->item_off.p,
                              (const int32_t*)ix->tile_off.p, ix->offsets, ix->nlist, pl.row_chunk,
                              pl.tile_q, (Tile*)ix->tiles.p, s));

@@ -65,6 +65,17 @@ __device__ __forceinline__ f32x4 mma_chunk(u32x4 a, u32x4 b, f32x4 acc) {
     return mma_chunk_f16(a, b, acc);
 }
 
+// Base address of this lane's query fragments in LDS.  The offset passes
+// through an empty asm so that the compiler cannot treat the fragment loads
+// as invariant across row blocks and hoist them all out of the row loop
+// (QB x chunks fragments would not fit in registers and would spill).
+__device__ __forceinline__ const u32x4* lane_arow(const u32x4* lds, int segs) {
+  const int lane = threadIdx.x & 63;
+  int off = (lane & 15) * segs + (lane >> 4);
+  asm volatile("" : "+v"(off));
+  return lds + off;
+}
+
 // Geometry of one query row in LDS, in 16-byte segments: 4 segments per chunk
 // plus one pad segment that staggers rows across LDS banks.
 template <int DT>
@@ -130,7 +141,7 @@ __device__ __forceinline__ void score_regs(const u32x4* __restrict__ lds, int se
   constexpr int kNC = D / DTraits<DT>::kChunkDims;
   const int lane = threadIdx.x & 63;
   const int h = lane >> 4, r16 = lane & 15;
-  const u32x4* arow = lds + r16 * segs + h;
+  const u32x4* arow = lane_arow(lds, segs);
   u32x4 a0[QB], a1[QB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
@@ -165,7 +176,7 @@ __device__ __forceinline__ void score_regs2(const u32x4* __restrict__ lds, int s
   constexpr int kAhead = 3;     // query fragments in flight from LDS
   const int lane = threadIdx.x & 63;
   const int h = lane >> 4, r16 = lane & 15;
-  const u32x4* arow = lds + r16 * segs + h;
+  const u32x4* arow = lane_arow(lds, segs);
   auto frag = [&](int t) { return arow[(t % QB) * 16 * segs + 4 * (t / QB)]; };
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
@@ -191,7 +202,7 @@ __device__ __forceinline__ void score_stream(const u32x4* __restrict__ lds, cons
                                              const u32x4* __restrict__ vrow, f32x4 (&acc)[QB]) {
   const int lane = threadIdx.x & 63;
   const int h = lane >> 4, r16 = lane & 15;
-  const u32x4* arow = lds + r16 * g.segs + h;
+  const u32x4* arow = lane_arow(lds, g.segs);
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) acc[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
   const u32x4 zero = {0u, 0u, 0u, 0u};
@@ -287,7 +298,7 @@ __device__ __forceinline__ void stream_rows_sliced(const u32x4* __restrict__ lds
   const int nwaves = blockDim.x >> 6;
   const int h = lane >> 4, r16 = lane & 15;
   const int64_t nrows = r1 - r0;
-  const u32x4* arow = lds + r16 * g.segs + h;
+  const u32x4* arow = lane_arow(lds, g.segs);
   auto rowc_of = [&](int64_t blk) {
     const int64_t row = r0 + blk * 16 + r16;
     return row < r1 ? row : r1 - 1;  // clamped: loads stay unconditional

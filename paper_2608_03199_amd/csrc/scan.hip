@@ -29,12 +29,48 @@
 namespace sieve {
 namespace {
 
+// Query staging: with kAsync the tile's query rows are copied global -> LDS
+// by the DMA path of the load unit (no registers) into one of two buffers
+// while the previous tile is still being multiplied; otherwise they are
+// staged through registers at the start of their tile.
 template <int DT, int D>
-__global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int qb_max) {
+constexpr bool async_stage_ok() {
+  if (D <= 0 || D % DTraits<DT>::kChunkDims != 0) return false;  // no partial chunk to zero
+  // two full-size buffers must fit the two-work-groups-per-CU budget
+  const int row = (4 * (D / DTraits<DT>::kChunkDims) + 1) * 16;
+  return 2 * 16 * qb_cap<DT, D>() * row <= 76 * 1024;
+}
+
+// Copy the query rows of a tile into a staging buffer with LDS-DMA loads:
+// 64 consecutive 16-byte slots of the buffer per wave instruction, slot
+// (row, seg) <- segment seg of the row's query.  Padding rows (past nq) and
+// the pad segment copy real data (a padding row repeats row 0): their scores
+// are never tested, and each buffer is padded to whole 64-slot chunks.
+template <int DT>
+__device__ __forceinline__ void dma_stage(u32x4* buf, const RowGeom<DT>& g,
+                                          const char* __restrict__ qbase, size_t row_bytes,
+                                          const int32_t* sq, int nq) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
+  const int total = ((nq + 15) >> 4) * 16 * g.segs;
+  const int nchunk = (total + 63) >> 6;
+  for (int c = wave; c < nchunk; c += nwaves) {
+    const int sidx = c * 64 + lane;
+    const int row = sidx / g.segs, seg = sidx - row * g.segs;
+    const int qrow = sq[row < nq ? row : 0];
+    const int segc = (seg < g.dsegs && sidx < total) ? seg : 0;
+    const char* src = qbase + (size_t)qrow * row_bytes + (size_t)segc * 16;
+    __builtin_amdgcn_global_load_lds((const void*)src,
+                                     (__attribute__((address_space(3))) void*)(buf + c * 64), 16,
+                                     0, 0);
+  }
+}
+
+template <int DT, int D, bool kAsync>
+__global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a) {
   extern __shared__ u32x4 lds[];
-  __shared__ int32_t s_q[kTileQ];
-  __shared__ int32_t s_rank[kTileQ];
-  __shared__ int64_t s_ex[kTileQ];
+  __shared__ int32_t s_q[2][kTileQ];     // item sets: the running tile and the next
+  __shared__ int32_t s_rank[2][kTileQ];
+  __shared__ int64_t s_ex[2][kTileQ];
   __shared__ int32_t s_hits[kTileQ];  // candidates per staged query in this tile
   __shared__ unsigned long long s_abase;  // first pool slot of the block's arena
   __shared__ int32_t s_asize;  // arena slots (0: no arena)
@@ -48,6 +84,7 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
   const int h = lane >> 4;
   const size_t row_bytes = (size_t)d * DTraits<DT>::kElem;
   const int ntiles = a.rc->ntiles;
+  const char* qbase = (const char*)a.queries;
   __shared__ int s_claim;
 
   // Tile schedule: the round's tiles are split into 8 contiguous ranges, one
@@ -55,10 +92,9 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
   // L2).  Static: the blocks of an XCD take its range's tiles in a fixed
   // stride (no atomics; best for small rounds).  Dynamic: thread 0 claims
   // tiles from its XCD's range with an atomic counter and moves on to the
-  // other ranges once it is drained (balances large rounds).  A block always
-  // holds two claims ahead: the tile it runs, whose descriptor and items were
-  // prefetched, and the next one, whose loads are issued under this tile's
-  // MFMAs; the claim after that is made then too and read after the MFMAs.
+  // other ranges once it is drained (balances large rounds).  While tile t
+  // runs, the block holds tile t+1 (items in LDS, queries staging) and the
+  // descriptor and items of tile t+2 (loads issued under t's MFMAs).
   const int home = blockIdx.x & 7;
   int xq = 0;    // thread 0, dynamic schedule: ranges already drained
   int kseq = 0;  // thread 0, static schedule: tiles taken so far
@@ -81,29 +117,37 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
     return -1;
   };
 
-  // prefetched state of the tile to run next
-  Tile nt = {};
-  Item nit = {};
-  int64_t nex = INT64_MIN, nr0 = 0, nr1 = 0;
-  auto prefetch = [&](int tt) {
-    if (tt < 0) return;
-    nt = a.tiles[tt];
-    const int64_t lb = a.list_offsets[nt.list];
-    nr0 = lb + (int64_t)nt.chunk * a.row_chunk;
-    nr1 = min(a.list_offsets[nt.list + 1], nr0 + a.row_chunk);
-    if ((int)threadIdx.x < nt.nq) {
-      nit = a.bucket[nt.item_begin + threadIdx.x];
-      nex = a.exclude ? a.exclude[nit.q] : INT64_MIN;
+  // Tile records and items flow through registers one tile ahead of use:
+  // each is loaded a whole tile before it is needed and never behind another
+  // load of the same tile (no dependent loads on the tile path).
+  auto load_rec = [&](int tt) -> Tile {
+    Tile r = {0, 0, 0, 0, 0};
+    tt = __builtin_amdgcn_readfirstlane(tt);  // uniform: scalar loads
+    if (tt >= 0) r = a.tiles[tt];
+    return r;
+  };
+  auto load_items = [&](const Tile& r) -> BItem {
+    // always a valid address: item 0 of the round stands in for no tile
+    const int64_t idx = r.nq > 0 ? r.item_begin + min((int)threadIdx.x, r.nq - 1) : 0;
+    return a.bucket[idx];
+  };
+  auto put_items = [&](int set, const Tile& r, const BItem& it) {
+    if ((int)threadIdx.x < r.nq) {
+      s_q[set][threadIdx.x] = it.q;
+      s_rank[set][threadIdx.x] = it.rank;
+      s_ex[set][threadIdx.x] = it.ex;
     }
   };
-  if (threadIdx.x == 0) s_claim = claim();
-  __syncthreads();
-  int t = s_claim;
-  __syncthreads();
-  if (threadIdx.x == 0) s_claim = claim();
-  __syncthreads();
-  int t_next = s_claim;
-  prefetch(t);
+
+  // four claims ahead: t (runs), tn (stages), ta (items load), tb (record
+  // loads); thread 0 claims the next one under each tile's MFMAs
+  __shared__ int s_first[4];
+  if (threadIdx.x == 0) {
+    s_first[0] = claim();
+    s_first[1] = claim();
+    s_first[2] = claim();
+    s_first[3] = claim();
+  }
   if (threadIdx.x < kTileQ) s_hits[threadIdx.x] = 0;
   if (threadIdx.x == 0) {
     const ArenaRec ar = a.arenas[blockIdx.x];  // the run left by the previous launch
@@ -113,25 +157,47 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
     s_afill = ar.fill;
     s_afall = 0;
   }
+  __syncthreads();
+  int t = s_first[0], tn = s_first[1], ta = s_first[2], tb = s_first[3];
+  Tile recT = load_rec(t), recN = load_rec(tn), recA = load_rec(ta);
+  BItem itN = load_items(recN);
+  put_items(0, recT, load_items(recT));
+  int set = 0;
+  __syncthreads();
+  if constexpr (kAsync) {
+    if (t >= 0) dma_stage<DT>(lds, g, qbase, row_bytes, s_q[0], recT.nq);
+    __builtin_amdgcn_s_waitcnt(0);
+  }
+  __syncthreads();
+
   for (; t >= 0;) {
-    const Tile tile = nt;
-    if ((int)threadIdx.x < tile.nq) {
-      s_q[threadIdx.x] = nit.q;
-      s_rank[threadIdx.x] = nit.rank;
-      s_ex[threadIdx.x] = nex;
+    // the next tile's items go to the other set
+    const int nset = set ^ 1;
+    put_items(nset, recN, itN);
+    __syncthreads();
+    int t_claim = -1;
+    if (threadIdx.x == 0) t_claim = claim();  // published at the end of this tile
+    u32x4* buf = lds;
+    if constexpr (kAsync) {
+      buf = lds + set * a.stage_u4;
+      if (tn >= 0) dma_stage<DT>(lds + nset * a.stage_u4, g, qbase, row_bytes, s_q[nset], recN.nq);
+    } else {
+      const int32_t* sq = s_q[set];
+      const int nq0 = recT.nq;
+      stage_queries<DT>(lds, g, ((nq0 + 15) >> 4) * 16, [&](int i) -> const u32x4* {
+        return i < nq0 ? (const u32x4*)(qbase + (size_t)sq[i] * row_bytes) : nullptr;
+      });
+      __syncthreads();
     }
-    __syncthreads();
-    const int nq = tile.nq;
+    // pipeline loads, used one tile from now
+    const BItem itA = load_items(recA);
+    const Tile recB = load_rec(tb);
+    const int32_t* sq = s_q[set];
+    const int32_t* srank = s_rank[set];
+    const int64_t* sex = s_ex[set];
+    const int nq = recT.nq;
     const int qb_n = (nq + 15) >> 4;
-    const int64_t r0 = nr0, r1 = nr1;
-    const char* qbase = (const char*)a.queries;
-    stage_queries<DT>(lds, g, qb_n * 16, [&](int i) -> const u32x4* {
-      return i < nq ? (const u32x4*)(qbase + (size_t)s_q[i] * row_bytes) : nullptr;
-    });
-    __syncthreads();
-    prefetch(t_next);  // next tile's descriptor and items load under this tile's MFMAs
-    int t_after = -1;
-    if (threadIdx.x == 0) t_after = claim();  // read after the MFMAs
+    const int64_t r0 = recT.r0, r1 = recT.r0 + recT.nrows;
 
     // Only the tile's last 16-query block can hold padding rows (qb_n =
     // ceil(nq / 16)); its four rows of this lane get threshold +inf when they
@@ -142,7 +208,7 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
     for (int r = 0; r < 4; ++r)
       thr_last[r] = ((qb_n - 1) * 16 + 4 * h + r) < nq ? tau : INFINITY;
     stream_rows<DT, D>(
-          lds, g, (const char*)a.vectors, row_bytes, a.ids, r0, r1, qb_n,
+          buf, g, (const char*)a.vectors, row_bytes, a.ids, r0, r1, qb_n,
           [&](const auto& acc, int64_t row, int64_t rid) {
             constexpr int QB = sizeof(acc) / sizeof(acc[0]);
             // tau test: one wave-wide vote in the common (no candidate) case;
@@ -165,13 +231,21 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
             const int r16 = lane & 15;
 #pragma unroll
             for (int qb = 0; qb < QB; ++qb) {
+              // skip query blocks without a candidate with one vote each
+              bool qany;
+              if (qb + 1 < QB)
+                qany = fmaxf(fmaxf(acc[qb][0], acc[qb][1]), fmaxf(acc[qb][2], acc[qb][3])) >= tau;
+              else
+                qany = acc[qb][0] >= thr_last[0] || acc[qb][1] >= thr_last[1] ||
+                       acc[qb][2] >= thr_last[2] || acc[qb][3] >= thr_last[3];
+              if (__ballot(any && qany) == 0) continue;
 #pragma unroll
               for (int r = 0; r < 4; ++r) {
                 const int i = qb * 16 + 4 * h + r;
                 const float sc = acc[qb][r];
                 bool hit = any && (sc >= (qb + 1 < QB ? tau : thr_last[r]));
                 if (__ballot(hit) == 0) continue;
-                hit = hit && rid != s_ex[i];  // self-exclusion, read only for qualifying pairs
+                hit = hit && rid != sex[i];  // self-exclusion, read only for qualifying pairs
                 const unsigned long long mask = __ballot(hit);
                 if (mask == 0) continue;
                 const int leader = __ffsll((long long)mask) - 1;  // wave-uniform
@@ -204,7 +278,7 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
                   if ((int64_t)slot < a.pool_cap) {
                     Hit hv;
                     hv.score = sc;
-                    hv.q = s_q[i];
+                    hv.q = sq[i];
                     hv.id = rid;
                     a.pool[slot] = hv;
                   }
@@ -216,12 +290,13 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
               }
             }
           });
-    __syncthreads();  // LDS is restaged by the next tile
+    if constexpr (kAsync) __builtin_amdgcn_s_waitcnt(0);  // this wave's staging copies landed
+    __syncthreads();  // every wave is done with this tile's buffer and items
     if ((int)threadIdx.x < nq && s_hits[threadIdx.x] > 0) {
       // this tile's candidates of one query: one count update, one hit flag
-      const int q = s_q[threadIdx.x];
+      const int q = sq[threadIdx.x];
       atomicAdd(&a.hcount[q], s_hits[threadIdx.x]);
-      atomicMax(&a.lmax[q], s_rank[threadIdx.x] + 1);
+      atomicMax(&a.lmax[q], srank[threadIdx.x] + 1);
       s_hits[threadIdx.x] = 0;
     }
     const bool refill = s_afall != 0;  // block-uniform: written before the barrier
@@ -236,7 +311,7 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
       __syncthreads();  // everyone has read the old arena before it is replaced
     }
     if (threadIdx.x == 0) {
-      s_claim = t_after;
+      s_claim = t_claim;
       if (refill) {
         const int sz = s_asize == 0 ? kArenaMin : min(2 * s_asize, kArenaMax);
         s_abase = atomicAdd(a.pool_count, (unsigned long long)sz);
@@ -247,8 +322,15 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a, int q
       }
     }
     __syncthreads();
-    t = t_next;
-    t_next = s_claim;
+    t = tn;
+    tn = ta;
+    ta = tb;
+    tb = s_claim;
+    recT = recN;
+    recN = recA;
+    recA = recB;
+    itN = itA;
+    set = nset;
   }
   if (threadIdx.x == 0) {
     ArenaRec ar;
@@ -304,15 +386,45 @@ __global__ __launch_bounds__(kScanThreads, 2) void rank_scores_kernel(
 // Dynamic LDS above 64 KB must be opted into once per kernel.
 constexpr int kMaxDynLds = 150 * 1024;
 
+// LDS per staging buffer (whole 64-slot chunks) and whether two of them fit
+// the budget that keeps two work-groups per CU.
+template <int DT, int D>
+size_t stage_bytes(int d, int tile_q) {
+  const size_t b = (size_t)tile_q * lds_row_bytes<DT>(D > 0 ? D : d);
+  return (b + 1023) & ~(size_t)1023;
+}
+
+template <int DT, int D>
+bool use_async(int d, int tile_q) {
+  if constexpr (!async_stage_ok<DT, D>()) {
+    (void)d;
+    (void)tile_q;
+    return false;
+  } else {
+    return 2 * stage_bytes<DT, D>(d, tile_q) <= (size_t)76 * 1024;
+  }
+}
+
+template <int DT, int D, bool kAsync>
+hipError_t launch_scan_k(ScanArgs a, int32_t grid, hipStream_t s) {
+  static const hipError_t attr =
+      hipFuncSetAttribute((const void*)scan_kernel<DT, D, kAsync>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, kMaxDynLds);
+  if (attr != hipSuccess) return attr;
+  const size_t one = stage_bytes<DT, D>(a.d, a.tile_q);
+  const size_t lds = kAsync ? 2 * one : one;
+  if (lds > (size_t)kMaxDynLds) return hipErrorInvalidValue;
+  a.stage_u4 = (int32_t)(one / 16);
+  hipLaunchKernelGGL((scan_kernel<DT, D, kAsync>), dim3(grid), dim3(kScanThreads), lds, s, a);
+  return hipGetLastError();
+}
+
 template <int DT, int D>
 hipError_t launch_scan_t(const ScanArgs& a, int32_t grid, hipStream_t s) {
-  static const hipError_t attr = hipFuncSetAttribute(
-      (const void*)scan_kernel<DT, D>, hipFuncAttributeMaxDynamicSharedMemorySize, kMaxDynLds);
-  if (attr != hipSuccess) return attr;
-  const size_t lds = (size_t)a.tile_q * lds_row_bytes<DT>(D > 0 ? D : a.d);
-  if (lds > (size_t)kMaxDynLds) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((scan_kernel<DT, D>), dim3(grid), dim3(kScanThreads), lds, s, a, kQB);
-  return hipGetLastError();
+  if constexpr (async_stage_ok<DT, D>()) {
+    if (use_async<DT, D>(a.d, a.tile_q)) return launch_scan_k<DT, D, true>(a, grid, s);
+  }
+  return launch_scan_k<DT, D, false>(a, grid, s);
 }
 
 template <int DT, int D>

@@ -135,13 +135,18 @@ __global__ __launch_bounds__(kOffThreads) void sched_offsets_kernel(
 
 __global__ void sched_scatter_kernel(const Item* __restrict__ items, int32_t n_items,
                                      const int32_t* __restrict__ P, int32_t n, int32_t q0,
-                                     int32_t* __restrict__ cursor, Item* __restrict__ bucket) {
+                                     const int64_t* __restrict__ exclude,
+                                     int32_t* __restrict__ cursor, BItem* __restrict__ bucket) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n_items) return;
   const Item it = items[i];
   const int p = P[(int64_t)(it.q - q0) * n + it.rank];
   const int pos = atomicAdd(&cursor[p], 1);
-  bucket[pos] = it;
+  BItem b;
+  b.q = it.q;
+  b.rank = it.rank;
+  b.ex = exclude ? exclude[it.q] : INT64_MIN;
+  bucket[pos] = b;
 }
 
 // One thread per list: write its tiles (query tiles x row chunks), tiles that
@@ -160,13 +165,15 @@ __global__ void sched_tiles_kernel(int32_t* __restrict__ cnt, const int32_t* __r
   const int ntq = (c + tile_q - 1) / tile_q;
   const int nch = (int)((len + row_chunk - 1) / row_chunk);
   int32_t o = tile_off[p];
+  const int64_t lb = list_offsets[p];
   for (int ch = 0; ch < nch; ++ch) {
     for (int tq = 0; tq < ntq; ++tq) {
       Tile t;
-      t.list = p;
+      t.r0 = lb + (int64_t)ch * row_chunk;
+      t.nrows = (int32_t)min<int64_t>(row_chunk, len - (int64_t)ch * row_chunk);
       t.item_begin = item_off[p] + tq * tile_q;
       t.nq = min(tile_q, c - tq * tile_q);
-      t.chunk = ch;
+      t.list = p;
       tiles[o++] = t;
     }
   }
@@ -328,10 +335,11 @@ hipError_t launch_sched_offsets(const int32_t* cnt, const int64_t* list_offsets,
 }
 
 hipError_t launch_sched_scatter(const Item* items, int32_t n_items, const int32_t* P, int32_t n,
-                                int32_t q0, int32_t* cursor, Item* bucket, hipStream_t s) {
+                                int32_t q0, const int64_t* exclude, int32_t* cursor,
+                                BItem* bucket, hipStream_t s) {
   if (n_items <= 0) return hipSuccess;
   hipLaunchKernelGGL(sched_scatter_kernel, dim3(blocks_for(n_items)), dim3(kThreads), 0, s, items,
-                     n_items, P, n, q0, cursor, bucket);
+                     n_items, P, n, q0, exclude, cursor, bucket);
   return hipGetLastError();
 }
 

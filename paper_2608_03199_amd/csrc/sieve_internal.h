@@ -18,10 +18,19 @@ struct Item {
 // One unit of partition-scan work: up to kTileQ items of one list, scored
 // against one chunk of that list's rows.
 struct Tile {
-  int32_t list;       // partition id
+  int64_t r0;         // first stored row of the tile's row chunk
+  int32_t nrows;      // rows in the chunk (1..row_chunk)
   int32_t item_begin; // first item of the tile in the partition-major bucket
   int32_t nq;         // items in the tile (1..kTileQ)
-  int32_t chunk;      // row chunk: rows [chunk*row_chunk, min(len, (chunk+1)*row_chunk))
+  int32_t list;       // partition id
+};
+
+// A bucketed item carries its query's exclusion id, so that the scan reads
+// everything about its next tile's items with one load per item.
+struct BItem {
+  int32_t q;
+  int32_t rank;
+  int64_t ex;  // exclude_ids[q], or INT64_MIN
 };
 
 // One qualifying candidate found by the scan (score >= tau, not excluded).
@@ -74,7 +83,7 @@ struct ScanArgs {
   const int64_t* ids;          // [n]
   const void* queries;         // [nq, d]
   const int64_t* exclude;      // [nq] or null
-  const Item* bucket;          // partition-major items of this round
+  const BItem* bucket;         // partition-major items of this round
   const Tile* tiles;
   RoundCounters* rc;
   int32_t* lmax;               // [nq] max 1-based hit rank this round (0 = none)
@@ -87,6 +96,7 @@ struct ScanArgs {
   int32_t row_chunk;
   int32_t tile_q;              // query rows per tile (multiple of 16, <= kTileQ)
   int32_t dynamic;             // 1: atomic work queue, 0: static strided schedule
+  int32_t stage_u4;            // 16-byte slots per query staging buffer (set by the launcher)
   float tau;
 };
 
@@ -121,7 +131,8 @@ hipError_t launch_sched_offsets(const int32_t* cnt, const int64_t* list_offsets,
                                 int32_t* cursor, int32_t* tile_off, RoundCounters* rc,
                                 hipStream_t s);
 hipError_t launch_sched_scatter(const Item* items, int32_t n_items, const int32_t* P, int32_t n,
-                                int32_t q0, int32_t* cursor, Item* bucket, hipStream_t s);
+                                int32_t q0, const int64_t* exclude, int32_t* cursor,
+                                BItem* bucket, hipStream_t s);
 hipError_t launch_sched_tiles(int32_t* cnt, const int32_t* item_off, const int32_t* tile_off,
                               const int64_t* list_offsets, int32_t nlist, int32_t row_chunk,
                               int32_t tile_q, Tile* tiles, hipStream_t s);
