@@ -1,0 +1,101 @@
+"""GPU parity at the benchmarked sizes.
+
+bench.py times the whole query batch of each workload with the library's default launch
+configuration.  Here the same full batches are searched the same way, and a seeded sample
+of queries is checked against the fp64 oracle, element by element (tests/parity.py), for
+the threshold search and the fixed-probe baseline.  Properties that hold at any size are
+checked on the whole batch: lookahead on and off give identical outputs, and W = infinity
+gives the fixed-probe result.
+
+Workloads: 1M x 128 fp32 (nlist 1,024, 10,000 queries), 10M x 768 fp16 (nlist 4,096,
+100,000 queries) and 100M x 128 fp16 (nlist 16,384, 1,000,000 queries).
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import sieve_workloads as sw
+from parity import assert_parity, compare
+
+pytestmark = pytest.mark.gpu
+
+NTHREADS = min(16, os.cpu_count() or 1)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _require_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    import paper_2608_03199_amd as ps
+    ps.load_library()
+
+
+def _host_sample(w, sel):
+    """Host copies for the oracle: the whole index, the sampled queries."""
+    return dict(vectors=w.vectors.cpu().numpy(), list_offsets=w.list_offsets.cpu().numpy(),
+                ids=w.ids.cpu().numpy(), centroids=w.centroids.cpu().numpy(),
+                queries=w.queries[torch.from_numpy(sel).to(w.queries.device)].cpu().numpy(),
+                exclude_ids=w.exclude_ids.cpu().numpy()[sel])
+
+
+def _run(name, n_sample, n_fixed_sample, check_identities):
+    import paper_2608_03199_amd as ps
+    spec = sw.SPECS[name]
+    print(f"[gpu-test] generating {name}", flush=True)
+    w = sw.make(spec, device="cuda")
+    ix = ps.Index(w.vectors, w.list_offsets, w.ids, w.centroids)
+    try:
+        ids, sc, pr = (t.cpu().numpy() for t in
+                       ix.search(w.queries, w.exclude_ids, spec.k, spec.tau, spec.W,
+                                 spec.nprobe_max))
+        rng = np.random.default_rng(spec.seed + 501)
+        sel = np.sort(rng.choice(spec.nq, n_sample, replace=False))
+        h = _host_sample(w, sel)
+        print(f"[gpu-test] {name}: oracle on {n_sample} sampled queries", flush=True)
+        o = oracle.search(h["vectors"], h["list_offsets"], h["ids"], h["centroids"],
+                          h["queries"], h["exclude_ids"], spec.k, spec.tau, spec.W,
+                          spec.nprobe_max, oracle.MODE_A, NTHREADS)
+        rep = compare(ids[sel], sc[sel], pr[sel], o)
+        print(f"[gpu-test] {name} sieve sample -> {rep}", flush=True)
+        assert_parity(rep)
+
+        fsel = sel[:n_fixed_sample]
+        f = [t.cpu().numpy() for t in ix.search_fixed(w.queries, w.exclude_ids, spec.k,
+                                                     spec.tau, spec.fixed_nprobe)]
+        hf = {k: (v[:n_fixed_sample] if k in ("queries", "exclude_ids") else v)
+              for k, v in h.items()}
+        of = oracle.search(hf["vectors"], hf["list_offsets"], hf["ids"], hf["centroids"],
+                           hf["queries"], hf["exclude_ids"], spec.k, spec.tau, oracle.W_INF,
+                           spec.fixed_nprobe, oracle.MODE_A, NTHREADS)
+        rep = compare(f[0][fsel], f[1][fsel], f[2][fsel], of)
+        print(f"[gpu-test] {name} fixed sample -> {rep}", flush=True)
+        assert_parity(rep)
+
+        if check_identities:
+            b = [t.cpu().numpy() for t in ix.search(w.queries, w.exclude_ids, spec.k, spec.tau,
+                                                    spec.W, spec.nprobe_max, lookahead=False)]
+            assert np.array_equal(ids, b[0]) and np.array_equal(pr, b[2])
+            assert np.array_equal(sc, b[1])
+            inf = [t.cpu().numpy() for t in ix.search(w.queries, w.exclude_ids, spec.k,
+                                                      spec.tau, 0x7FFFFFFF, spec.fixed_nprobe)]
+            for x, y in zip(inf, f):
+                assert np.array_equal(x, y)
+    finally:
+        ix.close()
+        del w
+        torch.cuda.empty_cache()
+
+
+def test_full_1m_d128_f32():
+    _run("c2", n_sample=1000, n_fixed_sample=200, check_identities=True)
+
+
+def test_full_10m_d768_f16():
+    _run("c3", n_sample=64, n_fixed_sample=16, check_identities=True)
+
+
+def test_full_100m_d128_f16():
+    _run("c5", n_sample=64, n_fixed_sample=8, check_identities=False)
