@@ -80,6 +80,9 @@ def main():
                     help="do not time the fixed-probe baseline (profiling runs)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (HBM counter calibration)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="W / lookahead / tau / fixed-nprobe sweep with recall on the 1M x 128 "
+                         "data (prints one JSON line with the table)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: this build measures one GPU only; --gpus must be 1", file=sys.stderr)
@@ -93,6 +96,8 @@ def main():
 
     dev = "cuda:0"
     torch.cuda.set_device(0)
+    if args.sweep:
+        return sweep(args, ps, sw, np, torch, dev)
     spec = sw.SPECS[args.config]
     log(f"[bench] generating {args.config} on {dev}")
     t0 = time.time()
@@ -235,6 +240,75 @@ def main():
                                                     "flag_kth_tie", "flagged_mismatch",
                                                     "max_score_err")}
     ix.close()
+    print(json.dumps(out), flush=True)
+
+
+W_INF = 0x7FFFFFFF
+
+
+def sweep(args, ps, sw, np, torch, dev):
+    """Operating sweep on the 1M x 128 fp32 data: W in {2, 4, 8, 16, inf} with lookahead on
+    and off (outputs must be identical), fixed nprobe in {32, 64, 128, 256}, each at tau in
+    {0.90, 0.95, 0.98}; queries/s over the whole 10,000-query batch, mean probes, and pooled
+    filtered top-10 recall (Sec. 6.1) on a seeded 2,000-query subset against exact filtered
+    brute force from the oracle (W = inf, nprobe = nlist)."""
+    import oracle
+    from sieve_workloads.metrics import pooled_recall
+    spec = sw.SPECS["c2"]
+    log("[sweep] generating c2")
+    w = sw.make(spec, device=dev)
+    ix = ps.Index(w.vectors, w.list_offsets, w.ids, w.centroids)
+    rng = np.random.default_rng(spec.seed + 4)
+    sel = np.sort(rng.choice(spec.nq, 2000, replace=False))
+    h = w.numpy()
+    steps = max(1, args.steps // 4)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            r = fn()
+        torch.cuda.synchronize()
+        return r, (time.perf_counter() - t0) / steps
+
+    # exact filtered top-10 at the lowest tau; a higher tau keeps the prefix whose fp64
+    # score reaches it (the top-10 order does not depend on tau)
+    log("[sweep] exact filtered top-10 of 2,000 queries (oracle brute force)")
+    exact = oracle.bruteforce(h["vectors"], h["ids"], h["queries"][sel], h["exclude_ids"][sel],
+                              spec.k, 0.90, os.cpu_count() or 1)
+    rows = []
+    for tau in (0.90, 0.95, 0.98):
+        truth_ids = np.where(exact.scores >= tau, exact.ids, -1)
+        for W in (2, 4, 8, 16, W_INF):
+            res = {}
+            for la in (True, False):
+                r, sec = timed(lambda: ix.search(w.queries, w.exclude_ids, spec.k, tau, W,
+                                                 spec.nprobe_max, lookahead=la))
+                res[la] = (r, sec)
+            a, b = res[True][0], res[False][0]
+            same = all(bool(torch.equal(x, y)) for x, y in zip(a, b))
+            ids = a[0].cpu().numpy()
+            rec = pooled_recall(ids[sel], truth_ids)[0]
+            rows.append({"mode": "sieve", "tau": tau, "W": "inf" if W == W_INF else W,
+                         "qps_lookahead": round(spec.nq / res[True][1], 1),
+                         "qps_no_lookahead": round(spec.nq / res[False][1], 1),
+                         "lookahead_identical": same,
+                         "mean_probes": round(float(a[2].float().mean()), 3),
+                         "recall_at_10": round(rec, 5)})
+            log(f"[sweep] {rows[-1]}")
+        for npb in (32, 64, 128, 256):
+            r, sec = timed(lambda: ix.search_fixed(w.queries, w.exclude_ids, spec.k, tau, npb))
+            ids = r[0].cpu().numpy()
+            rows.append({"mode": "fixed", "tau": tau, "nprobe": npb,
+                         "qps": round(spec.nq / sec, 1), "mean_probes": float(npb),
+                         "recall_at_10": round(pooled_recall(ids[sel], truth_ids)[0], 5)})
+            log(f"[sweep] {rows[-1]}")
+    ix.close()
+    out = {"metric": "operating sweep: queries/s, mean probes, pooled filtered recall@10",
+           "config": {"workload": workload_name(spec), "recall_subset": 2000,
+                      "nprobe_max": spec.nprobe_max},
+           "steps_per_point": steps, "sweep": rows}
     print(json.dumps(out), flush=True)
 
 
