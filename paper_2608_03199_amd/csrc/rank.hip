@@ -228,6 +228,120 @@ __global__ __launch_bounds__(NT) void rank_select_kernel(
   for (int r = t; r < n; r += NT) P[ql * ldp + r] = (int32_t)(ck[r] & 0xffffffffu);
 }
 
+// One query per block of 256 threads, its screen scores held in registers
+// (KPT per thread, nlist <= 256 * KPT): long prefixes over large centroid
+// sets, where one wave per query would hold too many keys.
+//   1. the n-th largest key is found bit by bit (32 steps; each step counts
+//      keys >= the candidate prefix with ballot popcounts per wave and one
+//      LDS exchange between the four waves);
+//   2. candidates (s32 >= v - 2 delta) are compacted with ballots into LDS;
+//   3. they are sorted by counting, near-tie runs are re-scored in fp64
+//      (waves of the block share the members), and the first n are written.
+// More than cap candidates (or fewer than n) sets rank_error.
+template <int DT, int KPT>
+__global__ __launch_bounds__(256) void rank_select_reg_kernel(
+    const void* __restrict__ queries, int64_t q0, const void* __restrict__ centroids,
+    int32_t nlist, int32_t d, const float* __restrict__ scores, int32_t n, int32_t cap,
+    double cmax, int32_t* __restrict__ P, int64_t ldp, RoundCounters* rc) {
+  extern __shared__ uint8_t smem[];
+  unsigned long long* ck = (unsigned long long*)smem;  // [cap]
+  unsigned long long* out = ck + cap;                  // [cap]
+  double* cs = (double*)(out + cap);                   // [cap]
+  uint8_t* link = (uint8_t*)(cs + cap);                // [cap]
+  __shared__ int s_cnt[2][4];
+  __shared__ double s_ss[4];
+  __shared__ int s_m;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int64_t ql = blockIdx.x;
+  const int64_t qg = q0 + ql;
+  const float* row = scores + ql * nlist;
+
+  uint32_t key[KPT];
+#pragma unroll
+  for (int j = 0; j < KPT; ++j) {
+    const int c = t + 256 * j;
+    const float v = row[c < nlist ? c : nlist - 1];  // clamped: the loads issue together
+    key[j] = c < nlist ? f2key(v) : 0u;              // 0 sorts below every score
+  }
+  double ss = 0.0;
+  for (int i = t; i < d; i += 256) {
+    const double v = load_elem<DT>(queries, qg * d + i);
+    ss += v * v;
+  }
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+  if (lane == 0) s_ss[wave] = ss;
+  if (t == 0) s_m = 0;
+  __syncthreads();
+  const double qn = sqrt(s_ss[0] + s_ss[1] + s_ss[2] + s_ss[3]);
+  const double delta = 2.0 * (double)(d + 2) * 5.9604644775390625e-08 * qn * cmax + 1e-30;
+  const double gap = 2.0 * delta;
+
+  // 1. exact n-th largest key (the two count slots alternate, one barrier a step)
+  uint32_t prefix = 0;
+  for (int bit = 31; bit >= 0; --bit) {
+    const uint32_t cand = prefix | (1u << bit);
+    int cnt = 0;  // this lane's keys >= cand, then the wave's sum
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) cnt += key[j] >= cand ? 1 : 0;
+    for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o);
+    if (lane == 0) s_cnt[bit & 1][wave] = cnt;
+    __syncthreads();
+    const int total = s_cnt[bit & 1][0] + s_cnt[bit & 1][1] + s_cnt[bit & 1][2] +
+                      s_cnt[bit & 1][3];
+    if (total >= n) prefix = cand;
+  }
+  const double lo = (double)key2f(prefix) - gap;
+
+  // 2. candidates, compacted with ballots (one LDS atomic per wave and slot)
+#pragma unroll
+  for (int j = 0; j < KPT; ++j) {
+    const int c = t + 256 * j;
+    const bool take = c < nlist && (double)key2f(key[j]) >= lo;
+    const unsigned long long mask = __ballot(take);
+    if (mask == 0) continue;
+    int base = 0;
+    if (lane == __ffsll((long long)mask) - 1) base = atomicAdd(&s_m, __popcll(mask));
+    base = __builtin_amdgcn_readlane(base, __ffsll((long long)mask) - 1);
+    const int pos = base + __popcll(mask & ((1ull << lane) - 1ull));
+    if (take && pos < cap) ck[pos] = ((unsigned long long)(~key[j]) << 32) | (unsigned)c;
+  }
+  __syncthreads();
+  const int m = s_m;
+  if (m > cap || m < n) {
+    if (t == 0) atomicExch(&rc->rank_error, 1);
+    for (int r = t; r < n; r += 256) P[ql * ldp + r] = r;  // valid placeholder
+    return;
+  }
+  // 3. exact sort by counting (keys are distinct), runs, fp64 refinement
+  for (int i = t; i < m; i += 256) {
+    const unsigned long long ki = ck[i];
+    int pos = 0;
+#pragma unroll 8
+    for (int j = 0; j < m; ++j) pos += ck[j] < ki ? 1 : 0;
+    out[pos] = ki;
+  }
+  __syncthreads();
+  for (int i = t; i < m; i += 256) {
+    bool l = false;
+    if (i + 1 < m) {
+      const double x = (double)key2f(~(uint32_t)(out[i] >> 32));
+      const double y = (double)key2f(~(uint32_t)(out[i + 1] >> 32));
+      l = (x - y) <= gap;
+    }
+    link[i] = l ? 1 : 0;
+  }
+  __syncthreads();
+  refine_members<DT>(out, cs, link, m, queries, qg, centroids, d, wave, 4);
+  __syncthreads();
+  {
+    const double gap64 =
+        2.0 * 2.0 * (double)(d + (d + 63) / 64 + 6) * 1.1102230246251565e-16 * qn * cmax + 1e-300;
+    order_runs<DT>(out, cs, link, m, queries, qg, centroids, d, gap64, t, 256);
+  }
+  __syncthreads();
+  for (int r = t; r < n; r += 256) P[ql * ldp + r] = (int32_t)(out[r] & 0xffffffffu);
+}
+
 // Boundary candidates per lane in the wave kernel (capw <= 64 * this).
 constexpr int kKeysPerLane = 8;
 
@@ -371,6 +485,28 @@ hipError_t launch_rank_select(int dtype, const void* queries, int64_t q0, int32_
                                         cmax, P, ldp, rc, s)
                : launch_wave<SIEVE_F16>(queries, q0, nqc, centroids, nlist, d, scores, n, capw,
                                         cmax, P, ldp, rc, s);
+  }
+  // register-resident block kernel: large centroid sets, narrow buffer
+  if (!wide && nlist > 1024 && nlist <= 256 * 64) {
+    const int32_t capr = n + 512 < nlist ? n + 512 : nlist;
+    const size_t ldsr = (size_t)capr * 25;
+    if (ldsr <= 64 * 1024) {
+      const int kpt = nlist <= 256 * 16 ? 16 : (nlist <= 256 * 32 ? 32 : 64);
+#define SIEVE_REG(DT, K)                                                                       \
+  hipLaunchKernelGGL((rank_select_reg_kernel<DT, K>), dim3(nqc), dim3(256), ldsr, s, queries, q0, \
+                     centroids, nlist, d, scores, n, capr, cmax, P, ldp, rc)
+      if (dtype == SIEVE_F32) {
+        if (kpt == 16) SIEVE_REG(SIEVE_F32, 16);
+        else if (kpt == 32) SIEVE_REG(SIEVE_F32, 32);
+        else SIEVE_REG(SIEVE_F32, 64);
+      } else {
+        if (kpt == 16) SIEVE_REG(SIEVE_F16, 16);
+        else if (kpt == 32) SIEVE_REG(SIEVE_F16, 32);
+        else SIEVE_REG(SIEVE_F16, 64);
+      }
+#undef SIEVE_REG
+      return hipGetLastError();
+    }
   }
   // block kernel: narrow (n + 512 boundary candidates) or wide (every
   // centroid, up to kMaxCand)

@@ -322,6 +322,48 @@ def test_sieve_matches_oracle_on_each_rank_path(name, lookahead, rank_path):
     _check(c, s.k, s.tau, s.W, s.nprobe_max, lookahead)
 
 
+@pytest.mark.parametrize("nlist,d,dtype", [(2048, 32, torch.float32), (5000, 64, torch.float16)])
+def test_rank_and_search_on_large_centroid_sets(nlist, d, dtype, rank_path):
+    """More than 1,024 centroids: long prefixes take the register-resident block selector,
+    short ones the fused screen (or the materialised path, forced); the order must be the
+    oracle's exactly and a search with nprobe = 150 must match it."""
+    rng = np.random.default_rng(nlist)
+    n, nq = 30000, 96
+    C = rng.standard_normal((nlist, d))
+    C /= np.linalg.norm(C, axis=1, keepdims=True)
+    X = rng.standard_normal((n, d))
+    X /= np.linalg.norm(X, axis=1, keepdims=True)
+    npdt = np.float32 if dtype == torch.float32 else np.float16
+    C, X = C.astype(npdt), X.astype(npdt)
+    lab = rng.integers(0, nlist, n)
+    order = np.argsort(lab, kind="stable")
+    X = X[order]
+    off = np.concatenate([[0], np.cumsum(np.bincount(lab, minlength=nlist))]).astype(np.int64)
+    ids = order.astype(np.int64)
+    qrows = rng.choice(n, nq, replace=False)
+    Q = X[qrows].copy()
+    ex = ids[qrows]
+    ps = _lib()
+    dev = "cuda"
+    ix = ps.Index(torch.from_numpy(X).to(dev), torch.from_numpy(off).to(dev),
+                  torch.from_numpy(ids).to(dev), torch.from_numpy(C).to(dev))
+    try:
+        tq = torch.from_numpy(Q).to(dev)
+        o = oracle.search(X, off, ids, C, Q, ex, 1, 2.0, 1, 300, want_order=True,
+                          nthreads=NTHREADS)
+        for R in (8, 64, 100, 300):
+            P = ix.rank(tq, R).cpu().numpy()
+            assert np.array_equal(P, o.order[:, :R]), R
+        g = ix.search(tq, torch.from_numpy(ex).to(dev), 10, 0.5, 4, 150)
+        og = oracle.search(X, off, ids, C, Q, ex, 10, 0.5, 4, 150, nthreads=NTHREADS)
+        assert_parity(compare(g[0].cpu().numpy(), g[1].cpu().numpy(), g[2].cpu().numpy(), og))
+        f = ix.search_fixed(tq, torch.from_numpy(ex).to(dev), 10, 0.5, 150)
+        of = oracle.search(X, off, ids, C, Q, ex, 10, 0.5, oracle.W_INF, 150, nthreads=NTHREADS)
+        assert_parity(compare(f[0].cpu().numpy(), f[1].cpu().numpy(), f[2].cpu().numpy(), of))
+    finally:
+        ix.close()
+
+
 def test_rank_with_many_exact_ties_takes_the_wide_path(rank_path):
     """800 identical centroids tie at the top: the one-wave selection runs out of
     boundary room, the search re-ranks with the wide kernel, and the order is
