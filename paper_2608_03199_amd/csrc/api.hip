@@ -203,6 +203,7 @@ struct SearchPlan {
   int64_t fix_chunk;   // queries per fixed-probe chunk
   int64_t item_cap;
   int r0;              // ranks ordered up front (the rest on demand)
+  bool wide;           // wide scan configuration (see tile_rows_wide)
   int scan_grid;       // scan work-groups (fixed for the whole search)
   bool wide_rank;      // rank with room for every boundary near-tie (retry path)
 };
@@ -325,6 +326,7 @@ ScanArgs make_scan_args(sieve_index* ix, const void* queries, const int64_t* exc
   a.d = ix->d;
   a.row_chunk = pl.row_chunk;
   a.tile_q = pl.tile_q;
+  a.wide = pl.wide ? 1 : 0;
   a.tau = pl.tau;
   return a;
 }
@@ -534,10 +536,12 @@ int plan_search(const sieve_index* ix, int64_t nq, int32_t k, float tau, int32_t
   pl->k = k;
   pl->tau = tau;
   pl->nq = nq;
-  pl->tile_q = tile_rows(ix->dtype, ix->d);
+  // default on where supported; SIEVE_SCAN_WIDE=2 turns it off (tuning only)
+  pl->wide = scan_wide_supported(ix->dtype, ix->d) && env_int("SIEVE_SCAN_WIDE", 1) == 1;
+  pl->tile_q = pl->wide ? tile_rows_wide(ix->dtype, ix->d) : tile_rows(ix->dtype, ix->d);
   pl->wide_rank = false;
   pl->row_chunk = row_chunk_for(ix);
-  pl->scan_grid = scan_grid(ix, pl->tile_q);
+  pl->scan_grid = pl->wide ? ((ix->cus + 7) / 8) * 8 : scan_grid(ix, pl->tile_q);
   // Lazy ranking: a stop line starts at min(W, n) and mostly stays near it,
   // so only the first r0 ranks are ordered up front (queries whose stop line
   // passes r0 get all n later).

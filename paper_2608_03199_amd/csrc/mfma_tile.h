@@ -263,7 +263,7 @@ __device__ __forceinline__ void mma_slice(const u32x4* __restrict__ arow, int se
 template <int DT, int D, int QB, int Reserve>
 constexpr int ring_depth() {
   constexpr int kNC = D / DTraits<DT>::kChunkDims;
-  if (kNC > kSliceChunks) return Reserve > 0 ? 2 : 3;  // slices of kSliceChunks chunks
+  if (kNC > kSliceChunks) return (Reserve > 0 || QB > 3) ? 2 : 3;  // slices of kSliceChunks chunks
   const int per = 4 * kNC;                             // VGPRs per buffered row block
   const int budget = (QB <= 2 ? 96 : (QB <= 4 ? 64 : 40)) - Reserve;
   const int nb = budget / per;
@@ -456,11 +456,11 @@ __device__ __forceinline__ void stream_rows_qb(const u32x4* __restrict__ lds,
 // Largest number of 16-query blocks a tile of compile-time dimension D can
 // stage (the 80 KB LDS budget that keeps two work-groups per CU; the host's
 // tile size follows the same rule).  D = 0: runtime dimension, up to 8.
-template <int DT, int D>
+template <int DT, int D, int kBudgetKB = 80>
 constexpr int qb_cap() {
   if (D == 0) return 8;
   const int segs = 4 * ((D + DTraits<DT>::kChunkDims - 1) / DTraits<DT>::kChunkDims) + 1;
-  const int qb = (80 * 1024) / (16 * segs * 16);
+  const int qb = (kBudgetKB * 1024) / (16 * segs * 16);
   return qb < 1 ? 1 : (qb > 8 ? 8 : qb);
 }
 
@@ -483,13 +483,15 @@ __device__ __forceinline__ void stream_rows_from(const u32x4* __restrict__ lds,
 
 // Dispatch on the tile's number of 16-query blocks (uniform per tile).
 // kIds: hand each row block's ids[row] to the epilogue (else 0).  QBLimit:
-// the caller's largest tile, in 16-query blocks.
-template <int DT, int D, bool kIds = true, int QBLimit = 8, typename Epi>
+// the caller's largest tile, in 16-query blocks; kBudgetKB: the LDS budget
+// the caller's tile size follows.
+template <int DT, int D, bool kIds = true, int QBLimit = 8, int kBudgetKB = 80, typename Epi>
 __device__ __forceinline__ void stream_rows(const u32x4* __restrict__ lds, const RowGeom<DT>& g,
                                             const char* __restrict__ base, size_t row_bytes,
                                             const int64_t* __restrict__ ids, int64_t r0,
                                             int64_t r1, int qb_n, Epi&& epi) {
-  constexpr int kMax = qb_cap<DT, D>() < QBLimit ? qb_cap<DT, D>() : QBLimit;
+  constexpr int kCap = qb_cap<DT, D, kBudgetKB>();
+  constexpr int kMax = kCap < QBLimit ? kCap : QBLimit;
   stream_rows_from<DT, D, 1, kIds, kMax>(lds, g, base, row_bytes, ids, r0, r1, qb_n, epi);
 }
 

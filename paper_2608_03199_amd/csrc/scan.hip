@@ -65,8 +65,8 @@ __device__ __forceinline__ void dma_stage(u32x4* buf, const RowGeom<DT>& g,
   }
 }
 
-template <int DT, int D, bool kAsync>
-__global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a) {
+template <int DT, int D, bool kAsync, int kNT>
+__global__ __launch_bounds__(kNT, kNT == kScanThreads ? 2 : 1) void scan_kernel(ScanArgs a) {
   extern __shared__ u32x4 lds[];
   __shared__ int32_t s_q[2][kTileQ];     // item sets: the running tile and the next
   __shared__ int32_t s_rank[2][kTileQ];
@@ -207,7 +207,7 @@ __global__ __launch_bounds__(kScanThreads, 2) void scan_kernel(ScanArgs a) {
 #pragma unroll
     for (int r = 0; r < 4; ++r)
       thr_last[r] = ((qb_n - 1) * 16 + 4 * h + r) < nq ? tau : INFINITY;
-    stream_rows<DT, D>(
+    stream_rows<DT, D, true, 8, kNT == kScanThreads ? 80 : 150>(
           buf, g, (const char*)a.vectors, row_bytes, a.ids, r0, r1, qb_n,
           [&](const auto& acc, int64_t row, int64_t rid) {
             constexpr int QB = sizeof(acc) / sizeof(acc[0]);
@@ -405,26 +405,29 @@ bool use_async(int d, int tile_q) {
   }
 }
 
-template <int DT, int D, bool kAsync>
+template <int DT, int D, bool kAsync, int kNT>
 hipError_t launch_scan_k(ScanArgs a, int32_t grid, hipStream_t s) {
   static const hipError_t attr =
-      hipFuncSetAttribute((const void*)scan_kernel<DT, D, kAsync>,
+      hipFuncSetAttribute((const void*)scan_kernel<DT, D, kAsync, kNT>,
                           hipFuncAttributeMaxDynamicSharedMemorySize, kMaxDynLds);
   if (attr != hipSuccess) return attr;
   const size_t one = stage_bytes<DT, D>(a.d, a.tile_q);
   const size_t lds = kAsync ? 2 * one : one;
   if (lds > (size_t)kMaxDynLds) return hipErrorInvalidValue;
   a.stage_u4 = (int32_t)(one / 16);
-  hipLaunchKernelGGL((scan_kernel<DT, D, kAsync>), dim3(grid), dim3(kScanThreads), lds, s, a);
+  hipLaunchKernelGGL((scan_kernel<DT, D, kAsync, kNT>), dim3(grid), dim3(kNT), lds, s, a);
   return hipGetLastError();
 }
 
 template <int DT, int D>
 hipError_t launch_scan_t(const ScanArgs& a, int32_t grid, hipStream_t s) {
-  if constexpr (async_stage_ok<DT, D>()) {
-    if (use_async<DT, D>(a.d, a.tile_q)) return launch_scan_k<DT, D, true>(a, grid, s);
+  if constexpr (D == 768) {
+    if (a.wide) return launch_scan_k<DT, D, false, kScanThreadsWide>(a, grid, s);
   }
-  return launch_scan_k<DT, D, false>(a, grid, s);
+  if constexpr (async_stage_ok<DT, D>()) {
+    if (use_async<DT, D>(a.d, a.tile_q)) return launch_scan_k<DT, D, true, kScanThreads>(a, grid, s);
+  }
+  return launch_scan_k<DT, D, false, kScanThreads>(a, grid, s);
 }
 
 template <int DT, int D>
@@ -450,6 +453,15 @@ size_t scan_lds_bytes(int dtype, int d, int rows) {
   return (size_t)rows * (dtype == SIEVE_F32 ? lds_row_bytes<SIEVE_F32>(d)
                                             : lds_row_bytes<SIEVE_F16>(d));
 }
+
+int tile_rows_wide(int dtype, int d) {
+  const int rb = dtype == SIEVE_F32 ? lds_row_bytes<SIEVE_F32>(d) : lds_row_bytes<SIEVE_F16>(d);
+  int qb = (150 * 1024) / (16 * rb);
+  qb = qb < 1 ? 1 : (qb > kQB ? kQB : qb);
+  return 16 * qb;
+}
+
+bool scan_wide_supported(int dtype, int d) { return dtype == SIEVE_F16 && d == 768; }
 
 int tile_rows(int dtype, int d) {
   const int rb = dtype == SIEVE_F32 ? lds_row_bytes<SIEVE_F32>(d) : lds_row_bytes<SIEVE_F16>(d);

@@ -97,12 +97,19 @@ struct ScanArgs {
   int32_t tile_q;              // query rows per tile (multiple of 16, <= kTileQ)
   int32_t dynamic;             // 1: atomic work queue, 0: static strided schedule
   int32_t stage_u4;            // 16-byte slots per query staging buffer (set by the launcher)
+  int32_t wide;                // 1: wide configuration (one big work-group per CU)
   float tau;
 };
 
 // Query rows per tile for a dtype and dimension: as many 16-row blocks (<= 8)
 // as fit an 80 KB LDS budget, so that two work-groups share a CU.
 int tile_rows(int dtype, int d);
+// Wide scan configuration: one work-group of kScanThreadsWide threads per CU
+// with a tile of up to 150 KB of staged queries (large rows: fewer re-reads
+// of each list by its query tiles).
+constexpr int kScanThreadsWide = 512;
+int tile_rows_wide(int dtype, int d);
+bool scan_wide_supported(int dtype, int d);
 
 // ---- launchers (each returns the hipError_t of its launch) ----
 hipError_t launch_rank_scores(int dtype, const void* queries, int64_t q0, int32_t nqc,
