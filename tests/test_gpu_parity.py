@@ -223,6 +223,14 @@ def test_uncommon_dimensions(d, dtype, rank_path):
     c = Case(sw.make(sp, device="cuda"))
     _check(c, 10, 0.9, 3, 12)
     _check(c, 10, 0.9, 3, 24, fixed=True)
+    if d == 768:
+        # the 768-dim scan also has the two-work-groups-per-CU configuration
+        os.environ["SIEVE_SCAN_WIDE"] = "2"
+        try:
+            _check(c, 10, 0.9, 3, 12)
+            _check(c, 10, 0.9, 3, 24, fixed=True)
+        finally:
+            del os.environ["SIEVE_SCAN_WIDE"]
 
 
 def test_empty_lists_and_unbalanced_index():
