@@ -78,6 +78,8 @@ def main():
     ap.add_argument("--no-oracle", action="store_true")
     ap.add_argument("--skip-fixed", action="store_true",
                     help="do not time the fixed-probe baseline (profiling runs)")
+    ap.add_argument("--skip-calibrated", action="store_true",
+                    help="do not time the in-call calibrated search (profiling runs)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (HBM counter calibration)")
     ap.add_argument("--sweep", action="store_true",
@@ -154,6 +156,34 @@ def main():
     torch.cuda.synchronize()
     t_fixed = time.perf_counter() - t0 if not args.skip_fixed else float("nan")
 
+    # in-call calibration (Appendix A): a seeded 2% sample fully probed, the
+    # window chosen for a 0.5% sample-relative loss target, the rest searched
+    # with it; the sample's full probing is inside the timed region
+    cal = None
+    if not args.skip_calibrated:
+        ns = max(1, nq // 50)
+        smp = torch.from_numpy(np.random.default_rng(spec.seed + 91).choice(
+            nq, ns, replace=False).astype(np.int32)).to(dev)
+
+        def calibrated(with_stats=True):
+            return ix.search_calibrated(w.queries, w.exclude_ids, spec.k, spec.tau,
+                                        spec.nprobe_max, smp, CAL_EPS, spec.W,
+                                        with_stats=with_stats)
+
+        calibrated()
+        csteps = max(1, min(args.steps, 5))
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(csteps):
+            cr = calibrated()
+        torch.cuda.synchronize()
+        t_cal = (time.perf_counter() - t0) / csteps
+        cal = {"W": cr[3], "sample": ns, "eps": CAL_EPS, "steps": csteps,
+               "qps": round(nq / t_cal, 1),
+               "speedup_vs_fixed": (None if args.skip_fixed else
+                                    round((t_fixed / args.steps) / t_cal, 3)),
+               "mean_probes": round(float(cr[2].float().mean().item()), 3)}
+
     ms_step = 1e3 * t_sieve / args.steps
     qps = nq * args.steps / t_sieve
     fixed_qps = nq * args.steps / t_fixed
@@ -213,6 +243,7 @@ def main():
         "fixed_phase_ms": ({k: round(mean(fstats, "ms_" + k), 4) for k in
                             ("rank", "sched", "scan", "finalize", "total")} if fstats else None),
         "roofline": roof,
+        "calibrated": cal,
     }
 
     if not args.no_oracle:
@@ -244,6 +275,7 @@ def main():
 
 
 W_INF = 0x7FFFFFFF
+CAL_EPS = 0.005  # sample-relative loss target of the calibrated leg (Appendix A)
 
 
 def sweep(args, ps, sw, np, torch, dev):

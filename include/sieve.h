@@ -153,6 +153,37 @@ SIEVE_API int sieve_search_fixed(const sieve_index* idx, const void* queries, in
                                  sieve_stats* stats, void* stream);
 
 /*
+ * sieve_search_calibrated -- threshold search whose window W is chosen inside
+ * the call (Appendix A, Algorithm 3).  The sampled queries are searched with
+ * full probing (nprobe = min(nprobe_max, nlist)) and keep that result; the
+ * stop rule is replayed over their recorded per-partition outcomes: each
+ * neighbour of a sampled fixed-probe result has a required window, the
+ * smallest W whose stop-rule prefix reaches the partition where it was found,
+ * and the chosen W is the smallest W < n whose sample-relative loss
+ * 1 - (neighbours with required window <= W) / (all neighbours) is < eps,
+ * else n (full probing).  Every other query is then searched with lookahead
+ * and the chosen W.  A sample without any neighbour (or ns = 0) uses
+ * W_fallback.
+ *   sample       [ns] int32 distinct query indices in [0, nq) (device); the
+ *                caller draws them (uniformly without replacement in the
+ *                paper).  ns <= 2^20.  Checked on a host copy (SIEVE_EINVAL).
+ *   eps          sample-relative loss target, 0 < eps <= 1 (e.g. 0.005).
+ *   W_fallback   >= 1, used when the sample has no neighbour.
+ *   out_W        HOST pointer: receives the window used for the rest.
+ * Other arguments and outputs as for sieve_search (out_probes of a sampled
+ * query is min(nprobe_max, nlist)).  stats (if given) are the sums over the
+ * two searches, the fixed-probe sample and the lookahead rest (nprobe_eff:
+ * min(nprobe_max, nlist)).  Calls that overlap on one index race, as for
+ * every search.
+ */
+SIEVE_API int sieve_search_calibrated(const sieve_index* idx, const void* queries, int64_t nq,
+                                      const int64_t* exclude_ids, int32_t k, float tau,
+                                      int32_t nprobe_max, const int32_t* sample, int64_t ns,
+                                      float eps, int32_t W_fallback, int64_t* out_ids,
+                                      float* out_scores, int32_t* out_probes, int32_t* out_W,
+                                      sieve_stats* stats, void* stream);
+
+/*
  * sieve_rank -- the probe order alone (Sec. 4.1): for each query, the first
  * min(nprobe, nlist) centroid indices by inner product, descending, ties to
  * the lower index, decided in fp64 (see the conventions above).

@@ -70,6 +70,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sieve_search_fixed.restype = ctypes.c_int
     lib.sieve_search_fixed.argtypes = [P, P, i64, P, i32, ctypes.c_float, i32, P, P, P,
                                        ctypes.POINTER(Stats), P]
+    lib.sieve_search_calibrated.restype = ctypes.c_int
+    lib.sieve_search_calibrated.argtypes = [P, P, i64, P, i32, ctypes.c_float, i32, P, i64,
+                                            ctypes.c_float, i32, P, P, P,
+                                            ctypes.POINTER(ctypes.c_int32),
+                                            ctypes.POINTER(Stats), P]
     lib.sieve_rank.restype = ctypes.c_int
     lib.sieve_rank.argtypes = [P, P, i64, i32, P, P]
     lib.sieve_free_index.restype = None
@@ -184,6 +189,29 @@ class Index:
                 osc.data_ptr(), op.data_ptr(), ctypes.byref(st) if st is not None else None,
                 _stream(stream)))
         return (oi, osc, op, st) if with_stats else (oi, osc, op)
+
+    def search_calibrated(self, queries: torch.Tensor, exclude_ids: Optional[torch.Tensor],
+                          k: int, tau: float, nprobe_max: int, sample: torch.Tensor,
+                          eps: float, W_fallback: int = 8, with_stats: bool = False,
+                          stream=None):
+        """Search whose window is chosen in the call from a fully probed sample
+        (Appendix A, Algorithm 3).  sample: distinct int32 query indices on the
+        queries' device.  Returns (ids, scores, probes, W[, Stats])."""
+        queries, ex, nq, oi, osc, op = self._prep(queries, exclude_ids, k)
+        smp = _dev(sample.to(torch.int32), "sample").reshape(-1)
+        if smp.device != queries.device:
+            raise ValueError("sample must be on the queries' device")
+        st = Stats() if with_stats else None
+        w = ctypes.c_int32(0)
+        with torch.cuda.device(self.device):
+            _check(self._lib, self._lib.sieve_search_calibrated(
+                self._h, queries.data_ptr(), nq, None if ex is None else ex.data_ptr(), int(k),
+                float(tau), int(nprobe_max), smp.data_ptr() if smp.numel() else None,
+                int(smp.numel()), float(eps), int(W_fallback), oi.data_ptr(), osc.data_ptr(),
+                op.data_ptr(), ctypes.byref(w), ctypes.byref(st) if st is not None else None,
+                _stream(stream)))
+        out = (oi, osc, op, int(w.value))
+        return out + (st,) if with_stats else out
 
     def search_fixed(self, queries: torch.Tensor, exclude_ids: Optional[torch.Tensor], k: int,
                      tau: float, nprobe: int, with_stats: bool = False, stream=None):

@@ -17,7 +17,8 @@ CSRC = os.path.join(HERE, "csrc")
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libsieve.so")
 BUILD_DIR = os.path.join(HERE, "_build")
-SOURCES = ["api.hip", "rank.hip", "rank_prefix.hip", "sched.hip", "scan.hip", "topk.hip"]
+SOURCES = ["api.hip", "rank.hip", "rank_prefix.hip", "sched.hip", "scan.hip", "topk.hip",
+           "calib.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -92,7 +92,7 @@ struct sieve_index {
   // workspace, grown on demand
   Buf scores, P, items, bucket, tiles, cnt, item_off, cursor, tile_off, rc, state_a, state_b,
       lmax, hcount, hoff, hcur, scan_tmp, pool, pool_sorted, arenas, have, ext, qext, Pext,
-      cand, ccount;
+      cand, ccount, cal_idx, cal_q, cal_x, cal_bits, cal_rank, cal_hist;
   int64_t pool_cap = 0;
   RoundCounters* rc_host = nullptr;
   // phase timing (only when stats are requested): events are recorded on the
@@ -354,9 +354,21 @@ int run_round(sieve_index* ix, const ScanArgs& sa, int n_items, int64_t q0, cons
   return SIEVE_OK;
 }
 
+// Extra outputs of the fixed-probe sample search of a calibrated call: per
+// query a bitmap of the ranks whose probe had a candidate, and the rank each
+// returned neighbour was found at.
+struct CalibOut {
+  uint32_t* hitbits;
+  int32_t words;
+  int32_t* frank;
+};
+
+// out_map: null, or [nq] output row of each query.  cal: null, or the
+// calibration outputs (then nq < kCalibMaxSample).
 int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t* exclude,
-                SearchPlan pl, int64_t* out_ids, float* out_scores, int32_t* out_probes,
-                sieve_stats* stats, hipStream_t s) {
+                SearchPlan pl, const int32_t* out_map, int64_t* out_ids, float* out_scores,
+                int32_t* out_probes, sieve_stats* stats, hipStream_t s,
+                const CalibOut* cal = nullptr) {
   int st;
   int dev = 0;
   HIP_TRY(hipGetDevice(&dev));
@@ -379,12 +391,17 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     ScanArgs sa = sa0;
     sa.pool = (Hit*)ix->pool.p;
     sa.pool_cap = ix->pool_cap;
+    if (cal) {
+      sa.hitbits = cal->hitbits;
+      sa.hit_words = cal->words;
+    }
 
     const int t_begin = mark(ix, timed, s);
     HIP_TRY(launch_zero_bytes(rc, sizeof(RoundCounters), s));
     HIP_TRY(launch_zero_bytes(ix->arenas.p, (size_t)pl.scan_grid * sizeof(ArenaRec), s));
     HIP_TRY(launch_fill_i32((int32_t*)ix->cnt.p, ix->nlist, 0, s));
     HIP_TRY(launch_fill_i32((int32_t*)ix->hcount.p, nq, 0, s));
+    if (cal) HIP_TRY(launch_zero_bytes(cal->hitbits, (size_t)nq * cal->words * 4, s));
     int32_t* P = (int32_t*)ix->P.p;
 
     if (pl.mode != 2) {
@@ -484,13 +501,13 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     HIP_TRY(launch_exclusive_scan((const int32_t*)ix->hcount.p, (int32_t*)ix->hoff.p,
                                   (int32_t*)ix->hcur.p, nq, (int32_t*)ix->scan_tmp.p, s));
     HIP_TRY(launch_pool_scatter((const Hit*)ix->pool.p, hits, (int32_t*)ix->hcur.p,
-                                (Hit*)ix->pool_sorted.p, s));
+                                (Hit*)ix->pool_sorted.p, cal != nullptr, s));
     const int32_t* probes_src = pl.mode == 0   ? (const int32_t*)ix->state_a.p
                                 : pl.mode == 1 ? (const int32_t*)ix->state_b.p
                                                : nullptr;
     HIP_TRY(launch_topk(nq, pl.k, (const Hit*)ix->pool_sorted.p, (const int32_t*)ix->hoff.p,
-                        (const int32_t*)ix->hcount.p, probes_src, pl.n, out_ids, out_scores,
-                        out_probes, rc, s));
+                        (const int32_t*)ix->hcount.p, probes_src, pl.n, out_map, out_ids,
+                        out_scores, out_probes, cal ? cal->frank : nullptr, rc, s));
     const int f1 = mark(ix, timed, s);
     span(ix, kFinal, f0, f1);
     span(ix, kTotal, t_begin, f1);
@@ -569,6 +586,26 @@ int plan_search(const sieve_index* ix, int64_t nq, int32_t k, float tau, int32_t
   }
   if (pl->item_cap < 1) pl->item_cap = 1;
   return SIEVE_OK;
+}
+
+void add_stats(sieve_stats* acc, const sieve_stats& x) {
+  acc->rounds += x.rounds;
+  acc->scan_launches += x.scan_launches;
+  acc->pool_retries += x.pool_retries;
+  acc->items += x.items;
+  acc->probes_total += x.probes_total;
+  acc->vectors_scanned += x.vectors_scanned;
+  acc->list_loads += x.list_loads;
+  acc->hits += x.hits;
+  acc->scan_bytes += x.scan_bytes;
+  acc->scan_flops += x.scan_flops;
+  acc->rank_flops += x.rank_flops;
+  acc->ms_rank += x.ms_rank;
+  acc->ms_sched += x.ms_sched;
+  acc->ms_scan += x.ms_scan;
+  acc->ms_update += x.ms_update;
+  acc->ms_finalize += x.ms_finalize;
+  acc->ms_total += x.ms_total;
 }
 
 }  // namespace
@@ -666,7 +703,8 @@ SIEVE_API void sieve_free_index(sieve_index* ix) {
                  &ix->item_off, &ix->cursor, &ix->tile_off, &ix->rc, &ix->state_a,
                  &ix->state_b, &ix->lmax, &ix->hcount, &ix->hoff, &ix->hcur, &ix->scan_tmp,
                  &ix->pool, &ix->pool_sorted, &ix->arenas, &ix->have, &ix->ext, &ix->qext,
-                 &ix->Pext, &ix->cand, &ix->ccount};
+                 &ix->Pext, &ix->cand, &ix->ccount, &ix->cal_idx, &ix->cal_q, &ix->cal_x,
+                 &ix->cal_bits, &ix->cal_rank, &ix->cal_hist};
   for (Buf* b : bufs)
     if (b->p) (void)hipFree(b->p);
   if (ix->vectors) (void)hipFree(ix->vectors);
@@ -697,8 +735,8 @@ SIEVE_API int sieve_search(const sieve_index* idx, const void* queries, int64_t 
     if (stats) stats->nprobe_eff = pl.n;
     return SIEVE_OK;
   }
-  return search_impl(ix, queries, nq, exclude_ids, pl, out_ids, out_scores, out_probes, stats,
-                     (hipStream_t)stream);
+  return search_impl(ix, queries, nq, exclude_ids, pl, nullptr, out_ids, out_scores, out_probes,
+                     stats, (hipStream_t)stream);
 }
 
 SIEVE_API int sieve_rank(const sieve_index* idx, const void* queries, int64_t nq, int32_t nprobe,
@@ -755,8 +793,123 @@ SIEVE_API int sieve_search_fixed(const sieve_index* idx, const void* queries, in
     if (stats) stats->nprobe_eff = pl.n;
     return SIEVE_OK;
   }
-  return search_impl(ix, queries, nq, exclude_ids, pl, out_ids, out_scores, out_probes, stats,
-                     (hipStream_t)stream);
+  return search_impl(ix, queries, nq, exclude_ids, pl, nullptr, out_ids, out_scores, out_probes,
+                     stats, (hipStream_t)stream);
+}
+
+SIEVE_API int sieve_search_calibrated(const sieve_index* idx, const void* queries, int64_t nq,
+                                      const int64_t* exclude_ids, int32_t k, float tau,
+                                      int32_t nprobe_max, const int32_t* sample, int64_t ns,
+                                      float eps, int32_t W_fallback, int64_t* out_ids,
+                                      float* out_scores, int32_t* out_probes, int32_t* out_W,
+                                      sieve_stats* stats, void* stream) {
+  g_err.clear();
+  int st = check_common(idx, queries, nq, k, tau, out_ids, out_scores, out_probes);
+  if (st) return st;
+  if (nprobe_max < 1) return fail(SIEVE_EINVAL, "nprobe_max = %d must be >= 1", nprobe_max);
+  if (!(eps > 0.f && eps <= 1.f)) return fail(SIEVE_EINVAL, "eps = %g outside (0, 1]", (double)eps);
+  if (W_fallback < 1) return fail(SIEVE_EINVAL, "W_fallback = %d must be >= 1", W_fallback);
+  if (!out_W) return fail(SIEVE_EINVAL, "out_W is NULL");
+  if (ns < 0 || ns > nq) return fail(SIEVE_EINVAL, "ns = %lld outside [0, nq]", (long long)ns);
+  if (ns > kCalibMaxSample)
+    return fail(SIEVE_EUNSUPPORTED, "ns = %lld exceeds %d", (long long)ns, kCalibMaxSample);
+  if (ns > 0 && !sample) return fail(SIEVE_EINVAL, "sample is NULL with ns > 0");
+  sieve_index* ix = const_cast<sieve_index*>(idx);
+  SearchPlan pf;
+  if ((st = plan_search(ix, ns, k, tau, SIEVE_W_INF, nprobe_max, 2, &pf))) return st;
+  if (stats) {
+    memset(stats, 0, sizeof(*stats));
+    stats->nprobe_eff = pf.n;
+  }
+  if (nq == 0) {
+    *out_W = W_fallback;
+    return SIEVE_OK;
+  }
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev != ix->device)
+    return fail(SIEVE_EINVAL, "current device %d differs from the index's device %d", dev,
+                ix->device);
+  hipStream_t s = (hipStream_t)stream;
+  const int64_t nr = nq - ns;
+  const int64_t row_bytes = (int64_t)ix->d * elem_bytes(ix->dtype);
+
+  // Output rows: the sample as given, then every other query in order.
+  std::vector<int32_t> rows((size_t)nq);
+  if (ns > 0) {
+    HIP_TRY(hipMemcpyAsync(rows.data(), sample, (size_t)ns * 4, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    std::vector<uint8_t> seen((size_t)nq, 0);
+    for (int64_t i = 0; i < ns; ++i) {
+      const int32_t q = rows[(size_t)i];
+      if (q < 0 || q >= nq)
+        return fail(SIEVE_EINVAL, "sample[%lld] = %d outside [0, nq)", (long long)i, q);
+      if (seen[(size_t)q]) return fail(SIEVE_EINVAL, "sample index %d appears twice", q);
+      seen[(size_t)q] = 1;
+    }
+    int64_t j = ns;
+    for (int64_t q = 0; q < nq; ++q)
+      if (!seen[(size_t)q]) rows[(size_t)j++] = (int32_t)q;
+  }
+  const int64_t gather_rows = ns > 0 ? std::max(ns, nr) : 0;
+  if ((st = ensure(ix->cal_idx, (size_t)nq * 4)) ||
+      (st = ensure(ix->cal_q, (size_t)gather_rows * row_bytes)) ||
+      (exclude_ids && (st = ensure(ix->cal_x, (size_t)gather_rows * 8))))
+    return st;
+  if (ns > 0)
+    HIP_TRY(hipMemcpyAsync(ix->cal_idx.p, rows.data(), (size_t)nq * 4, hipMemcpyHostToDevice, s));
+  const int32_t* d_rows = (const int32_t*)ix->cal_idx.p;
+  void* gq = ix->cal_q.p;
+  int64_t* gx = exclude_ids ? (int64_t*)ix->cal_x.p : nullptr;
+
+  // 1. Fixed-probe search of the sample, recording per-rank outcomes.
+  int W = W_fallback;
+  sieve_stats part;
+  if (ns > 0) {
+    const int32_t words = (pf.n + 31) / 32;
+    if ((st = ensure(ix->cal_bits, (size_t)ns * words * 4)) ||
+        (st = ensure(ix->cal_rank, (size_t)ns * k * 4)) ||
+        (st = ensure(ix->cal_hist, (size_t)(pf.n + 3) * 8)))
+      return st;
+    HIP_TRY(launch_gather_rows(d_rows, (int32_t)ns, queries, row_bytes, gq, s));
+    if (gx) HIP_TRY(launch_gather_i64(d_rows, ns, exclude_ids, gx, s));
+    const CalibOut co = {(uint32_t*)ix->cal_bits.p, words, (int32_t*)ix->cal_rank.p};
+    if ((st = search_impl(ix, gq, ns, gx, pf, d_rows, out_ids, out_scores, out_probes,
+                          stats ? &part : nullptr, s, &co)))
+      return st;
+    if (stats) add_stats(stats, part);
+    // 2. Replay the stop rule over the recorded outcomes; choose W.
+    //    cal_hist: H[0..n], then the neighbour count Z, then the chosen W.
+    unsigned long long* hist = (unsigned long long*)ix->cal_hist.p;
+    unsigned long long* z = hist + pf.n + 1;
+    int32_t* d_w = (int32_t*)(hist + pf.n + 2);
+    HIP_TRY(launch_zero_bytes(hist, (int64_t)(pf.n + 3) * 8, s));
+    HIP_TRY(launch_calib_replay(ns, pf.n, k, co.hitbits, words, co.frank, hist, z, s));
+    HIP_TRY(launch_calib_choose(pf.n, eps, hist, z, d_w, s));
+    int32_t w = 0;
+    HIP_TRY(hipMemcpyAsync(&w, d_w, 4, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    if (w > 0) W = w;
+  }
+  *out_W = W;
+
+  // 3. Lookahead search of every other query with the chosen window.
+  if (nr > 0) {
+    SearchPlan pr;
+    if ((st = plan_search(ix, nr, k, tau, W, nprobe_max, 0, &pr))) return st;
+    if (ns == 0) {
+      st = search_impl(ix, queries, nq, exclude_ids, pr, nullptr, out_ids, out_scores, out_probes,
+                       stats ? &part : nullptr, s);
+    } else {
+      HIP_TRY(launch_gather_rows(d_rows + ns, (int32_t)nr, queries, row_bytes, gq, s));
+      if (gx) HIP_TRY(launch_gather_i64(d_rows + ns, nr, exclude_ids, gx, s));
+      st = search_impl(ix, gq, nr, gx, pr, d_rows + ns, out_ids, out_scores, out_probes,
+                       stats ? &part : nullptr, s);
+    }
+    if (st) return st;
+    if (stats) add_stats(stats, part);
+  }
+  return SIEVE_OK;
 }
 
 }  // extern "C"

@@ -278,7 +278,7 @@ __global__ __launch_bounds__(kNT, kNT == kScanThreads ? 2 : 1) void scan_kernel(
                   if ((int64_t)slot < a.pool_cap) {
                     Hit hv;
                     hv.score = sc;
-                    hv.q = sq[i];
+                    hv.q = a.hitbits ? (sq[i] | (srank[i] << kRankShift)) : sq[i];
                     hv.id = rid;
                     a.pool[slot] = hv;
                   }
@@ -297,6 +297,10 @@ __global__ __launch_bounds__(kNT, kNT == kScanThreads ? 2 : 1) void scan_kernel(
       const int q = sq[threadIdx.x];
       atomicAdd(&a.hcount[q], s_hits[threadIdx.x]);
       atomicMax(&a.lmax[q], srank[threadIdx.x] + 1);
+      if (a.hitbits) {
+        const int rk = srank[threadIdx.x];
+        atomicOr(&a.hitbits[(int64_t)q * a.hit_words + (rk >> 5)], 1u << (rk & 31));
+      }
       s_hits[threadIdx.x] = 0;
     }
     const bool refill = s_afall != 0;  // block-uniform: written before the barrier

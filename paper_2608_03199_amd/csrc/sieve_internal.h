@@ -98,6 +98,11 @@ struct ScanArgs {
   int32_t dynamic;             // 1: atomic work queue, 0: static strided schedule
   int32_t stage_u4;            // 16-byte slots per query staging buffer (set by the launcher)
   int32_t wide;                // 1: wide configuration (one big work-group per CU)
+  // calibration outputs (Algorithm 3), null / 0 otherwise: per query a bitmap
+  // of the ranks whose probe had a candidate, and pool entries that carry
+  // the rank they were found at (Hit.q = query | rank << kRankShift)
+  uint32_t* hitbits = nullptr;
+  int32_t hit_words = 0;       // 32-bit words per query in hitbits
   float tau;
 };
 
@@ -171,11 +176,30 @@ hipError_t launch_exclusive_scan(const int32_t* in, int32_t* out, int32_t* out_c
 size_t exclusive_scan_tmp_elems(int64_t n);
 hipError_t launch_retire_arenas(const ArenaRec* arenas, int32_t n, Hit* pool, int64_t pool_cap,
                                 hipStream_t s);
+// Pool entries of a calibration search pack the rank into Hit.q.
+constexpr int kRankShift = 20;  // queries < 2^20, ranks < 2^11 (kMaxRanks)
+constexpr int32_t kQueryMask = (1 << kRankShift) - 1;
 hipError_t launch_pool_scatter(const Hit* pool, int64_t n, int32_t* cursor, Hit* sorted,
-                               hipStream_t s);
+                               bool packed, hipStream_t s);
+// out_map: null, or [nq] output row of each query (results of query q go to
+// row out_map[q] of out_ids / out_scores / out_probes).  out_rank: null, or
+// [nq * k] int32 (indexed by q, not mapped) receiving the 0-based rank each
+// returned candidate was found at (-1 for padding); needs packed pool entries.
 hipError_t launch_topk(int64_t nq, int32_t k, const Hit* sorted, const int32_t* hoff,
                        const int32_t* hcount, const int32_t* probes_src, int32_t probes_const,
-                       int64_t* out_ids, float* out_scores, int32_t* out_probes,
-                       RoundCounters* rc, hipStream_t s);
+                       const int32_t* out_map, int64_t* out_ids, float* out_scores,
+                       int32_t* out_probes, int32_t* out_rank, RoundCounters* rc, hipStream_t s);
+// ---- in-call window calibration (Algorithm 3) ----
+hipError_t launch_gather_i64(const int32_t* idx, int64_t n, const int64_t* src, int64_t* dst,
+                             hipStream_t s);
+// Required-window histogram hist[0..n] (hist[W]: neighbours whose required
+// window is W) and their total z, from ns sampled queries' rank bitmaps and
+// found ranks; then the chosen window into *w_out (0 when z = 0).
+hipError_t launch_calib_replay(int64_t ns, int32_t n, int32_t k, const uint32_t* hitbits,
+                               int32_t words, const int32_t* frank, unsigned long long* hist,
+                               unsigned long long* z, hipStream_t s);
+constexpr int kCalibMaxSample = 1 << kRankShift;
+hipError_t launch_calib_choose(int32_t n, float eps, const unsigned long long* hist,
+                               const unsigned long long* z, int32_t* w_out, hipStream_t s);
 
 }  // namespace sieve

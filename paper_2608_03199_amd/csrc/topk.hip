@@ -77,12 +77,13 @@ __global__ __launch_bounds__(kScanBlock) void scan_apply_kernel(const int32_t* i
 }
 
 __global__ void pool_scatter_kernel(const Hit* __restrict__ pool, int64_t n,
-                                    int32_t* __restrict__ cursor, Hit* __restrict__ sorted) {
+                                    int32_t* __restrict__ cursor, Hit* __restrict__ sorted,
+                                    int32_t qmask) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const Hit h = pool[i];
   if (h.q < 0) return;  // unused arena slot
-  const int pos = atomicAdd(&cursor[h.q], 1);
+  const int pos = atomicAdd(&cursor[h.q & qmask], 1);
   sorted[pos] = h;
 }
 
@@ -102,37 +103,43 @@ __global__ __launch_bounds__(256) void retire_arenas_kernel(const ArenaRec* __re
 struct Cand {
   float s;
   long long id;
+  int rank;  // carried only by the calibration variant of the top-k
 };
 
 __device__ __forceinline__ bool better(const Cand& a, const Cand& b) {
   return a.s > b.s || (a.s == b.s && a.id < b.id);
 }
 
+template <bool kRank>
 __device__ __forceinline__ Cand shfl_xor_cand(const Cand& c, int m) {
   Cand o;
   o.s = __shfl_xor(c.s, m);
   const int lo = __shfl_xor((int)(c.id & 0xffffffffll), m);
   const int hi = __shfl_xor((int)(c.id >> 32), m);
   o.id = ((long long)hi << 32) | (unsigned int)lo;
+  o.rank = kRank ? __shfl_xor(c.rank, m) : 0;
   return o;
 }
 
+template <bool kRank>
 __device__ __forceinline__ Cand shfl_cand(const Cand& c, int src) {
   Cand o;
   o.s = __shfl(c.s, src);
   const int lo = __shfl((int)(c.id & 0xffffffffll), src);
   const int hi = __shfl((int)(c.id >> 32), src);
   o.id = ((long long)hi << 32) | (unsigned int)lo;
+  o.rank = kRank ? __shfl(c.rank, src) : 0;
   return o;
 }
 
 // Sort 64 lane-held candidates, best first.
+template <bool kRank>
 __device__ __forceinline__ Cand wave_sort_desc(Cand v, int lane) {
 #pragma unroll
   for (int k = 2; k <= 64; k <<= 1) {
 #pragma unroll
     for (int j = k >> 1; j > 0; j >>= 1) {
-      const Cand o = shfl_xor_cand(v, j);
+      const Cand o = shfl_xor_cand<kRank>(v, j);
       const bool lower = (lane & j) == 0;
       const bool desc = (lane & k) == 0;  // final stage: whole wave descending
       const bool keep_better = (lower == desc);
@@ -144,10 +151,11 @@ __device__ __forceinline__ Cand wave_sort_desc(Cand v, int lane) {
 }
 
 // Sort a bitonic 64-sequence, best first.
+template <bool kRank>
 __device__ __forceinline__ Cand wave_merge_desc(Cand v, int lane) {
 #pragma unroll
   for (int j = 32; j > 0; j >>= 1) {
-    const Cand o = shfl_xor_cand(v, j);
+    const Cand o = shfl_xor_cand<kRank>(v, j);
     const bool lower = (lane & j) == 0;
     const bool ob = better(o, v);
     if (lower ? ob : !ob) v = o;
@@ -156,7 +164,9 @@ __device__ __forceinline__ Cand wave_merge_desc(Cand v, int lane) {
 }
 
 // One wave per query, grid-stride over the queries; each block adds its
-// probe and candidate totals to the round counters once.
+// probe and candidate totals to the round counters once.  kRank: pool
+// entries carry their rank (calibration search); out_rank receives it.
+template <bool kRank>
 __global__ __launch_bounds__(256) void topk_kernel(int64_t nq, int32_t k,
                                                    const Hit* __restrict__ sorted,
                                                    const int32_t* __restrict__ hoff,
@@ -166,11 +176,13 @@ __global__ __launch_bounds__(256) void topk_kernel(int64_t nq, int32_t k,
                                                    int64_t* __restrict__ out_ids,
                                                    float* __restrict__ out_scores,
                                                    int32_t* __restrict__ out_probes,
+                                                   const int32_t* __restrict__ out_map,
+                                                   int32_t* __restrict__ out_rank,
                                                    RoundCounters* rc) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   __shared__ unsigned long long s_probes[4], s_cands[4];
   unsigned long long probes = 0, cands = 0;
-  const Cand none = {-INFINITY, 0x7fffffffffffffffll};
+  const Cand none = {-INFINITY, 0x7fffffffffffffffll, -1};
   for (int64_t q = (int64_t)blockIdx.x * 4 + wave; q < nq; q += (int64_t)gridDim.x * 4) {
     const int m = hcount[q];
     const int beg = m > 0 ? hoff[q] : 0;
@@ -181,23 +193,26 @@ __global__ __launch_bounds__(256) void topk_kernel(int64_t nq, int32_t k,
         const Hit h = sorted[beg + b + lane];
         c.s = h.score;
         c.id = h.id;
+        c.rank = kRank ? (h.q >> kRankShift) : 0;
       }
-      c = wave_sort_desc(c, lane);
+      c = wave_sort_desc<kRank>(c, lane);
       if (b == 0) {
         top = c;
       } else {
-        const Cand r = shfl_cand(c, 63 - lane);  // reversed: top ++ reverse(c) is bitonic
+        const Cand r = shfl_cand<kRank>(c, 63 - lane);  // reversed: top ++ reverse(c) is bitonic
         top = better(top, r) ? top : r;
-        top = wave_merge_desc(top, lane);
+        top = wave_merge_desc<kRank>(top, lane);
       }
     }
+    const int64_t row = out_map ? (int64_t)out_map[q] : q;
     if (lane < k) {
       const bool real = top.id != none.id;
-      out_ids[q * k + lane] = real ? (int64_t)top.id : -1;
-      out_scores[q * k + lane] = real ? top.s : -INFINITY;
+      out_ids[row * k + lane] = real ? (int64_t)top.id : -1;
+      out_scores[row * k + lane] = real ? top.s : -INFINITY;
+      if (kRank) out_rank[q * k + lane] = real ? top.rank : -1;
     }
     const int32_t p = probes_src ? probes_src[q] : probes_const;
-    if (lane == 0) out_probes[q] = p;
+    if (lane == 0) out_probes[row] = p;
     probes += (unsigned long long)p;
     cands += (unsigned long long)m;
   }
@@ -239,22 +254,28 @@ hipError_t launch_retire_arenas(const ArenaRec* arenas, int32_t n, Hit* pool, in
 }
 
 hipError_t launch_pool_scatter(const Hit* pool, int64_t n, int32_t* cursor, Hit* sorted,
-                               hipStream_t s) {
+                               bool packed, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(pool_scatter_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, pool,
-                     n, cursor, sorted);
+                     n, cursor, sorted, packed ? kQueryMask : (int32_t)0x7fffffff);
   return hipGetLastError();
 }
 
 hipError_t launch_topk(int64_t nq, int32_t k, const Hit* sorted, const int32_t* hoff,
                        const int32_t* hcount, const int32_t* probes_src, int32_t probes_const,
-                       int64_t* out_ids, float* out_scores, int32_t* out_probes,
-                       RoundCounters* rc, hipStream_t s) {
+                       const int32_t* out_map, int64_t* out_ids, float* out_scores,
+                       int32_t* out_probes, int32_t* out_rank, RoundCounters* rc, hipStream_t s) {
   if (nq <= 0) return hipSuccess;
   const int64_t want = (nq + 3) / 4;
   const unsigned blocks = (unsigned)(want < 4096 ? want : 4096);
-  hipLaunchKernelGGL(topk_kernel, dim3(blocks), dim3(256), 0, s, nq, k, sorted,
-                     hoff, hcount, probes_src, probes_const, out_ids, out_scores, out_probes, rc);
+  if (out_rank)
+    hipLaunchKernelGGL(topk_kernel<true>, dim3(blocks), dim3(256), 0, s, nq, k, sorted, hoff,
+                       hcount, probes_src, probes_const, out_ids, out_scores, out_probes,
+                       out_map, out_rank, rc);
+  else
+    hipLaunchKernelGGL(topk_kernel<false>, dim3(blocks), dim3(256), 0, s, nq, k, sorted, hoff,
+                       hcount, probes_src, probes_const, out_ids, out_scores, out_probes,
+                       out_map, nullptr, rc);
   return hipGetLastError();
 }
 

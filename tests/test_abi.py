@@ -28,8 +28,8 @@ def declared_symbols():
 
 def test_header_declares_the_boundary():
     syms = declared_symbols()
-    for s in ("sieve_load_index", "sieve_search", "sieve_search_fixed", "sieve_free_index",
-              "sieve_last_error"):
+    for s in ("sieve_load_index", "sieve_search", "sieve_search_fixed", "sieve_search_calibrated",
+              "sieve_free_index", "sieve_last_error"):
         assert s in syms
 
 
@@ -67,6 +67,10 @@ def test_argument_errors_without_a_gpu(lib):
     assert rc == -1 and b"NULL" in lib.sieve_last_error()
     rc = lib.sieve_search_fixed(None, None, 0, None, 10, 0.9, 32, None, None, None, None, None)
     assert rc == -1
+    w = ctypes.c_int32(-7)
+    rc = lib.sieve_search_calibrated(None, None, 0, None, 10, 0.9, 32, None, 0, 0.005, 8, None,
+                                     None, None, ctypes.byref(w), None, None)
+    assert rc == -1 and w.value == -7
     h = ctypes.c_void_p()
     rc = lib.sieve_load_index(None, 0, 10, 64, None, 4, None, None, None, ctypes.byref(h))
     assert rc == -1 and h.value is None

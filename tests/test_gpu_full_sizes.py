@@ -99,3 +99,50 @@ def test_full_10m_d768_f16():
 
 def test_full_100m_d128_f16():
     _run("c5", n_sample=64, n_fixed_sample=8, check_identities=False)
+
+
+def test_full_1m_d128_f32_calibrated():
+    """In-call calibration on the whole 10,000-query batch with a 2% sample:
+    the chosen window equals the oracle's replay of the sample, the sampled
+    queries keep the oracle's fixed-probe result and a seeded sample of the
+    rest matches the oracle's search with that window."""
+    import paper_2608_03199_amd as ps
+    spec = sw.SPECS["c2"]
+    print("[gpu-test] generating c2", flush=True)
+    w = sw.make(spec, device="cuda")
+    ix = ps.Index(w.vectors, w.list_offsets, w.ids, w.centroids)
+    try:
+        rng = np.random.default_rng(spec.seed + 777)
+        smp = np.sort(rng.choice(spec.nq, spec.nq // 50, replace=False)).astype(np.int32)
+        eps = float(np.float32(0.005))
+        ids, sc, pr, W = ix.search_calibrated(w.queries, w.exclude_ids, spec.k, spec.tau,
+                                              spec.nprobe_max, torch.from_numpy(smp).cuda(), eps)
+        ids, sc, pr = ids.cpu().numpy(), sc.cpu().numpy(), pr.cpu().numpy()
+        h = _host_sample(w, smp)
+        print(f"[gpu-test] c2 calibrated: W={W}; oracle on the {smp.size} sampled queries",
+              flush=True)
+        of = oracle.search(h["vectors"], h["list_offsets"], h["ids"], h["centroids"],
+                           h["queries"], h["exclude_ids"], spec.k, spec.tau, oracle.W_INF,
+                           spec.nprobe_max, oracle.MODE_A, NTHREADS, want_hitseq=True)
+        w_or, _, z = oracle.calibrate(of.hitseq, of.rank, eps)
+        want = 8 if w_or is None else w_or
+        edge = int((of.flags & oracle.FLAG_TAU_EDGE).astype(bool).sum())
+        print(f"[gpu-test] c2 calibrated: oracle W={want} z={z} tau_edge={edge}", flush=True)
+        if edge == 0:
+            assert W == want
+        rep = compare(ids[smp], sc[smp], pr[smp], of)
+        print(f"[gpu-test] c2 calibrated sample -> {rep}", flush=True)
+        assert_parity(rep)
+        rest = np.setdiff1d(np.arange(spec.nq), smp)
+        sel = np.sort(rng.choice(rest, 300, replace=False))
+        hr = _host_sample(w, sel)
+        orr = oracle.search(hr["vectors"], hr["list_offsets"], hr["ids"], hr["centroids"],
+                            hr["queries"], hr["exclude_ids"], spec.k, spec.tau, W,
+                            spec.nprobe_max, oracle.MODE_A, NTHREADS)
+        rep = compare(ids[sel], sc[sel], pr[sel], orr)
+        print(f"[gpu-test] c2 calibrated rest sample -> {rep}", flush=True)
+        assert_parity(rep)
+    finally:
+        ix.close()
+        del w
+        torch.cuda.empty_cache()
