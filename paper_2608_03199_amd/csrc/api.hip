@@ -172,9 +172,12 @@ int env_int(const char* name, int dflt) {
 }
 
 int row_chunk_for(const sieve_index* ix) {
-  (void)ix;
-  const int rc = env_int("SIEVE_ROW_CHUNK", 512);
-  return ((rc + 63) / 64) * 64;
+  // the scan addresses a tile's rows with 32-bit byte offsets
+  const int64_t row_bytes = (int64_t)ix->d * elem_bytes(ix->dtype);
+  const int64_t lim = ((int64_t)INT32_MAX / row_bytes) / 64 * 64;
+  int64_t rc = env_int("SIEVE_ROW_CHUNK", 512);
+  rc = ((rc + 63) / 64) * 64;
+  return (int)std::max<int64_t>(64, std::min(rc, lim));
 }
 
 int scan_grid(const sieve_index* ix, int tile_q) {

@@ -162,40 +162,6 @@ __device__ __forceinline__ void score_regs(const u32x4* __restrict__ lds, int se
   }
 }
 
-// Two row blocks against the same staged queries: every query fragment read
-// from LDS feeds two MFMAs, which halves the LDS traffic per flop (the limit
-// of the fp16 path with many query blocks).  Same chunk order per output as
-// score_regs, so the same bits.
-template <int DT, int D, int QB>
-__device__ __forceinline__ void score_regs2(const u32x4* __restrict__ lds, int segs,
-                                            const u32x4 (&b0)[D / DTraits<DT>::kChunkDims],
-                                            const u32x4 (&b1)[D / DTraits<DT>::kChunkDims],
-                                            f32x4 (&acc0)[QB], f32x4 (&acc1)[QB]) {
-  constexpr int kNC = D / DTraits<DT>::kChunkDims;
-  constexpr int kN = kNC * QB;  // (chunk, query block) steps, chunk-major
-  constexpr int kAhead = 3;     // query fragments in flight from LDS
-  const int lane = threadIdx.x & 63;
-  const int h = lane >> 4, r16 = lane & 15;
-  const u32x4* arow = lane_arow(lds, segs);
-  auto frag = [&](int t) { return arow[(t % QB) * 16 * segs + 4 * (t / QB)]; };
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    acc0[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    acc1[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-  u32x4 a[kAhead + 1];
-#pragma unroll
-  for (int t = 0; t < kAhead && t < kN; ++t) a[t] = frag(t);
-#pragma unroll
-  for (int t = 0; t < kN; ++t) {
-    if (t + kAhead < kN) a[(t + kAhead) % (kAhead + 1)] = frag(t + kAhead);
-    const int qb = t % QB, c = t / QB;
-    acc0[qb] = mma_chunk<DT>(a[t % (kAhead + 1)], b0[c], acc0[qb]);
-    acc1[qb] = mma_chunk<DT>(a[t % (kAhead + 1)], b1[c], acc1[qb]);
-    __builtin_amdgcn_sched_barrier(0);
-  }
-}
-
 // Runtime-dimension variant: fragments are loaded chunk by chunk (one ahead).
 template <int DT, int QB>
 __device__ __forceinline__ void score_stream(const u32x4* __restrict__ lds, const RowGeom<DT>& g,
@@ -270,12 +236,33 @@ constexpr int ring_depth() {
   return nb < 2 ? 2 : (nb > 6 ? 6 : nb);
 }
 
-// Pairs of row blocks (score_regs2) where the LDS reads of query fragments
-// would bound the MFMA rate: fp16 rows of at most 8 chunks, 3+ query blocks.
-template <int DT, int D, int QB>
-constexpr bool pair_mode() {
-  constexpr int kNC = D / DTraits<DT>::kChunkDims;
-  return DT == SIEVE_F16 && kNC > 0 && kNC <= kSliceChunks && QB >= 3;
+// s_waitcnt immediate (gfx9 encoding): vmcnt(0), expcnt and lgkmcnt not waited.
+constexpr int kWaitVmcnt0 = 0x0F70;
+
+// The rows [r0, r1) a stream reads, addressed as a uniform base (row r0)
+// plus a 32-bit per-lane byte offset, so that loads take the scalar-base
+// form and row arithmetic stays 32-bit.  Callers keep (r1 - r0) * row_bytes
+// below 2^31.  Row blocks past the end re-read the last row: every load is
+// issued unconditionally, so the load sequence never depends on control flow
+// and the compiler's wait counts stay exact.
+struct RowStream {
+  const char* base;   // row r0
+  int nrows;          // r1 - r0
+  uint32_t rb;        // row bytes
+  __device__ __forceinline__ uint32_t lane_row(int blk) const {
+    const int rl = blk * 16 + (int)(threadIdx.x & 15);
+    return (uint32_t)(rl < nrows ? rl : nrows - 1);
+  }
+  // this lane's 16-byte segment of chunk 0 of row block blk
+  __device__ __forceinline__ const char* seg_ptr(int blk) const {
+    return base + (lane_row(blk) * rb + ((threadIdx.x >> 4) & 3u) * 16u);
+  }
+};
+
+// Index of this wave in the work-group, as a uniform (scalar) value: the row
+// loops below then run on scalar branches and scalar counters.
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
 }
 
 // Sliced variant of stream_rows_qb (see there) for kNC > kSliceChunks.  The
@@ -284,49 +271,44 @@ constexpr bool pair_mode() {
 // unrolled per iteration so that buffer indices are compile-time constants.
 // Chunks are accumulated in the same order as in the unsliced variant, so
 // scores are bit-identical.
-template <int DT, int D, int QB, int Reserve, bool kIds, typename Epi>
+template <int DT, int D, int QB, int Reserve, typename Epi>
 __device__ __forceinline__ void stream_rows_sliced(const u32x4* __restrict__ lds,
-                                                   const RowGeom<DT>& g,
-                                                   const char* __restrict__ base,
-                                                   size_t row_bytes,
-                                                   const int64_t* __restrict__ ids, int64_t r0,
-                                                   int64_t r1, Epi& epi) {
+                                                   const RowGeom<DT>& g, const RowStream& rs,
+                                                   int64_t r0, Epi& epi) {
   constexpr int kNC = D / DTraits<DT>::kChunkDims;
   constexpr int kNS = (kNC + kSliceChunks - 1) / kSliceChunks;  // slices per row block
   constexpr int NB = ring_depth<DT, D, QB, Reserve>();
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wave = wave_id();
   const int nwaves = blockDim.x >> 6;
-  const int h = lane >> 4, r16 = lane & 15;
-  const int64_t nrows = r1 - r0;
-  const u32x4* arow = lane_arow(lds, g.segs);
-  auto rowc_of = [&](int64_t blk) {
-    const int64_t row = r0 + blk * 16 + r16;
-    return row < r1 ? row : r1 - 1;  // clamped: loads stay unconditional
-  };
-  auto load = [&](int64_t blk, int s, u32x4(&dst)[kSliceChunks]) {
-    const u32x4* vrow = (const u32x4*)(base + (size_t)rowc_of(blk) * row_bytes) + h;
+  const int r16 = threadIdx.x & 15;
+  const int nrows = rs.nrows;
+  auto load = [&](int blk, int s, u32x4(&dst)[kSliceChunks]) {
+    const char* p = rs.seg_ptr(blk);
 #pragma unroll
     for (int c = 0; c < kSliceChunks; ++c)
-      if (s * kSliceChunks + c < kNC) dst[c] = vrow[4 * (s * kSliceChunks + c)];
+      if (s * kSliceChunks + c < kNC)
+        dst[c] = *(const u32x4*)(p + 64 * (s * kSliceChunks + c));
   };
   u32x4 buf[NB][kSliceChunks];
-  int64_t rb = wave;
+  int rb = wave;
   if (nrows <= 0) return;
-  // Prefetches are issued unconditionally (past the end they re-read the
-  // clamped last row): the load sequence then never depends on control
-  // flow, and the compiler's wait counts stay exact.
 #pragma unroll
   for (int u = 0; u < NB - 1; ++u) load(rb + (u / kNS) * nwaves, u % kNS, buf[u]);
+  // Nothing issued before the stream (staging copies, record loads, queue
+  // atomics) stays in flight inside it: mixed kinds of pending memory
+  // operations would make every wait below a wait for all of them.  (The
+  // fences keep the scheduler from moving the prefetch below the wait.)
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+  __builtin_amdgcn_sched_barrier(0);
   f32x4 acc[QB];
-  int64_t rid = 0;
   for (;;) {
 #pragma unroll
     for (int u = 0; u < NB * kNS; ++u) {
       const int s = u % kNS;
-      const int64_t blk = rb + (u / kNS) * nwaves;
+      const int blk = rb + (u / kNS) * nwaves;
       if (blk * 16 >= nrows) return;
       if (s == 0) {
-        if constexpr (kIds) rid = ids[rowc_of(blk)];
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) acc[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
       }
@@ -335,8 +317,10 @@ __device__ __forceinline__ void stream_rows_sliced(const u32x4* __restrict__ lds
       // keep the prefetch above the MFMAs (the scheduler would otherwise sink
       // loads towards their use to save registers, serialising the stream)
       __builtin_amdgcn_sched_barrier(0);
-      mma_slice<DT, D, QB>(arow, g.segs, s, buf[u % NB], acc);
-      if (s == kNS - 1) epi(acc, r0 + blk * 16 + r16, rid);
+      // the fragment base is re-derived per slice: computed once, the loads
+      // from it would be loop-invariant and get hoisted (and spilled)
+      mma_slice<DT, D, QB>(lane_arow(lds, g.segs), g.segs, s, buf[u % NB], acc);
+      if (s == kNS - 1) epi(acc, r0 + blk * 16 + r16);
     }
     rb += NB * nwaves;
   }
@@ -345,110 +329,58 @@ __device__ __forceinline__ void stream_rows_sliced(const u32x4* __restrict__ lds
 // Stream rows [r0, r1) of a row-major store through the waves of the block:
 // wave w scores row blocks w, w + W, w + 2W, ... (W = waves per block)
 // against QB staged query blocks and hands each finished block to
-// epi(acc, row, rid), row = the stored row this lane's column holds (it may
-// be >= r1 on the last block: the epilogue masks it; loads are clamped) and
-// rid = ids[row] when an id array is given (else 0).  With a compile-time
-// dimension, two fragment buffers alternate so that the next block's
-// fragments (and ids) load while the current block is multiplied.
-template <int DT, int D, int QB, typename Epi, int Reserve = 0, bool kIds = true>
+// epi(acc, row), row = the stored row this lane's column holds (it may be
+// >= r1 on the last block: the epilogue masks it; loads are clamped).  With a
+// compile-time dimension, fragment buffers rotate so that the next blocks'
+// fragments load while the current block is multiplied.
+template <int DT, int D, int QB, typename Epi, int Reserve = 0>
 __device__ __forceinline__ void stream_rows_qb(const u32x4* __restrict__ lds,
                                                const RowGeom<DT>& g,
                                                const char* __restrict__ base, size_t row_bytes,
-                                               const int64_t* __restrict__ ids, int64_t r0,
-                                               int64_t r1, Epi& epi) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+                                               int64_t r0, int64_t r1, Epi& epi) {
+  const int wave = wave_id();
   const int nwaves = blockDim.x >> 6;
-  const int h = lane >> 4, r16 = lane & 15;
-  const int64_t nrows = r1 - r0;
+  const int r16 = threadIdx.x & 15;
+  const RowStream rs = {base + (size_t)r0 * row_bytes, (int)(r1 - r0), (uint32_t)row_bytes};
+  const int nrows = rs.nrows;
   constexpr int kNC = D / DTraits<DT>::kChunkDims;
   if constexpr (kNC > kSliceChunks) {
-    stream_rows_sliced<DT, D, QB, Reserve, kIds>(lds, g, base, row_bytes, ids, r0, r1, epi);
-  } else if constexpr (pair_mode<DT, D, QB>()) {
-    // super-block sb = row blocks 2 sb and 2 sb + 1; super-block sb + W loads
-    // while sb is multiplied
-    auto load = [&](int64_t blk, u32x4(&dst)[kNC], int64_t& rid) {
-      const int64_t row = r0 + blk * 16 + r16;
-      const int64_t rowc = row < r1 ? row : r1 - 1;
-      const u32x4* vrow = (const u32x4*)(base + (size_t)rowc * row_bytes) + h;
-#pragma unroll
-      for (int c = 0; c < kNC; ++c) dst[c] = vrow[4 * c];
-      if constexpr (kIds) rid = ids[rowc];
-    };
-    u32x4 p0[kNC], p1[kNC], q0[kNC], q1[kNC];
-    int64_t ip0 = 0, ip1 = 0, iq0 = 0, iq1 = 0;
-    int64_t sb = wave;
-    if (nrows <= 0) return;
-    // unconditional prefetches (clamped rows past the end): a fixed load
-    // sequence keeps the compiler's wait counts exact
-    load(2 * sb, p0, ip0);
-    load(2 * sb + 1, p1, ip1);
-    while (sb * 32 < nrows) {
-      int64_t nsb = sb + nwaves;
-      load(2 * nsb, q0, iq0);
-      load(2 * nsb + 1, q1, iq1);
-      __builtin_amdgcn_sched_barrier(0);  // prefetch stays above the MFMAs
-      {
-        f32x4 acc0[QB], acc1[QB];
-        score_regs2<DT, D, QB>(lds, g.segs, p0, p1, acc0, acc1);
-        epi(acc0, r0 + 2 * sb * 16 + r16, ip0);
-        if ((2 * sb + 1) * 16 < nrows) epi(acc1, r0 + (2 * sb + 1) * 16 + r16, ip1);
-      }
-      sb = nsb;
-      if (sb * 32 >= nrows) break;
-      nsb = sb + nwaves;
-      load(2 * nsb, p0, ip0);
-      load(2 * nsb + 1, p1, ip1);
-      __builtin_amdgcn_sched_barrier(0);
-      {
-        f32x4 acc0[QB], acc1[QB];
-        score_regs2<DT, D, QB>(lds, g.segs, q0, q1, acc0, acc1);
-        epi(acc0, r0 + 2 * sb * 16 + r16, iq0);
-        if ((2 * sb + 1) * 16 < nrows) epi(acc1, r0 + (2 * sb + 1) * 16 + r16, iq1);
-      }
-      sb = nsb;
-    }
+    stream_rows_sliced<DT, D, QB, Reserve>(lds, g, rs, r0, epi);
   } else if constexpr (kNC > 0) {
     // NB fragment buffers: block rb + (NB - 1) W loads while block rb is
     // multiplied; NB blocks are unrolled per iteration (compile-time indices)
     constexpr int NB = ring_depth<DT, D, QB, Reserve>();
-    auto load = [&](int64_t blk, u32x4(&dst)[kNC], int64_t& rid) {
-      const int64_t row = r0 + blk * 16 + r16;
-      const int64_t rowc = row < r1 ? row : r1 - 1;
-      const u32x4* vrow = (const u32x4*)(base + (size_t)rowc * row_bytes) + h;
+    auto load = [&](int blk, u32x4(&dst)[kNC]) {
+      const char* p = rs.seg_ptr(blk);
 #pragma unroll
-      for (int c = 0; c < kNC; ++c) dst[c] = vrow[4 * c];
-      if constexpr (kIds) rid = ids[rowc];
+      for (int c = 0; c < kNC; ++c) dst[c] = *(const u32x4*)(p + 64 * c);
     };
     u32x4 buf[NB][kNC];
-    int64_t rid[NB];
     if (nrows <= 0) return;
-    // unconditional prefetches (clamped rows past the end): a fixed load
-    // sequence keeps the compiler's wait counts exact
 #pragma unroll
-    for (int j = 0; j < NB - 1; ++j) load(wave + j * nwaves, buf[j], rid[j]);
-    int64_t rb = wave;
+    for (int j = 0; j < NB - 1; ++j) load(wave + j * nwaves, buf[j]);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);  // see stream_rows_sliced
+    __builtin_amdgcn_sched_barrier(0);
+    int rb = wave;
     for (;;) {
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
         if (rb * 16 >= nrows) return;
-        load(rb + (NB - 1) * nwaves, buf[(j + NB - 1) % NB], rid[(j + NB - 1) % NB]);
+        load(rb + (NB - 1) * nwaves, buf[(j + NB - 1) % NB]);
         __builtin_amdgcn_sched_barrier(0);  // prefetch stays above the MFMAs
         f32x4 acc[QB];
         score_regs<DT, D, QB>(lds, g.segs, buf[j], acc);
-        epi(acc, r0 + rb * 16 + r16, rid[j]);
+        epi(acc, r0 + rb * 16 + r16);
         rb += nwaves;
       }
     }
   } else {
-    for (int64_t rb = wave; rb * 16 < nrows; rb += nwaves) {
-      const int64_t row = r0 + rb * 16 + r16;
-      const int64_t rowc = row < r1 ? row : r1 - 1;
-      const u32x4* vrow = (const u32x4*)(base + (size_t)rowc * row_bytes);
-      int64_t rid = 0;
-      if constexpr (kIds) rid = ids[rowc];
+    for (int rb = wave; rb * 16 < nrows; rb += nwaves) {
+      const u32x4* vrow = (const u32x4*)(rs.base + (size_t)rs.lane_row(rb) * rs.rb);
       f32x4 acc[QB];
       score_stream<DT, QB>(lds, g, vrow, acc);
-      epi(acc, row, rid);
+      epi(acc, r0 + rb * 16 + r16);
     }
   }
 }
@@ -464,35 +396,31 @@ constexpr int qb_cap() {
   return qb < 1 ? 1 : (qb > 8 ? 8 : qb);
 }
 
-template <int DT, int D, int QB, bool kIds, int kMax, typename Epi>
+template <int DT, int D, int QB, int kMax, typename Epi>
 __device__ __forceinline__ void stream_rows_from(const u32x4* __restrict__ lds,
                                                  const RowGeom<DT>& g,
                                                  const char* __restrict__ base, size_t row_bytes,
-                                                 const int64_t* __restrict__ ids, int64_t r0,
-                                                 int64_t r1, int qb_n, Epi& epi) {
+                                                 int64_t r0, int64_t r1, int qb_n, Epi& epi) {
   if constexpr (QB >= kMax) {
-    stream_rows_qb<DT, D, kMax, Epi, 0, kIds>(lds, g, base, row_bytes, ids, r0, r1, epi);
+    stream_rows_qb<DT, D, kMax, Epi>(lds, g, base, row_bytes, r0, r1, epi);
   } else {
     if (qb_n <= QB)
-      stream_rows_qb<DT, D, QB, Epi, 0, kIds>(lds, g, base, row_bytes, ids, r0, r1, epi);
+      stream_rows_qb<DT, D, QB, Epi>(lds, g, base, row_bytes, r0, r1, epi);
     else
-      stream_rows_from<DT, D, QB + 1, kIds, kMax>(lds, g, base, row_bytes, ids, r0, r1, qb_n,
-                                                  epi);
+      stream_rows_from<DT, D, QB + 1, kMax>(lds, g, base, row_bytes, r0, r1, qb_n, epi);
   }
 }
 
 // Dispatch on the tile's number of 16-query blocks (uniform per tile).
-// kIds: hand each row block's ids[row] to the epilogue (else 0).  QBLimit:
-// the caller's largest tile, in 16-query blocks; kBudgetKB: the LDS budget
-// the caller's tile size follows.
-template <int DT, int D, bool kIds = true, int QBLimit = 8, int kBudgetKB = 80, typename Epi>
+// QBLimit: the caller's largest tile, in 16-query blocks; kBudgetKB: the LDS
+// budget the caller's tile size follows.
+template <int DT, int D, int QBLimit = 8, int kBudgetKB = 80, typename Epi>
 __device__ __forceinline__ void stream_rows(const u32x4* __restrict__ lds, const RowGeom<DT>& g,
                                             const char* __restrict__ base, size_t row_bytes,
-                                            const int64_t* __restrict__ ids, int64_t r0,
-                                            int64_t r1, int qb_n, Epi&& epi) {
+                                            int64_t r0, int64_t r1, int qb_n, Epi&& epi) {
   constexpr int kCap = qb_cap<DT, D, kBudgetKB>();
   constexpr int kMax = kCap < QBLimit ? kCap : QBLimit;
-  stream_rows_from<DT, D, 1, kIds, kMax>(lds, g, base, row_bytes, ids, r0, r1, qb_n, epi);
+  stream_rows_from<DT, D, 1, kMax>(lds, g, base, row_bytes, r0, r1, qb_n, epi);
 }
 
 }  // namespace sieve

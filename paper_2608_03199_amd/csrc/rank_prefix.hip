@@ -23,15 +23,27 @@
 namespace sieve {
 namespace {
 
-constexpr int kPrefixQB = 4;           // 16-query blocks per work-group, at most
-constexpr int kPrefixRows = 16 * kPrefixQB;
-constexpr int kPrefixKeep = 128;       // values kept per query: 2 x 16 columns x 4 waves
+constexpr int kPrefixQB = 4;           // 16-query blocks per 256-thread work-group, at most
+constexpr int kPrefixQBWide = 6;       // the same for the 512-thread configuration
+constexpr int kPrefixRowsMax = 16 * kPrefixQBWide;
+// Wide configuration: one 512-thread work-group per CU with up to 150 KB of
+// staged queries, for long rows (fewer passes of the centroids per query).
+constexpr int kPrefixThreadsWide = 512;
+constexpr int kPrefixBudgetWideKB = 150;
 
-template <int DT, int D, int QB>
+// values kept per query after pass 1: 2 per (column, wave)
+template <int kNT>
+constexpr int prefix_keep() {
+  return 2 * 16 * (kNT / 64);
+}
+
+template <int DT, int D, int QB, int kNT>
 __device__ __forceinline__ void prefix_body(
     u32x4* lds, const RowGeom<DT>& g, const void* __restrict__ queries, int64_t q0, int qt0,
     int nq, const void* __restrict__ centroids, int32_t nlist, int d, int32_t R, double cmax,
     int32_t cap, unsigned long long* __restrict__ cand, float* s_lo, int32_t* s_cnt) {
+  constexpr int kKeep = prefix_keep<kNT>();
+  constexpr int kWaves = kNT / 64;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int h = lane >> 4, r16 = lane & 15;
   const size_t row_bytes = (size_t)d * DTraits<DT>::kElem;
@@ -46,31 +58,31 @@ __device__ __forceinline__ void prefix_body(
   float m1[QB * 4], m2[QB * 4];
 #pragma unroll
   for (int x = 0; x < QB * 4; ++x) m1[x] = m2[x] = -INFINITY;
-  auto top2 = [&](const auto& acc, int64_t c, int64_t) {
+  auto top2 = [&](const auto& acc, int64_t c) {
     const bool ok = c < nlist;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int x = qb * 4 + r;
+        // top two of {m1 >= m2, s}: the median of the three is the new second
         const float s = ok ? acc[qb][r] : -INFINITY;
-        const float lower = fminf(m1[x], s);
+        m2[x] = __builtin_amdgcn_fmed3f(m1[x], m2[x], s);
         m1[x] = fmaxf(m1[x], s);
-        m2[x] = fmaxf(m2[x], lower);
       }
     }
   };
-  stream_rows_qb<DT, D, QB, decltype(top2), 8 * QB, false>(lds, g, (const char*)centroids, row_bytes,
-                                                     nullptr, 0, nlist, top2);
+  stream_rows_qb<DT, D, QB, decltype(top2), 8 * QB>(lds, g, (const char*)centroids, row_bytes, 0,
+                                                    nlist, top2);
   __syncthreads();  // the staged queries are dead until re-staged below
 
-  float* keep = (float*)lds;  // [QB * 16][kPrefixKeep]
+  float* keep = (float*)lds;  // [QB * 16][kKeep]
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int i = qb * 16 + 4 * h + r;
-      float* dst = keep + i * kPrefixKeep + (wave * 16 + r16) * 2;
+      float* dst = keep + i * kKeep + (wave * 16 + r16) * 2;
       dst[0] = m1[qb * 4 + r];
       dst[1] = m2[qb * 4 + r];
     }
@@ -79,13 +91,17 @@ __device__ __forceinline__ void prefix_body(
 
   // lower limit per query: R-th largest kept value (bitwise search over the
   // order-preserving keys), less 2 delta, rounded down to fp32
-  for (int i = wave; i < nq; i += 4) {
-    const uint32_t ka = f2key(keep[i * kPrefixKeep + 2 * lane]);
-    const uint32_t kb = f2key(keep[i * kPrefixKeep + 2 * lane + 1]);
+  for (int i = wave; i < nq; i += kWaves) {
+    constexpr int kPer = kKeep / 64;  // kept values per lane
+    uint32_t kv[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) kv[j] = f2key(keep[i * kKeep + kPer * lane + j]);
     uint32_t prefix = 0;
     for (int bit = 31; bit >= 0; --bit) {
       const uint32_t c = prefix | (1u << bit);
-      const int cnt = __popcll(__ballot(ka >= c)) + __popcll(__ballot(kb >= c));
+      int cnt = 0;
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) cnt += __popcll(__ballot(kv[j] >= c));
       if (cnt >= R) prefix = c;
     }
     double ss = 0.0;
@@ -115,7 +131,7 @@ __device__ __forceinline__ void prefix_body(
       lim[qb * 4 + r] = i < nq ? s_lo[i] : INFINITY;
     }
   }
-  auto collect = [&](const auto& acc, int64_t c, int64_t) {
+  auto collect = [&](const auto& acc, int64_t c) {
     const bool ok = c < nlist;
     bool any = false;
 #pragma unroll
@@ -139,24 +155,24 @@ __device__ __forceinline__ void prefix_body(
       }
     }
   };
-  stream_rows_qb<DT, D, QB, decltype(collect), 4 * QB, false>(lds, g, (const char*)centroids,
-                                                      row_bytes, nullptr, 0, nlist, collect);
+  stream_rows_qb<DT, D, QB, decltype(collect), 4 * QB>(lds, g, (const char*)centroids, row_bytes,
+                                                       0, nlist, collect);
 }
 
-template <int DT, int D>
-__global__ __launch_bounds__(256, 2) void rank_prefix_kernel(
+template <int DT, int D, int kNT>
+__global__ __launch_bounds__(kNT, kNT == 256 ? 2 : 1) void rank_prefix_kernel(
     const void* __restrict__ queries, int64_t q0, int32_t nqc, const void* __restrict__ centroids,
     int32_t nlist, int32_t dd, int32_t R, int32_t rows, double cmax, int32_t cap,
     unsigned long long* __restrict__ cand, int32_t* __restrict__ ccount) {
   extern __shared__ u32x4 lds[];
-  __shared__ float s_lo[kPrefixRows];
-  __shared__ int32_t s_cnt[kPrefixRows];
+  __shared__ float s_lo[kPrefixRowsMax];
+  __shared__ int32_t s_cnt[kPrefixRowsMax];
   const int d = D > 0 ? D : dd;
   const RowGeom<DT> g = RowGeom<DT>::make(d);
   const int qt0 = blockIdx.x * rows;
   const int nq = min(rows, nqc - qt0);
   const int qb_n = (nq + 15) >> 4;
-  if (threadIdx.x < kPrefixRows) s_cnt[threadIdx.x] = 0;
+  if (threadIdx.x < kPrefixRowsMax) s_cnt[threadIdx.x] = 0;
   // stage once here; the body re-stages after pass 1
   const size_t row_bytes = (size_t)d * DTraits<DT>::kElem;
   const char* qbase = (const char*)queries + (size_t)(q0 + qt0) * row_bytes;
@@ -165,15 +181,19 @@ __global__ __launch_bounds__(256, 2) void rank_prefix_kernel(
   });
   __syncthreads();
   // the host sizes rows by the same LDS rule, so qb_n <= kQBMax
-  constexpr int kQBMax = qb_cap<DT, D>() < kPrefixQB ? qb_cap<DT, D>() : kPrefixQB;
-#define SIEVE_BODY(QB)                                                                        \
-  prefix_body<DT, D, QB>(lds, g, queries, q0, qt0, nq, centroids, nlist, d, R, cmax, cap, cand, \
-                         s_lo, s_cnt)
+  constexpr int kCap = kNT == 256 ? qb_cap<DT, D>() : qb_cap<DT, D, kPrefixBudgetWideKB>();
+  constexpr int kLim = kNT == 256 ? kPrefixQB : kPrefixQBWide;
+  constexpr int kQBMax = kCap < kLim ? kCap : kLim;
+#define SIEVE_BODY(QB)                                                                       \
+  prefix_body<DT, D, QB, kNT>(lds, g, queries, q0, qt0, nq, centroids, nlist, d, R, cmax, cap, \
+                              cand, s_lo, s_cnt)
   switch (qb_n) {
     case 1: SIEVE_BODY(1); break;
     case 2: if constexpr (kQBMax >= 2) SIEVE_BODY(2); break;
     case 3: if constexpr (kQBMax >= 3) SIEVE_BODY(3); break;
-    default: if constexpr (kQBMax >= 4) SIEVE_BODY(4); break;
+    case 4: if constexpr (kQBMax >= 4) SIEVE_BODY(4); break;
+    case 5: if constexpr (kQBMax >= 5) SIEVE_BODY(5); break;
+    default: if constexpr (kQBMax >= 6) SIEVE_BODY(6); break;
   }
 #undef SIEVE_BODY
   __syncthreads();
@@ -220,31 +240,49 @@ __global__ __launch_bounds__(256) void rank_prefix_finish_kernel(
 
 constexpr int kMaxDynLds = 150 * 1024;
 
+// Query rows per work-group: as many 16-row blocks as the LDS budget holds
+// (the kernel's compile-time cap follows the same rule).
 template <int DT>
-int prefix_rows(int d) {
+int prefix_rows(int d, bool wide) {
   const int rb = lds_row_bytes<DT>(d);
-  int qb = (80 * 1024) / (16 * rb);
-  qb = qb < 1 ? 1 : (qb > kPrefixQB ? kPrefixQB : qb);
+  const int budget = (wide ? kPrefixBudgetWideKB : 80) * 1024;
+  const int lim = wide ? kPrefixQBWide : kPrefixQB;
+  int qb = budget / (16 * rb);
+  qb = qb < 1 ? 1 : (qb > lim ? lim : qb);
   return 16 * qb;
 }
 
+template <int DT, int D, int kNT>
+hipError_t launch_prefix_k(const void* queries, int64_t q0, int32_t nqc, const void* centroids,
+                           int32_t nlist, int32_t d, int32_t R, double cmax, int32_t cap,
+                           unsigned long long* cand, int32_t* ccount, hipStream_t s) {
+  static const hipError_t attr =
+      hipFuncSetAttribute((const void*)rank_prefix_kernel<DT, D, kNT>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, kMaxDynLds);
+  if (attr != hipSuccess) return attr;
+  const int rows = prefix_rows<DT>(d, kNT != 256);
+  size_t lds = (size_t)rows * lds_row_bytes<DT>(d);
+  const size_t keep = (size_t)rows * prefix_keep<kNT>() * sizeof(float);
+  if (keep > lds) lds = keep;
+  if (lds > (size_t)kMaxDynLds) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((rank_prefix_kernel<DT, D, kNT>), dim3((unsigned)((nqc + rows - 1) / rows)),
+                     dim3(kNT), lds, s, queries, q0, nqc, centroids, nlist, d, R, rows, cmax, cap,
+                     cand, ccount);
+  return hipGetLastError();
+}
+
+// 768-dimension fp16 rows take the wide configuration: 96 queries per pass
+// of the centroids instead of 48.
 template <int DT, int D>
 hipError_t launch_prefix_t(const void* queries, int64_t q0, int32_t nqc, const void* centroids,
                            int32_t nlist, int32_t d, int32_t R, double cmax, int32_t cap,
                            unsigned long long* cand, int32_t* ccount, hipStream_t s) {
-  static const hipError_t attr =
-      hipFuncSetAttribute((const void*)rank_prefix_kernel<DT, D>,
-                          hipFuncAttributeMaxDynamicSharedMemorySize, kMaxDynLds);
-  if (attr != hipSuccess) return attr;
-  const int rows = prefix_rows<DT>(d);
-  size_t lds = (size_t)rows * lds_row_bytes<DT>(d);
-  const size_t keep = (size_t)rows * kPrefixKeep * sizeof(float);
-  if (keep > lds) lds = keep;
-  if (lds > (size_t)kMaxDynLds) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((rank_prefix_kernel<DT, D>), dim3((unsigned)((nqc + rows - 1) / rows)),
-                     dim3(256), lds, s, queries, q0, nqc, centroids, nlist, d, R, rows, cmax, cap,
-                     cand, ccount);
-  return hipGetLastError();
+  if constexpr (DT == SIEVE_F16 && D == 768)
+    return launch_prefix_k<DT, D, kPrefixThreadsWide>(queries, q0, nqc, centroids, nlist, d, R,
+                                                      cmax, cap, cand, ccount, s);
+  else
+    return launch_prefix_k<DT, D, 256>(queries, q0, nqc, centroids, nlist, d, R, cmax, cap, cand,
+                                       ccount, s);
 }
 
 template <int DT>

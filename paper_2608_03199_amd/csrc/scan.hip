@@ -207,9 +207,9 @@ __global__ __launch_bounds__(kNT, kNT == kScanThreads ? 2 : 1) void scan_kernel(
 #pragma unroll
     for (int r = 0; r < 4; ++r)
       thr_last[r] = ((qb_n - 1) * 16 + 4 * h + r) < nq ? tau : INFINITY;
-    stream_rows<DT, D, true, 8, kNT == kScanThreads ? 80 : 150>(
-          buf, g, (const char*)a.vectors, row_bytes, a.ids, r0, r1, qb_n,
-          [&](const auto& acc, int64_t row, int64_t rid) {
+    stream_rows<DT, D, 8, kNT == kScanThreads ? 80 : 150>(
+          buf, g, (const char*)a.vectors, row_bytes, r0, r1, qb_n,
+          [&](const auto& acc, int64_t row) {
             constexpr int QB = sizeof(acc) / sizeof(acc[0]);
             // tau test: one wave-wide vote in the common (no candidate) case;
             // full query blocks through a max tree, the last one per row
@@ -224,6 +224,8 @@ __global__ __launch_bounds__(kNT, kNT == kScanThreads ? 2 : 1) void scan_kernel(
             for (int r = 0; r < 4; ++r) any |= acc[QB - 1][r] >= thr_last[r];
             any = any && (row < r1);
             if (__ballot(any) == 0) return;
+            // row ids, needed only here (self-exclusion and the pool records)
+            const int64_t rid = a.ids[row < r1 ? row : r1 - 1];
             // Candidates: one ballot group (16 rows x 4 queries) takes its
             // pool slots with one LDS atomic on the block's arena; the
             // per-query counts go to LDS (one add per query of the group)
@@ -289,6 +291,12 @@ __global__ __launch_bounds__(kNT, kNT == kScanThreads ? 2 : 1) void scan_kernel(
                 }
               }
             }
+            // The candidate path issued global stores.  While stores and
+            // loads are both in flight the compiler can only wait for all
+            // of them before the next row block's MFMAs (including the
+            // prefetch just issued); draining the stores here, on this rare
+            // path, keeps the row loop's waits partial.
+            __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
           });
     if constexpr (kAsync) __builtin_amdgcn_s_waitcnt(0);  // this wave's staging copies landed
     __syncthreads();  // every wave is done with this tile's buffer and items
@@ -371,9 +379,8 @@ __global__ __launch_bounds__(kScanThreads, 2) void rank_scores_kernel(
   __syncthreads();
   const int64_t c0 = (int64_t)blockIdx.y * kScreenCents;
   const int64_t c1 = min<int64_t>(nlist, c0 + kScreenCents);
-  stream_rows<DT, D, false, kScreenQB>(lds, g, (const char*)centroids, row_bytes, nullptr, c0, c1,
-                                       qb_n,
-                     [&](const auto& acc, int64_t c, int64_t) {
+  stream_rows<DT, D, kScreenQB>(lds, g, (const char*)centroids, row_bytes, c0, c1, qb_n,
+                     [&](const auto& acc, int64_t c) {
                        constexpr int QB = sizeof(acc) / sizeof(acc[0]);
                        if (c >= c1) return;
 #pragma unroll
