@@ -521,18 +521,23 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
       int scan_launches = 0;
       read_timeline(ix, ms, &scan_launches);
       const RoundCounters& h = *ix->rc_host;
+      unsigned long long probes_sum = 0, cand_sum = 0;
+      for (int x = 0; x < kStatSlots; ++x) {
+        probes_sum += h.probes[x];
+        cand_sum += h.candidates[x];
+      }
       const double eb = (double)ix->d * e;
       stats->rounds = rounds;
       stats->nprobe_eff = pl.n;
       stats->scan_launches = scan_launches;
       stats->pool_retries = pool_retries;
       stats->items = items_total;
-      stats->probes_total = (int64_t)h.probes;
+      stats->probes_total = (int64_t)probes_sum;
       stats->vectors_scanned = (int64_t)h.item_rows;
       stats->list_loads = (int64_t)h.list_loads;
-      stats->hits = (int64_t)h.candidates;
+      stats->hits = (int64_t)cand_sum;
       stats->scan_bytes = (double)h.list_rows * eb + (double)items_total * (eb + sizeof(Item)) +
-                          (double)h.candidates * sizeof(Hit);
+                          (double)cand_sum * sizeof(Hit);
       stats->scan_flops = 2.0 * (double)ix->d * (double)h.item_rows;
       stats->rank_flops = 2.0 * (double)ix->d * (double)nq * (double)ix->nlist;
       stats->ms_rank = ms[kRank];

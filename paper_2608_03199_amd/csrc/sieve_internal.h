@@ -50,6 +50,8 @@ constexpr int kMaxCand = 4096;     // rank-boundary candidates kept for the exac
 constexpr int kMaxD = 4096;
 
 // Per-round scheduling counters (device).
+constexpr int kStatSlots = 32;
+
 struct RoundCounters {
   int32_t ntiles;          // tiles built this round
   int32_t new_items;       // items emitted by the update for the next round
@@ -60,8 +62,11 @@ struct RoundCounters {
   unsigned long long item_rows;   // sum over items of their list's length (this round)
   unsigned long long list_loads;  // active non-empty lists (this round)
   unsigned long long hits;        // pool slots claimed (whole search; includes arena tails)
-  unsigned long long probes;      // sum of out_probes (whole search)
-  unsigned long long candidates;  // qualifying candidates merged by the final top-k
+  // Sums of out_probes and of the qualifying candidates merged by the final
+  // top-k, spread over kStatSlots counters (work-group b adds to slot
+  // b % kStatSlots): thousands of adds to one address would serialise.
+  unsigned long long probes[kStatSlots];
+  unsigned long long candidates[kStatSlots];
 };
 
 // Candidate-pool arenas: a scan work-group claims pool slots in runs (first

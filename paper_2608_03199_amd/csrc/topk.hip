@@ -222,8 +222,9 @@ __global__ __launch_bounds__(256) void topk_kernel(int64_t nq, int32_t k,
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    atomicAdd(&rc->probes, s_probes[0] + s_probes[1] + s_probes[2] + s_probes[3]);
-    atomicAdd(&rc->candidates, s_cands[0] + s_cands[1] + s_cands[2] + s_cands[3]);
+    const int slot = blockIdx.x % kStatSlots;
+    atomicAdd(&rc->probes[slot], s_probes[0] + s_probes[1] + s_probes[2] + s_probes[3]);
+    atomicAdd(&rc->candidates[slot], s_cands[0] + s_cands[1] + s_cands[2] + s_cands[3]);
   }
 }
 
