@@ -171,11 +171,11 @@ int env_int(const char* name, int dflt) {
   return x > 0 ? x : dflt;
 }
 
-int row_chunk_for(const sieve_index* ix) {
+int row_chunk_for(const sieve_index* ix, const char* knob, int dflt) {
   // the scan addresses a tile's rows with 32-bit byte offsets
   const int64_t row_bytes = (int64_t)ix->d * elem_bytes(ix->dtype);
   const int64_t lim = ((int64_t)INT32_MAX / row_bytes) / 64 * 64;
-  int64_t rc = env_int("SIEVE_ROW_CHUNK", 512);
+  int64_t rc = env_int(knob, dflt);
   rc = ((rc + 63) / 64) * 64;
   return (int)std::max<int64_t>(64, std::min(rc, lim));
 }
@@ -201,7 +201,9 @@ struct SearchPlan {
   float tau;
   int64_t nq;
   int tile_q;
-  int row_chunk;
+  int row_chunk;        // rows per tile in sparse rounds
+  int row_chunk_dense;  // rows per tile in dense rounds (long tiles amortise the tile start)
+  int dense_q;          // a round is dense with at least this many items per list on average
   int64_t rank_chunk;  // queries per centroid-screen chunk
   int64_t fix_chunk;   // queries per fixed-probe chunk
   int64_t item_cap;
@@ -338,14 +340,16 @@ ScanArgs make_scan_args(sieve_index* ix, const void* queries, const int64_t* exc
 int run_round(sieve_index* ix, const ScanArgs& sa, int n_items, int64_t q0, const int32_t* P,
               const SearchPlan& pl, hipStream_t s, bool timed) {
   RoundCounters* rc = (RoundCounters*)ix->rc.p;
+  const int chunk = (int64_t)n_items >= (int64_t)pl.dense_q * ix->nlist ? pl.row_chunk_dense
+                                                                        : pl.row_chunk;
   const int e0 = mark(ix, timed, s);
-  HIP_TRY(launch_sched_offsets((const int32_t*)ix->cnt.p, ix->offsets, ix->nlist, pl.row_chunk,
+  HIP_TRY(launch_sched_offsets((const int32_t*)ix->cnt.p, ix->offsets, ix->nlist, chunk,
                                pl.tile_q, (int32_t*)ix->item_off.p, (int32_t*)ix->cursor.p,
                                (int32_t*)ix->tile_off.p, rc, s));
   HIP_TRY(launch_sched_scatter((const Item*)ix->items.p, n_items, P, pl.n, (int32_t)q0, sa.exclude,
                                (int32_t*)ix->cursor.p, (BItem*)ix->bucket.p, s));
   HIP_TRY(launch_sched_tiles((int32_t*)ix->cnt.p, (const int32_t*)ix->item_off.p,
-                             (const int32_t*)ix->tile_off.p, ix->offsets, ix->nlist, pl.row_chunk,
+                             (const int32_t*)ix->tile_off.p, ix->offsets, ix->nlist, chunk,
                              pl.tile_q, (Tile*)ix->tiles.p, s));
   const int e1 = mark(ix, timed, s);
   ScanArgs sr = sa;
@@ -565,7 +569,15 @@ int plan_search(const sieve_index* ix, int64_t nq, int32_t k, float tau, int32_t
   pl->wide = scan_wide_supported(ix->dtype, ix->d) && env_int("SIEVE_SCAN_WIDE", 1) == 1;
   pl->tile_q = pl->wide ? tile_rows_wide(ix->dtype, ix->d) : tile_rows(ix->dtype, ix->d);
   pl->wide_rank = false;
-  pl->row_chunk = row_chunk_for(ix);
+  pl->row_chunk = row_chunk_for(ix, "SIEVE_ROW_CHUNK", 512);
+  // Dense rounds over short lists (at most 2048 rows on average) take whole
+  // lists as one tile, which halves the tile starts of a 1,000-row list; with
+  // long lists the 512-row tiles measured as fast or faster.
+  const int64_t avg_len = ix->n / ix->nlist;
+  pl->row_chunk_dense =
+      row_chunk_for(ix, "SIEVE_ROW_CHUNK_DENSE", avg_len <= 2048 ? 4096 : pl->row_chunk);
+  if (pl->row_chunk_dense < pl->row_chunk) pl->row_chunk_dense = pl->row_chunk;
+  pl->dense_q = env_int("SIEVE_DENSE_Q", 64);
   pl->scan_grid = pl->wide ? ((ix->cus + 7) / 8) * 8 : scan_grid(ix, pl->tile_q);
   // Lazy ranking: a stop line starts at min(W, n) and mostly stays near it,
   // so only the first r0 ranks are ordered up front (queries whose stop line

@@ -65,6 +65,29 @@ __device__ __forceinline__ f32x4 mma_chunk(u32x4 a, u32x4 b, f32x4 acc) {
     return mma_chunk_f16(a, b, acc);
 }
 
+// One chunk against QB query blocks.  fp32 issues its four k-steps
+// k-major across the query blocks, so that consecutive MFMAs write
+// different accumulators (a chain of four dependent fp32 MFMAs on one
+// accumulator stalls on each result).  Every accumulator still sees its
+// k-steps in the same order as mma_chunk_f32: the same bits.
+template <int DT, int QB>
+__device__ __forceinline__ void mma_chunk_qb(const u32x4 (&a)[QB], u32x4 b, f32x4 (&acc)[QB]) {
+  if constexpr (DT == SIEVE_F32) {
+    const f32x4 bf = __builtin_bit_cast(f32x4, b);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        const f32x4 af = __builtin_bit_cast(f32x4, a[qb]);
+        acc[qb] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[k], bf[k], acc[qb], 0, 0, 0);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) acc[qb] = mma_chunk_f16(a[qb], b, acc[qb]);
+  }
+}
+
 // Base address of this lane's query fragments in LDS.  The offset passes
 // through an empty asm so that the compiler cannot treat the fragment loads
 // as invariant across row blocks and hoist them all out of the row loop
@@ -156,8 +179,7 @@ __device__ __forceinline__ void score_regs(const u32x4* __restrict__ lds, int se
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) nxt[qb] = arow[qb * 16 * segs + 4 * (c + 1)];
     }
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) acc[qb] = mma_chunk<DT>(cur[qb], b[c], acc[qb]);
+    mma_chunk_qb<DT, QB>(cur, b[c], acc);
     __builtin_amdgcn_sched_barrier(0);
   }
 }
@@ -181,11 +203,10 @@ __device__ __forceinline__ void score_stream(const u32x4* __restrict__ lds, cons
     const int sn = 4 * (c + 1) + h;
     bn = vrow[sn < g.dsegs ? sn : 0];
     if (sn >= g.dsegs) bn = zero;
+    u32x4 av[QB];
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-      const u32x4 av = arow[qb * 16 * g.segs + 4 * c];
-      acc[qb] = mma_chunk<DT>(av, bc, acc[qb]);
-    }
+    for (int qb = 0; qb < QB; ++qb) av[qb] = arow[qb * 16 * g.segs + 4 * c];
+    mma_chunk_qb<DT, QB>(av, bc, acc);
   }
 }
 
@@ -214,8 +235,7 @@ __device__ __forceinline__ void mma_slice(const u32x4* __restrict__ arow, int se
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) nxt[qb] = arow[qb * 16 * segs + 4 * (c0 + c + 1)];
       }
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb) acc[qb] = mma_chunk<DT>(cur[qb], b[c], acc[qb]);
+      mma_chunk_qb<DT, QB>(cur, b[c], acc);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
