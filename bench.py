@@ -82,6 +82,13 @@ def main():
                     help="do not time the in-call calibrated search (profiling runs)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (HBM counter calibration)")
+    ap.add_argument("--envelope", action="store_true",
+                    help="k in {5, 10, 20, 50} and tau in {0.10 .. 0.90} on the 1M x 128 data: "
+                         "queries/s, speedup over fixed probing, candidates, overlap with the "
+                         "fixed-probe output (one JSON line)")
+    ap.add_argument("--concurrency", action="store_true",
+                    help="queries per call in {1, 10, 100, 1000, 10000} on the 1M x 128 data, "
+                         "for lookahead, basic and serial dispatch (one JSON line)")
     ap.add_argument("--sweep", action="store_true",
                     help="W / lookahead / tau / fixed-nprobe sweep with recall on the 1M x 128 "
                          "data (prints one JSON line with the table)")
@@ -100,6 +107,10 @@ def main():
     torch.cuda.set_device(0)
     if args.sweep:
         return sweep(args, ps, sw, np, torch, dev)
+    if args.envelope:
+        return envelope(args, ps, sw, np, torch, dev)
+    if args.concurrency:
+        return concurrency(args, ps, sw, np, torch, dev)
     spec = sw.SPECS[args.config]
     log(f"[bench] generating {args.config} on {dev}")
     t0 = time.time()
@@ -341,6 +352,82 @@ def sweep(args, ps, sw, np, torch, dev):
            "config": {"workload": workload_name(spec), "recall_subset": 2000,
                       "nprobe_max": spec.nprobe_max},
            "steps_per_point": steps, "sweep": rows}
+    print(json.dumps(out), flush=True)
+
+
+def _timed(torch, fn, steps):
+    fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        r = fn()
+    torch.cuda.synchronize()
+    return r, (time.perf_counter() - t0) / steps
+
+
+def envelope(args, ps, sw, np, torch, dev):
+    """Operating envelope on the 1M x 128 fp32 data (Sec. 6.4: thresholds down to 0.10, k up
+    to 50): W = 8 with lookahead against fixed nprobe = 128 on the whole 10,000-query batch;
+    overlap = pooled fraction of the fixed-probe result that the threshold search returns."""
+    spec = sw.SPECS["c2"]
+    log("[envelope] generating c2")
+    w = sw.make(spec, device=dev)
+    ix = ps.Index(w.vectors, w.list_offsets, w.ids, w.centroids)
+    steps = max(1, args.steps // 4)
+    rows = []
+    points = [(k, spec.tau) for k in (5, 10, 20, 50)] + \
+             [(spec.k, t) for t in (0.10, 0.30, 0.50, 0.70, 0.90)]
+    for k, tau in points:
+        r, sec = _timed(torch, lambda: ix.search(w.queries, w.exclude_ids, k, tau, spec.W,
+                                                 spec.nprobe_max, with_stats=True), steps)
+        f, fsec = _timed(torch, lambda: ix.search_fixed(w.queries, w.exclude_ids, k, tau,
+                                                        spec.fixed_nprobe), steps)
+        a, b = r[0].cpu().numpy(), f[0].cpu().numpy()
+        tot = int((b >= 0).sum())
+        kept = sum(len(set(x[x >= 0].tolist()) & set(y[y >= 0].tolist())) for x, y in zip(a, b))
+        rows.append({"k": k, "tau": tau, "qps": round(spec.nq / sec, 1),
+                     "fixed_qps": round(spec.nq / fsec, 1), "speedup": round(fsec / sec, 3),
+                     "mean_probes": round(float(r[2].float().mean()), 3),
+                     "candidates": int(r[3].hits), "rounds": int(r[3].rounds),
+                     "overlap_with_fixed": round(kept / tot, 5) if tot else None})
+        log(f"[envelope] {rows[-1]}")
+    ix.close()
+    out = {"metric": "operating envelope: queries/s and speedup over fixed probing",
+           "config": {"workload": workload_name(spec), "W": spec.W,
+                      "fixed_nprobe": spec.fixed_nprobe},
+           "steps_per_point": steps, "envelope": rows}
+    print(json.dumps(out), flush=True)
+
+
+def concurrency(args, ps, sw, np, torch, dev):
+    """Queries per call (Sec. 6.4's request-size sweep) on the 1M x 128 fp32 data, W = 8:
+    lookahead, basic (Algorithm 1) and serial dispatch.  Each point issues consecutive calls
+    over a prefix of the 10,000-query batch (at most 200 calls) and reports queries/s."""
+    spec = sw.SPECS["c2"]
+    log("[concurrency] generating c2")
+    w = sw.make(spec, device=dev)
+    ix = ps.Index(w.vectors, w.list_offsets, w.ids, w.centroids)
+    rows = []
+    for per in (1, 10, 100, 1000, 10000):
+        calls = min(200, spec.nq // per)
+        row = {"queries_per_call": per, "calls": calls}
+        for name, kw in (("lookahead", dict(lookahead=True)), ("basic", dict(lookahead=False)),
+                         ("serial", dict(serial=True))):
+            def run():
+                for c in range(calls):
+                    q0 = c * per
+                    r = ix.search(w.queries[q0:q0 + per], w.exclude_ids[q0:q0 + per], spec.k,
+                                  spec.tau, spec.W, spec.nprobe_max, **kw)
+                return r
+            _, sec = _timed(torch, run, 1)
+            row[name + "_qps"] = round(calls * per / sec, 1)
+        rows.append(row)
+        log(f"[concurrency] {row}")
+    ix.close()
+    out = {"metric": "queries/s by queries per call (W=8): lookahead, basic and serial dispatch",
+           "config": {"workload": workload_name(spec), "W": spec.W,
+                      "nprobe_max": spec.nprobe_max},
+           "concurrency": rows}
     print(json.dumps(out), flush=True)
 
 

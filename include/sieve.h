@@ -125,7 +125,10 @@ SIEVE_API int sieve_load_index(const void* vectors, int32_t dtype, int64_t n, in
  *   W            consecutive-empty window, W >= 1 (SIEVE_W_INF: never stop).
  *   nprobe_max   >= 1; clamped to nlist; the clamped value must be <= 2048
  *                (else SIEVE_EUNSUPPORTED).
- *   lookahead    0 (Algorithm 1) or 1 (Algorithm 2); outputs are identical.
+ *   lookahead    0 (Algorithm 1), 1 (Algorithm 2), or 2 (serial traversal,
+ *                the ablation baseline of Sec. 6.3: one rank per query per
+ *                round as in Algorithm 1, and no partition scan is shared by
+ *                two queries).  Outputs are identical in all three.
  *   out_ids      [nq * k] int64, out_scores [nq * k] float: per query the
  *                top-k qualifying candidates, score descending then id
  *                ascending, padded with (-1, -INFINITY).

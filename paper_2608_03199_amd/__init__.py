@@ -178,14 +178,16 @@ class Index:
 
     def search(self, queries: torch.Tensor, exclude_ids: Optional[torch.Tensor], k: int,
                tau: float, W: int, nprobe_max: int, lookahead: bool = True,
-               with_stats: bool = False, stream=None):
-        """Threshold-aware search; returns (ids, scores, probes[, Stats])."""
+               with_stats: bool = False, stream=None, serial: bool = False):
+        """Threshold-aware search; returns (ids, scores, probes[, Stats]).  serial: the
+        serial-traversal ablation (no shared partition scans; lookahead is ignored)."""
         queries, ex, nq, oi, osc, op = self._prep(queries, exclude_ids, k)
         st = Stats() if with_stats else None
         with torch.cuda.device(self.device):
             _check(self._lib, self._lib.sieve_search(
                 self._h, queries.data_ptr(), nq, None if ex is None else ex.data_ptr(), int(k),
-                float(tau), int(W), int(nprobe_max), 1 if lookahead else 0, oi.data_ptr(),
+                float(tau), int(W), int(nprobe_max), 2 if serial else (1 if lookahead else 0),
+                oi.data_ptr(),
                 osc.data_ptr(), op.data_ptr(), ctypes.byref(st) if st is not None else None,
                 _stream(stream)))
         return (oi, osc, op, st) if with_stats else (oi, osc, op)

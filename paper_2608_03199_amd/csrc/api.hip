@@ -200,7 +200,8 @@ struct SearchPlan {
   int k;
   float tau;
   int64_t nq;
-  int tile_q;
+  int tile_q;           // query rows a tile stages (LDS sizing)
+  int group_q;          // items of one list grouped into a tile (tile_q; 1 = serial)
   int row_chunk;        // rows per tile in sparse rounds
   int row_chunk_dense;  // rows per tile in dense rounds (long tiles amortise the tile start)
   int dense_q;          // a round is dense with at least this many items per list on average
@@ -237,7 +238,7 @@ int grow_workspace(sieve_index* ix, const SearchPlan& pl) {
   if ((st = ensure(ix->bucket, (size_t)pl.item_cap * sizeof(BItem)))) return st;
   // tiles: sum_p ceil(c_p / tq) * ceil(len_p / rc) <= items * max_chunks / tq + lists + rows / rc
   const int64_t max_ch = (ix->max_list + pl.row_chunk - 1) / pl.row_chunk;
-  const int64_t tile_cap = pl.item_cap / pl.tile_q * (max_ch > 0 ? max_ch : 1) + ix->nlist +
+  const int64_t tile_cap = pl.item_cap / pl.group_q * (max_ch > 0 ? max_ch : 1) + ix->nlist +
                            ix->n / pl.row_chunk + 16;
   if (tile_cap > INT32_MAX) return fail(SIEVE_EUNSUPPORTED, "tile count bound overflows int32");
   if ((st = ensure(ix->tiles, (size_t)tile_cap * sizeof(Tile)))) return st;
@@ -344,13 +345,13 @@ int run_round(sieve_index* ix, const ScanArgs& sa, int n_items, int64_t q0, cons
                                                                         : pl.row_chunk;
   const int e0 = mark(ix, timed, s);
   HIP_TRY(launch_sched_offsets((const int32_t*)ix->cnt.p, ix->offsets, ix->nlist, chunk,
-                               pl.tile_q, (int32_t*)ix->item_off.p, (int32_t*)ix->cursor.p,
+                               pl.group_q, (int32_t*)ix->item_off.p, (int32_t*)ix->cursor.p,
                                (int32_t*)ix->tile_off.p, rc, s));
   HIP_TRY(launch_sched_scatter((const Item*)ix->items.p, n_items, P, pl.n, (int32_t)q0, sa.exclude,
                                (int32_t*)ix->cursor.p, (BItem*)ix->bucket.p, s));
   HIP_TRY(launch_sched_tiles((int32_t*)ix->cnt.p, (const int32_t*)ix->item_off.p,
                              (const int32_t*)ix->tile_off.p, ix->offsets, ix->nlist, chunk,
-                             pl.tile_q, (Tile*)ix->tiles.p, s));
+                             pl.group_q, (Tile*)ix->tiles.p, s));
   const int e1 = mark(ix, timed, s);
   ScanArgs sr = sa;
   sr.dynamic = scan_dynamic(n_items);
@@ -568,6 +569,7 @@ int plan_search(const sieve_index* ix, int64_t nq, int32_t k, float tau, int32_t
   // default on where supported; SIEVE_SCAN_WIDE=2 turns it off (tuning only)
   pl->wide = scan_wide_supported(ix->dtype, ix->d) && env_int("SIEVE_SCAN_WIDE", 1) == 1;
   pl->tile_q = pl->wide ? tile_rows_wide(ix->dtype, ix->d) : tile_rows(ix->dtype, ix->d);
+  pl->group_q = pl->tile_q;
   pl->wide_rank = false;
   pl->row_chunk = row_chunk_for(ix, "SIEVE_ROW_CHUNK", 512);
   // Dense rounds over short lists (at most 2048 rows on average) take whole
@@ -746,10 +748,11 @@ SIEVE_API int sieve_search(const sieve_index* idx, const void* queries, int64_t 
   if (st) return st;
   if (W < 1) return fail(SIEVE_EINVAL, "W = %d must be >= 1", W);
   if (nprobe_max < 1) return fail(SIEVE_EINVAL, "nprobe_max = %d must be >= 1", nprobe_max);
-  if (lookahead != 0 && lookahead != 1) return fail(SIEVE_EINVAL, "lookahead must be 0 or 1");
+  if (lookahead < 0 || lookahead > 2) return fail(SIEVE_EINVAL, "lookahead must be 0, 1 or 2");
   sieve_index* ix = const_cast<sieve_index*>(idx);
   SearchPlan pl;
-  if ((st = plan_search(ix, nq, k, tau, W, nprobe_max, lookahead ? 0 : 1, &pl))) return st;
+  if ((st = plan_search(ix, nq, k, tau, W, nprobe_max, lookahead == 1 ? 0 : 1, &pl))) return st;
+  if (lookahead == 2) pl.group_q = 1;  // serial: no query shares a partition scan
   if (stats) memset(stats, 0, sizeof(*stats));
   if (nq == 0) {
     if (stats) stats->nprobe_eff = pl.n;

@@ -18,6 +18,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+#include <utility>
+
 #include "sieve_internal.h"
 
 namespace sieve {
@@ -278,6 +281,14 @@ struct RowStream {
     return base + (lane_row(blk) * rb + ((threadIdx.x >> 4) & 3u) * 16u);
   }
 };
+
+// f(std::integral_constant<int, J>{}) for J = 0 .. N-1, unrolled at compile
+// time (fragment ring indices must be constants: a runtime index would put
+// the ring in scratch memory).
+template <typename F, int... J>
+__device__ __forceinline__ void unroll_steps(F&& f, std::integer_sequence<int, J...>) {
+  (f(std::integral_constant<int, J>{}), ...);
+}
 
 // Index of this wave in the work-group, as a uniform (scalar) value: the row
 // loops below then run on scalar branches and scalar counters.

@@ -17,6 +17,8 @@
 // runs in fp64 and writes the first R centroids.  A query with more than
 // `cap` candidates (or fewer than R) sets rank_error: the caller re-ranks
 // from materialised scores with a wide buffer.
+#include <type_traits>
+
 #include "mfma_tile.h"
 #include "rank_common.h"
 
@@ -200,6 +202,242 @@ __global__ __launch_bounds__(kNT, kNT == 256 ? 2 : 1) void rank_prefix_kernel(
   if ((int)threadIdx.x < nq) ccount[qt0 + threadIdx.x] = s_cnt[threadIdx.x];
 }
 
+// Register-query variant for short fp16 rows (at most 128 dimensions).  The
+// eight waves of a work-group form 8 / kQRSplit groups; a group owns kQW
+// 16-query blocks, whose MFMA fragments each of its waves keeps in registers
+// for the whole kernel, and its kQRSplit waves split the centroid row blocks
+// (wave j of a group takes blocks j, j + kQRSplit, ...).  A pass over the
+// centroids thus serves kQRRows = 128 queries (twice the LDS-staged kernel)
+// and reads no LDS in its inner loop.  Each query row is seen by 16 kQRSplit
+// lanes holding disjoint centroid sets; pass 1 keeps their two largest
+// screen scores, so the R-th largest of those 128 values is at most the R-th
+// largest screen score (the bound of rank_prefix_kernel, just as tight).
+// Pass 2 recomputes the same scores (the same instruction sequence, so the
+// same bits) and appends every centroid at or above the limit.
+constexpr int kQRWaves = 8;
+constexpr int kQRSplit = 4;
+constexpr int kQW = 4;
+constexpr int kQRRows = (kQRWaves / kQRSplit) * kQW * 16;  // queries per work-group
+constexpr int kQRKeep = 2 * 16 * kQRSplit;                // kept values per query
+constexpr int kQRRing = 4;                                 // centroid fragment buffers
+
+template <int D>
+__global__ __launch_bounds__(kQRWaves * 64, 1) void rank_prefix_qreg_kernel(
+    const void* __restrict__ queries, int64_t q0, int32_t nqc, const void* __restrict__ centroids,
+    int32_t nlist, int32_t R, double cmax, int32_t cap, unsigned long long* __restrict__ cand,
+    int32_t* __restrict__ ccount) {
+  constexpr int DT = SIEVE_F16;
+  constexpr int kNC = D / DTraits<DT>::kChunkDims;
+  static_assert(kNC >= 1 && kNC <= 4, "short rows only");
+  __shared__ float s_keep[kQRRows * kQRKeep];
+  __shared__ float s_lo[kQRRows];
+  __shared__ double s_ss[kQRRows];  // squared query norms (fp64, exact from fp16)
+  __shared__ int32_t s_cnt[kQRRows];
+  const int lane = threadIdx.x & 63;
+  const int wave = wave_id();
+  const int grp = wave / kQRSplit, mem = wave % kQRSplit;
+  const int h = lane >> 4, r16 = lane & 15;
+  const size_t row_bytes = (size_t)D * 2;
+  for (int i = threadIdx.x; i < kQRRows; i += blockDim.x) s_cnt[i] = 0;
+  const int qt0 = blockIdx.x * kQRRows;  // first query of the work-group
+  const int w0 = grp * kQW * 16;         // first local query row of the group
+  // A operand: lane l supplies query row (block qb, row l % 16), segment 4c + l / 16
+  u32x4 qf[kQW][kNC];
+#pragma unroll
+  for (int qb = 0; qb < kQW; ++qb) {
+    const int row = qt0 + w0 + qb * 16 + r16;
+    const bool ok = row < nqc;
+    const char* src = (const char*)queries + (size_t)(q0 + (ok ? row : 0)) * row_bytes;
+#pragma unroll
+    for (int c = 0; c < kNC; ++c) {
+      const u32x4 v = *(const u32x4*)(src + (size_t)(4 * c + h) * 16);
+      qf[qb][c] = ok ? v : u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+  // squared norms of the group's query rows from the fragments: the four
+  // lanes of a row (l / 16 = 0..3) hold its 16-byte segments 4c + l / 16
+  if (mem == 0) {
+#pragma unroll
+    for (int qb = 0; qb < kQW; ++qb) {
+      double ss = 0.0;
+#pragma unroll
+      for (int c = 0; c < kNC; ++c) {
+        const f16x8 hv = __builtin_bit_cast(f16x8, qf[qb][c]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ss += (double)hv[e] * (double)hv[e];
+      }
+      ss += __shfl_xor(ss, 16);
+      ss += __shfl_xor(ss, 32);
+      if (h == 0) s_ss[w0 + qb * 16 + r16] = ss;
+    }
+  }
+
+  const RowStream rs = {(const char*)centroids, nlist, (uint32_t)row_bytes};
+  const int nblk = (nlist + 15) >> 4;
+  // This wave's centroid row blocks (mem, mem + kQRSplit, ...) against its
+  // group's query blocks.  Fragments come through a ring of kQRRing buffers
+  // (kQRRing - 1 blocks in flight: the centroids come from L2, whose latency
+  // one block's 16 MFMAs do not cover), and the epilogue is software-
+  // pipelined: the MFMAs of block t issue interleaved with the VALU work
+  // fast(acc, blk) of block t - 1, which returns whether slow(acc, blk) must
+  // run for that block.  A fixed number of ring rounds runs; padding blocks
+  // (past the last) skip their epilogue.
+  auto sweep = [&](auto&& fast, auto&& slow) {
+    u32x4 buf[kQRRing][kNC];
+    f32x4 acc[2][kQW];
+    auto load = [&](int blk, u32x4(&dst)[kNC]) {
+      const char* p = rs.seg_ptr(blk < nblk ? blk : nblk - 1);
+#pragma unroll
+      for (int c = 0; c < kNC; ++c) dst[c] = *(const u32x4*)(p + 64 * c);
+    };
+#pragma unroll
+    for (int u = 0; u < kQRRing - 1; ++u) load(mem + u * kQRSplit, buf[u]);
+    const int mine = mem < nblk ? (nblk - mem + kQRSplit - 1) / kQRSplit : 0;
+    const int rounds = (mine + kQRRing - 1) / kQRRing;
+    int blk = mem;
+    for (int it = 0; it < rounds; ++it) {
+      unroll_steps([&](auto uc) {
+        constexpr int u = decltype(uc)::value;
+        constexpr int cur = u & 1, prev = cur ^ 1;  // kQRRing is even
+        load(blk + (kQRRing - 1) * kQRSplit, buf[(u + kQRRing - 1) % kQRRing]);
+        __builtin_amdgcn_sched_barrier(0);
+        auto multiply = [&]() {
+#pragma unroll
+          for (int qb = 0; qb < kQW; ++qb) acc[cur][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int c = 0; c < kNC; ++c) {
+            u32x4 a[kQW];
+#pragma unroll
+            for (int qb = 0; qb < kQW; ++qb) a[qb] = qf[qb][c];
+            mma_chunk_qb<DT, kQW>(a, buf[u][c], acc[cur]);
+          }
+        };
+        const int pblk = blk - kQRSplit;
+        // the previous block's columns that hold real centroids (none before
+        // the first block); the epilogue runs branch-free under this mask so
+        // that it issues interleaved with this block's MFMAs
+        const bool pok = (u > 0 || it > 0) && pblk * 16 + r16 < nlist;
+        multiply();
+        const bool need = fast(acc[prev], pok);
+#pragma unroll
+        for (int x = 0; x < kQW * kNC; ++x) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+          __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);  // three VALU
+        }
+        if (__ballot(need) != 0) slow(acc[prev], pblk);
+        blk += kQRSplit;
+      }, std::make_integer_sequence<int, kQRRing>{});
+    }
+    // the last block's epilogue
+    const int lblk = blk - kQRSplit;
+    if (rounds > 0 && lblk < nblk) {
+      constexpr int last = (kQRRing - 1) & 1;
+      if (__ballot(fast(acc[last], lblk * 16 + r16 < nlist)) != 0) slow(acc[last], lblk);
+    }
+  };
+
+  // pass 1: the two largest screen scores per (lane, query row)
+  float pinf = INFINITY;
+  asm volatile("" : "+v"(pinf));
+  float m1[kQW * 4], m2[kQW * 4];
+#pragma unroll
+  for (int x = 0; x < kQW * 4; ++x) m1[x] = m2[x] = -INFINITY;
+  sweep(
+      [&](const f32x4(&acc)[kQW], bool ok) -> bool {
+#pragma unroll
+        for (int qb = 0; qb < kQW; ++qb) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int x = qb * 4 + r;
+            // top two of {m1 >= m2, s}: the median of the three is the new
+            // second, the median of {m1, s, +inf} the new first (+inf passes
+            // through an empty asm so that the median is not rewritten as a
+            // maximum, which would canonicalise its operands first)
+            const float sc = ok ? acc[qb][r] : -INFINITY;
+            m2[x] = __builtin_amdgcn_fmed3f(m1[x], m2[x], sc);
+            m1[x] = __builtin_amdgcn_fmed3f(m1[x], sc, pinf);
+          }
+        }
+        return false;
+      },
+      [&](const f32x4(&)[kQW], int) {});
+#pragma unroll
+  for (int qb = 0; qb < kQW; ++qb) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float* dst = s_keep + (w0 + qb * 16 + 4 * h + r) * kQRKeep + (mem * 16 + r16) * 2;
+      dst[0] = m1[qb * 4 + r];
+      dst[1] = m2[qb * 4 + r];
+    }
+  }
+  __syncthreads();
+
+  // lower limit per query: R-th largest kept value (bitwise search over the
+  // order-preserving keys), less 2 delta, rounded down to fp32
+  for (int i = wave; i < kQRRows; i += kQRWaves) {
+    constexpr int kPer = kQRKeep / 64;  // kept values per lane
+    uint32_t kv[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) kv[j] = f2key(s_keep[i * kQRKeep + kPer * lane + j]);
+    uint32_t prefix = 0;
+    for (int bit = 31; bit >= 0; --bit) {
+      const uint32_t c = prefix | (1u << bit);
+      int cnt = 0;
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) cnt += __popcll(__ballot(kv[j] >= c));
+      if (cnt >= R) prefix = c;
+    }
+    const int row = qt0 + i;
+    const double ss = s_ss[i];
+    const double delta =
+        2.0 * (double)(D + 2) * 5.9604644775390625e-08 * sqrt(ss) * cmax + 1e-30;
+    const double lo = (double)key2f(prefix) - 2.0 * delta;
+    float lof = (float)lo;
+    if ((double)lof > lo) lof = nextafterf(lof, -INFINITY);
+    if (lane == 0) s_lo[i] = row < nqc ? lof : INFINITY;
+  }
+  __syncthreads();
+
+  // pass 2: append every centroid at or above its query's limit
+  float lim[kQW * 4];
+#pragma unroll
+  for (int qb = 0; qb < kQW; ++qb) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) lim[qb * 4 + r] = s_lo[w0 + qb * 16 + 4 * h + r];
+  }
+  sweep(
+      [&](const f32x4(&acc)[kQW], bool ok) -> bool {
+        bool any = false;
+#pragma unroll
+        for (int qb = 0; qb < kQW; ++qb) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) any |= acc[qb][r] >= lim[qb * 4 + r];
+        }
+        return ok && any;
+      },
+      [&](const f32x4(&acc)[kQW], int blk) {
+        const int c = blk * 16 + r16;
+        const bool ok = c < nlist;
+#pragma unroll
+        for (int qb = 0; qb < kQW; ++qb) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float sc = acc[qb][r];
+            if (ok && sc >= lim[qb * 4 + r]) {
+              const int i = w0 + qb * 16 + 4 * h + r;  // local query row
+              const int slot = atomicAdd(&s_cnt[i], 1);
+              if (slot < cap)
+                cand[(int64_t)(qt0 + i) * cap + slot] =
+                    ((unsigned long long)(~f2key(sc)) << 32) | (unsigned)c;
+            }
+          }
+        }
+      });
+  __syncthreads();
+  for (int i = threadIdx.x; i < kQRRows; i += blockDim.x)
+    if (qt0 + i < nqc) ccount[qt0 + i] = s_cnt[i];
+}
+
 // One wave per query: sort the candidate list, order near-tie runs in fp64,
 // write the first R centroids.
 template <int DT>
@@ -317,6 +555,14 @@ hipError_t launch_rank_prefix(int dtype, const void* queries, int64_t q0, int32_
   if (R < 1 || R > kRankPrefixMax || R > nlist) return hipErrorInvalidValue;
   const int cap = rank_prefix_cap(R, nlist);
   hipError_t e;
+  if (dtype == SIEVE_F16 && d == 128) {
+    const unsigned grid = (unsigned)((nqc + kQRRows - 1) / kQRRows);
+    hipLaunchKernelGGL((rank_prefix_qreg_kernel<128>), dim3(grid), dim3(kQRWaves * 64), 0, s,
+                       queries, q0, nqc, centroids, nlist, R, cmax, cap, cand, ccount);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return launch_finish_t<SIEVE_F16>(queries, q0, nqc, centroids, d, R, cap, cmax, cand, ccount,
+                                      P, ldp, rc, s);
+  }
 #define SIEVE_PREFIX(DT, D)                                                                  \
   launch_prefix_t<DT, D>(queries, q0, nqc, centroids, nlist, d, R, cmax, cap, cand, ccount, s)
   if (dtype == SIEVE_F32) {

@@ -163,6 +163,29 @@ def test_lazy_rank_extension(name, W, short_rank_prefix, rank_path):
     _check(c, s.k, tau, W, s.nprobe_max, lookahead=False)
 
 
+@pytest.mark.parametrize("name", ["tiny16", "c1"])
+@pytest.mark.parametrize("W", [1, 3, 8])
+def test_serial_traversal_matches_batched_dispatch(name, W):
+    """Serial traversal (Sec. 6.3's ablation baseline: one rank per query per round, no
+    partition scan shared between queries) returns exactly what the batched dispatches
+    return, and the oracle's result."""
+    c = case(name)
+    s = c.w.spec
+    q, ex = c.w.queries, c.w.exclude_ids
+    a = c.ix.search(q, ex, s.k, s.tau, W, s.nprobe_max, lookahead=True, with_stats=True)
+    b = c.ix.search(q, ex, s.k, s.tau, W, s.nprobe_max, serial=True, with_stats=True)
+    for x, y in zip(a[:3], b[:3]):
+        assert torch.equal(x, y)
+    # the same (query, partition) searches, each in a tile of its own
+    assert a[3].items == b[3].items and a[3].vectors_scanned == b[3].vectors_scanned
+    assert b[3].rounds >= a[3].rounds
+    o = c.oracle(s.k, s.tau, W, s.nprobe_max)
+    rep = compare(b[0].cpu().numpy(), b[1].cpu().numpy(), b[2].cpu().numpy(), o)
+    print(f"[gpu-test] serial {name} W={W} rounds {b[3].rounds} vs {a[3].rounds} -> {rep}",
+          flush=True)
+    assert_parity(rep)
+
+
 def test_infinite_window_equals_fixed():
     c = case("c1")
     s = c.w.spec
@@ -330,7 +353,8 @@ def test_sieve_matches_oracle_on_each_rank_path(name, lookahead, rank_path):
     _check(c, s.k, s.tau, s.W, s.nprobe_max, lookahead)
 
 
-@pytest.mark.parametrize("nlist,d,dtype", [(2048, 32, torch.float32), (5000, 64, torch.float16)])
+@pytest.mark.parametrize("nlist,d,dtype", [(2048, 32, torch.float32), (5000, 64, torch.float16),
+                                           (1500, 128, torch.float16)])
 def test_rank_and_search_on_large_centroid_sets(nlist, d, dtype, rank_path):
     """More than 1,024 centroids: long prefixes take the register-resident block selector,
     short ones the fused screen (or the materialised path, forced); the order must be the
@@ -370,6 +394,34 @@ def test_rank_and_search_on_large_centroid_sets(nlist, d, dtype, rank_path):
         assert_parity(compare(f[0].cpu().numpy(), f[1].cpu().numpy(), f[2].cpu().numpy(), of))
     finally:
         ix.close()
+
+
+@pytest.mark.parametrize("R", [8, 32, 33, 64])
+def test_rank_prefix_on_many_work_groups(R, rank_path):
+    """128-dim fp16 queries on a large centroid set: the fused prefix keeps the queries of
+    each wave in registers, 512 queries per work-group; 1,100 queries span three
+    work-groups, the last one ragged; R = 32 and 33 straddle the two kept-value widths."""
+    rng = np.random.default_rng(900 + R)
+    nlist, d, nq = 1800, 128, 1100
+    C = rng.standard_normal((nlist, d))
+    C /= np.linalg.norm(C, axis=1, keepdims=True)
+    Q = rng.standard_normal((nq, d))
+    Q /= np.linalg.norm(Q, axis=1, keepdims=True)
+    C, Q = C.astype(np.float16), Q.astype(np.float16)
+    X = C[:4].copy()  # a token index: only the order is checked
+    off = np.zeros(nlist + 1, np.int64)
+    off[1:] = 4
+    ids = np.arange(4, dtype=np.int64)
+    ps = _lib()
+    ix = ps.Index(torch.from_numpy(X).cuda(), torch.from_numpy(off).cuda(),
+                  torch.from_numpy(ids).cuda(), torch.from_numpy(C).cuda())
+    try:
+        P = ix.rank(torch.from_numpy(Q).cuda(), R).cpu().numpy()
+    finally:
+        ix.close()
+    o = oracle.search(X, off, ids, C, Q, None, 1, 2.0, 1, R, want_order=True, nthreads=NTHREADS)
+    print(f"[gpu-test] rank prefix R={R} path={rank_path}", flush=True)
+    assert np.array_equal(P, o.order[:, :R])
 
 
 def test_rank_with_many_exact_ties_takes_the_wide_path(rank_path):
