@@ -187,6 +187,27 @@ SIEVE_API int sieve_search_calibrated(const sieve_index* idx, const void* querie
                                       sieve_stats* stats, void* stream);
 
 /*
+ * sieve_search_multi -- threshold search over several independently built
+ * indexes of one corpus (the coarse shards of the paper's 100M layout,
+ * Sec. 6.1): each index runs sieve_search with its own stop rule, and the
+ * per-query results are merged into one top-k in the result order (score
+ * descending, id ascending).
+ *   idxs         HOST array of nidx (1 .. SIEVE_MULTI_MAX) handles on one
+ *                device, with the same dtype and d; row ids must be unique
+ *                across the indexes (the merge does not deduplicate).
+ *   out_probes   [nq] the sum over the indexes of the partitions searched.
+ * Other arguments as for sieve_search (exclude_ids apply to every index).
+ * Workspace for the per-index results lives in idxs[0].  stats (if given)
+ * are sums over the indexes.
+ */
+#define SIEVE_MULTI_MAX 256
+SIEVE_API int sieve_search_multi(const sieve_index* const* idxs, int32_t nidx,
+                                 const void* queries, int64_t nq, const int64_t* exclude_ids,
+                                 int32_t k, float tau, int32_t W, int32_t nprobe_max,
+                                 int32_t lookahead, int64_t* out_ids, float* out_scores,
+                                 int32_t* out_probes, sieve_stats* stats, void* stream);
+
+/*
  * sieve_rank -- the probe order alone (Sec. 4.1): for each query, the first
  * min(nprobe, nlist) centroid indices by inner product, descending, ties to
  * the lower index, decided in fp64 (see the conventions above).

@@ -145,6 +145,37 @@ def bruteforce(vectors, ids, queries, exclude_ids, k, tau, nthreads=1) -> Oracle
     return r
 
 
+def search_multi(shards, queries, exclude_ids, k, tau, W, nprobe_max, mode=MODE_A, nthreads=1):
+    """Search over several independently built indexes (Sec. 6.1's coarse shards): each shard
+    runs the threshold search with its own stop rule (oracle.search), and the per-query union
+    of the shard results is ordered by (score desc, id asc) and cut to k.  shards: a list of
+    dicts with vectors, list_offsets, ids, centroids.  probes = the sum over the shards.
+    The tie flags are recomputed on the merged list; TAU_EDGE and KTH_TIE of any shard are
+    kept (a shard's (k+1)-th candidate never reaches the merge)."""
+    parts = [search(sh["vectors"], sh["list_offsets"], sh["ids"], sh["centroids"], queries,
+                    exclude_ids, k, tau, W, nprobe_max, mode, nthreads) for sh in shards]
+    nq = np.asarray(queries).shape[0]
+    r = OracleResult(ids=np.full((nq, k), -1, np.int64), scores=np.full((nq, k), -np.inf),
+                     probes=np.zeros(nq, np.int32), flags=np.zeros(nq, np.int32))
+    for i in range(nq):
+        cand = [(float(p.scores[i, j]), int(p.ids[i, j])) for p in parts for j in range(k)
+                if p.ids[i, j] >= 0]
+        cand.sort(key=lambda t: (-t[0], t[1]))
+        for j, (sc, cid) in enumerate(cand[:k]):
+            r.ids[i, j] = cid
+            r.scores[i, j] = sc
+        r.probes[i] = sum(int(p.probes[i]) for p in parts)
+        f = 0
+        for p in parts:
+            f |= int(p.flags[i]) & (FLAG_TAU_EDGE | FLAG_KTH_TIE)
+        if len(cand) > k and cand[k - 1][0] - cand[k][0] < 1e-4:
+            f |= FLAG_KTH_TIE
+        if any(cand[j][0] - cand[j + 1][0] < 1e-4 for j in range(min(k, len(cand)) - 1)):
+            f |= FLAG_ORDER_TIE
+        r.flags[i] = f
+    return r
+
+
 def calibrate(hitseq, found_rank, eps):
     """Required-window histogram and chosen W from recorded fixed-probe outcomes."""
     lib = _load()

@@ -16,7 +16,7 @@ from typing import Optional
 import torch
 
 __all__ = ["SieveError", "Index", "Stats", "load_library", "LIB_PATH", "W_INF", "K_MAX",
-           "F32", "F16"]
+           "F32", "F16", "search_multi"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsieve.so")
 W_INF = 0x7FFFFFFF
@@ -75,6 +75,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                             ctypes.c_float, i32, P, P, P,
                                             ctypes.POINTER(ctypes.c_int32),
                                             ctypes.POINTER(Stats), P]
+    lib.sieve_search_multi.restype = ctypes.c_int
+    lib.sieve_search_multi.argtypes = [P, i32, P, i64, P, i32, ctypes.c_float, i32, i32, i32, P,
+                                       P, P, ctypes.POINTER(Stats), P]
     lib.sieve_rank.restype = ctypes.c_int
     lib.sieve_rank.argtypes = [P, P, i64, i32, P, P]
     lib.sieve_free_index.restype = None
@@ -226,3 +229,25 @@ class Index:
                 float(tau), int(nprobe), oi.data_ptr(), osc.data_ptr(), op.data_ptr(),
                 ctypes.byref(st) if st is not None else None, _stream(stream)))
         return (oi, osc, op, st) if with_stats else (oi, osc, op)
+
+
+def search_multi(indexes, queries: torch.Tensor, exclude_ids: Optional[torch.Tensor], k: int,
+                 tau: float, W: int, nprobe_max: int, lookahead: bool = True,
+                 serial: bool = False, with_stats: bool = False, stream=None):
+    """Threshold search over several independently built indexes of one corpus, each with its
+    own stop rule, merged into one top-k (``sieve_search_multi``).  Returns
+    (ids, scores, probes[, Stats]); probes are summed over the indexes."""
+    indexes = list(indexes)
+    if not indexes:
+        raise ValueError("at least one index is required")
+    first = indexes[0]
+    queries, ex, nq, oi, osc, op = first._prep(queries, exclude_ids, k)
+    handles = (ctypes.c_void_p * len(indexes))(*[ix._h.value for ix in indexes])
+    st = Stats() if with_stats else None
+    with torch.cuda.device(first.device):
+        _check(first._lib, first._lib.sieve_search_multi(
+            handles, len(indexes), queries.data_ptr(), nq, None if ex is None else ex.data_ptr(),
+            int(k), float(tau), int(W), int(nprobe_max),
+            2 if serial else (1 if lookahead else 0), oi.data_ptr(), osc.data_ptr(),
+            op.data_ptr(), ctypes.byref(st) if st is not None else None, _stream(stream)))
+    return (oi, osc, op, st) if with_stats else (oi, osc, op)

@@ -92,7 +92,8 @@ struct sieve_index {
   // workspace, grown on demand
   Buf scores, P, items, bucket, tiles, cnt, item_off, cursor, tile_off, rc, state_a, state_b,
       lmax, hcount, hoff, hcur, scan_tmp, pool, pool_sorted, arenas, have, ext, qext, Pext,
-      cand, ccount, cal_idx, cal_q, cal_x, cal_bits, cal_rank, cal_hist;
+      cand, ccount, cal_idx, cal_q, cal_x, cal_bits, cal_rank, cal_hist, mix_ids, mix_scores,
+      mix_probes;
   int64_t pool_cap = 0;
   RoundCounters* rc_host = nullptr;
   // phase timing (only when stats are requested): events are recorded on the
@@ -726,7 +727,8 @@ SIEVE_API void sieve_free_index(sieve_index* ix) {
                  &ix->state_b, &ix->lmax, &ix->hcount, &ix->hoff, &ix->hcur, &ix->scan_tmp,
                  &ix->pool, &ix->pool_sorted, &ix->arenas, &ix->have, &ix->ext, &ix->qext,
                  &ix->Pext, &ix->cand, &ix->ccount, &ix->cal_idx, &ix->cal_q, &ix->cal_x,
-                 &ix->cal_bits, &ix->cal_rank, &ix->cal_hist};
+                 &ix->cal_bits, &ix->cal_rank, &ix->cal_hist, &ix->mix_ids, &ix->mix_scores,
+                 &ix->mix_probes};
   for (Buf* b : bufs)
     if (b->p) (void)hipFree(b->p);
   if (ix->vectors) (void)hipFree(ix->vectors);
@@ -932,6 +934,60 @@ SIEVE_API int sieve_search_calibrated(const sieve_index* idx, const void* querie
     if (st) return st;
     if (stats) add_stats(stats, part);
   }
+  return SIEVE_OK;
+}
+
+SIEVE_API int sieve_search_multi(const sieve_index* const* idxs, int32_t nidx,
+                                 const void* queries, int64_t nq, const int64_t* exclude_ids,
+                                 int32_t k, float tau, int32_t W, int32_t nprobe_max,
+                                 int32_t lookahead, int64_t* out_ids, float* out_scores,
+                                 int32_t* out_probes, sieve_stats* stats, void* stream) {
+  g_err.clear();
+  if (!idxs || nidx < 1 || nidx > SIEVE_MULTI_MAX)
+    return fail(SIEVE_EINVAL, "idxs must hold 1 .. %d index handles", SIEVE_MULTI_MAX);
+  for (int32_t i = 0; i < nidx; ++i) {
+    if (!idxs[i]) return fail(SIEVE_EINVAL, "idxs[%d] is NULL", i);
+    if (idxs[i]->dtype != idxs[0]->dtype || idxs[i]->d != idxs[0]->d ||
+        idxs[i]->device != idxs[0]->device)
+      return fail(SIEVE_EINVAL, "idxs[%d] differs from idxs[0] in dtype, d or device", i);
+  }
+  int st = check_common(idxs[0], queries, nq, k, tau, out_ids, out_scores, out_probes);
+  if (st) return st;
+  if (W < 1) return fail(SIEVE_EINVAL, "W = %d must be >= 1", W);
+  if (nprobe_max < 1) return fail(SIEVE_EINVAL, "nprobe_max = %d must be >= 1", nprobe_max);
+  if (lookahead < 0 || lookahead > 2) return fail(SIEVE_EINVAL, "lookahead must be 0, 1 or 2");
+  std::vector<SearchPlan> plans((size_t)nidx);
+  for (int32_t i = 0; i < nidx; ++i) {
+    sieve_index* ix = const_cast<sieve_index*>(idxs[i]);
+    if ((st = plan_search(ix, nq, k, tau, W, nprobe_max, lookahead == 1 ? 0 : 1, &plans[i])))
+      return st;
+    if (lookahead == 2) plans[i].group_q = 1;
+  }
+  if (stats) memset(stats, 0, sizeof(*stats));
+  if (nq == 0) return SIEVE_OK;
+  hipStream_t s = (hipStream_t)stream;
+  // per-index results, [nidx][nq][k], in the first index's workspace
+  sieve_index* ws = const_cast<sieve_index*>(idxs[0]);
+  const size_t rows = (size_t)nidx * (size_t)nq;
+  if ((st = ensure(ws->mix_ids, rows * k * sizeof(int64_t))) ||
+      (st = ensure(ws->mix_scores, rows * k * sizeof(float))) ||
+      (st = ensure(ws->mix_probes, rows * sizeof(int32_t))))
+    return st;
+  int64_t* mids = (int64_t*)ws->mix_ids.p;
+  float* msc = (float*)ws->mix_scores.p;
+  int32_t* mpr = (int32_t*)ws->mix_probes.p;
+  sieve_stats part;
+  for (int32_t i = 0; i < nidx; ++i) {
+    sieve_index* ix = const_cast<sieve_index*>(idxs[i]);
+    const size_t r0 = (size_t)i * (size_t)nq;
+    if ((st = search_impl(ix, queries, nq, exclude_ids, plans[i], nullptr, mids + r0 * k,
+                          msc + r0 * k, mpr + r0, stats ? &part : nullptr, s)))
+      return st;
+    if (stats) add_stats(stats, part);
+  }
+  HIP_TRY(launch_merge_shards(nq, k, nidx, mids, msc, mpr, out_ids, out_scores, out_probes, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  if (stats) stats->nprobe_eff = plans[0].n;
   return SIEVE_OK;
 }
 

@@ -194,6 +194,11 @@ hipError_t launch_topk(int64_t nq, int32_t k, const Hit* sorted, const int32_t* 
                        const int32_t* hcount, const int32_t* probes_src, int32_t probes_const,
                        const int32_t* out_map, int64_t* out_ids, float* out_scores,
                        int32_t* out_probes, int32_t* out_rank, RoundCounters* rc, hipStream_t s);
+// Best k of nshard per-index top-k lists per query ([nshard][nq][k], id -1
+// padding) and the sum of the per-index probe counts ([nshard][nq]).
+hipError_t launch_merge_shards(int64_t nq, int32_t k, int32_t nshard, const int64_t* sids,
+                               const float* sscores, const int32_t* sprobes, int64_t* out_ids,
+                               float* out_scores, int32_t* out_probes, hipStream_t s);
 // ---- in-call window calibration (Algorithm 3) ----
 hipError_t launch_gather_i64(const int32_t* idx, int64_t n, const int64_t* src, int64_t* dst,
                              hipStream_t s);

@@ -228,7 +228,69 @@ __global__ __launch_bounds__(256) void topk_kernel(int64_t nq, int32_t k,
   }
 }
 
+// Multi-index merge: one wave per query takes the nshard per-index top-k
+// lists (rows of sids / sscores, shard-major [nshard][nq][k], padded with
+// id -1), keeps the best k in the same total order, and sums the per-index
+// probe counts.
+__global__ __launch_bounds__(256) void merge_shards_kernel(int64_t nq, int32_t k,
+                                                           int32_t nshard,
+                                                           const int64_t* __restrict__ sids,
+                                                           const float* __restrict__ sscores,
+                                                           const int32_t* __restrict__ sprobes,
+                                                           int64_t* __restrict__ out_ids,
+                                                           float* __restrict__ out_scores,
+                                                           int32_t* __restrict__ out_probes) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const Cand none = {-INFINITY, 0x7fffffffffffffffll, -1};
+  for (int64_t q = (int64_t)blockIdx.x * 4 + wave; q < nq; q += (int64_t)gridDim.x * 4) {
+    const int m = nshard * k;  // candidates of this query, shard by shard
+    Cand top = none;
+    for (int b = 0; b < m; b += 64) {
+      Cand c = none;
+      const int j = b + lane;
+      if (j < m) {
+        const int sh = j / k, r = j - sh * k;
+        const int64_t at = ((int64_t)sh * nq + q) * k + r;
+        const int64_t id = sids[at];
+        if (id >= 0) {
+          c.s = sscores[at];
+          c.id = id;
+        }
+      }
+      c = wave_sort_desc<false>(c, lane);
+      if (b == 0) {
+        top = c;
+      } else {
+        const Cand rv = shfl_cand<false>(c, 63 - lane);
+        top = better(top, rv) ? top : rv;
+        top = wave_merge_desc<false>(top, lane);
+      }
+    }
+    if (lane < k) {
+      const bool real = top.id != none.id;
+      out_ids[q * k + lane] = real ? (int64_t)top.id : -1;
+      out_scores[q * k + lane] = real ? top.s : -INFINITY;
+    }
+    if (lane == 0) {
+      int32_t p = 0;
+      for (int sh = 0; sh < nshard; ++sh) p += sprobes[(int64_t)sh * nq + q];
+      out_probes[q] = p;
+    }
+  }
+}
+
 }  // namespace
+
+hipError_t launch_merge_shards(int64_t nq, int32_t k, int32_t nshard, const int64_t* sids,
+                               const float* sscores, const int32_t* sprobes, int64_t* out_ids,
+                               float* out_scores, int32_t* out_probes, hipStream_t s) {
+  if (nq <= 0) return hipSuccess;
+  const int64_t want = (nq + 3) / 4;
+  const unsigned blocks = (unsigned)(want < 4096 ? want : 4096);
+  hipLaunchKernelGGL(merge_shards_kernel, dim3(blocks), dim3(256), 0, s, nq, k, nshard, sids,
+                     sscores, sprobes, out_ids, out_scores, out_probes);
+  return hipGetLastError();
+}
 
 size_t exclusive_scan_tmp_elems(int64_t n) { return (size_t)((n + kScanTile - 1) / kScanTile) + 1; }
 

@@ -29,7 +29,7 @@ def declared_symbols():
 def test_header_declares_the_boundary():
     syms = declared_symbols()
     for s in ("sieve_load_index", "sieve_search", "sieve_search_fixed", "sieve_search_calibrated",
-              "sieve_free_index", "sieve_last_error"):
+              "sieve_search_multi", "sieve_free_index", "sieve_last_error"):
         assert s in syms
 
 
@@ -71,6 +71,9 @@ def test_argument_errors_without_a_gpu(lib):
     rc = lib.sieve_search_calibrated(None, None, 0, None, 10, 0.9, 32, None, 0, 0.005, 8, None,
                                      None, None, ctypes.byref(w), None, None)
     assert rc == -1 and w.value == -7
+    rc = lib.sieve_search_multi(None, 0, None, 0, None, 10, 0.9, 8, 32, 1, None, None, None,
+                                None, None)
+    assert rc == -1
     h = ctypes.c_void_p()
     rc = lib.sieve_load_index(None, 0, 10, 64, None, 4, None, None, None, ctypes.byref(h))
     assert rc == -1 and h.value is None

@@ -164,6 +164,55 @@ def test_full_probe_equals_exact_filtered_topk(seed, oracle_lib):
             assert r.probes[i] == nlist
 
 
+def _shard(w, parts, seed):
+    """Split an index's rows into `parts` independently built indexes (same centroids, each
+    row kept in its list), ids unchanged."""
+    rng = np.random.default_rng(seed)
+    owner = rng.integers(0, parts, len(w["ids"]))
+    off = np.asarray(w["list_offsets"])
+    lists = np.repeat(np.arange(len(off) - 1), np.diff(off))
+    out = []
+    for p in range(parts):
+        rows = np.nonzero(owner == p)[0]  # ascending: lists stay contiguous and in order
+        cnt = np.bincount(lists[rows], minlength=len(off) - 1)
+        out.append({"vectors": np.ascontiguousarray(w["vectors"][rows]),
+                    "ids": np.ascontiguousarray(w["ids"][rows]),
+                    "list_offsets": np.concatenate([[0], np.cumsum(cnt)]).astype(np.int64),
+                    "centroids": w["centroids"]})
+    return out
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_multi_index_full_probe_equals_exact_filtered_topk(seed, oracle_lib):
+    """Multi-index search (Sec. 6.1's shards): with no early stop and every list probed in
+    every shard, the merged result is the exact filtered top-k over the union of the shards,
+    and probes add up over the shards."""
+    w = random_index(seed, empty_lists=0)
+    nlist = w["centroids"].shape[0]
+    shards = _shard(w, 3, seed)
+    r = oracle.search_multi(shards, w["queries"], w["exclude_ids"], 7, 0.8, oracle.W_INF, nlist)
+    for i in range(len(w["queries"])):
+        ei, es, _ = np_filtered_topk(w["vectors"], w["ids"], w["queries"][i],
+                                     w["exclude_ids"][i], 0.8, 7)
+        assert np.array_equal(r.ids[i], ei)
+        fin = np.isfinite(es)
+        assert np.allclose(r.scores[i][fin], es[fin], atol=1e-12, rtol=0)
+        assert r.probes[i] == 3 * nlist
+
+
+def test_multi_index_keeps_each_shards_stop_rule(tiny):
+    """Each shard stops on its own: the merged probes are the sum of the shards' searches
+    run alone, and one shard alone gives its own result back."""
+    shards = _shard(tiny, 2, 5)
+    args = (tiny["queries"], tiny["exclude_ids"], 10, 0.9, 3, 12)
+    r = oracle.search_multi(shards, *args)
+    alone = [oracle.search(sh["vectors"], sh["list_offsets"], sh["ids"], sh["centroids"], *args)
+             for sh in shards]
+    assert np.array_equal(r.probes, alone[0].probes + alone[1].probes)
+    one = oracle.search_multi(shards[:1], *args)
+    assert np.array_equal(one.ids, alone[0].ids)
+
+
 @pytest.mark.parametrize("W", [1, 2, 3, 5, 12])
 def test_probes_match_replay_and_closed_form(tiny, W):
     r = run(tiny, W=W, nprobe_max=12)
