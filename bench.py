@@ -89,6 +89,14 @@ def main():
     ap.add_argument("--concurrency", action="store_true",
                     help="queries per call in {1, 10, 100, 1000, 10000} on the 1M x 128 data, "
                          "for lookahead, basic and serial dispatch (one JSON line)")
+    ap.add_argument("--multi", action="store_true",
+                    help="multi-index search: the 100M x 128 data split into 16 coarse shards, "
+                         "each its own IVF with its own stop rule, one global top-k; against "
+                         "fixed probing of every shard (one JSON line)")
+    ap.add_argument("--multi-shards", type=int, default=16)
+    ap.add_argument("--multi-nprobe", type=int, default=64,
+                    help="per-shard nprobe of the fixed baseline and per-shard cap of the "
+                         "threshold search")
     ap.add_argument("--sweep", action="store_true",
                     help="W / lookahead / tau / fixed-nprobe sweep with recall on the 1M x 128 "
                          "data (prints one JSON line with the table)")
@@ -111,6 +119,8 @@ def main():
         return envelope(args, ps, sw, np, torch, dev)
     if args.concurrency:
         return concurrency(args, ps, sw, np, torch, dev)
+    if args.multi:
+        return multi(args, ps, sw, np, torch, dev)
     spec = sw.SPECS[args.config]
     log(f"[bench] generating {args.config} on {dev}")
     t0 = time.time()
@@ -428,6 +438,78 @@ def concurrency(args, ps, sw, np, torch, dev):
            "config": {"workload": workload_name(spec), "W": spec.W,
                       "nprobe_max": spec.nprobe_max},
            "concurrency": rows}
+    print(json.dumps(out), flush=True)
+
+
+def _coarse_groups(torch, centroids, groups, iters=15, seed=7):
+    """Lloyd's k-means over the list centroids (fp32, seeded): each list goes to one coarse
+    group, so each group is a set of whole lists."""
+    c = centroids.float()
+    g = torch.Generator(device=c.device).manual_seed(seed)
+    cen = c[torch.randperm(c.shape[0], generator=g, device=c.device)[:groups]].clone()
+    for _ in range(iters):
+        a = torch.argmax(c @ cen.T, dim=1)
+        for j in range(groups):
+            m = a == j
+            if bool(m.any()):
+                v = c[m].sum(0)
+                cen[j] = v / v.norm().clamp_min(1e-12)
+    return torch.argmax(c @ cen.T, dim=1)
+
+
+def multi(args, ps, sw, np, torch, dev):
+    """Multi-index search (Sec. 6.1's public 100M layout: coarse k-means shards, each with its
+    own IVF; every shard searched with its own stop rule, one global top-k merge) on one GPU.
+    The 100M x 128 fp16 data's lists are grouped into coarse shards by k-means over their
+    centroids; each shard keeps its lists (so every row stays with its nearest centroid).
+    Threshold search W = 8 with lookahead, per-shard cap = the fixed baseline's per-shard
+    nprobe; overlap = pooled fraction of the fixed-probe output returned."""
+    spec = sw.SPECS["c5"]
+    S, P = args.multi_shards, args.multi_nprobe
+    log(f"[multi] generating c5 on {dev}")
+    w = sw.make(spec, device=dev)
+    off = w.list_offsets
+    counts = off[1:] - off[:-1]
+    grp = _coarse_groups(torch, w.centroids, S)
+    row_grp = torch.repeat_interleave(grp, counts)
+    ixs, sizes = [], []
+    for j in range(S):
+        lists = torch.nonzero(grp == j).flatten()
+        if lists.numel() == 0:
+            continue
+        rows = torch.nonzero(row_grp == j).flatten()  # ascending: lists stay whole, in order
+        loff = torch.zeros(lists.numel() + 1, dtype=torch.int64, device=dev)
+        loff[1:] = torch.cumsum(counts[lists], 0)
+        ixs.append(ps.Index(w.vectors[rows], loff, w.ids[rows], w.centroids[lists]))
+        sizes.append((int(lists.numel()), int(rows.numel())))
+        del rows, loff
+    del row_grp
+    torch.cuda.synchronize()
+    log(f"[multi] {len(ixs)} shards (lists, rows): {sizes}")
+    steps = max(1, args.steps // 4)
+    r, sec = _timed(torch, lambda: ps.search_multi(ixs, w.queries, w.exclude_ids, spec.k,
+                                                   spec.tau, spec.W, P, with_stats=True), steps)
+    f, fsec = _timed(torch, lambda: ps.search_multi(ixs, w.queries, w.exclude_ids, spec.k,
+                                                    spec.tau, 0x7FFFFFFF, P), steps)
+    a, b = r[0].cpu().numpy(), f[0].cpu().numpy()
+    tot = int((b >= 0).sum())
+    kept = int(sum(np.intersect1d(x[x >= 0], y[y >= 0]).size for x, y in zip(a, b)))
+    st = r[3]
+    row = {"shards": len(ixs), "per_shard_nprobe": P, "qps": round(spec.nq / sec, 1),
+           "fixed_qps": round(spec.nq / fsec, 1), "speedup": round(fsec / sec, 3),
+           "mean_probes": round(float(r[2].double().mean()), 3),
+           "fixed_probes": int(f[2][0]), "candidates": int(st.hits),
+           "overlap_with_fixed": round(kept / tot, 5) if tot else None,
+           "ms_rank": round(st.ms_rank, 2), "ms_scan": round(st.ms_scan, 2),
+           "ms_total": round(st.ms_total, 2)}
+    log(f"[multi] {row}")
+    for ix in ixs:
+        ix.close()
+    out = {"metric": "multi-index threshold search: queries/s and speedup over fixed probing",
+           "config": {"workload": workload_name(spec), "shards": len(ixs),
+                      "shard_lists": [x[0] for x in sizes], "shard_rows": [x[1] for x in sizes],
+                      "W": spec.W, "per_shard_nprobe": P},
+           "steps": steps, "multi": row}
     print(json.dumps(out), flush=True)
 
 
