@@ -399,8 +399,9 @@ def test_rank_and_search_on_large_centroid_sets(nlist, d, dtype, rank_path):
 @pytest.mark.parametrize("R", [8, 32, 33, 64])
 def test_rank_prefix_on_many_work_groups(R, rank_path):
     """128-dim fp16 queries on a large centroid set: the fused prefix keeps the queries of
-    each wave in registers, 512 queries per work-group; 1,100 queries span three
-    work-groups, the last one ragged; R = 32 and 33 straddle the two kept-value widths."""
+    each wave in registers, 128 queries per work-group; 1,100 queries span nine
+    work-groups, the last one ragged (76 queries); R runs from 8 to the 64-rank maximum
+    of the fused prefix."""
     rng = np.random.default_rng(900 + R)
     nlist, d, nq = 1800, 128, 1100
     C = rng.standard_normal((nlist, d))
