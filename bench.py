@@ -88,7 +88,8 @@ def main():
                          "fixed-probe output (one JSON line)")
     ap.add_argument("--concurrency", action="store_true",
                     help="queries per call in {1, 10, 100, 1000, 10000} on the 1M x 128 data, "
-                         "for lookahead, basic and serial dispatch (one JSON line)")
+                         "for lookahead, basic and serial dispatch and fixed probing (one JSON "
+                         "line)")
     ap.add_argument("--multi", action="store_true",
                     help="multi-index search: the 100M x 128 data split into 16 coarse shards, "
                          "each its own IVF with its own stop rule, one global top-k; against "
@@ -258,6 +259,7 @@ def main():
         "partition_vectors_per_s": round(st.vectors_scanned * args.steps / t_sieve, 1),
         "scan_hbm_gbs": round(gbs, 1),
         "mean_probes": round(float(probes.float().mean().item()), 3),
+        "scanned_probes_per_query": round(st.items / nq, 3),
         "rounds": st.rounds,
         "phase_ms": {k: round(mean(stats, "ms_" + k), 4) for k in
                      ("rank", "sched", "scan", "update", "finalize", "total")},
@@ -398,6 +400,7 @@ def envelope(args, ps, sw, np, torch, dev):
         rows.append({"k": k, "tau": tau, "qps": round(spec.nq / sec, 1),
                      "fixed_qps": round(spec.nq / fsec, 1), "speedup": round(fsec / sec, 3),
                      "mean_probes": round(float(r[2].float().mean()), 3),
+                     "scanned_probes_per_query": round(r[3].items / spec.nq, 3),
                      "candidates": int(r[3].hits), "rounds": int(r[3].rounds),
                      "overlap_with_fixed": round(kept / tot, 5) if tot else None})
         log(f"[envelope] {rows[-1]}")
@@ -422,19 +425,26 @@ def concurrency(args, ps, sw, np, torch, dev):
         calls = min(200, spec.nq // per)
         row = {"queries_per_call": per, "calls": calls}
         for name, kw in (("lookahead", dict(lookahead=True)), ("basic", dict(lookahead=False)),
-                         ("serial", dict(serial=True))):
+                         ("serial", dict(serial=True)), ("fixed", None)):
             def run():
                 for c in range(calls):
                     q0 = c * per
-                    r = ix.search(w.queries[q0:q0 + per], w.exclude_ids[q0:q0 + per], spec.k,
-                                  spec.tau, spec.W, spec.nprobe_max, **kw)
+                    q, ex = w.queries[q0:q0 + per], w.exclude_ids[q0:q0 + per]
+                    if kw is None:
+                        r = ix.search_fixed(q, ex, spec.k, spec.tau, spec.fixed_nprobe)
+                    else:
+                        r = ix.search(q, ex, spec.k, spec.tau, spec.W, spec.nprobe_max, **kw)
                 return r
             _, sec = _timed(torch, run, 1)
             row[name + "_qps"] = round(calls * per / sec, 1)
+        row["lookahead_vs_fixed"] = round(row["lookahead_qps"] / row["fixed_qps"], 3)
+        row["basic_vs_fixed"] = round(row["basic_qps"] / row["fixed_qps"], 3)
+        row["serial_vs_fixed"] = round(row["serial_qps"] / row["fixed_qps"], 3)
         rows.append(row)
         log(f"[concurrency] {row}")
     ix.close()
-    out = {"metric": "queries/s by queries per call (W=8): lookahead, basic and serial dispatch",
+    out = {"metric": "queries/s by queries per call (W=8): lookahead, basic and serial dispatch, "
+                     "and fixed probing",
            "config": {"workload": workload_name(spec), "W": spec.W,
                       "nprobe_max": spec.nprobe_max},
            "concurrency": rows}

@@ -93,7 +93,7 @@ struct sieve_index {
   Buf scores, P, items, bucket, tiles, cnt, item_off, cursor, tile_off, rc, state_a, state_b,
       lmax, hcount, hoff, hcur, scan_tmp, pool, pool_sorted, arenas, have, ext, qext, Pext,
       cand, ccount, cal_idx, cal_q, cal_x, cal_bits, cal_rank, cal_hist, mix_ids, mix_scores,
-      mix_probes;
+      mix_probes, spec_bits;
   int64_t pool_cap = 0;
   RoundCounters* rc_host = nullptr;
   // phase timing (only when stats are requested): events are recorded on the
@@ -172,6 +172,21 @@ int env_int(const char* name, int dflt) {
   return x > 0 ? x : dflt;
 }
 
+// A count that may be zero.
+int env_count(const char* name, int dflt) {
+  const char* v = getenv(name);
+  if (!v || !*v) return dflt;
+  const int x = atoi(v);
+  return x >= 0 ? x : dflt;
+}
+
+// An on/off switch: "0" turns it off, any other value on.
+bool env_flag(const char* name, bool dflt) {
+  const char* v = getenv(name);
+  if (!v || !*v) return dflt;
+  return atoi(v) != 0;
+}
+
 int row_chunk_for(const sieve_index* ix, const char* knob, int dflt) {
   // the scan addresses a tile's rows with 32-bit byte offsets
   const int64_t row_bytes = (int64_t)ix->d * elem_bytes(ix->dtype);
@@ -213,6 +228,11 @@ struct SearchPlan {
   bool wide;           // wide scan configuration (see tile_rows_wide)
   int scan_grid;       // scan work-groups (fixed for the whole search)
   bool wide_rank;      // rank with room for every boundary near-tie (retry path)
+  bool spec;           // lookahead with speculative issue past the stop line
+  int spec_round;      // first round whose update speculates
+  int spec_max;        // ranks issued past the stop line, at most
+  int spec_min;        // a line must move at least this far to speculate
+  int hit_words;       // 32-bit words per query of the rank bitmap (spec)
 };
 
 int check_common(const sieve_index* ix, const void* queries, int64_t nq, int32_t k, float tau,
@@ -255,6 +275,7 @@ int grow_workspace(sieve_index* ix, const SearchPlan& pl) {
       (st = ensure(ix->hoff, qn)) || (st = ensure(ix->hcur, qn)))
     return st;
   if ((st = ensure(ix->scan_tmp, exclusive_scan_tmp_elems(nq) * 4))) return st;
+  if (pl.spec && (st = ensure(ix->spec_bits, (size_t)nq * pl.hit_words * 4))) return st;
   if ((st = ensure(ix->arenas, (size_t)pl.scan_grid * sizeof(ArenaRec)))) return st;
   // arena runs can leave up to kArenaMax unused slots per scan work-group
   const int64_t slack = (int64_t)pl.scan_grid * kArenaMax;
@@ -411,6 +432,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     HIP_TRY(launch_fill_i32((int32_t*)ix->cnt.p, ix->nlist, 0, s));
     HIP_TRY(launch_fill_i32((int32_t*)ix->hcount.p, nq, 0, s));
     if (cal) HIP_TRY(launch_zero_bytes(cal->hitbits, (size_t)nq * cal->words * 4, s));
+    bool spec_used = false;  // a round kept the rank bitmap (its ranks may pass stop lines)
     int32_t* P = (int32_t*)ix->P.p;
 
     if (pl.mode != 2) {
@@ -424,14 +446,24 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
       span(ix, kRank, r0, mark(ix, timed, s));
       int64_t n_items = nq * s0;
       while (n_items > 0) {
+        // speculative issue from round spec_round on: its scans keep the rank bitmap
+        const bool spec_now = pl.spec && rounds >= pl.spec_round;
+        if (spec_now && !spec_used) {
+          HIP_TRY(launch_zero_bytes(ix->spec_bits.p, (size_t)nq * pl.hit_words * 4, s));
+          sa.hitbits = (uint32_t*)ix->spec_bits.p;
+          sa.hit_words = pl.hit_words;
+          spec_used = true;
+        }
         if ((st = run_round(ix, sa, (int)n_items, 0, P, pl, s, timed))) return st;
         const int u0 = mark(ix, timed, s);
         int32_t* have = (int32_t*)ix->have.p;
         int32_t* ext = (int32_t*)ix->ext.p;
         if (pl.mode == 0)
-          HIP_TRY(launch_update_lookahead(nq, P, pl.n, pl.W, (int32_t*)ix->state_a.p,
-                                          (int32_t*)ix->lmax.p, have, ext, (Item*)ix->items.p,
-                                          (int32_t*)ix->cnt.p, rc, s));
+          HIP_TRY(launch_update_lookahead(
+              nq, P, pl.n, pl.W, (int32_t*)ix->state_a.p, (int32_t*)ix->lmax.p, have, ext,
+              (Item*)ix->items.p, (int32_t*)ix->cnt.p, rc, spec_now ? sa.hitbits : nullptr,
+              sa.hit_words, pl.spec ? (int32_t*)ix->state_b.p : nullptr, pl.spec_max,
+              pl.spec_min, s));
         else
           HIP_TRY(launch_update_basic(nq, P, pl.n, pl.W, (int32_t*)ix->state_a.p,
                                       (int32_t*)ix->state_b.p, (int32_t*)ix->lmax.p, have, ext,
@@ -456,7 +488,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
           HIP_TRY(launch_scatter_ranks(ext, n_ext, (const int32_t*)ix->Pext.p, pl.n, P, s));
           HIP_TRY(launch_emit_pending(ext, n_ext, pl.mode, P, pl.n, (const int32_t*)ix->state_a.p,
                                       have, pl.n, (Item*)ix->items.p, (int32_t*)ix->cnt.p, rc,
-                                      s));
+                                      pl.spec ? (int32_t*)ix->state_b.p : nullptr, s));
           span(ix, kRank, x0, mark(ix, timed, s));
           HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost,
                                  s));
@@ -510,13 +542,14 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     HIP_TRY(launch_exclusive_scan((const int32_t*)ix->hcount.p, (int32_t*)ix->hoff.p,
                                   (int32_t*)ix->hcur.p, nq, (int32_t*)ix->scan_tmp.p, s));
     HIP_TRY(launch_pool_scatter((const Hit*)ix->pool.p, hits, (int32_t*)ix->hcur.p,
-                                (Hit*)ix->pool_sorted.p, cal != nullptr, s));
+                                (Hit*)ix->pool_sorted.p, cal != nullptr || spec_used, s));
     const int32_t* probes_src = pl.mode == 0   ? (const int32_t*)ix->state_a.p
                                 : pl.mode == 1 ? (const int32_t*)ix->state_b.p
                                                : nullptr;
     HIP_TRY(launch_topk(nq, pl.k, (const Hit*)ix->pool_sorted.p, (const int32_t*)ix->hoff.p,
                         (const int32_t*)ix->hcount.p, probes_src, pl.n, out_map, out_ids,
-                        out_scores, out_probes, cal ? cal->frank : nullptr, rc, s));
+                        out_scores, out_probes, cal ? cal->frank : nullptr,
+                        spec_used ? (const int32_t*)ix->state_a.p : nullptr, rc, s));
     const int f1 = mark(ix, timed, s);
     span(ix, kFinal, f0, f1);
     span(ix, kTotal, t_begin, f1);
@@ -581,6 +614,18 @@ int plan_search(const sieve_index* ix, int64_t nq, int32_t k, float tau, int32_t
       row_chunk_for(ix, "SIEVE_ROW_CHUNK_DENSE", avg_len <= 2048 ? 4096 : pl->row_chunk);
   if (pl->row_chunk_dense < pl->row_chunk) pl->row_chunk_dense = pl->row_chunk;
   pl->dense_q = env_int("SIEVE_DENSE_Q", 64);
+  // Speculative issue needs the rank packed beside the query in pool entries
+  // (queries < 2^kRankShift) and a stop rule that can stop early (W < n).
+  pl->spec = mode == 0 && W < pl->n && nq <= (int64_t)kQueryMask + 1 &&
+             env_flag("SIEVE_SPECULATE", true);
+  pl->spec_max = pl->spec ? (int)std::min<int64_t>(pl->n, 3ll * W) : 0;
+  // Lines that move far keep moving (queries in large near-duplicate groups):
+  // speculating for those merges their next ranks into the larger, earlier
+  // rounds, where a list read serves more queries.  Short moves are common
+  // and mostly final; speculating there reads extra lists for nothing.
+  pl->spec_round = env_count("SIEVE_SPEC_ROUND", 0);
+  pl->spec_min = env_int("SIEVE_SPEC_MIN", std::max(1, W / 2));
+  pl->hit_words = (pl->n + 31) / 32;
   pl->scan_grid = pl->wide ? ((ix->cus + 7) / 8) * 8 : scan_grid(ix, pl->tile_q);
   // Lazy ranking: a stop line starts at min(W, n) and mostly stays near it,
   // so only the first r0 ranks are ordered up front (queries whose stop line
@@ -603,7 +648,10 @@ int plan_search(const sieve_index* ix, int64_t nq, int32_t k, float tau, int32_t
   } else {
     pl->fix_chunk = 0;
     const int s0 = mode == 0 ? (W < pl->n ? W : pl->n) : 1;
-    pl->item_cap = nq * (int64_t)s0;
+    // A lookahead update issues at most W ranks up to the new stop line
+    // (every line comes from a hit below the old one) and, speculating, at
+    // most spec_max more past it.
+    pl->item_cap = nq * (int64_t)std::min<int64_t>(pl->n, (int64_t)s0 + pl->spec_max);
     if (pl->item_cap > INT32_MAX)
       return fail(SIEVE_EUNSUPPORTED, "nq * min(W, n) = %lld exceeds int32", (long long)pl->item_cap);
   }

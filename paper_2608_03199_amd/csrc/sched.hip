@@ -52,6 +52,7 @@ __global__ void emit_initial_kernel(const int32_t* __restrict__ P, int32_t n, in
   }
   if (mode == 0) {
     state_a[q] = s0;
+    state_b[q] = s0;  // ranks issued (speculative issue)
     lmax[q] = 0;
   } else if (mode == 1) {
     state_a[q] = 0;  // next (0-based rank in flight)
@@ -184,29 +185,83 @@ __global__ void update_lookahead_kernel(int64_t nq, const int32_t* __restrict__ 
                                         int32_t* __restrict__ lmax,
                                         const int32_t* __restrict__ have,
                                         int32_t* __restrict__ ext, Item* __restrict__ items,
-                                        int32_t* __restrict__ cnt, RoundCounters* rc) {
+                                        int32_t* __restrict__ cnt, RoundCounters* rc,
+                                        const uint32_t* __restrict__ hitbits, int32_t words,
+                                        int32_t* __restrict__ issued, int32_t spec_max,
+                                        int32_t spec_min) {
   const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (q >= nq) return;
   const int L = lmax[q];  // 1-based highest hit rank of this round, 0 = none
   if (L == 0) return;
   lmax[q] = 0;
   const int s = stop[q];
-  const int reach = (W > n - L) ? n : L + W;  // min(L + W, n) without overflow
-  if (reach <= s) return;
   const int hv = have[q];
-  const int e0 = min(s, hv), e1 = min(reach, hv);  // emitted so far / after this update
-  if (e1 > e0) {
-    const int base = atomicAdd(&rc->new_items, e1 - e0);
-    for (int j = e0; j < e1; ++j) {
+  if (!hitbits) {
+    // committed ranks only (issued, when kept, stays equal to the emitted end)
+    const int reach = (W > n - L) ? n : L + W;  // min(L + W, n) without overflow
+    if (reach <= s) return;
+    const int e0 = min(s, hv), e1 = min(reach, hv);  // emitted so far / after this update
+    if (e1 > e0) {
+      const int base = atomicAdd(&rc->new_items, e1 - e0);
+      for (int j = e0; j < e1; ++j) {
+        Item it;
+        it.q = (int32_t)q;
+        it.rank = j;
+        items[base + (j - e0)] = it;
+        atomicAdd(&cnt[P[q * n + j]], 1);
+      }
+      if (issued) issued[q] = e1;
+    }
+    if (reach > hv) ext[atomicAdd(&rc->n_ext, 1)] = (int32_t)q;
+    stop[q] = reach;
+    return;
+  }
+  // Speculative issue.  Ranks [0, i) are scanned, some of them past the stop
+  // line s.  Replay the stop rule over the hit ranks in order: a hit at rank
+  // r counts only once the line has reached it (r < s'), and then moves the
+  // line to min(r + 1 + W, n).  Hits below s - W were counted by earlier
+  // updates (every line so far came from a hit at most W below it): counting
+  // one again changes nothing, and so does a missing bit there (ranks scanned
+  // before the bitmap was kept).  The bits of this round's ranks are all set.
+  const int i = issued[q];
+  const uint32_t* bits = hitbits + q * words;
+  int reach = s;
+  int bound = min(reach, i);
+  for (int j = s > W ? s - W : 0; j < bound;) {
+    const int w = j >> 5;
+    uint32_t b = bits[w] & (~0u << (j & 31));
+    while (b) {
+      const int r = (w << 5) + __builtin_ctz(b);
+      if (r >= bound) break;
+      const int to = (W > n - (r + 1)) ? n : r + 1 + W;
+      if (to > reach) {
+        reach = to;
+        bound = min(reach, i);
+      }
+      b &= b - 1;
+    }
+    j = (w + 1) << 5;
+  }
+  stop[q] = reach;
+  if (reach <= i) return;  // the line ends inside the scanned ranks: stopped
+  // The line passed the scanned ranks: issue up to it and, when it moved by
+  // at least spec_min ranks in this update, as far again (at most spec_max)
+  // past it.
+  const int adv = reach - s >= spec_min ? min(reach - s, spec_max) : 0;
+  const int tgt = (adv > n - reach) ? n : reach + adv;
+  const int e1 = min(tgt, hv);
+  if (e1 > i) {
+    const int base = atomicAdd(&rc->new_items, e1 - i);
+    for (int j = i; j < e1; ++j) {
       Item it;
       it.q = (int32_t)q;
       it.rank = j;
-      items[base + (j - e0)] = it;
+      items[base + (j - i)] = it;
       atomicAdd(&cnt[P[q * n + j]], 1);
     }
+    issued[q] = e1;
   }
   if (reach > hv) ext[atomicAdd(&rc->n_ext, 1)] = (int32_t)q;
-  stop[q] = reach;
 }
 
 // next[q]: rank in flight (0-based) or -1 once stopped; on stopping,
@@ -275,7 +330,7 @@ __global__ void emit_pending_kernel(const int32_t* __restrict__ ext, int32_t n_e
                                     const int32_t* __restrict__ state_a,
                                     int32_t* __restrict__ have, int32_t new_have,
                                     Item* __restrict__ items, int32_t* __restrict__ cnt,
-                                    RoundCounters* rc) {
+                                    RoundCounters* rc, int32_t* __restrict__ issued) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n_ext) return;
   const int64_t q = ext[i];
@@ -299,6 +354,7 @@ __global__ void emit_pending_kernel(const int32_t* __restrict__ ext, int32_t n_e
       items[base + (j - e0)] = it;
       atomicAdd(&cnt[P[q * n + j]], 1);
     }
+    if (mode == 0 && issued) issued[q] = e1;  // e0 == issued[q]: the update stopped at have
   }
   have[q] = new_have > hv ? new_have : hv;
 }
@@ -354,9 +410,12 @@ hipError_t launch_sched_tiles(int32_t* cnt, const int32_t* item_off, const int32
 hipError_t launch_update_lookahead(int64_t nq, const int32_t* P, int32_t n, int32_t W,
                                    int32_t* stop, int32_t* lmax, const int32_t* have,
                                    int32_t* ext, Item* items, int32_t* cnt, RoundCounters* rc,
-                                   hipStream_t s) {
+                                   const uint32_t* hitbits, int32_t words, int32_t* issued,
+                                   int32_t spec_max, int32_t spec_min, hipStream_t s) {
+  if (hitbits && (!issued || words * 32 < n || spec_max < 0)) return hipErrorInvalidValue;
   hipLaunchKernelGGL(update_lookahead_kernel, dim3(blocks_for(nq)), dim3(kThreads), 0, s, nq, P, n,
-                     W, stop, lmax, have, ext, items, cnt, rc);
+                     W, stop, lmax, have, ext, items, cnt, rc, hitbits, words, issued, spec_max,
+                     spec_min);
   return hipGetLastError();
 }
 
@@ -392,10 +451,10 @@ hipError_t launch_scatter_ranks(const int32_t* ext, int32_t n_ext, const int32_t
 hipError_t launch_emit_pending(const int32_t* ext, int32_t n_ext, int32_t mode, const int32_t* P,
                                int32_t n, const int32_t* state_a, int32_t* have,
                                int32_t new_have, Item* items, int32_t* cnt, RoundCounters* rc,
-                               hipStream_t s) {
+                               int32_t* issued, hipStream_t s) {
   if (n_ext <= 0) return hipSuccess;
   hipLaunchKernelGGL(emit_pending_kernel, dim3(blocks_for(n_ext)), dim3(kThreads), 0, s, ext,
-                     n_ext, mode, P, n, state_a, have, new_have, items, cnt, rc);
+                     n_ext, mode, P, n, state_a, have, new_have, items, cnt, rc, issued);
   return hipGetLastError();
 }
 

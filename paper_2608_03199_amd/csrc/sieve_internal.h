@@ -156,10 +156,17 @@ hipError_t launch_sched_tiles(int32_t* cnt, const int32_t* item_off, const int32
 hipError_t launch_scan(int dtype, const ScanArgs& a, int32_t grid, hipStream_t s);
 // The updates emit ranks below have[q] (ranks already ordered in P) and
 // list the queries that need more in ext[] (count in rc->n_ext).
+// issued: null, or [nq] end of the issued ranks of each query (kept by every
+// update once given).  Speculative issue (hitbits non-null, issued required):
+// ranks past the stop line may already be scanned; hitbits ([nq][words], bit
+// r = the probe at rank r had a candidate, set for every rank scanned in the
+// round just finished) replays the stop rule over them.  A line that moved by
+// at least spec_min ranks gets as many more issued past it, at most spec_max.
 hipError_t launch_update_lookahead(int64_t nq, const int32_t* P, int32_t n, int32_t W,
                                    int32_t* stop, int32_t* lmax, const int32_t* have,
                                    int32_t* ext, Item* items, int32_t* cnt, RoundCounters* rc,
-                                   hipStream_t s);
+                                   const uint32_t* hitbits, int32_t words, int32_t* issued,
+                                   int32_t spec_max, int32_t spec_min, hipStream_t s);
 hipError_t launch_update_basic(int64_t nq, const int32_t* P, int32_t n, int32_t W, int32_t* next,
                                int32_t* stale, int32_t* lmax, const int32_t* have, int32_t* ext,
                                Item* items, int32_t* cnt, RoundCounters* rc, hipStream_t s);
@@ -172,7 +179,7 @@ hipError_t launch_scatter_ranks(const int32_t* ext, int32_t n_ext, const int32_t
 hipError_t launch_emit_pending(const int32_t* ext, int32_t n_ext, int32_t mode, const int32_t* P,
                                int32_t n, const int32_t* state_a, int32_t* have,
                                int32_t new_have, Item* items, int32_t* cnt, RoundCounters* rc,
-                               hipStream_t s);
+                               int32_t* issued, hipStream_t s);
 
 hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
 hipError_t launch_zero_bytes(void* p, int64_t bytes, hipStream_t s);
@@ -190,10 +197,13 @@ hipError_t launch_pool_scatter(const Hit* pool, int64_t n, int32_t* cursor, Hit*
 // row out_map[q] of out_ids / out_scores / out_probes).  out_rank: null, or
 // [nq * k] int32 (indexed by q, not mapped) receiving the 0-based rank each
 // returned candidate was found at (-1 for padding); needs packed pool entries.
+// rank_limit: null, or [nq] -- pool entries (packed) found at a rank >= the
+// query's limit are left out (speculatively scanned ranks past the stop line).
 hipError_t launch_topk(int64_t nq, int32_t k, const Hit* sorted, const int32_t* hoff,
                        const int32_t* hcount, const int32_t* probes_src, int32_t probes_const,
                        const int32_t* out_map, int64_t* out_ids, float* out_scores,
-                       int32_t* out_probes, int32_t* out_rank, RoundCounters* rc, hipStream_t s);
+                       int32_t* out_probes, int32_t* out_rank, const int32_t* rank_limit,
+                       RoundCounters* rc, hipStream_t s);
 // Best k of nshard per-index top-k lists per query ([nshard][nq][k], id -1
 // padding) and the sum of the per-index probe counts ([nshard][nq]).
 hipError_t launch_merge_shards(int64_t nq, int32_t k, int32_t nshard, const int64_t* sids,

@@ -178,6 +178,7 @@ __global__ __launch_bounds__(256) void topk_kernel(int64_t nq, int32_t k,
                                                    int32_t* __restrict__ out_probes,
                                                    const int32_t* __restrict__ out_map,
                                                    int32_t* __restrict__ out_rank,
+                                                   const int32_t* __restrict__ rank_limit,
                                                    RoundCounters* rc) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   __shared__ unsigned long long s_probes[4], s_cands[4];
@@ -186,14 +187,17 @@ __global__ __launch_bounds__(256) void topk_kernel(int64_t nq, int32_t k,
   for (int64_t q = (int64_t)blockIdx.x * 4 + wave; q < nq; q += (int64_t)gridDim.x * 4) {
     const int m = hcount[q];
     const int beg = m > 0 ? hoff[q] : 0;
+    const int lim = rank_limit ? rank_limit[q] : 0x7fffffff;
     Cand top = none;
     for (int b = 0; b < m; b += 64) {
       Cand c = none;
       if (b + lane < m) {
         const Hit h = sorted[beg + b + lane];
-        c.s = h.score;
-        c.id = h.id;
-        c.rank = kRank ? (h.q >> kRankShift) : 0;
+        if (!rank_limit || (h.q >> kRankShift) < lim) {
+          c.s = h.score;
+          c.id = h.id;
+          c.rank = kRank ? (h.q >> kRankShift) : 0;
+        }
       }
       c = wave_sort_desc<kRank>(c, lane);
       if (b == 0) {
@@ -327,18 +331,19 @@ hipError_t launch_pool_scatter(const Hit* pool, int64_t n, int32_t* cursor, Hit*
 hipError_t launch_topk(int64_t nq, int32_t k, const Hit* sorted, const int32_t* hoff,
                        const int32_t* hcount, const int32_t* probes_src, int32_t probes_const,
                        const int32_t* out_map, int64_t* out_ids, float* out_scores,
-                       int32_t* out_probes, int32_t* out_rank, RoundCounters* rc, hipStream_t s) {
+                       int32_t* out_probes, int32_t* out_rank, const int32_t* rank_limit,
+                       RoundCounters* rc, hipStream_t s) {
   if (nq <= 0) return hipSuccess;
   const int64_t want = (nq + 3) / 4;
   const unsigned blocks = (unsigned)(want < 4096 ? want : 4096);
   if (out_rank)
     hipLaunchKernelGGL(topk_kernel<true>, dim3(blocks), dim3(256), 0, s, nq, k, sorted, hoff,
                        hcount, probes_src, probes_const, out_ids, out_scores, out_probes,
-                       out_map, out_rank, rc);
+                       out_map, out_rank, rank_limit, rc);
   else
     hipLaunchKernelGGL(topk_kernel<false>, dim3(blocks), dim3(256), 0, s, nq, k, sorted, hoff,
                        hcount, probes_src, probes_const, out_ids, out_scores, out_probes,
-                       out_map, nullptr, rc);
+                       out_map, nullptr, rank_limit, rc);
   return hipGetLastError();
 }
 

@@ -89,6 +89,19 @@ def _check(c: Case, k, tau, W, nprobe, lookahead=True, fixed=False, nq=None, exc
     return g_ids, g_sc, g_pr, o
 
 
+@pytest.fixture
+def no_speculation():
+    """Lookahead issues only committed ranks (no speculative issue past the stop line), so
+    that it searches exactly the (query, partition) pairs the other dispatches search."""
+    old = os.environ.get("SIEVE_SPECULATE")
+    os.environ["SIEVE_SPECULATE"] = "0"
+    yield
+    if old is None:
+        del os.environ["SIEVE_SPECULATE"]
+    else:
+        os.environ["SIEVE_SPECULATE"] = old
+
+
 @pytest.mark.parametrize("name", ["tiny", "tiny16", "c1"])
 @pytest.mark.parametrize("lookahead", [True, False])
 def test_sieve_matches_oracle(name, lookahead):
@@ -106,7 +119,7 @@ def test_fixed_matches_oracle(name):
 
 @pytest.mark.parametrize("name", ["tiny16", "c1"])
 @pytest.mark.parametrize("W", [1, 2, 4, 16])
-def test_lookahead_invariance_and_window_sweep(name, W):
+def test_lookahead_invariance_and_window_sweep(name, W, no_speculation):
     c = case(name)
     s = c.w.spec
     a = c.gpu(s.k, s.tau, W, s.nprobe_max, lookahead=True, stats=True)
@@ -147,7 +160,7 @@ def short_rank_prefix():
 
 @pytest.mark.parametrize("name", ["tiny", "c1"])
 @pytest.mark.parametrize("W", [1, 2, 4])
-def test_lazy_rank_extension(name, W, short_rank_prefix, rank_path):
+def test_lazy_rank_extension(name, W, short_rank_prefix, rank_path, no_speculation):
     # tau = 0.5 makes cluster mates qualify in some queries, so stop lines go deep
     c = case(name)
     s = c.w.spec
@@ -165,7 +178,7 @@ def test_lazy_rank_extension(name, W, short_rank_prefix, rank_path):
 
 @pytest.mark.parametrize("name", ["tiny16", "c1"])
 @pytest.mark.parametrize("W", [1, 3, 8])
-def test_serial_traversal_matches_batched_dispatch(name, W):
+def test_serial_traversal_matches_batched_dispatch(name, W, no_speculation):
     """Serial traversal (Sec. 6.3's ablation baseline: one rank per query per round, no
     partition scan shared between queries) returns exactly what the batched dispatches
     return, and the oracle's result."""
@@ -184,6 +197,75 @@ def test_serial_traversal_matches_batched_dispatch(name, W):
     print(f"[gpu-test] serial {name} W={W} rounds {b[3].rounds} vs {a[3].rounds} -> {rep}",
           flush=True)
     assert_parity(rep)
+
+
+def _with_speculation(on, fn, first_round=0, spec_min=1):
+    """Run fn with speculative issue on or off, from round first_round on, for stop lines
+    that moved at least spec_min ranks (None: the library's default)."""
+    keys = ("SIEVE_SPECULATE", "SIEVE_SPEC_ROUND", "SIEVE_SPEC_MIN")
+    old = {k: os.environ.get(k) for k in keys}
+    os.environ["SIEVE_SPECULATE"] = "1" if on else "0"
+    os.environ["SIEVE_SPEC_ROUND"] = str(first_round)
+    if spec_min is None:
+        os.environ.pop("SIEVE_SPEC_MIN", None)
+    else:
+        os.environ["SIEVE_SPEC_MIN"] = str(spec_min)
+    try:
+        return fn()
+    finally:
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
+
+@pytest.mark.parametrize("name,tau", [("tiny", 0.9), ("tiny", 0.5), ("tiny16", 0.6),
+                                      ("c1", 0.9), ("c1", 0.5), ("c1", 0.3)])
+@pytest.mark.parametrize("W", [1, 2, 5, 8])
+@pytest.mark.parametrize("first_round,spec_min", [(0, 1), (1, 1), (2, 1), (0, None)])
+def test_speculative_issue_matches_committed_issue(name, tau, W, first_round, spec_min):
+    """Lookahead with speculative issue (ranks past the stop line scanned early, the stop
+    rule replayed over the per-rank hit bitmap, candidates past the final line dropped)
+    returns exactly what committed-only issue returns, and the oracle's result; it never
+    needs more rounds, and it searches a superset of the pairs.  first_round: the first
+    round whose update speculates (the earlier ones issue committed ranks only); spec_min:
+    the shortest move of a stop line that speculates (None: the default, W / 2)."""
+    c = case(name)
+    s = c.w.spec
+    q, ex = c.w.queries, c.w.exclude_ids
+    run = lambda: c.ix.search(q, ex, s.k, tau, W, s.nprobe_max, with_stats=True)
+    a = _with_speculation(True, run, first_round, spec_min)
+    b = _with_speculation(False, run)
+    for x, y in zip(a[:3], b[:3]):
+        assert torch.equal(x, y)
+    assert a[3].probes_total == b[3].probes_total == int(a[2].sum())
+    assert a[3].items >= b[3].items
+    assert a[3].rounds <= b[3].rounds
+    o = c.oracle(s.k, tau, W, s.nprobe_max)
+    rep = compare(a[0].cpu().numpy(), a[1].cpu().numpy(), a[2].cpu().numpy(), o)
+    print(f"[gpu-test] speculative {name} tau={tau} W={W} from round {first_round}, "
+          f"min move {spec_min}: "
+          f"rounds {a[3].rounds} vs "
+          f"{b[3].rounds}, items {a[3].items} vs {b[3].items} -> {rep}", flush=True)
+    assert_parity(rep)
+
+
+def test_speculative_issue_with_rank_extension(short_rank_prefix):
+    """Speculation stops at the ordered prefix; stop lines that pass it extend the order and
+    issue only committed ranks beyond it."""
+    c = case("c1")
+    s = c.w.spec
+    q, ex = c.w.queries, c.w.exclude_ids
+    for W in (1, 3):
+        run = lambda: c.ix.search(q, ex, s.k, 0.4, W, s.nprobe_max, with_stats=True)
+        a = _with_speculation(True, run, 0)
+        b = _with_speculation(False, run)
+        assert int(a[2].max()) > 2 * W
+        for x, y in zip(a[:3], b[:3]):
+            assert torch.equal(x, y)
+        assert a[3].rounds <= b[3].rounds
+        _with_speculation(True, lambda: _check(c, s.k, 0.4, W, s.nprobe_max, lookahead=True))
 
 
 def test_infinite_window_equals_fixed():
