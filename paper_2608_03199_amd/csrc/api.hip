@@ -441,7 +441,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
       HIP_TRY(launch_fill_i32((int32_t*)ix->have.p, nq, pl.r0, s));
       const int s0 = pl.mode == 0 ? (pl.W < pl.n ? pl.W : pl.n) : 1;
       HIP_TRY(launch_emit_initial(P, pl.n, nq, 0, s0, pl.mode, (Item*)ix->items.p,
-                                  (int32_t*)ix->cnt.p, (int32_t*)ix->state_a.p,
+                                  (int32_t*)ix->cnt.p, ix->nlist, (int32_t*)ix->state_a.p,
                                   (int32_t*)ix->state_b.p, (int32_t*)ix->lmax.p, s));
       span(ix, kRank, r0, mark(ix, timed, s));
       int64_t n_items = nq * s0;
@@ -507,7 +507,8 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
         const int r0 = mark(ix, timed, s);
         if ((st = rank_queries(ix, queries, q0, c, pl.n, pl.n, pl, P, s))) return st;
         HIP_TRY(launch_emit_initial(P, pl.n, c, (int32_t)q0, pl.n, 2, (Item*)ix->items.p,
-                                    (int32_t*)ix->cnt.p, nullptr, nullptr, nullptr, s));
+                                    (int32_t*)ix->cnt.p, ix->nlist, nullptr, nullptr, nullptr,
+                                    s));
         span(ix, kRank, r0, mark(ix, timed, s));
         if ((st = run_round(ix, sa, (int)(c * pl.n), q0, P, pl, s, timed))) return st;
         items_total += c * pl.n;

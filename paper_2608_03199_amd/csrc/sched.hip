@@ -28,6 +28,8 @@ namespace sieve {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kInitThreads = 1024;
+constexpr int kInitBlocksMax = 512;
 
 inline int blocks_for(int64_t n, int per = kThreads) {
   int64_t b = (n + per - 1) / per;
@@ -36,29 +38,40 @@ inline int blocks_for(int64_t n, int per = kThreads) {
 
 // Initial admission: ranks [0, s0) of every query of the chunk [q0, q0+nqc).
 // mode 0: lookahead (stop line s0), 1: basic (next = 0, stale = 0), 2: fixed.
-__global__ void emit_initial_kernel(const int32_t* __restrict__ P, int32_t n, int64_t nqc,
-                                    int32_t q0, int32_t s0, int32_t mode, Item* __restrict__ items,
-                                    int32_t* __restrict__ cnt, int32_t* __restrict__ state_a,
-                                    int32_t* __restrict__ state_b, int32_t* __restrict__ lmax) {
-  const int64_t ql = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (ql >= nqc) return;
-  const int32_t q = q0 + (int32_t)ql;
-  for (int j = 0; j < s0; ++j) {
-    Item it;
-    it.q = q;
-    it.rank = j;
-    items[ql * s0 + j] = it;
-    atomicAdd(&cnt[P[ql * n + j]], 1);
+// The partition histogram of the items is taken in LDS (nlist bins) and
+// added to the global one once per work-group: the first ranks of many
+// queries fall on the same few partitions, and global atomics on one
+// address serialise.
+__global__ __launch_bounds__(kInitThreads) void emit_initial_kernel(
+    const int32_t* __restrict__ P, int32_t n, int64_t nqc, int32_t q0, int32_t s0, int32_t mode,
+    Item* __restrict__ items, int32_t* __restrict__ cnt, int32_t nlist,
+    int32_t* __restrict__ state_a, int32_t* __restrict__ state_b, int32_t* __restrict__ lmax) {
+  extern __shared__ int32_t s_hist[];  // [nlist]
+  for (int i = threadIdx.x; i < nlist; i += blockDim.x) s_hist[i] = 0;
+  __syncthreads();
+  for (int64_t ql = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; ql < nqc;
+       ql += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t q = q0 + (int32_t)ql;
+    for (int j = 0; j < s0; ++j) {
+      Item it;
+      it.q = q;
+      it.rank = j;
+      items[ql * s0 + j] = it;
+      atomicAdd(&s_hist[P[ql * n + j]], 1);
+    }
+    if (mode == 0) {
+      state_a[q] = s0;
+      state_b[q] = s0;  // ranks issued (speculative issue)
+      lmax[q] = 0;
+    } else if (mode == 1) {
+      state_a[q] = 0;  // next (0-based rank in flight)
+      state_b[q] = 0;  // stale
+      lmax[q] = 0;
+    }
   }
-  if (mode == 0) {
-    state_a[q] = s0;
-    state_b[q] = s0;  // ranks issued (speculative issue)
-    lmax[q] = 0;
-  } else if (mode == 1) {
-    state_a[q] = 0;  // next (0-based rank in flight)
-    state_b[q] = 0;  // stale
-    lmax[q] = 0;
-  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < nlist; i += blockDim.x)
+    if (s_hist[i]) atomicAdd(&cnt[i], s_hist[i]);
 }
 
 // One work-group: exclusive scans over the lists of the item histogram and
@@ -374,10 +387,13 @@ __global__ void zero_bytes_kernel(uint8_t* p, int64_t n) {
 }  // namespace
 
 hipError_t launch_emit_initial(const int32_t* P, int32_t n, int64_t nqc, int32_t q0, int32_t s0,
-                               int32_t mode, Item* items, int32_t* cnt, int32_t* state_a,
-                               int32_t* state_b, int32_t* lmax, hipStream_t s) {
-  hipLaunchKernelGGL(emit_initial_kernel, dim3(blocks_for(nqc)), dim3(kThreads), 0, s, P, n, nqc,
-                     q0, s0, mode, items, cnt, state_a, state_b, lmax);
+                               int32_t mode, Item* items, int32_t* cnt, int32_t nlist,
+                               int32_t* state_a, int32_t* state_b, int32_t* lmax, hipStream_t s) {
+  if (nqc <= 0) return hipSuccess;
+  if (nlist < 1 || nlist > kMaxNlist) return hipErrorInvalidValue;
+  const int b = std::min(blocks_for(nqc, kInitThreads), kInitBlocksMax);
+  hipLaunchKernelGGL(emit_initial_kernel, dim3(b), dim3(kInitThreads), (size_t)nlist * 4, s, P,
+                     n, nqc, q0, s0, mode, items, cnt, nlist, state_a, state_b, lmax);
   return hipGetLastError();
 }
 
