@@ -96,6 +96,8 @@ struct sieve_index {
       mix_probes, spec_bits;
   int64_t pool_cap = 0;
   RoundCounters* rc_host = nullptr;
+  RoundSummary* rs_host = nullptr;  // coherent pinned memory the update launches write
+  RoundSummary* rs_dev = nullptr;   // its device address
   // phase timing (only when stats are requested): events are recorded on the
   // stream as the search goes and read once after its final synchronisation
   std::vector<hipEvent_t> ev_pool;
@@ -287,6 +289,11 @@ int grow_workspace(sieve_index* ix, const SearchPlan& pl) {
   if ((st = ensure(ix->pool, (size_t)ix->pool_cap * sizeof(Hit)))) return st;
   if ((st = ensure(ix->pool_sorted, (size_t)ix->pool_cap * sizeof(Hit)))) return st;
   if (!ix->rc_host) HIP_TRY(hipHostMalloc((void**)&ix->rc_host, sizeof(RoundCounters), 0));
+  if (!ix->rs_host) {
+    HIP_TRY(hipHostMalloc((void**)&ix->rs_host, sizeof(RoundSummary),
+                          hipHostMallocCoherent | hipHostMallocMapped));
+    HIP_TRY(hipHostGetDevicePointer((void**)&ix->rs_dev, ix->rs_host, 0));
+  }
   return SIEVE_OK;
 }
 
@@ -433,6 +440,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     HIP_TRY(launch_fill_i32((int32_t*)ix->hcount.p, nq, 0, s));
     if (cal) HIP_TRY(launch_zero_bytes(cal->hitbits, (size_t)nq * cal->words * 4, s));
     bool spec_used = false;  // a round kept the rank bitmap (its ranks may pass stop lines)
+    RoundSummary sm = {0, 0, 0, 0, 0};  // the host's view of the last round
     int32_t* P = (int32_t*)ix->P.p;
 
     if (pl.mode != 2) {
@@ -463,18 +471,23 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
               nq, P, pl.n, pl.W, (int32_t*)ix->state_a.p, (int32_t*)ix->lmax.p, have, ext,
               (Item*)ix->items.p, (int32_t*)ix->cnt.p, rc, spec_now ? sa.hitbits : nullptr,
               sa.hit_words, pl.spec ? (int32_t*)ix->state_b.p : nullptr, pl.spec_max,
-              pl.spec_min, s));
+              pl.spec_min, ix->rs_dev, s));
         else
           HIP_TRY(launch_update_basic(nq, P, pl.n, pl.W, (int32_t*)ix->state_a.p,
                                       (int32_t*)ix->state_b.p, (int32_t*)ix->lmax.p, have, ext,
-                                      (Item*)ix->items.p, (int32_t*)ix->cnt.p, rc, s));
+                                      (Item*)ix->items.p, (int32_t*)ix->cnt.p, rc, ix->rs_dev,
+                                      s));
         span(ix, kUpdate, u0, mark(ix, timed, s));
-        HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
         HIP_TRY(hipStreamSynchronize(s));
+        const volatile RoundSummary* rs = ix->rs_host;
+        sm.new_items = rs->new_items;
+        sm.n_ext = rs->n_ext;
+        sm.rank_error = rs->rank_error;
+        sm.hits = rs->hits;
         items_total += n_items;
         ++rounds;
-        if (ix->rc_host->rank_error) break;  // handled below: re-rank wide or fail
-        if (const int32_t n_ext = ix->rc_host->n_ext) {
+        if (sm.rank_error) break;  // handled below: re-rank wide or fail
+        if (const int32_t n_ext = sm.n_ext) {
           // stop lines passed the ordered prefix: order every rank of those queries
           const int x0 = mark(ix, timed, s);
           const int64_t rb = (int64_t)ix->d * e;
@@ -494,9 +507,11 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
                                  s));
           HIP_TRY(hipStreamSynchronize(s));
           ext_total += n_ext;
-          if (ix->rc_host->rank_error) break;
+          sm.new_items = ix->rc_host->new_items;
+          sm.rank_error = ix->rc_host->rank_error;
+          if (sm.rank_error) break;
         }
-        n_items = ix->rc_host->new_items;
+        n_items = sm.new_items;
         if (n_items > pl.item_cap)
           return fail(SIEVE_EINTERNAL, "round emitted %lld items, capacity %lld",
                       (long long)n_items, (long long)pl.item_cap);
@@ -516,8 +531,10 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
       }
       HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
       HIP_TRY(hipStreamSynchronize(s));
+      sm.rank_error = ix->rc_host->rank_error;
+      sm.hits = ix->rc_host->hits;
     }
-    if (ix->rc_host->rank_error) {
+    if (sm.rank_error) {
       if (pl.wide_rank)
         return fail(SIEVE_EUNSUPPORTED,
                     "more than %d centroids tie within the fp32 screening bound at a rank "
@@ -526,7 +543,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
       continue;
     }
 
-    const int64_t hits = (int64_t)ix->rc_host->hits;
+    const int64_t hits = (int64_t)sm.hits;
     if (hits > ix->pool_cap) {
       // the pool overflowed: grow it and run again (the search is deterministic)
       ix->pool_cap = hits + hits / 8 + (int64_t)pl.scan_grid * kArenaMax;
@@ -554,7 +571,9 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     const int f1 = mark(ix, timed, s);
     span(ix, kFinal, f0, f1);
     span(ix, kTotal, t_begin, f1);
-    HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
+    // the statistics read the final counters; the outputs only need the stream drained
+    if (timed)
+      HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
     if (timed) {
       float ms[kPhases];
@@ -785,6 +804,7 @@ SIEVE_API void sieve_free_index(sieve_index* ix) {
   if (ix->ids) (void)hipFree(ix->ids);
   if (ix->centroids) (void)hipFree(ix->centroids);
   if (ix->rc_host) (void)hipHostFree(ix->rc_host);
+  if (ix->rs_host) (void)hipHostFree(ix->rs_host);
   for (hipEvent_t e : ix->ev_pool) (void)hipEventDestroy(e);
   delete ix;
 }

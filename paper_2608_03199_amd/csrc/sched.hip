@@ -193,17 +193,30 @@ __global__ void sched_tiles_kernel(int32_t* __restrict__ cnt, const int32_t* __r
   }
 }
 
-__global__ void update_lookahead_kernel(int64_t nq, const int32_t* __restrict__ P, int32_t n,
-                                        int32_t W, int32_t* __restrict__ stop,
-                                        int32_t* __restrict__ lmax,
-                                        const int32_t* __restrict__ have,
-                                        int32_t* __restrict__ ext, Item* __restrict__ items,
-                                        int32_t* __restrict__ cnt, RoundCounters* rc,
-                                        const uint32_t* __restrict__ hitbits, int32_t words,
-                                        int32_t* __restrict__ issued, int32_t spec_max,
-                                        int32_t spec_min) {
-  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (q >= nq) return;
+// The round's summary for the host: one wave reads the counters (the
+// update launch before it on the stream has finished) and writes them to
+// coherent pinned host memory with system-scope stores.
+__global__ void publish_round_kernel(const RoundCounters* __restrict__ rc,
+                                     RoundSummary* __restrict__ out) {
+  if (threadIdx.x != 0) return;
+  __hip_atomic_store(&out->new_items, rc->new_items, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  __hip_atomic_store(&out->n_ext, rc->n_ext, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  __hip_atomic_store(&out->rank_error, rc->rank_error, __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_SYSTEM);
+  __hip_atomic_store(&out->hits, rc->hits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  __threadfence_system();
+}
+
+__device__ __forceinline__ void lookahead_one(int64_t q, const int32_t* __restrict__ P, int32_t n,
+                                              int32_t W, int32_t* __restrict__ stop,
+                                              int32_t* __restrict__ lmax,
+                                              const int32_t* __restrict__ have,
+                                              int32_t* __restrict__ ext,
+                                              Item* __restrict__ items,
+                                              int32_t* __restrict__ cnt, RoundCounters* rc,
+                                              const uint32_t* __restrict__ hitbits,
+                                              int32_t words, int32_t* __restrict__ issued,
+                                              int32_t spec_max, int32_t spec_min) {
   const int L = lmax[q];  // 1-based highest hit rank of this round, 0 = none
   if (L == 0) return;
   lmax[q] = 0;
@@ -277,16 +290,30 @@ __global__ void update_lookahead_kernel(int64_t nq, const int32_t* __restrict__ 
   if (reach > hv) ext[atomicAdd(&rc->n_ext, 1)] = (int32_t)q;
 }
 
+__global__ void update_lookahead_kernel(int64_t nq, const int32_t* __restrict__ P, int32_t n,
+                                        int32_t W, int32_t* __restrict__ stop,
+                                        int32_t* __restrict__ lmax,
+                                        const int32_t* __restrict__ have,
+                                        int32_t* __restrict__ ext, Item* __restrict__ items,
+                                        int32_t* __restrict__ cnt, RoundCounters* rc,
+                                        const uint32_t* __restrict__ hitbits, int32_t words,
+                                        int32_t* __restrict__ issued, int32_t spec_max,
+                                        int32_t spec_min) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q < nq)
+    lookahead_one(q, P, n, W, stop, lmax, have, ext, items, cnt, rc, hitbits, words, issued,
+                  spec_max, spec_min);
+}
+
 // next[q]: rank in flight (0-based) or -1 once stopped; on stopping,
 // stale[q] is overwritten with the probe count.
-__global__ void update_basic_kernel(int64_t nq, const int32_t* __restrict__ P, int32_t n,
-                                    int32_t W, int32_t* __restrict__ next,
-                                    int32_t* __restrict__ stale, int32_t* __restrict__ lmax,
-                                    const int32_t* __restrict__ have, int32_t* __restrict__ ext,
-                                    Item* __restrict__ items, int32_t* __restrict__ cnt,
-                                    RoundCounters* rc) {
-  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (q >= nq) return;
+__device__ __forceinline__ void basic_one(int64_t q, const int32_t* __restrict__ P, int32_t n,
+                                          int32_t W, int32_t* __restrict__ next,
+                                          int32_t* __restrict__ stale,
+                                          int32_t* __restrict__ lmax,
+                                          const int32_t* __restrict__ have,
+                                          int32_t* __restrict__ ext, Item* __restrict__ items,
+                                          int32_t* __restrict__ cnt, RoundCounters* rc) {
   const int cur = next[q];
   if (cur < 0) return;
   const bool hit = lmax[q] == cur + 1;
@@ -310,6 +337,16 @@ __global__ void update_basic_kernel(int64_t nq, const int32_t* __restrict__ P, i
     next[q] = -1;
     stale[q] = nx;  // probes
   }
+}
+
+__global__ void update_basic_kernel(int64_t nq, const int32_t* __restrict__ P, int32_t n,
+                                    int32_t W, int32_t* __restrict__ next,
+                                    int32_t* __restrict__ stale, int32_t* __restrict__ lmax,
+                                    const int32_t* __restrict__ have, int32_t* __restrict__ ext,
+                                    Item* __restrict__ items, int32_t* __restrict__ cnt,
+                                    RoundCounters* rc) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q < nq) basic_one(q, P, n, W, next, stale, lmax, have, ext, items, cnt, rc);
 }
 
 // Row copy in 16-byte units: dst row i <- src row ext[i].
@@ -427,19 +464,23 @@ hipError_t launch_update_lookahead(int64_t nq, const int32_t* P, int32_t n, int3
                                    int32_t* stop, int32_t* lmax, const int32_t* have,
                                    int32_t* ext, Item* items, int32_t* cnt, RoundCounters* rc,
                                    const uint32_t* hitbits, int32_t words, int32_t* issued,
-                                   int32_t spec_max, int32_t spec_min, hipStream_t s) {
+                                   int32_t spec_max, int32_t spec_min, RoundSummary* out,
+                                   hipStream_t s) {
   if (hitbits && (!issued || words * 32 < n || spec_max < 0)) return hipErrorInvalidValue;
   hipLaunchKernelGGL(update_lookahead_kernel, dim3(blocks_for(nq)), dim3(kThreads), 0, s, nq, P, n,
                      W, stop, lmax, have, ext, items, cnt, rc, hitbits, words, issued, spec_max,
                      spec_min);
+  if (out) hipLaunchKernelGGL(publish_round_kernel, dim3(1), dim3(64), 0, s, rc, out);
   return hipGetLastError();
 }
 
 hipError_t launch_update_basic(int64_t nq, const int32_t* P, int32_t n, int32_t W, int32_t* next,
                                int32_t* stale, int32_t* lmax, const int32_t* have, int32_t* ext,
-                               Item* items, int32_t* cnt, RoundCounters* rc, hipStream_t s) {
+                               Item* items, int32_t* cnt, RoundCounters* rc, RoundSummary* out,
+                               hipStream_t s) {
   hipLaunchKernelGGL(update_basic_kernel, dim3(blocks_for(nq)), dim3(kThreads), 0, s, nq, P, n, W,
                      next, stale, lmax, have, ext, items, cnt, rc);
+  if (out) hipLaunchKernelGGL(publish_round_kernel, dim3(1), dim3(64), 0, s, rc, out);
   return hipGetLastError();
 }
 

@@ -69,6 +69,16 @@ struct RoundCounters {
   unsigned long long candidates[kStatSlots];
 };
 
+// What the host needs after each round, written by a one-wave kernel after
+// the update straight into coherent pinned host memory (no copy command).
+struct RoundSummary {
+  int32_t new_items;
+  int32_t n_ext;
+  int32_t rank_error;
+  int32_t pad;
+  unsigned long long hits;
+};
+
 // Candidate-pool arenas: a scan work-group claims pool slots in runs (first
 // kArenaMin, doubling per refill up to kArenaMax) and keeps its current run
 // across the launches of one search in an ArenaRec indexed by block.  The
@@ -166,10 +176,12 @@ hipError_t launch_update_lookahead(int64_t nq, const int32_t* P, int32_t n, int3
                                    int32_t* stop, int32_t* lmax, const int32_t* have,
                                    int32_t* ext, Item* items, int32_t* cnt, RoundCounters* rc,
                                    const uint32_t* hitbits, int32_t words, int32_t* issued,
-                                   int32_t spec_max, int32_t spec_min, hipStream_t s);
+                                   int32_t spec_max, int32_t spec_min, RoundSummary* out,
+                                   hipStream_t s);
 hipError_t launch_update_basic(int64_t nq, const int32_t* P, int32_t n, int32_t W, int32_t* next,
                                int32_t* stale, int32_t* lmax, const int32_t* have, int32_t* ext,
-                               Item* items, int32_t* cnt, RoundCounters* rc, hipStream_t s);
+                               Item* items, int32_t* cnt, RoundCounters* rc, RoundSummary* out,
+                               hipStream_t s);
 // Lazy ranking: copy the listed queries' rows together, copy their new rank
 // rows into P, and emit the items the extension unblocked.
 hipError_t launch_gather_rows(const int32_t* ext, int32_t n_ext, const void* src,
