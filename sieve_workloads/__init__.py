@@ -259,8 +259,7 @@ def make(spec: WorkloadSpec | str, device: Optional[str] = None, seed: Optional[
         assign = torch.empty(ns, dtype=torch.int64, device=dev)
         for a, b in _rows(ns, mchunk):
             assign[a:b] = (xsamp[a:b] @ cent.T).argmax(dim=1)
-        sums = torch.zeros_like(cent).index_add_(0, assign, xsamp)
-        cnt = torch.bincount(assign, minlength=spec.nlist)
+        sums, cnt = _cluster_sums(xsamp, assign, spec.nlist)
         keep = cnt == 0
         newc = _normalize(sums)
         cent = torch.where(keep[:, None], cent, newc)
@@ -285,6 +284,19 @@ def make(spec: WorkloadSpec | str, device: Optional[str] = None, seed: Optional[
     del xs_store
     return Workload(spec, vectors.contiguous(), ids, offsets, c_store.contiguous(),
                     queries.contiguous(), qrows.to(torch.int64), refined)
+
+
+def _cluster_sums(x: torch.Tensor, assign: torch.Tensor, k: int):
+    """Per-cluster sums of the rows of x, in a fixed order (no float atomics, so the same
+    inputs give the same bits in every process): rows sorted by cluster (stable), fp64
+    prefix sums, differences at the cluster boundaries."""
+    order = torch.sort(assign, stable=True).indices
+    cnt = torch.bincount(assign, minlength=k)
+    ends = torch.cumsum(cnt, 0)
+    pre = torch.zeros(x.shape[0] + 1, x.shape[1], dtype=torch.float64, device=x.device)
+    pre[1:] = torch.cumsum(x[order].double(), 0)
+    sums = (pre[ends] - pre[ends - cnt]).float()
+    return sums, cnt
 
 
 def list_stats(list_offsets) -> dict:
