@@ -76,15 +76,39 @@ __global__ __launch_bounds__(kScanBlock) void scan_apply_kernel(const int32_t* i
                   nullptr);
 }
 
-__global__ void pool_scatter_kernel(const Hit* __restrict__ pool, int64_t n,
-                                    int32_t* __restrict__ cursor, Hit* __restrict__ sorted,
-                                    int32_t qmask) {
+// The claims are aggregated per wave: one atomic per distinct query among the
+// wave's 64 entries (a tile appends the candidates of a few queries row after
+// row, so neighbouring entries mostly share queries, and one-address atomics
+// serialise).  The order inside a query's segment is free: the top-k merge
+// uses a total order.
+__global__ __launch_bounds__(256) void pool_scatter_kernel(const Hit* __restrict__ pool, int64_t n,
+                                                           int32_t* __restrict__ cursor,
+                                                           Hit* __restrict__ sorted,
+                                                           int32_t qmask) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  const Hit h = pool[i];
-  if (h.q < 0) return;  // unused arena slot
-  const int pos = atomicAdd(&cursor[h.q & qmask], 1);
-  sorted[pos] = h;
+  const int lane = threadIdx.x & 63;
+  Hit h = {-INFINITY, -1, -1};
+  if (i < n) h = pool[i];
+  const int q = h.q < 0 ? -1 : (h.q & qmask);  // -1: past the end or an unused arena slot
+  // group the lanes by query (register work only), then every group's first
+  // lane claims the group's slots, all groups at once
+  unsigned long long todo = __ballot(q >= 0);
+  int leader = lane, rank = 0, count = 0;
+  while (todo) {  // wave-uniform
+    const int first = __builtin_ctzll(todo);
+    const int qf = __shfl(q, first);
+    const unsigned long long same = __ballot(q == qf);
+    if (q == qf) {
+      leader = first;
+      rank = __popcll(same & ((1ull << lane) - 1ull));
+      count = __popcll(same);
+    }
+    todo &= ~same;
+  }
+  int base = 0;
+  if (q >= 0 && rank == 0) base = atomicAdd(&cursor[q], count);
+  base = __shfl(base, leader);
+  if (q >= 0) sorted[base + rank] = h;
 }
 
 // Sentinels over the unused tail of every block's last arena (one block per
