@@ -367,12 +367,14 @@ ScanArgs make_scan_args(sieve_index* ix, const void* queries, const int64_t* exc
 }
 
 // One scheduling round over n_items ready items (already histogrammed).
+// at: an event recorded at the stream's current position (-1: none), which
+// then opens the schedule span; on return, the event that closes the scan.
 int run_round(sieve_index* ix, const ScanArgs& sa, int n_items, int64_t q0, const int32_t* P,
-              const SearchPlan& pl, hipStream_t s, bool timed) {
+              const SearchPlan& pl, hipStream_t s, bool timed, int* at) {
   RoundCounters* rc = (RoundCounters*)ix->rc.p;
   const int chunk = (int64_t)n_items >= (int64_t)pl.dense_q * ix->nlist ? pl.row_chunk_dense
                                                                         : pl.row_chunk;
-  const int e0 = mark(ix, timed, s);
+  const int e0 = *at >= 0 ? *at : mark(ix, timed, s);
   HIP_TRY(launch_sched_offsets((const int32_t*)ix->cnt.p, ix->offsets, ix->nlist, chunk,
                                pl.group_q, (int32_t*)ix->item_off.p, (int32_t*)ix->cursor.p,
                                (int32_t*)ix->tile_off.p, rc, s));
@@ -388,6 +390,7 @@ int run_round(sieve_index* ix, const ScanArgs& sa, int n_items, int64_t q0, cons
   const int e2 = mark(ix, timed, s);
   span(ix, kSched, e0, e1);
   span(ix, kScan, e1, e2);
+  *at = e2;
   return SIEVE_OK;
 }
 
@@ -434,6 +437,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     }
 
     const int t_begin = mark(ix, timed, s);
+    int at = -1;  // an event at the stream's current position, when one was just recorded
     HIP_TRY(launch_zero_bytes(rc, sizeof(RoundCounters), s));
     HIP_TRY(launch_zero_bytes(ix->arenas.p, (size_t)pl.scan_grid * sizeof(ArenaRec), s));
     HIP_TRY(launch_fill_i32((int32_t*)ix->cnt.p, ix->nlist, 0, s));
@@ -451,7 +455,9 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
       HIP_TRY(launch_emit_initial(P, pl.n, nq, 0, s0, pl.mode, (Item*)ix->items.p,
                                   (int32_t*)ix->cnt.p, ix->nlist, (int32_t*)ix->state_a.p,
                                   (int32_t*)ix->state_b.p, (int32_t*)ix->lmax.p, s));
-      span(ix, kRank, r0, mark(ix, timed, s));
+      // adjacent phases share the event between them (fewer records per round)
+      at = mark(ix, timed, s);
+      span(ix, kRank, r0, at);
       int64_t n_items = nq * s0;
       while (n_items > 0) {
         // speculative issue from round spec_round on: its scans keep the rank bitmap
@@ -462,8 +468,8 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
           sa.hit_words = pl.hit_words;
           spec_used = true;
         }
-        if ((st = run_round(ix, sa, (int)n_items, 0, P, pl, s, timed))) return st;
-        const int u0 = mark(ix, timed, s);
+        if ((st = run_round(ix, sa, (int)n_items, 0, P, pl, s, timed, &at))) return st;
+        const int u0 = at;
         int32_t* have = (int32_t*)ix->have.p;
         int32_t* ext = (int32_t*)ix->ext.p;
         if (pl.mode == 0)
@@ -477,7 +483,8 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
                                       (int32_t*)ix->state_b.p, (int32_t*)ix->lmax.p, have, ext,
                                       (Item*)ix->items.p, (int32_t*)ix->cnt.p, rc, ix->rs_dev,
                                       s));
-        span(ix, kUpdate, u0, mark(ix, timed, s));
+        at = mark(ix, timed, s);
+        span(ix, kUpdate, u0, at);
         HIP_TRY(hipStreamSynchronize(s));
         const volatile RoundSummary* rs = ix->rs_host;
         sm.new_items = rs->new_items;
@@ -489,7 +496,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
         if (sm.rank_error) break;  // handled below: re-rank wide or fail
         if (const int32_t n_ext = sm.n_ext) {
           // stop lines passed the ordered prefix: order every rank of those queries
-          const int x0 = mark(ix, timed, s);
+          const int x0 = at;
           const int64_t rb = (int64_t)ix->d * e;
           if ((st = ensure(ix->qext, (size_t)n_ext * rb)) ||
               (st = ensure(ix->Pext, (size_t)n_ext * pl.n * sizeof(int32_t))))
@@ -502,7 +509,8 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
           HIP_TRY(launch_emit_pending(ext, n_ext, pl.mode, P, pl.n, (const int32_t*)ix->state_a.p,
                                       have, pl.n, (Item*)ix->items.p, (int32_t*)ix->cnt.p, rc,
                                       pl.spec ? (int32_t*)ix->state_b.p : nullptr, s));
-          span(ix, kRank, x0, mark(ix, timed, s));
+          at = mark(ix, timed, s);
+          span(ix, kRank, x0, at);
           HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost,
                                  s));
           HIP_TRY(hipStreamSynchronize(s));
@@ -524,13 +532,15 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
         HIP_TRY(launch_emit_initial(P, pl.n, c, (int32_t)q0, pl.n, 2, (Item*)ix->items.p,
                                     (int32_t*)ix->cnt.p, ix->nlist, nullptr, nullptr, nullptr,
                                     s));
-        span(ix, kRank, r0, mark(ix, timed, s));
-        if ((st = run_round(ix, sa, (int)(c * pl.n), q0, P, pl, s, timed))) return st;
+        at = mark(ix, timed, s);
+        span(ix, kRank, r0, at);
+        if ((st = run_round(ix, sa, (int)(c * pl.n), q0, P, pl, s, timed, &at))) return st;
         items_total += c * pl.n;
         ++rounds;
       }
       HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
       HIP_TRY(hipStreamSynchronize(s));
+      at = -1;  // the copy ran after the last event
       sm.rank_error = ix->rc_host->rank_error;
       sm.hits = ix->rc_host->hits;
     }
@@ -554,7 +564,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     }
 
     // finalize: group the pool by query, then per-query top-k
-    const int f0 = mark(ix, timed, s);
+    const int f0 = at >= 0 ? at : mark(ix, timed, s);
     HIP_TRY(launch_retire_arenas((const ArenaRec*)ix->arenas.p, pl.scan_grid, (Hit*)ix->pool.p,
                                  ix->pool_cap, s));
     HIP_TRY(launch_exclusive_scan((const int32_t*)ix->hcount.p, (int32_t*)ix->hoff.p,
