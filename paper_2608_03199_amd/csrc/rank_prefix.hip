@@ -225,7 +225,7 @@ template <int D>
 __global__ __launch_bounds__(kQRWaves * 64, 1) void rank_prefix_qreg_kernel(
     const void* __restrict__ queries, int64_t q0, int32_t nqc, const void* __restrict__ centroids,
     int32_t nlist, int32_t R, double cmax, int32_t cap, unsigned long long* __restrict__ cand,
-    int32_t* __restrict__ ccount) {
+    int32_t* __restrict__ ccount, int32_t nblk1) {
   constexpr int DT = SIEVE_F16;
   constexpr int kNC = D / DTraits<DT>::kChunkDims;
   static_assert(kNC >= 1 && kNC <= 4, "short rows only");
@@ -282,17 +282,17 @@ __global__ __launch_bounds__(kQRWaves * 64, 1) void rank_prefix_qreg_kernel(
   // fast(acc, blk) of block t - 1, which returns whether slow(acc, blk) must
   // run for that block.  A fixed number of ring rounds runs; padding blocks
   // (past the last) skip their epilogue.
-  auto sweep = [&](auto&& fast, auto&& slow) {
+  auto sweep = [&](int nb, auto&& fast, auto&& slow) {
     u32x4 buf[kQRRing][kNC];
     f32x4 acc[2][kQW];
     auto load = [&](int blk, u32x4(&dst)[kNC]) {
-      const char* p = rs.seg_ptr(blk < nblk ? blk : nblk - 1);
+      const char* p = rs.seg_ptr(blk < nb ? blk : nb - 1);
 #pragma unroll
       for (int c = 0; c < kNC; ++c) dst[c] = *(const u32x4*)(p + 64 * c);
     };
 #pragma unroll
     for (int u = 0; u < kQRRing - 1; ++u) load(mem + u * kQRSplit, buf[u]);
-    const int mine = mem < nblk ? (nblk - mem + kQRSplit - 1) / kQRSplit : 0;
+    const int mine = mem < nb ? (nb - mem + kQRSplit - 1) / kQRSplit : 0;
     const int rounds = (mine + kQRRing - 1) / kQRRing;
     int blk = mem;
     for (int it = 0; it < rounds; ++it) {
@@ -330,7 +330,7 @@ __global__ __launch_bounds__(kQRWaves * 64, 1) void rank_prefix_qreg_kernel(
     }
     // the last block's epilogue
     const int lblk = blk - kQRSplit;
-    if (rounds > 0 && lblk < nblk) {
+    if (rounds > 0 && lblk < nb) {
       constexpr int last = (kQRRing - 1) & 1;
       if (__ballot(fast(acc[last], lblk * 16 + r16 < nlist)) != 0) slow(acc[last], lblk);
     }
@@ -342,7 +342,7 @@ __global__ __launch_bounds__(kQRWaves * 64, 1) void rank_prefix_qreg_kernel(
   float m1[kQW * 4], m2[kQW * 4];
 #pragma unroll
   for (int x = 0; x < kQW * 4; ++x) m1[x] = m2[x] = -INFINITY;
-  sweep(
+  sweep(nblk1,
       [&](const f32x4(&acc)[kQW], bool ok) -> bool {
 #pragma unroll
         for (int qb = 0; qb < kQW; ++qb) {
@@ -405,7 +405,7 @@ __global__ __launch_bounds__(kQRWaves * 64, 1) void rank_prefix_qreg_kernel(
 #pragma unroll
     for (int r = 0; r < 4; ++r) lim[qb * 4 + r] = s_lo[w0 + qb * 16 + 4 * h + r];
   }
-  sweep(
+  sweep(nblk,
       [&](const f32x4(&acc)[kQW], bool ok) -> bool {
         bool any = false;
 #pragma unroll
@@ -557,8 +557,17 @@ hipError_t launch_rank_prefix(int dtype, const void* queries, int64_t q0, int32_
   hipError_t e;
   if (dtype == SIEVE_F16 && d == 128) {
     const unsigned grid = (unsigned)((nqc + kQRRows - 1) / kQRRows);
+    // Pass 1 may bound the R-th score from the first 1/div of the centroids
+    // (a subset's R-th largest never exceeds the whole set's): a looser bound,
+    // so more candidates, for a shorter first pass.  Every wave keeps at least
+    // four blocks, so every kept value is finite.
+    const int nblk = (nlist + 15) / 16;
+    const char* dv = getenv("SIEVE_RANK_PASS1_DIV");
+    const int div = dv && atoi(dv) > 1 ? atoi(dv) : 1;
+    int nblk1 = (nblk + div - 1) / div;
+    if (nblk1 < 4 * kQRSplit) nblk1 = nblk < 4 * kQRSplit ? nblk : 4 * kQRSplit;
     hipLaunchKernelGGL((rank_prefix_qreg_kernel<128>), dim3(grid), dim3(kQRWaves * 64), 0, s,
-                       queries, q0, nqc, centroids, nlist, R, cmax, cap, cand, ccount);
+                       queries, q0, nqc, centroids, nlist, R, cmax, cap, cand, ccount, nblk1);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return launch_finish_t<SIEVE_F16>(queries, q0, nqc, centroids, d, R, cap, cmax, cand, ccount,
                                       P, ldp, rc, s);
