@@ -76,6 +76,21 @@ __global__ __launch_bounds__(kScanBlock) void scan_apply_kernel(const int32_t* i
                   nullptr);
 }
 
+// Small inputs (a few tiles): one work-group scans the tiles in order with a
+// running carry, in one launch instead of three.
+constexpr int kScanSingleTiles = 16;
+
+__global__ __launch_bounds__(kScanBlock) void scan_single_kernel(const int32_t* in, int64_t n,
+                                                                int32_t* out, int32_t* out2) {
+  __shared__ int32_t tot;
+  int32_t carry = 0;
+  for (int64_t base = 0; base < n; base += kScanTile) {
+    block_scan_tile(in, out, out2, n, base, carry, &tot);  // ends with a barrier
+    carry += tot;
+    __syncthreads();  // every thread has read tot before the next tile writes it
+  }
+}
+
 // The claims are aggregated per wave: one atomic per distinct query among the
 // wave's 64 entries (a tile appends the candidates of a few queries row after
 // row, so neighbouring entries mostly share queries, and one-address atomics
@@ -327,6 +342,10 @@ hipError_t launch_exclusive_scan(const int32_t* in, int32_t* out, int32_t* out_c
   if (n <= 0) return hipSuccess;
   const int64_t nb = (n + kScanTile - 1) / kScanTile;
   if (nb > kScanTile) return hipErrorInvalidValue;
+  if (nb <= kScanSingleTiles) {
+    hipLaunchKernelGGL(scan_single_kernel, dim3(1), dim3(kScanBlock), 0, s, in, n, out, out_copy);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(scan_partials_kernel, dim3((unsigned)nb), dim3(kScanBlock), 0, s, in, n,
                      block_tmp);
   hipLaunchKernelGGL(scan_partials_top_kernel, dim3(1), dim3(kScanBlock), 0, s, block_tmp,
