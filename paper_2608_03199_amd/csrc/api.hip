@@ -648,7 +648,8 @@ int plan_search(const sieve_index* ix, int64_t nq, int32_t k, float tau, int32_t
   // (queries < 2^kRankShift) and a stop rule that can stop early (W < n).
   pl->spec = mode == 0 && W < pl->n && nq <= (int64_t)kQueryMask + 1 &&
              env_flag("SIEVE_SPECULATE", true);
-  pl->spec_max = pl->spec ? (int)std::min<int64_t>(pl->n, 3ll * W) : 0;
+  pl->spec_max =
+      pl->spec ? (int)std::min<int64_t>(pl->n, (int64_t)env_int("SIEVE_SPEC_DEPTH", 3) * W) : 0;
   // Lines that move far keep moving (queries in large near-duplicate groups):
   // speculating for those merges their next ranks into the larger, earlier
   // rounds, where a list read serves more queries.  Short moves are common
