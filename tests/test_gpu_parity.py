@@ -478,12 +478,27 @@ def test_rank_and_search_on_large_centroid_sets(nlist, d, dtype, rank_path):
         ix.close()
 
 
+@pytest.fixture(params=[1, 2, 4])
+def pass1_div(request):
+    """The register-query prefix bounds the R-th score from the first 1/div of the
+    centroids (1: all of them); a looser bound admits more candidates, and a query whose
+    candidates overflow its buffer is re-ranked by the wide fallback."""
+    old = os.environ.get("SIEVE_RANK_PASS1_DIV")
+    os.environ["SIEVE_RANK_PASS1_DIV"] = str(request.param)
+    yield request.param
+    if old is None:
+        os.environ.pop("SIEVE_RANK_PASS1_DIV", None)
+    else:
+        os.environ["SIEVE_RANK_PASS1_DIV"] = old
+
+
 @pytest.mark.parametrize("R", [8, 32, 33, 64])
-def test_rank_prefix_on_many_work_groups(R, rank_path):
+def test_rank_prefix_on_many_work_groups(R, rank_path, pass1_div):
     """128-dim fp16 queries on a large centroid set: the fused prefix keeps the queries of
     each wave in registers, 128 queries per work-group; 1,100 queries span nine
     work-groups, the last one ragged (76 queries); R runs from 8 to the 64-rank maximum
-    of the fused prefix."""
+    of the fused prefix.  The order is exact whatever part of the centroids bounds the
+    first pass."""
     rng = np.random.default_rng(900 + R)
     nlist, d, nq = 1800, 128, 1100
     C = rng.standard_normal((nlist, d))
@@ -503,7 +518,7 @@ def test_rank_prefix_on_many_work_groups(R, rank_path):
     finally:
         ix.close()
     o = oracle.search(X, off, ids, C, Q, None, 1, 2.0, 1, R, want_order=True, nthreads=NTHREADS)
-    print(f"[gpu-test] rank prefix R={R} path={rank_path}", flush=True)
+    print(f"[gpu-test] rank prefix R={R} path={rank_path} pass-1 div={pass1_div}", flush=True)
     assert np.array_equal(P, o.order[:, :R])
 
 
