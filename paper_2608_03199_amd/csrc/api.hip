@@ -438,11 +438,19 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
 
     const int t_begin = mark(ix, timed, s);
     int at = -1;  // an event at the stream's current position, when one was just recorded
-    HIP_TRY(launch_zero_bytes(rc, sizeof(RoundCounters), s));
-    HIP_TRY(launch_zero_bytes(ix->arenas.p, (size_t)pl.scan_grid * sizeof(ArenaRec), s));
-    HIP_TRY(launch_fill_i32((int32_t*)ix->cnt.p, ix->nlist, 0, s));
-    HIP_TRY(launch_fill_i32((int32_t*)ix->hcount.p, nq, 0, s));
-    if (cal) HIP_TRY(launch_zero_bytes(cal->hitbits, (size_t)nq * cal->words * 4, s));
+    {
+      // every per-search reset in one launch: counters, arenas, partition histogram,
+      // per-query candidate counts, the calibration bitmap, the ordered-prefix lengths
+      static_assert(sizeof(RoundCounters) % 4 == 0 && sizeof(ArenaRec) % 4 == 0, "word fills");
+      FillSegs f = {};
+      f.seg[0] = {(int32_t*)rc, (int64_t)(sizeof(RoundCounters) / 4), 0};
+      f.seg[1] = {(int32_t*)ix->arenas.p, (int64_t)pl.scan_grid * (int64_t)(sizeof(ArenaRec) / 4), 0};
+      f.seg[2] = {(int32_t*)ix->cnt.p, (int64_t)ix->nlist, 0};
+      f.seg[3] = {(int32_t*)ix->hcount.p, nq, 0};
+      if (cal) f.seg[4] = {(int32_t*)cal->hitbits, nq * (int64_t)cal->words, 0};
+      if (pl.mode != 2) f.seg[5] = {(int32_t*)ix->have.p, nq, pl.r0};
+      HIP_TRY(launch_fill_multi(f, s));
+    }
     bool spec_used = false;  // a round kept the rank bitmap (its ranks may pass stop lines)
     RoundSummary sm = {0, 0, 0, 0, 0};  // the host's view of the last round
     int32_t* P = (int32_t*)ix->P.p;
@@ -450,7 +458,6 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     if (pl.mode != 2) {
       const int r0 = mark(ix, timed, s);
       if ((st = rank_queries(ix, queries, 0, nq, pl.r0, pl.n, pl, P, s))) return st;
-      HIP_TRY(launch_fill_i32((int32_t*)ix->have.p, nq, pl.r0, s));
       const int s0 = pl.mode == 0 ? (pl.W < pl.n ? pl.W : pl.n) : 1;
       HIP_TRY(launch_emit_initial(P, pl.n, nq, 0, s0, pl.mode, (Item*)ix->items.p,
                                   (int32_t*)ix->cnt.p, ix->nlist, (int32_t*)ix->state_a.p,

@@ -415,6 +415,17 @@ __global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
     p[i] = v;
 }
 
+__global__ void fill_multi_kernel(FillSegs f) {
+  const int64_t step = (int64_t)gridDim.x * blockDim.x;
+#pragma unroll
+  for (int k = 0; k < kFillSegs; ++k) {
+    int32_t* __restrict__ p = f.seg[k].p;
+    const int64_t n = f.seg[k].n;
+    const int32_t v = f.seg[k].v;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += step) p[i] = v;
+  }
+}
+
 __global__ void zero_bytes_kernel(uint8_t* p, int64_t n) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x)
@@ -519,6 +530,18 @@ hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   int b = blocks_for(n);
   hipLaunchKernelGGL(fill_i32_kernel, dim3(b > 4096 ? 4096 : b), dim3(kThreads), 0, s, p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_multi(const FillSegs& f, hipStream_t s) {
+  int64_t most = 0;
+  for (int k = 0; k < kFillSegs; ++k) {
+    if (f.seg[k].n < 0 || (f.seg[k].n > 0 && !f.seg[k].p)) return hipErrorInvalidValue;
+    most = f.seg[k].n > most ? f.seg[k].n : most;
+  }
+  if (most == 0) return hipSuccess;
+  const int b = std::min(blocks_for(most), 4096);
+  hipLaunchKernelGGL(fill_multi_kernel, dim3(b), dim3(kThreads), 0, s, f);
   return hipGetLastError();
 }
 

@@ -194,6 +194,17 @@ hipError_t launch_emit_pending(const int32_t* ext, int32_t n_ext, int32_t mode, 
                                int32_t* issued, hipStream_t s);
 
 hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
+// Several 32-bit fills in one launch (segments with n = 0 are skipped).
+constexpr int kFillSegs = 6;
+struct FillSeg {
+  int32_t* p;
+  int64_t n;  // 32-bit words
+  int32_t v;
+};
+struct FillSegs {
+  FillSeg seg[kFillSegs];
+};
+hipError_t launch_fill_multi(const FillSegs& f, hipStream_t s);
 hipError_t launch_zero_bytes(void* p, int64_t bytes, hipStream_t s);
 hipError_t launch_exclusive_scan(const int32_t* in, int32_t* out, int32_t* out_copy, int64_t n,
                                  int32_t* block_tmp, hipStream_t s);
