@@ -207,6 +207,22 @@ __global__ void publish_round_kernel(const RoundCounters* __restrict__ rc,
   __threadfence_system();
 }
 
+// The summary written by the update launch itself when it is one work-group:
+// the counter updates the summary reads (new_items, n_ext) are atomics whose
+// results their threads consumed before the barrier, so they are done.
+__device__ __forceinline__ void publish_from_block(const RoundCounters* rc, RoundSummary* out) {
+  __syncthreads();
+  if (threadIdx.x != 0) return;
+  const int32_t ni = __hip_atomic_load(&rc->new_items, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const int32_t ne = __hip_atomic_load(&rc->n_ext, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(&out->new_items, ni, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  __hip_atomic_store(&out->n_ext, ne, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  __hip_atomic_store(&out->rank_error, rc->rank_error, __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_SYSTEM);
+  __hip_atomic_store(&out->hits, rc->hits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  __threadfence_system();
+}
+
 __device__ __forceinline__ void lookahead_one(int64_t q, const int32_t* __restrict__ P, int32_t n,
                                               int32_t W, int32_t* __restrict__ stop,
                                               int32_t* __restrict__ lmax,
@@ -298,11 +314,12 @@ __global__ void update_lookahead_kernel(int64_t nq, const int32_t* __restrict__ 
                                         int32_t* __restrict__ cnt, RoundCounters* rc,
                                         const uint32_t* __restrict__ hitbits, int32_t words,
                                         int32_t* __restrict__ issued, int32_t spec_max,
-                                        int32_t spec_min) {
+                                        int32_t spec_min, RoundSummary* out) {
   const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (q < nq)
     lookahead_one(q, P, n, W, stop, lmax, have, ext, items, cnt, rc, hitbits, words, issued,
                   spec_max, spec_min);
+  if (out) publish_from_block(rc, out);  // one work-group only
 }
 
 // next[q]: rank in flight (0-based) or -1 once stopped; on stopping,
@@ -344,9 +361,10 @@ __global__ void update_basic_kernel(int64_t nq, const int32_t* __restrict__ P, i
                                     int32_t* __restrict__ stale, int32_t* __restrict__ lmax,
                                     const int32_t* __restrict__ have, int32_t* __restrict__ ext,
                                     Item* __restrict__ items, int32_t* __restrict__ cnt,
-                                    RoundCounters* rc) {
+                                    RoundCounters* rc, RoundSummary* out) {
   const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (q < nq) basic_one(q, P, n, W, next, stale, lmax, have, ext, items, cnt, rc);
+  if (out) publish_from_block(rc, out);  // one work-group only
 }
 
 // Row copy in 16-byte units: dst row i <- src row ext[i].
@@ -480,8 +498,9 @@ hipError_t launch_update_lookahead(int64_t nq, const int32_t* P, int32_t n, int3
   if (hitbits && (!issued || words * 32 < n || spec_max < 0)) return hipErrorInvalidValue;
   hipLaunchKernelGGL(update_lookahead_kernel, dim3(blocks_for(nq)), dim3(kThreads), 0, s, nq, P, n,
                      W, stop, lmax, have, ext, items, cnt, rc, hitbits, words, issued, spec_max,
-                     spec_min);
-  if (out) hipLaunchKernelGGL(publish_round_kernel, dim3(1), dim3(64), 0, s, rc, out);
+                     spec_min, blocks_for(nq) == 1 ? out : nullptr);
+  if (out && blocks_for(nq) > 1)
+    hipLaunchKernelGGL(publish_round_kernel, dim3(1), dim3(64), 0, s, rc, out);
   return hipGetLastError();
 }
 
@@ -490,8 +509,10 @@ hipError_t launch_update_basic(int64_t nq, const int32_t* P, int32_t n, int32_t 
                                Item* items, int32_t* cnt, RoundCounters* rc, RoundSummary* out,
                                hipStream_t s) {
   hipLaunchKernelGGL(update_basic_kernel, dim3(blocks_for(nq)), dim3(kThreads), 0, s, nq, P, n, W,
-                     next, stale, lmax, have, ext, items, cnt, rc);
-  if (out) hipLaunchKernelGGL(publish_round_kernel, dim3(1), dim3(64), 0, s, rc, out);
+                     next, stale, lmax, have, ext, items, cnt, rc,
+                     blocks_for(nq) == 1 ? out : nullptr);
+  if (out && blocks_for(nq) > 1)
+    hipLaunchKernelGGL(publish_round_kernel, dim3(1), dim3(64), 0, s, rc, out);
   return hipGetLastError();
 }
 
