@@ -76,11 +76,14 @@ typedef struct sieve_stats {
   int32_t nprobe_eff;       /* min(nprobe_max, nlist)                                      */
   int32_t scan_launches;    /* partition-scan kernel launches                              */
   int32_t pool_retries;     /* re-runs after the candidate pool overflowed (results equal) */
-  int64_t items;            /* (query, rank) searches executed                             */
+  int64_t items;            /* (query, rank) searches executed; with lookahead this may
+                               exceed probes_total: ranks past a stop line can be
+                               searched early, and what they find is discarded            */
   int64_t probes_total;     /* sum over queries of out_probes                              */
   int64_t vectors_scanned;  /* sum over items of the probed list's length                  */
   int64_t list_loads;       /* sum over rounds of distinct non-empty lists probed          */
-  int64_t hits;             /* qualifying (query, row) pairs found                         */
+  int64_t hits;             /* qualifying (query, row) pairs found (searched ranks past the
+                               final stop line included)                                  */
   double scan_bytes;        /* algorithmic bytes of the scan: list rows + per-item query
                                rows and item records + candidate records written          */
   double scan_flops;        /* 2 * d * vectors_scanned                                     */
