@@ -375,14 +375,18 @@ int run_round(sieve_index* ix, const ScanArgs& sa, int n_items, int64_t q0, cons
   const int chunk = (int64_t)n_items >= (int64_t)pl.dense_q * ix->nlist ? pl.row_chunk_dense
                                                                         : pl.row_chunk;
   const int e0 = *at >= 0 ? *at : mark(ix, timed, s);
-  HIP_TRY(launch_sched_offsets((const int32_t*)ix->cnt.p, ix->offsets, ix->nlist, chunk,
-                               pl.group_q, (int32_t*)ix->item_off.p, (int32_t*)ix->cursor.p,
-                               (int32_t*)ix->tile_off.p, rc, s));
+  // few lists: the offsets launch also writes the tiles
+  const bool fuse = ix->nlist <= kFuseTilesMaxLists;
+  HIP_TRY(launch_sched_offsets((int32_t*)ix->cnt.p, ix->offsets, ix->nlist, chunk, pl.group_q,
+                               (int32_t*)ix->item_off.p, (int32_t*)ix->cursor.p,
+                               (int32_t*)ix->tile_off.p, rc, fuse ? (Tile*)ix->tiles.p : nullptr,
+                               s));
   HIP_TRY(launch_sched_scatter((const Item*)ix->items.p, n_items, P, pl.n, (int32_t)q0, sa.exclude,
                                (int32_t*)ix->cursor.p, (BItem*)ix->bucket.p, s));
-  HIP_TRY(launch_sched_tiles((int32_t*)ix->cnt.p, (const int32_t*)ix->item_off.p,
-                             (const int32_t*)ix->tile_off.p, ix->offsets, ix->nlist, chunk,
-                             pl.group_q, (Tile*)ix->tiles.p, s));
+  if (!fuse)
+    HIP_TRY(launch_sched_tiles((int32_t*)ix->cnt.p, (const int32_t*)ix->item_off.p,
+                               (const int32_t*)ix->tile_off.p, ix->offsets, ix->nlist, chunk,
+                               pl.group_q, (Tile*)ix->tiles.p, s));
   const int e1 = mark(ix, timed, s);
   ScanArgs sr = sa;
   sr.dynamic = scan_dynamic(n_items);

@@ -78,10 +78,13 @@ __global__ __launch_bounds__(kInitThreads) void emit_initial_kernel(
 // of the per-list tile counts; resets the round's counters.
 constexpr int kOffThreads = 1024;
 
+// tiles non-null: also write the round's tiles and clear the histogram (the
+// work of sched_tiles_kernel), for indexes with few lists per thread.
 __global__ __launch_bounds__(kOffThreads) void sched_offsets_kernel(
-    const int32_t* __restrict__ cnt, const int64_t* __restrict__ list_offsets, int32_t nlist,
+    int32_t* cnt, const int64_t* __restrict__ list_offsets, int32_t nlist,
     int32_t row_chunk, int32_t tile_q, int32_t* __restrict__ item_off,
-    int32_t* __restrict__ cursor, int32_t* __restrict__ tile_off, RoundCounters* rc) {
+    int32_t* __restrict__ cursor, int32_t* __restrict__ tile_off, RoundCounters* rc,
+    Tile* __restrict__ tiles) {
   __shared__ int64_t s_items[kOffThreads];
   __shared__ int64_t s_tiles[kOffThreads];
   __shared__ unsigned long long s_stat[3];
@@ -121,6 +124,28 @@ __global__ __launch_bounds__(kOffThreads) void sched_offsets_kernel(
     item_off[p] = (int32_t)ri;
     cursor[p] = (int32_t)ri;
     tile_off[p] = (int32_t)rt;
+    if (tiles) {
+      // the tiles of the list, written here (few lists per thread), and the
+      // list's histogram entry cleared for the next round
+      cnt[p] = 0;
+      if (c > 0 && len > 0) {
+        const int ntq = (c + tile_q - 1) / tile_q;
+        const int nch = (int)((len + row_chunk - 1) / row_chunk);
+        int32_t o = (int32_t)rt;
+        const int64_t lb = list_offsets[p];
+        for (int ch = 0; ch < nch; ++ch) {
+          for (int tq = 0; tq < ntq; ++tq) {
+            Tile tl;
+            tl.r0 = lb + (int64_t)ch * row_chunk;
+            tl.nrows = (int32_t)min<int64_t>(row_chunk, len - (int64_t)ch * row_chunk);
+            tl.item_begin = (int32_t)ri + tq * tile_q;
+            tl.nq = min(tile_q, c - tq * tile_q);
+            tl.list = p;
+            tiles[o++] = tl;
+          }
+        }
+      }
+    }
     ri += c;
     if (c > 0 && len > 0)
       rt += (int64_t)((c + tile_q - 1) / tile_q) * ((len + row_chunk - 1) / row_chunk);
@@ -463,12 +488,13 @@ hipError_t launch_emit_initial(const int32_t* P, int32_t n, int64_t nqc, int32_t
   return hipGetLastError();
 }
 
-hipError_t launch_sched_offsets(const int32_t* cnt, const int64_t* list_offsets, int32_t nlist,
+hipError_t launch_sched_offsets(int32_t* cnt, const int64_t* list_offsets, int32_t nlist,
                                 int32_t row_chunk, int32_t tile_q, int32_t* item_off,
                                 int32_t* cursor, int32_t* tile_off, RoundCounters* rc,
-                                hipStream_t s) {
+                                Tile* tiles, hipStream_t s) {
+  if (tiles && nlist > kFuseTilesMaxLists) return hipErrorInvalidValue;
   hipLaunchKernelGGL(sched_offsets_kernel, dim3(1), dim3(kOffThreads), 0, s, cnt, list_offsets,
-                     nlist, row_chunk, tile_q, item_off, cursor, tile_off, rc);
+                     nlist, row_chunk, tile_q, item_off, cursor, tile_off, rc, tiles);
   return hipGetLastError();
 }
 

@@ -153,10 +153,13 @@ hipError_t launch_rank_select(int dtype, const void* queries, int64_t q0, int32_
 hipError_t launch_emit_initial(const int32_t* P, int32_t n, int64_t nqc, int32_t q0, int32_t s0,
                                int32_t mode, Item* items, int32_t* cnt, int32_t nlist,
                                int32_t* state_a, int32_t* state_b, int32_t* lmax, hipStream_t s);
-hipError_t launch_sched_offsets(const int32_t* cnt, const int64_t* list_offsets, int32_t nlist,
+// tiles: non-null (at most kFuseTilesMaxLists lists) to write the round's
+// tiles and clear the histogram in the same launch (no sched_tiles launch).
+constexpr int kFuseTilesMaxLists = 1024;
+hipError_t launch_sched_offsets(int32_t* cnt, const int64_t* list_offsets, int32_t nlist,
                                 int32_t row_chunk, int32_t tile_q, int32_t* item_off,
                                 int32_t* cursor, int32_t* tile_off, RoundCounters* rc,
-                                hipStream_t s);
+                                Tile* tiles, hipStream_t s);
 hipError_t launch_sched_scatter(const Item* items, int32_t n_items, const int32_t* P, int32_t n,
                                 int32_t q0, const int64_t* exclude, int32_t* cursor,
                                 BItem* bucket, hipStream_t s);
