@@ -18,10 +18,13 @@
  *   - partitions are probed in centroid-ranked order P_i         (Sec. 4.1)
  *   - a probe is "empty" when no candidate reaches tau; a hit
  *     resets the consecutive-empty counter, W empties stop      (Sec. 3.5, 4.1, Table 2)
- *   - mode A: continuous batching with per-query stopping,
- *     here for one query at a time (next / stale / results)     (Sec. 4.2, Algorithm 1)
- *   - mode B: lookahead stop line s and enqueue cursor e,
- *     completions processed in LIFO order on purpose            (Sec. 4.3, Algorithm 2)
+ *   - mode A: the stop rule walked sequentially, one probe
+ *     at a time (Algorithm 1's per-query rule)                  (Sec. 3.5, 4.1, 4.2)
+ *   - mode B: lookahead over the committed prefix (stop line),
+ *     newest committed rank searched first on purpose            (Sec. 4.3, Algorithm 2)
+ *   - flags: queries whose result may legitimately differ in a
+ *     lower-precision implementation (a score within 1e-4 of tau,
+ *     of the k-th/(k+1)-th boundary, or of a returned neighbour)
  *   - final MergeTopK over all accumulated local results        (Algorithm 1, final merge)
  *   - fixed probing = the same traversal with no stop rule      (Sec. 2.3)
  *   - exhaustive filtered top-k over the whole corpus           (Sec. 6.1 ground truth)
@@ -55,8 +58,8 @@
 #define OR_EDGE_BAND 1e-4
 #define OR_CENTROID_BAND 1e-12
 
-#define OR_MODE_A 0  /* Algorithm 1: next / stale counter            */
-#define OR_MODE_B 1  /* Algorithm 2: stop line and enqueue cursor     */
+#define OR_MODE_A 0  /* sequential walk of the stop rule (Algorithm 1)   */
+#define OR_MODE_B 1  /* committed prefix under a stop line (Algorithm 2) */
 
 /* ---------------------------------------------------------------------- */
 /* IEEE 754 binary16 -> double, from the format definition:               */
@@ -182,6 +185,7 @@ static int search_list(const or_index* ix, const double* q, int list, int rank, 
     if (has_excl && ix->ids[r] == excl) continue;
     double v = dot_row(q, ix->vectors, ix->dtype, r, ix->d);
     (*scanned)++;
+    /* a score this close to tau may be decided either way in lower precision */
     if (fabs(v - tau) < OR_EDGE_BAND) *flags |= OR_FLAG_TAU_EDGE;
     if (v >= tau) {
       hit = 1;
@@ -237,40 +241,44 @@ static int one_query(const or_job* jb, int64_t qi, double* qd, int* order, doubl
   int probes = 0, last_hit = 0;
 
   if (jb->mode == OR_MODE_A) {
-    /* Algorithm 1 for a single query: next starts at rank 1, stale at 0. */
-    int next = 1, stale = 0;
-    for (;;) {
-      int j = next; /* the ready item (q_i, j) */
+    /* The stop rule as a sequential walk (Sec. 3.5, Sec. 4.1): ranks are
+     * probed one at a time in order; a hit clears the run of consecutive
+     * empty probes, an empty probe lengthens it, and the query is done when
+     * the run reaches W or all n ranks are probed.  Algorithm 1 applies the
+     * same rule per query, one completed probe at a time. */
+    int run = 0;
+    for (int j = 1; j <= n; ++j) {
       int h = search_list(ix, qd, order[j - 1], j, excl, has_excl, jb->tau, cv, &flags, &scanned);
       if (h < 0) return -1;
       hit_at[j - 1] = (uint8_t)h;
       probes = j;
-      next = j + 1;
       if (h) {
-        stale = 0;
+        run = 0;
         last_hit = j;
-      } else {
-        stale = stale + 1;
+      } else if (++run >= W) {
+        break;
       }
-      if (!(stale < W && next <= n)) break; /* otherwise enqueue (q_i, next) */
     }
   } else {
-    /* Algorithm 2: stop line s, enqueue cursor e, a LIFO ready stack so that
-     * completions arrive out of rank order on purpose. */
-    int top = 0; /* stack holds n ints: each rank is pushed at most once */
+    /* Lookahead (Sec. 4.3, Algorithm 2): the ranks up to the stop line s are
+     * committed; s starts at min(W, n), and a hit found at rank j commits
+     * every rank up to min(j + W, n).  Each committed rank is searched once.
+     * Here the most recently committed rank is searched first, so outcomes
+     * arrive out of rank order on purpose; the query is done when nothing
+     * committed is left unsearched, and its probe count is s. */
     int s = W < n ? W : n;
-    int e = 1;
-    while (e <= s) stack[top++] = e++;
-    while (top > 0) {
+    int committed = 0, top = 0; /* stack holds at most n ranks */
+    for (;;) {
+      while (committed < s) stack[top++] = ++committed;
+      if (top == 0) break;
       int j = stack[--top];
       int h = search_list(ix, qd, order[j - 1], j, excl, has_excl, jb->tau, cv, &flags, &scanned);
       if (h < 0) return -1;
       hit_at[j - 1] = (uint8_t)h;
       if (h) {
-        int reach = (W > n - j) ? n : j + W; /* min(j + W, n) without overflow */
-        if (reach > s) s = reach;
+        int line = (W > n - j) ? n : j + W; /* min(j + W, n) without overflow */
+        if (line > s) s = line;
         if (j > last_hit) last_hit = j;
-        while (e <= s) stack[top++] = e++;
       }
     }
     probes = s;
@@ -279,8 +287,11 @@ static int one_query(const or_job* jb, int64_t qi, double* qd, int* order, doubl
   /* MergeTopK over all accumulated local results. */
   qsort(cv->v, (size_t)cv->len, sizeof(cand), cand_cmp);
   int k = jb->k;
+  /* the last returned slot may go either way: the best candidate left out
+   * scores within the band of it */
   if (cv->len > k && cv->v[k - 1].s - cv->v[k].s < OR_EDGE_BAND) flags |= OR_FLAG_KTH_TIE;
   int kept = cv->len < k ? (int)cv->len : k;
+  /* two returned neighbours whose relative order may go either way */
   for (int r = 0; r + 1 < kept; ++r)
     if (cv->v[r].s - cv->v[r + 1].s < OR_EDGE_BAND) flags |= OR_FLAG_ORDER_TIE;
   for (int r = 0; r < k; ++r) {

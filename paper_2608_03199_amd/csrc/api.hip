@@ -21,6 +21,7 @@
 #include <string>
 #include <vector>
 
+#include "host_limits.h"
 #include "sieve_internal.h"
 
 namespace sieve {
@@ -89,11 +90,17 @@ struct sieve_index {
   std::vector<int64_t> h_offsets;
   int64_t max_list = 0;
   double cmax = 0.0;
-  // workspace, grown on demand
-  Buf scores, P, items, bucket, tiles, cnt, item_off, cursor, tile_off, rc, state_a, state_b,
-      lmax, hcount, hoff, hcur, scan_tmp, pool, pool_sorted, arenas, have, ext, qext, Pext,
-      cand, ccount, cal_idx, cal_q, cal_x, cal_bits, cal_rank, cal_hist, mix_ids, mix_scores,
-      mix_probes, spec_bits;
+  // workspace, grown on demand (every buffer is listed once, in SIEVE_WORKSPACE,
+  // so that sieve_free_index releases all of them)
+#define SIEVE_WORKSPACE(X)                                                                 \
+  X(scores) X(P) X(items) X(bucket) X(tiles) X(cnt) X(item_off) X(cursor) X(tile_off) X(rc) \
+  X(state_a) X(state_b) X(lmax) X(hcount) X(hoff) X(hcur) X(scan_tmp) X(pool)              \
+  X(pool_sorted) X(arenas) X(have) X(ext) X(qext) X(Pext) X(cand) X(ccount) X(cal_idx)      \
+  X(cal_q) X(cal_x) X(cal_bits) X(cal_rank) X(cal_hist) X(mix_ids) X(mix_scores)            \
+  X(mix_probes) X(spec_bits)
+#define SIEVE_DECLARE_BUF(name) Buf name;
+  SIEVE_WORKSPACE(SIEVE_DECLARE_BUF)
+#undef SIEVE_DECLARE_BUF
   int64_t pool_cap = 0;
   RoundCounters* rc_host = nullptr;
   RoundSummary* rs_host = nullptr;  // coherent pinned memory the update launches write
@@ -565,6 +572,11 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     }
 
     const int64_t hits = (int64_t)sm.hits;
+    const int64_t limit = pool_index_limit(getenv("SIEVE_POOL_LIMIT"));
+    if (!pool_slots_fit(sm.hits, limit))
+      return fail(SIEVE_EUNSUPPORTED,
+                  "the search claimed %llu candidate-pool slots; the final merge indexes at "
+                  "most %lld (32-bit offsets)", (unsigned long long)sm.hits, (long long)limit);
     if (hits > ix->pool_cap) {
       // the pool overflowed: grow it and run again (the search is deterministic)
       ix->pool_cap = hits + hits / 8 + (int64_t)pl.scan_grid * kArenaMax;
@@ -812,15 +824,10 @@ SIEVE_API int sieve_load_index(const void* vectors, int32_t dtype, int64_t n, in
 
 SIEVE_API void sieve_free_index(sieve_index* ix) {
   if (!ix) return;
-  Buf* bufs[] = {&ix->scores, &ix->P, &ix->items, &ix->bucket, &ix->tiles, &ix->cnt,
-                 &ix->item_off, &ix->cursor, &ix->tile_off, &ix->rc, &ix->state_a,
-                 &ix->state_b, &ix->lmax, &ix->hcount, &ix->hoff, &ix->hcur, &ix->scan_tmp,
-                 &ix->pool, &ix->pool_sorted, &ix->arenas, &ix->have, &ix->ext, &ix->qext,
-                 &ix->Pext, &ix->cand, &ix->ccount, &ix->cal_idx, &ix->cal_q, &ix->cal_x,
-                 &ix->cal_bits, &ix->cal_rank, &ix->cal_hist, &ix->mix_ids, &ix->mix_scores,
-                 &ix->mix_probes};
-  for (Buf* b : bufs)
-    if (b->p) (void)hipFree(b->p);
+#define SIEVE_FREE_BUF(name) \
+  if (ix->name.p) (void)hipFree(ix->name.p);
+  SIEVE_WORKSPACE(SIEVE_FREE_BUF)
+#undef SIEVE_FREE_BUF
   if (ix->vectors) (void)hipFree(ix->vectors);
   if (ix->offsets) (void)hipFree(ix->offsets);
   if (ix->ids) (void)hipFree(ix->ids);

@@ -359,6 +359,213 @@ def test_exact_score_ties_break_by_id(oracle_lib):
     assert r.probes[0] == 3 and r.hitseq[0].tolist() == [0, 1, 0]
 
 
+# ------------------------------------------------------------------ flags
+# The flags mark the queries whose outcome a lower-precision implementation may
+# legitimately decide the other way (the parity bar excuses mismatches only
+# there): TAU_EDGE when a scanned, non-excluded score in a visited list lies
+# within 1e-4 of tau; KTH_TIE when the best candidate left out of the top-k lies
+# within 1e-4 of the k-th; ORDER_TIE when two returned neighbours lie within
+# 1e-4 of each other.  Scores are placed exactly by construction: the query is
+# e0 and a row (a, sqrt(1 - a^2), 0, ...) scores a.
+BAND = 1e-4
+
+
+def _ladder_index(scores, ids=None, exclude=-1, far_list_scores=()):
+    """One query q = e0.  List 0 (ranked first) holds rows scoring exactly the
+    given fp32 values; list 1 (ranked second, never visited with nprobe 1)
+    holds rows scoring far_list_scores."""
+    d = 8
+    rows = []
+    for a in list(scores) + list(far_list_scores):
+        a = float(np.float32(a))
+        x = np.zeros(d)
+        x[0] = a
+        x[1] = np.sqrt(max(0.0, 1.0 - a * a))
+        rows.append(x)
+    X = np.array(rows, np.float32) if rows else np.zeros((0, d), np.float32)
+    # the score is X[:, 0] exactly: q has a single non-zero, 1.0, in dimension 0
+    C = np.zeros((2, d), np.float32)
+    C[0, 0], C[0, 2] = 0.9, np.sqrt(1 - 0.81)
+    C[1, 0], C[1, 2] = 0.5, np.sqrt(1 - 0.25)
+    q = np.zeros((1, d), np.float32)
+    q[0, 0] = 1.0
+    n0 = len(scores)
+    ids = np.arange(len(rows), dtype=np.int64) + 100 if ids is None else np.asarray(ids, np.int64)
+    return {"vectors": X, "ids": ids, "list_offsets": np.array([0, n0, len(rows)], np.int64),
+            "centroids": C, "queries": q, "exclude_ids": np.array([exclude], np.int64)}
+
+
+def _flags(w, tau, k=3, nprobe=1, W=1):
+    r = run(w, tau=tau, k=k, W=W, nprobe_max=nprobe)
+    f = int(r.flags[0])
+    return (bool(f & oracle.FLAG_TAU_EDGE), bool(f & oracle.FLAG_KTH_TIE),
+            bool(f & oracle.FLAG_ORDER_TIE))
+
+
+def test_flag_tau_edge_band(oracle_lib):
+    tau = float(np.float32(0.9))
+    far = [0.1]
+    for off, want in ((5e-5, True), (-5e-5, True), (0.0, True), (2e-4, False), (-2e-4, False),
+                      (3e-3, False)):
+        w = _ladder_index([0.2, tau + off], far_list_scores=far)
+        assert _flags(w, tau)[0] == want, off
+    # the query's own row is never scanned, so it never flags
+    w = _ladder_index([0.2, tau + 1e-5], ids=[100, 101, 102], exclude=101, far_list_scores=far)
+    assert _flags(w, tau)[0] is False
+    # a list the stop rule never visits never flags
+    w = _ladder_index([0.2, 0.3], far_list_scores=[tau + 1e-5])
+    assert _flags(w, tau, nprobe=1)[0] is False
+    assert _flags(w, tau, nprobe=2, W=5)[0] is True
+
+
+def test_flag_kth_tie_band(oracle_lib):
+    tau = 0.5
+    base = [0.99, 0.98, 0.97]  # k = 3 returned
+    for gap, want in ((5e-5, True), (0.0, True), (2e-4, False), (1e-3, False)):
+        w = _ladder_index(base + [0.97 - gap, 0.6])
+        assert _flags(w, tau, k=3)[1] == want, gap
+    # no (k+1)-th candidate: nothing can take the k-th slot
+    assert _flags(_ladder_index(base), tau, k=3)[1] is False
+    # a near tie below the boundary ((k+1)-th vs (k+2)-th) is not a k-th tie
+    w = _ladder_index(base + [0.90, 0.90 - 1e-5])
+    assert _flags(w, tau, k=3)[1] is False
+    # a near tie above it (1st vs (k+1)-th within the band only through the k-th) is not either
+    w = _ladder_index([0.99, 0.99 - 5e-5, 0.95, 0.80])
+    assert _flags(w, tau, k=3)[1] is False
+    # candidates below tau do not count as the (k+1)-th
+    w = _ladder_index(base + [0.97 - 5e-5])
+    assert _flags(w, 0.97 - 1e-3 + 0.0, k=3)[1] is True
+    assert _flags(w, float(np.float32(0.97)) + 0.0, k=3)[1] is False
+
+
+def test_flag_order_tie_band(oracle_lib):
+    tau = 0.5
+    for gap, want in ((5e-5, True), (0.0, True), (2e-4, False)):
+        w = _ladder_index([0.99, 0.95, 0.95 - gap, 0.7])
+        assert _flags(w, tau, k=3)[2] == want, gap
+    # only returned neighbours count: a tie between the k-th and the (k+1)-th
+    # is a k-th tie, not an order tie
+    w = _ladder_index([0.99, 0.95, 0.90, 0.90 - 5e-5])
+    assert _flags(w, tau, k=3) == (False, True, False)
+    # the first and the last returned pair are both inspected
+    w = _ladder_index([0.99, 0.99 - 5e-5, 0.90, 0.80])
+    assert _flags(w, tau, k=3)[2] is True
+    w = _ladder_index([0.99, 0.90, 0.80, 0.80 - 5e-5, 0.6])
+    assert _flags(w, tau, k=4)[2] is True
+
+
+def _np_flags_one(w, i, tau, k, W, n, order):
+    """Flags of query i from numpy float64 scores over the visited prefix (numpy order,
+    numpy hit sequence, replayed stop rule): (tau_edge, kth_tie, order_tie, candidates)."""
+    X, ids, off = w["vectors"], w["ids"], w["list_offsets"]
+    q, ex = w["queries"][i], w["exclude_ids"][i]
+    t = np.float64(np.float32(tau))
+    h = np_hit_sequence(w, q, ex, tau, order[:n])
+    p = replay_probes(h, W)
+    edge = False
+    cand = []
+    for j in range(p):
+        rows = np.arange(off[order[j]], off[order[j] + 1])
+        rows = rows[ids[rows] != ex]
+        s = _np_f64(X[rows]) @ _np_f64(q)
+        edge |= bool(np.any(np.abs(s - t) < BAND))
+        cand += [(float(v), int(x)) for v, x in zip(s, ids[rows]) if v >= t]
+    cand.sort(key=lambda c: (-c[0], c[1]))
+    kth = len(cand) > k and cand[k - 1][0] - cand[k][0] < BAND
+    top = cand[:k]
+    otie = any(top[j][0] - top[j + 1][0] < BAND for j in range(len(top) - 1))
+    return edge, kth, otie, cand
+
+
+def _flag_rich_index(seed, tau):
+    """A random index with score ladders planted around tau and around each query's
+    top candidates, so that every flag is set for some queries and clear for others."""
+    rng = np.random.default_rng(seed)
+    w = random_index(seed, n=500, d=16, nlist=6, nq=24)
+    X = w["vectors"].astype(np.float64)
+    extra = []
+    for qv in w["queries"].astype(np.float64):
+        qn = qv / np.linalg.norm(qv)
+        for _ in range(4):
+            # a row scoring tau + u (|u| up to 3e-4) and a pair 0 .. 2e-4 apart near 0.97
+            for a in (tau + rng.uniform(-3e-4, 3e-4), 0.97, 0.97 - rng.uniform(0, 2e-4)):
+                u = rng.standard_normal(X.shape[1])
+                u -= (u @ qn) * qn
+                u /= np.linalg.norm(u)
+                extra.append(a * qn + np.sqrt(1 - a * a) * u)
+    E = np.array(extra)
+    Xa = np.concatenate([X, E]).astype(np.float32)
+    # every planted row joins its nearest centroid's list (row order by list)
+    C = w["centroids"].astype(np.float64)
+    lst = np.argmax(Xa.astype(np.float64) @ C.T, axis=1)
+    o = np.argsort(lst, kind="stable")
+    ids = np.arange(len(Xa), dtype=np.int64)[o] + 7
+    qrows = rng.choice(len(X), len(w["queries"]), replace=False)
+    Xs = Xa[o]
+    pos = np.empty(len(o), np.int64)
+    pos[o] = np.arange(len(o))
+    return {"vectors": Xs, "ids": ids,
+            "list_offsets": np.concatenate([[0], np.cumsum(np.bincount(lst, minlength=len(C)))]
+                                           ).astype(np.int64),
+            "centroids": w["centroids"], "queries": Xa[qrows], "exclude_ids": qrows + 7}
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_flags_match_numpy_on_random_indexes(seed, oracle_lib):
+    """Every flag bit, recomputed from numpy float64 scores over the visited prefix."""
+    tau = 0.6
+    w = _flag_rich_index(seed, tau)
+    nlist = w["centroids"].shape[0]
+    seen = np.zeros(3, int)
+    for W, k, npb in ((1, 3, nlist), (2, 5, 4), (oracle.W_INF, 4, nlist)):
+        r = run(w, tau=tau, k=k, W=W, nprobe_max=npb)
+        n = min(npb, nlist)
+        for i in range(len(w["queries"])):
+            order, _ = np_order(w["centroids"], w["queries"][i])
+            edge, kth, otie, _ = _np_flags_one(w, i, tau, k, W, n, order)
+            f = int(r.flags[i])
+            got = (bool(f & oracle.FLAG_TAU_EDGE), bool(f & oracle.FLAG_KTH_TIE),
+                   bool(f & oracle.FLAG_ORDER_TIE))
+            assert got == (edge, kth, otie), (seed, W, k, i)
+            seen += np.array(got, int)
+    # the planted ladders make every flag occur (and not everywhere)
+    total = 3 * len(w["queries"])
+    assert np.all(seen > 0) and np.all(seen < total), seen
+
+
+def test_multi_index_flags_match_numpy(oracle_lib):
+    """search_multi's flags: TAU_EDGE of any shard (each shard's own visited lists);
+    KTH_TIE of any shard or at the boundary of the merged candidates; ORDER_TIE among
+    the merged top-k."""
+    tau, k, W = 0.6, 4, 1
+    w = _flag_rich_index(5, tau)
+    nlist = w["centroids"].shape[0]
+    shards = _shard(w, 3, 11)
+    r = oracle.search_multi(shards, w["queries"], w["exclude_ids"], k, tau, W, nlist)
+    seen = np.zeros(3, int)
+    for i in range(len(w["queries"])):
+        edge = kth = False
+        allc = []
+        for sh in shards:
+            sh_w = dict(sh, queries=w["queries"], exclude_ids=w["exclude_ids"])
+            order, _ = np_order(sh["centroids"], w["queries"][i])
+            e, kt, _, c = _np_flags_one(sh_w, i, tau, k, W, nlist, order)
+            edge |= e
+            kth |= kt
+            allc += c
+        allc.sort(key=lambda c: (-c[0], c[1]))
+        kth |= len(allc) > k and allc[k - 1][0] - allc[k][0] < BAND
+        top = allc[:k]
+        otie = any(top[j][0] - top[j + 1][0] < BAND for j in range(len(top) - 1))
+        f = int(r.flags[i])
+        got = (bool(f & oracle.FLAG_TAU_EDGE), bool(f & oracle.FLAG_KTH_TIE),
+               bool(f & oracle.FLAG_ORDER_TIE))
+        assert got == (edge, kth, otie), i
+        assert [x for x in r.ids[i] if x >= 0] == [c[1] for c in top]
+        seen += np.array(got, int)
+    assert np.all(seen > 0), seen
+
+
 # ------------------------------------------------------------ calibration
 def test_calibration_replay_matches_direct_runs(tiny):
     """Appendix A: H's prefix sums equal the retained counts of actual W runs."""
@@ -403,7 +610,7 @@ def test_pooled_recall_toy():
 
 # -------------------------------------------------------------- mutation
 MUTANTS = {
-    "no_stale_reset": ("        stale = 0;\n        last_hit = j;", "        last_hit = j;"),
+    "no_stale_reset": ("        run = 0;\n        last_hit = j;", "        last_hit = j;"),
     "strict_threshold": ("    if (v >= tau) {", "    if (v > tau) {"),
     "id_tiebreak_reversed": ("  if (a->id < b->id) return -1;\n  if (a->id > b->id) return 1;",
                              "  if (a->id < b->id) return 1;\n  if (a->id > b->id) return -1;"),
@@ -413,12 +620,29 @@ MUTANTS = {
                          "  for (int t = 0; t < d - 1; ++t) s += q[t]"),
     "no_self_exclusion": ("    if (has_excl && ix->ids[r] == excl) continue;\n    double v",
                           "    double v"),
-    "stop_line_short": ("int reach = (W > n - j) ? n : j + W;",
-                        "int reach = (W > n - j) ? n : j + W - 1;"),
-    "stop_one_late": ("      if (!(stale < W && next <= n)) break;",
-                      "      if (!(stale <= W && next <= n)) break;"),
+    "stop_line_short": ("int line = (W > n - j) ? n : j + W;",
+                        "int line = (W > n - j) ? n : j + W - 1;"),
+    "stop_one_late": ("      } else if (++run >= W) {", "      } else if (++run > W) {"),
     "order_ascending": ("  if (a->s > b->s) return -1;\n  if (a->s < b->s) return 1;\n  return (a->c",
                         "  if (a->s > b->s) return 1;\n  if (a->s < b->s) return -1;\n  return (a->c"),
+    # the tie/threshold flags that excuse GPU/oracle differences
+    "edge_band_too_wide": ("#define OR_EDGE_BAND 1e-4", "#define OR_EDGE_BAND 1e-2"),
+    "tau_edge_always": ("    if (fabs(v - tau) < OR_EDGE_BAND) *flags |= OR_FLAG_TAU_EDGE;",
+                        "    *flags |= OR_FLAG_TAU_EDGE;"),
+    "tau_edge_counts_excluded": (
+        "    if (has_excl && ix->ids[r] == excl) continue;\n"
+        "    double v = dot_row(q, ix->vectors, ix->dtype, r, ix->d);\n"
+        "    (*scanned)++;\n"
+        "    /* a score this close to tau may be decided either way in lower precision */\n"
+        "    if (fabs(v - tau) < OR_EDGE_BAND) *flags |= OR_FLAG_TAU_EDGE;\n",
+        "    double v = dot_row(q, ix->vectors, ix->dtype, r, ix->d);\n"
+        "    if (fabs(v - tau) < OR_EDGE_BAND) *flags |= OR_FLAG_TAU_EDGE;\n"
+        "    if (has_excl && ix->ids[r] == excl) continue;\n"
+        "    (*scanned)++;\n"),
+    "kth_tie_wrong_index": ("cv->v[k - 1].s - cv->v[k].s < OR_EDGE_BAND",
+                            "cv->v[0].s - cv->v[k].s < OR_EDGE_BAND"),
+    "order_tie_off_by_one": ("  for (int r = 0; r + 1 < kept; ++r)\n    if (cv->v[r].s",
+                             "  for (int r = 0; r + 2 < kept; ++r)\n    if (cv->v[r].s"),
 }
 
 
@@ -451,6 +675,10 @@ checks = [
     lambda: T.test_probes_match_replay_and_closed_form(tiny, 3),
     lambda: T.test_lookahead_equivalence_mode_a_equals_mode_b("tiny", 3, type("R", (), {{"getfixturevalue": lambda s, n: tiny}})()),
     lambda: T.test_rank_order_matches_numpy("tiny", type("R", (), {{"getfixturevalue": lambda s, n: tiny}})()),
+    lambda: T.test_flag_tau_edge_band(None),
+    lambda: T.test_flag_kth_tie_band(None),
+    lambda: T.test_flag_order_tie_band(None),
+    lambda: T.test_flags_match_numpy_on_random_indexes(0, None),
 ]
 failed = 0
 for c in checks:
