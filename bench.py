@@ -1,16 +1,21 @@
-"""Benchmark: threshold-aware IVF search (W = 8, lookahead) on one MI355X.
+"""Benchmark: threshold-aware IVF search (W = 8) on one MI355X, every workload in one run.
 
-One step = one sieve_search call over the workload's whole query batch with
-inputs resident in HBM: centroid ranking, partition-major scheduling rounds,
-the partition scan with the tau test, the stop-rule updates and the final
-top-k.  The default workload is the mid-size self-join (N = 1,000,000 rows,
-d = 128, fp32, nlist = 1,024, Q = 10,000, k = 10, tau = 0.92, W = 8,
-nprobe_max = 128).  The same run times the fixed-probe baseline (nprobe = 128)
-on the same GPU for the speedup, reads the partition-scan kernel's device
-time from the library's HIP events on the search stream for the roofline,
-and times the CPU oracle on a bounded query sample (cpu_baseline).
+One step = one sieve_search call over a workload's whole query batch with inputs resident in
+HBM: centroid ranking, partition-major scheduling rounds, the partition scan with the tau test,
+the stop-rule updates and the final top-k.  The headline (`value`, `config`, `roofline`,
+`cpu_baseline`) is the largest workload, the 100M x 128 fp16 self-join (nlist 16,384, 1M
+queries, k = 10, tau = 0.90, W = 8, nprobe_max = 512), searched with Algorithm 2 lookahead
+(committed ranks only); the smaller workloads are reported under `configs` from the same run.
+Per workload the run also times:
+  * speculative issue (the library's addition to Algorithm 2; identical outputs),
+  * the fixed-probe baseline at the workload's nprobe on the same GPU (speedup),
+  * the in-call calibrated search (Appendix A),
+  * the CPU oracle: one thread on a small seeded sample, and all host threads (at most 16)
+    on the seeded parity subset, whose GPU results are compared with it element by element.
+The partition scan's device time per round comes from the library's HIP events on the search
+stream (sieve_round_log), over the timed steps.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config c2]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config all|c1|c2|c3|c5]
 
 Prints exactly one JSON line (last line of stdout).
 """
@@ -29,8 +34,12 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"f32": 157.3, "f16": 2500.0}
 PMC_FILE = os.path.join(ROOT, "profiles", "scan_traffic_pmc.json")
-# oracle sample per workload: roughly 10-30 s of single-thread fp64 work
-ORACLE_SAMPLE = {"tiny": 150, "tiny16": 150, "c1": 1000, "c2": 10000, "c3": 200, "c5": 300}
+CONFIG_ORDER = ["c1", "c2", "c3", "c5"]
+# single-thread oracle sample per workload: roughly 5-15 s of fp64 work
+ORACLE_ONE_THREAD = {"tiny": 150, "tiny16": 150, "c1": 1000, "c2": 4000, "c3": 100, "c5": 150}
+# parity subset, checked with the threaded oracle (all queries of the small workloads)
+ORACLE_PARITY = {"tiny": 150, "tiny16": 150, "c1": 1000, "c2": 10000, "c3": 5000, "c5": 5000}
+ORACLE_MAX_THREADS = 16
 SCAN_SOURCES = ["paper_2608_03199_amd/csrc/scan.hip", "paper_2608_03199_amd/csrc/mfma_tile.h"]
 
 
@@ -63,7 +72,240 @@ def measured_traffic(config: str):
 def workload_name(spec) -> str:
     return (f"{spec.name}: self-join N={spec.n:,} d={spec.d} {spec.dtype}, nlist={spec.nlist:,}, "
             f"Q={spec.nq:,}, k={spec.k}, tau={spec.tau}, W={spec.W}, "
-            f"nprobe_max={spec.nprobe_max}, lookahead on")
+            f"nprobe_max={spec.nprobe_max}, Algorithm 2 lookahead")
+
+
+def roofline(dtype, rounds, config):
+    """Roofline of the partition scan over the timed steps' rounds.
+
+    Step-aggregate form (`frac`): the summed algorithmic bytes and flops of a step priced
+    against the bound they imply, achieved = per-launch work / average launch time.
+    Per-round form (`frac_rounds`): sum over rounds of max(B_r / BW, F_r / P) divided by
+    the summed measured scan time, each round against its own bound."""
+    peak_f = MFMA_PEAK_TFLOPS[dtype]
+    launches = len(rounds)
+    B = sum(r["scan_bytes"] for r in rounds)
+    F = sum(r["scan_flops"] for r in rounds)
+    T = sum(r["ms_scan"] for r in rounds) * 1e-3
+    t_hbm = B / (HBM_PEAK_GBS * 1e9)
+    t_mfma = F / (peak_f * 1e12)
+    bound = "hbm" if t_hbm >= t_mfma else "mfma"
+    avg_s = T / max(launches, 1)
+    gbs = (B / max(launches, 1)) / avg_s / 1e9 if avg_s > 0 else 0.0
+    tfs = (F / max(launches, 1)) / avg_s / 1e12 if avg_s > 0 else 0.0
+    if bound == "hbm":
+        roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    else:
+        roof = {"bound": "mfma", "achieved": round(tfs, 2), "peak": peak_f, "unit": "TFLOP/s",
+                "frac": round(tfs / peak_f, 4)}
+    roof["traffic"] = measured_traffic(config)
+    roof["kernel"] = "scan_kernel (partition scan + tau test)"
+    roof["launches_per_step"] = launches
+    roof["avg_launch_ms"] = round(avg_s * 1e3, 5)
+    roof["alg_bytes_per_launch"] = round(B / max(launches, 1))
+    roof["alg_flops_per_launch"] = round(F / max(launches, 1))
+    roof["other_bound_frac"] = round((tfs / peak_f) if bound == "hbm" else (gbs / HBM_PEAK_GBS),
+                                     4)
+    per, tstar_sum = [], 0.0
+    for r in rounds:
+        tb = r["scan_bytes"] / (HBM_PEAK_GBS * 1e9)
+        tf = r["scan_flops"] / (peak_f * 1e12)
+        ts = max(tb, tf)
+        tstar_sum += ts
+        t = r["ms_scan"] * 1e-3
+        per.append({"items": r["items"], "list_loads": r["list_loads"],
+                    "bytes": round(r["scan_bytes"]), "flops": round(r["scan_flops"]),
+                    "ms": round(r["ms_scan"], 4), "bound": "hbm" if tb >= tf else "mfma",
+                    "bound_ms": round(ts * 1e3, 4), "frac": round(ts / t, 4) if t > 0 else None})
+    roof["frac_rounds"] = round(tstar_sum / T, 4) if T > 0 else None
+    roof["rounds"] = per
+    return roof
+
+
+def e1_diagnostics(np, ids, probes, W, n):
+    """The paper's Figure 1 analogue from the outputs: the share of queries without a
+    neighbour, and the last-hit rank L of the others (probes = min(L + W, n), so L is
+    probes - W wherever the query stopped before n)."""
+    zero = float((ids[:, 0] < 0).mean())
+    p = probes.astype(np.int64)
+    stopped = p < n
+    L = np.where(stopped, p - W, -1)
+    with_hit = L[(L > 0)]
+    pct = {f"p{q}": (int(np.percentile(with_hit, q)) if with_hit.size else None)
+           for q in (50, 90, 99)}
+    return {"zero_neighbour_share": round(zero, 5),
+            "last_hit_rank": dict(pct, max=int(with_hit.max()) if with_hit.size else None,
+                                  queries=int(with_hit.size)),
+            "reached_nprobe_max": int((~stopped).sum())}
+
+
+def _timed_steps(torch, fn, steps):
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    out = []
+    for _ in range(steps):
+        out.append(fn())
+    torch.cuda.synchronize()
+    return out, time.perf_counter() - t0
+
+
+def run_config(name, args, ps, sw, np, torch, dev, headline):
+    spec = sw.SPECS[name]
+    log(f"[bench] {name}: generating on {dev}")
+    t0 = time.time()
+    w = sw.make(spec, device=dev)
+    torch.cuda.synchronize()
+    lists = sw.list_stats(w.list_offsets.cpu().numpy())
+    log(f"[bench] {name}: generated in {time.time() - t0:.1f}s; lists {lists}")
+    ix = ps.Index(w.vectors, w.list_offsets, w.ids, w.centroids)
+    nq = spec.nq
+    K = args.steps
+
+    def sieve(with_stats=True, speculative=False):
+        return ix.search(w.queries, w.exclude_ids, spec.k, spec.tau, spec.W, spec.nprobe_max,
+                         lookahead=True, speculative=speculative, with_stats=with_stats)
+
+    def fixed(with_stats=True):
+        return ix.search_fixed(w.queries, w.exclude_ids, spec.k, spec.tau, spec.fixed_nprobe,
+                               with_stats=with_stats)
+
+    if args.copy_probe:
+        # 1 GiB fill (writes 1 GiB) and 1 GiB elementwise scale (reads 1 GiB, writes 1 GiB):
+        # the HBM byte counters of these two kernels calibrate the scan kernel's counters.
+        a = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        a.fill_(1.0)
+        torch.mul(a, 2.0, out=b)
+        torch.cuda.synchronize()
+        del a, b
+
+    for _ in range(args.warmup):
+        sieve()
+    # timed region: exactly K steps of the threshold search (Algorithm 2 lookahead); the
+    # per-round scan times of every step come from the library's event log
+    log(f"[bench] {name}: timing {K} steps")
+    rounds = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(K):
+        r = sieve()
+        rounds.extend(x.as_dict() for x in ix.round_log())
+    torch.cuda.synchronize()
+    t_sieve = time.perf_counter() - t0
+    ids, scores, probes, st = r
+    stats = st
+    res = {"workload": workload_name(spec), "queries": nq, "steps": K,
+           "qps": round(nq * K / t_sieve, 1), "ms_per_step": round(1e3 * t_sieve / K, 4),
+           "mean_probes": round(float(probes.float().mean().item()), 3),
+           "scanned_probes_per_query": round(stats.items / nq, 3), "rounds": stats.rounds,
+           "partition_vectors_per_s": round(stats.vectors_scanned * K / t_sieve, 1),
+           "candidates": int(stats.hits)}
+    roof = roofline(spec.dtype, rounds, name)
+    # per-step round table: the last step's rounds (every step runs the same rounds)
+    roof["rounds"] = roof["rounds"][-stats.rounds:] if stats.rounds else []
+    res["scan_hbm_gbs"] = round(sum(x["scan_bytes"] for x in rounds) /
+                                max(sum(x["ms_scan"] for x in rounds) * 1e-3, 1e-12) / 1e9, 1)
+    res["phase_ms"] = {k: round(getattr(stats, "ms_" + k), 4) for k in
+                       ("rank", "sched", "scan", "update", "finalize", "total")}
+    res["roofline"] = roof
+    res["lists"] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in lists.items()}
+    h_ids, h_probes = ids.cpu().numpy(), probes.cpu().numpy()
+    res["e1"] = e1_diagnostics(np, h_ids, h_probes, spec.W, min(spec.nprobe_max, spec.nlist))
+
+    # speculative issue past the stop line (same outputs, fewer rounds, more searches)
+    ks = max(1, min(K, 5))
+    sp, t_sp = _timed_steps(torch, lambda: sieve(speculative=True), ks)
+    same = all(bool(torch.equal(x, y)) for x, y in zip(sp[-1][:3], (ids, scores, probes)))
+    res["speculative"] = {"qps": round(nq * ks / t_sp, 1), "steps": ks,
+                          "rounds": sp[-1][3].rounds,
+                          "scanned_probes_per_query": round(sp[-1][3].items / nq, 3),
+                          "identical_outputs": same}
+
+    # fixed-probe baseline on the same GPU
+    kf = K if spec.n <= 1_000_000 else max(1, min(K, 3))
+    fixed()
+    fr, t_fixed = _timed_steps(torch, fixed, kf)
+    fst = fr[-1][3]
+    res["fixed_nprobe"] = spec.fixed_nprobe
+    res["fixed_qps"] = round(nq * kf / t_fixed, 1)
+    res["speedup_vs_fixed"] = round((t_fixed / kf) / (t_sieve / K), 3)
+    res["speculative"]["speedup_vs_fixed"] = round((t_fixed / kf) / (t_sp / ks), 3)
+    res["fixed_phase_ms"] = {k: round(getattr(fst, "ms_" + k), 4) for k in
+                             ("rank", "sched", "scan", "finalize", "total")}
+    res["fixed_roofline"] = {k: v for k, v in roofline(
+        spec.dtype, [x.as_dict() for x in ix.round_log()], name).items()
+        if k not in ("rounds", "traffic")}
+
+    # in-call calibration (Appendix A): a seeded 2% sample fully probed, the window chosen
+    # for a 0.5% sample-relative loss target, the rest searched with it; the sample's full
+    # probing is inside the timed region
+    if not args.skip_calibrated:
+        ns = max(1, nq // 50)
+        smp = torch.from_numpy(np.random.default_rng(spec.seed + 91).choice(
+            nq, ns, replace=False).astype(np.int32)).to(dev)
+        cal_fn = lambda: ix.search_calibrated(w.queries, w.exclude_ids, spec.k, spec.tau,
+                                              spec.nprobe_max, smp, CAL_EPS, spec.W)
+        cal_fn()
+        kc = max(1, min(K, 3))
+        cr, t_cal = _timed_steps(torch, cal_fn, kc)
+        res["calibrated"] = {"W": cr[-1][3], "sample": ns, "eps": CAL_EPS, "steps": kc,
+                             "qps": round(nq * kc / t_cal, 1),
+                             "speedup_vs_fixed": round((t_fixed / kf) / (t_cal / kc), 3),
+                             "mean_probes": round(float(cr[-1][2].float().mean().item()), 3)}
+    ix.close()
+
+    if not args.no_oracle:
+        res.update(oracle_legs(name, spec, w, np, h_ids, scores.cpu().numpy(), h_probes, args))
+    del w, ids, scores, probes
+    torch.cuda.empty_cache()
+    return res
+
+
+def oracle_legs(name, spec, w, np, ids, scores, probes, args):
+    """cpu_baseline: the oracle (mode A) on one thread over a small seeded sample, then on
+    all host threads (at most 16) over the seeded parity subset; the GPU results of the
+    parity subset are compared with it element by element."""
+    import oracle
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from parity import compare
+    h = {k: getattr(w, k).cpu().numpy() for k in
+         ("vectors", "ids", "list_offsets", "centroids", "exclude_ids")}
+    nq = spec.nq
+    rng = np.random.default_rng(spec.seed + 77)
+    m1 = min(args.oracle_queries or ORACLE_ONE_THREAD.get(name, 1000), nq)
+    sel1 = np.sort(rng.choice(nq, m1, replace=False))
+    q1 = w.queries[np.asarray(sel1)].cpu().numpy()
+    log(f"[bench] {name}: oracle on {m1} queries, 1 thread")
+    t0 = time.perf_counter()
+    oracle.search(h["vectors"], h["list_offsets"], h["ids"], h["centroids"], q1,
+                  h["exclude_ids"][sel1], spec.k, spec.tau, spec.W, spec.nprobe_max,
+                  oracle.MODE_A, 1)
+    t1 = time.perf_counter() - t0
+    mp = min(ORACLE_PARITY.get(name, 1000), nq)
+    selp = np.sort(np.random.default_rng(spec.seed + 501).choice(nq, mp, replace=False))
+    qp = w.queries[np.asarray(selp)].cpu().numpy()
+    nth = max(1, min(ORACLE_MAX_THREADS, os.cpu_count() or 1))
+    log(f"[bench] {name}: oracle on {mp} queries, {nth} threads")
+    t0 = time.perf_counter()
+    o = oracle.search(h["vectors"], h["list_offsets"], h["ids"], h["centroids"], qp,
+                      h["exclude_ids"][selp], spec.k, spec.tau, spec.W, spec.nprobe_max,
+                      oracle.MODE_A, nth)
+    tp = time.perf_counter() - t0
+    rep = compare(ids[selp], scores[selp], probes[selp], o)
+    return {
+        "cpu_baseline": {"value": round(m1 / t1, 2), "unit": "queries/s", "cores": 1,
+                         "kind": "oracle",
+                         "sample": f"{m1} seeded queries of the same workload, one thread, "
+                                   f"{t1:.1f}s",
+                         "threaded": {"value": round(mp / tp, 2), "cores": nth,
+                                      "sample": f"the {mp}-query parity subset, {nth} "
+                                                f"threads over disjoint query blocks, "
+                                                f"{tp:.1f}s"},
+                         "cpu": _cpu_model()},
+        "parity_sample": {k: rep[k] for k in ("queries", "mismatch", "flag_tau_edge",
+                                              "flag_kth_tie", "flag_order_tie",
+                                              "flagged_mismatch", "max_score_err")}}
 
 
 def main():
@@ -71,13 +313,13 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="c2")
+    ap.add_argument("--config", default="all",
+                    help="all (every workload, the 100M one as the headline) or one of "
+                         "c1, c2, c3, c5")
     ap.add_argument("--oracle-queries", type=int, default=None,
-                    help="queries in the single-thread oracle sample (default: about 10-30 s "
+                    help="queries in the single-thread oracle sample (default: about 5-15 s "
                          "of oracle work for the workload)")
     ap.add_argument("--no-oracle", action="store_true")
-    ap.add_argument("--skip-fixed", action="store_true",
-                    help="do not time the fixed-probe baseline (profiling runs)")
     ap.add_argument("--skip-calibrated", action="store_true",
                     help="do not time the in-call calibrated search (profiling runs)")
     ap.add_argument("--copy-probe", action="store_true",
@@ -88,8 +330,8 @@ def main():
                          "fixed-probe output (one JSON line)")
     ap.add_argument("--concurrency", action="store_true",
                     help="queries per call in {1, 10, 100, 1000, 10000} on the 1M x 128 data, "
-                         "for lookahead, basic and serial dispatch and fixed probing (one JSON "
-                         "line)")
+                         "for Algorithm 2 lookahead (with and without speculative issue), "
+                         "basic and serial dispatch and fixed probing (one JSON line)")
     ap.add_argument("--multi", action="store_true",
                     help="multi-index search: the 100M x 128 data split into 16 coarse shards, "
                          "each its own IVF with its own stop rule, one global top-k; against "
@@ -103,7 +345,8 @@ def main():
                          "data (prints one JSON line with the table)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py: this build measures one GPU only; --gpus must be 1", file=sys.stderr)
+        print("bench.py: this build measures one GPU; every box here has one GPU, so --gpus "
+              "must be 1 (the multi-GPU design is described, not built)", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -122,178 +365,53 @@ def main():
         return concurrency(args, ps, sw, np, torch, dev)
     if args.multi:
         return multi(args, ps, sw, np, torch, dev)
-    spec = sw.SPECS[args.config]
-    log(f"[bench] generating {args.config} on {dev}")
-    t0 = time.time()
-    w = sw.make(spec, device=dev)
-    torch.cuda.synchronize()
-    log(f"[bench] generated in {time.time() - t0:.1f}s; lists {sw.list_stats(w.list_offsets.cpu().numpy())}")
-    ix = ps.Index(w.vectors, w.list_offsets, w.ids, w.centroids)
-    nq = spec.nq
-
-    if args.copy_probe:
-        # 1 GiB fill (writes 1 GiB) and 1 GiB elementwise scale (reads 1 GiB,
-        # writes 1 GiB): the HBM byte counters of these two kernels calibrate
-        # the counters read on the scan kernel.
-        a = torch.empty(1 << 28, dtype=torch.float32, device=dev)
-        b = torch.empty_like(a)
-        a.fill_(1.0)
-        torch.mul(a, 2.0, out=b)
-        torch.cuda.synchronize()
-        del a, b
-
-    def sieve(with_stats=True):
-        return ix.search(w.queries, w.exclude_ids, spec.k, spec.tau, spec.W, spec.nprobe_max,
-                         lookahead=True, with_stats=with_stats)
-
-    def fixed(with_stats=True):
-        return ix.search_fixed(w.queries, w.exclude_ids, spec.k, spec.tau, spec.fixed_nprobe,
-                               with_stats=with_stats)
-
-    for _ in range(args.warmup):
-        sieve()
-        if not args.skip_fixed:
-            fixed()
-    torch.cuda.synchronize()
-
-    # timed region: exactly K sieve steps
-    log(f"[bench] timing {args.steps} steps")
-    stats = []
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        r = sieve()
-        stats.append(r[3])
-    torch.cuda.synchronize()
-    t_sieve = time.perf_counter() - t0
-    ids, scores, probes = r[0], r[1], r[2]
-
-    # fixed-probe baseline on the same GPU (same number of steps)
-    fstats = []
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(0 if args.skip_fixed else args.steps):
-        fr = fixed()
-        fstats.append(fr[3])
-    torch.cuda.synchronize()
-    t_fixed = time.perf_counter() - t0 if not args.skip_fixed else float("nan")
-
-    # in-call calibration (Appendix A): a seeded 2% sample fully probed, the
-    # window chosen for a 0.5% sample-relative loss target, the rest searched
-    # with it; the sample's full probing is inside the timed region
-    cal = None
-    if not args.skip_calibrated:
-        ns = max(1, nq // 50)
-        smp = torch.from_numpy(np.random.default_rng(spec.seed + 91).choice(
-            nq, ns, replace=False).astype(np.int32)).to(dev)
-
-        def calibrated(with_stats=True):
-            return ix.search_calibrated(w.queries, w.exclude_ids, spec.k, spec.tau,
-                                        spec.nprobe_max, smp, CAL_EPS, spec.W,
-                                        with_stats=with_stats)
-
-        calibrated()
-        csteps = max(1, min(args.steps, 5))
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(csteps):
-            cr = calibrated()
-        torch.cuda.synchronize()
-        t_cal = (time.perf_counter() - t0) / csteps
-        cal = {"W": cr[3], "sample": ns, "eps": CAL_EPS, "steps": csteps,
-               "qps": round(nq / t_cal, 1),
-               "speedup_vs_fixed": (None if args.skip_fixed else
-                                    round((t_fixed / args.steps) / t_cal, 3)),
-               "mean_probes": round(float(cr[2].float().mean().item()), 3)}
-
-    ms_step = 1e3 * t_sieve / args.steps
-    qps = nq * args.steps / t_sieve
-    fixed_qps = nq * args.steps / t_fixed
-    st = stats[-1]
-    mean = lambda xs, f: float(np.mean([getattr(x, f) for x in xs]))
-    ms_scan = mean(stats, "ms_scan")
-    launches = st.scan_launches
-    bytes_launch = st.scan_bytes / max(launches, 1)
-    flops_launch = st.scan_flops / max(launches, 1)
-    avg_launch_ms = ms_scan / max(launches, 1)
-    peak_f = MFMA_PEAK_TFLOPS[spec.dtype]
-    t_hbm = st.scan_bytes / (HBM_PEAK_GBS * 1e9)
-    t_mfma = st.scan_flops / (peak_f * 1e12)
-    bound = "hbm" if t_hbm >= t_mfma else "mfma"
-    gbs = bytes_launch / (avg_launch_ms * 1e-3) / 1e9
-    tfs = flops_launch / (avg_launch_ms * 1e-3) / 1e12
-    traffic = measured_traffic(args.config)
-    if bound == "hbm":
-        roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(gbs / HBM_PEAK_GBS, 4)}
-    else:
-        roof = {"bound": "mfma", "achieved": round(tfs, 2), "peak": peak_f, "unit": "TFLOP/s",
-                "frac": round(tfs / peak_f, 4)}
-    roof["traffic"] = traffic
-    roof["kernel"] = "scan_kernel (partition scan + tau test)"
-    roof["launches_per_step"] = launches
-    roof["avg_launch_ms"] = round(avg_launch_ms, 5)
-    roof["alg_bytes_per_launch"] = round(bytes_launch)
-    roof["alg_flops_per_launch"] = round(flops_launch)
-    roof["other_bound_frac"] = round((tfs / peak_f) if bound == "hbm" else (gbs / HBM_PEAK_GBS), 4)
-    roof["roofline_time_frac"] = round(max(t_hbm, t_mfma) / (ms_scan * 1e-3), 4)
-
+    names = CONFIG_ORDER if args.config == "all" else [args.config]
+    head = "c5" if "c5" in names else names[-1]
+    results = {}
+    for name in names:
+        results[name] = run_config(name, args, ps, sw, np, torch, dev, name == head)
+        log(f"[bench] {name}: {json.dumps({k: results[name].get(k) for k in ('qps', 'speedup_vs_fixed', 'rounds', 'mean_probes')})}")
+    hr = results[head]
+    spec = sw.SPECS[head]
     out = {
         "metric": "queries/sec at W=8 (k=10, tau); speedup vs fixed-nprobe; scan HBM GB/s",
-        "value": round(qps, 1),
+        "value": hr["qps"],
         "unit": "queries/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 4),
+        "ms_per_step": hr["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": spec.dtype,
         "data": "synthetic (seeded mixture + near-duplicate groups, spherical k-means IVF)",
-        "config": {"workload": workload_name(spec), "queries": nq, "k": spec.k,
+        "config": {"workload": hr["workload"], "queries": spec.nq, "k": spec.k,
                    "tau": spec.tau, "W": spec.W, "nprobe_max": spec.nprobe_max,
-                   "fixed_nprobe": spec.fixed_nprobe, "parallelism": "single GPU"},
-        "speedup_vs_fixed": None if args.skip_fixed else round(t_fixed / t_sieve, 3),
-        "fixed_qps": None if args.skip_fixed else round(fixed_qps, 1),
-        "partition_vectors_per_s": round(st.vectors_scanned * args.steps / t_sieve, 1),
-        "scan_hbm_gbs": round(gbs, 1),
-        "mean_probes": round(float(probes.float().mean().item()), 3),
-        "scanned_probes_per_query": round(st.items / nq, 3),
-        "rounds": st.rounds,
-        "phase_ms": {k: round(mean(stats, "ms_" + k), 4) for k in
-                     ("rank", "sched", "scan", "update", "finalize", "total")},
-        "fixed_phase_ms": ({k: round(mean(fstats, "ms_" + k), 4) for k in
-                            ("rank", "sched", "scan", "finalize", "total")} if fstats else None),
-        "roofline": roof,
-        "calibrated": cal,
+                   "fixed_nprobe": spec.fixed_nprobe, "lookahead": "Algorithm 2 (committed)",
+                   "parallelism": "single GPU"},
+        "speedup_vs_fixed": hr["speedup_vs_fixed"],
+        "fixed_qps": hr["fixed_qps"],
+        "partition_vectors_per_s": hr["partition_vectors_per_s"],
+        "scan_hbm_gbs": hr["scan_hbm_gbs"],
+        "mean_probes": hr["mean_probes"],
+        "scanned_probes_per_query": hr["scanned_probes_per_query"],
+        "rounds": hr["rounds"],
+        "phase_ms": hr["phase_ms"],
+        "fixed_phase_ms": hr["fixed_phase_ms"],
+        "roofline": hr["roofline"],
+        "speculative": hr["speculative"],
+        "calibrated": hr.get("calibrated"),
+        "e1": hr["e1"],
+        "lists": hr["lists"],
+        "paper_context": "4.1-7.6x over fixed probing on 10M workloads and 6.1-8.4x on 100M "
+                         "workloads at W=8, 32-core EPYC 7K62 CPU, RaBitQ-coded Lance "
+                         "indexes (context only)",
+        "configs": {n: results[n] for n in names if n != head},
     }
-
-    if not args.no_oracle:
-        import oracle
-        sys.path.insert(0, os.path.join(ROOT, "tests"))
-        from parity import compare
-        h = w.numpy()
-        m = min(args.oracle_queries or ORACLE_SAMPLE.get(args.config, 1000), nq)
-        rng = np.random.default_rng(spec.seed + 77)
-        sel = np.sort(rng.choice(nq, m, replace=False))
-        log(f"[bench] oracle on {m} queries, 1 thread")
-        t0 = time.perf_counter()
-        o = oracle.search(h["vectors"], h["list_offsets"], h["ids"], h["centroids"],
-                          h["queries"][sel], h["exclude_ids"][sel], spec.k, spec.tau, spec.W,
-                          spec.nprobe_max, oracle.MODE_A, 1)
-        t_or = time.perf_counter() - t0
-        rep = compare(ids.cpu().numpy()[sel], scores.cpu().numpy()[sel],
-                      probes.cpu().numpy()[sel], o)
-        out["cpu_baseline"] = {"value": round(m / t_or, 2), "unit": "queries/s", "cores": 1,
-                               "kind": "oracle",
-                               "sample": f"{m} seeded queries of the same workload, "
-                                         f"single thread, {t_or:.1f}s",
-                               "cpu": _cpu_model()}
-        out["parity_sample"] = {k: rep[k] for k in ("queries", "mismatch", "flag_tau_edge",
-                                                    "flag_kth_tie", "flagged_mismatch",
-                                                    "max_score_err")}
-    ix.close()
+    if "cpu_baseline" in hr:
+        out["cpu_baseline"] = hr["cpu_baseline"]
+        out["parity_sample"] = hr["parity_sample"]
     print(json.dumps(out), flush=True)
 
 
@@ -414,7 +532,8 @@ def envelope(args, ps, sw, np, torch, dev):
 
 def concurrency(args, ps, sw, np, torch, dev):
     """Queries per call (Sec. 6.4's request-size sweep) on the 1M x 128 fp32 data, W = 8:
-    lookahead, basic (Algorithm 1) and serial dispatch.  Each point issues consecutive calls
+    Algorithm 2 lookahead with and without speculative issue, basic (Algorithm 1) and serial
+    dispatch.  Each point issues consecutive calls
     over a prefix of the 10,000-query batch (at most 200 calls) and reports queries/s."""
     spec = sw.SPECS["c2"]
     log("[concurrency] generating c2")
@@ -424,8 +543,10 @@ def concurrency(args, ps, sw, np, torch, dev):
     for per in (1, 10, 100, 1000, 10000):
         calls = min(200, spec.nq // per)
         row = {"queries_per_call": per, "calls": calls}
-        for name, kw in (("lookahead", dict(lookahead=True)), ("basic", dict(lookahead=False)),
-                         ("serial", dict(serial=True)), ("fixed", None)):
+        for name, kw in (("lookahead", dict(lookahead=True)),
+                         ("speculative", dict(lookahead=True, speculative=True)),
+                         ("basic", dict(lookahead=False)), ("serial", dict(serial=True)),
+                         ("fixed", None)):
             def run():
                 for c in range(calls):
                     q0 = c * per
@@ -438,6 +559,7 @@ def concurrency(args, ps, sw, np, torch, dev):
             _, sec = _timed(torch, run, 1)
             row[name + "_qps"] = round(calls * per / sec, 1)
         row["lookahead_vs_fixed"] = round(row["lookahead_qps"] / row["fixed_qps"], 3)
+        row["speculative_vs_fixed"] = round(row["speculative_qps"] / row["fixed_qps"], 3)
         row["basic_vs_fixed"] = round(row["basic_qps"] / row["fixed_qps"], 3)
         row["serial_vs_fixed"] = round(row["serial_qps"] / row["fixed_qps"], 3)
         rows.append(row)

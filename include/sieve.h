@@ -68,6 +68,26 @@ typedef enum sieve_dtype {
 /* Largest k accepted (the paper's k sweep reaches 50, Sec. 6.4). */
 #define SIEVE_K_MAX 64
 
+/* Values of the lookahead argument of sieve_search and sieve_search_multi.
+ * They change only how the (query, partition) searches are grouped into
+ * rounds; the outputs are identical for all four (Sec. 4.3).
+ *   OFF          Algorithm 1: one rank per query per round (next / stale).
+ *   COMMITTED    Algorithm 2: every rank up to the stop line is issued as soon
+ *                as it is committed, and no rank past it is ever searched.
+ *   SERIAL       the serial-traversal ablation of Sec. 6.3: Algorithm 1's
+ *                rounds, and no partition scan is shared by two queries.
+ *   SPECULATIVE  Algorithm 2 plus speculative issue, an addition of this
+ *                library: when a stop line moves far, ranks past it are issued
+ *                too (at most 3 W); the stop rule is then replayed over the
+ *                recorded per-rank outcomes, and what ranks past the final line
+ *                found is discarded.  It can search more (query, partition)
+ *                pairs than Algorithm 2 (stats.items) and take fewer rounds.
+ *                Batches of more than 2^20 queries issue committed ranks only. */
+#define SIEVE_LOOKAHEAD_OFF 0
+#define SIEVE_LOOKAHEAD_COMMITTED 1
+#define SIEVE_LOOKAHEAD_SERIAL 2
+#define SIEVE_LOOKAHEAD_SPECULATIVE 3
+
 typedef struct sieve_index sieve_index; /* opaque, owned by the library */
 
 /* Counters of one search call (filled when a non-NULL pointer is passed). */
@@ -76,9 +96,9 @@ typedef struct sieve_stats {
   int32_t nprobe_eff;       /* min(nprobe_max, nlist)                                      */
   int32_t scan_launches;    /* partition-scan kernel launches                              */
   int32_t pool_retries;     /* re-runs after the candidate pool overflowed (results equal) */
-  int64_t items;            /* (query, rank) searches executed; with lookahead this may
-                               exceed probes_total: ranks past a stop line can be
-                               searched early, and what they find is discarded            */
+  int64_t items;            /* (query, rank) searches executed; with speculative issue
+                               this may exceed probes_total: ranks past a stop line can
+                               be searched early, and what they find is discarded        */
   int64_t probes_total;     /* sum over queries of out_probes                              */
   int64_t vectors_scanned;  /* sum over items of the probed list's length                  */
   int64_t list_loads;       /* sum over rounds of distinct non-empty lists probed          */
@@ -117,7 +137,7 @@ SIEVE_API int sieve_load_index(const void* vectors, int32_t dtype, int64_t n, in
 /*
  * sieve_search -- threshold-aware search with the consecutive-empty stop rule
  * (Sec. 4.1), partition-major continuous batching (Sec. 4.2, Algorithm 1) and,
- * when lookahead = 1, committed-prefix lookahead (Sec. 4.3, Algorithm 2).
+ * with lookahead, committed-prefix lookahead (Sec. 4.3, Algorithm 2).
  *   queries      [nq * d] of the index dtype; nq >= 0 (0 returns at once).
  *   exclude_ids  [nq] int64 or NULL: row id to skip for each query (a
  *                self-join passes each query's own id); the skipped row is
@@ -128,10 +148,8 @@ SIEVE_API int sieve_load_index(const void* vectors, int32_t dtype, int64_t n, in
  *   W            consecutive-empty window, W >= 1 (SIEVE_W_INF: never stop).
  *   nprobe_max   >= 1; clamped to nlist; the clamped value must be <= 2048
  *                (else SIEVE_EUNSUPPORTED).
- *   lookahead    0 (Algorithm 1), 1 (Algorithm 2), or 2 (serial traversal,
- *                the ablation baseline of Sec. 6.3: one rank per query per
- *                round as in Algorithm 1, and no partition scan is shared by
- *                two queries).  Outputs are identical in all three.
+ *   lookahead    one of the SIEVE_LOOKAHEAD_* values above (else
+ *                SIEVE_EINVAL); outputs are identical for all of them.
  *   out_ids      [nq * k] int64, out_scores [nq * k] float: per query the
  *                top-k qualifying candidates, score descending then id
  *                ascending, padded with (-1, -INFINITY).
@@ -167,8 +185,8 @@ SIEVE_API int sieve_search_fixed(const sieve_index* idx, const void* queries, in
  * smallest W whose stop-rule prefix reaches the partition where it was found,
  * and the chosen W is the smallest W < n whose sample-relative loss
  * 1 - (neighbours with required window <= W) / (all neighbours) is < eps,
- * else n (full probing).  Every other query is then searched with lookahead
- * and the chosen W.  A sample without any neighbour (or ns = 0) uses
+ * else n (full probing).  Every other query is then searched with Algorithm 2
+ * lookahead (SIEVE_LOOKAHEAD_COMMITTED) and the chosen W.  A sample without any neighbour (or ns = 0) uses
  * W_fallback.
  *   sample       [ns] int32 distinct query indices in [0, nq) (device); the
  *                caller draws them (uniformly without replacement in the
@@ -219,6 +237,30 @@ SIEVE_API int sieve_search_multi(const sieve_index* const* idxs, int32_t nidx,
  */
 SIEVE_API int sieve_rank(const sieve_index* idx, const void* queries, int64_t nq, int32_t nprobe,
                          int32_t* out_order, void* stream);
+
+/*
+ * sieve_round_log -- per-round record of the last search call on this handle
+ * that was given a stats pointer (for fixed probing, one record per query
+ * chunk).  Diagnostics for the roofline of the partition scan: each record
+ * holds the round's algorithmic scan work and the scan launch's device time.
+ *   out          HOST array of max records (may be NULL when max = 0).
+ *   n_rounds     HOST pointer: receives the number of rounds of that search
+ *                (records past max, or past the 256 kept, are not written).
+ * Returns SIEVE_EINVAL for a NULL handle or n_rounds, or max < 0.
+ */
+typedef struct sieve_round {
+  int64_t items;       /* (query, rank) searches dispatched in the round                */
+  int64_t list_rows;   /* rows of the distinct non-empty lists touched (read once each) */
+  int64_t item_rows;   /* sum over the items of their list's rows (rows scored)         */
+  int64_t list_loads;  /* distinct non-empty lists touched                              */
+  int64_t candidates;  /* candidate records the scan wrote                              */
+  double scan_bytes;   /* list rows + per-item query rows and records + candidates, B   */
+  double scan_flops;   /* 2 * d * item_rows                                             */
+  float ms_scan;       /* device time of the round's scan launch (HIP events)           */
+  int32_t kind;        /* 0: threshold-search round, 1: fixed-probe chunk               */
+} sieve_round;
+SIEVE_API int sieve_round_log(const sieve_index* idx, sieve_round* out, int32_t max,
+                              int32_t* n_rounds);
 
 /* Release an index and its cached workspace.  NULL is a no-op. */
 SIEVE_API void sieve_free_index(sieve_index* idx);

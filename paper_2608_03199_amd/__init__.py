@@ -15,13 +15,16 @@ from typing import Optional
 
 import torch
 
-__all__ = ["SieveError", "Index", "Stats", "load_library", "LIB_PATH", "W_INF", "K_MAX",
-           "F32", "F16", "search_multi"]
+__all__ = ["SieveError", "Index", "Stats", "Round", "load_library", "LIB_PATH", "W_INF",
+           "K_MAX", "F32", "F16", "search_multi", "LOOKAHEAD_OFF", "LOOKAHEAD_COMMITTED",
+           "LOOKAHEAD_SERIAL", "LOOKAHEAD_SPECULATIVE"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsieve.so")
 W_INF = 0x7FFFFFFF
 K_MAX = 64
 F32, F16 = 0, 1
+# values of the lookahead argument (SIEVE_LOOKAHEAD_* in include/sieve.h)
+LOOKAHEAD_OFF, LOOKAHEAD_COMMITTED, LOOKAHEAD_SERIAL, LOOKAHEAD_SPECULATIVE = 0, 1, 2, 3
 _STATUS = {0: "SIEVE_OK", -1: "SIEVE_EINVAL", -2: "SIEVE_ENOMEM", -3: "SIEVE_EDEVICE",
            -4: "SIEVE_EUNSUPPORTED", -5: "SIEVE_EINTERNAL"}
 
@@ -46,6 +49,26 @@ class Stats(ctypes.Structure):
 
     def as_dict(self) -> dict:
         return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+class Round(ctypes.Structure):
+    """Mirror of ``sieve_round`` (one record of ``sieve_round_log``)."""
+    _fields_ = [("items", ctypes.c_int64), ("list_rows", ctypes.c_int64),
+                ("item_rows", ctypes.c_int64), ("list_loads", ctypes.c_int64),
+                ("candidates", ctypes.c_int64), ("scan_bytes", ctypes.c_double),
+                ("scan_flops", ctypes.c_double), ("ms_scan", ctypes.c_float),
+                ("kind", ctypes.c_int32)]
+
+    def as_dict(self) -> dict:
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+def _lookahead_code(lookahead: bool, speculative: bool, serial: bool) -> int:
+    if serial:
+        return LOOKAHEAD_SERIAL
+    if not lookahead:
+        return LOOKAHEAD_OFF
+    return LOOKAHEAD_SPECULATIVE if speculative else LOOKAHEAD_COMMITTED
 
 
 _lib = None
@@ -78,6 +101,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sieve_search_multi.restype = ctypes.c_int
     lib.sieve_search_multi.argtypes = [P, i32, P, i64, P, i32, ctypes.c_float, i32, i32, i32, P,
                                        P, P, ctypes.POINTER(Stats), P]
+    lib.sieve_round_log.restype = ctypes.c_int
+    lib.sieve_round_log.argtypes = [P, ctypes.POINTER(Round), i32, ctypes.POINTER(ctypes.c_int32)]
     lib.sieve_rank.restype = ctypes.c_int
     lib.sieve_rank.argtypes = [P, P, i64, i32, P, P]
     lib.sieve_free_index.restype = None
@@ -179,18 +204,30 @@ class Index:
                                                    out.data_ptr(), _stream(stream)))
         return out[:, :n]
 
+    def round_log(self) -> list:
+        """Per-round records (``Round``) of the last search on this index that collected
+        statistics (``sieve_round_log``)."""
+        n = ctypes.c_int32(0)
+        _check(self._lib, self._lib.sieve_round_log(self._h, None, 0, ctypes.byref(n)))
+        buf = (Round * max(n.value, 1))()
+        _check(self._lib, self._lib.sieve_round_log(self._h, buf, n.value, ctypes.byref(n)))
+        return [buf[i] for i in range(min(n.value, len(buf)))]
+
     def search(self, queries: torch.Tensor, exclude_ids: Optional[torch.Tensor], k: int,
                tau: float, W: int, nprobe_max: int, lookahead: bool = True,
-               with_stats: bool = False, stream=None, serial: bool = False):
-        """Threshold-aware search; returns (ids, scores, probes[, Stats]).  serial: the
-        serial-traversal ablation (no shared partition scans; lookahead is ignored)."""
+               with_stats: bool = False, stream=None, serial: bool = False,
+               speculative: bool = False):
+        """Threshold-aware search; returns (ids, scores, probes[, Stats]).  lookahead:
+        Algorithm 2 (else Algorithm 1); speculative: Algorithm 2 with speculative issue past
+        the stop line; serial: the serial-traversal ablation (no shared partition scans;
+        lookahead is ignored).  The outputs are the same in every mode."""
         queries, ex, nq, oi, osc, op = self._prep(queries, exclude_ids, k)
         st = Stats() if with_stats else None
         with torch.cuda.device(self.device):
             _check(self._lib, self._lib.sieve_search(
                 self._h, queries.data_ptr(), nq, None if ex is None else ex.data_ptr(), int(k),
-                float(tau), int(W), int(nprobe_max), 2 if serial else (1 if lookahead else 0),
-                oi.data_ptr(),
+                float(tau), int(W), int(nprobe_max),
+                _lookahead_code(lookahead, speculative, serial), oi.data_ptr(),
                 osc.data_ptr(), op.data_ptr(), ctypes.byref(st) if st is not None else None,
                 _stream(stream)))
         return (oi, osc, op, st) if with_stats else (oi, osc, op)
@@ -233,7 +270,8 @@ class Index:
 
 def search_multi(indexes, queries: torch.Tensor, exclude_ids: Optional[torch.Tensor], k: int,
                  tau: float, W: int, nprobe_max: int, lookahead: bool = True,
-                 serial: bool = False, with_stats: bool = False, stream=None):
+                 serial: bool = False, with_stats: bool = False, stream=None,
+                 speculative: bool = False):
     """Threshold search over several independently built indexes of one corpus, each with its
     own stop rule, merged into one top-k (``sieve_search_multi``).  Returns
     (ids, scores, probes[, Stats]); probes are summed over the indexes."""
@@ -248,6 +286,6 @@ def search_multi(indexes, queries: torch.Tensor, exclude_ids: Optional[torch.Ten
         _check(first._lib, first._lib.sieve_search_multi(
             handles, len(indexes), queries.data_ptr(), nq, None if ex is None else ex.data_ptr(),
             int(k), float(tau), int(W), int(nprobe_max),
-            2 if serial else (1 if lookahead else 0), oi.data_ptr(), osc.data_ptr(),
+            _lookahead_code(lookahead, speculative, serial), oi.data_ptr(), osc.data_ptr(),
             op.data_ptr(), ctypes.byref(st) if st is not None else None, _stream(stream)))
     return (oi, osc, op, st) if with_stats else (oi, osc, op)

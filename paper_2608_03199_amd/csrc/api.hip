@@ -97,7 +97,7 @@ struct sieve_index {
   X(state_a) X(state_b) X(lmax) X(hcount) X(hoff) X(hcur) X(scan_tmp) X(pool)              \
   X(pool_sorted) X(arenas) X(have) X(ext) X(qext) X(Pext) X(cand) X(ccount) X(cal_idx)      \
   X(cal_q) X(cal_x) X(cal_bits) X(cal_rank) X(cal_hist) X(mix_ids) X(mix_scores)            \
-  X(mix_probes) X(spec_bits)
+  X(mix_probes) X(spec_bits) X(rlog)
 #define SIEVE_DECLARE_BUF(name) Buf name;
   SIEVE_WORKSPACE(SIEVE_DECLARE_BUF)
 #undef SIEVE_DECLARE_BUF
@@ -110,6 +110,12 @@ struct sieve_index {
   std::vector<hipEvent_t> ev_pool;
   size_t ev_used = 0;
   std::vector<int> span_phase, span_a, span_b;
+  // per-round log of the last timed search: items and the scan span of each
+  // round as it runs, the finished records after the final synchronisation
+  std::vector<int64_t> round_items;
+  std::vector<int> round_span;
+  std::vector<sieve_round> rounds_log;
+  int32_t rounds_logged = 0;  // rounds of that search (records past kMaxLogRounds are dropped)
 };
 
 namespace {
@@ -154,6 +160,8 @@ void reset_timeline(sieve_index* ix) {
   ix->span_phase.clear();
   ix->span_a.clear();
   ix->span_b.clear();
+  ix->round_items.clear();
+  ix->round_span.clear();
 }
 
 // After the stream has drained: milliseconds per phase, and scan span count.
@@ -187,13 +195,6 @@ int env_count(const char* name, int dflt) {
   if (!v || !*v) return dflt;
   const int x = atoi(v);
   return x >= 0 ? x : dflt;
-}
-
-// An on/off switch: "0" turns it off, any other value on.
-bool env_flag(const char* name, bool dflt) {
-  const char* v = getenv(name);
-  if (!v || !*v) return dflt;
-  return atoi(v) != 0;
 }
 
 int row_chunk_for(const sieve_index* ix, const char* knob, int dflt) {
@@ -286,6 +287,7 @@ int grow_workspace(sieve_index* ix, const SearchPlan& pl) {
   if ((st = ensure(ix->scan_tmp, exclusive_scan_tmp_elems(nq) * 4))) return st;
   if (pl.spec && (st = ensure(ix->spec_bits, (size_t)nq * pl.hit_words * 4))) return st;
   if ((st = ensure(ix->arenas, (size_t)pl.scan_grid * sizeof(ArenaRec)))) return st;
+  if ((st = ensure(ix->rlog, (size_t)kMaxLogRounds * sizeof(RoundSnap)))) return st;
   // arena runs can leave up to kArenaMax unused slots per scan work-group
   const int64_t slack = (int64_t)pl.scan_grid * kArenaMax;
   if (ix->pool_cap < slack + (1 << 20)) {
@@ -402,6 +404,51 @@ int run_round(sieve_index* ix, const ScanArgs& sa, int n_items, int64_t q0, cons
   span(ix, kSched, e0, e1);
   span(ix, kScan, e1, e2);
   *at = e2;
+  if (timed) {
+    // the round's counters, for the per-round log (sieve_round_log)
+    const int slot = (int)ix->round_items.size();
+    ix->round_items.push_back(n_items);
+    ix->round_span.push_back(e1 >= 0 && e2 >= 0 ? (int)ix->span_phase.size() - 1 : -1);
+    if (slot < kMaxLogRounds)
+      HIP_TRY(launch_snapshot_round(rc, (RoundSnap*)ix->rlog.p + slot, 0, s));
+  }
+  return SIEVE_OK;
+}
+
+// Turn the per-round counter snapshots of a timed search into its round log
+// (differences of consecutive snapshots, scan time from the round's span).
+int finish_round_log(sieve_index* ix, int32_t kind, hipStream_t s) {
+  const int n = (int)std::min<size_t>(ix->round_items.size(), kMaxLogRounds);
+  std::vector<RoundSnap> snap((size_t)n);
+  if (n > 0) {
+    HIP_TRY(hipMemcpyAsync(snap.data(), ix->rlog.p, (size_t)n * sizeof(RoundSnap),
+                           hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+  }
+  const double eb = (double)ix->d * elem_bytes(ix->dtype);
+  ix->rounds_log.assign((size_t)n, sieve_round{});
+  ix->rounds_logged = (int32_t)ix->round_items.size();
+  RoundSnap prev = {0, 0, 0, 0};
+  for (int r = 0; r < n; ++r) {
+    sieve_round& o = ix->rounds_log[(size_t)r];
+    o.items = ix->round_items[(size_t)r];
+    o.list_rows = (int64_t)(snap[r].list_rows - prev.list_rows);
+    o.item_rows = (int64_t)(snap[r].item_rows - prev.item_rows);
+    o.list_loads = (int64_t)(snap[r].list_loads - prev.list_loads);
+    o.candidates = (int64_t)(snap[r].cands - prev.cands);
+    o.scan_bytes = (double)o.list_rows * eb + (double)o.items * (eb + sizeof(Item)) +
+                   (double)o.candidates * sizeof(Hit);
+    o.scan_flops = 2.0 * (double)ix->d * (double)o.item_rows;
+    o.kind = kind;
+    o.ms_scan = 0.f;
+    const int sp = ix->round_span[(size_t)r];
+    if (sp >= 0 && hipEventElapsedTime(&o.ms_scan, ix->ev_pool[ix->span_a[sp]],
+                                       ix->ev_pool[ix->span_b[sp]]) != hipSuccess) {
+      (void)hipGetLastError();
+      o.ms_scan = 0.f;
+    }
+    prev = snap[r];
+  }
   return SIEVE_OK;
 }
 
@@ -612,6 +659,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
       float ms[kPhases];
       int scan_launches = 0;
       read_timeline(ix, ms, &scan_launches);
+      if ((st = finish_round_log(ix, pl.mode == 2 ? 1 : 0, s))) return st;
       const RoundCounters& h = *ix->rc_host;
       unsigned long long probes_sum = 0, cand_sum = 0;
       for (int x = 0; x < kStatSlots; ++x) {
@@ -643,8 +691,11 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
   }
 }
 
+// mode: 0 lookahead (Algorithm 2), 1 basic (Algorithm 1), 2 fixed probing.
+// speculative: with mode 0, also issue ranks past the stop line (see
+// launch_update_lookahead); outputs are the same either way.
 int plan_search(const sieve_index* ix, int64_t nq, int32_t k, float tau, int32_t W,
-                int32_t nprobe, int mode, SearchPlan* pl) {
+                int32_t nprobe, int mode, bool speculative, SearchPlan* pl) {
   pl->n = nprobe < ix->nlist ? nprobe : ix->nlist;
   if (pl->n > kMaxRanks)
     return fail(SIEVE_EUNSUPPORTED, "min(nprobe, nlist) = %d exceeds %d", pl->n, kMaxRanks);
@@ -669,8 +720,7 @@ int plan_search(const sieve_index* ix, int64_t nq, int32_t k, float tau, int32_t
   pl->dense_q = env_int("SIEVE_DENSE_Q", 64);
   // Speculative issue needs the rank packed beside the query in pool entries
   // (queries < 2^kRankShift) and a stop rule that can stop early (W < n).
-  pl->spec = mode == 0 && W < pl->n && nq <= (int64_t)kQueryMask + 1 &&
-             env_flag("SIEVE_SPECULATE", true);
+  pl->spec = speculative && mode == 0 && W < pl->n && nq <= (int64_t)kQueryMask + 1;
   pl->spec_max =
       pl->spec ? (int)std::min<int64_t>(pl->n, (int64_t)env_int("SIEVE_SPEC_DEPTH", 3) * W) : 0;
   // Lines that move far keep moving (queries in large near-duplicate groups):
@@ -711,6 +761,13 @@ int plan_search(const sieve_index* ix, int64_t nq, int32_t k, float tau, int32_t
   }
   if (pl->item_cap < 1) pl->item_cap = 1;
   return SIEVE_OK;
+}
+
+// Round structure of a lookahead argument: 0 for Algorithm 2 (with or
+// without speculative issue), 1 for Algorithm 1's one rank per round.
+int lookahead_mode(int32_t lookahead) {
+  return lookahead == SIEVE_LOOKAHEAD_COMMITTED || lookahead == SIEVE_LOOKAHEAD_SPECULATIVE ? 0
+                                                                                            : 1;
 }
 
 void add_stats(sieve_stats* acc, const sieve_stats& x) {
@@ -848,11 +905,14 @@ SIEVE_API int sieve_search(const sieve_index* idx, const void* queries, int64_t 
   if (st) return st;
   if (W < 1) return fail(SIEVE_EINVAL, "W = %d must be >= 1", W);
   if (nprobe_max < 1) return fail(SIEVE_EINVAL, "nprobe_max = %d must be >= 1", nprobe_max);
-  if (lookahead < 0 || lookahead > 2) return fail(SIEVE_EINVAL, "lookahead must be 0, 1 or 2");
+  if (lookahead < SIEVE_LOOKAHEAD_OFF || lookahead > SIEVE_LOOKAHEAD_SPECULATIVE)
+    return fail(SIEVE_EINVAL, "lookahead = %d must be 0, 1, 2 or 3", lookahead);
   sieve_index* ix = const_cast<sieve_index*>(idx);
   SearchPlan pl;
-  if ((st = plan_search(ix, nq, k, tau, W, nprobe_max, lookahead == 1 ? 0 : 1, &pl))) return st;
-  if (lookahead == 2) pl.group_q = 1;  // serial: no query shares a partition scan
+  if ((st = plan_search(ix, nq, k, tau, W, nprobe_max, lookahead_mode(lookahead),
+                        lookahead == SIEVE_LOOKAHEAD_SPECULATIVE, &pl)))
+    return st;
+  if (lookahead == SIEVE_LOOKAHEAD_SERIAL) pl.group_q = 1;  // no query shares a partition scan
   if (stats) memset(stats, 0, sizeof(*stats));
   if (nq == 0) {
     if (stats) stats->nprobe_eff = pl.n;
@@ -860,6 +920,17 @@ SIEVE_API int sieve_search(const sieve_index* idx, const void* queries, int64_t 
   }
   return search_impl(ix, queries, nq, exclude_ids, pl, nullptr, out_ids, out_scores, out_probes,
                      stats, (hipStream_t)stream);
+}
+
+SIEVE_API int sieve_round_log(const sieve_index* idx, sieve_round* out, int32_t max,
+                              int32_t* n_rounds) {
+  g_err.clear();
+  if (!idx || !n_rounds) return fail(SIEVE_EINVAL, "idx and n_rounds must be non-NULL");
+  if (max < 0 || (max > 0 && !out)) return fail(SIEVE_EINVAL, "bad output array");
+  const int n = (int)idx->rounds_log.size();
+  for (int r = 0; r < n && r < max; ++r) out[r] = idx->rounds_log[(size_t)r];
+  *n_rounds = idx->rounds_logged;
+  return SIEVE_OK;
 }
 
 SIEVE_API int sieve_rank(const sieve_index* idx, const void* queries, int64_t nq, int32_t nprobe,
@@ -875,7 +946,7 @@ SIEVE_API int sieve_rank(const sieve_index* idx, const void* queries, int64_t nq
   sieve_index* ix = const_cast<sieve_index*>(idx);
   SearchPlan pl;
   int st;
-  if ((st = plan_search(ix, nq, 1, 0.f, 1, nprobe, 1, &pl))) return st;
+  if ((st = plan_search(ix, nq, 1, 0.f, 1, nprobe, 1, false, &pl))) return st;
   if (nq == 0) return SIEVE_OK;
   if ((int64_t)nq * pl.n > (int64_t)INT32_MAX * 8)
     return fail(SIEVE_EUNSUPPORTED, "nq * nprobe too large");
@@ -910,7 +981,7 @@ SIEVE_API int sieve_search_fixed(const sieve_index* idx, const void* queries, in
   if (nprobe < 1) return fail(SIEVE_EINVAL, "nprobe = %d must be >= 1", nprobe);
   sieve_index* ix = const_cast<sieve_index*>(idx);
   SearchPlan pl;
-  if ((st = plan_search(ix, nq, k, tau, SIEVE_W_INF, nprobe, 2, &pl))) return st;
+  if ((st = plan_search(ix, nq, k, tau, SIEVE_W_INF, nprobe, 2, false, &pl))) return st;
   if (stats) memset(stats, 0, sizeof(*stats));
   if (nq == 0) {
     if (stats) stats->nprobe_eff = pl.n;
@@ -939,7 +1010,7 @@ SIEVE_API int sieve_search_calibrated(const sieve_index* idx, const void* querie
   if (ns > 0 && !sample) return fail(SIEVE_EINVAL, "sample is NULL with ns > 0");
   sieve_index* ix = const_cast<sieve_index*>(idx);
   SearchPlan pf;
-  if ((st = plan_search(ix, ns, k, tau, SIEVE_W_INF, nprobe_max, 2, &pf))) return st;
+  if ((st = plan_search(ix, ns, k, tau, SIEVE_W_INF, nprobe_max, 2, false, &pf))) return st;
   if (stats) {
     memset(stats, 0, sizeof(*stats));
     stats->nprobe_eff = pf.n;
@@ -1019,7 +1090,7 @@ SIEVE_API int sieve_search_calibrated(const sieve_index* idx, const void* querie
   // 3. Lookahead search of every other query with the chosen window.
   if (nr > 0) {
     SearchPlan pr;
-    if ((st = plan_search(ix, nr, k, tau, W, nprobe_max, 0, &pr))) return st;
+    if ((st = plan_search(ix, nr, k, tau, W, nprobe_max, 0, false, &pr))) return st;
     if (ns == 0) {
       st = search_impl(ix, queries, nq, exclude_ids, pr, nullptr, out_ids, out_scores, out_probes,
                        stats ? &part : nullptr, s);
@@ -1053,13 +1124,15 @@ SIEVE_API int sieve_search_multi(const sieve_index* const* idxs, int32_t nidx,
   if (st) return st;
   if (W < 1) return fail(SIEVE_EINVAL, "W = %d must be >= 1", W);
   if (nprobe_max < 1) return fail(SIEVE_EINVAL, "nprobe_max = %d must be >= 1", nprobe_max);
-  if (lookahead < 0 || lookahead > 2) return fail(SIEVE_EINVAL, "lookahead must be 0, 1 or 2");
+  if (lookahead < SIEVE_LOOKAHEAD_OFF || lookahead > SIEVE_LOOKAHEAD_SPECULATIVE)
+    return fail(SIEVE_EINVAL, "lookahead = %d must be 0, 1, 2 or 3", lookahead);
   std::vector<SearchPlan> plans((size_t)nidx);
   for (int32_t i = 0; i < nidx; ++i) {
     sieve_index* ix = const_cast<sieve_index*>(idxs[i]);
-    if ((st = plan_search(ix, nq, k, tau, W, nprobe_max, lookahead == 1 ? 0 : 1, &plans[i])))
+    if ((st = plan_search(ix, nq, k, tau, W, nprobe_max, lookahead_mode(lookahead),
+                          lookahead == SIEVE_LOOKAHEAD_SPECULATIVE, &plans[i])))
       return st;
-    if (lookahead == 2) plans[i].group_q = 1;
+    if (lookahead == SIEVE_LOOKAHEAD_SERIAL) plans[i].group_q = 1;
   }
   if (stats) memset(stats, 0, sizeof(*stats));
   if (nq == 0) return SIEVE_OK;

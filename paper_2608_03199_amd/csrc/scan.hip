@@ -300,6 +300,12 @@ __global__ __launch_bounds__(kNT, kNT == kScanThreads ? 2 : 1) void scan_kernel(
           });
     if constexpr (kAsync) __builtin_amdgcn_s_waitcnt(0);  // this wave's staging copies landed
     __syncthreads();  // every wave is done with this tile's buffer and items
+    {
+      // candidates of the tile, for the round statistics: one add per wave
+      unsigned long long c = (int)threadIdx.x < nq ? (unsigned long long)s_hits[threadIdx.x] : 0;
+      for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o);
+      if (lane == 0 && c) atomicAdd(&a.rc->cands, c);
+    }
     if ((int)threadIdx.x < nq && s_hits[threadIdx.x] > 0) {
       // this tile's candidates of one query: one count update, one hit flag
       const int q = sq[threadIdx.x];

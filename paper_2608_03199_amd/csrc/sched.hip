@@ -452,6 +452,17 @@ __global__ void emit_pending_kernel(const int32_t* __restrict__ ext, int32_t n_e
   have[q] = new_have > hv ? new_have : hv;
 }
 
+__global__ void snapshot_round_kernel(const RoundCounters* __restrict__ rc,
+                                      RoundSnap* __restrict__ log, int32_t slot) {
+  if (threadIdx.x != 0) return;
+  RoundSnap r;
+  r.list_rows = rc->list_rows;
+  r.item_rows = rc->item_rows;
+  r.list_loads = rc->list_loads;
+  r.cands = rc->cands;
+  log[slot] = r;
+}
+
 __global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x)
@@ -570,6 +581,13 @@ hipError_t launch_emit_pending(const int32_t* ext, int32_t n_ext, int32_t mode, 
   if (n_ext <= 0) return hipSuccess;
   hipLaunchKernelGGL(emit_pending_kernel, dim3(blocks_for(n_ext)), dim3(kThreads), 0, s, ext,
                      n_ext, mode, P, n, state_a, have, new_have, items, cnt, rc, issued);
+  return hipGetLastError();
+}
+
+hipError_t launch_snapshot_round(const RoundCounters* rc, RoundSnap* log, int32_t slot,
+                                 hipStream_t s) {
+  if (slot < 0 || slot >= kMaxLogRounds) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(snapshot_round_kernel, dim3(1), dim3(64), 0, s, rc, log, slot);
   return hipGetLastError();
 }
 

@@ -62,6 +62,7 @@ struct RoundCounters {
   unsigned long long item_rows;   // sum over items of their list's length (this round)
   unsigned long long list_loads;  // active non-empty lists (this round)
   unsigned long long hits;        // pool slots claimed (whole search; includes arena tails)
+  unsigned long long cands;       // candidates the scans wrote (whole search)
   // Sums of out_probes and of the qualifying candidates merged by the final
   // top-k, spread over kStatSlots counters (work-group b adds to slot
   // b % kStatSlots): thousands of adds to one address would serialise.
@@ -77,6 +78,13 @@ struct RoundSummary {
   int32_t rank_error;
   int32_t pad;
   unsigned long long hits;
+};
+
+// Cumulative scan counters after one round (the per-round log of a timed
+// search takes differences of consecutive snapshots).
+constexpr int kMaxLogRounds = 256;
+struct RoundSnap {
+  unsigned long long list_rows, item_rows, list_loads, cands;
 };
 
 // Candidate-pool arenas: a scan work-group claims pool slots in runs (first
@@ -196,6 +204,8 @@ hipError_t launch_emit_pending(const int32_t* ext, int32_t n_ext, int32_t mode, 
                                int32_t new_have, Item* items, int32_t* cnt, RoundCounters* rc,
                                int32_t* issued, hipStream_t s);
 
+hipError_t launch_snapshot_round(const RoundCounters* rc, RoundSnap* log, int32_t slot,
+                                 hipStream_t s);
 hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
 // Several 32-bit fills in one launch (segments with n = 0 are skipped).
 constexpr int kFillSegs = 6;

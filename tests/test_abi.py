@@ -29,7 +29,7 @@ def declared_symbols():
 def test_header_declares_the_boundary():
     syms = declared_symbols()
     for s in ("sieve_load_index", "sieve_search", "sieve_search_fixed", "sieve_search_calibrated",
-              "sieve_search_multi", "sieve_free_index", "sieve_last_error"):
+              "sieve_search_multi", "sieve_round_log", "sieve_free_index", "sieve_last_error"):
         assert s in syms
 
 
@@ -61,6 +61,22 @@ def test_stats_struct_layout_matches_c(tmp_path):
     assert vals[1:] == [getattr(ps.Stats, f).offset for f in fields]
 
 
+def test_round_struct_layout_matches_c(tmp_path):
+    import paper_2608_03199_amd as ps
+    fields = [f for f, _ in ps.Round._fields_]
+    src = tmp_path / "round.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "sieve.h"\nint main(void){'
+                   'printf("%zu", sizeof(sieve_round));' +
+                   "".join(f'printf(" %zu", offsetof(sieve_round, {f}));' for f in fields) +
+                   "return 0;}\n")
+    exe = tmp_path / "round"
+    subprocess.run(["gcc", "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)], check=True)
+    vals = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True,
+                                           check=True).stdout.split()]
+    assert vals[0] == ctypes.sizeof(ps.Round)
+    assert vals[1:] == [getattr(ps.Round, f).offset for f in fields]
+
+
 def test_argument_errors_without_a_gpu(lib):
     # no handle: rejected before any HIP call
     rc = lib.sieve_search(None, None, 0, None, 10, 0.9, 8, 32, 1, None, None, None, None, None)
@@ -74,6 +90,9 @@ def test_argument_errors_without_a_gpu(lib):
     rc = lib.sieve_search_multi(None, 0, None, 0, None, 10, 0.9, 8, 32, 1, None, None, None,
                                 None, None)
     assert rc == -1
+    n = ctypes.c_int32(-3)
+    rc = lib.sieve_round_log(None, None, 0, ctypes.byref(n))
+    assert rc == -1 and n.value == -3
     h = ctypes.c_void_p()
     rc = lib.sieve_load_index(None, 0, 10, 64, None, 4, None, None, None, ctypes.byref(h))
     assert rc == -1 and h.value is None

@@ -45,13 +45,14 @@ class Case:
         self.ix = ps.Index(w.vectors, w.list_offsets, w.ids, w.centroids)
 
     def gpu(self, k, tau, W, nprobe, lookahead=True, queries=None, exclude=True, fixed=False,
-            stats=False):
+            stats=False, speculative=False):
         q = self.w.queries if queries is None else queries
         ex = self.w.exclude_ids[: q.shape[0]] if exclude else None
         if fixed:
             r = self.ix.search_fixed(q, ex, k, tau, nprobe, with_stats=stats)
         else:
-            r = self.ix.search(q, ex, k, tau, W, nprobe, lookahead=lookahead, with_stats=stats)
+            r = self.ix.search(q, ex, k, tau, W, nprobe, lookahead=lookahead, with_stats=stats,
+                               speculative=speculative)
         torch.cuda.synchronize()
         out = [r[0].cpu().numpy(), r[1].cpu().numpy(), r[2].cpu().numpy()]
         if stats:
@@ -77,10 +78,11 @@ def case(name, **kw) -> Case:
     return _cases[key]
 
 
-def _check(c: Case, k, tau, W, nprobe, lookahead=True, fixed=False, nq=None, exclude=True):
+def _check(c: Case, k, tau, W, nprobe, lookahead=True, fixed=False, nq=None, exclude=True,
+           speculative=False):
     q = c.w.queries if nq is None else c.w.queries[:nq]
     g_ids, g_sc, g_pr = c.gpu(k, tau, W, nprobe, lookahead, queries=q, exclude=exclude,
-                              fixed=fixed)
+                              fixed=fixed, speculative=speculative)
     o = c.oracle(k, tau, oracle.W_INF if fixed else W, nprobe, nq=q.shape[0], exclude=exclude)
     rep = compare(g_ids, g_sc, g_pr, o)
     print(f"[gpu-test] k={k} tau={tau} W={W} nprobe={nprobe} la={lookahead} fixed={fixed} "
@@ -91,15 +93,9 @@ def _check(c: Case, k, tau, W, nprobe, lookahead=True, fixed=False, nq=None, exc
 
 @pytest.fixture
 def no_speculation():
-    """Lookahead issues only committed ranks (no speculative issue past the stop line), so
-    that it searches exactly the (query, partition) pairs the other dispatches search."""
-    old = os.environ.get("SIEVE_SPECULATE")
-    os.environ["SIEVE_SPECULATE"] = "0"
+    """Lookahead is Algorithm 2 (committed ranks only) unless speculative issue is asked
+    for, so it searches exactly the (query, partition) pairs the other dispatches search."""
     yield
-    if old is None:
-        del os.environ["SIEVE_SPECULATE"]
-    else:
-        os.environ["SIEVE_SPECULATE"] = old
 
 
 @pytest.mark.parametrize("name", ["tiny", "tiny16", "c1"])
@@ -200,18 +196,17 @@ def test_serial_traversal_matches_batched_dispatch(name, W, no_speculation):
 
 
 def _with_speculation(on, fn, first_round=0, spec_min=1):
-    """Run fn with speculative issue on or off, from round first_round on, for stop lines
-    that moved at least spec_min ranks (None: the library's default)."""
-    keys = ("SIEVE_SPECULATE", "SIEVE_SPEC_ROUND", "SIEVE_SPEC_MIN")
+    """Run fn(speculative) with speculative issue on or off, from round first_round on, for
+    stop lines that moved at least spec_min ranks (None: the library's default)."""
+    keys = ("SIEVE_SPEC_ROUND", "SIEVE_SPEC_MIN")
     old = {k: os.environ.get(k) for k in keys}
-    os.environ["SIEVE_SPECULATE"] = "1" if on else "0"
     os.environ["SIEVE_SPEC_ROUND"] = str(first_round)
     if spec_min is None:
         os.environ.pop("SIEVE_SPEC_MIN", None)
     else:
         os.environ["SIEVE_SPEC_MIN"] = str(spec_min)
     try:
-        return fn()
+        return fn(on)
     finally:
         for k, v in old.items():
             if v is None:
@@ -234,7 +229,8 @@ def test_speculative_issue_matches_committed_issue(name, tau, W, first_round, sp
     c = case(name)
     s = c.w.spec
     q, ex = c.w.queries, c.w.exclude_ids
-    run = lambda: c.ix.search(q, ex, s.k, tau, W, s.nprobe_max, with_stats=True)
+    run = lambda sp: c.ix.search(q, ex, s.k, tau, W, s.nprobe_max, with_stats=True,
+                                 speculative=sp)
     a = _with_speculation(True, run, first_round, spec_min)
     b = _with_speculation(False, run)
     for x, y in zip(a[:3], b[:3]):
@@ -258,14 +254,16 @@ def test_speculative_issue_with_rank_extension(short_rank_prefix):
     s = c.w.spec
     q, ex = c.w.queries, c.w.exclude_ids
     for W in (1, 3):
-        run = lambda: c.ix.search(q, ex, s.k, 0.4, W, s.nprobe_max, with_stats=True)
+        run = lambda sp: c.ix.search(q, ex, s.k, 0.4, W, s.nprobe_max, with_stats=True,
+                                     speculative=sp)
         a = _with_speculation(True, run, 0)
         b = _with_speculation(False, run)
         assert int(a[2].max()) > 2 * W
         for x, y in zip(a[:3], b[:3]):
             assert torch.equal(x, y)
         assert a[3].rounds <= b[3].rounds
-        _with_speculation(True, lambda: _check(c, s.k, 0.4, W, s.nprobe_max, lookahead=True))
+        _with_speculation(True, lambda sp: _check(c, s.k, 0.4, W, s.nprobe_max, lookahead=True,
+                                                  speculative=sp))
 
 
 def test_infinite_window_equals_fixed():
@@ -548,3 +546,44 @@ def test_rank_with_many_exact_ties_takes_the_wide_path(rank_path):
     g = ix.search(torch.from_numpy(Q).to(dev), None, 10, 0.5, 3, 16)
     o = oracle.search(X, off, ids, C, Q, None, 10, 0.5, 3, 16)
     assert_parity(compare(g[0].cpu().numpy(), g[1].cpu().numpy(), g[2].cpu().numpy(), o))
+
+
+def test_round_log_matches_stats():
+    """sieve_round_log: one record per round whose sums are the search's statistics."""
+    c = case("c1")
+    s = c.w.spec
+    for kw in (dict(lookahead=True), dict(lookahead=False), dict(lookahead=True,
+                                                                  speculative=True)):
+        r = c.ix.search(c.w.queries, c.w.exclude_ids, s.k, 0.5, s.W, s.nprobe_max,
+                        with_stats=True, **kw)
+        st = r[3]
+        log = c.ix.round_log()
+        assert len(log) == st.rounds
+        assert sum(x.items for x in log) == st.items
+        assert sum(x.item_rows for x in log) == st.vectors_scanned
+        assert sum(x.list_loads for x in log) == st.list_loads
+        assert sum(x.candidates for x in log) == st.hits
+        assert all(x.ms_scan > 0 and x.kind == 0 for x in log)
+        assert abs(sum(x.ms_scan for x in log) - st.ms_scan) <= 1e-3 * max(st.ms_scan, 1.0)
+    f = c.ix.search_fixed(c.w.queries, c.w.exclude_ids, s.k, s.tau, s.nprobe_max,
+                          with_stats=True)
+    log = c.ix.round_log()
+    assert len(log) == f[3].rounds and all(x.kind == 1 for x in log)
+    assert sum(x.items for x in log) == f[3].items
+
+
+def test_pool_index_limit_gives_a_clean_error():
+    """A search that would hold more candidate-pool slots than the final merge can index
+    fails with SIEVE_EUNSUPPORTED before the merge runs; the limit is lowered through its
+    knob so that no large pool is needed, and the handle keeps working afterwards."""
+    ps = _lib()
+    c = case("c1")
+    s = c.w.spec
+    os.environ["SIEVE_POOL_LIMIT"] = "1000"
+    try:
+        with pytest.raises(ps.SieveError) as e:
+            c.ix.search(c.w.queries, c.w.exclude_ids, s.k, 0.3, s.W, s.nprobe_max)
+        assert e.value.code == -4 and "32-bit" in str(e.value)
+    finally:
+        del os.environ["SIEVE_POOL_LIMIT"]
+    _check(c, s.k, s.tau, s.W, s.nprobe_max)
