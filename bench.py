@@ -200,7 +200,8 @@ def run_config(name, args, ps, sw, np, torch, dev, headline):
            "mean_probes": round(float(probes.float().mean().item()), 3),
            "scanned_probes_per_query": round(stats.items / nq, 3), "rounds": stats.rounds,
            "partition_vectors_per_s": round(stats.vectors_scanned * K / t_sieve, 1),
-           "candidates": int(stats.hits)}
+           "candidates": int(stats.hits), "pool_entries": int(stats.pool_entries),
+           "heavy_records": int(stats.heavy_records)}
     roof = roofline(spec.dtype, rounds, name)
     # per-step round table: the last step's rounds (every step runs the same rounds)
     roof["rounds"] = roof["rounds"][-stats.rounds:] if stats.rounds else []

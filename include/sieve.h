@@ -109,6 +109,11 @@ typedef struct sieve_stats {
   double scan_flops;        /* 2 * d * vectors_scanned                                     */
   double rank_flops;        /* 2 * d * nq * nlist (the centroid screen)                    */
   float ms_rank, ms_sched, ms_scan, ms_update, ms_finalize, ms_total; /* device time, ms */
+  int64_t pool_entries;     /* candidate records written for the final merge: at most k per
+                               (query, scan tile), at most hits                           */
+  int64_t heavy_records;    /* groups of up to 16 (query, tile) pairs whose qualifying rows
+                               outnumbered the scan's per-tile slots and went through the
+                               exact top-k pass                                           */
 } sieve_stats;
 
 /*
@@ -117,8 +122,9 @@ typedef struct sieve_stats {
  *   vectors      [n * d] of dtype, partition-major: the rows of list l are
  *                rows list_offsets[l] .. list_offsets[l+1]-1.
  *   dtype        SIEVE_F32 or SIEVE_F16 (queries and centroids share it).
- *   n            number of rows (>= 0); d: dimension, 8 <= d <= 4096 and a
- *                multiple of 8 (else SIEVE_EUNSUPPORTED).
+ *   n            number of rows (>= 0); d: dimension, a multiple of 8 with
+ *                8 <= d <= 4096 for fp16 and <= 2048 for fp32 (else
+ *                SIEVE_EUNSUPPORTED).
  *   list_offsets [nlist + 1] int64: non-decreasing, list_offsets[0] == 0,
  *                list_offsets[nlist] == n (checked on a host copy; else
  *                SIEVE_EINVAL).  Empty lists are allowed.

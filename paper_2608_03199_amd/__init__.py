@@ -45,7 +45,8 @@ class Stats(ctypes.Structure):
                 ("scan_flops", ctypes.c_double), ("rank_flops", ctypes.c_double),
                 ("ms_rank", ctypes.c_float), ("ms_sched", ctypes.c_float),
                 ("ms_scan", ctypes.c_float), ("ms_update", ctypes.c_float),
-                ("ms_finalize", ctypes.c_float), ("ms_total", ctypes.c_float)]
+                ("ms_finalize", ctypes.c_float), ("ms_total", ctypes.c_float),
+                ("pool_entries", ctypes.c_int64), ("heavy_records", ctypes.c_int64)]
 
     def as_dict(self) -> dict:
         return {name: getattr(self, name) for name, _ in self._fields_}

@@ -95,13 +95,14 @@ struct sieve_index {
 #define SIEVE_WORKSPACE(X)                                                                 \
   X(scores) X(P) X(items) X(bucket) X(tiles) X(cnt) X(item_off) X(cursor) X(tile_off) X(rc) \
   X(state_a) X(state_b) X(lmax) X(hcount) X(hoff) X(hcur) X(scan_tmp) X(pool)              \
-  X(pool_sorted) X(arenas) X(have) X(ext) X(qext) X(Pext) X(cand) X(ccount) X(cal_idx)      \
+  X(pool_sorted) X(heavy) X(spill) X(have) X(ext) X(qext) X(Pext) X(cand) X(ccount) X(cal_idx)      \
   X(cal_q) X(cal_x) X(cal_bits) X(cal_rank) X(cal_hist) X(mix_ids) X(mix_scores)            \
   X(mix_probes) X(spec_bits) X(rlog)
 #define SIEVE_DECLARE_BUF(name) Buf name;
   SIEVE_WORKSPACE(SIEVE_DECLARE_BUF)
 #undef SIEVE_DECLARE_BUF
   int64_t pool_cap = 0;
+  int64_t heavy_cap = 0;  // HeavyRec records the heavy buffer holds
   RoundCounters* rc_host = nullptr;
   RoundSummary* rs_host = nullptr;  // coherent pinned memory the update launches write
   RoundSummary* rs_dev = nullptr;   // its device address
@@ -210,7 +211,8 @@ int scan_grid(const sieve_index* ix, int tile_q) {
   const size_t lds = scan_lds_bytes(ix->dtype, ix->d, tile_q) + 4096;
   int per_cu = (int)((160 * 1024) / lds);
   per_cu = per_cu < 1 ? 1 : (per_cu > 2 ? 2 : per_cu);
-  per_cu = env_int("SIEVE_SCAN_BLOCKS_PER_CU", per_cu);
+  if (scan_uses_rega(ix->dtype, ix->d)) per_cu = 1;  // the whole register file per wave
+  per_cu = std::min(env_int("SIEVE_SCAN_BLOCKS_PER_CU", per_cu), 2);  // <= the spill grid
   return ((ix->cus * per_cu + 7) / 8) * 8;  // the scan's schedule needs a multiple of 8
 }
 
@@ -228,6 +230,8 @@ struct SearchPlan {
   int64_t nq;
   int tile_q;           // query rows a tile stages (LDS sizing)
   int group_q;          // items of one list grouped into a tile (tile_q; 1 = serial)
+  bool rega;            // register-A scan: dense and sparse rounds take different tiles
+  int min_group;        // smallest tile grouping of any round (workspace bound)
   int row_chunk;        // rows per tile in sparse rounds
   int row_chunk_dense;  // rows per tile in dense rounds (long tiles amortise the tile start)
   int dense_q;          // a round is dense with at least this many items per list on average
@@ -258,6 +262,20 @@ int check_common(const sieve_index* ix, const void* queries, int64_t nq, int32_t
   return SIEVE_OK;
 }
 
+// Spill entries per scan work-group (rows past a query's LDS slots in one
+// tile); 0 when a tile could hold more rows than the entries can address.
+int spill_cap(const sieve_index* ix) {
+  if (ix->max_list >= ((int64_t)1 << kSpillRowBits)) return 0;
+  // SIEVE_SPILL_CAP lowers it (tests of the overflow path)
+  return std::min(env_count("SIEVE_SPILL_CAP", 16384), 16384);
+}
+// The candidate arena packs a row offset in 24 bits; SIEVE_ARENA = 0 turns it
+// off (every tile with candidates then takes the exact top-k pass; tests).
+bool arena_on(const sieve_index* ix) {
+  return ix->max_list < ((int64_t)1 << kSpillRowBits) && env_count("SIEVE_ARENA", 1) != 0;
+}
+int spill_grid(const sieve_index* ix) { return ((2 * ix->cus + 7) / 8) * 8; }
+
 int grow_workspace(sieve_index* ix, const SearchPlan& pl) {
   const int64_t nq = pl.nq;
   const int n = pl.n;
@@ -269,8 +287,9 @@ int grow_workspace(sieve_index* ix, const SearchPlan& pl) {
   if ((st = ensure(ix->bucket, (size_t)pl.item_cap * sizeof(BItem)))) return st;
   // tiles: sum_p ceil(c_p / tq) * ceil(len_p / rc) <= items * max_chunks / tq + lists + rows / rc
   const int64_t max_ch = (ix->max_list + pl.row_chunk - 1) / pl.row_chunk;
-  const int64_t tile_cap = pl.item_cap / pl.group_q * (max_ch > 0 ? max_ch : 1) + ix->nlist +
-                           ix->n / pl.row_chunk + 16;
+  const int64_t tile_cap = pl.item_cap / std::min(pl.group_q, pl.min_group) *
+                               (max_ch > 0 ? max_ch : 1) +
+                           ix->nlist + ix->n / pl.row_chunk + 16;
   if (tile_cap > INT32_MAX) return fail(SIEVE_EUNSUPPORTED, "tile count bound overflows int32");
   if ((st = ensure(ix->tiles, (size_t)tile_cap * sizeof(Tile)))) return st;
   const size_t nl = (size_t)ix->nlist;
@@ -286,15 +305,25 @@ int grow_workspace(sieve_index* ix, const SearchPlan& pl) {
     return st;
   if ((st = ensure(ix->scan_tmp, exclusive_scan_tmp_elems(nq) * 4))) return st;
   if (pl.spec && (st = ensure(ix->spec_bits, (size_t)nq * pl.hit_words * 4))) return st;
-  if ((st = ensure(ix->arenas, (size_t)pl.scan_grid * sizeof(ArenaRec)))) return st;
   if ((st = ensure(ix->rlog, (size_t)kMaxLogRounds * sizeof(RoundSnap)))) return st;
-  // arena runs can leave up to kArenaMax unused slots per scan work-group
-  const int64_t slack = (int64_t)pl.scan_grid * kArenaMax;
-  if (ix->pool_cap < slack + (1 << 20)) {
+  // The pool holds at most k entries per (query, tile); most searches need far
+  // fewer, so it starts small and grows (the search is then re-run) only when
+  // a search needs more.
+  if (ix->pool_cap < (1 << 20)) {
     int64_t cap = nq * 16;
-    if (cap < (1 << 20)) cap = 1 << 20;
-    ix->pool_cap = cap + slack;
+    ix->pool_cap = cap < (1 << 20) ? (1 << 20) : cap;
   }
+  // overflow records: a first size (SIEVE_HEAVY_CAP0 lowers it for tests of the
+  // regrowth), then grown on demand
+  if (ix->heavy_cap == 0)
+    ix->heavy_cap = env_int("SIEVE_HEAVY_CAP0", (int)std::min<int64_t>(std::max<int64_t>(4096, nq / 8), 1 << 24));
+  if ((st = ensure(ix->heavy, (size_t)ix->heavy_cap * sizeof(HeavyRec)))) return st;
+  // per scan work-group: the candidate arena's global extension and the
+  // tile's grouped arena (every grid of this search has at most spill_grid
+  // work-groups)
+  if ((st = ensure(ix->spill,
+                   (size_t)spill_grid(ix) * arena_block_entries(spill_cap(ix)) * sizeof(TileSpill))))
+    return st;
   if ((st = ensure(ix->pool, (size_t)ix->pool_cap * sizeof(Hit)))) return st;
   if ((st = ensure(ix->pool_sorted, (size_t)ix->pool_cap * sizeof(Hit)))) return st;
   if (!ix->rc_host) HIP_TRY(hipHostMalloc((void**)&ix->rc_host, sizeof(RoundCounters), 0));
@@ -364,9 +393,15 @@ ScanArgs make_scan_args(sieve_index* ix, const void* queries, const int64_t* exc
   a.lmax = (int32_t*)ix->lmax.p;
   a.hcount = (int32_t*)ix->hcount.p;
   a.pool = (Hit*)ix->pool.p;
-  a.arenas = (ArenaRec*)ix->arenas.p;
   a.pool_count = &rc->hits;
   a.pool_cap = ix->pool_cap;
+  a.heavy = (HeavyRec*)ix->heavy.p;
+  a.heavy_count = &rc->heavy;
+  a.heavy_cap = ix->heavy_cap;
+  a.k = pl.k;
+  a.spill = (TileSpill*)ix->spill.p;
+  a.spill_cap = spill_cap(ix);
+  a.arena_on = arena_on(ix) ? 1 : 0;
   a.d = ix->d;
   a.row_chunk = pl.row_chunk;
   a.tile_q = pl.tile_q;
@@ -381,12 +416,22 @@ ScanArgs make_scan_args(sieve_index* ix, const void* queries, const int64_t* exc
 int run_round(sieve_index* ix, const ScanArgs& sa, int n_items, int64_t q0, const int32_t* P,
               const SearchPlan& pl, hipStream_t s, bool timed, int* at) {
   RoundCounters* rc = (RoundCounters*)ix->rc.p;
-  const int chunk = (int64_t)n_items >= (int64_t)pl.dense_q * ix->nlist ? pl.row_chunk_dense
-                                                                        : pl.row_chunk;
+  const bool dense = (int64_t)n_items >= (int64_t)pl.dense_q * ix->nlist;
+  const int chunk = dense ? pl.row_chunk_dense : pl.row_chunk;
+  int group = pl.group_q, tile_q = pl.tile_q, grid = pl.scan_grid;
+  if (pl.rega) {
+    // dense rounds: 128-query tiles of whole lists, one work-group per CU;
+    // sparse rounds: 64-query tiles of 512 rows, two per CU
+    // (SIEVE_REGA_DENSE = 0 gives dense rounds the sparse shape; tuning only)
+    const bool big = dense && env_count("SIEVE_REGA_DENSE", 1) != 0;
+    tile_q = scan_rega_tile_q(big);
+    group = pl.group_q == 1 ? 1 : tile_q;
+    grid = ((ix->cus * (big ? 1 : 2) + 7) / 8) * 8;
+  }
   const int e0 = *at >= 0 ? *at : mark(ix, timed, s);
   // few lists: the offsets launch also writes the tiles
   const bool fuse = ix->nlist <= kFuseTilesMaxLists;
-  HIP_TRY(launch_sched_offsets((int32_t*)ix->cnt.p, ix->offsets, ix->nlist, chunk, pl.group_q,
+  HIP_TRY(launch_sched_offsets((int32_t*)ix->cnt.p, ix->offsets, ix->nlist, chunk, group,
                                (int32_t*)ix->item_off.p, (int32_t*)ix->cursor.p,
                                (int32_t*)ix->tile_off.p, rc, fuse ? (Tile*)ix->tiles.p : nullptr,
                                s));
@@ -395,11 +440,12 @@ int run_round(sieve_index* ix, const ScanArgs& sa, int n_items, int64_t q0, cons
   if (!fuse)
     HIP_TRY(launch_sched_tiles((int32_t*)ix->cnt.p, (const int32_t*)ix->item_off.p,
                                (const int32_t*)ix->tile_off.p, ix->offsets, ix->nlist, chunk,
-                               pl.group_q, (Tile*)ix->tiles.p, s));
+                               group, (Tile*)ix->tiles.p, s));
   const int e1 = mark(ix, timed, s);
   ScanArgs sr = sa;
   sr.dynamic = scan_dynamic(n_items);
-  HIP_TRY(launch_scan(ix->dtype, sr, pl.scan_grid, s));
+  sr.tile_q = tile_q;
+  HIP_TRY(launch_scan(ix->dtype, sr, grid, s));
   const int e2 = mark(ix, timed, s);
   span(ix, kSched, e0, e1);
   span(ix, kScan, e1, e2);
@@ -489,6 +535,8 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     ScanArgs sa = sa0;
     sa.pool = (Hit*)ix->pool.p;
     sa.pool_cap = ix->pool_cap;
+    sa.heavy = (HeavyRec*)ix->heavy.p;
+    sa.heavy_cap = ix->heavy_cap;
     if (cal) {
       sa.hitbits = cal->hitbits;
       sa.hit_words = cal->words;
@@ -497,12 +545,11 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     const int t_begin = mark(ix, timed, s);
     int at = -1;  // an event at the stream's current position, when one was just recorded
     {
-      // every per-search reset in one launch: counters, arenas, partition histogram,
+      // every per-search reset in one launch: counters, partition histogram,
       // per-query candidate counts, the calibration bitmap, the ordered-prefix lengths
-      static_assert(sizeof(RoundCounters) % 4 == 0 && sizeof(ArenaRec) % 4 == 0, "word fills");
+      static_assert(sizeof(RoundCounters) % 4 == 0, "word fills");
       FillSegs f = {};
       f.seg[0] = {(int32_t*)rc, (int64_t)(sizeof(RoundCounters) / 4), 0};
-      f.seg[1] = {(int32_t*)ix->arenas.p, (int64_t)pl.scan_grid * (int64_t)(sizeof(ArenaRec) / 4), 0};
       f.seg[2] = {(int32_t*)ix->cnt.p, (int64_t)ix->nlist, 0};
       f.seg[3] = {(int32_t*)ix->hcount.p, nq, 0};
       if (cal) f.seg[4] = {(int32_t*)cal->hitbits, nq * (int64_t)cal->words, 0};
@@ -555,6 +602,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
         sm.new_items = rs->new_items;
         sm.n_ext = rs->n_ext;
         sm.rank_error = rs->rank_error;
+        sm.heavy = rs->heavy;
         sm.hits = rs->hits;
         items_total += n_items;
         ++rounds;
@@ -607,6 +655,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
       HIP_TRY(hipStreamSynchronize(s));
       at = -1;  // the copy ran after the last event
       sm.rank_error = ix->rc_host->rank_error;
+      sm.heavy = ix->rc_host->heavy;
       sm.hits = ix->rc_host->hits;
     }
     if (sm.rank_error) {
@@ -618,25 +667,56 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
       continue;
     }
 
-    const int64_t hits = (int64_t)sm.hits;
+    // Overflowed (tile, query) groups: the exact top-k pass appends their
+    // candidates to the pool.  A record buffer too small for them grows, and
+    // the search runs again (it is deterministic).
+    const int64_t n_heavy = sm.heavy;
+    if (n_heavy > ix->heavy_cap) {
+      ix->heavy_cap = n_heavy + n_heavy / 4 + 1024;
+      if ((st = ensure(ix->heavy, (size_t)ix->heavy_cap * sizeof(HeavyRec)))) return st;
+      if (++pool_retries > 4) return fail(SIEVE_EINTERNAL, "overflow records kept overflowing");
+      continue;
+    }
+    const int f0 = at >= 0 ? at : mark(ix, timed, s);
+    unsigned long long pool_n = sm.hits;
+    if (n_heavy > 0 && pool_n <= (unsigned long long)ix->pool_cap) {
+      HeavyArgs ha;
+      ha.vectors = ix->vectors;
+      ha.ids = ix->ids;
+      ha.queries = queries;
+      ha.recs = (const HeavyRec*)ix->heavy.p;
+      ha.nrec = (int32_t)n_heavy;
+      ha.d = ix->d;
+      ha.k = pl.k;
+      ha.pack_rank = sa.hitbits != nullptr ? 1 : 0;
+      ha.tau = pl.tau;
+      ha.hcount = (int32_t*)ix->hcount.p;
+      ha.pool = (Hit*)ix->pool.p;
+      ha.pool_count = &rc->hits;
+      ha.pool_cap = ix->pool_cap;
+      const int grid = (int)std::min<int64_t>(n_heavy, (int64_t)ix->cus * 16);
+      HIP_TRY(launch_scan_heavy(ix->dtype, ha, grid, s));
+      HIP_TRY(hipMemcpyAsync(&ix->rc_host->hits, &rc->hits, sizeof(unsigned long long),
+                             hipMemcpyDeviceToHost, s));
+      HIP_TRY(hipStreamSynchronize(s));
+      pool_n = ix->rc_host->hits;
+    }
+    const int64_t hits = (int64_t)pool_n;
     const int64_t limit = pool_index_limit(getenv("SIEVE_POOL_LIMIT"));
-    if (!pool_slots_fit(sm.hits, limit))
+    if (!pool_slots_fit(pool_n, limit))
       return fail(SIEVE_EUNSUPPORTED,
-                  "the search claimed %llu candidate-pool slots; the final merge indexes at "
-                  "most %lld (32-bit offsets)", (unsigned long long)sm.hits, (long long)limit);
+                  "the search wrote %llu candidate-pool entries; the final merge indexes at "
+                  "most %lld (32-bit offsets)", pool_n, (long long)limit);
     if (hits > ix->pool_cap) {
       // the pool overflowed: grow it and run again (the search is deterministic)
-      ix->pool_cap = hits + hits / 8 + (int64_t)pl.scan_grid * kArenaMax;
+      ix->pool_cap = hits + hits / 8 + 4096;
       if ((st = ensure(ix->pool, (size_t)ix->pool_cap * sizeof(Hit)))) return st;
       if ((st = ensure(ix->pool_sorted, (size_t)ix->pool_cap * sizeof(Hit)))) return st;
-      if (++pool_retries > 2) return fail(SIEVE_EINTERNAL, "candidate pool kept overflowing");
+      if (++pool_retries > 4) return fail(SIEVE_EINTERNAL, "candidate pool kept overflowing");
       continue;
     }
 
     // finalize: group the pool by query, then per-query top-k
-    const int f0 = at >= 0 ? at : mark(ix, timed, s);
-    HIP_TRY(launch_retire_arenas((const ArenaRec*)ix->arenas.p, pl.scan_grid, (Hit*)ix->pool.p,
-                                 ix->pool_cap, s));
     HIP_TRY(launch_exclusive_scan((const int32_t*)ix->hcount.p, (int32_t*)ix->hoff.p,
                                   (int32_t*)ix->hcur.p, nq, (int32_t*)ix->scan_tmp.p, s));
     HIP_TRY(launch_pool_scatter((const Hit*)ix->pool.p, hits, (int32_t*)ix->hcur.p,
@@ -675,7 +755,9 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
       stats->probes_total = (int64_t)probes_sum;
       stats->vectors_scanned = (int64_t)h.item_rows;
       stats->list_loads = (int64_t)h.list_loads;
-      stats->hits = (int64_t)cand_sum;
+      stats->hits = (int64_t)h.cands;
+      stats->pool_entries = (int64_t)cand_sum;
+      stats->heavy_records = (int64_t)h.heavy;
       stats->scan_bytes = (double)h.list_rows * eb + (double)items_total * (eb + sizeof(Item)) +
                           (double)cand_sum * sizeof(Hit);
       stats->scan_flops = 2.0 * (double)ix->d * (double)h.item_rows;
@@ -706,16 +788,25 @@ int plan_search(const sieve_index* ix, int64_t nq, int32_t k, float tau, int32_t
   pl->nq = nq;
   // default on where supported; SIEVE_SCAN_WIDE=2 turns it off (tuning only)
   pl->wide = scan_wide_supported(ix->dtype, ix->d) && env_int("SIEVE_SCAN_WIDE", 1) == 1;
-  pl->tile_q = pl->wide ? tile_rows_wide(ix->dtype, ix->d) : tile_rows(ix->dtype, ix->d);
+  pl->rega = scan_uses_rega(ix->dtype, ix->d);
+  pl->tile_q = pl->wide   ? tile_rows_wide(ix->dtype, ix->d)
+               : pl->rega ? scan_rega_tile_q(true)
+                          : tile_rows(ix->dtype, ix->d);
   pl->group_q = pl->tile_q;
+  pl->min_group = pl->rega ? scan_rega_tile_q(false) : pl->tile_q;
   pl->wide_rank = false;
   pl->row_chunk = row_chunk_for(ix, "SIEVE_ROW_CHUNK", 512);
   // Dense rounds over short lists (at most 2048 rows on average) take whole
   // lists as one tile, which halves the tile starts of a 1,000-row list; with
   // long lists the 512-row tiles measured as fast or faster.
   const int64_t avg_len = ix->n / ix->nlist;
-  pl->row_chunk_dense =
-      row_chunk_for(ix, "SIEVE_ROW_CHUNK_DENSE", avg_len <= 2048 ? 4096 : pl->row_chunk);
+  // Register-held queries make a tile's start cheap, so dense rounds take
+  // whole lists; otherwise the query staging favours 512-row tiles on long
+  // lists.
+  const int whole = (int)std::min<int64_t>(std::max<int64_t>(ix->max_list, 64), INT32_MAX / 2);
+  pl->row_chunk_dense = row_chunk_for(
+      ix, "SIEVE_ROW_CHUNK_DENSE",
+      scan_uses_rega(ix->dtype, ix->d) ? whole : (avg_len <= 2048 ? 4096 : pl->row_chunk));
   if (pl->row_chunk_dense < pl->row_chunk) pl->row_chunk_dense = pl->row_chunk;
   pl->dense_q = env_int("SIEVE_DENSE_Q", 64);
   // Speculative issue needs the rank packed beside the query in pool entries
@@ -779,6 +870,8 @@ void add_stats(sieve_stats* acc, const sieve_stats& x) {
   acc->vectors_scanned += x.vectors_scanned;
   acc->list_loads += x.list_loads;
   acc->hits += x.hits;
+  acc->pool_entries += x.pool_entries;
+  acc->heavy_records += x.heavy_records;
   acc->scan_bytes += x.scan_bytes;
   acc->scan_flops += x.scan_flops;
   acc->rank_flops += x.rank_flops;
@@ -810,6 +903,10 @@ SIEVE_API int sieve_load_index(const void* vectors, int32_t dtype, int64_t n, in
     return fail(SIEVE_EINVAL, "a required pointer is NULL");
   if (d % 8 != 0 || d > kMaxD)
     return fail(SIEVE_EUNSUPPORTED, "d = %d: must be a multiple of 8 and <= %d", d, kMaxD);
+  // a 16-query tile of fp32 rows must fit the scan's LDS
+  if (dtype == SIEVE_F32 && d > kMaxD / 2)
+    return fail(SIEVE_EUNSUPPORTED, "d = %d: fp32 rows must have at most %d dimensions", d,
+                kMaxD / 2);
   if (nlist > kMaxNlist) return fail(SIEVE_EUNSUPPORTED, "nlist = %d exceeds %d", nlist, kMaxNlist);
   if ((n > 0 && !aligned16(vectors)) || !aligned16(centroids) || !aligned16(list_offsets) ||
       (n > 0 && !aligned16(ids)))

@@ -416,6 +416,118 @@ __device__ __forceinline__ void stream_rows_qb(const u32x4* __restrict__ lds,
   }
 }
 
+// ---- register-held query fragments ----
+// For short rows (at most kRegAChunks MFMA chunks) a wave keeps its A
+// fragments for the whole tile in registers instead of reading them from
+// LDS for every 16-row block: with 8 query blocks the LDS reads of the
+// LDS-staged path (QB * 1 KB per chunk and row block per wave) would exceed
+// the LDS bandwidth long before the MFMA pipe is busy.  qf[c][qb] is lane
+// l's fragment of chunk c of query block qb (row l % 16, segment 4c + l / 16
+// of the staged tile), exactly what score_regs reads, so the scores are
+// bit-identical to the LDS-staged path.
+constexpr int kRegAChunks = 4;
+
+template <int DT, int D>
+constexpr bool rega_ok() {
+  return D > 0 && D % DTraits<DT>::kChunkDims == 0 && D / DTraits<DT>::kChunkDims <= kRegAChunks;
+}
+
+template <int DT, int D, int QB>
+__device__ __forceinline__ void load_afrags(const u32x4* __restrict__ lds, int segs,
+                                            u32x4 (&qf)[D / DTraits<DT>::kChunkDims][QB]) {
+  constexpr int kNC = D / DTraits<DT>::kChunkDims;
+  const int lane = threadIdx.x & 63;
+  const u32x4* arow = lds + (lane & 15) * segs + (lane >> 4);
+#pragma unroll
+  for (int c = 0; c < kNC; ++c) {
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) qf[c][qb] = arow[qb * 16 * segs + 4 * c];
+  }
+}
+
+// Fragment buffers of the register-A stream: the A fragments take 4 * kNC * QB
+// registers and the two accumulator sets 8 * QB, so the ring shrinks as QB
+// grows.  kRegs: registers per lane of one wave (512 at one wave per SIMD,
+// 256 at two).  The ring depth is even (accumulator sets alternate by step).
+template <int DT, int D, int QB, int kRegs>
+constexpr int rega_ring() {
+  constexpr int kNC = D / DTraits<DT>::kChunkDims;
+  const int per = 4 * kNC + 2;  // fragments and row ids of one row block
+  int nb = (kRegs - 4 * kNC * QB - 8 * QB - (kRegs > 256 ? 200 : 130)) / per;
+  nb = nb > 8 ? 8 : nb;
+  nb &= ~1;
+  return nb < 2 ? 2 : nb;
+}
+
+// Stream rows [r0, r1) through the block's waves (wave w takes row blocks w,
+// w + W, ...) against the register-held fragments qf, calling
+// epi(acc, row, rid) per 16-row block: row = the stored row of this lane's
+// column (it may be >= r1 on the last block; loads are clamped) and rid =
+// ids[row] (clamped likewise), loaded with the block's fragments so that the
+// epilogue never waits on it.  Chunks are multiplied in ascending order into
+// each accumulator, as in score_regs: the same bits.  The epilogue of block
+// b runs after the MFMAs of block b + W are issued (two accumulator sets), so
+// that its vector work overlaps them.
+template <int DT, int D, int QB, int kRegs, typename Epi>
+__device__ __forceinline__ void stream_rows_rega(const u32x4 (&qf)[D / DTraits<DT>::kChunkDims][QB],
+                                                 const char* __restrict__ base, size_t row_bytes,
+                                                 const int64_t* __restrict__ ids, int64_t r0,
+                                                 int64_t r1, Epi& epi) {
+  constexpr int kNC = D / DTraits<DT>::kChunkDims;
+  constexpr int NB = rega_ring<DT, D, QB, kRegs>();
+  const int wave = wave_id();
+  const int nwaves = blockDim.x >> 6;
+  const int r16 = threadIdx.x & 15;
+  const RowStream rs = {base + (size_t)r0 * row_bytes, (int)(r1 - r0), (uint32_t)row_bytes};
+  const int nrows = rs.nrows;
+  const int64_t* idb = ids + r0;
+  auto load = [&](int blk, u32x4(&dst)[kNC], int64_t& rid) {
+    const char* p = rs.seg_ptr(blk);
+#pragma unroll
+    for (int c = 0; c < kNC; ++c) dst[c] = *(const u32x4*)(p + 64 * c);
+    rid = idb[rs.lane_row(blk)];
+  };
+  u32x4 buf[NB][kNC];
+  int64_t rid[NB];
+  if (nrows <= 0) return;
+#pragma unroll
+  for (int j = 0; j < NB - 1; ++j) load(wave + j * nwaves, buf[j], rid[j]);
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);  // see stream_rows_sliced
+  __builtin_amdgcn_sched_barrier(0);
+  f32x4 acc[2][QB];
+  int rb = wave;
+  bool done = false, have_prev = false;
+  int64_t prev_row = 0;
+  // NB row blocks per trip, expanded at compile time so that every ring and
+  // accumulator index is a constant (a runtime index would put them in scratch)
+  while (!done) {
+    unroll_steps([&](auto jc) {
+      constexpr int j = decltype(jc)::value;
+      constexpr int cur = j & 1, prv = cur ^ 1;  // NB is even
+      if (done) return;
+      const bool live = rb * 16 < nrows;  // uniform
+      const int64_t rid_prev = rid[(j + NB - 1) % NB];  // its slot is refilled below
+      if (live) {
+        load(rb + (NB - 1) * nwaves, buf[(j + NB - 1) % NB], rid[(j + NB - 1) % NB]);
+        __builtin_amdgcn_sched_barrier(0);  // prefetch stays above the MFMAs
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) acc[cur][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < kNC; ++c) mma_chunk_qb<DT, QB>(qf[c], buf[j][c], acc[cur]);
+      }
+      if (have_prev) epi(acc[prv], prev_row, rid_prev);
+      if (!live) {
+        done = true;
+        return;
+      }
+      have_prev = true;
+      prev_row = r0 + rb * 16 + r16;
+      rb += nwaves;
+    }, std::make_integer_sequence<int, NB>{});
+  }
+}
+
 // Largest number of 16-query blocks a tile of compile-time dimension D can
 // stage (the 80 KB LDS budget that keeps two work-groups per CU; the host's
 // tile size follows the same rule).  D = 0: runtime dimension, up to 8.

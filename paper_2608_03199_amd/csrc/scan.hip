@@ -1,30 +1,36 @@
 // scan.hip -- partition scan (within-partition search, Sec. 2.3 and Sec. 5)
-// fused with the tau test, and the centroid-screen GEMM of the ranking step
-// (Sec. 4.1).  Both use the MFMA tile engine of mfma_tile.h.
+// fused with the tau test, the exact top-k pass for tiles whose candidates
+// overflow, and the centroid-screen GEMM of the ranking step (Sec. 4.1).  All
+// use the MFMA tile engine of mfma_tile.h.
 //
 // Partition scan: each tile holds up to 16*QB ready items (q_i, j) of one
-// partition (Sec. 4.2's partition group) and one chunk of that partition's
-// rows.  The queries are staged once in LDS; every wave streams 16 rows at a
-// time from HBM into registers and scores them against all staged queries.
-// A score that reaches tau (inclusive, Sec. 2.2) for a row whose id is not
-// the query's exclusion id makes the probe a hit (Sec. 4.1): the candidate is
-// appended to the hit pool and the query's highest hit rank of the round is
-// raised with an atomic max.  The hit test depends only on the pair's own
+// partition (Sec. 4.2's partition group) and a range of that partition's rows
+// (the whole list in dense rounds).  The tile's query rows are staged in LDS;
+// every wave streams 16 rows at a time from HBM into registers and scores
+// them against all the tile's queries.  For short rows (at most 4 MFMA
+// chunks, e.g. 128-dim fp16) each wave first copies its query fragments from
+// LDS into registers and keeps them for the whole tile (the staging buffer is
+// then refilled with the next tile's queries while this one streams); longer
+// rows read the fragments from LDS per row block.  A score that reaches tau
+// (inclusive, Sec. 2.2) for a row whose id is not the query's exclusion id
+// makes the probe a hit (Sec. 4.1): the query's highest hit rank of the round
+// is raised with an atomic max.  The hit test depends only on the pair's own
 // score, never on other candidates, so it is the same whatever the dispatch
 // order (the property the lookahead equivalence of Sec. 4.3 needs).
+//
+// Local results (Algorithm 1 keeps each partition's filtered top-k for the
+// final MergeTopK): a qualifying pair goes to the work-group's candidate
+// arena (LDS, then a global extension); at the end of the tile each query
+// writes its candidates, or its exact top k when it has more, to the pool.
+// A (query, tile) pair thus writes at most k pool entries.  A tile whose
+// arena overflows records its queries, with the tile's rows, for the exact
+// top-k pass instead.
 //
 // Work distribution: a persistent grid pulls tiles from a per-XCD work queue
 // (see the kernel); every block exits after its claims run dry, at most
 // tiles + 8 claims per block.
-//
-// Candidate pool: a block appends into a run of pool slots (its arena) that
-// it claimed with one global atomic, handing out slots with one LDS atomic
-// per ballot group of candidates.  A group that does not fit the arena claims
-// its slots from the global counter directly, and at the end of that tile the
-// block gives the arena's unused tail sentinel entries and claims a run twice
-// as long (up to kArenaMax).  The arena carries over to the block's next
-// launch in the same search; blocks that never meet a candidate claim nothing.
 #include "mfma_tile.h"
+#include "wave_sort.h"
 
 namespace sieve {
 namespace {
@@ -65,18 +71,66 @@ __device__ __forceinline__ void dma_stage(u32x4* buf, const RowGeom<DT>& g,
   }
 }
 
-template <int DT, int D, bool kAsync, int kNT>
-__global__ __launch_bounds__(kNT, kNT == kScanThreads ? 2 : 1) void scan_kernel(ScanArgs a) {
+// f(std::integral_constant<int, QB>) for the tile's number of 16-query
+// blocks qb_n (uniform per tile), QB = 1 .. kMax.
+template <int QB, int kMax, typename F>
+__device__ __forceinline__ void with_qb(int qb_n, F&& f) {
+  if constexpr (QB >= kMax) {
+    f(std::integral_constant<int, kMax>{});
+  } else {
+    if (qb_n <= QB)
+      f(std::integral_constant<int, QB>{});
+    else
+      with_qb<QB + 1, kMax>(qb_n, f);
+  }
+}
+
+// Register-A tiles come in two shapes.  Dense rounds (many items per list):
+// tiles of up to 8 query blocks, whose fragments take 128 registers at
+// 128-dim fp16, so the kernel runs one work-group per CU and takes the whole
+// register file (512 per lane).  Sparse rounds: tiles of up to 4 query
+// blocks at two work-groups per CU (256 registers each), twice the waves to
+// keep row loads in flight.
+template <int kOcc>
+constexpr int rega_max_qb() {
+  return kOcc == 1 ? 8 : 4;
+}
+
+// Element x = 4 qb + r of a row block's accumulators, x uniform: a chain of
+// selects on a scalar condition (no indexed register access).
+template <int QB>
+__device__ __forceinline__ float pick_score(const f32x4 (&acc)[QB], int x) {
+  float v = acc[0][0];
+#pragma unroll
+  for (int y = 1; y < 4 * QB; ++y) v = x == y ? acc[y >> 2][y & 3] : v;
+  return v;
+}
+
+// Staging modes of the scan kernel.
+constexpr int kStageSync = 0;   // staged through registers at the start of each tile
+constexpr int kStageAsync = 1;  // LDS-DMA into the other of two buffers, one tile ahead
+constexpr int kStageRegA = 2;   // LDS-DMA into one buffer; fragments kept in registers
+
+template <int DT, int D, int kMode, int kNT, int kOcc>
+__global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
   extern __shared__ u32x4 lds[];
   __shared__ int32_t s_q[2][kTileQ];     // item sets: the running tile and the next
   __shared__ int32_t s_rank[2][kTileQ];
   __shared__ int64_t s_ex[2][kTileQ];
-  __shared__ int32_t s_hits[kTileQ];  // candidates per staged query in this tile
-  __shared__ unsigned long long s_abase;  // first pool slot of the block's arena
-  __shared__ int32_t s_asize;  // arena slots (0: no arena)
-  __shared__ int32_t s_aused;  // arena slots handed out (may run past s_asize)
-  __shared__ int32_t s_afill;  // arena slots actually used (a prefix of the arena)
-  __shared__ int32_t s_afall;  // a group fell back to the global counter this tile
+  __shared__ int32_t s_hits[kTileQ];  // qualifying rows per staged query in this tile
+  __shared__ int32_t s_over[kTileQ];  // staged queries whose candidates overflowed
+  __shared__ int32_t s_sel[kTileQ];   // staged queries selected from slots + spill
+  __shared__ int32_t s_soff[kTileQ];  // their segment in the sorted spill
+  __shared__ int32_t s_scur[kTileQ];
+  __shared__ int32_t s_poff[kTileQ];  // their first pool entry (after the tile's base)
+  __shared__ int32_t s_pool_n, s_over_n, s_sel_n, s_rbase, s_spill_n, s_spill_ovf;
+  __shared__ unsigned long long s_pbase;
+  // per work-group: the arena's global extension (spill_cap entries), then
+  // the tile's whole arena grouped by query (LDS part and extension)
+  TileSpill* const arena_g = a.spill + (size_t)blockIdx.x * arena_block_entries(a.spill_cap);
+  TileSpill* const arena_srt = arena_g + a.spill_cap;
+  TileSpill* s_arena = (TileSpill*)(lds + a.cand_u4);  // [arena_lds]
+  const int arena_lds = a.arena_lds;
 
   const int d = D > 0 ? D : a.d;
   const RowGeom<DT> g = RowGeom<DT>::make(d);
@@ -147,16 +201,13 @@ __global__ __launch_bounds__(kNT, kNT == kScanThreads ? 2 : 1) void scan_kernel(
     s_first[1] = claim();
     s_first[2] = claim();
     s_first[3] = claim();
+    s_pool_n = 0;
+    s_over_n = 0;
+    s_sel_n = 0;
+    s_spill_n = 0;
+    s_spill_ovf = 0;
   }
   if (threadIdx.x < kTileQ) s_hits[threadIdx.x] = 0;
-  if (threadIdx.x == 0) {
-    const ArenaRec ar = a.arenas[blockIdx.x];  // the run left by the previous launch
-    s_abase = ar.base;
-    s_asize = ar.size;
-    s_aused = ar.fill;  // no run (size 0): every group takes the global path
-    s_afill = ar.fill;
-    s_afall = 0;
-  }
   __syncthreads();
   int t = s_first[0], tn = s_first[1], ta = s_first[2], tb = s_first[3];
   Tile recT = load_rec(t), recN = load_rec(tn), recA = load_rec(ta);
@@ -164,40 +215,25 @@ __global__ __launch_bounds__(kNT, kNT == kScanThreads ? 2 : 1) void scan_kernel(
   put_items(0, recT, load_items(recT));
   int set = 0;
   __syncthreads();
-  if constexpr (kAsync) {
+  if constexpr (kMode != kStageSync) {
     if (t >= 0) dma_stage<DT>(lds, g, qbase, row_bytes, s_q[0], recT.nq);
     __builtin_amdgcn_s_waitcnt(0);
   }
   __syncthreads();
 
   for (; t >= 0;) {
-    // the next tile's items go to the other set
     const int nset = set ^ 1;
-    put_items(nset, recN, itN);
-    __syncthreads();
-    int t_claim = -1;
-    if (threadIdx.x == 0) t_claim = claim();  // published at the end of this tile
-    u32x4* buf = lds;
-    if constexpr (kAsync) {
-      buf = lds + set * a.stage_u4;
-      if (tn >= 0) dma_stage<DT>(lds + nset * a.stage_u4, g, qbase, row_bytes, s_q[nset], recN.nq);
-    } else {
-      const int32_t* sq = s_q[set];
-      const int nq0 = recT.nq;
-      stage_queries<DT>(lds, g, ((nq0 + 15) >> 4) * 16, [&](int i) -> const u32x4* {
-        return i < nq0 ? (const u32x4*)(qbase + (size_t)sq[i] * row_bytes) : nullptr;
-      });
-      __syncthreads();
-    }
-    // pipeline loads, used one tile from now
-    const BItem itA = load_items(recA);
-    const Tile recB = load_rec(tb);
     const int32_t* sq = s_q[set];
     const int32_t* srank = s_rank[set];
     const int64_t* sex = s_ex[set];
     const int nq = recT.nq;
     const int qb_n = (nq + 15) >> 4;
     const int64_t r0 = recT.r0, r1 = recT.r0 + recT.nrows;
+    // the next tile's items go to the other set
+    put_items(nset, recN, itN);
+    BItem itA;
+    Tile recB;
+    int t_claim = -1;
 
     // Only the tile's last 16-query block can hold padding rows (qb_n =
     // ceil(nq / 16)); its four rows of this lane get threshold +inf when they
@@ -207,137 +243,257 @@ __global__ __launch_bounds__(kNT, kNT == kScanThreads ? 2 : 1) void scan_kernel(
 #pragma unroll
     for (int r = 0; r < 4; ++r)
       thr_last[r] = ((qb_n - 1) * 16 + 4 * h + r) < nq ? tau : INFINITY;
-    stream_rows<DT, D, 8, kNT == kScanThreads ? 80 : 150>(
-          buf, g, (const char*)a.vectors, row_bytes, r0, r1, qb_n,
-          [&](const auto& acc, int64_t row) {
-            constexpr int QB = sizeof(acc) / sizeof(acc[0]);
-            // tau test: one wave-wide vote in the common (no candidate) case;
-            // full query blocks through a max tree, the last one per row
-            float mx = -INFINITY;
+    // tau test: one wave-wide vote in the common (no candidate) case; full
+    // query blocks through a max tree, the last one per row
+    auto vote = [&](const auto& acc, int64_t row) -> bool {
+      constexpr int QB = sizeof(acc) / sizeof(acc[0]);
+      float mx = -INFINITY;
 #pragma unroll
-            for (int qb = 0; qb + 1 < QB; ++qb) {
+      for (int qb = 0; qb + 1 < QB; ++qb) {
 #pragma unroll
-              for (int r = 0; r < 4; ++r) mx = fmaxf(mx, acc[qb][r]);
-            }
-            bool any = mx >= tau;
+        for (int r = 0; r < 4; ++r) mx = fmaxf(mx, acc[qb][r]);
+      }
+      bool any = mx >= tau;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) any |= acc[QB - 1][r] >= thr_last[r];
-            any = any && (row < r1);
-            if (__ballot(any) == 0) return;
-            // row ids, needed only here (self-exclusion and the pool records)
-            const int64_t rid = a.ids[row < r1 ? row : r1 - 1];
-            // Candidates: one ballot group (16 rows x 4 queries) takes its
-            // pool slots with one LDS atomic on the block's arena; the
-            // per-query counts go to LDS (one add per query of the group)
-            // and reach global memory once per tile.
-            const int r16 = lane & 15;
+      for (int r = 0; r < 4; ++r) any |= acc[QB - 1][r] >= thr_last[r];
+      return any && (row < r1);
+    };
+    // Qualifying pairs of the row block (any: this lane's column may hold one;
+    // rid: the column's row id, for the self-exclusion).  The per-(query
+    // block, row) tests are folded into one bit mask per lane, and a loop
+    // (not unrolled: one copy of its code) visits only the (block, row) pairs
+    // that hold a candidate.
+    auto candidates = [&](const auto& acc, int64_t row, bool any, int64_t rid) {
+      constexpr int QB = sizeof(acc) / sizeof(acc[0]);
+      const int r16 = lane & 15;
+      const uint32_t roff = (uint32_t)(row - r0);
+      uint32_t lm = 0;
 #pragma unroll
-            for (int qb = 0; qb < QB; ++qb) {
-              // skip query blocks without a candidate with one vote each
-              bool qany;
-              if (qb + 1 < QB)
-                qany = fmaxf(fmaxf(acc[qb][0], acc[qb][1]), fmaxf(acc[qb][2], acc[qb][3])) >= tau;
-              else
-                qany = acc[qb][0] >= thr_last[0] || acc[qb][1] >= thr_last[1] ||
-                       acc[qb][2] >= thr_last[2] || acc[qb][3] >= thr_last[3];
-              if (__ballot(any && qany) == 0) continue;
+      for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
-              for (int r = 0; r < 4; ++r) {
-                const int i = qb * 16 + 4 * h + r;
-                const float sc = acc[qb][r];
-                bool hit = any && (sc >= (qb + 1 < QB ? tau : thr_last[r]));
-                if (__ballot(hit) == 0) continue;
-                hit = hit && rid != sex[i];  // self-exclusion, read only for qualifying pairs
-                const unsigned long long mask = __ballot(hit);
-                if (mask == 0) continue;
-                const int leader = __ffsll((long long)mask) - 1;  // wave-uniform
-                const int cnt = __popcll(mask);
-                int o = 0;
-                if (lane == leader) {
-                  o = atomicAdd(&s_aused, cnt);
-                  if (o + cnt <= s_asize) atomicAdd(&s_afill, cnt);
-                }
-                o = __builtin_amdgcn_readlane(o, leader);
-                unsigned long long base;
-                if (o + cnt <= s_asize) {  // wave-uniform; the common case
-                  base = s_abase + (unsigned long long)o;
-                } else {
-                  // The global claim sits in its own branch: waiting for its
-                  // result also waits for every load in flight (the prefetched
-                  // rows), which must not happen on the common path.
-                  unsigned long long gb = 0;
-                  if (lane == leader) {
-                    gb = atomicAdd(a.pool_count, (unsigned long long)cnt);
-                    s_afall = 1;
-                  }
-                  base = ((unsigned long long)(uint32_t)__builtin_amdgcn_readlane(
-                              (int)(gb >> 32), leader) << 32) |
-                         (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)gb, leader);
-                }
-                if (hit) {
-                  const unsigned long long slot =
-                      base + (unsigned long long)__popcll(mask & ((1ull << lane) - 1ull));
-                  if ((int64_t)slot < a.pool_cap) {
-                    Hit hv;
-                    hv.score = sc;
-                    hv.q = a.hitbits ? (sq[i] | (srank[i] << kRankShift)) : sq[i];
-                    hv.id = rid;
-                    a.pool[slot] = hv;
-                  }
-                }
-                if (r16 == 0) {
-                  const int c = __popcll((mask >> (16 * h)) & 0xffffull);
-                  if (c) atomicAdd(&s_hits[i], c);
-                }
-              }
-            }
-            // The candidate path issued global stores.  While stores and
-            // loads are both in flight the compiler can only wait for all
-            // of them before the next row block's MFMAs (including the
-            // prefetch just issued); draining the stores here, on this rare
-            // path, keeps the row loop's waits partial.
-            __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-          });
-    if constexpr (kAsync) __builtin_amdgcn_s_waitcnt(0);  // this wave's staging copies landed
-    __syncthreads();  // every wave is done with this tile's buffer and items
-    {
-      // candidates of the tile, for the round statistics: one add per wave
-      unsigned long long c = (int)threadIdx.x < nq ? (unsigned long long)s_hits[threadIdx.x] : 0;
-      for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o);
-      if (lane == 0 && c) atomicAdd(&a.rc->cands, c);
+        for (int r = 0; r < 4; ++r) {
+          const float thr = qb + 1 < QB ? tau : thr_last[r];
+          lm |= (uint32_t)(any && acc[qb][r] >= thr) << (qb * 4 + r);
+        }
+      }
+      uint32_t wm = lm;
+      for (int o = 32; o > 0; o >>= 1) wm |= (uint32_t)__shfl_xor((int)wm, o);
+      wm = __builtin_amdgcn_readfirstlane(wm);
+      while (wm) {
+        const int x = __builtin_ctz(wm);
+        wm &= wm - 1;
+        const int i = (x >> 2) * 16 + 4 * h + (x & 3);  // staged query of this lane's group
+        const float sc = pick_score(acc, x);
+        const bool hit = ((lm >> x) & 1u) && rid != sex[i];  // self-exclusion
+        const unsigned long long mask = __ballot(hit);
+        if (mask == 0) continue;
+        // per query (lane group) count, and the arena slots of the whole vote
+        const uint32_t gm = (uint32_t)(mask >> (16 * h)) & 0xffffu;
+        if (r16 == 0 && gm) atomicAdd(&s_hits[i], __popc(gm));
+        const int lead = __ffsll((long long)mask) - 1;
+        int ab = 0;
+        if (lane == lead) ab = atomicAdd(&s_spill_n, __popcll(mask));
+        ab = __shfl(ab, lead);
+        if (hit) {
+          const int pos = ab + __popcll(mask & ((1ull << lane) - 1ull));
+          const TileSpill ent{sc, roff | ((uint32_t)i << kSpillRowBits)};
+          if (pos < arena_lds)
+            s_arena[pos] = ent;
+          else if (pos - arena_lds < a.spill_cap)
+            arena_g[pos - arena_lds] = ent;
+          else
+            s_spill_ovf = 1;
+        }
+      }
+    };
+    // epilogue with the row id at hand (register-A stream) or loaded here
+    auto epi3 = [&](const auto& acc, int64_t row, int64_t rid) {
+      const bool any = vote(acc, row);
+      if (__ballot(any) == 0) return;
+      candidates(acc, row, any, rid);
+    };
+    auto epi = [&](const auto& acc, int64_t row) {
+      const bool any = vote(acc, row);
+      if (__ballot(any) == 0) return;
+      candidates(acc, row, any, a.ids[row < r1 ? row : r1 - 1]);
+    };
+
+    if constexpr (kMode == kStageRegA) {
+      with_qb<1, rega_max_qb<kOcc>()>(qb_n, [&](auto qbc) {
+        constexpr int QB = decltype(qbc)::value;
+        constexpr int kNC = D / DTraits<DT>::kChunkDims;
+        u32x4 qf[kNC][QB];
+        load_afrags<DT, D, QB>(lds, g.segs, qf);
+        __builtin_amdgcn_s_waitcnt(0);  // fragments in registers
+        __syncthreads();  // every wave has its fragments: the staging buffer is free
+        if (threadIdx.x == 0) t_claim = claim();  // published at the end of this tile
+        if (tn >= 0) dma_stage<DT>(lds, g, qbase, row_bytes, s_q[nset], recN.nq);
+        // pipeline loads, used one tile from now
+        itA = load_items(recA);
+        recB = load_rec(tb);
+        stream_rows_rega<DT, D, QB, kOcc == 1 ? 512 : 256>(qf, (const char*)a.vectors, row_bytes,
+                                                            a.ids, r0, r1, epi3);
+      });
+    } else {
+      __syncthreads();
+      if (threadIdx.x == 0) t_claim = claim();  // published at the end of this tile
+      u32x4* buf = lds;
+      if constexpr (kMode == kStageAsync) {
+        buf = lds + set * a.stage_u4;
+        if (tn >= 0)
+          dma_stage<DT>(lds + nset * a.stage_u4, g, qbase, row_bytes, s_q[nset], recN.nq);
+      } else {
+        stage_queries<DT>(lds, g, qb_n * 16, [&](int i) -> const u32x4* {
+          return i < nq ? (const u32x4*)(qbase + (size_t)sq[i] * row_bytes) : nullptr;
+        });
+        __syncthreads();
+      }
+      itA = load_items(recA);
+      recB = load_rec(tb);
+      stream_rows<DT, D, 8, kNT == kScanThreads ? 80 : 150>(
+          buf, g, (const char*)a.vectors, row_bytes, r0, r1, qb_n, epi);
     }
-    if ((int)threadIdx.x < nq && s_hits[threadIdx.x] > 0) {
-      // this tile's candidates of one query: one count update, one hit flag
-      const int q = sq[threadIdx.x];
-      atomicAdd(&a.hcount[q], s_hits[threadIdx.x]);
-      atomicMax(&a.lmax[q], srank[threadIdx.x] + 1);
-      if (a.hitbits) {
+    // this wave's staging copies and arena stores are complete (in L2)
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();  // every wave is done with this tile's queries, items and candidates
+    // Candidates in the arena's global extension were stored by other waves of
+    // the work-group: an acquire at agent scope invalidates the CU's vector L1,
+    // whose lines of that area may be stale (read in an earlier tile).
+    if (s_spill_n > arena_lds) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+
+    // End of the tile.  Per staged query: the hit flag; then its candidates to
+    // the pool (all of them, or its exact top k when it has more), or, when
+    // the arena overflowed, a heavy record for the exact top-k pass.
+    const bool arena_ok = s_spill_ovf == 0;  // block-uniform
+    int c = 0, keep = 0;
+    if ((int)threadIdx.x < nq) {
+      c = s_hits[threadIdx.x];
+      if (c > 0) {
+        const int q = sq[threadIdx.x];
         const int rk = srank[threadIdx.x];
-        atomicOr(&a.hitbits[(int64_t)q * a.hit_words + (rk >> 5)], 1u << (rk & 31));
+        atomicMax(&a.lmax[q], rk + 1);
+        if (a.hitbits)
+          atomicOr(&a.hitbits[(int64_t)q * a.hit_words + (rk >> 5)], 1u << (rk & 31));
+        if (arena_ok) {
+          keep = min(c, a.k);
+          s_poff[threadIdx.x] = atomicAdd(&s_pool_n, keep);
+          atomicAdd(&a.hcount[q], keep);
+          if (c > a.k) s_sel[atomicAdd(&s_sel_n, 1)] = threadIdx.x;
+        } else {
+          s_over[atomicAdd(&s_over_n, 1)] = threadIdx.x;
+        }
       }
-      s_hits[threadIdx.x] = 0;
     }
-    const bool refill = s_afall != 0;  // block-uniform: written before the barrier
-    if (refill) {
-      // sentinels over the unused tail of the arena being replaced
-      const unsigned long long ab = s_abase;
-      const Hit none = {-INFINITY, -1, -1};
-      for (int i = s_afill + (int)threadIdx.x; i < s_asize; i += blockDim.x) {
-        const unsigned long long slot = ab + (unsigned long long)i;
-        if ((int64_t)slot < a.pool_cap) a.pool[slot] = none;
+    {
+      // qualifying pairs of the tile, for the statistics: one add per wave
+      unsigned long long cs = (unsigned long long)c;
+      for (int o = 32; o > 0; o >>= 1) cs += __shfl_xor(cs, o);
+      if (lane == 0 && cs) atomicAdd(&a.rc->cands, cs);
+    }
+    __syncthreads();
+    const int pool_n = s_pool_n, over_n = s_over_n, sel_n = s_sel_n;  // block-uniform
+    if (pool_n + over_n > 0) {
+      if (threadIdx.x == 0) {
+        s_pbase = pool_n ? atomicAdd(a.pool_count, (unsigned long long)pool_n) : 0ull;
+        s_rbase = over_n ? atomicAdd(&a.rc->heavy, (over_n + kHeavyQ - 1) / kHeavyQ) : 0;
+        // segments of the grouped arena, by staged query
+        int run = 0;
+        for (int i = 0; i < nq; ++i) {
+          s_soff[i] = run;
+          s_scur[i] = 0;
+          run += s_hits[i];
+        }
       }
-      __syncthreads();  // everyone has read the old arena before it is replaced
+      __syncthreads();
+      if ((int)threadIdx.x < over_n) {
+        const int gi = threadIdx.x / kHeavyQ, m = threadIdx.x % kHeavyQ;
+        const int64_t rec = (int64_t)s_rbase + gi;
+        if (rec < a.heavy_cap) {
+          HeavyRec* hr = a.heavy + rec;
+          const int i = s_over[threadIdx.x];
+          hr->q[m] = sq[i];
+          hr->rank[m] = srank[i];
+          hr->ex[m] = sex[i];
+          if (m == 0) {
+            hr->r0 = r0;
+            hr->nrows = (int32_t)(r1 - r0);
+            hr->nq = min(kHeavyQ, over_n - gi * kHeavyQ);
+          }
+        }
+      }
+      if (pool_n > 0) {
+        // group the arena by staged query (counting sort into the sorted area)
+        const int na = s_spill_n;
+        for (int e = threadIdx.x; e < na; e += blockDim.x) {
+          const TileSpill ts = e < arena_lds ? s_arena[e] : arena_g[e - arena_lds];
+          const int qs = (int)(ts.rowq >> kSpillRowBits);
+          arena_srt[s_soff[qs] + atomicAdd(&s_scur[qs], 1)] = ts;
+        }
+        // the grouped area is read by other waves: stores complete, barrier,
+        // L1 invalidated (as above)
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        // queries with at most k candidates: all of them, one thread per query
+        if ((int)threadIdx.x < nq && c > 0 && c <= a.k) {
+          const int i = threadIdx.x;
+          const unsigned long long base = s_pbase + (unsigned long long)s_poff[i];
+          const int32_t qv = a.hitbits ? (sq[i] | (srank[i] << kRankShift)) : sq[i];
+          for (int e = 0; e < c; ++e) {
+            const TileSpill ts = arena_srt[s_soff[i] + e];
+            if ((int64_t)(base + e) < a.pool_cap) {
+              Hit hv;
+              hv.score = ts.score;
+              hv.q = qv;
+              hv.id = a.ids[r0 + (ts.rowq & ((1u << kSpillRowBits) - 1u))];
+              a.pool[base + e] = hv;
+            }
+          }
+        }
+        // queries with more: one wave merges the query's segment into its
+        // top k, 64 candidates at a time
+        const Cand none = {-INFINITY, 0x7fffffffffffffffll, -1};
+        for (int j = threadIdx.x >> 6; j < sel_n; j += blockDim.x >> 6) {
+          const int i = s_sel[j];
+          const int ci = s_hits[i];
+          Cand top = none;
+          for (int b0 = 0; b0 < ci; b0 += 64) {
+            Cand cnd = none;
+            if (b0 + lane < ci) {
+              const TileSpill ts = arena_srt[s_soff[i] + b0 + lane];
+              const uint32_t ro = ts.rowq & ((1u << kSpillRowBits) - 1u);
+              cnd = Cand{ts.score, (long long)a.ids[r0 + ro], 0};
+            }
+            cnd = wave_sort_desc<false>(cnd, lane);
+            if (b0 == 0) {
+              top = cnd;
+            } else {
+              const Cand rv = shfl_cand<false>(cnd, 63 - lane);  // top ++ reverse(cnd): bitonic
+              top = better(top, rv) ? top : rv;
+              top = wave_merge_desc<false>(top, lane);
+            }
+          }
+          const int kk = min(ci, a.k);
+          const unsigned long long base = s_pbase + (unsigned long long)s_poff[i];
+          if (lane < kk && (int64_t)(base + lane) < a.pool_cap) {
+            Hit hv;
+            hv.score = top.s;
+            hv.q = a.hitbits ? (sq[i] | (srank[i] << kRankShift)) : sq[i];
+            hv.id = top.id;
+            a.pool[base + lane] = hv;
+          }
+        }
+      }
     }
+    __syncthreads();  // the counts and the spill are read; reset them for the next tile
+    if ((int)threadIdx.x < nq) s_hits[threadIdx.x] = 0;
     if (threadIdx.x == 0) {
       s_claim = t_claim;
-      if (refill) {
-        const int sz = s_asize == 0 ? kArenaMin : min(2 * s_asize, kArenaMax);
-        s_abase = atomicAdd(a.pool_count, (unsigned long long)sz);
-        s_asize = sz;
-        s_aused = 0;
-        s_afill = 0;
-        s_afall = 0;
-      }
+      s_pool_n = 0;
+      s_over_n = 0;
+      s_sel_n = 0;
+      s_spill_n = 0;
+      s_spill_ovf = 0;
     }
     __syncthreads();
     t = tn;
@@ -350,12 +506,145 @@ __global__ __launch_bounds__(kNT, kNT == kScanThreads ? 2 : 1) void scan_kernel(
     itN = itA;
     set = nset;
   }
-  if (threadIdx.x == 0) {
-    ArenaRec ar;
-    ar.base = s_abase;
-    ar.size = s_asize;
-    ar.fill = s_afill;
-    a.arenas[blockIdx.x] = ar;
+}
+
+// Exact top-k of overflowed (tile, query) groups: one wave per HeavyRec
+// scores its queries (a 16-query block, staged in LDS) against the tile's
+// rows with the scan's MFMA sequence (the same bits) and keeps, per query, the
+// qualifying rows in an LDS buffer.  Rows below the query's running k-th
+// score are not kept; whenever a buffer fills up, the wave sorts it (score
+// descending, id ascending) and keeps its first k, whose k-th score becomes
+// the new admission threshold (the final k-th can only be higher).  At the
+// end each query's first k go to the pool.
+constexpr int kHeavyCap = 128;  // buffered candidates per query (two per lane when sorting)
+
+template <int DT, int D>
+__global__ __launch_bounds__(64) void scan_heavy_kernel(HeavyArgs a) {
+  extern __shared__ u32x4 lds[];
+  __shared__ TileCand s_buf[kHeavyQ][kHeavyCap];
+  __shared__ int32_t s_cnt[kHeavyQ];
+  __shared__ int32_t s_qv[kHeavyQ];  // pool entry query field (rank packed when asked)
+  __shared__ int32_t s_qi[kHeavyQ];  // query index
+  __shared__ int64_t s_ex[kHeavyQ];
+  const int d = D > 0 ? D : a.d;
+  const RowGeom<DT> g = RowGeom<DT>::make(d);
+  const int lane = threadIdx.x & 63;
+  const int h = lane >> 4, r16 = lane & 15;
+  const size_t row_bytes = (size_t)d * DTraits<DT>::kElem;
+  const char* qbase = (const char*)a.queries;
+  const int k = a.k;
+  const Cand none = {-INFINITY, 0x7fffffffffffffffll, -1};
+
+  for (int rec = blockIdx.x; rec < a.nrec; rec += gridDim.x) {
+    const HeavyRec* hr = a.recs + rec;
+    const int nq = __builtin_amdgcn_readfirstlane(hr->nq);
+    const int64_t r0 = hr->r0;
+    const int64_t r1 = r0 + hr->nrows;
+    if (lane < kHeavyQ) {
+      const int i = lane < nq ? lane : 0;
+      s_qv[lane] = a.pack_rank ? (hr->q[i] | (hr->rank[i] << kRankShift)) : hr->q[i];
+      s_qi[lane] = hr->q[i];
+      s_ex[lane] = hr->ex[i];
+      s_cnt[lane] = 0;
+    }
+    // (nq >= 1: row 0 is always a real query, as stage_queries needs)
+    stage_queries<DT>(lds, g, kHeavyQ, [&](int i) -> const u32x4* {
+      return i < nq ? (const u32x4*)(qbase + (size_t)hr->q[i] * row_bytes) : nullptr;
+    });
+    __syncthreads();
+    // admission threshold of this lane's four queries (4h + r)
+    float thr[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) thr[r] = (4 * h + r) < nq ? a.tau : INFINITY;
+
+    // keep the first k of query j's buffer (sorted), raise its threshold
+    auto compact = [&](int j, bool final_pass, unsigned long long pbase) {
+      const int n = s_cnt[j];
+      Cand x = none, y = none;
+      if (lane < n) {
+        const TileCand tc = s_buf[j][lane];
+        x = Cand{tc.score, (long long)a.ids[r0 + tc.row], (int)tc.row};
+      }
+      if (lane + 64 < n) {
+        const TileCand tc = s_buf[j][lane + 64];
+        y = Cand{tc.score, (long long)a.ids[r0 + tc.row], (int)tc.row};
+      }
+      x = wave_sort_desc<true>(x, lane);
+      Cand top = x;
+      if (n > 64) {
+        y = wave_sort_desc<true>(y, lane);
+        const Cand ry = shfl_cand<true>(y, 63 - lane);  // x ++ reverse(y) is bitonic
+        top = better(x, ry) ? x : ry;
+        top = wave_merge_desc<true>(top, lane);
+      }
+      const int kk = n < k ? n : k;
+      if (final_pass) {
+        if (lane < kk) {
+          Hit hv;
+          hv.score = top.s;
+          hv.q = s_qv[j];
+          hv.id = top.id;
+          if ((int64_t)(pbase + lane) < a.pool_cap) a.pool[pbase + lane] = hv;
+        }
+        return;
+      }
+      __builtin_amdgcn_wave_barrier();
+      if (lane < kk) s_buf[j][lane] = TileCand{top.s, (uint32_t)top.rank};
+      if (lane == 0) s_cnt[j] = kk;
+      if (kk == k) {
+        const float tk = __shfl(top.s, k - 1);
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (h == (j >> 2) && r == (j & 3)) thr[r] = fmaxf(thr[r], tk);
+      }
+      __builtin_amdgcn_wave_barrier();
+    };
+
+    auto epi = [&](const auto& acc, int64_t row) {
+      bool pass[4];
+      bool any = false;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        pass[r] = row < r1 && acc[0][r] >= thr[r];
+        any |= pass[r];
+      }
+      if (__ballot(any) == 0) return;
+      const int64_t rid = a.ids[row < r1 ? row : r1 - 1];
+      const uint32_t roff = (uint32_t)(row - r0);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int j = 4 * h + r;  // this lane group's query for element r
+        const bool ok = pass[r] && rid != s_ex[j];
+        const unsigned long long mask = __ballot(ok);
+        if (mask == 0) continue;
+        const uint32_t gm = (uint32_t)(mask >> (16 * h)) & 0xffffu;
+        const int base = s_cnt[j];
+        __builtin_amdgcn_wave_barrier();
+        if (ok) s_buf[j][base + __popc(gm & ((1u << r16) - 1u))] = TileCand{acc[0][r], roff};
+        if (r16 == 0 && gm) s_cnt[j] = base + __popc(gm);
+        __builtin_amdgcn_wave_barrier();
+      }
+      // a buffer that could not take another full row block is compacted
+      for (int j = 0; j < nq; ++j)
+        if (s_cnt[j] > kHeavyCap - 16) compact(j, false, 0);
+    };
+    stream_rows_qb<DT, D, 1>(lds, g, (const char*)a.vectors, row_bytes, r0, r1, epi);
+
+    // each query's first k to the pool: one claim for the record
+    int tot = 0;
+    for (int j = 0; j < nq; ++j) tot += min(s_cnt[j], k);
+    unsigned long long pbase = 0;
+    if (lane == 0 && tot) pbase = atomicAdd(a.pool_count, (unsigned long long)tot);
+    pbase = ((unsigned long long)(uint32_t)__shfl((int)(pbase >> 32), 0) << 32) |
+            (uint32_t)__shfl((int)(uint32_t)pbase, 0);
+    for (int j = 0; j < nq; ++j) {
+      const int kk = min(s_cnt[j], k);
+      if (kk == 0) continue;
+      compact(j, true, pbase);
+      if (lane == 0) atomicAdd(&a.hcount[s_qi[j]], kk);
+      pbase += kk;
+    }
+    __syncthreads();  // the staging buffer and the candidate buffers are reused
   }
 }
 
@@ -422,29 +711,61 @@ bool use_async(int d, int tile_q) {
   }
 }
 
-template <int DT, int D, bool kAsync, int kNT>
+template <int DT, int D, int kMode, int kNT, int kOcc>
 hipError_t launch_scan_k(ScanArgs a, int32_t grid, hipStream_t s) {
   static const hipError_t attr =
-      hipFuncSetAttribute((const void*)scan_kernel<DT, D, kAsync, kNT>,
+      hipFuncSetAttribute((const void*)scan_kernel<DT, D, kMode, kNT, kOcc>,
                           hipFuncAttributeMaxDynamicSharedMemorySize, kMaxDynLds);
   if (attr != hipSuccess) return attr;
+  if (a.tile_q > kTileQ || a.k < 1 || a.k > 64) return hipErrorInvalidValue;
   const size_t one = stage_bytes<DT, D>(a.d, a.tile_q);
-  const size_t lds = kAsync ? 2 * one : one;
+  const size_t stage = kMode == kStageAsync ? 2 * one : one;
+  // the LDS arena takes what the staging leaves of the work-group's share of
+  // the CU's 160 KB (its static LDS is about 8 KB), at most kArenaLdsMax
+  const size_t share = kOcc == 1 ? (size_t)kMaxDynLds : (size_t)(72 * 1024);
+  const size_t room = share > stage ? share - stage : 0;
+  a.arena_lds = a.arena_on ? (int32_t)std::min<size_t>(room / sizeof(TileSpill), kArenaLdsMax) : 0;
+  if (!a.arena_on) a.spill_cap = 0;
+  const size_t lds = stage + (size_t)a.arena_lds * sizeof(TileSpill);
   if (lds > (size_t)kMaxDynLds) return hipErrorInvalidValue;
   a.stage_u4 = (int32_t)(one / 16);
-  hipLaunchKernelGGL((scan_kernel<DT, D, kAsync, kNT>), dim3(grid), dim3(kNT), lds, s, a);
+  a.cand_u4 = (int32_t)(stage / 16);
+  hipLaunchKernelGGL((scan_kernel<DT, D, kMode, kNT, kOcc>), dim3(grid), dim3(kNT), lds, s, a);
   return hipGetLastError();
 }
 
 template <int DT, int D>
 hipError_t launch_scan_t(const ScanArgs& a, int32_t grid, hipStream_t s) {
-  if constexpr (D == 768) {
-    if (a.wide) return launch_scan_k<DT, D, false, kScanThreadsWide>(a, grid, s);
+  if constexpr (rega_ok<DT, D>()) {
+    if (a.tile_q > 16 * rega_max_qb<2>())
+      return launch_scan_k<DT, D, kStageRegA, kScanThreads, 1>(a, grid, s);
+    return launch_scan_k<DT, D, kStageRegA, kScanThreads, 2>(a, grid, s);
+  } else {
+    if constexpr (D == 768) {
+      if (a.wide) return launch_scan_k<DT, D, kStageSync, kScanThreadsWide, 1>(a, grid, s);
+    }
+    if constexpr (async_stage_ok<DT, D>()) {
+      if (use_async<DT, D>(a.d, a.tile_q))
+        return launch_scan_k<DT, D, kStageAsync, kScanThreads, 2>(a, grid, s);
+    }
+    return launch_scan_k<DT, D, kStageSync, kScanThreads, 2>(a, grid, s);
   }
-  if constexpr (async_stage_ok<DT, D>()) {
-    if (use_async<DT, D>(a.d, a.tile_q)) return launch_scan_k<DT, D, true, kScanThreads>(a, grid, s);
-  }
-  return launch_scan_k<DT, D, false, kScanThreads>(a, grid, s);
+}
+
+// The heavy kernel's static LDS (its candidate buffers) leaves this much of
+// the 160 KB for the staged queries.
+constexpr int kMaxDynLdsHeavy = 136 * 1024;
+
+template <int DT, int D>
+hipError_t launch_heavy_t(const HeavyArgs& a, int32_t grid, hipStream_t s) {
+  static const hipError_t attr =
+      hipFuncSetAttribute((const void*)scan_heavy_kernel<DT, D>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, kMaxDynLdsHeavy);
+  if (attr != hipSuccess) return attr;
+  const size_t lds = (size_t)kHeavyQ * lds_row_bytes<DT>(D > 0 ? D : a.d);
+  if (lds > (size_t)kMaxDynLdsHeavy) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((scan_heavy_kernel<DT, D>), dim3(grid), dim3(64), lds, s, a);
+  return hipGetLastError();
 }
 
 template <int DT, int D>
@@ -480,6 +801,12 @@ int tile_rows_wide(int dtype, int d) {
 
 bool scan_wide_supported(int dtype, int d) { return dtype == SIEVE_F16 && d == 768; }
 
+bool scan_uses_rega(int dtype, int d) {
+  return (dtype == SIEVE_F16 && (d == 64 || d == 128)) || (dtype == SIEVE_F32 && d == 64);
+}
+
+int scan_rega_tile_q(bool dense) { return 16 * (dense ? rega_max_qb<1>() : rega_max_qb<2>()); }
+
 int tile_rows(int dtype, int d) {
   const int rb = dtype == SIEVE_F32 ? lds_row_bytes<SIEVE_F32>(d) : lds_row_bytes<SIEVE_F16>(d);
   int qb = (80 * 1024) / (16 * rb);
@@ -496,9 +823,28 @@ hipError_t launch_scan(int dtype, const ScanArgs& a, int32_t grid, hipStream_t s
     }
   }
   switch (a.d) {
+    case 64: return launch_scan_t<SIEVE_F16, 64>(a, grid, s);
     case 128: return launch_scan_t<SIEVE_F16, 128>(a, grid, s);
     case 768: return launch_scan_t<SIEVE_F16, 768>(a, grid, s);
     default: return launch_scan_t<SIEVE_F16, 0>(a, grid, s);
+  }
+}
+
+hipError_t launch_scan_heavy(int dtype, const HeavyArgs& a, int32_t grid, hipStream_t s) {
+  if (a.nrec <= 0) return hipSuccess;
+  if (a.k < 1 || a.k > 64 || grid < 1) return hipErrorInvalidValue;
+  if (dtype == SIEVE_F32) {
+    switch (a.d) {
+      case 64: return launch_heavy_t<SIEVE_F32, 64>(a, grid, s);
+      case 128: return launch_heavy_t<SIEVE_F32, 128>(a, grid, s);
+      default: return launch_heavy_t<SIEVE_F32, 0>(a, grid, s);
+    }
+  }
+  switch (a.d) {
+    case 64: return launch_heavy_t<SIEVE_F16, 64>(a, grid, s);
+    case 128: return launch_heavy_t<SIEVE_F16, 128>(a, grid, s);
+    case 768: return launch_heavy_t<SIEVE_F16, 768>(a, grid, s);
+    default: return launch_heavy_t<SIEVE_F16, 0>(a, grid, s);
   }
 }
 

@@ -228,6 +228,7 @@ __global__ void publish_round_kernel(const RoundCounters* __restrict__ rc,
   __hip_atomic_store(&out->n_ext, rc->n_ext, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   __hip_atomic_store(&out->rank_error, rc->rank_error, __ATOMIC_RELAXED,
                      __HIP_MEMORY_SCOPE_SYSTEM);
+  __hip_atomic_store(&out->heavy, rc->heavy, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   __hip_atomic_store(&out->hits, rc->hits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   __threadfence_system();
 }
@@ -244,6 +245,7 @@ __device__ __forceinline__ void publish_from_block(const RoundCounters* rc, Roun
   __hip_atomic_store(&out->n_ext, ne, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   __hip_atomic_store(&out->rank_error, rc->rank_error, __ATOMIC_RELAXED,
                      __HIP_MEMORY_SCOPE_SYSTEM);
+  __hip_atomic_store(&out->heavy, rc->heavy, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   __hip_atomic_store(&out->hits, rc->hits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   __threadfence_system();
 }

@@ -61,8 +61,10 @@ struct RoundCounters {
   unsigned long long list_rows;   // sum over active lists of their length (this round)
   unsigned long long item_rows;   // sum over items of their list's length (this round)
   unsigned long long list_loads;  // active non-empty lists (this round)
-  unsigned long long hits;        // pool slots claimed (whole search; includes arena tails)
-  unsigned long long cands;       // candidates the scans wrote (whole search)
+  unsigned long long hits;        // candidate-pool entries written (whole search)
+  unsigned long long cands;       // qualifying (query, row) pairs the scans found (whole search)
+  int32_t heavy;                  // HeavyRec records claimed (whole search)
+  int32_t pad_;
   // Sums of out_probes and of the qualifying candidates merged by the final
   // top-k, spread over kStatSlots counters (work-group b adds to slot
   // b % kStatSlots): thousands of adds to one address would serialise.
@@ -76,8 +78,8 @@ struct RoundSummary {
   int32_t new_items;
   int32_t n_ext;
   int32_t rank_error;
-  int32_t pad;
-  unsigned long long hits;
+  int32_t heavy;             // HeavyRec records claimed so far
+  unsigned long long hits;  // pool entries written so far
 };
 
 // Cumulative scan counters after one round (the per-round log of a timed
@@ -87,18 +89,45 @@ struct RoundSnap {
   unsigned long long list_rows, item_rows, list_loads, cands;
 };
 
-// Candidate-pool arenas: a scan work-group claims pool slots in runs (first
-// kArenaMin, doubling per refill up to kArenaMax) and keeps its current run
-// across the launches of one search in an ArenaRec indexed by block.  The
-// slots of a run it never fills are given a sentinel entry (q = -1) that the
-// final merge skips, once per search.
-constexpr int kArenaMin = 256;
-constexpr int kArenaMax = 4096;
-struct ArenaRec {
-  unsigned long long base;  // first pool slot of the run
-  int32_t size;             // slots in the run, 0 = no run
-  int32_t fill;             // slots used (a prefix of the run)
+// The qualifying rows a tile finds go to a candidate arena: the work-group's
+// LDS first, then a per-work-group extension in global memory.  At the end of
+// the tile the arena is grouped by staged query (counting sort into the
+// work-group's sorted area) and each query writes its candidates to the pool
+// when it has at most k of them, else its exact top k (score descending, id
+// ascending): a (query, tile) pair writes at most k pool entries, so the pool
+// is bounded by (items x row chunks per list x k).  A tile whose arena
+// overflows hands its queries with candidates to the exact top-k pass
+// (scan_heavy) in HeavyRec records instead.
+struct TileSpill {
+  float score;
+  uint32_t rowq;  // row offset inside the tile (low 24 bits) | staged query << 24
 };
+constexpr int kSpillRowBits = 24;
+// TileCand: a candidate of the exact top-k pass's LDS buffers.
+struct TileCand {
+  float score;
+  uint32_t row;  // row offset inside the tile
+};
+
+// Up to kHeavyQ overflowed queries of one tile, with the tile's rows (used
+// when the work-group's spill area overflows).
+constexpr int kHeavyQ = 16;
+struct HeavyRec {
+  int64_t r0;     // first stored row
+  int32_t nrows;  // rows
+  int32_t nq;     // queries in the record (1..kHeavyQ)
+  int32_t q[kHeavyQ];
+  int32_t rank[kHeavyQ];
+  int64_t ex[kHeavyQ];
+};
+
+// LDS arena entries at most.  A work-group's global area holds the arena's
+// extension (spill_cap entries) and the grouped copy of the whole arena (at
+// most kArenaLdsMax + spill_cap entries).
+constexpr int kArenaLdsMax = 12288;
+__host__ __device__ inline size_t arena_block_entries(int spill_cap) {
+  return 2 * (size_t)spill_cap + kArenaLdsMax;
+}
 
 struct ScanArgs {
   const void* vectors;         // [n, d] partition-major
@@ -112,14 +141,24 @@ struct ScanArgs {
   int32_t* lmax;               // [nq] max 1-based hit rank this round (0 = none)
   int32_t* hcount;             // [nq] pool entries per query
   Hit* pool;
-  ArenaRec* arenas;            // [scan grid] per-block pool runs
   unsigned long long* pool_count;
   int64_t pool_cap;
+  HeavyRec* heavy;             // overflowed (tile, query) groups for the exact top-k pass
+  int32_t* heavy_count;
+  int64_t heavy_cap;
+  int32_t k;
+  TileSpill* spill;            // [grid][arena_block_entries(spill_cap)]: per work-group
+                               // arena extension, then the grouped arena
+  int32_t spill_cap;           // arena entries in global memory per work-group (0: none)
+  int32_t arena_on;            // 0: no arena (tiles of 2^24 rows or more); every tile with
+                               // candidates takes the exact top-k pass
   int32_t d;
   int32_t row_chunk;
   int32_t tile_q;              // query rows per tile (multiple of 16, <= kTileQ)
   int32_t dynamic;             // 1: atomic work queue, 0: static strided schedule
   int32_t stage_u4;            // 16-byte slots per query staging buffer (set by the launcher)
+  int32_t cand_u4;             // 16-byte offset of the LDS arena in dynamic LDS (launcher)
+  int32_t arena_lds;           // LDS arena entries (launcher)
   int32_t wide;                // 1: wide configuration (one big work-group per CU)
   // calibration outputs (Algorithm 3), null / 0 otherwise: per query a bitmap
   // of the ranks whose probe had a candidate, and pool entries that carry
@@ -138,6 +177,12 @@ int tile_rows(int dtype, int d);
 constexpr int kScanThreadsWide = 512;
 int tile_rows_wide(int dtype, int d);
 bool scan_wide_supported(int dtype, int d);
+// Whether the scan keeps the tile's query fragments in registers (short rows;
+// one work-group per CU, whole lists per tile in dense rounds).
+bool scan_uses_rega(int dtype, int d);
+// Query rows per register-A tile: dense rounds (one work-group per CU) and
+// sparse rounds (two per CU); the launch picks the kernel from tile_q.
+int scan_rega_tile_q(bool dense);
 
 // ---- launchers (each returns the hipError_t of its launch) ----
 hipError_t launch_rank_scores(int dtype, const void* queries, int64_t q0, int32_t nqc,
@@ -222,8 +267,25 @@ hipError_t launch_zero_bytes(void* p, int64_t bytes, hipStream_t s);
 hipError_t launch_exclusive_scan(const int32_t* in, int32_t* out, int32_t* out_copy, int64_t n,
                                  int32_t* block_tmp, hipStream_t s);
 size_t exclusive_scan_tmp_elems(int64_t n);
-hipError_t launch_retire_arenas(const ArenaRec* arenas, int32_t n, Hit* pool, int64_t pool_cap,
-                                hipStream_t s);
+// Exact top-k pass over the overflowed (tile, query) groups: one wave per
+// HeavyRec selects each query's top k (score desc, id asc) among the tile's
+// qualifying rows and appends them to the pool.
+struct HeavyArgs {
+  const void* vectors;
+  const int64_t* ids;
+  const void* queries;
+  const HeavyRec* recs;
+  int32_t nrec;
+  int32_t d;
+  int32_t k;
+  int32_t pack_rank;  // pool entries carry their rank (q | rank << kRankShift)
+  float tau;
+  int32_t* hcount;
+  Hit* pool;
+  unsigned long long* pool_count;
+  int64_t pool_cap;
+};
+hipError_t launch_scan_heavy(int dtype, const HeavyArgs& a, int32_t grid, hipStream_t s);
 // Pool entries of a calibration search pack the rank into Hit.q.
 constexpr int kRankShift = 20;  // queries < 2^20, ranks < 2^11 (kMaxRanks)
 constexpr int32_t kQueryMask = (1 << kRankShift) - 1;

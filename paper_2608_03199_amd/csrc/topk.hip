@@ -12,6 +12,7 @@
 // sorting networks over lane shuffles.  The total order makes the result
 // independent of the pool's order.
 #include "sieve_internal.h"
+#include "wave_sort.h"
 
 namespace sieve {
 namespace {
@@ -104,7 +105,7 @@ __global__ __launch_bounds__(256) void pool_scatter_kernel(const Hit* __restrict
   const int lane = threadIdx.x & 63;
   Hit h = {-INFINITY, -1, -1};
   if (i < n) h = pool[i];
-  const int q = h.q < 0 ? -1 : (h.q & qmask);  // -1: past the end or an unused arena slot
+  const int q = h.q < 0 ? -1 : (h.q & qmask);  // -1: past the end
   // group the lanes by query (register work only), then every group's first
   // lane claims the group's slots, all groups at once
   unsigned long long todo = __ballot(q >= 0);
@@ -124,82 +125,6 @@ __global__ __launch_bounds__(256) void pool_scatter_kernel(const Hit* __restrict
   if (q >= 0 && rank == 0) base = atomicAdd(&cursor[q], count);
   base = __shfl(base, leader);
   if (q >= 0) sorted[base + rank] = h;
-}
-
-// Sentinels over the unused tail of every block's last arena (one block per
-// arena record).
-__global__ __launch_bounds__(256) void retire_arenas_kernel(const ArenaRec* __restrict__ arenas,
-                                                            Hit* __restrict__ pool,
-                                                            int64_t pool_cap) {
-  const ArenaRec ar = arenas[blockIdx.x];
-  const Hit none = {-INFINITY, -1, -1};
-  for (int i = ar.fill + (int)threadIdx.x; i < ar.size; i += blockDim.x) {
-    const unsigned long long slot = ar.base + (unsigned long long)i;
-    if ((int64_t)slot < pool_cap) pool[slot] = none;
-  }
-}
-
-struct Cand {
-  float s;
-  long long id;
-  int rank;  // carried only by the calibration variant of the top-k
-};
-
-__device__ __forceinline__ bool better(const Cand& a, const Cand& b) {
-  return a.s > b.s || (a.s == b.s && a.id < b.id);
-}
-
-template <bool kRank>
-__device__ __forceinline__ Cand shfl_xor_cand(const Cand& c, int m) {
-  Cand o;
-  o.s = __shfl_xor(c.s, m);
-  const int lo = __shfl_xor((int)(c.id & 0xffffffffll), m);
-  const int hi = __shfl_xor((int)(c.id >> 32), m);
-  o.id = ((long long)hi << 32) | (unsigned int)lo;
-  o.rank = kRank ? __shfl_xor(c.rank, m) : 0;
-  return o;
-}
-
-template <bool kRank>
-__device__ __forceinline__ Cand shfl_cand(const Cand& c, int src) {
-  Cand o;
-  o.s = __shfl(c.s, src);
-  const int lo = __shfl((int)(c.id & 0xffffffffll), src);
-  const int hi = __shfl((int)(c.id >> 32), src);
-  o.id = ((long long)hi << 32) | (unsigned int)lo;
-  o.rank = kRank ? __shfl(c.rank, src) : 0;
-  return o;
-}
-
-// Sort 64 lane-held candidates, best first.
-template <bool kRank>
-__device__ __forceinline__ Cand wave_sort_desc(Cand v, int lane) {
-#pragma unroll
-  for (int k = 2; k <= 64; k <<= 1) {
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      const Cand o = shfl_xor_cand<kRank>(v, j);
-      const bool lower = (lane & j) == 0;
-      const bool desc = (lane & k) == 0;  // final stage: whole wave descending
-      const bool keep_better = (lower == desc);
-      const bool ob = better(o, v);
-      if (keep_better ? ob : !ob) v = o;
-    }
-  }
-  return v;
-}
-
-// Sort a bitonic 64-sequence, best first.
-template <bool kRank>
-__device__ __forceinline__ Cand wave_merge_desc(Cand v, int lane) {
-#pragma unroll
-  for (int j = 32; j > 0; j >>= 1) {
-    const Cand o = shfl_xor_cand<kRank>(v, j);
-    const bool lower = (lane & j) == 0;
-    const bool ob = better(o, v);
-    if (lower ? ob : !ob) v = o;
-  }
-  return v;
 }
 
 // One wave per query, grid-stride over the queries; each block adds its
@@ -352,14 +277,6 @@ hipError_t launch_exclusive_scan(const int32_t* in, int32_t* out, int32_t* out_c
                      (int32_t)nb);
   hipLaunchKernelGGL(scan_apply_kernel, dim3((unsigned)nb), dim3(kScanBlock), 0, s, in, n,
                      block_tmp, out, out_copy);
-  return hipGetLastError();
-}
-
-hipError_t launch_retire_arenas(const ArenaRec* arenas, int32_t n, Hit* pool, int64_t pool_cap,
-                                hipStream_t s) {
-  if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(retire_arenas_kernel, dim3((unsigned)n), dim3(256), 0, s, arenas, pool,
-                     pool_cap);
   return hipGetLastError();
 }
 

@@ -363,25 +363,33 @@ def test_empty_lists_and_unbalanced_index():
         assert_parity(rep)
 
 
-def test_low_threshold_overflows_pool_and_retries():
-    """tau = -1: every scanned row qualifies (about 5M candidates for 1,000 queries x 16
-    probes of ~312 rows), more than a fresh index's first candidate pool holds (1M slots
-    plus 4,096 per scan work-group), so the pool grows and the search re-runs."""
+def test_low_threshold_pool_and_overflow_records_grow():
+    """tau = -1: every scanned row qualifies.  With k = 64 and 32 probes per query the
+    pool, though bounded by k entries per (query, tile), needs about 2M entries for 1,000
+    queries, more than a fresh index's first pool (about 1M), so it grows and the search
+    re-runs; with the overflow-record buffer started at 16 records through its knob, that
+    buffer grows too.  A second search needs no retry and gives the same result."""
     ps = _lib()
     c = case("c1")
     ix = ps.Index(c.w.vectors, c.w.list_offsets, c.w.ids, c.w.centroids)
     try:
-        g_ids, g_sc, g_pr, st = (t.cpu().numpy() if hasattr(t, "cpu") else t for t in
-                                 ix.search(c.w.queries, c.w.exclude_ids, 10, -1.0, 4, 16,
-                                           with_stats=True))
-        assert st.pool_retries >= 1 and st.hits > 4_000_000
-        # a second search on the grown pool needs no retry and gives the same result
-        g2 = ix.search(c.w.queries, c.w.exclude_ids, 10, -1.0, 4, 16, with_stats=True)
-        assert g2[3].pool_retries == 0 and g2[3].hits == st.hits
-        assert np.array_equal(g2[0].cpu().numpy(), g_ids)
+        os.environ["SIEVE_HEAVY_CAP0"] = "16"  # read when the first search sizes the buffer
+        try:
+            r = ix.search(c.w.queries, c.w.exclude_ids, 64, -1.0, 4, 32, with_stats=True)
+        finally:
+            del os.environ["SIEVE_HEAVY_CAP0"]
+        g_ids, g_sc, g_pr, st = (t.cpu().numpy() if hasattr(t, "cpu") else t for t in r)
+        print(f"[gpu-test] tau -1, k 64: retries {st.pool_retries}, found {st.hits}, "
+              f"pool {st.pool_entries}, heavy records {st.heavy_records}", flush=True)
+        assert st.pool_retries >= 2 and st.heavy_records > 16
+        assert st.hits > 8_000_000 and st.pool_entries > (1 << 20)
+        g2 = ix.search(c.w.queries, c.w.exclude_ids, 64, -1.0, 4, 32, with_stats=True)
+        assert g2[3].pool_retries == 0 and g2[3].pool_entries == st.pool_entries
+        for x, y in zip(g2[:3], (g_ids, g_sc, g_pr)):
+            assert np.array_equal(x.cpu().numpy(), y)
     finally:
         ix.close()
-    o = c.oracle(10, -1.0, 4, 16)
+    o = c.oracle(64, -1.0, 4, 32)
     rep = compare(g_ids, g_sc, g_pr, o)
     print(f"[gpu-test] low tau -> {rep}", flush=True)
     assert_parity(rep)
@@ -587,3 +595,49 @@ def test_pool_index_limit_gives_a_clean_error():
     finally:
         del os.environ["SIEVE_POOL_LIMIT"]
     _check(c, s.k, s.tau, s.W, s.nprobe_max)
+
+
+@pytest.mark.parametrize("k", [1, 10, 64])
+@pytest.mark.parametrize("fixed", [False, True])
+@pytest.mark.parametrize("knob", [None, ("SIEVE_SPILL_CAP", "0"), ("SIEVE_ARENA", "0")])
+def test_candidate_memory_bounded_by_k_per_tile(k, fixed, knob):
+    """Local results keep at most k candidates per (query, tile): at tau = 0.1 about a third
+    of the scanned rows qualify, yet the pool holds at most k entries per (query, row chunk).
+    A tile's qualifying rows go to its work-group's candidate arena (LDS, then a global
+    extension), and each query's exact top k is selected from it at the end of the tile.
+    With the extension removed, tiles whose rows overflow the LDS arena, and with the arena
+    off, all tiles with candidates, take the exact top-k pass instead.  The result equals
+    the oracle's every way."""
+    c = case("c1")
+    s = c.w.spec
+    q, ex = c.w.queries, c.w.exclude_ids
+    ix = c.ix
+    if knob is not None:
+        # the knobs are read when a search sizes its workspace: a fresh index
+        ps = _lib()
+        os.environ[knob[0]] = knob[1]
+        ix = ps.Index(c.w.vectors, c.w.list_offsets, c.w.ids, c.w.centroids)
+    try:
+        if fixed:
+            r = ix.search_fixed(q, ex, k, 0.1, s.nprobe_max, with_stats=True)
+        else:
+            r = ix.search(q, ex, k, 0.1, s.W, s.nprobe_max, with_stats=True)
+    finally:
+        if knob is not None:
+            del os.environ[knob[0]]
+            ix.close()
+    st = r[3]
+    off = c.h["list_offsets"]
+    chunks = int(np.ceil(np.diff(off).max() / 512))
+    print(f"[gpu-test] k={k} fixed={fixed} knob={knob}: found {st.hits}, pool "
+          f"{st.pool_entries}, heavy records {st.heavy_records}, items {st.items}", flush=True)
+    assert st.pool_entries <= k * st.items * chunks
+    assert st.hits > st.pool_entries
+    if knob is not None:
+        assert st.heavy_records > 0
+    else:
+        assert st.heavy_records == 0
+    o = c.oracle(k, 0.1, oracle.W_INF if fixed else s.W, s.nprobe_max)
+    rep = compare(r[0].cpu().numpy(), r[1].cpu().numpy(), r[2].cpu().numpy(), o)
+    print(f"[gpu-test] -> {rep}", flush=True)
+    assert_parity(rep)
