@@ -306,12 +306,7 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
         }
       }
     };
-    // epilogue with the row id at hand (register-A stream) or loaded here
-    auto epi3 = [&](const auto& acc, int64_t row, int64_t rid) {
-      const bool any = vote(acc, row);
-      if (__ballot(any) == 0) return;
-      candidates(acc, row, any, rid);
-    };
+    // epilogue of the LDS-staged streams (the row id is loaded here)
     auto epi = [&](const auto& acc, int64_t row) {
       const bool any = vote(acc, row);
       if (__ballot(any) == 0) return;
@@ -332,7 +327,7 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
         itA = load_items(recA);
         recB = load_rec(tb);
         stream_rows_rega<DT, D, QB, kOcc == 1 ? 512 : 256>(qf, (const char*)a.vectors, row_bytes,
-                                                            a.ids, r0, r1, epi3);
+                                                            a.ids, r0, r1, vote, candidates);
       });
     } else {
       __syncthreads();
