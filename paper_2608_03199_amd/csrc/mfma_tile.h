@@ -73,8 +73,10 @@ __device__ __forceinline__ f32x4 mma_chunk(u32x4 a, u32x4 b, f32x4 acc) {
 // different accumulators (a chain of four dependent fp32 MFMAs on one
 // accumulator stalls on each result).  Every accumulator still sees its
 // k-steps in the same order as mma_chunk_f32: the same bits.
-template <int DT, int QB>
+template <int DT, int QB, bool kZero = false>
 __device__ __forceinline__ void mma_chunk_qb(const u32x4 (&a)[QB], u32x4 b, f32x4 (&acc)[QB]) {
+  // kZero: the accumulators start from zero (their values are not read)
+  const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
   if constexpr (DT == SIEVE_F32) {
     const f32x4 bf = __builtin_bit_cast(f32x4, b);
 #pragma unroll
@@ -82,12 +84,13 @@ __device__ __forceinline__ void mma_chunk_qb(const u32x4 (&a)[QB], u32x4 b, f32x
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
         const f32x4 af = __builtin_bit_cast(f32x4, a[qb]);
-        acc[qb] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[k], bf[k], acc[qb], 0, 0, 0);
+        acc[qb] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[k], bf[k],
+                                                       (kZero && k == 0) ? zero : acc[qb], 0, 0, 0);
       }
     }
   } else {
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) acc[qb] = mma_chunk_f16(a[qb], b, acc[qb]);
+    for (int qb = 0; qb < QB; ++qb) acc[qb] = mma_chunk_f16(a[qb], b, kZero ? zero : acc[qb]);
   }
 }
 
@@ -452,8 +455,8 @@ __device__ __forceinline__ void load_afrags(const u32x4* __restrict__ lds, int s
 template <int DT, int D, int QB, int kRegs>
 constexpr int rega_ring() {
   constexpr int kNC = D / DTraits<DT>::kChunkDims;
-  const int per = 4 * kNC + 2;  // fragments and row ids of one row block
-  int nb = (kRegs - 4 * kNC * QB - 8 * QB - (kRegs > 256 ? 200 : 130)) / per;
+  const int per = 4 * kNC;  // fragments of one row block
+  int nb = (kRegs - 4 * kNC * QB - 8 * QB - (kRegs > 256 ? 120 : 130)) / per;
   nb = nb > 8 ? 8 : nb;
   nb &= ~1;
   return nb < 2 ? 2 : nb;
@@ -461,21 +464,18 @@ constexpr int rega_ring() {
 
 // Stream rows [r0, r1) through the block's waves (wave w takes row blocks w,
 // w + W, ...) against the register-held fragments qf.  Per 16-row block:
-// any = vote(acc, row) (straight-line vector work, wave-uniform result
-// through a ballot), then cand(acc, row, any, rid) when any lane voted.  row
-// = the stored row of this lane's column (it may be >= r1 on the last block;
-// loads are clamped) and rid = ids[row] (clamped likewise), loaded with the
-// block's fragments so that the epilogue never waits on it.  Chunks are
+// vote(acc, row), a wave-uniform test computed with straight-line vector
+// work, then cand(acc, row) when it holds.  row = the stored row of this
+// lane's column; it is >= r1 on the last block and on padding blocks (loads
+// are clamped), and the vote then fails.  Chunks are
 // multiplied in ascending order into each accumulator, as in score_regs: the
 // same bits.  The vote of block b is issued between the MFMAs of block
-// b + W (two accumulator sets, interleaving hints), so that its vector work
-// runs under them; one step past the last block multiplies a clamped block
-// whose result is never used, which keeps every step one basic block.
+// b + W (two accumulator sets, interleaving hints), so that it runs under
+// them.
 template <int DT, int D, int QB, int kRegs, typename Vote, typename Cand>
 __device__ __forceinline__ void stream_rows_rega(const u32x4 (&qf)[D / DTraits<DT>::kChunkDims][QB],
                                                  const char* __restrict__ base, size_t row_bytes,
-                                                 const int64_t* __restrict__ ids, int64_t r0,
-                                                 int64_t r1, Vote& vote, Cand& cand) {
+                                                 int64_t r0, int64_t r1, Vote& vote, Cand& cand) {
   constexpr int kNC = D / DTraits<DT>::kChunkDims;
   constexpr int NB = rega_ring<DT, D, QB, kRegs>();
   const int wave = wave_id();
@@ -483,24 +483,15 @@ __device__ __forceinline__ void stream_rows_rega(const u32x4 (&qf)[D / DTraits<D
   const int r16 = threadIdx.x & 15;
   const RowStream rs = {base + (size_t)r0 * row_bytes, (int)(r1 - r0), (uint32_t)row_bytes};
   const int nrows = rs.nrows;
-  const int64_t* idb = ids + r0;
   auto load = [&](int blk, u32x4(&dst)[kNC]) {
     const char* p = rs.seg_ptr(blk);
 #pragma unroll
     for (int c = 0; c < kNC; ++c) dst[c] = *(const u32x4*)(p + 64 * c);
   };
-  // Row ids ride one step behind the rows: the id of block b is read by the
-  // epilogue one step after its MFMAs, so its slot is refilled (with block
-  // b + NB) only after that read.  Sharing the row slot instead would keep two
-  // ids of one slot alive at once, and the register allocator then rotates
-  // the ring with copies at the loop latch, each copy a wait on its load.
   u32x4 buf[NB][kNC];
-  int64_t rid[NB];
   if (nrows <= 0 || wave * 16 >= nrows) return;
 #pragma unroll
   for (int j = 0; j < NB - 1; ++j) load(wave + j * nwaves, buf[j]);
-#pragma unroll
-  for (int j = 0; j < NB - 2; ++j) rid[j] = idb[rs.lane_row(wave + j * nwaves)];
   __builtin_amdgcn_sched_barrier(0);
   __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);  // see stream_rows_sliced
   __builtin_amdgcn_sched_barrier(0);
@@ -508,45 +499,38 @@ __device__ __forceinline__ void stream_rows_rega(const u32x4 (&qf)[D / DTraits<D
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) acc[1][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
   int rb = wave;
-  bool have_prev = false;
-  int64_t prev_row = 0;
+  int64_t prev_row = r1;  // no block before the first
   // One step per row block of this wave, plus one that only runs the last
-  // block's epilogue.  Steps are expanded NB at a time at compile time, so
-  // that every ring and accumulator index is a constant (a runtime index would
-  // put them in scratch); the loop over whole trips has no exit inside, and
-  // the remaining steps follow it.  An exit path inside the trip would join
-  // the loop header with its own pending loads, and the compiler's wait
-  // counts there would turn conservative (a near drain of the ring per trip).
+  // block's vote, rounded up to whole trips of NB steps: the steps past the
+  // end multiply clamped rows whose vote is empty.  Steps are expanded NB at
+  // a time at compile time, so that every ring and accumulator index is a
+  // constant (a runtime index would put them in scratch), and the loop has no
+  // exit inside a trip: an exit path would join the loop header with its own
+  // pending loads, and the compiler's wait counts there would turn
+  // conservative (a near drain of the ring per trip).
   auto step = [&](auto jc) {
     constexpr int j = decltype(jc)::value;
     constexpr int cur = j & 1, prv = cur ^ 1;  // NB is even
-    const int64_t rid_prev = rid[(j + NB - 1) % NB];
     load(rb + (NB - 1) * nwaves, buf[(j + NB - 1) % NB]);
-    rid[(j + NB - 2) % NB] = idb[rs.lane_row(rb + (NB - 2) * nwaves)];
+    // chunk 0 starts each accumulator from zero (an inline constant operand)
+    mma_chunk_qb<DT, QB, true>(qf[0], buf[j][0], acc[cur]);
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) acc[cur][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int c = 0; c < kNC; ++c) mma_chunk_qb<DT, QB>(qf[c], buf[j][c], acc[cur]);
-    const bool any = have_prev && vote(acc[prv], prev_row);
-    const bool some = __ballot(any) != 0;
+    for (int c = 1; c < kNC; ++c) mma_chunk_qb<DT, QB>(qf[c], buf[j][c], acc[cur]);
+    const bool some = vote(acc[prv], prev_row);
     // loads first, then the MFMAs with the previous block's vote in between
-    __builtin_amdgcn_sched_group_barrier(0x020, kNC + 1, 0);  // VMEM reads
+    __builtin_amdgcn_sched_group_barrier(0x020, kNC, 0);  // VMEM reads
 #pragma unroll
     for (int x = 0; x < kNC * QB; ++x) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-      __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);  // three VALU
+      __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);  // one VALU
     }
-    if (some) cand(acc[prv], prev_row, any, rid_prev);
-    have_prev = true;
+    if (some) cand(acc[prv], prev_row);
     prev_row = r0 + rb * 16 + r16;
     rb += nwaves;
   };
   const int nsteps = ((nrows + 15) / 16 - wave + nwaves - 1) / nwaves + 1;
-  for (int t = nsteps / NB; t > 0; --t) unroll_steps(step, std::make_integer_sequence<int, NB>{});
-  const int rem = nsteps % NB;
-  unroll_steps([&](auto jc) {
-    if (decltype(jc)::value < rem) step(jc);
-  }, std::make_integer_sequence<int, NB>{});
+  for (int t = (nsteps + NB - 1) / NB; t > 0; --t)
+    unroll_steps(step, std::make_integer_sequence<int, NB>{});
 }
 
 // Largest number of 16-query blocks a tile of compile-time dimension D can

@@ -119,11 +119,13 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
   __shared__ int64_t s_ex[2][kTileQ];
   __shared__ int32_t s_hits[kTileQ];  // qualifying rows per staged query in this tile
   __shared__ int32_t s_over[kTileQ];  // staged queries whose candidates overflowed
+  __shared__ int32_t s_lost[kTileQ];  // their qualifying rows the full arena did not take
   __shared__ int32_t s_sel[kTileQ];   // staged queries selected from slots + spill
   __shared__ int32_t s_soff[kTileQ];  // their segment in the sorted spill
   __shared__ int32_t s_scur[kTileQ];
   __shared__ int32_t s_poff[kTileQ];  // their first pool entry (after the tile's base)
-  __shared__ int32_t s_pool_n, s_over_n, s_sel_n, s_rbase, s_spill_n, s_spill_ovf;
+  __shared__ int32_t s_pool_n, s_over_n, s_sel_n, s_rbase;
+  __shared__ int32_t s_wcnt[kNT / 64];  // pairs each wave appended in this tile
   __shared__ unsigned long long s_pbase;
   // per work-group: the arena's global extension (spill_cap entries), then
   // the tile's whole arena grouped by query (LDS part and extension)
@@ -131,6 +133,12 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
   TileSpill* const arena_srt = arena_g + a.spill_cap;
   TileSpill* s_arena = (TileSpill*)(lds + a.cand_u4);  // [arena_lds]
   const int arena_lds = a.arena_lds;
+  // Each wave appends to a private part of the arena (no atomics): wcap
+  // entries in LDS, then gcap in the global extension.
+  const int nwv = (int)(blockDim.x >> 6);
+  const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int wcap = arena_lds / nwv, gcap = a.spill_cap / nwv;
+  int wcnt = 0;  // this wave's pairs in the running tile (uniform)
 
   const int d = D > 0 ? D : a.d;
   const RowGeom<DT> g = RowGeom<DT>::make(d);
@@ -204,10 +212,11 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
     s_pool_n = 0;
     s_over_n = 0;
     s_sel_n = 0;
-    s_spill_n = 0;
-    s_spill_ovf = 0;
   }
-  if (threadIdx.x < kTileQ) s_hits[threadIdx.x] = 0;
+  if (threadIdx.x < kTileQ) {
+    s_hits[threadIdx.x] = 0;
+    s_lost[threadIdx.x] = 0;
+  }
   __syncthreads();
   int t = s_first[0], tn = s_first[1], ta = s_first[2], tb = s_first[3];
   Tile recT = load_rec(t), recN = load_rec(tn), recA = load_rec(ta);
@@ -243,74 +252,98 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
 #pragma unroll
     for (int r = 0; r < 4; ++r)
       thr_last[r] = ((qb_n - 1) * 16 + 4 * h + r) < nq ? tau : INFINITY;
-    // tau test: one wave-wide vote in the common (no candidate) case; full
-    // query blocks through a max tree, the last one per row
+    // tau test of a row block, true (wave-uniform) when some lane's row
+    // scores at least tau against some staged query: full query blocks
+    // through a max tree, the last one (which may hold padding queries, with
+    // threshold +inf) element by element.  Rows past r1 get threshold +inf.
     auto vote = [&](const auto& acc, int64_t row) -> bool {
       constexpr int QB = sizeof(acc) / sizeof(acc[0]);
+      const float tr = row < r1 ? tau : INFINITY;
       float mx = -INFINITY;
 #pragma unroll
       for (int qb = 0; qb + 1 < QB; ++qb) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) mx = fmaxf(mx, acc[qb][r]);
       }
-      bool any = mx >= tau;
+      bool any = mx >= tr;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) any |= acc[QB - 1][r] >= thr_last[r];
-      return any && (row < r1);
+      for (int r = 0; r < 4; ++r) any |= acc[QB - 1][r] >= fmaxf(tr, thr_last[r]);
+      return __ballot(any) != 0ull;
     };
-    // Qualifying pairs of the row block (any: this lane's column may hold one;
-    // rid: the column's row id, for the self-exclusion).  The per-(query
-    // block, row) tests are folded into one bit mask per lane, and a loop
-    // (not unrolled: one copy of its code) visits only the (block, row) pairs
-    // that hold a candidate.
-    auto candidates = [&](const auto& acc, int64_t row, bool any, int64_t rid) {
+    // Qualifying pairs of the row block go to the wave's part of the arena as
+    // (score, row offset, staged query): lanes fill a run of slots in lane
+    // order (an exclusive prefix of their counts, bit plane by bit plane), each
+    // with its own pairs in (query block, element) order.  The common case
+    // (the run fits the LDS part) is straight-line code with LDS stores only.
+    // The self-exclusion is left to the end of the tile, except for pairs the
+    // full arena cannot take: those are counted per query, own row excluded,
+    // and the query's exact top k is recomputed by the heavy pass.
+    auto candidates = [&](const auto& acc, int64_t row) {
       constexpr int QB = sizeof(acc) / sizeof(acc[0]);
-      const int r16 = lane & 15;
+      const float tr = row < r1 ? tau : INFINITY;
       const uint32_t roff = (uint32_t)(row - r0);
-      uint32_t lm = 0;
+      auto pass = [&](int qb, int r) {
+        return acc[qb][r] >= (qb + 1 < QB ? tr : fmaxf(tr, thr_last[r]));
+      };
+      int cnt = 0;
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float thr = qb + 1 < QB ? tau : thr_last[r];
-          lm |= (uint32_t)(any && acc[qb][r] >= thr) << (qb * 4 + r);
-        }
+        for (int r = 0; r < 4; ++r) cnt += pass(qb, r) ? 1 : 0;
       }
-      uint32_t wm = lm;
-      for (int o = 32; o > 0; o >>= 1) wm |= (uint32_t)__shfl_xor((int)wm, o);
-      wm = __builtin_amdgcn_readfirstlane(wm);
-      while (wm) {
-        const int x = __builtin_ctz(wm);
-        wm &= wm - 1;
-        const int i = (x >> 2) * 16 + 4 * h + (x & 3);  // staged query of this lane's group
-        const float sc = pick_score(acc, x);
-        const bool hit = ((lm >> x) & 1u) && rid != sex[i];  // self-exclusion
-        const unsigned long long mask = __ballot(hit);
-        if (mask == 0) continue;
-        // per query (lane group) count, and the arena slots of the whole vote
-        const uint32_t gm = (uint32_t)(mask >> (16 * h)) & 0xffffu;
-        if (r16 == 0 && gm) atomicAdd(&s_hits[i], __popc(gm));
-        const int lead = __ffsll((long long)mask) - 1;
-        int ab = 0;
-        if (lane == lead) ab = atomicAdd(&s_spill_n, __popcll(mask));
-        ab = __shfl(ab, lead);
-        if (hit) {
-          const int pos = ab + __popcll(mask & ((1ull << lane) - 1ull));
-          const TileSpill ent{sc, roff | ((uint32_t)i << kSpillRowBits)};
-          if (pos < arena_lds)
-            s_arena[pos] = ent;
-          else if (pos - arena_lds < a.spill_cap)
-            arena_g[pos - arena_lds] = ent;
-          else
-            s_spill_ovf = 1;
-        }
+      int pre = 0, tot = 0;  // cnt <= 32: six bit planes
+#pragma unroll
+      for (int b = 0; b < 6; ++b) {
+        const unsigned long long m = __ballot((cnt >> b) & 1);
+        pre += (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                              __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u)) << b;
+        tot += __popcll(m) << b;
       }
+      int pos = wcnt + pre;
+      if (wcnt + tot <= wcap) {
+        TileSpill* const dst = s_arena + wv * wcap;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const bool ok = pass(qb, r);
+            if (ok)
+              dst[pos] = TileSpill{acc[qb][r],
+                                   roff | ((uint32_t)(qb * 16 + 4 * h + r) << kSpillRowBits)};
+            pos += ok ? 1 : 0;
+          }
+        }
+      } else {
+        // past the LDS part: the global part, then per-query counts
+        uint32_t lm = 0;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) lm |= (pass(qb, r) ? 1u : 0u) << (qb * 4 + r);
+        }
+        while (lm) {
+          const int x = __builtin_ctz(lm);
+          lm &= lm - 1;
+          const int i = (x >> 2) * 16 + 4 * h + (x & 3);
+          const TileSpill ent{pick_score(acc, x), roff | ((uint32_t)i << kSpillRowBits)};
+          if (pos < wcap)
+            s_arena[wv * wcap + pos] = ent;
+          else if (pos - wcap < gcap)
+            arena_g[wv * gcap + pos - wcap] = ent;
+          else if (a.ids[row] != sex[i])
+            atomicAdd(&s_lost[i], 1);
+          ++pos;
+        }
+        // Its global accesses complete here: a store left pending would make
+        // the compiler wait for every load of the row stream, not just the
+        // oldest.
+        __builtin_amdgcn_s_waitcnt(0);
+      }
+      wcnt += tot;
     };
-    // epilogue of the LDS-staged streams (the row id is loaded here)
+    // epilogue of the LDS-staged streams
     auto epi = [&](const auto& acc, int64_t row) {
-      const bool any = vote(acc, row);
-      if (__ballot(any) == 0) return;
-      candidates(acc, row, any, a.ids[row < r1 ? row : r1 - 1]);
+      if (vote(acc, row)) candidates(acc, row);
     };
 
     if constexpr (kMode == kStageRegA) {
@@ -322,12 +355,15 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
         __builtin_amdgcn_s_waitcnt(0);  // fragments in registers
         __syncthreads();  // every wave has its fragments: the staging buffer is free
         if (threadIdx.x == 0) t_claim = claim();  // published at the end of this tile
-        if (tn >= 0) dma_stage<DT>(lds, g, qbase, row_bytes, s_q[nset], recN.nq);
         // pipeline loads, used one tile from now
         itA = load_items(recA);
         recB = load_rec(tb);
         stream_rows_rega<DT, D, QB, kOcc == 1 ? 512 : 256>(qf, (const char*)a.vectors, row_bytes,
-                                                            a.ids, r0, r1, vote, candidates);
+                                                            r0, r1, vote, candidates);
+        // The next tile's queries are staged after the stream, under the end
+        // of this tile: an LDS-DMA load in flight during the stream makes the
+        // compiler wait for every load there, not just the oldest ones.
+        if (tn >= 0) dma_stage<DT>(lds, g, qbase, row_bytes, s_q[nset], recN.nq);
       });
     } else {
       __syncthreads();
@@ -348,28 +384,74 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
       stream_rows<DT, D, 8, kNT == kScanThreads ? 80 : 150>(
           buf, g, (const char*)a.vectors, row_bytes, r0, r1, qb_n, epi);
     }
+    if (lane == 0) s_wcnt[wv] = wcnt;
+    wcnt = 0;
     // this wave's staging copies and arena stores are complete (in L2)
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();  // every wave is done with this tile's queries, items and candidates
+    // the arena's parts: pairs held per wave, their prefix; any global part?
+    int wn[kNT / 64], wpre[kNT / 64 + 1];
+    bool ext = false;
+    wpre[0] = 0;
+#pragma unroll
+    for (int w = 0; w < kNT / 64; ++w) {
+      const int cw = w < nwv ? s_wcnt[w] : 0;
+      wn[w] = min(cw, wcap + gcap);
+      ext |= cw > wcap;
+      wpre[w + 1] = wpre[w] + wn[w];
+    }
     // Candidates in the arena's global extension were stored by other waves of
     // the work-group: an acquire at agent scope invalidates the CU's vector L1,
     // whose lines of that area may be stale (read in an earlier tile).
-    if (s_spill_n > arena_lds) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    if (ext) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 
-    // End of the tile.  Per staged query: the hit flag; then its candidates to
-    // the pool (all of them, or its exact top k when it has more), or, when
-    // the arena overflowed, a heavy record for the exact top-k pass.
-    const bool arena_ok = s_spill_ovf == 0;  // block-uniform
+    // End of the tile.  The arena's pairs are counted per staged query, each
+    // query's own row excluded (a pair whose row id is the query's excluded
+    // id); four pairs per thread are in flight at once.
+    const int na = wpre[kNT / 64];  // pairs the arena holds
+    auto arena_at = [&](int e) -> TileSpill {
+      int w = 0;
+#pragma unroll
+      for (int u = 1; u < kNT / 64; ++u) w += e >= wpre[u] ? 1 : 0;
+      const int ew = e - wpre[w];
+      return ew < wcap ? s_arena[w * wcap + ew] : arena_g[w * gcap + ew - wcap];
+    };
+    auto excluded = [&](const TileSpill& ts, int64_t id) {
+      return id == sex[ts.rowq >> kSpillRowBits];
+    };
+    auto row_id = [&](const TileSpill& ts) -> int64_t {
+      return a.ids[r0 + (ts.rowq & ((1u << kSpillRowBits) - 1u))];
+    };
+    for (int e0 = threadIdx.x; e0 < na; e0 += 4 * (int)blockDim.x) {
+      TileSpill ts[4];
+      int64_t id[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int e = e0 + u * (int)blockDim.x;
+        ts[u] = arena_at(e < na ? e : e0);
+        id[u] = row_id(ts[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (e0 + u * (int)blockDim.x < na && !excluded(ts[u], id[u]))
+          atomicAdd(&s_hits[ts[u].rowq >> kSpillRowBits], 1);
+    }
+    __syncthreads();
+
+    // Per staged query: the hit flag; then its candidates to the pool (all of
+    // them, or its exact top k when it has more), or, when the arena could not
+    // take all of them, a heavy record for the exact top-k pass.
     int c = 0, keep = 0;
     if ((int)threadIdx.x < nq) {
+      const int lost = s_lost[threadIdx.x];
       c = s_hits[threadIdx.x];
-      if (c > 0) {
+      if (c + lost > 0) {
         const int q = sq[threadIdx.x];
         const int rk = srank[threadIdx.x];
         atomicMax(&a.lmax[q], rk + 1);
         if (a.hitbits)
           atomicOr(&a.hitbits[(int64_t)q * a.hit_words + (rk >> 5)], 1u << (rk & 31));
-        if (arena_ok) {
+        if (lost == 0) {
           keep = min(c, a.k);
           s_poff[threadIdx.x] = atomicAdd(&s_pool_n, keep);
           atomicAdd(&a.hcount[q], keep);
@@ -378,6 +460,7 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
           s_over[atomicAdd(&s_over_n, 1)] = threadIdx.x;
         }
       }
+      c += lost;
     }
     {
       // qualifying pairs of the tile, for the statistics: one add per wave
@@ -417,10 +500,11 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
         }
       }
       if (pool_n > 0) {
-        // group the arena by staged query (counting sort into the sorted area)
-        const int na = s_spill_n;
+        // group the arena by staged query (counting sort into the sorted
+        // area), own rows left out
         for (int e = threadIdx.x; e < na; e += blockDim.x) {
-          const TileSpill ts = e < arena_lds ? s_arena[e] : arena_g[e - arena_lds];
+          const TileSpill ts = arena_at(e);
+          if (excluded(ts, row_id(ts))) continue;
           const int qs = (int)(ts.rowq >> kSpillRowBits);
           arena_srt[s_soff[qs] + atomicAdd(&s_scur[qs], 1)] = ts;
         }
@@ -430,7 +514,7 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
         __syncthreads();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         // queries with at most k candidates: all of them, one thread per query
-        if ((int)threadIdx.x < nq && c > 0 && c <= a.k) {
+        if ((int)threadIdx.x < nq && keep > 0 && c <= a.k) {
           const int i = threadIdx.x;
           const unsigned long long base = s_pbase + (unsigned long long)s_poff[i];
           const int32_t qv = a.hitbits ? (sq[i] | (srank[i] << kRankShift)) : sq[i];
@@ -481,14 +565,15 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
       }
     }
     __syncthreads();  // the counts and the spill are read; reset them for the next tile
-    if ((int)threadIdx.x < nq) s_hits[threadIdx.x] = 0;
+    if ((int)threadIdx.x < nq) {
+      s_hits[threadIdx.x] = 0;
+      s_lost[threadIdx.x] = 0;
+    }
     if (threadIdx.x == 0) {
       s_claim = t_claim;
       s_pool_n = 0;
       s_over_n = 0;
       s_sel_n = 0;
-      s_spill_n = 0;
-      s_spill_ovf = 0;
     }
     __syncthreads();
     t = tn;
