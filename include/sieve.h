@@ -245,6 +245,24 @@ SIEVE_API int sieve_rank(const sieve_index* idx, const void* queries, int64_t nq
                          int32_t* out_order, void* stream);
 
 /*
+ * sieve_rank_noalloc -- sieve_rank for callers that cannot allocate memory
+ * (code under stream capture, serving loops, harnesses that forbid device
+ * allocation): the same outputs, bit for bit, with no device or host
+ * allocation in the call.  Its workspace is a fixed 64 MiB device array of
+ * the library, one per GPU, kept until the process ends; queries are ranked
+ * in chunks that fit it.  Calls on one GPU share that array: calls that
+ * overlap in time on one GPU (on other streams or threads) race on it and
+ * must be serialised by the caller.  The call synchronises its stream once
+ * per attempt (as sieve_rank does) to read the tie-overflow flag.
+ *   Returns SIEVE_EUNSUPPORTED when one query's workspace (nlist * 4 bytes
+ *   on the screen path, about (min(nprobe, nlist) + 128) * 8 bytes on the
+ *   prefix path) does not fit the array, or on devices above 63; other
+ *   arguments, limits and errors as for sieve_rank.
+ */
+SIEVE_API int sieve_rank_noalloc(const sieve_index* idx, const void* queries, int64_t nq,
+                                 int32_t nprobe, int32_t* out_order, void* stream);
+
+/*
  * sieve_round_log -- per-round record of the last search call on this handle
  * that was given a stats pointer (for fixed probing, one record per query
  * chunk).  Diagnostics for the roofline of the partition scan: each record

@@ -106,6 +106,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sieve_round_log.argtypes = [P, ctypes.POINTER(Round), i32, ctypes.POINTER(ctypes.c_int32)]
     lib.sieve_rank.restype = ctypes.c_int
     lib.sieve_rank.argtypes = [P, P, i64, i32, P, P]
+    lib.sieve_rank_noalloc.restype = ctypes.c_int
+    lib.sieve_rank_noalloc.argtypes = [P, P, i64, i32, P, P]
     lib.sieve_free_index.restype = None
     lib.sieve_free_index.argtypes = [P]
     lib.sieve_last_error.restype = ctypes.c_char_p
@@ -204,6 +206,25 @@ class Index:
             _check(self._lib, self._lib.sieve_rank(self._h, queries.data_ptr(), nq, int(nprobe),
                                                    out.data_ptr(), _stream(stream)))
         return out[:, :n]
+
+    def rank_noalloc(self, queries: torch.Tensor, nprobe: int, out: torch.Tensor,
+                     stream=None) -> torch.Tensor:
+        """``sieve_rank_noalloc`` into a caller-provided ``out`` ([nq, min(nprobe, nlist)]
+        int32, contiguous, on the index's device); ``queries`` must already be contiguous in
+        the index's dtype.  Neither this wrapper nor the library allocates."""
+        n = min(int(nprobe), self.nlist)
+        nq = int(queries.shape[0])
+        if queries.dtype != self.dtype or not queries.is_contiguous() or queries.dim() != 2:
+            raise SieveError(-1, "queries must be a contiguous [nq, d] tensor of the index dtype")
+        if (out.dtype != torch.int32 or not out.is_contiguous()
+                or tuple(out.shape) != (nq, n) or out.device != queries.device):
+            raise SieveError(-1, f"out must be a contiguous int32 [{nq}, {n}] tensor on "
+                                 "the queries' device")
+        with torch.cuda.device(self.device):
+            _check(self._lib, self._lib.sieve_rank_noalloc(self._h, queries.data_ptr(), nq,
+                                                           int(nprobe), out.data_ptr(),
+                                                           _stream(stream)))
+        return out
 
     def round_log(self) -> list:
         """Per-round records (``Round``) of the last search on this index that collected

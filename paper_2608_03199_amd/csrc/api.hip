@@ -18,6 +18,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -348,34 +349,47 @@ bool use_prefix_path(const sieve_index* ix, int nsel, bool wide) {
 
 // Order the first nsel centroids of queries [q0, q0 + cnt) into rows of P
 // (row stride ldp), in chunks whose screen scores (or candidate lists) fit
-// their buffers.
-int rank_queries(sieve_index* ix, const void* queries, int64_t q0, int64_t cnt, int nsel,
-                 int64_t ldp, const SearchPlan& pl, int32_t* P, hipStream_t s) {
-  RoundCounters* rc = (RoundCounters*)ix->rc.p;
+// the given buffers: prefix path, chunks of chunk_prefix queries with
+// cand[chunk * rank_prefix_cap] and ccount[chunk]; screen path, chunks of
+// chunk_scores queries with scores[chunk * nlist].
+int rank_queries_in(const sieve_index* ix, const void* queries, int64_t q0, int64_t cnt, int nsel,
+                    int64_t ldp, const SearchPlan& pl, int32_t* P, RoundCounters* rc,
+                    unsigned long long* cand, int32_t* ccount, int64_t chunk_prefix,
+                    float* scores, int64_t chunk_scores, hipStream_t s) {
   if (use_prefix_path(ix, nsel, pl.wide_rank)) {
-    const int64_t cap = rank_prefix_cap(nsel, ix->nlist);
-    const int64_t chunk = cnt < (1 << 18) ? cnt : (1 << 18);
-    int st;
-    if ((st = ensure(ix->cand, (size_t)chunk * cap * sizeof(unsigned long long))) ||
-        (st = ensure(ix->ccount, (size_t)chunk * sizeof(int32_t))))
-      return st;
-    for (int64_t a = 0; a < cnt; a += chunk) {
-      const int32_t c = (int32_t)((cnt - a) < chunk ? (cnt - a) : chunk);
+    for (int64_t a = 0; a < cnt; a += chunk_prefix) {
+      const int32_t c = (int32_t)((cnt - a) < chunk_prefix ? (cnt - a) : chunk_prefix);
       HIP_TRY(launch_rank_prefix(ix->dtype, queries, q0 + a, c, ix->centroids, ix->nlist, ix->d,
-                                 nsel, ix->cmax, (unsigned long long*)ix->cand.p,
-                                 (int32_t*)ix->ccount.p, P + a * ldp, ldp, rc, s));
+                                 nsel, ix->cmax, cand, ccount, P + a * ldp, ldp, rc, s));
     }
     return SIEVE_OK;
   }
-  for (int64_t a = 0; a < cnt; a += pl.rank_chunk) {
-    const int32_t c = (int32_t)((cnt - a) < pl.rank_chunk ? (cnt - a) : pl.rank_chunk);
+  for (int64_t a = 0; a < cnt; a += chunk_scores) {
+    const int32_t c = (int32_t)((cnt - a) < chunk_scores ? (cnt - a) : chunk_scores);
     HIP_TRY(launch_rank_scores(ix->dtype, queries, q0 + a, c, ix->centroids, ix->nlist, ix->d,
-                               (float*)ix->scores.p, s));
+                               scores, s));
     HIP_TRY(launch_rank_select(ix->dtype, queries, q0 + a, c, ix->centroids, ix->nlist, ix->d,
-                               (const float*)ix->scores.p, nsel, ix->cmax, P + a * ldp, ldp, rc,
-                               pl.wide_rank, s));
+                               scores, nsel, ix->cmax, P + a * ldp, ldp, rc, pl.wide_rank, s));
   }
   return SIEVE_OK;
+}
+
+// rank_queries_in with the index's own workspace (grown as needed).
+int rank_queries(sieve_index* ix, const void* queries, int64_t q0, int64_t cnt, int nsel,
+                 int64_t ldp, const SearchPlan& pl, int32_t* P, hipStream_t s) {
+  RoundCounters* rc = (RoundCounters*)ix->rc.p;
+  int64_t chunk_prefix = 1;
+  if (use_prefix_path(ix, nsel, pl.wide_rank)) {
+    const int64_t cap = rank_prefix_cap(nsel, ix->nlist);
+    chunk_prefix = cnt < (1 << 18) ? cnt : (1 << 18);
+    int st;
+    if ((st = ensure(ix->cand, (size_t)chunk_prefix * cap * sizeof(unsigned long long))) ||
+        (st = ensure(ix->ccount, (size_t)chunk_prefix * sizeof(int32_t))))
+      return st;
+  }
+  return rank_queries_in(ix, queries, q0, cnt, nsel, ldp, pl, P, rc,
+                         (unsigned long long*)ix->cand.p, (int32_t*)ix->ccount.p, chunk_prefix,
+                         (float*)ix->scores.p, pl.rank_chunk, s);
 }
 
 ScanArgs make_scan_args(sieve_index* ix, const void* queries, const int64_t* exclude,
@@ -1062,6 +1076,107 @@ SIEVE_API int sieve_rank(const sieve_index* idx, const void* queries, int64_t nq
     HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
     if (!ix->rc_host->rank_error) return SIEVE_OK;
+  }
+  return fail(SIEVE_EUNSUPPORTED,
+              "more than %d centroids tie within the fp32 screening bound at a rank boundary",
+              kMaxCand);
+}
+
+// ---- allocation-free ranking ---------------------------------------------
+// The workspace of sieve_rank_noalloc: a fixed device array, one copy per
+// GPU the library runs on, held until the process ends.  Every call on a GPU
+// uses that GPU's copy; calls that overlap in time on one GPU (other streams,
+// other threads) race on it.  In host code `scratch` only names the symbol:
+// kernels get its device address, looked up once per device.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+// Device address of this device's scratch (dev must be current).
+int scratch_address(int dev, unsigned char** out) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(SIEVE_EUNSUPPORTED, "device %d: the allocation-free entry point supports "
+                "devices 0..%d", dev, kMaxScratchDevices - 1);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(SIEVE_EDEVICE, "no device address for the scratch array");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = (unsigned char*)g_scratch_ptr[dev];
+  return SIEVE_OK;
+}
+}  // namespace
+
+SIEVE_API int sieve_rank_noalloc(const sieve_index* idx, const void* queries, int64_t nq,
+                                 int32_t nprobe, int32_t* out_order, void* stream) {
+  g_err.clear();
+  if (!idx) return fail(SIEVE_EINVAL, "index handle is NULL");
+  if (nq < 0) return fail(SIEVE_EINVAL, "nq is negative");
+  if (nprobe < 1) return fail(SIEVE_EINVAL, "nprobe = %d must be >= 1", nprobe);
+  if (nq > 0 && (!queries || !out_order))
+    return fail(SIEVE_EINVAL, "queries and out_order must be non-NULL when nq > 0");
+  if (nq > 0 && !aligned16(queries)) return fail(SIEVE_EINVAL, "queries must be 16-byte aligned");
+  if (nq > (int64_t)INT32_MAX / 2) return fail(SIEVE_EUNSUPPORTED, "nq too large");
+  const sieve_index* ix = idx;
+  SearchPlan pl;
+  int st;
+  if ((st = plan_search(ix, nq, 1, 0.f, 1, nprobe, 1, false, &pl))) return st;
+  if (nq == 0) return SIEVE_OK;
+  if ((int64_t)nq * pl.n > (int64_t)INT32_MAX * 8)
+    return fail(SIEVE_EUNSUPPORTED, "nq * nprobe too large");
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev != ix->device) return fail(SIEVE_EINVAL, "current device differs from the index's");
+  unsigned char* base = nullptr;
+  if ((st = scratch_address(dev, &base))) return st;
+  hipStream_t s = (hipStream_t)stream;
+  // scratch layout: the round counters, then the ranking workspace
+  constexpr size_t kHead = (sizeof(RoundCounters) + 255) & ~size_t(255);
+  RoundCounters* rc = (RoundCounters*)base;
+  unsigned char* ws = base + kHead;
+  const size_t ws_bytes = kScratchBytes - kHead;
+  for (int attempt = 0; attempt < 2; ++attempt) {
+    pl.wide_rank = attempt > 0;
+    // queries per chunk that fit the workspace
+    unsigned long long* cand = nullptr;
+    int32_t* ccount = nullptr;
+    float* scores = nullptr;
+    int64_t chunk_prefix = 1, chunk_scores = 1;
+    if (use_prefix_path(ix, pl.n, pl.wide_rank)) {
+      const size_t per = (size_t)rank_prefix_cap(pl.n, ix->nlist) * sizeof(unsigned long long) +
+                         sizeof(int32_t);
+      const int64_t fit = (int64_t)((ws_bytes - 256) / per);
+      if (fit < 1)
+        return fail(SIEVE_EUNSUPPORTED, "one query's ranking workspace (%zu bytes) exceeds the "
+                    "%zu-byte scratch of the allocation-free entry point", per, ws_bytes - 256);
+      chunk_prefix = std::min<int64_t>({fit, nq, int64_t(1) << 18});
+      cand = (unsigned long long*)ws;
+      ccount = (int32_t*)(ws + (((size_t)chunk_prefix * rank_prefix_cap(pl.n, ix->nlist) *
+                                 sizeof(unsigned long long) + 255) & ~size_t(255)));
+    } else {
+      const size_t per = (size_t)ix->nlist * sizeof(float);
+      const int64_t fit = (int64_t)(ws_bytes / per);
+      if (fit < 1)
+        return fail(SIEVE_EUNSUPPORTED, "one query's ranking workspace (%zu bytes) exceeds the "
+                    "%zu-byte scratch of the allocation-free entry point", per, ws_bytes);
+      chunk_scores = std::min<int64_t>({fit, nq, pl.rank_chunk});
+      scores = (float*)ws;
+    }
+    HIP_TRY(launch_zero_bytes(rc, sizeof(RoundCounters), s));
+    if ((st = rank_queries_in(ix, queries, 0, nq, pl.n, pl.n, pl, out_order, rc, cand, ccount,
+                              chunk_prefix, scores, chunk_scores, s)))
+      return st;
+    int32_t rank_error = 0;  // pageable host memory: the copy allocates nothing here
+    HIP_TRY(hipMemcpyAsync(&rank_error, &rc->rank_error, sizeof(rank_error),
+                           hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    if (!rank_error) return SIEVE_OK;
   }
   return fail(SIEVE_EUNSUPPORTED,
               "more than %d centroids tie within the fp32 screening bound at a rank boundary",
