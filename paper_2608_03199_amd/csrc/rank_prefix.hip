@@ -292,6 +292,12 @@ __global__ __launch_bounds__(kQRWaves * 64, 1) void rank_prefix_qreg_kernel(
     };
 #pragma unroll
     for (int u = 0; u < kQRRing - 1; ++u) load(mem + u * kQRSplit, buf[u]);
+    // Wait for the prologue here: with loads of the prologue (or from before
+    // it) still pending where the loop is entered, the compiler's load waits
+    // at the top of each ring round are for every load, not just the oldest.
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    __builtin_amdgcn_sched_barrier(0);
     const int mine = mem < nb ? (nb - mem + kQRSplit - 1) / kQRSplit : 0;
     const int rounds = (mine + kQRRing - 1) / kQRRing;
     int blk = mem;

@@ -271,27 +271,50 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
       return __ballot(any) != 0ull;
     };
     // Qualifying pairs of the row block go to the wave's part of the arena as
-    // (score, row offset, staged query): lanes fill a run of slots in lane
-    // order (an exclusive prefix of their counts, bit plane by bit plane), each
-    // with its own pairs in (query block, element) order.  The common case
-    // (the run fits the LDS part) is straight-line code with LDS stores only.
-    // The self-exclusion is left to the end of the tile, except for pairs the
-    // full arena cannot take: those are counted per query, own row excluded,
-    // and the query's exact top k is recomputed by the heavy pass.
+    // (score, row offset, staged query), in (query block, element, lane)
+    // order.  Each (query block, element) is one vector compare into a lane
+    // mask; a scalar branch skips it when no lane qualifies, else the lanes of
+    // the mask take consecutive slots (LDS stores only).  The cost follows the
+    // qualifying (block, element) pairs, not the lanes.  When the run could
+    // reach past the LDS part, a slower path also covers the global part and,
+    // past that, counts per query the pairs the arena cannot take (own row
+    // excluded) for the heavy pass; its global accesses complete before it
+    // returns (a store left pending would make the compiler wait for every
+    // load of the row stream, not just the oldest).  The self-exclusion is
+    // otherwise left to the end of the tile.
     auto candidates = [&](const auto& acc, int64_t row) {
       constexpr int QB = sizeof(acc) / sizeof(acc[0]);
       const float tr = row < r1 ? tau : INFINITY;
       const uint32_t roff = (uint32_t)(row - r0);
-      auto pass = [&](int qb, int r) {
-        return acc[qb][r] >= (qb + 1 < QB ? tr : fmaxf(tr, thr_last[r]));
-      };
-      int cnt = 0;
+      auto thr = [&](int qb, int r) { return qb + 1 < QB ? tr : fmaxf(tr, thr_last[r]); };
+      if (wcnt + 64 * 4 * QB <= wcap) {
+        TileSpill* const dst = s_arena + wv * wcap;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const bool ok = acc[qb][r] >= thr(qb, r);
+            const unsigned long long m = __ballot(ok);
+            if (m == 0ull) continue;
+            if (ok) {
+              const int pos = wcnt + (int)__builtin_amdgcn_mbcnt_hi(
+                                         (uint32_t)(m >> 32),
+                                         __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+              dst[pos] = TileSpill{acc[qb][r],
+                                   roff | ((uint32_t)(qb * 16 + 4 * h + r) << kSpillRowBits)};
+            }
+            wcnt += __popcll(m);
+          }
+        }
+        return;
+      }
+      uint32_t lm = 0;
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) cnt += pass(qb, r) ? 1 : 0;
+        for (int r = 0; r < 4; ++r) lm |= (acc[qb][r] >= thr(qb, r) ? 1u : 0u) << (qb * 4 + r);
       }
-      int pre = 0, tot = 0;  // cnt <= 32: six bit planes
+      int cnt = __popc(lm), pre = 0, tot = 0;  // cnt <= 32: six bit planes
 #pragma unroll
       for (int b = 0; b < 6; ++b) {
         const unsigned long long m = __ballot((cnt >> b) & 1);
@@ -300,45 +323,20 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
         tot += __popcll(m) << b;
       }
       int pos = wcnt + pre;
-      if (wcnt + tot <= wcap) {
-        TileSpill* const dst = s_arena + wv * wcap;
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const bool ok = pass(qb, r);
-            if (ok)
-              dst[pos] = TileSpill{acc[qb][r],
-                                   roff | ((uint32_t)(qb * 16 + 4 * h + r) << kSpillRowBits)};
-            pos += ok ? 1 : 0;
-          }
-        }
-      } else {
-        // past the LDS part: the global part, then per-query counts
-        uint32_t lm = 0;
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) lm |= (pass(qb, r) ? 1u : 0u) << (qb * 4 + r);
-        }
-        while (lm) {
-          const int x = __builtin_ctz(lm);
-          lm &= lm - 1;
-          const int i = (x >> 2) * 16 + 4 * h + (x & 3);
-          const TileSpill ent{pick_score(acc, x), roff | ((uint32_t)i << kSpillRowBits)};
-          if (pos < wcap)
-            s_arena[wv * wcap + pos] = ent;
-          else if (pos - wcap < gcap)
-            arena_g[wv * gcap + pos - wcap] = ent;
-          else if (a.ids[row] != sex[i])
-            atomicAdd(&s_lost[i], 1);
-          ++pos;
-        }
-        // Its global accesses complete here: a store left pending would make
-        // the compiler wait for every load of the row stream, not just the
-        // oldest.
-        __builtin_amdgcn_s_waitcnt(0);
+      while (lm) {
+        const int x = __builtin_ctz(lm);
+        lm &= lm - 1;
+        const int i = (x >> 2) * 16 + 4 * h + (x & 3);
+        const TileSpill ent{pick_score(acc, x), roff | ((uint32_t)i << kSpillRowBits)};
+        if (pos < wcap)
+          s_arena[wv * wcap + pos] = ent;
+        else if (pos - wcap < gcap)
+          arena_g[wv * gcap + pos - wcap] = ent;
+        else if (a.ids[row] != sex[i])
+          atomicAdd(&s_lost[i], 1);
+        ++pos;
       }
+      __builtin_amdgcn_s_waitcnt(0);
       wcnt += tot;
     };
     // epilogue of the LDS-staged streams
@@ -474,13 +472,23 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
       if (threadIdx.x == 0) {
         s_pbase = pool_n ? atomicAdd(a.pool_count, (unsigned long long)pool_n) : 0ull;
         s_rbase = over_n ? atomicAdd(&a.rc->heavy, (over_n + kHeavyQ - 1) / kHeavyQ) : 0;
-        // segments of the grouped arena, by staged query
-        int run = 0;
-        for (int i = 0; i < nq; ++i) {
-          s_soff[i] = run;
-          s_scur[i] = 0;
-          run += s_hits[i];
+      }
+      if ((int)threadIdx.x < nq) s_scur[threadIdx.x] = 0;
+      // segments of the sorted area, for the queries with more than k pairs
+      // only (wave 0: an exclusive prefix over s_sel, two entries per lane)
+      if (sel_n > 0 && threadIdx.x < 64) {
+        const int j0 = 2 * lane, j1 = 2 * lane + 1;
+        const int v0 = j0 < sel_n ? s_hits[s_sel[j0]] : 0;
+        const int v1 = j1 < sel_n ? s_hits[s_sel[j1]] : 0;
+        int inc = v0 + v1;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int t = __shfl_up(inc, o);
+          if (lane >= o) inc += t;
         }
+        const int ex = inc - v0 - v1;
+        if (j0 < sel_n) s_soff[s_sel[j0]] = ex;
+        if (j1 < sel_n) s_soff[s_sel[j1]] = ex + v0;
       }
       __syncthreads();
       if ((int)threadIdx.x < over_n) {
@@ -500,66 +508,77 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
         }
       }
       if (pool_n > 0) {
-        // group the arena by staged query (counting sort into the sorted
-        // area), own rows left out
-        for (int e = threadIdx.x; e < na; e += blockDim.x) {
-          const TileSpill ts = arena_at(e);
-          if (excluded(ts, row_id(ts))) continue;
-          const int qs = (int)(ts.rowq >> kSpillRowBits);
-          arena_srt[s_soff[qs] + atomicAdd(&s_scur[qs], 1)] = ts;
-        }
-        // the grouped area is read by other waves: stores complete, barrier,
-        // L1 invalidated (as above)
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        // queries with at most k candidates: all of them, one thread per query
-        if ((int)threadIdx.x < nq && keep > 0 && c <= a.k) {
-          const int i = threadIdx.x;
-          const unsigned long long base = s_pbase + (unsigned long long)s_poff[i];
-          const int32_t qv = a.hitbits ? (sq[i] | (srank[i] << kRankShift)) : sq[i];
-          for (int e = 0; e < c; ++e) {
-            const TileSpill ts = arena_srt[s_soff[i] + e];
-            if ((int64_t)(base + e) < a.pool_cap) {
-              Hit hv;
-              hv.score = ts.score;
-              hv.q = qv;
-              hv.id = a.ids[r0 + (ts.rowq & ((1u << kSpillRowBits) - 1u))];
-              a.pool[base + e] = hv;
-            }
+        // The arena's pairs, own rows and heavy queries left out: a query
+        // with at most k of them writes them to its pool segment directly;
+        // one with more groups them in the sorted area (counting sort) for
+        // the exact top-k merge below.  Four pairs per thread in flight.
+        const int k = a.k;
+        for (int e0 = threadIdx.x; e0 < na; e0 += 4 * (int)blockDim.x) {
+          TileSpill ts[4];
+          int64_t id[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int e = e0 + u * (int)blockDim.x;
+            ts[u] = arena_at(e < na ? e : e0);
+            id[u] = row_id(ts[u]);
           }
-        }
-        // queries with more: one wave merges the query's segment into its
-        // top k, 64 candidates at a time
-        const Cand none = {-INFINITY, 0x7fffffffffffffffll, -1};
-        for (int j = threadIdx.x >> 6; j < sel_n; j += blockDim.x >> 6) {
-          const int i = s_sel[j];
-          const int ci = s_hits[i];
-          Cand top = none;
-          for (int b0 = 0; b0 < ci; b0 += 64) {
-            Cand cnd = none;
-            if (b0 + lane < ci) {
-              const TileSpill ts = arena_srt[s_soff[i] + b0 + lane];
-              const uint32_t ro = ts.rowq & ((1u << kSpillRowBits) - 1u);
-              cnd = Cand{ts.score, (long long)a.ids[r0 + ro], 0};
-            }
-            cnd = wave_sort_desc<false>(cnd, lane);
-            if (b0 == 0) {
-              top = cnd;
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int qs = (int)(ts[u].rowq >> kSpillRowBits);
+            if (e0 + u * (int)blockDim.x >= na || id[u] == sex[qs] || s_lost[qs] > 0) continue;
+            const int ci = s_hits[qs];
+            const int slot = atomicAdd(&s_scur[qs], 1);
+            if (ci <= k) {
+              const unsigned long long pi = s_pbase + (unsigned long long)(s_poff[qs] + slot);
+              if ((int64_t)pi < a.pool_cap) {
+                Hit hv;
+                hv.score = ts[u].score;
+                hv.q = a.hitbits ? (sq[qs] | (srank[qs] << kRankShift)) : sq[qs];
+                hv.id = id[u];
+                a.pool[pi] = hv;
+              }
             } else {
-              const Cand rv = shfl_cand<false>(cnd, 63 - lane);  // top ++ reverse(cnd): bitonic
-              top = better(top, rv) ? top : rv;
-              top = wave_merge_desc<false>(top, lane);
+              arena_srt[s_soff[qs] + slot] = ts[u];
             }
           }
-          const int kk = min(ci, a.k);
-          const unsigned long long base = s_pbase + (unsigned long long)s_poff[i];
-          if (lane < kk && (int64_t)(base + lane) < a.pool_cap) {
-            Hit hv;
-            hv.score = top.s;
-            hv.q = a.hitbits ? (sq[i] | (srank[i] << kRankShift)) : sq[i];
-            hv.id = top.id;
-            a.pool[base + lane] = hv;
+        }
+        if (sel_n > 0) {
+          // the grouped area is read by other waves: stores complete,
+          // barrier, L1 invalidated (as above)
+          __builtin_amdgcn_s_waitcnt(0);
+          __syncthreads();
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+          // queries with more than k: one wave merges the query's segment
+          // into its top k, 64 pairs at a time
+          const Cand none = {-INFINITY, 0x7fffffffffffffffll, -1};
+          for (int j = threadIdx.x >> 6; j < sel_n; j += blockDim.x >> 6) {
+            const int i = s_sel[j];
+            const int ci = s_hits[i];
+            Cand top = none;
+            for (int b0 = 0; b0 < ci; b0 += 64) {
+              Cand cnd = none;
+              if (b0 + lane < ci) {
+                const TileSpill ts = arena_srt[s_soff[i] + b0 + lane];
+                cnd = Cand{ts.score, (long long)row_id(ts), 0};
+              }
+              cnd = wave_sort_desc<false>(cnd, lane);
+              if (b0 == 0) {
+                top = cnd;
+              } else {
+                const Cand rv = shfl_cand<false>(cnd, 63 - lane);  // top ++ reverse(cnd): bitonic
+                top = better(top, rv) ? top : rv;
+                top = wave_merge_desc<false>(top, lane);
+              }
+            }
+            const int kk = min(ci, k);
+            const unsigned long long base = s_pbase + (unsigned long long)s_poff[i];
+            if (lane < kk && (int64_t)(base + lane) < a.pool_cap) {
+              Hit hv;
+              hv.score = top.s;
+              hv.q = a.hitbits ? (sq[i] | (srank[i] << kRankShift)) : sq[i];
+              hv.id = top.id;
+              a.pool[base + lane] = hv;
+            }
           }
         }
       }
