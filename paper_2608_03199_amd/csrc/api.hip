@@ -268,7 +268,7 @@ int check_common(const sieve_index* ix, const void* queries, int64_t nq, int32_t
 int spill_cap(const sieve_index* ix) {
   if (ix->max_list >= ((int64_t)1 << kSpillRowBits)) return 0;
   // SIEVE_SPILL_CAP lowers it (tests of the overflow path)
-  return std::min(env_count("SIEVE_SPILL_CAP", 16384), 16384);
+  return std::min(env_count("SIEVE_SPILL_CAP", 16384), 16384) & ~1;  // even: see SrtEnt
 }
 // The candidate arena packs a row offset in 24 bits; SIEVE_ARENA = 0 turns it
 // off (every tile with candidates then takes the exact top-k pass; tests).

@@ -130,7 +130,7 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
   // per work-group: the arena's global extension (spill_cap entries), then
   // the tile's whole arena grouped by query (LDS part and extension)
   TileSpill* const arena_g = a.spill + (size_t)blockIdx.x * arena_block_entries(a.spill_cap);
-  TileSpill* const arena_srt = arena_g + a.spill_cap;
+  SrtEnt* const arena_srt = (SrtEnt*)(arena_g + a.spill_cap);
   TileSpill* s_arena = (TileSpill*)(lds + a.cand_u4);  // [arena_lds]
   const int arena_lds = a.arena_lds;
   // Each wave appends to a private part of the arena (no atomics): wcap
@@ -538,7 +538,7 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
                 a.pool[pi] = hv;
               }
             } else {
-              arena_srt[s_soff[qs] + slot] = ts[u];
+              arena_srt[s_soff[qs] + slot] = SrtEnt{ts[u].score, 0, id[u]};
             }
           }
         }
@@ -549,26 +549,30 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
           __syncthreads();
           __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
           // queries with more than k: one wave merges the query's segment
-          // into its top k, 64 pairs at a time
+          // into its top k, 64 pairs at a time (the next batch loads under
+          // this one's sort); a batch none of whose pairs reaches the k-th
+          // score kept so far cannot change the top k and is not sorted
           const Cand none = {-INFINITY, 0x7fffffffffffffffll, -1};
           for (int j = threadIdx.x >> 6; j < sel_n; j += blockDim.x >> 6) {
             const int i = s_sel[j];
             const int ci = s_hits[i];
-            Cand top = none;
-            for (int b0 = 0; b0 < ci; b0 += 64) {
-              Cand cnd = none;
-              if (b0 + lane < ci) {
-                const TileSpill ts = arena_srt[s_soff[i] + b0 + lane];
-                cnd = Cand{ts.score, (long long)row_id(ts), 0};
-              }
+            const SrtEnt* seg = arena_srt + s_soff[i];
+            auto fetch = [&](int b0) -> Cand {
+              if (b0 + lane >= ci) return none;
+              const SrtEnt se = seg[b0 + lane];
+              return Cand{se.score, (long long)se.id, 0};
+            };
+            Cand top = wave_sort_desc<false>(fetch(0), lane);
+            Cand nxt = fetch(64);
+            for (int b0 = 64; b0 < ci; b0 += 64) {
+              Cand cnd = nxt;
+              nxt = fetch(b0 + 64);
+              const Cand kth = shfl_cand<false>(top, k - 1);
+              if (__ballot(!better(kth, cnd)) == 0ull) continue;
               cnd = wave_sort_desc<false>(cnd, lane);
-              if (b0 == 0) {
-                top = cnd;
-              } else {
-                const Cand rv = shfl_cand<false>(cnd, 63 - lane);  // top ++ reverse(cnd): bitonic
-                top = better(top, rv) ? top : rv;
-                top = wave_merge_desc<false>(top, lane);
-              }
+              const Cand rv = shfl_cand<false>(cnd, 63 - lane);  // top ++ reverse(cnd): bitonic
+              top = better(top, rv) ? top : rv;
+              top = wave_merge_desc<false>(top, lane);
             }
             const int kk = min(ci, k);
             const unsigned long long base = s_pbase + (unsigned long long)s_poff[i];

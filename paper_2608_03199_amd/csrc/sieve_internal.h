@@ -122,11 +122,19 @@ struct HeavyRec {
 };
 
 // LDS arena entries at most.  A work-group's global area holds the arena's
-// extension (spill_cap entries) and the grouped copy of the whole arena (at
-// most kArenaLdsMax + spill_cap entries).
+// extension (spill_cap entries) and the grouped copy of the pairs of the
+// queries with more than k of them (at most kArenaLdsMax + spill_cap
+// entries, each with its row id: two TileSpill units).  spill_cap is even, so
+// the grouped copy is 16-byte aligned.
 constexpr int kArenaLdsMax = 12288;
+struct SrtEnt {
+  float score;
+  int32_t pad;
+  int64_t id;
+};
+static_assert(sizeof(SrtEnt) == 2 * sizeof(TileSpill), "grouped entries take two arena units");
 __host__ __device__ inline size_t arena_block_entries(int spill_cap) {
-  return 2 * (size_t)spill_cap + kArenaLdsMax;
+  return (size_t)spill_cap + 2 * ((size_t)spill_cap + kArenaLdsMax);
 }
 
 struct ScanArgs {
