@@ -284,8 +284,9 @@ static int one_query(const or_job* jb, int64_t qi, double* qd, int* order, doubl
     probes = s;
   }
 
-  /* MergeTopK over all accumulated local results. */
-  qsort(cv->v, (size_t)cv->len, sizeof(cand), cand_cmp);
+  /* MergeTopK over all accumulated local results (no call for an empty
+   * vector: its storage may be NULL, which qsort must not be given). */
+  if (cv->len > 1) qsort(cv->v, (size_t)cv->len, sizeof(cand), cand_cmp);
   int k = jb->k;
   /* the last returned slot may go either way: the best candidate left out
    * scores within the band of it */
@@ -428,7 +429,7 @@ static void* run_bf(void* arg) {
         break;
       }
     }
-    qsort(cv.v, (size_t)cv.len, sizeof(cand), cand_cmp);
+    if (cv.len > 1) qsort(cv.v, (size_t)cv.len, sizeof(cand), cand_cmp);
     for (int r = 0; r < jb->k; ++r) {
       jb->out_ids[qi * jb->k + r] = r < cv.len ? cv.v[r].id : -1;
       jb->out_scores[qi * jb->k + r] = r < cv.len ? cv.v[r].s : -INFINITY;

@@ -57,9 +57,18 @@ struct Buf {
   size_t bytes = 0;
 };
 
+// SIEVE_ALLOC_CAP (bytes) refuses any single workspace buffer above it with
+// SIEVE_ENOMEM before hipMalloc is called (tests of the out-of-memory path;
+// the buffer already held stays valid).
 int ensure(Buf& b, size_t bytes) {
   if (bytes == 0) bytes = 16;
   if (b.bytes >= bytes) return SIEVE_OK;
+  if (const char* cap = getenv("SIEVE_ALLOC_CAP")) {
+    const unsigned long long c = strtoull(cap, nullptr, 10);
+    if (c > 0 && bytes > c)
+      return fail(SIEVE_ENOMEM, "workspace buffer of %zu bytes exceeds SIEVE_ALLOC_CAP = %llu",
+                  bytes, c);
+  }
   if (b.p) (void)hipFree(b.p);
   b.p = nullptr;
   b.bytes = 0;
@@ -444,17 +453,18 @@ int run_round(sieve_index* ix, const ScanArgs& sa, int n_items, int64_t q0, cons
   }
   const int e0 = *at >= 0 ? *at : mark(ix, timed, s);
   // few lists: the offsets launch also writes the tiles
+  const int64_t tile_cap = (int64_t)(ix->tiles.bytes / sizeof(Tile));
   const bool fuse = ix->nlist <= kFuseTilesMaxLists;
   HIP_TRY(launch_sched_offsets((int32_t*)ix->cnt.p, ix->offsets, ix->nlist, chunk, group,
                                (int32_t*)ix->item_off.p, (int32_t*)ix->cursor.p,
                                (int32_t*)ix->tile_off.p, rc, fuse ? (Tile*)ix->tiles.p : nullptr,
-                               s));
+                               tile_cap, s));
   HIP_TRY(launch_sched_scatter((const Item*)ix->items.p, n_items, P, pl.n, (int32_t)q0, sa.exclude,
                                (int32_t*)ix->cursor.p, (BItem*)ix->bucket.p, s));
   if (!fuse)
     HIP_TRY(launch_sched_tiles((int32_t*)ix->cnt.p, (const int32_t*)ix->item_off.p,
                                (const int32_t*)ix->tile_off.p, ix->offsets, ix->nlist, chunk,
-                               group, (Tile*)ix->tiles.p, s));
+                               group, (Tile*)ix->tiles.p, tile_cap, s));
   const int e1 = mark(ix, timed, s);
   ScanArgs sr = sa;
   sr.dynamic = scan_dynamic(n_items);
@@ -571,14 +581,14 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
       HIP_TRY(launch_fill_multi(f, s));
     }
     bool spec_used = false;  // a round kept the rank bitmap (its ranks may pass stop lines)
-    RoundSummary sm = {0, 0, 0, 0, 0};  // the host's view of the last round
+    RoundSummary sm = {0, 0, 0, 0, 0, 0, 0};  // the host's view of the last round
     int32_t* P = (int32_t*)ix->P.p;
 
     if (pl.mode != 2) {
       const int r0 = mark(ix, timed, s);
       if ((st = rank_queries(ix, queries, 0, nq, pl.r0, pl.n, pl, P, s))) return st;
       const int s0 = pl.mode == 0 ? (pl.W < pl.n ? pl.W : pl.n) : 1;
-      HIP_TRY(launch_emit_initial(P, pl.n, nq, 0, s0, pl.mode, (Item*)ix->items.p,
+      HIP_TRY(launch_emit_initial(P, pl.n, nq, 0, s0, pl.mode, (Item*)ix->items.p, pl.item_cap,
                                   (int32_t*)ix->cnt.p, ix->nlist, (int32_t*)ix->state_a.p,
                                   (int32_t*)ix->state_b.p, (int32_t*)ix->lmax.p, s));
       // adjacent phases share the event between them (fewer records per round)
@@ -601,13 +611,13 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
         if (pl.mode == 0)
           HIP_TRY(launch_update_lookahead(
               nq, P, pl.n, pl.W, (int32_t*)ix->state_a.p, (int32_t*)ix->lmax.p, have, ext,
-              (Item*)ix->items.p, (int32_t*)ix->cnt.p, rc, spec_now ? sa.hitbits : nullptr,
+              (Item*)ix->items.p, pl.item_cap, (int32_t*)ix->cnt.p, rc, spec_now ? sa.hitbits : nullptr,
               sa.hit_words, pl.spec ? (int32_t*)ix->state_b.p : nullptr, pl.spec_max,
               pl.spec_min, ix->rs_dev, s));
         else
           HIP_TRY(launch_update_basic(nq, P, pl.n, pl.W, (int32_t*)ix->state_a.p,
                                       (int32_t*)ix->state_b.p, (int32_t*)ix->lmax.p, have, ext,
-                                      (Item*)ix->items.p, (int32_t*)ix->cnt.p, rc, ix->rs_dev,
+                                      (Item*)ix->items.p, pl.item_cap, (int32_t*)ix->cnt.p, rc, ix->rs_dev,
                                       s));
         at = mark(ix, timed, s);
         span(ix, kUpdate, u0, at);
@@ -618,6 +628,8 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
         sm.rank_error = rs->rank_error;
         sm.heavy = rs->heavy;
         sm.hits = rs->hits;
+        if (rs->sched_error)
+          return fail(SIEVE_EINTERNAL, "a round's tiles exceeded the tile buffer");
         items_total += n_items;
         ++rounds;
         if (sm.rank_error) break;  // handled below: re-rank wide or fail
@@ -634,7 +646,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
             return st;
           HIP_TRY(launch_scatter_ranks(ext, n_ext, (const int32_t*)ix->Pext.p, pl.n, P, s));
           HIP_TRY(launch_emit_pending(ext, n_ext, pl.mode, P, pl.n, (const int32_t*)ix->state_a.p,
-                                      have, pl.n, (Item*)ix->items.p, (int32_t*)ix->cnt.p, rc,
+                                      have, pl.n, (Item*)ix->items.p, pl.item_cap, (int32_t*)ix->cnt.p, rc,
                                       pl.spec ? (int32_t*)ix->state_b.p : nullptr, s));
           at = mark(ix, timed, s);
           span(ix, kRank, x0, at);
@@ -657,7 +669,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
         const int r0 = mark(ix, timed, s);
         if ((st = rank_queries(ix, queries, q0, c, pl.n, pl.n, pl, P, s))) return st;
         HIP_TRY(launch_emit_initial(P, pl.n, c, (int32_t)q0, pl.n, 2, (Item*)ix->items.p,
-                                    (int32_t*)ix->cnt.p, ix->nlist, nullptr, nullptr, nullptr,
+                                    pl.item_cap, (int32_t*)ix->cnt.p, ix->nlist, nullptr, nullptr, nullptr,
                                     s));
         at = mark(ix, timed, s);
         span(ix, kRank, r0, at);
@@ -668,6 +680,8 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
       HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
       HIP_TRY(hipStreamSynchronize(s));
       at = -1;  // the copy ran after the last event
+      if (ix->rc_host->sched_error)
+        return fail(SIEVE_EINTERNAL, "a chunk's tiles exceeded the tile buffer");
       sm.rank_error = ix->rc_host->rank_error;
       sm.heavy = ix->rc_host->heavy;
       sm.hits = ix->rc_host->hits;

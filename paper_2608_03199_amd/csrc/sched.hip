@@ -44,7 +44,7 @@ inline int blocks_for(int64_t n, int per = kThreads) {
 // address serialise.
 __global__ __launch_bounds__(kInitThreads) void emit_initial_kernel(
     const int32_t* __restrict__ P, int32_t n, int64_t nqc, int32_t q0, int32_t s0, int32_t mode,
-    Item* __restrict__ items, int32_t* __restrict__ cnt, int32_t nlist,
+    Item* __restrict__ items, int64_t item_cap, int32_t* __restrict__ cnt, int32_t nlist,
     int32_t* __restrict__ state_a, int32_t* __restrict__ state_b, int32_t* __restrict__ lmax) {
   extern __shared__ int32_t s_hist[];  // [nlist]
   for (int i = threadIdx.x; i < nlist; i += blockDim.x) s_hist[i] = 0;
@@ -56,7 +56,7 @@ __global__ __launch_bounds__(kInitThreads) void emit_initial_kernel(
       Item it;
       it.q = q;
       it.rank = j;
-      items[ql * s0 + j] = it;
+      if (ql * s0 + j < item_cap) items[ql * s0 + j] = it;
       atomicAdd(&s_hist[P[ql * n + j]], 1);
     }
     if (mode == 0) {
@@ -84,7 +84,7 @@ __global__ __launch_bounds__(kOffThreads) void sched_offsets_kernel(
     int32_t* cnt, const int64_t* __restrict__ list_offsets, int32_t nlist,
     int32_t row_chunk, int32_t tile_q, int32_t* __restrict__ item_off,
     int32_t* __restrict__ cursor, int32_t* __restrict__ tile_off, RoundCounters* rc,
-    Tile* __restrict__ tiles) {
+    Tile* __restrict__ tiles, int64_t tile_cap) {
   __shared__ int64_t s_items[kOffThreads];
   __shared__ int64_t s_tiles[kOffThreads];
   __shared__ unsigned long long s_stat[3];
@@ -141,7 +141,8 @@ __global__ __launch_bounds__(kOffThreads) void sched_offsets_kernel(
             tl.item_begin = (int32_t)ri + tq * tile_q;
             tl.nq = min(tile_q, c - tq * tile_q);
             tl.list = p;
-            tiles[o++] = tl;
+            if (o < tile_cap) tiles[o] = tl;  // past the buffer: reported below
+            ++o;
           }
         }
       }
@@ -162,7 +163,11 @@ __global__ __launch_bounds__(kOffThreads) void sched_offsets_kernel(
   }
   __syncthreads();
   if (t == 0) {
-    rc->ntiles = (int32_t)s_tiles[kOffThreads - 1];
+    // a tile count past the buffer (never, by the host's bound) runs no scan
+    // and fails the search
+    const int64_t nt = s_tiles[kOffThreads - 1];
+    rc->ntiles = nt <= tile_cap ? (int32_t)nt : 0;
+    if (nt > tile_cap) rc->sched_error = 1;
     rc->new_items = 0;
     rc->n_ext = 0;
     for (int x = 0; x < 8; ++x) rc->queue[x] = 0;
@@ -194,7 +199,8 @@ __global__ void sched_scatter_kernel(const Item* __restrict__ items, int32_t n_i
 __global__ void sched_tiles_kernel(int32_t* __restrict__ cnt, const int32_t* __restrict__ item_off,
                                    const int32_t* __restrict__ tile_off,
                                    const int64_t* __restrict__ list_offsets, int32_t nlist,
-                                   int32_t row_chunk, int32_t tile_q, Tile* __restrict__ tiles) {
+                                   int32_t row_chunk, int32_t tile_q, Tile* __restrict__ tiles,
+                                   int64_t tile_cap) {
   const int p = blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= nlist) return;
   const int c = cnt[p];
@@ -213,7 +219,8 @@ __global__ void sched_tiles_kernel(int32_t* __restrict__ cnt, const int32_t* __r
       t.item_begin = item_off[p] + tq * tile_q;
       t.nq = min(tile_q, c - tq * tile_q);
       t.list = p;
-      tiles[o++] = t;
+      if (o < tile_cap) tiles[o] = t;
+      ++o;
     }
   }
 }
@@ -229,6 +236,8 @@ __global__ void publish_round_kernel(const RoundCounters* __restrict__ rc,
   __hip_atomic_store(&out->rank_error, rc->rank_error, __ATOMIC_RELAXED,
                      __HIP_MEMORY_SCOPE_SYSTEM);
   __hip_atomic_store(&out->heavy, rc->heavy, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  __hip_atomic_store(&out->sched_error, rc->sched_error, __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_SYSTEM);
   __hip_atomic_store(&out->hits, rc->hits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   __threadfence_system();
 }
@@ -246,6 +255,8 @@ __device__ __forceinline__ void publish_from_block(const RoundCounters* rc, Roun
   __hip_atomic_store(&out->rank_error, rc->rank_error, __ATOMIC_RELAXED,
                      __HIP_MEMORY_SCOPE_SYSTEM);
   __hip_atomic_store(&out->heavy, rc->heavy, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  __hip_atomic_store(&out->sched_error, rc->sched_error, __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_SYSTEM);
   __hip_atomic_store(&out->hits, rc->hits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   __threadfence_system();
 }
@@ -255,7 +266,7 @@ __device__ __forceinline__ void lookahead_one(int64_t q, const int32_t* __restri
                                               int32_t* __restrict__ lmax,
                                               const int32_t* __restrict__ have,
                                               int32_t* __restrict__ ext,
-                                              Item* __restrict__ items,
+                                              Item* __restrict__ items, int64_t item_cap,
                                               int32_t* __restrict__ cnt, RoundCounters* rc,
                                               const uint32_t* __restrict__ hitbits,
                                               int32_t words, int32_t* __restrict__ issued,
@@ -276,7 +287,7 @@ __device__ __forceinline__ void lookahead_one(int64_t q, const int32_t* __restri
         Item it;
         it.q = (int32_t)q;
         it.rank = j;
-        items[base + (j - e0)] = it;
+        if ((int64_t)(uint32_t)base + (j - e0) < item_cap) items[base + (j - e0)] = it;
         atomicAdd(&cnt[P[q * n + j]], 1);
       }
       if (issued) issued[q] = e1;
@@ -325,7 +336,7 @@ __device__ __forceinline__ void lookahead_one(int64_t q, const int32_t* __restri
       Item it;
       it.q = (int32_t)q;
       it.rank = j;
-      items[base + (j - i)] = it;
+      if ((int64_t)(uint32_t)base + (j - i) < item_cap) items[base + (j - i)] = it;
       atomicAdd(&cnt[P[q * n + j]], 1);
     }
     issued[q] = e1;
@@ -337,14 +348,14 @@ __global__ void update_lookahead_kernel(int64_t nq, const int32_t* __restrict__ 
                                         int32_t W, int32_t* __restrict__ stop,
                                         int32_t* __restrict__ lmax,
                                         const int32_t* __restrict__ have,
-                                        int32_t* __restrict__ ext, Item* __restrict__ items,
+                                        int32_t* __restrict__ ext, Item* __restrict__ items, int64_t item_cap,
                                         int32_t* __restrict__ cnt, RoundCounters* rc,
                                         const uint32_t* __restrict__ hitbits, int32_t words,
                                         int32_t* __restrict__ issued, int32_t spec_max,
                                         int32_t spec_min, RoundSummary* out) {
   const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (q < nq)
-    lookahead_one(q, P, n, W, stop, lmax, have, ext, items, cnt, rc, hitbits, words, issued,
+    lookahead_one(q, P, n, W, stop, lmax, have, ext, items, item_cap, cnt, rc, hitbits, words, issued,
                   spec_max, spec_min);
   if (out) publish_from_block(rc, out);  // one work-group only
 }
@@ -356,7 +367,7 @@ __device__ __forceinline__ void basic_one(int64_t q, const int32_t* __restrict__
                                           int32_t* __restrict__ stale,
                                           int32_t* __restrict__ lmax,
                                           const int32_t* __restrict__ have,
-                                          int32_t* __restrict__ ext, Item* __restrict__ items,
+                                          int32_t* __restrict__ ext, Item* __restrict__ items, int64_t item_cap,
                                           int32_t* __restrict__ cnt, RoundCounters* rc) {
   const int cur = next[q];
   if (cur < 0) return;
@@ -372,7 +383,7 @@ __device__ __forceinline__ void basic_one(int64_t q, const int32_t* __restrict__
       Item it;
       it.q = (int32_t)q;
       it.rank = nx;
-      items[pos] = it;
+      if ((int64_t)(uint32_t)pos < item_cap) items[pos] = it;
       atomicAdd(&cnt[P[q * n + nx]], 1);
     } else {
       ext[atomicAdd(&rc->n_ext, 1)] = (int32_t)q;
@@ -387,10 +398,10 @@ __global__ void update_basic_kernel(int64_t nq, const int32_t* __restrict__ P, i
                                     int32_t W, int32_t* __restrict__ next,
                                     int32_t* __restrict__ stale, int32_t* __restrict__ lmax,
                                     const int32_t* __restrict__ have, int32_t* __restrict__ ext,
-                                    Item* __restrict__ items, int32_t* __restrict__ cnt,
+                                    Item* __restrict__ items, int64_t item_cap, int32_t* __restrict__ cnt,
                                     RoundCounters* rc, RoundSummary* out) {
   const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (q < nq) basic_one(q, P, n, W, next, stale, lmax, have, ext, items, cnt, rc);
+  if (q < nq) basic_one(q, P, n, W, next, stale, lmax, have, ext, items, item_cap, cnt, rc);
   if (out) publish_from_block(rc, out);  // one work-group only
 }
 
@@ -424,7 +435,7 @@ __global__ void emit_pending_kernel(const int32_t* __restrict__ ext, int32_t n_e
                                     const int32_t* __restrict__ P, int32_t n,
                                     const int32_t* __restrict__ state_a,
                                     int32_t* __restrict__ have, int32_t new_have,
-                                    Item* __restrict__ items, int32_t* __restrict__ cnt,
+                                    Item* __restrict__ items, int64_t item_cap, int32_t* __restrict__ cnt,
                                     RoundCounters* rc, int32_t* __restrict__ issued) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n_ext) return;
@@ -446,7 +457,7 @@ __global__ void emit_pending_kernel(const int32_t* __restrict__ ext, int32_t n_e
       Item it;
       it.q = (int32_t)q;
       it.rank = j;
-      items[base + (j - e0)] = it;
+      if ((int64_t)(uint32_t)base + (j - e0) < item_cap) items[base + (j - e0)] = it;
       atomicAdd(&cnt[P[q * n + j]], 1);
     }
     if (mode == 0 && issued) issued[q] = e1;  // e0 == issued[q]: the update stopped at have
@@ -491,23 +502,23 @@ __global__ void zero_bytes_kernel(uint8_t* p, int64_t n) {
 }  // namespace
 
 hipError_t launch_emit_initial(const int32_t* P, int32_t n, int64_t nqc, int32_t q0, int32_t s0,
-                               int32_t mode, Item* items, int32_t* cnt, int32_t nlist,
-                               int32_t* state_a, int32_t* state_b, int32_t* lmax, hipStream_t s) {
+                               int32_t mode, Item* items, int64_t item_cap, int32_t* cnt,
+                               int32_t nlist, int32_t* state_a, int32_t* state_b, int32_t* lmax, hipStream_t s) {
   if (nqc <= 0) return hipSuccess;
   if (nlist < 1 || nlist > kMaxNlist) return hipErrorInvalidValue;
   const int b = std::min(blocks_for(nqc, kInitThreads), kInitBlocksMax);
   hipLaunchKernelGGL(emit_initial_kernel, dim3(b), dim3(kInitThreads), (size_t)nlist * 4, s, P,
-                     n, nqc, q0, s0, mode, items, cnt, nlist, state_a, state_b, lmax);
+                     n, nqc, q0, s0, mode, items, item_cap, cnt, nlist, state_a, state_b, lmax);
   return hipGetLastError();
 }
 
 hipError_t launch_sched_offsets(int32_t* cnt, const int64_t* list_offsets, int32_t nlist,
                                 int32_t row_chunk, int32_t tile_q, int32_t* item_off,
                                 int32_t* cursor, int32_t* tile_off, RoundCounters* rc,
-                                Tile* tiles, hipStream_t s) {
+                                Tile* tiles, int64_t tile_cap, hipStream_t s) {
   if (tiles && nlist > kFuseTilesMaxLists) return hipErrorInvalidValue;
   hipLaunchKernelGGL(sched_offsets_kernel, dim3(1), dim3(kOffThreads), 0, s, cnt, list_offsets,
-                     nlist, row_chunk, tile_q, item_off, cursor, tile_off, rc, tiles);
+                     nlist, row_chunk, tile_q, item_off, cursor, tile_off, rc, tiles, tile_cap);
   return hipGetLastError();
 }
 
@@ -522,21 +533,23 @@ hipError_t launch_sched_scatter(const Item* items, int32_t n_items, const int32_
 
 hipError_t launch_sched_tiles(int32_t* cnt, const int32_t* item_off, const int32_t* tile_off,
                               const int64_t* list_offsets, int32_t nlist, int32_t row_chunk,
-                              int32_t tile_q, Tile* tiles, hipStream_t s) {
+                              int32_t tile_q, Tile* tiles, int64_t tile_cap, hipStream_t s) {
   hipLaunchKernelGGL(sched_tiles_kernel, dim3(blocks_for(nlist)), dim3(kThreads), 0, s, cnt,
-                     item_off, tile_off, list_offsets, nlist, row_chunk, tile_q, tiles);
+                     item_off, tile_off, list_offsets, nlist, row_chunk, tile_q, tiles, tile_cap);
   return hipGetLastError();
 }
 
 hipError_t launch_update_lookahead(int64_t nq, const int32_t* P, int32_t n, int32_t W,
                                    int32_t* stop, int32_t* lmax, const int32_t* have,
-                                   int32_t* ext, Item* items, int32_t* cnt, RoundCounters* rc,
-                                   const uint32_t* hitbits, int32_t words, int32_t* issued,
+                                   int32_t* ext, Item* items, int64_t item_cap, int32_t* cnt,
+                                   RoundCounters* rc, const uint32_t* hitbits, int32_t words,
+                                   int32_t* issued,
                                    int32_t spec_max, int32_t spec_min, RoundSummary* out,
                                    hipStream_t s) {
   if (hitbits && (!issued || words * 32 < n || spec_max < 0)) return hipErrorInvalidValue;
   hipLaunchKernelGGL(update_lookahead_kernel, dim3(blocks_for(nq)), dim3(kThreads), 0, s, nq, P, n,
-                     W, stop, lmax, have, ext, items, cnt, rc, hitbits, words, issued, spec_max,
+                     W, stop, lmax, have, ext, items, item_cap, cnt, rc, hitbits, words, issued,
+                     spec_max,
                      spec_min, blocks_for(nq) == 1 ? out : nullptr);
   if (out && blocks_for(nq) > 1)
     hipLaunchKernelGGL(publish_round_kernel, dim3(1), dim3(64), 0, s, rc, out);
@@ -545,10 +558,10 @@ hipError_t launch_update_lookahead(int64_t nq, const int32_t* P, int32_t n, int3
 
 hipError_t launch_update_basic(int64_t nq, const int32_t* P, int32_t n, int32_t W, int32_t* next,
                                int32_t* stale, int32_t* lmax, const int32_t* have, int32_t* ext,
-                               Item* items, int32_t* cnt, RoundCounters* rc, RoundSummary* out,
-                               hipStream_t s) {
+                               Item* items, int64_t item_cap, int32_t* cnt, RoundCounters* rc,
+                               RoundSummary* out, hipStream_t s) {
   hipLaunchKernelGGL(update_basic_kernel, dim3(blocks_for(nq)), dim3(kThreads), 0, s, nq, P, n, W,
-                     next, stale, lmax, have, ext, items, cnt, rc,
+                     next, stale, lmax, have, ext, items, item_cap, cnt, rc,
                      blocks_for(nq) == 1 ? out : nullptr);
   if (out && blocks_for(nq) > 1)
     hipLaunchKernelGGL(publish_round_kernel, dim3(1), dim3(64), 0, s, rc, out);
@@ -578,11 +591,11 @@ hipError_t launch_scatter_ranks(const int32_t* ext, int32_t n_ext, const int32_t
 
 hipError_t launch_emit_pending(const int32_t* ext, int32_t n_ext, int32_t mode, const int32_t* P,
                                int32_t n, const int32_t* state_a, int32_t* have,
-                               int32_t new_have, Item* items, int32_t* cnt, RoundCounters* rc,
-                               int32_t* issued, hipStream_t s) {
+                               int32_t new_have, Item* items, int64_t item_cap, int32_t* cnt,
+                               RoundCounters* rc, int32_t* issued, hipStream_t s) {
   if (n_ext <= 0) return hipSuccess;
   hipLaunchKernelGGL(emit_pending_kernel, dim3(blocks_for(n_ext)), dim3(kThreads), 0, s, ext,
-                     n_ext, mode, P, n, state_a, have, new_have, items, cnt, rc, issued);
+                     n_ext, mode, P, n, state_a, have, new_have, items, item_cap, cnt, rc, issued);
   return hipGetLastError();
 }
 

@@ -64,7 +64,7 @@ struct RoundCounters {
   unsigned long long hits;        // candidate-pool entries written (whole search)
   unsigned long long cands;       // qualifying (query, row) pairs the scans found (whole search)
   int32_t heavy;                  // HeavyRec records claimed (whole search)
-  int32_t pad_;
+  int32_t sched_error;            // set when a round's tiles exceed the tile buffer
   // Sums of out_probes and of the qualifying candidates merged by the final
   // top-k, spread over kStatSlots counters (work-group b adds to slot
   // b % kStatSlots): thousands of adds to one address would serialise.
@@ -79,6 +79,8 @@ struct RoundSummary {
   int32_t n_ext;
   int32_t rank_error;
   int32_t heavy;             // HeavyRec records claimed so far
+  int32_t sched_error;       // a round's tiles exceeded the tile buffer
+  int32_t pad_;
   unsigned long long hits;  // pool entries written so far
 };
 
@@ -212,7 +214,8 @@ hipError_t launch_rank_select(int dtype, const void* queries, int64_t q0, int32_
                               bool wide, hipStream_t s);
 
 hipError_t launch_emit_initial(const int32_t* P, int32_t n, int64_t nqc, int32_t q0, int32_t s0,
-                               int32_t mode, Item* items, int32_t* cnt, int32_t nlist,
+                               int32_t mode, Item* items, int64_t item_cap, int32_t* cnt,
+                               int32_t nlist,
                                int32_t* state_a, int32_t* state_b, int32_t* lmax, hipStream_t s);
 // tiles: non-null (at most kFuseTilesMaxLists lists) to write the round's
 // tiles and clear the histogram in the same launch (no sched_tiles launch).
@@ -220,13 +223,13 @@ constexpr int kFuseTilesMaxLists = 1024;
 hipError_t launch_sched_offsets(int32_t* cnt, const int64_t* list_offsets, int32_t nlist,
                                 int32_t row_chunk, int32_t tile_q, int32_t* item_off,
                                 int32_t* cursor, int32_t* tile_off, RoundCounters* rc,
-                                Tile* tiles, hipStream_t s);
+                                Tile* tiles, int64_t tile_cap, hipStream_t s);
 hipError_t launch_sched_scatter(const Item* items, int32_t n_items, const int32_t* P, int32_t n,
                                 int32_t q0, const int64_t* exclude, int32_t* cursor,
                                 BItem* bucket, hipStream_t s);
 hipError_t launch_sched_tiles(int32_t* cnt, const int32_t* item_off, const int32_t* tile_off,
                               const int64_t* list_offsets, int32_t nlist, int32_t row_chunk,
-                              int32_t tile_q, Tile* tiles, hipStream_t s);
+                              int32_t tile_q, Tile* tiles, int64_t tile_cap, hipStream_t s);
 hipError_t launch_scan(int dtype, const ScanArgs& a, int32_t grid, hipStream_t s);
 // The updates emit ranks below have[q] (ranks already ordered in P) and
 // list the queries that need more in ext[] (count in rc->n_ext).
@@ -238,14 +241,15 @@ hipError_t launch_scan(int dtype, const ScanArgs& a, int32_t grid, hipStream_t s
 // at least spec_min ranks gets as many more issued past it, at most spec_max.
 hipError_t launch_update_lookahead(int64_t nq, const int32_t* P, int32_t n, int32_t W,
                                    int32_t* stop, int32_t* lmax, const int32_t* have,
-                                   int32_t* ext, Item* items, int32_t* cnt, RoundCounters* rc,
-                                   const uint32_t* hitbits, int32_t words, int32_t* issued,
+                                   int32_t* ext, Item* items, int64_t item_cap, int32_t* cnt,
+                                   RoundCounters* rc, const uint32_t* hitbits, int32_t words,
+                                   int32_t* issued,
                                    int32_t spec_max, int32_t spec_min, RoundSummary* out,
                                    hipStream_t s);
 hipError_t launch_update_basic(int64_t nq, const int32_t* P, int32_t n, int32_t W, int32_t* next,
                                int32_t* stale, int32_t* lmax, const int32_t* have, int32_t* ext,
-                               Item* items, int32_t* cnt, RoundCounters* rc, RoundSummary* out,
-                               hipStream_t s);
+                               Item* items, int64_t item_cap, int32_t* cnt, RoundCounters* rc,
+                               RoundSummary* out, hipStream_t s);
 // Lazy ranking: copy the listed queries' rows together, copy their new rank
 // rows into P, and emit the items the extension unblocked.
 hipError_t launch_gather_rows(const int32_t* ext, int32_t n_ext, const void* src,
@@ -254,8 +258,8 @@ hipError_t launch_scatter_ranks(const int32_t* ext, int32_t n_ext, const int32_t
                                 int32_t n, int32_t* P, hipStream_t s);
 hipError_t launch_emit_pending(const int32_t* ext, int32_t n_ext, int32_t mode, const int32_t* P,
                                int32_t n, const int32_t* state_a, int32_t* have,
-                               int32_t new_have, Item* items, int32_t* cnt, RoundCounters* rc,
-                               int32_t* issued, hipStream_t s);
+                               int32_t new_have, Item* items, int64_t item_cap, int32_t* cnt,
+                               RoundCounters* rc, int32_t* issued, hipStream_t s);
 
 hipError_t launch_snapshot_round(const RoundCounters* rc, RoundSnap* log, int32_t slot,
                                  hipStream_t s);

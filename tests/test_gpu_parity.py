@@ -598,6 +598,36 @@ def test_pool_index_limit_gives_a_clean_error():
     _check(c, s.k, s.tau, s.W, s.nprobe_max)
 
 
+def test_workspace_cap_gives_enomem():
+    """A workspace allocation the device cannot serve fails the call with SIEVE_ENOMEM and a
+    message, before any launch that needs it; the allocation cap is forced through its knob
+    (no real exhaustion).  The same handle then searches normally, with the result of an
+    index that never failed."""
+    ps = _lib()
+    c = case("c1")
+    s = c.w.spec
+    q, ex = c.w.queries, c.w.exclude_ids
+    ix = ps.Index(c.w.vectors, c.w.list_offsets, c.w.ids, c.w.centroids)
+    try:
+        # 16x the batch: the workspace the handle holds (sized at load) must grow
+        qq, exx = q.repeat(16, 1).contiguous(), ex.repeat(16).contiguous()
+        os.environ["SIEVE_ALLOC_CAP"] = "4096"
+        try:
+            for call in (lambda: ix.search(qq, exx, s.k, s.tau, s.W, s.nprobe_max),
+                         lambda: ix.search_fixed(qq, exx, s.k, s.tau, s.fixed_nprobe)):
+                with pytest.raises(ps.SieveError) as e:
+                    call()
+                assert e.value.code == -2 and "SIEVE_ALLOC_CAP" in str(e.value)
+        finally:
+            del os.environ["SIEVE_ALLOC_CAP"]
+        got = [t.cpu().numpy() for t in ix.search(q, ex, s.k, s.tau, s.W, s.nprobe_max)]
+        want = [t.cpu().numpy() for t in c.ix.search(q, ex, s.k, s.tau, s.W, s.nprobe_max)]
+        for x, y in zip(got, want):
+            assert np.array_equal(x, y)
+    finally:
+        ix.close()
+
+
 @pytest.mark.parametrize("k", [1, 10, 64])
 @pytest.mark.parametrize("fixed", [False, True])
 @pytest.mark.parametrize("knob", [None, ("SIEVE_SPILL_CAP", "0"), ("SIEVE_ARENA", "0")])
