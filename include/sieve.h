@@ -235,6 +235,24 @@ SIEVE_API int sieve_search_multi(const sieve_index* const* idxs, int32_t nidx,
                                  int32_t* out_probes, sieve_stats* stats, void* stream);
 
 /*
+ * sieve_search_multi_calibrated -- sieve_search_multi with the in-call window
+ * calibration of Appendix A done per index: every index runs
+ * sieve_search_calibrated on the same sampled query indices (its own sample
+ * outcomes choose its own W, its sampled queries keep its fixed-probe
+ * result, the rest use its W with Algorithm 2 lookahead), and the per-query
+ * results are merged as in sieve_search_multi.
+ *   out_W        HOST array of nidx: the window each index used.
+ * Other arguments as for sieve_search_calibrated and sieve_search_multi.
+ */
+SIEVE_API int sieve_search_multi_calibrated(const sieve_index* const* idxs, int32_t nidx,
+                                            const void* queries, int64_t nq,
+                                            const int64_t* exclude_ids, int32_t k, float tau,
+                                            int32_t nprobe_max, const int32_t* sample, int64_t ns,
+                                            float eps, int32_t W_fallback, int64_t* out_ids,
+                                            float* out_scores, int32_t* out_probes,
+                                            int32_t* out_W, sieve_stats* stats, void* stream);
+
+/*
  * sieve_rank -- the probe order alone (Sec. 4.1): for each query, the first
  * min(nprobe, nlist) centroid indices by inner product, descending, ties to
  * the lower index, decided in fp64 (see the conventions above).

@@ -153,9 +153,12 @@ def search_multi(shards, queries, exclude_ids, k, tau, W, nprobe_max, mode=MODE_
     of the shard results is ordered by (score desc, id asc) and cut to k.  shards: a list of
     dicts with vectors, list_offsets, ids, centroids.  probes = the sum over the shards.
     The tie flags are recomputed on the merged list; TAU_EDGE and KTH_TIE of any shard are
-    kept (a shard's (k+1)-th candidate never reaches the merge)."""
+    kept (a shard's (k+1)-th candidate never reaches the merge).  W: one window for every
+    shard, or a list with one per shard (per-shard calibration, Appendix A)."""
+    Ws = list(W) if isinstance(W, (list, tuple)) else [W] * len(shards)
     parts = [search(sh["vectors"], sh["list_offsets"], sh["ids"], sh["centroids"], queries,
-                    exclude_ids, k, tau, W, nprobe_max, mode, nthreads) for sh in shards]
+                    exclude_ids, k, tau, w, nprobe_max, mode, nthreads)
+             for sh, w in zip(shards, Ws)]
     nq = np.asarray(queries).shape[0]
     r = OracleResult(ids=np.full((nq, k), -1, np.int64), scores=np.full((nq, k), -np.inf),
                      probes=np.zeros(nq, np.int32), flags=np.zeros(nq, np.int32))

@@ -102,6 +102,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sieve_search_multi.restype = ctypes.c_int
     lib.sieve_search_multi.argtypes = [P, i32, P, i64, P, i32, ctypes.c_float, i32, i32, i32, P,
                                        P, P, ctypes.POINTER(Stats), P]
+    lib.sieve_search_multi_calibrated.restype = ctypes.c_int
+    lib.sieve_search_multi_calibrated.argtypes = [P, i32, P, i64, P, i32, ctypes.c_float, i32, P,
+                                                  i64, ctypes.c_float, i32, P, P, P,
+                                                  ctypes.POINTER(ctypes.c_int32),
+                                                  ctypes.POINTER(Stats), P]
     lib.sieve_round_log.restype = ctypes.c_int
     lib.sieve_round_log.argtypes = [P, ctypes.POINTER(Round), i32, ctypes.POINTER(ctypes.c_int32)]
     lib.sieve_rank.restype = ctypes.c_int
@@ -311,3 +316,31 @@ def search_multi(indexes, queries: torch.Tensor, exclude_ids: Optional[torch.Ten
             _lookahead_code(lookahead, speculative, serial), oi.data_ptr(), osc.data_ptr(),
             op.data_ptr(), ctypes.byref(st) if st is not None else None, _stream(stream)))
     return (oi, osc, op, st) if with_stats else (oi, osc, op)
+
+
+def search_multi_calibrated(indexes, queries: torch.Tensor, exclude_ids: Optional[torch.Tensor],
+                            k: int, tau: float, nprobe_max: int, sample: torch.Tensor,
+                            eps: float, W_fallback: int = 8, with_stats: bool = False,
+                            stream=None):
+    """``search_multi`` with the in-call window calibration (Appendix A) done per index on the
+    same sampled query indices (``sieve_search_multi_calibrated``).  Returns
+    (ids, scores, probes, [W per index][, Stats])."""
+    indexes = list(indexes)
+    if not indexes:
+        raise ValueError("at least one index is required")
+    first = indexes[0]
+    queries, ex, nq, oi, osc, op = first._prep(queries, exclude_ids, k)
+    smp = _dev(sample.to(torch.int32), "sample").reshape(-1)
+    if smp.device != queries.device:
+        raise ValueError("sample must be on the queries' device")
+    handles = (ctypes.c_void_p * len(indexes))(*[ix._h.value for ix in indexes])
+    ws = (ctypes.c_int32 * len(indexes))()
+    st = Stats() if with_stats else None
+    with torch.cuda.device(first.device):
+        _check(first._lib, first._lib.sieve_search_multi_calibrated(
+            handles, len(indexes), queries.data_ptr(), nq, None if ex is None else ex.data_ptr(),
+            int(k), float(tau), int(nprobe_max), smp.data_ptr() if smp.numel() else None,
+            int(smp.numel()), float(eps), int(W_fallback), oi.data_ptr(), osc.data_ptr(),
+            op.data_ptr(), ws, ctypes.byref(st) if st is not None else None, _stream(stream)))
+    out = (oi, osc, op, [int(x) for x in ws])
+    return out + (st,) if with_stats else out

@@ -1217,30 +1217,19 @@ SIEVE_API int sieve_search_fixed(const sieve_index* idx, const void* queries, in
                      stats, (hipStream_t)stream);
 }
 
-SIEVE_API int sieve_search_calibrated(const sieve_index* idx, const void* queries, int64_t nq,
-                                      const int64_t* exclude_ids, int32_t k, float tau,
-                                      int32_t nprobe_max, const int32_t* sample, int64_t ns,
-                                      float eps, int32_t W_fallback, int64_t* out_ids,
-                                      float* out_scores, int32_t* out_probes, int32_t* out_W,
-                                      sieve_stats* stats, void* stream) {
-  g_err.clear();
-  int st = check_common(idx, queries, nq, k, tau, out_ids, out_scores, out_probes);
-  if (st) return st;
-  if (nprobe_max < 1) return fail(SIEVE_EINVAL, "nprobe_max = %d must be >= 1", nprobe_max);
-  if (!(eps > 0.f && eps <= 1.f)) return fail(SIEVE_EINVAL, "eps = %g outside (0, 1]", (double)eps);
-  if (W_fallback < 1) return fail(SIEVE_EINVAL, "W_fallback = %d must be >= 1", W_fallback);
-  if (!out_W) return fail(SIEVE_EINVAL, "out_W is NULL");
-  if (ns < 0 || ns > nq) return fail(SIEVE_EINVAL, "ns = %lld outside [0, nq]", (long long)ns);
-  if (ns > kCalibMaxSample)
-    return fail(SIEVE_EUNSUPPORTED, "ns = %lld exceeds %d", (long long)ns, kCalibMaxSample);
-  if (ns > 0 && !sample) return fail(SIEVE_EINVAL, "sample is NULL with ns > 0");
-  sieve_index* ix = const_cast<sieve_index*>(idx);
+}  // extern "C"
+
+namespace {
+// The calibrated search of one index (arguments checked by the caller):
+// stats, if given, are added to (the caller zeroes them).
+int calibrated_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t* exclude_ids,
+                    int32_t k, float tau, int32_t nprobe_max, const int32_t* sample, int64_t ns,
+                    float eps, int32_t W_fallback, int64_t* out_ids, float* out_scores,
+                    int32_t* out_probes, int32_t* out_W, sieve_stats* stats, hipStream_t s) {
+  int st;
   SearchPlan pf;
   if ((st = plan_search(ix, ns, k, tau, SIEVE_W_INF, nprobe_max, 2, false, &pf))) return st;
-  if (stats) {
-    memset(stats, 0, sizeof(*stats));
-    stats->nprobe_eff = pf.n;
-  }
+  if (stats) stats->nprobe_eff = pf.n;
   if (nq == 0) {
     *out_W = W_fallback;
     return SIEVE_OK;
@@ -1250,7 +1239,6 @@ SIEVE_API int sieve_search_calibrated(const sieve_index* idx, const void* querie
   if (dev != ix->device)
     return fail(SIEVE_EINVAL, "current device %d differs from the index's device %d", dev,
                 ix->device);
-  hipStream_t s = (hipStream_t)stream;
   const int64_t nr = nq - ns;
   const int64_t row_bytes = (int64_t)ix->d * elem_bytes(ix->dtype);
 
@@ -1332,6 +1320,33 @@ SIEVE_API int sieve_search_calibrated(const sieve_index* idx, const void* querie
   return SIEVE_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
+SIEVE_API int sieve_search_calibrated(const sieve_index* idx, const void* queries, int64_t nq,
+                                      const int64_t* exclude_ids, int32_t k, float tau,
+                                      int32_t nprobe_max, const int32_t* sample, int64_t ns,
+                                      float eps, int32_t W_fallback, int64_t* out_ids,
+                                      float* out_scores, int32_t* out_probes, int32_t* out_W,
+                                      sieve_stats* stats, void* stream) {
+  g_err.clear();
+  int st = check_common(idx, queries, nq, k, tau, out_ids, out_scores, out_probes);
+  if (st) return st;
+  if (nprobe_max < 1) return fail(SIEVE_EINVAL, "nprobe_max = %d must be >= 1", nprobe_max);
+  if (!(eps > 0.f && eps <= 1.f)) return fail(SIEVE_EINVAL, "eps = %g outside (0, 1]", (double)eps);
+  if (W_fallback < 1) return fail(SIEVE_EINVAL, "W_fallback = %d must be >= 1", W_fallback);
+  if (!out_W) return fail(SIEVE_EINVAL, "out_W is NULL");
+  if (ns < 0 || ns > nq) return fail(SIEVE_EINVAL, "ns = %lld outside [0, nq]", (long long)ns);
+  if (ns > kCalibMaxSample)
+    return fail(SIEVE_EUNSUPPORTED, "ns = %lld exceeds %d", (long long)ns, kCalibMaxSample);
+  if (ns > 0 && !sample) return fail(SIEVE_EINVAL, "sample is NULL with ns > 0");
+  if (stats) memset(stats, 0, sizeof(*stats));
+  return calibrated_impl(const_cast<sieve_index*>(idx), queries, nq, exclude_ids, k, tau,
+                         nprobe_max, sample, ns, eps, W_fallback, out_ids, out_scores, out_probes,
+                         out_W, stats, (hipStream_t)stream);
+}
+
 SIEVE_API int sieve_search_multi(const sieve_index* const* idxs, int32_t nidx,
                                  const void* queries, int64_t nq, const int64_t* exclude_ids,
                                  int32_t k, float tau, int32_t W, int32_t nprobe_max,
@@ -1385,6 +1400,68 @@ SIEVE_API int sieve_search_multi(const sieve_index* const* idxs, int32_t nidx,
   HIP_TRY(launch_merge_shards(nq, k, nidx, mids, msc, mpr, out_ids, out_scores, out_probes, s));
   HIP_TRY(hipStreamSynchronize(s));
   if (stats) stats->nprobe_eff = plans[0].n;
+  return SIEVE_OK;
+}
+
+SIEVE_API int sieve_search_multi_calibrated(const sieve_index* const* idxs, int32_t nidx,
+                                            const void* queries, int64_t nq,
+                                            const int64_t* exclude_ids, int32_t k, float tau,
+                                            int32_t nprobe_max, const int32_t* sample, int64_t ns,
+                                            float eps, int32_t W_fallback, int64_t* out_ids,
+                                            float* out_scores, int32_t* out_probes,
+                                            int32_t* out_W, sieve_stats* stats, void* stream) {
+  g_err.clear();
+  if (!idxs || nidx < 1 || nidx > SIEVE_MULTI_MAX)
+    return fail(SIEVE_EINVAL, "idxs must hold 1 .. %d index handles", SIEVE_MULTI_MAX);
+  for (int32_t i = 0; i < nidx; ++i) {
+    if (!idxs[i]) return fail(SIEVE_EINVAL, "idxs[%d] is NULL", i);
+    if (idxs[i]->dtype != idxs[0]->dtype || idxs[i]->d != idxs[0]->d ||
+        idxs[i]->device != idxs[0]->device)
+      return fail(SIEVE_EINVAL, "idxs[%d] differs from idxs[0] in dtype, d or device", i);
+  }
+  int st = check_common(idxs[0], queries, nq, k, tau, out_ids, out_scores, out_probes);
+  if (st) return st;
+  if (nprobe_max < 1) return fail(SIEVE_EINVAL, "nprobe_max = %d must be >= 1", nprobe_max);
+  if (!(eps > 0.f && eps <= 1.f)) return fail(SIEVE_EINVAL, "eps = %g outside (0, 1]", (double)eps);
+  if (W_fallback < 1) return fail(SIEVE_EINVAL, "W_fallback = %d must be >= 1", W_fallback);
+  if (!out_W) return fail(SIEVE_EINVAL, "out_W is NULL");
+  if (ns < 0 || ns > nq) return fail(SIEVE_EINVAL, "ns = %lld outside [0, nq]", (long long)ns);
+  if (ns > kCalibMaxSample)
+    return fail(SIEVE_EUNSUPPORTED, "ns = %lld exceeds %d", (long long)ns, kCalibMaxSample);
+  if (ns > 0 && !sample) return fail(SIEVE_EINVAL, "sample is NULL with ns > 0");
+  if (stats) memset(stats, 0, sizeof(*stats));
+  if (nq == 0) {
+    for (int32_t i = 0; i < nidx; ++i) out_W[i] = W_fallback;
+    return SIEVE_OK;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  // per-index results, [nidx][nq][k], in the first index's workspace
+  sieve_index* ws = const_cast<sieve_index*>(idxs[0]);
+  const size_t rows = (size_t)nidx * (size_t)nq;
+  if ((st = ensure(ws->mix_ids, rows * k * sizeof(int64_t))) ||
+      (st = ensure(ws->mix_scores, rows * k * sizeof(float))) ||
+      (st = ensure(ws->mix_probes, rows * sizeof(int32_t))))
+    return st;
+  int64_t* mids = (int64_t*)ws->mix_ids.p;
+  float* msc = (float*)ws->mix_scores.p;
+  int32_t* mpr = (int32_t*)ws->mix_probes.p;
+  // each index calibrates its own window on the same sampled queries
+  for (int32_t i = 0; i < nidx; ++i) {
+    sieve_index* ix = const_cast<sieve_index*>(idxs[i]);
+    const size_t r0 = (size_t)i * (size_t)nq;
+    sieve_stats part;
+    memset(&part, 0, sizeof(part));
+    if ((st = calibrated_impl(ix, queries, nq, exclude_ids, k, tau, nprobe_max, sample, ns, eps,
+                              W_fallback, mids + r0 * k, msc + r0 * k, mpr + r0, out_W + i,
+                              stats ? &part : nullptr, s)))
+      return st;
+    if (stats) {
+      add_stats(stats, part);
+      stats->nprobe_eff = part.nprobe_eff;
+    }
+  }
+  HIP_TRY(launch_merge_shards(nq, k, nidx, mids, msc, mpr, out_ids, out_scores, out_probes, s));
+  HIP_TRY(hipStreamSynchronize(s));
   return SIEVE_OK;
 }
 

@@ -80,3 +80,44 @@ def test_multi_index_of_one_equals_plain_search(sharded):
         assert torch.equal(x, y)
     with pytest.raises(ps.SieveError):
         ps.search_multi(ixs, w.queries, w.exclude_ids, 0, s.tau, s.W, s.nprobe_max)
+
+
+@pytest.mark.parametrize("eps", [0.05, 0.005])
+def test_multi_index_calibrated_per_shard(sharded, eps):
+    """Per-shard calibration (Appendix A): every shard replays its own fixed-probe outcomes on
+    the same sampled query indices and chooses its own W.  Each chosen W equals the oracle's
+    replay of that shard's sample; the sampled queries carry the merge of the shards'
+    fixed-probe results and the other queries the merge of each shard's search with its own
+    W, both against the oracle."""
+    import paper_2608_03199_amd as ps
+    w, h, shards, ixs = sharded
+    s = w.spec
+    rng = np.random.default_rng(1234)
+    smp = np.sort(rng.choice(s.nq, s.nq // 10, replace=False)).astype(np.int32)
+    ids, sc, pr, Ws = ps.search_multi_calibrated(ixs, w.queries, w.exclude_ids, s.k, s.tau,
+                                                 s.nprobe_max, torch.from_numpy(smp).cuda(), eps)
+    ids, sc, pr = ids.cpu().numpy(), sc.cpu().numpy(), pr.cpu().numpy()
+    qs, xs = h["queries"][smp], h["exclude_ids"][smp]
+    want, edge = [], 0
+    for sh in shards:
+        o = oracle.search(sh["vectors"], sh["list_offsets"], sh["ids"], sh["centroids"], qs, xs,
+                          s.k, s.tau, oracle.W_INF, s.nprobe_max, oracle.MODE_A, NTHREADS,
+                          want_hitseq=True)
+        wo, _, _ = oracle.calibrate(o.hitseq, o.rank, eps)
+        want.append(8 if wo is None else wo)
+        edge += int((o.flags & oracle.FLAG_TAU_EDGE).astype(bool).sum())
+    print(f"[gpu-test] multi calibrated eps={eps}: W {Ws}, oracle {want}, tau-edge {edge}",
+          flush=True)
+    if edge == 0:
+        assert Ws == want
+    of = oracle.search_multi(shards, qs, xs, s.k, s.tau, oracle.W_INF, s.nprobe_max,
+                             nthreads=NTHREADS)
+    rep = compare(ids[smp], sc[smp], pr[smp], of)
+    print(f"[gpu-test] multi calibrated sample -> {rep}", flush=True)
+    assert_parity(rep)
+    rest = np.setdiff1d(np.arange(s.nq), smp)
+    orr = oracle.search_multi(shards, h["queries"][rest], h["exclude_ids"][rest], s.k, s.tau,
+                              list(Ws), s.nprobe_max, nthreads=NTHREADS)
+    rep = compare(ids[rest], sc[rest], pr[rest], orr)
+    print(f"[gpu-test] multi calibrated rest -> {rep}", flush=True)
+    assert_parity(rep)
