@@ -214,6 +214,13 @@ def run_config(name, args, ps, sw, np, torch, dev, headline):
     h_ids, h_probes = ids.cpu().numpy(), probes.cpu().numpy()
     res["e1"] = e1_diagnostics(np, h_ids, h_probes, spec.W, min(spec.nprobe_max, spec.nlist))
 
+    if args.sieve_only:
+        # counter runs: the threshold-search steps alone (no other scan launches follow)
+        ix.close()
+        del w
+        torch.cuda.empty_cache()
+        return res
+
     # speculative issue past the stop line (same outputs, fewer rounds, more searches)
     ks = max(1, min(K, 5))
     sp, t_sp = _timed_steps(torch, lambda: sieve(speculative=True), ks)
@@ -323,6 +330,9 @@ def main():
     ap.add_argument("--no-oracle", action="store_true")
     ap.add_argument("--skip-calibrated", action="store_true",
                     help="do not time the in-call calibrated search (profiling runs)")
+    ap.add_argument("--sieve-only", action="store_true",
+                    help="time the threshold-search steps only (no speculative, fixed-probe, "
+                         "calibrated or oracle legs): for counter runs")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (HBM counter calibration)")
     ap.add_argument("--envelope", action="store_true",
@@ -391,17 +401,17 @@ def main():
                    "tau": spec.tau, "W": spec.W, "nprobe_max": spec.nprobe_max,
                    "fixed_nprobe": spec.fixed_nprobe, "lookahead": "Algorithm 2 (committed)",
                    "parallelism": "single GPU"},
-        "speedup_vs_fixed": hr["speedup_vs_fixed"],
-        "fixed_qps": hr["fixed_qps"],
+        "speedup_vs_fixed": hr.get("speedup_vs_fixed"),
+        "fixed_qps": hr.get("fixed_qps"),
         "partition_vectors_per_s": hr["partition_vectors_per_s"],
         "scan_hbm_gbs": hr["scan_hbm_gbs"],
         "mean_probes": hr["mean_probes"],
         "scanned_probes_per_query": hr["scanned_probes_per_query"],
         "rounds": hr["rounds"],
         "phase_ms": hr["phase_ms"],
-        "fixed_phase_ms": hr["fixed_phase_ms"],
+        "fixed_phase_ms": hr.get("fixed_phase_ms"),
         "roofline": hr["roofline"],
-        "speculative": hr["speculative"],
+        "speculative": hr.get("speculative"),
         "calibrated": hr.get("calibrated"),
         "e1": hr["e1"],
         "lists": hr["lists"],
