@@ -96,6 +96,12 @@ constexpr int rega_max_qb() {
   return kOcc == 1 ? 8 : 4;
 }
 
+// Largest of one query block's four accumulator elements (the same tree in
+// the vote and in the candidate test, so the two share it).
+__device__ __forceinline__ float block_max(const f32x4& v) {
+  return fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
+}
+
 // Element x = 4 qb + r of a row block's accumulators, x uniform: a chain of
 // selects on a scalar condition (no indexed register access).
 template <int QB>
@@ -261,10 +267,7 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
       const float tr = row < r1 ? tau : INFINITY;
       float mx = -INFINITY;
 #pragma unroll
-      for (int qb = 0; qb + 1 < QB; ++qb) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) mx = fmaxf(mx, acc[qb][r]);
-      }
+      for (int qb = 0; qb + 1 < QB; ++qb) mx = fmaxf(mx, block_max(acc[qb]));
       bool any = mx >= tr;
 #pragma unroll
       for (int r = 0; r < 4; ++r) any |= acc[QB - 1][r] >= fmaxf(tr, thr_last[r]);
@@ -272,10 +275,11 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
     };
     // Qualifying pairs of the row block go to the wave's part of the arena as
     // (score, row offset, staged query), in (query block, element, lane)
-    // order.  Each (query block, element) is one vector compare into a lane
-    // mask; a scalar branch skips it when no lane qualifies, else the lanes of
-    // the mask take consecutive slots (LDS stores only).  The cost follows the
-    // qualifying (block, element) pairs, not the lanes.  When the run could
+    // order.  A query block whose maximum misses tau is skipped with one
+    // compare; otherwise each of its elements is one vector compare into a
+    // lane mask, a scalar branch skips it when no lane qualifies, else the
+    // lanes of the mask take consecutive slots (LDS stores only).  The cost
+    // follows the qualifying (block, element) pairs, not the lanes.  When the run could
     // reach past the LDS part, a slower path also covers the global part and,
     // past that, counts per query the pairs the arena cannot take (own row
     // excluded) for the heavy pass; its global accesses complete before it
@@ -291,6 +295,16 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
         TileSpill* const dst = s_arena + wv * wcap;
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
+          // most query blocks of a passing row block hold no qualifying pair:
+          // one compare of the block's maximum skips them
+          bool okq = false;
+          if (qb + 1 < QB) {
+            okq = block_max(acc[qb]) >= tr;
+          } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) okq |= acc[qb][r] >= thr(qb, r);
+          }
+          if (__ballot(okq) == 0ull) continue;
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const bool ok = acc[qb][r] >= thr(qb, r);
