@@ -96,6 +96,20 @@ constexpr int rega_max_qb() {
   return kOcc == 1 ? 8 : 4;
 }
 
+// Unsigned key whose order is the float order of finite and infinite scores
+// (sign flipped for positive values, all bits flipped for negative ones; -0
+// takes +0's key, as the two compare equal).
+__device__ __forceinline__ uint32_t order_key(float x) {
+  const uint32_t u = __float_as_uint(x == 0.0f ? 0.0f : x);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Top-k selection at the end of a tile: score keys per lane held in
+// registers, and the LDS arena entries (8 bytes) each wave borrows to compact
+// 64 segment positions.
+constexpr int kSelR = 8;
+constexpr int kSelSlots = 64 * (int)sizeof(int32_t) / (int)sizeof(TileSpill);
+
 // Largest of one query block's four accumulator elements (the same tree in
 // the vote and in the candidate test, so the two share it).
 __device__ __forceinline__ float block_max(const f32x4& v) {
@@ -562,11 +576,21 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
           __builtin_amdgcn_s_waitcnt(0);
           __syncthreads();
           __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-          // queries with more than k: one wave merges the query's segment
-          // into its top k, 64 pairs at a time (the next batch loads under
-          // this one's sort); a batch none of whose pairs reaches the k-th
-          // score kept so far cannot change the top k and is not sorted
+          // queries with more than k: one wave selects the query's top k from
+          // its segment.  Up to kSelR * 64 pairs: their score keys sit in
+          // registers, kSelR per lane; the k-th largest of the 64 lane maxima (a radix
+          // select over order-preserving score keys, ballots only) is a lower
+          // bound L on the k-th score, since k lanes hold a pair >= L.  When at
+          // most 64 pairs reach L, their positions are compacted through the
+          // wave's slice of the (now idle) LDS arena, and the pairs are loaded
+          // and sorted once: every pair of the top k is among them, ties at L
+          // included.  Otherwise (and for longer
+          // segments) the segment is merged 64 pairs at a time: the next batch
+          // loads under this one's sort, and a batch none of whose pairs
+          // reaches the k-th score kept so far is not sorted.
           const Cand none = {-INFINITY, 0x7fffffffffffffffll, -1};
+          const bool slots_ok = arena_lds >= nwv * kSelSlots;  // uniform
+          int32_t* const wslot = (int32_t*)(s_arena + wv * kSelSlots);
           for (int j = threadIdx.x >> 6; j < sel_n; j += blockDim.x >> 6) {
             const int i = s_sel[j];
             const int ci = s_hits[i];
@@ -576,17 +600,69 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
               const SrtEnt se = seg[b0 + lane];
               return Cand{se.score, (long long)se.id, 0};
             };
-            Cand top = wave_sort_desc<false>(fetch(0), lane);
-            Cand nxt = fetch(64);
-            for (int b0 = 64; b0 < ci; b0 += 64) {
-              Cand cnd = nxt;
-              nxt = fetch(b0 + 64);
-              const Cand kth = shfl_cand<false>(top, k - 1);
-              if (__ballot(!better(kth, cnd)) == 0ull) continue;
-              cnd = wave_sort_desc<false>(cnd, lane);
-              const Cand rv = shfl_cand<false>(cnd, 63 - lane);  // top ++ reverse(cnd): bitonic
-              top = better(top, rv) ? top : rv;
-              top = wave_merge_desc<false>(top, lane);
+            Cand top = none;
+            bool picked = false;
+            if (slots_ok && ci > 64 && ci <= kSelR * 64) {
+              uint32_t key[kSelR];
+              uint32_t kmax = 0;
+#pragma unroll
+              for (int r = 0; r < kSelR; ++r) {
+                const int e = r * 64 + lane;
+                key[r] = e < ci ? order_key(seg[e].score) : 0u;
+                kmax = max(kmax, key[r]);
+              }
+              // k-th largest lane maximum (every lane holds a pair: ci > 64)
+              uint32_t pre = 0, msk = 0;
+              int need = k;
+              for (int b = 31; b >= 0; --b) {
+                const uint32_t bit = 1u << b;
+                const int nhi = __popcll(__ballot((kmax & msk) == pre && (kmax & bit) != 0u));
+                if (nhi >= need)
+                  pre |= bit;
+                else
+                  need -= nhi;
+                msk |= bit;
+              }
+              int cnt = 0;
+#pragma unroll
+              for (int r = 0; r < kSelR; ++r) cnt += __popcll(__ballot(key[r] >= pre));
+              if (cnt <= 64) {
+                // segment positions of the pairs that reach L, then one load each
+                int pos = 0;
+#pragma unroll
+                for (int r = 0; r < kSelR; ++r) {
+                  const bool take = key[r] >= pre;
+                  const unsigned long long m = __ballot(take);
+                  if (take)
+                    wslot[pos + (int)__builtin_amdgcn_mbcnt_hi(
+                                    (uint32_t)(m >> 32),
+                                    __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u))] = r * 64 + lane;
+                  pos += __popcll(m);
+                }
+                __builtin_amdgcn_wave_barrier();
+                Cand c = none;
+                if (lane < cnt) {
+                  const SrtEnt se = seg[wslot[lane]];
+                  c = Cand{se.score, (long long)se.id, 0};
+                }
+                __builtin_amdgcn_wave_barrier();  // slots read before the next query's
+                top = wave_sort_desc<false>(c, lane);
+                picked = true;
+              }
+            }
+            if (!picked) {
+              top = wave_sort_desc<false>(fetch(0), lane);
+              Cand nxt = fetch(64);
+              for (int b0 = 64; b0 < ci; b0 += 64) {
+                Cand cnd = nxt;
+                nxt = fetch(b0 + 64);
+                const Cand kth = shfl_cand<false>(top, k - 1);
+                if (__ballot(!better(kth, cnd)) == 0ull) continue;
+                cnd = wave_sort_desc<false>(cnd, lane);
+                const Cand rv = shfl_cand<false>(cnd, 63 - lane);  // top ++ reverse(cnd): bitonic
+                top = better(top, rv) ? top : rv;
+                top = wave_merge_desc<false>(top, lane);
+              }
             }
             const int kk = min(ci, k);
             const unsigned long long base = s_pbase + (unsigned long long)s_poff[i];
