@@ -226,9 +226,18 @@ int scan_grid(const sieve_index* ix, int tile_q) {
   return ((ix->cus * per_cu + 7) / 8) * 8;  // the scan's schedule needs a multiple of 8
 }
 
-// Large rounds balance better with the atomic queue, small ones without it.
-int scan_dynamic(int64_t n_items) {
-  return n_items >= (int64_t)env_int("SIEVE_DYNAMIC_MIN_ITEMS", 200000) ? 1 : 0;
+// Rounds with many tiles per work-group balance better with the atomic
+// queue, rounds with a few without it.  The round's tile count is estimated on
+// the host from its size: every touched list gives at least one tile per row
+// chunk, and a dense round about n_items / group more per chunk.
+int scan_dynamic(const sieve_index* ix, int64_t n_items, bool dense, int chunk, int group,
+                 int grid) {
+  const int64_t avg_len = std::max<int64_t>(ix->n / std::max(ix->nlist, 1), 1);
+  const int64_t chunks = (avg_len + chunk - 1) / chunk;
+  const int64_t lists = std::min<int64_t>(n_items, ix->nlist);
+  const int64_t groups = dense ? lists + n_items / std::max(group, 1) : lists;
+  const int64_t min_tiles = (int64_t)env_int("SIEVE_DYNAMIC_MIN_TILES", 16) * grid;
+  return groups * chunks >= min_tiles ? 1 : 0;
 }
 
 struct SearchPlan {
@@ -467,7 +476,7 @@ int run_round(sieve_index* ix, const ScanArgs& sa, int n_items, int64_t q0, cons
                                group, (Tile*)ix->tiles.p, tile_cap, s));
   const int e1 = mark(ix, timed, s);
   ScanArgs sr = sa;
-  sr.dynamic = scan_dynamic(n_items);
+  sr.dynamic = scan_dynamic(ix, n_items, dense, chunk, group, grid);
   sr.tile_q = tile_q;
   HIP_TRY(launch_scan(ix->dtype, sr, grid, s));
   const int e2 = mark(ix, timed, s);
@@ -823,10 +832,12 @@ int plan_search(const sieve_index* ix, int64_t nq, int32_t k, float tau, int32_t
   pl->group_q = pl->tile_q;
   pl->min_group = pl->rega ? scan_rega_tile_q(false) : pl->tile_q;
   pl->wide_rank = false;
-  pl->row_chunk = row_chunk_for(ix, "SIEVE_ROW_CHUNK", 512);
+  // sparse rounds: 1,024-row tiles for register-held queries (a tile's start
+  // drains its row ring once), else 512
+  pl->row_chunk = row_chunk_for(ix, "SIEVE_ROW_CHUNK", pl->rega ? 1024 : 512);
   // Dense rounds over short lists (at most 2048 rows on average) take whole
   // lists as one tile, which halves the tile starts of a 1,000-row list; with
-  // long lists the 512-row tiles measured as fast or faster.
+  // long lists 1,024-row tiles measured fastest.
   const int64_t avg_len = ix->n / ix->nlist;
   // Register-held queries make a tile's start cheap, so dense rounds take
   // whole lists; otherwise the query staging favours 512-row tiles on long
@@ -834,7 +845,7 @@ int plan_search(const sieve_index* ix, int64_t nq, int32_t k, float tau, int32_t
   const int whole = (int)std::min<int64_t>(std::max<int64_t>(ix->max_list, 64), INT32_MAX / 2);
   pl->row_chunk_dense = row_chunk_for(
       ix, "SIEVE_ROW_CHUNK_DENSE",
-      scan_uses_rega(ix->dtype, ix->d) ? whole : (avg_len <= 2048 ? 4096 : pl->row_chunk));
+      scan_uses_rega(ix->dtype, ix->d) ? whole : (avg_len <= 2048 ? 4096 : 1024));
   if (pl->row_chunk_dense < pl->row_chunk) pl->row_chunk_dense = pl->row_chunk;
   pl->dense_q = env_int("SIEVE_DENSE_Q", 64);
   // Speculative issue needs the rank packed beside the query in pool entries

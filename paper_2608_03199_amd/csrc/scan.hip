@@ -93,7 +93,7 @@ __device__ __forceinline__ void with_qb(int qb_n, F&& f) {
 // keep row loads in flight.
 template <int kOcc>
 constexpr int rega_max_qb() {
-  return kOcc == 1 ? 8 : 4;
+  return kOcc == 1 ? kRegAQB : 4;
 }
 
 // Unsigned key whose order is the float order of finite and infinite scores
@@ -131,19 +131,27 @@ constexpr int kStageSync = 0;   // staged through registers at the start of each
 constexpr int kStageAsync = 1;  // LDS-DMA into the other of two buffers, one tile ahead
 constexpr int kStageRegA = 2;   // LDS-DMA into one buffer; fragments kept in registers
 
+// Largest tile (staged queries) of a scan kernel configuration: its
+// per-query LDS arrays are sized for it.
+template <int kMode, int kOcc>
+constexpr int scan_tile_max() {
+  return kMode == kStageRegA ? 16 * rega_max_qb<kOcc>() : 16 * kQB;
+}
+
 template <int DT, int D, int kMode, int kNT, int kOcc>
 __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
+  constexpr int kTQ = scan_tile_max<kMode, kOcc>();  // staged queries, at most
   extern __shared__ u32x4 lds[];
-  __shared__ int32_t s_q[2][kTileQ];     // item sets: the running tile and the next
-  __shared__ int32_t s_rank[2][kTileQ];
-  __shared__ int64_t s_ex[2][kTileQ];
-  __shared__ int32_t s_hits[kTileQ];  // qualifying rows per staged query in this tile
-  __shared__ int32_t s_over[kTileQ];  // staged queries whose candidates overflowed
-  __shared__ int32_t s_lost[kTileQ];  // their qualifying rows the full arena did not take
-  __shared__ int32_t s_sel[kTileQ];   // staged queries selected from slots + spill
-  __shared__ int32_t s_soff[kTileQ];  // their segment in the sorted spill
-  __shared__ int32_t s_scur[kTileQ];
-  __shared__ int32_t s_poff[kTileQ];  // their first pool entry (after the tile's base)
+  __shared__ int32_t s_q[2][kTQ];     // item sets: the running tile and the next
+  __shared__ int32_t s_rank[2][kTQ];
+  __shared__ int64_t s_ex[2][kTQ];
+  __shared__ int32_t s_hits[kTQ];  // qualifying rows per staged query in this tile
+  __shared__ int32_t s_over[kTQ];  // staged queries whose candidates overflowed
+  __shared__ int32_t s_lost[kTQ];  // their qualifying rows the full arena did not take
+  __shared__ int32_t s_sel[kTQ];   // staged queries selected from slots + spill
+  __shared__ int32_t s_soff[kTQ];  // their segment in the sorted spill
+  __shared__ int32_t s_scur[kTQ];
+  __shared__ int32_t s_poff[kTQ];  // their first pool entry (after the tile's base)
   __shared__ int32_t s_pool_n, s_over_n, s_sel_n, s_rbase;
   __shared__ int32_t s_wcnt[kNT / 64];  // pairs each wave appended in this tile
   __shared__ unsigned long long s_pbase;
@@ -233,7 +241,7 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
     s_over_n = 0;
     s_sel_n = 0;
   }
-  if (threadIdx.x < kTileQ) {
+  if (threadIdx.x < kTQ) {
     s_hits[threadIdx.x] = 0;
     s_lost[threadIdx.x] = 0;
   }
@@ -503,20 +511,31 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
       }
       if ((int)threadIdx.x < nq) s_scur[threadIdx.x] = 0;
       // segments of the sorted area, for the queries with more than k pairs
-      // only (wave 0: an exclusive prefix over s_sel, two entries per lane)
+      // only (wave 0: an exclusive prefix over s_sel, kPer consecutive
+      // entries per lane)
       if (sel_n > 0 && threadIdx.x < 64) {
-        const int j0 = 2 * lane, j1 = 2 * lane + 1;
-        const int v0 = j0 < sel_n ? s_hits[s_sel[j0]] : 0;
-        const int v1 = j1 < sel_n ? s_hits[s_sel[j1]] : 0;
-        int inc = v0 + v1;
+        constexpr int kPer = (kTQ + 63) / 64;
+        int v[kPer];
+        int tot = 0;
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+          const int j = kPer * lane + u;
+          v[u] = j < sel_n ? s_hits[s_sel[j]] : 0;
+          tot += v[u];
+        }
+        int inc = tot;
 #pragma unroll
         for (int o = 1; o < 64; o <<= 1) {
           const int t = __shfl_up(inc, o);
           if (lane >= o) inc += t;
         }
-        const int ex = inc - v0 - v1;
-        if (j0 < sel_n) s_soff[s_sel[j0]] = ex;
-        if (j1 < sel_n) s_soff[s_sel[j1]] = ex + v0;
+        int ex = inc - tot;
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+          const int j = kPer * lane + u;
+          if (j < sel_n) s_soff[s_sel[j]] = ex;
+          ex += v[u];
+        }
       }
       __syncthreads();
       if ((int)threadIdx.x < over_n) {
@@ -906,21 +925,37 @@ bool use_async(int d, int tile_q) {
 
 template <int DT, int D, int kMode, int kNT, int kOcc>
 hipError_t launch_scan_k(ScanArgs a, int32_t grid, hipStream_t s) {
+  // dynamic LDS: what the device's per-work-group LDS leaves beside the
+  // kernel's static LDS, at most kMaxDynLds (the attribute is set to that)
+  static const size_t dyn_max = [] {
+    hipFuncAttributes fa{};
+    int dev = 0, per_block = 0;
+    if (hipFuncGetAttributes(&fa, (const void*)scan_kernel<DT, D, kMode, kNT, kOcc>) !=
+            hipSuccess ||
+        hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&per_block, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) !=
+            hipSuccess)
+      return (size_t)0;
+    const size_t left =
+        (size_t)per_block > fa.sharedSizeBytes ? (size_t)per_block - fa.sharedSizeBytes : 0;
+    return std::min(left, (size_t)kMaxDynLds);
+  }();
+  if (dyn_max == 0) return hipErrorInvalidValue;
   static const hipError_t attr =
       hipFuncSetAttribute((const void*)scan_kernel<DT, D, kMode, kNT, kOcc>,
-                          hipFuncAttributeMaxDynamicSharedMemorySize, kMaxDynLds);
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn_max);
   if (attr != hipSuccess) return attr;
-  if (a.tile_q > kTileQ || a.k < 1 || a.k > 64) return hipErrorInvalidValue;
+  if (a.tile_q > scan_tile_max<kMode, kOcc>() || a.k < 1 || a.k > 64) return hipErrorInvalidValue;
   const size_t one = stage_bytes<DT, D>(a.d, a.tile_q);
   const size_t stage = kMode == kStageAsync ? 2 * one : one;
-  // the LDS arena takes what the staging leaves of the work-group's share of
-  // the CU's 160 KB (its static LDS is about 8 KB), at most kArenaLdsMax
-  const size_t share = kOcc == 1 ? (size_t)kMaxDynLds : (size_t)(72 * 1024);
+  // the LDS arena takes what the staging leaves of the work-group's share,
+  // at most kArenaLdsMax entries
+  const size_t share = kOcc == 1 ? dyn_max : std::min(dyn_max, (size_t)(72 * 1024));
   const size_t room = share > stage ? share - stage : 0;
   a.arena_lds = a.arena_on ? (int32_t)std::min<size_t>(room / sizeof(TileSpill), kArenaLdsMax) : 0;
   if (!a.arena_on) a.spill_cap = 0;
   const size_t lds = stage + (size_t)a.arena_lds * sizeof(TileSpill);
-  if (lds > (size_t)kMaxDynLds) return hipErrorInvalidValue;
+  if (lds > dyn_max) return hipErrorInvalidValue;
   a.stage_u4 = (int32_t)(one / 16);
   a.cand_u4 = (int32_t)(stage / 16);
   hipLaunchKernelGGL((scan_kernel<DT, D, kMode, kNT, kOcc>), dim3(grid), dim3(kNT), lds, s, a);

@@ -80,6 +80,17 @@ constexpr int kOffThreads = 1024;
 
 // tiles non-null: also write the round's tiles and clear the histogram (the
 // work of sched_tiles_kernel), for indexes with few lists per thread.
+// Items per query tile when a list's c items split into ntq = ceil(c / tile_q)
+// tiles: the same share for every tile, in whole 16-query blocks where
+// tile_q allows (tiles of one list then take about the same time, which keeps
+// their reads of the list's rows close together), at most tile_q.  Every
+// tile is non-empty: (ntq - 1) * gs <= (ntq - 1) * tile_q < c.
+__device__ __forceinline__ int group_size(int c, int ntq, int tile_q) {
+  const int share = (c + ntq - 1) / ntq;
+  const int gs = tile_q >= 16 ? (share + 15) / 16 * 16 : share;
+  return min(gs, tile_q);
+}
+
 __global__ __launch_bounds__(kOffThreads) void sched_offsets_kernel(
     int32_t* cnt, const int64_t* __restrict__ list_offsets, int32_t nlist,
     int32_t row_chunk, int32_t tile_q, int32_t* __restrict__ item_off,
@@ -130,6 +141,7 @@ __global__ __launch_bounds__(kOffThreads) void sched_offsets_kernel(
       cnt[p] = 0;
       if (c > 0 && len > 0) {
         const int ntq = (c + tile_q - 1) / tile_q;
+        const int gs = group_size(c, ntq, tile_q);
         const int nch = (int)((len + row_chunk - 1) / row_chunk);
         int32_t o = (int32_t)rt;
         const int64_t lb = list_offsets[p];
@@ -138,8 +150,8 @@ __global__ __launch_bounds__(kOffThreads) void sched_offsets_kernel(
             Tile tl;
             tl.r0 = lb + (int64_t)ch * row_chunk;
             tl.nrows = (int32_t)min<int64_t>(row_chunk, len - (int64_t)ch * row_chunk);
-            tl.item_begin = (int32_t)ri + tq * tile_q;
-            tl.nq = min(tile_q, c - tq * tile_q);
+            tl.item_begin = (int32_t)ri + tq * gs;
+            tl.nq = min(gs, c - tq * gs);
             tl.list = p;
             if (o < tile_cap) tiles[o] = tl;  // past the buffer: reported below
             ++o;
@@ -208,6 +220,7 @@ __global__ void sched_tiles_kernel(int32_t* __restrict__ cnt, const int32_t* __r
   const int64_t len = list_offsets[p + 1] - list_offsets[p];
   if (c == 0 || len == 0) return;
   const int ntq = (c + tile_q - 1) / tile_q;
+  const int gs = group_size(c, ntq, tile_q);
   const int nch = (int)((len + row_chunk - 1) / row_chunk);
   int32_t o = tile_off[p];
   const int64_t lb = list_offsets[p];
@@ -216,8 +229,8 @@ __global__ void sched_tiles_kernel(int32_t* __restrict__ cnt, const int32_t* __r
       Tile t;
       t.r0 = lb + (int64_t)ch * row_chunk;
       t.nrows = (int32_t)min<int64_t>(row_chunk, len - (int64_t)ch * row_chunk);
-      t.item_begin = item_off[p] + tq * tile_q;
-      t.nq = min(tile_q, c - tq * tile_q);
+      t.item_begin = item_off[p] + tq * gs;
+      t.nq = min(gs, c - tq * gs);
       t.list = p;
       if (o < tile_cap) tiles[o] = t;
       ++o;

@@ -40,9 +40,13 @@ struct Hit {
   int64_t id;
 };
 
-// Query-tile width of the scan: 8 blocks of 16 queries (MFMA M = 16).
+// Query-tile width of the scan, in blocks of 16 queries (MFMA M = 16): at
+// most 8 for tiles whose query rows stay in LDS and for the dense-round tiles
+// whose query fragments are held in registers (12-block register tiles read
+// the lists less often but leave too few registers for the row ring).
 constexpr int kQB = 8;
-constexpr int kTileQ = 16 * kQB;
+constexpr int kRegAQB = 8;
+constexpr int kTileQ = 16 * (kQB > kRegAQB ? kQB : kRegAQB);
 constexpr int kScanThreads = 256;  // 4 wave64
 constexpr int kMaxRanks = 2048;    // largest n = min(nprobe_max, nlist)
 constexpr int kMaxNlist = 16384;   // centroid scores of one query fit in LDS
