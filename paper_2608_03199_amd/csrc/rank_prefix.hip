@@ -322,7 +322,10 @@ __global__ __launch_bounds__(kQRWaves * 64, 1) void rank_prefix_qreg_kernel(
         // the previous block's columns that hold real centroids (none before
         // the first block); the epilogue runs branch-free under this mask so
         // that it issues interleaved with this block's MFMAs
-        const bool pok = (u > 0 || it > 0) && pblk * 16 + r16 < nlist;
+        // (blocks past nb are clamped re-loads of block nb - 1: when pass 1
+        // covers a subset, their columns are real centroids seen twice, and
+        // a duplicate kept value could raise the bound)
+        const bool pok = (u > 0 || it > 0) && pblk < nb && pblk * 16 + r16 < nlist;
         multiply();
         const bool need = fast(acc[prev], pok);
 #pragma unroll
