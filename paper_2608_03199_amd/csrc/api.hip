@@ -320,9 +320,9 @@ int grow_workspace(sieve_index* ix, const SearchPlan& pl) {
   if ((st = ensure(ix->have, qn)) || (st = ensure(ix->ext, qn))) return st;
   if ((st = ensure(ix->state_a, qn)) || (st = ensure(ix->state_b, qn)) ||
       (st = ensure(ix->lmax, qn)) || (st = ensure(ix->hcount, qn)) ||
-      (st = ensure(ix->hoff, qn)) || (st = ensure(ix->hcur, qn)))
+      (st = ensure(ix->hoff, (size_t)nq * 8)) || (st = ensure(ix->hcur, (size_t)nq * 8)))
     return st;
-  if ((st = ensure(ix->scan_tmp, exclusive_scan_tmp_elems(nq) * 4))) return st;
+  if ((st = ensure(ix->scan_tmp, exclusive_scan_tmp_elems(nq) * 8))) return st;
   if (pl.spec && (st = ensure(ix->spec_bits, (size_t)nq * pl.hit_words * 4))) return st;
   if ((st = ensure(ix->rlog, (size_t)kMaxLogRounds * sizeof(RoundSnap)))) return st;
   // The pool holds at most k entries per (query, tile); most searches need far
@@ -742,8 +742,8 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     const int64_t limit = pool_index_limit(getenv("SIEVE_POOL_LIMIT"));
     if (!pool_slots_fit(pool_n, limit))
       return fail(SIEVE_EUNSUPPORTED,
-                  "the search wrote %llu candidate-pool entries; the final merge indexes at "
-                  "most %lld (32-bit offsets)", pool_n, (long long)limit);
+                  "the search wrote %llu candidate-pool entries; the final merge takes at "
+                  "most %lld", pool_n, (long long)limit);
     if (hits > ix->pool_cap) {
       // the pool overflowed: grow it and run again (the search is deterministic)
       ix->pool_cap = hits + hits / 8 + 4096;
@@ -754,14 +754,14 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     }
 
     // finalize: group the pool by query, then per-query top-k
-    HIP_TRY(launch_exclusive_scan((const int32_t*)ix->hcount.p, (int32_t*)ix->hoff.p,
-                                  (int32_t*)ix->hcur.p, nq, (int32_t*)ix->scan_tmp.p, s));
-    HIP_TRY(launch_pool_scatter((const Hit*)ix->pool.p, hits, (int32_t*)ix->hcur.p,
+    HIP_TRY(launch_exclusive_scan((const int32_t*)ix->hcount.p, (int64_t*)ix->hoff.p,
+                                  (int64_t*)ix->hcur.p, nq, (int64_t*)ix->scan_tmp.p, s));
+    HIP_TRY(launch_pool_scatter((const Hit*)ix->pool.p, hits, (int64_t*)ix->hcur.p,
                                 (Hit*)ix->pool_sorted.p, cal != nullptr || spec_used, s));
     const int32_t* probes_src = pl.mode == 0   ? (const int32_t*)ix->state_a.p
                                 : pl.mode == 1 ? (const int32_t*)ix->state_b.p
                                                : nullptr;
-    HIP_TRY(launch_topk(nq, pl.k, (const Hit*)ix->pool_sorted.p, (const int32_t*)ix->hoff.p,
+    HIP_TRY(launch_topk(nq, pl.k, (const Hit*)ix->pool_sorted.p, (const int64_t*)ix->hoff.p,
                         (const int32_t*)ix->hcount.p, probes_src, pl.n, out_map, out_ids,
                         out_scores, out_probes, cal ? cal->frank : nullptr,
                         spec_used ? (const int32_t*)ix->state_a.p : nullptr, rc, s));

@@ -7,13 +7,14 @@
 
 namespace sieve {
 
-// The final merge groups the candidate pool by query with 32-bit per-query
+// The final merge groups the candidate pool by query with 64-bit per-query
 // offsets (exclusive scan of the counts, scatter cursors, segment starts), so
-// a search may hold at most INT32_MAX candidate slots.  knob: the value of an
+// the limit on candidate slots is a sanity bound, 2^38, far more than device
+// memory holds (the pool's allocation fails first).  knob: the value of an
 // override (tests lower the limit to reach the error path without filling
 // memory); null, empty or non-positive means no override.
 inline int64_t pool_index_limit(const char* knob) {
-  const int64_t hard = 0x7fffffffll;
+  const int64_t hard = (int64_t)1 << 38;
   if (!knob || !*knob) return hard;
   const long long v = atoll(knob);
   return v > 0 && v < hard ? (int64_t)v : hard;

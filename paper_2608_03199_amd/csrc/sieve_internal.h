@@ -280,8 +280,8 @@ struct FillSegs {
 };
 hipError_t launch_fill_multi(const FillSegs& f, hipStream_t s);
 hipError_t launch_zero_bytes(void* p, int64_t bytes, hipStream_t s);
-hipError_t launch_exclusive_scan(const int32_t* in, int32_t* out, int32_t* out_copy, int64_t n,
-                                 int32_t* block_tmp, hipStream_t s);
+hipError_t launch_exclusive_scan(const int32_t* in, int64_t* out, int64_t* out_copy, int64_t n,
+                                 int64_t* block_tmp, hipStream_t s);
 size_t exclusive_scan_tmp_elems(int64_t n);
 // Exact top-k pass over the overflowed (tile, query) groups: one wave per
 // HeavyRec selects each query's top k (score desc, id asc) among the tile's
@@ -305,7 +305,7 @@ hipError_t launch_scan_heavy(int dtype, const HeavyArgs& a, int32_t grid, hipStr
 // Pool entries of a calibration search pack the rank into Hit.q.
 constexpr int kRankShift = 20;  // queries < 2^20, ranks < 2^11 (kMaxRanks)
 constexpr int32_t kQueryMask = (1 << kRankShift) - 1;
-hipError_t launch_pool_scatter(const Hit* pool, int64_t n, int32_t* cursor, Hit* sorted,
+hipError_t launch_pool_scatter(const Hit* pool, int64_t n, int64_t* cursor, Hit* sorted,
                                bool packed, hipStream_t s);
 // out_map: null, or [nq] output row of each query (results of query q go to
 // row out_map[q] of out_ids / out_scores / out_probes).  out_rank: null, or
@@ -313,7 +313,7 @@ hipError_t launch_pool_scatter(const Hit* pool, int64_t n, int32_t* cursor, Hit*
 // returned candidate was found at (-1 for padding); needs packed pool entries.
 // rank_limit: null, or [nq] -- pool entries (packed) found at a rank >= the
 // query's limit are left out (speculatively scanned ranks past the stop line).
-hipError_t launch_topk(int64_t nq, int32_t k, const Hit* sorted, const int32_t* hoff,
+hipError_t launch_topk(int64_t nq, int32_t k, const Hit* sorted, const int64_t* hoff,
                        const int32_t* hcount, const int32_t* probes_src, int32_t probes_const,
                        const int32_t* out_map, int64_t* out_ids, float* out_scores,
                        int32_t* out_probes, int32_t* out_rank, const int32_t* rank_limit,

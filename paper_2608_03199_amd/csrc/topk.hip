@@ -21,28 +21,30 @@ constexpr int kScanBlock = 1024;
 constexpr int kScanPer = 4;
 constexpr int kScanTile = kScanBlock * kScanPer;
 
-// In-block exclusive scan of kScanTile int32 values starting at base; returns
-// the block total through *total.
-__device__ void block_scan_tile(const int32_t* in, int32_t* out, int32_t* out2, int64_t n,
-                                int64_t base, int32_t add, int32_t* total) {
-  __shared__ int32_t s[kScanBlock];
+// In-block exclusive scan of kScanTile values starting at base, in 64-bit
+// sums (a search may write more than 2^31 pool entries); returns the block
+// total through *total.
+template <typename TIn>
+__device__ void block_scan_tile(const TIn* in, int64_t* out, int64_t* out2, int64_t n,
+                                int64_t base, int64_t add, int64_t* total) {
+  __shared__ int64_t s[kScanBlock];
   const int t = threadIdx.x;
-  int32_t v[kScanPer];
-  int32_t sum = 0;
+  int64_t v[kScanPer];
+  int64_t sum = 0;
   for (int e = 0; e < kScanPer; ++e) {
     const int64_t i = base + (int64_t)t * kScanPer + e;
-    v[e] = i < n ? in[i] : 0;
+    v[e] = i < n ? (int64_t)in[i] : 0;
     sum += v[e];
   }
   s[t] = sum;
   __syncthreads();
   for (int off = 1; off < kScanBlock; off <<= 1) {
-    const int32_t x = t >= off ? s[t - off] : 0;
+    const int64_t x = t >= off ? s[t - off] : 0;
     __syncthreads();
     s[t] += x;
     __syncthreads();
   }
-  int32_t run = s[t] - sum + add;
+  int64_t run = s[t] - sum + add;
   if (out) {
     for (int e = 0; e < kScanPer; ++e) {
       const int64_t i = base + (int64_t)t * kScanPer + e;
@@ -58,21 +60,21 @@ __device__ void block_scan_tile(const int32_t* in, int32_t* out, int32_t* out2, 
 }
 
 __global__ __launch_bounds__(kScanBlock) void scan_partials_kernel(const int32_t* in, int64_t n,
-                                                                  int32_t* partial) {
+                                                                  int64_t* partial) {
   block_scan_tile(in, nullptr, nullptr, n, (int64_t)blockIdx.x * kScanTile, 0,
                   &partial[blockIdx.x]);
 }
 
-__global__ __launch_bounds__(kScanBlock) void scan_partials_top_kernel(int32_t* partial,
+__global__ __launch_bounds__(kScanBlock) void scan_partials_top_kernel(int64_t* partial,
                                                                       int32_t nparts) {
   // nparts <= kScanTile: exclusive scan in place
-  __shared__ int32_t tot;
+  __shared__ int64_t tot;
   block_scan_tile(partial, partial, nullptr, nparts, 0, 0, &tot);
 }
 
 __global__ __launch_bounds__(kScanBlock) void scan_apply_kernel(const int32_t* in, int64_t n,
-                                                               const int32_t* partial,
-                                                               int32_t* out, int32_t* out2) {
+                                                               const int64_t* partial,
+                                                               int64_t* out, int64_t* out2) {
   block_scan_tile(in, out, out2, n, (int64_t)blockIdx.x * kScanTile, partial[blockIdx.x],
                   nullptr);
 }
@@ -82,9 +84,9 @@ __global__ __launch_bounds__(kScanBlock) void scan_apply_kernel(const int32_t* i
 constexpr int kScanSingleTiles = 16;
 
 __global__ __launch_bounds__(kScanBlock) void scan_single_kernel(const int32_t* in, int64_t n,
-                                                                int32_t* out, int32_t* out2) {
-  __shared__ int32_t tot;
-  int32_t carry = 0;
+                                                                int64_t* out, int64_t* out2) {
+  __shared__ int64_t tot;
+  int64_t carry = 0;
   for (int64_t base = 0; base < n; base += kScanTile) {
     block_scan_tile(in, out, out2, n, base, carry, &tot);  // ends with a barrier
     carry += tot;
@@ -96,35 +98,40 @@ __global__ __launch_bounds__(kScanBlock) void scan_single_kernel(const int32_t* 
 // wave's 64 entries (a tile appends the candidates of a few queries row after
 // row, so neighbouring entries mostly share queries, and one-address atomics
 // serialise).  The order inside a query's segment is free: the top-k merge
-// uses a total order.
+// uses a total order.  Grid-stride over the pool in whole work-groups: a
+// dispatch holds at most 2^32 work-items, fewer than a large pool's entries.
 __global__ __launch_bounds__(256) void pool_scatter_kernel(const Hit* __restrict__ pool, int64_t n,
-                                                           int32_t* __restrict__ cursor,
+                                                           int64_t* __restrict__ cursor,
                                                            Hit* __restrict__ sorted,
                                                            int32_t qmask) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int lane = threadIdx.x & 63;
-  Hit h = {-INFINITY, -1, -1};
-  if (i < n) h = pool[i];
-  const int q = h.q < 0 ? -1 : (h.q & qmask);  // -1: past the end
-  // group the lanes by query (register work only), then every group's first
-  // lane claims the group's slots, all groups at once
-  unsigned long long todo = __ballot(q >= 0);
-  int leader = lane, rank = 0, count = 0;
-  while (todo) {  // wave-uniform
-    const int first = __builtin_ctzll(todo);
-    const int qf = __shfl(q, first);
-    const unsigned long long same = __ballot(q == qf);
-    if (q == qf) {
-      leader = first;
-      rank = __popcll(same & ((1ull << lane) - 1ull));
-      count = __popcll(same);
+  for (int64_t b0 = (int64_t)blockIdx.x * blockDim.x; b0 < n;
+       b0 += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = b0 + threadIdx.x;
+    Hit h = {-INFINITY, -1, -1};
+    if (i < n) h = pool[i];
+    const int q = h.q < 0 ? -1 : (h.q & qmask);  // -1: past the end
+    // group the lanes by query (register work only), then every group's first
+    // lane claims the group's slots, all groups at once
+    unsigned long long todo = __ballot(q >= 0);
+    int leader = lane, rank = 0, count = 0;
+    while (todo) {  // wave-uniform
+      const int first = __builtin_ctzll(todo);
+      const int qf = __shfl(q, first);
+      const unsigned long long same = __ballot(q == qf);
+      if (q == qf) {
+        leader = first;
+        rank = __popcll(same & ((1ull << lane) - 1ull));
+        count = __popcll(same);
+      }
+      todo &= ~same;
     }
-    todo &= ~same;
+    long long base = 0;
+    if (q >= 0 && rank == 0)
+      base = (long long)atomicAdd((unsigned long long*)&cursor[q], (unsigned long long)count);
+    base = __shfl(base, leader);
+    if (q >= 0) sorted[base + rank] = h;
   }
-  int base = 0;
-  if (q >= 0 && rank == 0) base = atomicAdd(&cursor[q], count);
-  base = __shfl(base, leader);
-  if (q >= 0) sorted[base + rank] = h;
 }
 
 // One wave per query, grid-stride over the queries; each block adds its
@@ -133,7 +140,7 @@ __global__ __launch_bounds__(256) void pool_scatter_kernel(const Hit* __restrict
 template <bool kRank>
 __global__ __launch_bounds__(256) void topk_kernel(int64_t nq, int32_t k,
                                                    const Hit* __restrict__ sorted,
-                                                   const int32_t* __restrict__ hoff,
+                                                   const int64_t* __restrict__ hoff,
                                                    const int32_t* __restrict__ hcount,
                                                    const int32_t* __restrict__ probes_src,
                                                    int32_t probes_const,
@@ -150,7 +157,7 @@ __global__ __launch_bounds__(256) void topk_kernel(int64_t nq, int32_t k,
   const Cand none = {-INFINITY, 0x7fffffffffffffffll, -1};
   for (int64_t q = (int64_t)blockIdx.x * 4 + wave; q < nq; q += (int64_t)gridDim.x * 4) {
     const int m = hcount[q];
-    const int beg = m > 0 ? hoff[q] : 0;
+    const int64_t beg = m > 0 ? hoff[q] : 0;
     const int lim = rank_limit ? rank_limit[q] : 0x7fffffff;
     Cand top = none;
     for (int b = 0; b < m; b += 64) {
@@ -262,8 +269,8 @@ hipError_t launch_merge_shards(int64_t nq, int32_t k, int32_t nshard, const int6
 
 size_t exclusive_scan_tmp_elems(int64_t n) { return (size_t)((n + kScanTile - 1) / kScanTile) + 1; }
 
-hipError_t launch_exclusive_scan(const int32_t* in, int32_t* out, int32_t* out_copy, int64_t n,
-                                 int32_t* block_tmp, hipStream_t s) {
+hipError_t launch_exclusive_scan(const int32_t* in, int64_t* out, int64_t* out_copy, int64_t n,
+                                 int64_t* block_tmp, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   const int64_t nb = (n + kScanTile - 1) / kScanTile;
   if (nb > kScanTile) return hipErrorInvalidValue;
@@ -280,15 +287,17 @@ hipError_t launch_exclusive_scan(const int32_t* in, int32_t* out, int32_t* out_c
   return hipGetLastError();
 }
 
-hipError_t launch_pool_scatter(const Hit* pool, int64_t n, int32_t* cursor, Hit* sorted,
+hipError_t launch_pool_scatter(const Hit* pool, int64_t n, int64_t* cursor, Hit* sorted,
                                bool packed, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(pool_scatter_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, pool,
-                     n, cursor, sorted, packed ? kQueryMask : (int32_t)0x7fffffff);
+  const int64_t want = (n + 255) / 256;
+  const unsigned blocks = (unsigned)(want < (1 << 20) ? want : (1 << 20));
+  hipLaunchKernelGGL(pool_scatter_kernel, dim3(blocks), dim3(256), 0, s, pool, n, cursor, sorted,
+                     packed ? kQueryMask : (int32_t)0x7fffffff);
   return hipGetLastError();
 }
 
-hipError_t launch_topk(int64_t nq, int32_t k, const Hit* sorted, const int32_t* hoff,
+hipError_t launch_topk(int64_t nq, int32_t k, const Hit* sorted, const int64_t* hoff,
                        const int32_t* hcount, const int32_t* probes_src, int32_t probes_const,
                        const int32_t* out_map, int64_t* out_ids, float* out_scores,
                        int32_t* out_probes, int32_t* out_rank, const int32_t* rank_limit,

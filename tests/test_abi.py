@@ -116,16 +116,17 @@ def test_no_cpu_fallback_in_binding():
 
 
 def test_pool_index_limit_host_rule(tmp_path):
-    """The candidate-pool guard: a search may hold at most INT32_MAX pool slots (the final
-    merge indexes the pool with 32-bit offsets); the override only lowers the limit."""
+    """The candidate-pool guard: a search may hold at most 2^38 pool slots (a sanity bound
+    far above device memory: the final merge uses 64-bit offsets); the override only lowers
+    the limit."""
     src = tmp_path / "limits.cpp"
     src.write_text(
         '#include <stdio.h>\n#include "host_limits.h"\nusing namespace sieve;\nint main(){'
         'printf("%lld %lld %lld %lld %lld\\n", (long long)pool_index_limit(0),'
         ' (long long)pool_index_limit(""), (long long)pool_index_limit("1000"),'
         ' (long long)pool_index_limit("-5"), (long long)pool_index_limit("99999999999"));'
-        'printf("%d %d %d %d\\n", pool_slots_fit(2147483647ull, pool_index_limit(0)),'
-        ' pool_slots_fit(2147483648ull, pool_index_limit(0)), pool_slots_fit(1000, 1000),'
+        'printf("%d %d %d %d\\n", pool_slots_fit(274877906944ull, pool_index_limit(0)),'
+        ' pool_slots_fit(274877906945ull, pool_index_limit(0)), pool_slots_fit(1000, 1000),'
         ' pool_slots_fit(1001, 1000));return 0;}\n')
     exe = tmp_path / "limits"
     csrc = os.path.join(ROOT, "paper_2608_03199_amd", "csrc")
@@ -133,5 +134,6 @@ def test_pool_index_limit_host_rule(tmp_path):
                     str(exe)], check=True)
     lines = subprocess.run([str(exe)], capture_output=True, text=True,
                            check=True).stdout.split("\n")
-    assert lines[0].split() == ["2147483647", "2147483647", "1000", "2147483647", "2147483647"]
+    assert lines[0].split() == ["274877906944", "274877906944", "1000", "274877906944",
+                                "99999999999"]
     assert lines[1].split() == ["1", "0", "1", "0"]

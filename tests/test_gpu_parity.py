@@ -592,7 +592,7 @@ def test_pool_index_limit_gives_a_clean_error():
     try:
         with pytest.raises(ps.SieveError) as e:
             c.ix.search(c.w.queries, c.w.exclude_ids, s.k, 0.3, s.W, s.nprobe_max)
-        assert e.value.code == -4 and "32-bit" in str(e.value)
+        assert e.value.code == -4 and "candidate-pool entries" in str(e.value)
     finally:
         del os.environ["SIEVE_POOL_LIMIT"]
     _check(c, s.k, s.tau, s.W, s.nprobe_max)
