@@ -261,6 +261,8 @@ struct SearchPlan {
   bool wide;           // wide scan configuration (see tile_rows_wide)
   int scan_grid;       // scan work-groups (fixed for the whole search)
   bool wide_rank;      // rank with room for every boundary near-tie (retry path)
+  int rank_div;        // register-query prefix ranking: first pass over 1/rank_div of the
+                       // centroids (a looser bound; 1 after an overflow)
   bool spec;           // lookahead with speculative issue past the stop line
   int spec_round;      // first round whose update speculates
   int spec_max;        // ranks issued past the stop line, at most
@@ -378,7 +380,8 @@ int rank_queries_in(const sieve_index* ix, const void* queries, int64_t q0, int6
     for (int64_t a = 0; a < cnt; a += chunk_prefix) {
       const int32_t c = (int32_t)((cnt - a) < chunk_prefix ? (cnt - a) : chunk_prefix);
       HIP_TRY(launch_rank_prefix(ix->dtype, queries, q0 + a, c, ix->centroids, ix->nlist, ix->d,
-                                 nsel, ix->cmax, cand, ccount, P + a * ldp, ldp, rc, s));
+                                 nsel, ix->cmax, cand, ccount, P + a * ldp, ldp, rc, pl.rank_div,
+                                 s));
     }
     return SIEVE_OK;
   }
@@ -696,6 +699,12 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
       sm.hits = ix->rc_host->hits;
     }
     if (sm.rank_error) {
+      // a query's rank candidates overflowed: first with the first pass over
+      // every centroid (the tight bound), then with the wide buffers
+      if (pl.rank_div > 1 && !pl.wide_rank) {
+        pl.rank_div = 1;
+        continue;
+      }
       if (pl.wide_rank)
         return fail(SIEVE_EUNSUPPORTED,
                     "more than %d centroids tie within the fp32 screening bound at a rank "
@@ -832,6 +841,10 @@ int plan_search(const sieve_index* ix, int64_t nq, int32_t k, float tau, int32_t
   pl->group_q = pl->tile_q;
   pl->min_group = pl->rega ? scan_rega_tile_q(false) : pl->tile_q;
   pl->wide_rank = false;
+  // the register-query prefix ranking bounds the R-th score from the first
+  // half of the centroids (any subset's R-th largest score is a valid lower
+  // bound); a query whose candidates then overflow re-ranks with the full pass
+  pl->rank_div = env_int("SIEVE_RANK_PASS1_DIV", 2);
   // sparse rounds: 1,024-row tiles for register-held queries (a tile's start
   // drains its row ring once), else 512
   pl->row_chunk = row_chunk_for(ix, "SIEVE_ROW_CHUNK", pl->rega ? 1024 : 512);
@@ -1094,8 +1107,12 @@ SIEVE_API int sieve_rank(const sieve_index* idx, const void* queries, int64_t nq
   if ((st = ensure(ix->rc, sizeof(RoundCounters)))) return st;
   if (!ix->rc_host) HIP_TRY(hipHostMalloc((void**)&ix->rc_host, sizeof(RoundCounters), 0));
   RoundCounters* rc = (RoundCounters*)ix->rc.p;
-  for (int attempt = 0; attempt < 2; ++attempt) {
-    pl.wide_rank = attempt > 0;
+  const int div0 = pl.rank_div;
+  for (int attempt = 0; attempt < 3; ++attempt) {
+    // the first pass over a subset, then over every centroid, then wide buffers
+    if (attempt == 1 && div0 <= 1) continue;
+    pl.rank_div = attempt == 0 ? div0 : 1;
+    pl.wide_rank = attempt == 2;
     HIP_TRY(launch_zero_bytes(rc, sizeof(RoundCounters), s));
     if ((st = rank_queries(ix, queries, 0, nq, pl.n, pl.n, pl, out_order, s))) return st;
     HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost, s));
@@ -1166,8 +1183,12 @@ SIEVE_API int sieve_rank_noalloc(const sieve_index* idx, const void* queries, in
   RoundCounters* rc = (RoundCounters*)base;
   unsigned char* ws = base + kHead;
   const size_t ws_bytes = kScratchBytes - kHead;
-  for (int attempt = 0; attempt < 2; ++attempt) {
-    pl.wide_rank = attempt > 0;
+  const int div0 = pl.rank_div;
+  for (int attempt = 0; attempt < 3; ++attempt) {
+    // the first pass over a subset, then over every centroid, then wide buffers
+    if (attempt == 1 && div0 <= 1) continue;
+    pl.rank_div = attempt == 0 ? div0 : 1;
+    pl.wide_rank = attempt == 2;
     // queries per chunk that fit the workspace
     unsigned long long* cand = nullptr;
     int32_t* ccount = nullptr;

@@ -559,7 +559,7 @@ int rank_prefix_cap(int32_t R, int32_t nlist) {
 hipError_t launch_rank_prefix(int dtype, const void* queries, int64_t q0, int32_t nqc,
                               const void* centroids, int32_t nlist, int32_t d, int32_t R,
                               double cmax, unsigned long long* cand, int32_t* ccount, int32_t* P,
-                              int64_t ldp, RoundCounters* rc, hipStream_t s) {
+                              int64_t ldp, RoundCounters* rc, int32_t pass1_div, hipStream_t s) {
   if (nqc <= 0) return hipSuccess;
   if (R < 1 || R > kRankPrefixMax || R > nlist) return hipErrorInvalidValue;
   const int cap = rank_prefix_cap(R, nlist);
@@ -571,8 +571,7 @@ hipError_t launch_rank_prefix(int dtype, const void* queries, int64_t q0, int32_
     // so more candidates, for a shorter first pass.  Every wave keeps at least
     // four blocks, so every kept value is finite.
     const int nblk = (nlist + 15) / 16;
-    const char* dv = getenv("SIEVE_RANK_PASS1_DIV");
-    const int div = dv && atoi(dv) > 1 ? atoi(dv) : 1;
+    const int div = pass1_div > 1 ? pass1_div : 1;
     int nblk1 = (nblk + div - 1) / div;
     if (nblk1 < 4 * kQRSplit) nblk1 = nblk < 4 * kQRSplit ? nblk : 4 * kQRSplit;
     hipLaunchKernelGGL((rank_prefix_qreg_kernel<128>), dim3(grid), dim3(kQRWaves * 64), 0, s,

@@ -211,7 +211,7 @@ int rank_prefix_cap(int32_t R, int32_t nlist);
 hipError_t launch_rank_prefix(int dtype, const void* queries, int64_t q0, int32_t nqc,
                               const void* centroids, int32_t nlist, int32_t d, int32_t R,
                               double cmax, unsigned long long* cand, int32_t* ccount, int32_t* P,
-                              int64_t ldp, RoundCounters* rc, hipStream_t s);
+                              int64_t ldp, RoundCounters* rc, int32_t pass1_div, hipStream_t s);
 hipError_t launch_rank_select(int dtype, const void* queries, int64_t q0, int32_t nqc,
                               const void* centroids, int32_t nlist, int32_t d, const float* scores,
                               int32_t n, double cmax, int32_t* P, int64_t ldp, RoundCounters* rc,
