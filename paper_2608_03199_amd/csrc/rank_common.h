@@ -180,14 +180,19 @@ __device__ __forceinline__ void finish_candidates_wave(
     link[i] = l ? 1 : 0;
   }
   wave_sync();
+  // Only positions [0, n) are written, and a run only reorders its own
+  // members: runs that start at or past n cannot change them.  The candidates
+  // that matter end with the run holding position n - 1.
+  int me = n < m ? n : m;
+  while (me < m && link[me - 1]) ++me;
   // 4c. fp64 scores of run members (this wave alone)
-  refine_members<DT>(out, cs, link, m, queries, qg, centroids, d, 0, 1);
+  refine_members<DT>(out, cs, link, me, queries, qg, centroids, d, 0, 1);
   wave_sync();
   // 4d. order inside each run (exact sequential sums where tier 1 is too close)
   {
     const double gap64 =
         2.0 * 2.0 * (double)(d + (d + 63) / 64 + 6) * 1.1102230246251565e-16 * qn * cmax + 1e-300;
-    order_runs<DT>(out, cs, link, m, queries, qg, centroids, d, gap64, lane, 64);
+    order_runs<DT>(out, cs, link, me, queries, qg, centroids, d, gap64, lane, 64);
   }
   wave_sync();
   for (int r = lane; r < n; r += 64) Prow[r] = (int32_t)(out[r] & 0xffffffffu);
