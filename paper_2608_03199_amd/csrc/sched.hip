@@ -77,6 +77,7 @@ __global__ __launch_bounds__(kInitThreads) void emit_initial_kernel(
 // One work-group: exclusive scans over the lists of the item histogram and
 // of the per-list tile counts; resets the round's counters.
 constexpr int kOffThreads = 1024;
+constexpr int kOffPer = (kMaxNlist + kOffThreads - 1) / kOffThreads;  // lists per thread, at most
 
 // tiles non-null: also write the round's tiles and clear the histogram (the
 // work of sched_tiles_kernel), for indexes with few lists per thread.
@@ -99,14 +100,44 @@ __global__ __launch_bounds__(kOffThreads) void sched_offsets_kernel(
   __shared__ int64_t s_items[kOffThreads];
   __shared__ int64_t s_tiles[kOffThreads];
   __shared__ unsigned long long s_stat[3];
+  // every list's item count and length (rows < 2^31, checked at load) in
+  // LDS: the loads are coalesced and all in flight at once, and each thread
+  // then reads its own contiguous range of lists from LDS
+  extern __shared__ int32_t s_lists[];  // [nlist] counts, then [nlist] lengths
+  int32_t* const s_c = s_lists;
+  int32_t* const s_l = s_lists + nlist;
   const int t = threadIdx.x;
+  {
+    int32_t cv[kOffPer];
+    int64_t a0[kOffPer], a1[kOffPer];
+#pragma unroll
+    for (int u = 0; u < kOffPer; ++u) {
+      const int p = u * kOffThreads + t;
+      cv[u] = 0;
+      a0[u] = a1[u] = 0;
+      if (p < nlist) {
+        cv[u] = cnt[p];
+        a0[u] = list_offsets[p];
+        a1[u] = list_offsets[p + 1];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kOffPer; ++u) {
+      const int p = u * kOffThreads + t;
+      if (p < nlist) {
+        s_c[p] = cv[u];
+        s_l[p] = (int32_t)(a1[u] - a0[u]);
+      }
+    }
+  }
+  __syncthreads();
   const int per = (nlist + kOffThreads - 1) / kOffThreads;
   const int b = t * per, e = min(nlist, b + per);
   int64_t si = 0, st = 0;
   unsigned long long list_rows = 0, item_rows = 0, loads = 0;
   for (int p = b; p < e; ++p) {
-    const int64_t len = list_offsets[p + 1] - list_offsets[p];
-    const int c = cnt[p];
+    const int64_t len = s_l[p];
+    const int c = s_c[p];
     si += c;
     if (c > 0 && len > 0) {
       st += (int64_t)((c + tile_q - 1) / tile_q) * ((len + row_chunk - 1) / row_chunk);
@@ -130,8 +161,8 @@ __global__ __launch_bounds__(kOffThreads) void sched_offsets_kernel(
   }
   int64_t ri = s_items[t] - si, rt = s_tiles[t] - st;  // exclusive prefixes
   for (int p = b; p < e; ++p) {
-    const int64_t len = list_offsets[p + 1] - list_offsets[p];
-    const int c = cnt[p];
+    const int64_t len = s_l[p];
+    const int c = s_c[p];
     item_off[p] = (int32_t)ri;
     cursor[p] = (int32_t)ri;
     tile_off[p] = (int32_t)rt;
@@ -530,8 +561,14 @@ hipError_t launch_sched_offsets(int32_t* cnt, const int64_t* list_offsets, int32
                                 int32_t* cursor, int32_t* tile_off, RoundCounters* rc,
                                 Tile* tiles, int64_t tile_cap, hipStream_t s) {
   if (tiles && nlist > kFuseTilesMaxLists) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(sched_offsets_kernel, dim3(1), dim3(kOffThreads), 0, s, cnt, list_offsets,
-                     nlist, row_chunk, tile_q, item_off, cursor, tile_off, rc, tiles, tile_cap);
+  static const hipError_t attr =
+      hipFuncSetAttribute((const void*)sched_offsets_kernel,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, 8 * kMaxNlist);
+  if (attr != hipSuccess) return attr;
+  if (nlist > kMaxNlist) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(sched_offsets_kernel, dim3(1), dim3(kOffThreads), (size_t)8 * nlist, s, cnt,
+                     list_offsets, nlist, row_chunk, tile_q, item_off, cursor, tile_off, rc, tiles,
+                     tile_cap);
   return hipGetLastError();
 }
 
