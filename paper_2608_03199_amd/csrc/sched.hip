@@ -314,7 +314,8 @@ __device__ __forceinline__ void lookahead_one(int64_t q, const int32_t* __restri
                                               int32_t* __restrict__ cnt, RoundCounters* rc,
                                               const uint32_t* __restrict__ hitbits,
                                               int32_t words, int32_t* __restrict__ issued,
-                                              int32_t spec_max, int32_t spec_min) {
+                                              int32_t spec_max, int32_t spec_min, int* emit_from,
+                                              int* emit_n) {
   const int L = lmax[q];  // 1-based highest hit rank of this round, 0 = none
   if (L == 0) return;
   lmax[q] = 0;
@@ -326,14 +327,9 @@ __device__ __forceinline__ void lookahead_one(int64_t q, const int32_t* __restri
     if (reach <= s) return;
     const int e0 = min(s, hv), e1 = min(reach, hv);  // emitted so far / after this update
     if (e1 > e0) {
-      const int base = atomicAdd(&rc->new_items, e1 - e0);
-      for (int j = e0; j < e1; ++j) {
-        Item it;
-        it.q = (int32_t)q;
-        it.rank = j;
-        if ((int64_t)(uint32_t)base + (j - e0) < item_cap) items[base + (j - e0)] = it;
-        atomicAdd(&cnt[P[q * n + j]], 1);
-      }
+      // ranks [e0, e1) are emitted by the caller, after one claim per wave
+      *emit_from = e0;
+      *emit_n = e1 - e0;
       if (issued) issued[q] = e1;
     }
     if (reach > hv) ext[atomicAdd(&rc->n_ext, 1)] = (int32_t)q;
@@ -398,9 +394,34 @@ __global__ void update_lookahead_kernel(int64_t nq, const int32_t* __restrict__ 
                                         int32_t* __restrict__ issued, int32_t spec_max,
                                         int32_t spec_min, RoundSummary* out) {
   const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int e0 = 0, ne = 0;
   if (q < nq)
     lookahead_one(q, P, n, W, stop, lmax, have, ext, items, item_cap, cnt, rc, hitbits, words, issued,
-                  spec_max, spec_min);
+                  spec_max, spec_min, &e0, &ne);
+  // The new items of the committed path: one claim on the item counter per
+  // wave (a one-address atomic per query would serialise the first round's
+  // updates), each lane's share at its prefix of the wave's claim.
+  const int lane = threadIdx.x & 63;
+  int inc = ne;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int t = __shfl_up(inc, o);
+    if (lane >= o) inc += t;
+  }
+  const int total = __shfl(inc, 63);
+  int wbase = 0;
+  if (lane == 63 && total > 0) wbase = atomicAdd(&rc->new_items, total);
+  wbase = __shfl(wbase, 63);
+  if (ne > 0) {
+    const int base = wbase + inc - ne;
+    for (int j = 0; j < ne; ++j) {
+      Item it;
+      it.q = (int32_t)q;
+      it.rank = e0 + j;
+      if ((int64_t)(uint32_t)base + j < item_cap) items[base + j] = it;
+      atomicAdd(&cnt[P[q * n + e0 + j]], 1);
+    }
+  }
   if (out) publish_from_block(rc, out);  // one work-group only
 }
 
