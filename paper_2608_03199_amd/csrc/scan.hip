@@ -176,6 +176,8 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
   const int ntiles = a.rc->ntiles;
   const char* qbase = (const char*)a.queries;
   __shared__ int s_claim;
+  __shared__ int s_next;  // one-ahead claims: the tile claimed at this tile's start
+  constexpr bool kShallow = kMode == kStageRegA && kOcc == 1;
 
   // Tile schedule: the round's tiles are split into 8 contiguous ranges, one
   // per XCD (block b runs on XCD b % 8, so tiles of one list share that XCD's
@@ -230,13 +232,20 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
   };
 
   // four claims ahead: t (runs), tn (stages), ta (items load), tb (record
-  // loads); thread 0 claims the next one under each tile's MFMAs
+  // loads); thread 0 claims the next one under each tile's MFMAs.  The dense
+  // register-query kernel (kShallow) claims one tile ahead instead: it claims
+  // tile t+1 at the start of tile t, loads its record and items under t's
+  // row stream and stages its queries under t's end.  Its tiles are long, so
+  // the chain fits in one tile, and a list's query tiles, claimed one after
+  // another, then start within about one tile duration of each other instead
+  // of four: they read the list's rows closer together, and more of those
+  // reads hit L2.
   __shared__ int s_first[4];
   if (threadIdx.x == 0) {
     s_first[0] = claim();
-    s_first[1] = claim();
-    s_first[2] = claim();
-    s_first[3] = claim();
+    s_first[1] = kShallow ? -1 : claim();
+    s_first[2] = kShallow ? -1 : claim();
+    s_first[3] = kShallow ? -1 : claim();
     s_pool_n = 0;
     s_over_n = 0;
     s_sel_n = 0;
@@ -267,7 +276,7 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
     const int qb_n = (nq + 15) >> 4;
     const int64_t r0 = recT.r0, r1 = recT.r0 + recT.nrows;
     // the next tile's items go to the other set
-    put_items(nset, recN, itN);
+    if constexpr (!kShallow) put_items(nset, recN, itN);
     BItem itA;
     Tile recB;
     int t_claim = -1;
@@ -385,19 +394,36 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
         constexpr int QB = decltype(qbc)::value;
         constexpr int kNC = D / DTraits<DT>::kChunkDims;
         u32x4 qf[kNC][QB];
+        int nxt = -1;
+        if constexpr (kShallow) {
+          if (threadIdx.x == 0) nxt = claim();
+        }
         load_afrags<DT, D, QB>(lds, g.segs, qf);
         __builtin_amdgcn_s_waitcnt(0);  // fragments in registers
+        if constexpr (kShallow) {
+          if (threadIdx.x == 0) s_next = nxt;
+        }
         __syncthreads();  // every wave has its fragments: the staging buffer is free
-        if (threadIdx.x == 0) t_claim = claim();  // published at the end of this tile
-        // pipeline loads, used one tile from now
-        itA = load_items(recA);
-        recB = load_rec(tb);
+        if constexpr (kShallow) {
+          tn = s_next;
+          recN = load_rec(tn);
+          itN = load_items(recN);
+        } else {
+          if (threadIdx.x == 0) t_claim = claim();  // published at the end of this tile
+          // pipeline loads, used one tile from now
+          itA = load_items(recA);
+          recB = load_rec(tb);
+        }
         stream_rows_rega<DT, D, QB, kOcc == 1 ? 512 : 256>(qf, (const char*)a.vectors, row_bytes,
                                                             r0, r1, vote, candidates);
         // The next tile's queries are staged after the stream, under the end
         // of this tile: an LDS-DMA load in flight during the stream makes the
         // compiler wait for every load there, not just the oldest ones.
-        if (tn >= 0) dma_stage<DT>(lds, g, qbase, row_bytes, s_q[nset], recN.nq);
+        if constexpr (kShallow) {
+          put_items(nset, recN, itN);  // staged after the barrier below
+        } else {
+          if (tn >= 0) dma_stage<DT>(lds, g, qbase, row_bytes, s_q[nset], recN.nq);
+        }
       });
     } else {
       __syncthreads();
@@ -423,6 +449,9 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
     // this wave's staging copies and arena stores are complete (in L2)
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();  // every wave is done with this tile's queries, items and candidates
+    if constexpr (kShallow) {
+      if (tn >= 0) dma_stage<DT>(lds, g, qbase, row_bytes, s_q[nset], recN.nq);
+    }
     // the arena's parts: pairs held per wave, their prefix; any global part?
     int wn[kNT / 64], wpre[kNT / 64 + 1];
     bool ext = false;
@@ -707,7 +736,14 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
       s_over_n = 0;
       s_sel_n = 0;
     }
+    if constexpr (kShallow) __builtin_amdgcn_s_waitcnt(0);  // the next tile's staging
     __syncthreads();
+    if constexpr (kShallow) {
+      t = tn;
+      recT = recN;
+      set = nset;
+      continue;
+    }
     t = tn;
     tn = ta;
     ta = tb;
