@@ -567,7 +567,6 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     reset_timeline(ix);
     int rounds = 0;
     int64_t items_total = 0;
-    int64_t ext_total = 0;
     ScanArgs sa = sa0;
     sa.pool = (Hit*)ix->pool.p;
     sa.pool_cap = ix->pool_cap;
@@ -665,7 +664,6 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
           HIP_TRY(hipMemcpyAsync(ix->rc_host, rc, sizeof(RoundCounters), hipMemcpyDeviceToHost,
                                  s));
           HIP_TRY(hipStreamSynchronize(s));
-          ext_total += n_ext;
           sm.new_items = ix->rc_host->new_items;
           sm.rank_error = ix->rc_host->rank_error;
           if (sm.rank_error) break;
