@@ -177,7 +177,8 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
   const char* qbase = (const char*)a.queries;
   __shared__ int s_claim;
   __shared__ int s_next;  // one-ahead claims: the tile claimed at this tile's start
-  constexpr bool kShallow = kMode == kStageRegA && kOcc == 1;
+  constexpr bool kShallow = (kMode == kStageRegA && kOcc == 1) ||
+                            (kMode == kStageSync && kNT == kScanThreadsWide);
 
   // Tile schedule: the round's tiles are split into 8 contiguous ranges, one
   // per XCD (block b runs on XCD b % 8, so tiles of one list share that XCD's
@@ -233,13 +234,14 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
 
   // four claims ahead: t (runs), tn (stages), ta (items load), tb (record
   // loads); thread 0 claims the next one under each tile's MFMAs.  The dense
-  // register-query kernel (kShallow) claims one tile ahead instead: it claims
-  // tile t+1 at the start of tile t, loads its record and items under t's
-  // row stream and stages its queries under t's end.  Its tiles are long, so
-  // the chain fits in one tile, and a list's query tiles, claimed one after
-  // another, then start within about one tile duration of each other instead
-  // of four: they read the list's rows closer together, and more of those
-  // reads hit L2.
+  // register-query kernel and the wide 768-dimension kernel (kShallow) claim
+  // one tile ahead instead: tile t+1 is claimed at the start of tile t, its
+  // record and items load under t's row stream, and its queries are staged
+  // under t's end (register-query kernel) or at its own start (wide kernel).
+  // Their tiles are long, so the chain fits in one tile, and a list's query
+  // tiles, claimed one after another, then start within about one tile
+  // duration of each other instead of four: they read the list's rows closer
+  // together, and more of those reads hit L2.
   __shared__ int s_first[4];
   if (threadIdx.x == 0) {
     s_first[0] = claim();
@@ -426,8 +428,17 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
         }
       });
     } else {
+      if constexpr (kShallow) {
+        if (threadIdx.x == 0) s_next = claim();
+      }
       __syncthreads();
-      if (threadIdx.x == 0) t_claim = claim();  // published at the end of this tile
+      if constexpr (kShallow) {
+        tn = s_next;
+        recN = load_rec(tn);
+        itN = load_items(recN);
+      } else {
+        if (threadIdx.x == 0) t_claim = claim();  // published at the end of this tile
+      }
       u32x4* buf = lds;
       if constexpr (kMode == kStageAsync) {
         buf = lds + set * a.stage_u4;
@@ -439,17 +450,20 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
         });
         __syncthreads();
       }
-      itA = load_items(recA);
-      recB = load_rec(tb);
+      if constexpr (!kShallow) {
+        itA = load_items(recA);
+        recB = load_rec(tb);
+      }
       stream_rows<DT, D, 8, kNT == kScanThreads ? 80 : 150>(
           buf, g, (const char*)a.vectors, row_bytes, r0, r1, qb_n, epi);
+      if constexpr (kShallow) put_items(nset, recN, itN);  // staged at the next tile's start
     }
     if (lane == 0) s_wcnt[wv] = wcnt;
     wcnt = 0;
     // this wave's staging copies and arena stores are complete (in L2)
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();  // every wave is done with this tile's queries, items and candidates
-    if constexpr (kShallow) {
+    if constexpr (kShallow && kMode == kStageRegA) {
       if (tn >= 0) dma_stage<DT>(lds, g, qbase, row_bytes, s_q[nset], recN.nq);
     }
     // the arena's parts: pairs held per wave, their prefix; any global part?
