@@ -97,6 +97,7 @@ struct sieve_index {
   int64_t* offsets = nullptr;
   int64_t* ids = nullptr;
   void* centroids = nullptr;
+  void* cfrag = nullptr;  // fragment-order centroids (ranking), or null
   std::vector<int64_t> h_offsets;
   int64_t max_list = 0;
   double cmax = 0.0;
@@ -379,9 +380,9 @@ int rank_queries_in(const sieve_index* ix, const void* queries, int64_t q0, int6
   if (use_prefix_path(ix, nsel, pl.wide_rank)) {
     for (int64_t a = 0; a < cnt; a += chunk_prefix) {
       const int32_t c = (int32_t)((cnt - a) < chunk_prefix ? (cnt - a) : chunk_prefix);
-      HIP_TRY(launch_rank_prefix(ix->dtype, queries, q0 + a, c, ix->centroids, ix->nlist, ix->d,
-                                 nsel, ix->cmax, cand, ccount, P + a * ldp, ldp, rc, pl.rank_div,
-                                 s));
+      HIP_TRY(launch_rank_prefix(ix->dtype, queries, q0 + a, c, ix->centroids, ix->cfrag,
+                                 ix->nlist, ix->d, nsel, ix->cmax, cand, ccount, P + a * ldp, ldp,
+                                 rc, pl.rank_div, s));
     }
     return SIEVE_OK;
   }
@@ -994,18 +995,21 @@ SIEVE_API int sieve_load_index(const void* vectors, int32_t dtype, int64_t n, in
     return code;
   };
   const size_t vbytes = (size_t)n * d * e, cbytes = (size_t)nlist * d * e;
+  const size_t fbytes = centroid_frag_bytes(dtype, d, nlist);
   hipError_t err;
   if ((err = hipMalloc(&ix->vectors, vbytes ? vbytes : 16)) != hipSuccess ||
       (err = hipMalloc((void**)&ix->offsets, sizeof(int64_t) * (nlist + 1))) != hipSuccess ||
       (err = hipMalloc((void**)&ix->ids, n > 0 ? sizeof(int64_t) * n : 16)) != hipSuccess ||
-      (err = hipMalloc(&ix->centroids, cbytes)) != hipSuccess) {
+      (err = hipMalloc(&ix->centroids, cbytes)) != hipSuccess ||
+      (fbytes && (err = hipMalloc(&ix->cfrag, fbytes)) != hipSuccess)) {
     (void)hipGetLastError();
     return bail(fail(SIEVE_ENOMEM, "index allocation failed: %s", hipGetErrorString(err)));
   }
   if ((vbytes && (err = hipMemcpyAsync(ix->vectors, vectors, vbytes, hipMemcpyDeviceToDevice, s)) != hipSuccess) ||
       (err = hipMemcpyAsync(ix->offsets, list_offsets, sizeof(int64_t) * (nlist + 1), hipMemcpyDeviceToDevice, s)) != hipSuccess ||
       (n > 0 && (err = hipMemcpyAsync(ix->ids, ids, sizeof(int64_t) * n, hipMemcpyDeviceToDevice, s)) != hipSuccess) ||
-      (err = hipMemcpyAsync(ix->centroids, centroids, cbytes, hipMemcpyDeviceToDevice, s)) != hipSuccess)
+      (err = hipMemcpyAsync(ix->centroids, centroids, cbytes, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
+      (fbytes && (err = launch_centroid_frag(ix->centroids, nlist, ix->cfrag, s)) != hipSuccess))
     return bail(fail(SIEVE_EDEVICE, "index copy failed: %s", hipGetErrorString(err)));
   std::vector<uint8_t> hc(cbytes);
   if ((err = hipMemcpyAsync(hc.data(), centroids, cbytes, hipMemcpyDeviceToHost, s)) != hipSuccess ||
@@ -1036,6 +1040,7 @@ SIEVE_API void sieve_free_index(sieve_index* ix) {
   if (ix->offsets) (void)hipFree(ix->offsets);
   if (ix->ids) (void)hipFree(ix->ids);
   if (ix->centroids) (void)hipFree(ix->centroids);
+  if (ix->cfrag) (void)hipFree(ix->cfrag);
   if (ix->rc_host) (void)hipHostFree(ix->rc_host);
   if (ix->rs_host) (void)hipHostFree(ix->rs_host);
   for (hipEvent_t e : ix->ev_pool) (void)hipEventDestroy(e);

@@ -223,7 +223,7 @@ constexpr int kQRRing = 4;                                 // centroid fragment 
 
 template <int D>
 __global__ __launch_bounds__(kQRWaves * 64, 1) void rank_prefix_qreg_kernel(
-    const void* __restrict__ queries, int64_t q0, int32_t nqc, const void* __restrict__ centroids,
+    const void* __restrict__ queries, int64_t q0, int32_t nqc, const char* __restrict__ cfrag,
     int32_t nlist, int32_t R, double cmax, int32_t cap, unsigned long long* __restrict__ cand,
     int32_t* __restrict__ ccount, int32_t nblk1) {
   constexpr int DT = SIEVE_F16;
@@ -272,8 +272,9 @@ __global__ __launch_bounds__(kQRWaves * 64, 1) void rank_prefix_qreg_kernel(
     }
   }
 
-  const RowStream rs = {(const char*)centroids, nlist, (uint32_t)row_bytes};
   const int nblk = (nlist + 15) >> 4;
+  // this lane's 16-byte slot of chunk 0 of block 0 in the fragment-order copy
+  const char* fbase = cfrag + (size_t)lane * 16;
   // This wave's centroid row blocks (mem, mem + kQRSplit, ...) against its
   // group's query blocks.  Fragments come through a ring of kQRRing buffers
   // (kQRRing - 1 blocks in flight: the centroids come from L2, whose latency
@@ -285,10 +286,13 @@ __global__ __launch_bounds__(kQRWaves * 64, 1) void rank_prefix_qreg_kernel(
   auto sweep = [&](int nb, auto&& fast, auto&& slow) {
     u32x4 buf[kQRRing][kNC];
     f32x4 acc[2][kQW];
+    // a wave's fragment load reads 1 KB of consecutive bytes (row-major
+    // rows would put the 64 lanes' 16-byte pieces on 16 rows, and the
+    // address unit would take each lane's piece on its own)
     auto load = [&](int blk, u32x4(&dst)[kNC]) {
-      const char* p = rs.seg_ptr(blk < nb ? blk : nb - 1);
+      const char* p = fbase + (size_t)(blk < nb ? blk : nb - 1) * (kNC * 1024);
 #pragma unroll
-      for (int c = 0; c < kNC; ++c) dst[c] = *(const u32x4*)(p + 64 * c);
+      for (int c = 0; c < kNC; ++c) dst[c] = *(const u32x4*)(p + 1024 * c);
     };
 #pragma unroll
     for (int u = 0; u < kQRRing - 1; ++u) load(mem + u * kQRSplit, buf[u]);
@@ -485,6 +489,23 @@ __global__ __launch_bounds__(256) void rank_prefix_finish_kernel(
                              cmax, P + ql * ldp);
 }
 
+// Fragment-order copy of fp16 128-dimension centroids: one thread per
+// 16-byte slot (4 b + c) 64 + l <- row 16 b + l % 16, bytes 64 c + 16 (l / 16)
+// of the row (zeros past the last row).
+__global__ __launch_bounds__(256) void centroid_frag_kernel(const char* __restrict__ centroids,
+                                                           int32_t nlist, u32x4* __restrict__ frag,
+                                                           int64_t nslots) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= nslots) return;
+  const int l = (int)(i & 63);
+  const int64_t bc = i >> 6;  // 4 b + c
+  const int c = (int)(bc & 3);
+  const int64_t row = (bc >> 2) * 16 + (l & 15);
+  u32x4 v = {0u, 0u, 0u, 0u};
+  if (row < nlist) v = *(const u32x4*)(centroids + row * 256 + 64 * c + 16 * (l >> 4));
+  frag[i] = v;
+}
+
 constexpr int kMaxDynLds = 150 * 1024;
 
 // Query rows per work-group: as many 16-row blocks as the LDS budget holds
@@ -551,20 +572,34 @@ hipError_t launch_finish_t(const void* queries, int64_t q0, int32_t nqc, const v
 
 }  // namespace
 
+size_t centroid_frag_bytes(int dtype, int d, int32_t nlist) {
+  return dtype == SIEVE_F16 && d == 128 && nlist > 0 ? (size_t)((nlist + 15) / 16) * 4096 : 0;
+}
+
+hipError_t launch_centroid_frag(const void* centroids, int32_t nlist, void* frag, hipStream_t s) {
+  const int64_t nslots = (int64_t)((nlist + 15) / 16) * 256;
+  if (nslots <= 0) return hipSuccess;
+  hipLaunchKernelGGL(centroid_frag_kernel, dim3((unsigned)((nslots + 255) / 256)), dim3(256), 0,
+                     s, (const char*)centroids, nlist, (u32x4*)frag, nslots);
+  return hipGetLastError();
+}
+
 int rank_prefix_cap(int32_t R, int32_t nlist) {
   const int cap = R + 128;
   return cap < nlist ? cap : nlist;
 }
 
 hipError_t launch_rank_prefix(int dtype, const void* queries, int64_t q0, int32_t nqc,
-                              const void* centroids, int32_t nlist, int32_t d, int32_t R,
-                              double cmax, unsigned long long* cand, int32_t* ccount, int32_t* P,
-                              int64_t ldp, RoundCounters* rc, int32_t pass1_div, hipStream_t s) {
+                              const void* centroids, const void* cfrag, int32_t nlist, int32_t d,
+                              int32_t R, double cmax, unsigned long long* cand, int32_t* ccount,
+                              int32_t* P, int64_t ldp, RoundCounters* rc, int32_t pass1_div,
+                              hipStream_t s) {
   if (nqc <= 0) return hipSuccess;
   if (R < 1 || R > kRankPrefixMax || R > nlist) return hipErrorInvalidValue;
   const int cap = rank_prefix_cap(R, nlist);
   hipError_t e;
   if (dtype == SIEVE_F16 && d == 128) {
+    if (!cfrag) return hipErrorInvalidValue;
     const unsigned grid = (unsigned)((nqc + kQRRows - 1) / kQRRows);
     // Pass 1 may bound the R-th score from the first 1/div of the centroids
     // (a subset's R-th largest never exceeds the whole set's): a looser bound,
@@ -575,7 +610,8 @@ hipError_t launch_rank_prefix(int dtype, const void* queries, int64_t q0, int32_
     int nblk1 = (nblk + div - 1) / div;
     if (nblk1 < 4 * kQRSplit) nblk1 = nblk < 4 * kQRSplit ? nblk : 4 * kQRSplit;
     hipLaunchKernelGGL((rank_prefix_qreg_kernel<128>), dim3(grid), dim3(kQRWaves * 64), 0, s,
-                       queries, q0, nqc, centroids, nlist, R, cmax, cap, cand, ccount, nblk1);
+                       queries, q0, nqc, (const char*)cfrag, nlist, R, cmax, cap, cand, ccount,
+                       nblk1);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return launch_finish_t<SIEVE_F16>(queries, q0, nqc, centroids, d, R, cap, cmax, cand, ccount,
                                       P, ldp, rc, s);

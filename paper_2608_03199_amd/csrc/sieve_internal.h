@@ -208,10 +208,21 @@ size_t scan_lds_bytes(int dtype, int d, int rows);
 // nqc * rank_prefix_cap(R, nlist) keys and ccount nqc counts.
 constexpr int kRankPrefixMax = 64;
 int rank_prefix_cap(int32_t R, int32_t nlist);
+// Centroids in MFMA fragment order, for the register-query ranking kernel
+// (fp16, 128 dimensions): 16-row block b, 32-dimension chunk c and lane l
+// hold the 16 bytes at slot (4 b + c) 64 + l, taken from row 16 b + l % 16,
+// dimensions 32 c + 8 (l / 16) .. + 8 (zeros past the last row), so that a
+// wave's fragment load reads 1 KB of consecutive bytes.  frag_bytes is 0
+// where the kernel does not apply.
+size_t centroid_frag_bytes(int dtype, int d, int32_t nlist);
+hipError_t launch_centroid_frag(const void* centroids, int32_t nlist, void* frag, hipStream_t s);
+// cfrag: the index's fragment-order centroids (centroid_frag_bytes > 0), or
+// null where it has none.
 hipError_t launch_rank_prefix(int dtype, const void* queries, int64_t q0, int32_t nqc,
-                              const void* centroids, int32_t nlist, int32_t d, int32_t R,
-                              double cmax, unsigned long long* cand, int32_t* ccount, int32_t* P,
-                              int64_t ldp, RoundCounters* rc, int32_t pass1_div, hipStream_t s);
+                              const void* centroids, const void* cfrag, int32_t nlist, int32_t d,
+                              int32_t R, double cmax, unsigned long long* cand, int32_t* ccount,
+                              int32_t* P, int64_t ldp, RoundCounters* rc, int32_t pass1_div,
+                              hipStream_t s);
 hipError_t launch_rank_select(int dtype, const void* queries, int64_t q0, int32_t nqc,
                               const void* centroids, int32_t nlist, int32_t d, const float* scores,
                               int32_t n, double cmax, int32_t* P, int64_t ldp, RoundCounters* rc,
