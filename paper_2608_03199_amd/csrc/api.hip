@@ -98,6 +98,7 @@ struct sieve_index {
   int64_t* ids = nullptr;
   void* centroids = nullptr;
   void* cfrag = nullptr;  // fragment-order centroids (ranking), or null
+  void* vfrag = nullptr;  // fragment-order vectors (scan), or null
   std::vector<int64_t> h_offsets;
   int64_t max_list = 0;
   double cmax = 0.0;
@@ -419,6 +420,7 @@ ScanArgs make_scan_args(sieve_index* ix, const void* queries, const int64_t* exc
   ScanArgs a;
   RoundCounters* rc = (RoundCounters*)ix->rc.p;
   a.vectors = ix->vectors;
+  a.vfrag = ix->vfrag;
   a.list_offsets = ix->offsets;
   a.ids = ix->ids;
   a.queries = queries;
@@ -727,6 +729,7 @@ int search_impl(sieve_index* ix, const void* queries, int64_t nq, const int64_t*
     if (n_heavy > 0 && pool_n <= (unsigned long long)ix->pool_cap) {
       HeavyArgs ha;
       ha.vectors = ix->vectors;
+      ha.vfrag = ix->vfrag;
       ha.ids = ix->ids;
       ha.queries = queries;
       ha.recs = (const HeavyRec*)ix->heavy.p;
@@ -996,12 +999,14 @@ SIEVE_API int sieve_load_index(const void* vectors, int32_t dtype, int64_t n, in
   };
   const size_t vbytes = (size_t)n * d * e, cbytes = (size_t)nlist * d * e;
   const size_t fbytes = centroid_frag_bytes(dtype, d, nlist);
+  const size_t vfbytes = vector_frag_bytes(dtype, d, n);
   hipError_t err;
   if ((err = hipMalloc(&ix->vectors, vbytes ? vbytes : 16)) != hipSuccess ||
       (err = hipMalloc((void**)&ix->offsets, sizeof(int64_t) * (nlist + 1))) != hipSuccess ||
       (err = hipMalloc((void**)&ix->ids, n > 0 ? sizeof(int64_t) * n : 16)) != hipSuccess ||
       (err = hipMalloc(&ix->centroids, cbytes)) != hipSuccess ||
-      (fbytes && (err = hipMalloc(&ix->cfrag, fbytes)) != hipSuccess)) {
+      (fbytes && (err = hipMalloc(&ix->cfrag, fbytes)) != hipSuccess) ||
+      (vfbytes && (err = hipMalloc(&ix->vfrag, vfbytes)) != hipSuccess)) {
     (void)hipGetLastError();
     return bail(fail(SIEVE_ENOMEM, "index allocation failed: %s", hipGetErrorString(err)));
   }
@@ -1009,7 +1014,8 @@ SIEVE_API int sieve_load_index(const void* vectors, int32_t dtype, int64_t n, in
       (err = hipMemcpyAsync(ix->offsets, list_offsets, sizeof(int64_t) * (nlist + 1), hipMemcpyDeviceToDevice, s)) != hipSuccess ||
       (n > 0 && (err = hipMemcpyAsync(ix->ids, ids, sizeof(int64_t) * n, hipMemcpyDeviceToDevice, s)) != hipSuccess) ||
       (err = hipMemcpyAsync(ix->centroids, centroids, cbytes, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
-      (fbytes && (err = launch_centroid_frag(ix->centroids, nlist, ix->cfrag, s)) != hipSuccess))
+      (fbytes && (err = launch_centroid_frag(ix->centroids, nlist, ix->cfrag, s)) != hipSuccess) ||
+      (vfbytes && (err = launch_vector_frag(dtype, d, ix->vectors, n, ix->vfrag, s)) != hipSuccess))
     return bail(fail(SIEVE_EDEVICE, "index copy failed: %s", hipGetErrorString(err)));
   std::vector<uint8_t> hc(cbytes);
   if ((err = hipMemcpyAsync(hc.data(), centroids, cbytes, hipMemcpyDeviceToHost, s)) != hipSuccess ||
@@ -1041,6 +1047,7 @@ SIEVE_API void sieve_free_index(sieve_index* ix) {
   if (ix->ids) (void)hipFree(ix->ids);
   if (ix->centroids) (void)hipFree(ix->centroids);
   if (ix->cfrag) (void)hipFree(ix->cfrag);
+  if (ix->vfrag) (void)hipFree(ix->vfrag);
   if (ix->rc_host) (void)hipHostFree(ix->rc_host);
   if (ix->rs_host) (void)hipHostFree(ix->rs_host);
   for (hipEvent_t e : ix->ev_pool) (void)hipEventDestroy(e);

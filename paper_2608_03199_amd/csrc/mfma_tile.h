@@ -272,6 +272,7 @@ constexpr int kWaitVmcnt0 = 0x0F70;
 // issued unconditionally, so the load sequence never depends on control flow
 // and the compiler's wait counts stay exact.
 struct RowStream {
+  static constexpr uint32_t kChunkStride = 64;  // bytes from chunk c to c + 1 of a lane
   const char* base;   // row r0
   int nrows;          // r1 - r0
   uint32_t rb;        // row bytes
@@ -284,6 +285,40 @@ struct RowStream {
     return base + (lane_row(blk) * rb + ((threadIdx.x >> 4) & 3u) * 16u);
   }
 };
+
+// The same rows read from a fragment-order copy of the whole store (rows
+// r0 .. r0 + nrows - 1 of it).  The copy keeps, for each 16-row block B of
+// the store (rows 16 B .. 16 B + 15, counted from the store's first row) and
+// each 64-byte chunk c of a row, the 64 16-byte segments that one fragment
+// load of that block takes, in lane order: segment 4 c + s of row 16 B + i
+// sits at 16-byte slot (B nch + c) 64 + i + 16 s.  A wave's fragment load of
+// a stream block then reads two runs of consecutive bytes per 16-lane group
+// (one when r0 is a multiple of 16) instead of 16 separate rows, so the
+// address unit coalesces it.  Rows past the store's end and segments past a
+// row's end hold zeros.
+struct FragStream {
+  static constexpr uint32_t kChunkStride = 1024;
+  const char* frag;   // the copy
+  int64_t r0;         // stream row 0 = store row r0
+  int nrows;
+  uint32_t nch;       // 64-byte chunks per row
+  __device__ __forceinline__ const char* seg_ptr(int blk) const {
+    const int rl = blk * 16 + (int)(threadIdx.x & 15);
+    const int64_t r = r0 + (rl < nrows ? rl : nrows - 1);
+    return frag + (((r >> 4) * nch) << 10) +
+           (((uint32_t)(r & 15) + (threadIdx.x & 48u)) << 4);
+  }
+};
+
+// The stream type of a row source: the row-major store or its fragment copy.
+template <bool kFrag>
+__device__ __forceinline__ auto make_row_stream(const char* base, size_t row_bytes, int64_t r0,
+                                                int64_t r1) {
+  if constexpr (kFrag)
+    return FragStream{base, r0, (int)(r1 - r0), (uint32_t)((row_bytes + 63) / 64)};
+  else
+    return RowStream{base + (size_t)r0 * row_bytes, (int)(r1 - r0), (uint32_t)row_bytes};
+}
 
 // f(std::integral_constant<int, J>{}) for J = 0 .. N-1, unrolled at compile
 // time (fragment ring indices must be constants: a runtime index would put
@@ -305,9 +340,9 @@ __device__ __forceinline__ int wave_id() {
 // unrolled per iteration so that buffer indices are compile-time constants.
 // Chunks are accumulated in the same order as in the unsliced variant, so
 // scores are bit-identical.
-template <int DT, int D, int QB, int Reserve, typename Epi>
+template <int DT, int D, int QB, int Reserve, typename Epi, typename RS>
 __device__ __forceinline__ void stream_rows_sliced(const u32x4* __restrict__ lds,
-                                                   const RowGeom<DT>& g, const RowStream& rs,
+                                                   const RowGeom<DT>& g, const RS& rs,
                                                    int64_t r0, Epi& epi) {
   constexpr int kNC = D / DTraits<DT>::kChunkDims;
   constexpr int kNS = (kNC + kSliceChunks - 1) / kSliceChunks;  // slices per row block
@@ -321,7 +356,7 @@ __device__ __forceinline__ void stream_rows_sliced(const u32x4* __restrict__ lds
 #pragma unroll
     for (int c = 0; c < kSliceChunks; ++c)
       if (s * kSliceChunks + c < kNC)
-        dst[c] = *(const u32x4*)(p + 64 * (s * kSliceChunks + c));
+        dst[c] = *(const u32x4*)(p + RS::kChunkStride * (s * kSliceChunks + c));
   };
   u32x4 buf[NB][kSliceChunks];
   int rb = wave;
@@ -367,7 +402,7 @@ __device__ __forceinline__ void stream_rows_sliced(const u32x4* __restrict__ lds
 // >= r1 on the last block: the epilogue masks it; loads are clamped).  With a
 // compile-time dimension, fragment buffers rotate so that the next blocks'
 // fragments load while the current block is multiplied.
-template <int DT, int D, int QB, typename Epi, int Reserve = 0>
+template <int DT, int D, int QB, typename Epi, int Reserve = 0, bool kFrag = false>
 __device__ __forceinline__ void stream_rows_qb(const u32x4* __restrict__ lds,
                                                const RowGeom<DT>& g,
                                                const char* __restrict__ base, size_t row_bytes,
@@ -375,7 +410,9 @@ __device__ __forceinline__ void stream_rows_qb(const u32x4* __restrict__ lds,
   const int wave = wave_id();
   const int nwaves = blockDim.x >> 6;
   const int r16 = threadIdx.x & 15;
-  const RowStream rs = {base + (size_t)r0 * row_bytes, (int)(r1 - r0), (uint32_t)row_bytes};
+  static_assert(!kFrag || D > 0, "the fragment copy serves compile-time dimensions");
+  const auto rs = make_row_stream<kFrag>(base, row_bytes, r0, r1);
+  using RS = decltype(rs);
   const int nrows = rs.nrows;
   constexpr int kNC = D / DTraits<DT>::kChunkDims;
   if constexpr (kNC > kSliceChunks) {
@@ -387,7 +424,7 @@ __device__ __forceinline__ void stream_rows_qb(const u32x4* __restrict__ lds,
     auto load = [&](int blk, u32x4(&dst)[kNC]) {
       const char* p = rs.seg_ptr(blk);
 #pragma unroll
-      for (int c = 0; c < kNC; ++c) dst[c] = *(const u32x4*)(p + 64 * c);
+      for (int c = 0; c < kNC; ++c) dst[c] = *(const u32x4*)(p + RS::kChunkStride * c);
     };
     u32x4 buf[NB][kNC];
     if (nrows <= 0) return;
@@ -409,7 +446,7 @@ __device__ __forceinline__ void stream_rows_qb(const u32x4* __restrict__ lds,
         rb += nwaves;
       }
     }
-  } else {
+  } else if constexpr (!kFrag) {
     for (int rb = wave; rb * 16 < nrows; rb += nwaves) {
       const u32x4* vrow = (const u32x4*)(rs.base + (size_t)rs.lane_row(rb) * rs.rb);
       f32x4 acc[QB];
@@ -472,7 +509,7 @@ constexpr int rega_ring() {
 // same bits.  The vote of block b is issued between the MFMAs of block
 // b + W (two accumulator sets, interleaving hints), so that it runs under
 // them.
-template <int DT, int D, int QB, int kRegs, typename Vote, typename Cand>
+template <int DT, int D, int QB, int kRegs, bool kFrag, typename Vote, typename Cand>
 __device__ __forceinline__ void stream_rows_rega(const u32x4 (&qf)[D / DTraits<DT>::kChunkDims][QB],
                                                  const char* __restrict__ base, size_t row_bytes,
                                                  int64_t r0, int64_t r1, Vote& vote, Cand& cand) {
@@ -481,12 +518,13 @@ __device__ __forceinline__ void stream_rows_rega(const u32x4 (&qf)[D / DTraits<D
   const int wave = wave_id();
   const int nwaves = blockDim.x >> 6;
   const int r16 = threadIdx.x & 15;
-  const RowStream rs = {base + (size_t)r0 * row_bytes, (int)(r1 - r0), (uint32_t)row_bytes};
+  const auto rs = make_row_stream<kFrag>(base, row_bytes, r0, r1);
+  using RS = decltype(rs);
   const int nrows = rs.nrows;
   auto load = [&](int blk, u32x4(&dst)[kNC]) {
     const char* p = rs.seg_ptr(blk);
 #pragma unroll
-    for (int c = 0; c < kNC; ++c) dst[c] = *(const u32x4*)(p + 64 * c);
+    for (int c = 0; c < kNC; ++c) dst[c] = *(const u32x4*)(p + RS::kChunkStride * c);
   };
   u32x4 buf[NB][kNC];
   if (nrows <= 0 || wave * 16 >= nrows) return;
@@ -544,31 +582,32 @@ constexpr int qb_cap() {
   return qb < 1 ? 1 : (qb > 8 ? 8 : qb);
 }
 
-template <int DT, int D, int QB, int kMax, typename Epi>
+template <int DT, int D, int QB, int kMax, bool kFrag, typename Epi>
 __device__ __forceinline__ void stream_rows_from(const u32x4* __restrict__ lds,
                                                  const RowGeom<DT>& g,
                                                  const char* __restrict__ base, size_t row_bytes,
                                                  int64_t r0, int64_t r1, int qb_n, Epi& epi) {
   if constexpr (QB >= kMax) {
-    stream_rows_qb<DT, D, kMax, Epi>(lds, g, base, row_bytes, r0, r1, epi);
+    stream_rows_qb<DT, D, kMax, Epi, 0, kFrag>(lds, g, base, row_bytes, r0, r1, epi);
   } else {
     if (qb_n <= QB)
-      stream_rows_qb<DT, D, QB, Epi>(lds, g, base, row_bytes, r0, r1, epi);
+      stream_rows_qb<DT, D, QB, Epi, 0, kFrag>(lds, g, base, row_bytes, r0, r1, epi);
     else
-      stream_rows_from<DT, D, QB + 1, kMax>(lds, g, base, row_bytes, r0, r1, qb_n, epi);
+      stream_rows_from<DT, D, QB + 1, kMax, kFrag>(lds, g, base, row_bytes, r0, r1, qb_n, epi);
   }
 }
 
 // Dispatch on the tile's number of 16-query blocks (uniform per tile).
 // QBLimit: the caller's largest tile, in 16-query blocks; kBudgetKB: the LDS
-// budget the caller's tile size follows.
-template <int DT, int D, int QBLimit = 8, int kBudgetKB = 80, typename Epi>
+// budget the caller's tile size follows; kFrag: base is the store's
+// fragment-order copy (FragStream), not the row-major store.
+template <int DT, int D, int QBLimit = 8, int kBudgetKB = 80, bool kFrag = false, typename Epi>
 __device__ __forceinline__ void stream_rows(const u32x4* __restrict__ lds, const RowGeom<DT>& g,
                                             const char* __restrict__ base, size_t row_bytes,
                                             int64_t r0, int64_t r1, int qb_n, Epi&& epi) {
   constexpr int kCap = qb_cap<DT, D, kBudgetKB>();
   constexpr int kMax = kCap < QBLimit ? kCap : QBLimit;
-  stream_rows_from<DT, D, 1, kMax>(lds, g, base, row_bytes, r0, r1, qb_n, epi);
+  stream_rows_from<DT, D, 1, kMax, kFrag>(lds, g, base, row_bytes, r0, r1, qb_n, epi);
 }
 
 }  // namespace sieve

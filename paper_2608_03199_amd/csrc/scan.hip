@@ -416,8 +416,9 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
           itA = load_items(recA);
           recB = load_rec(tb);
         }
-        stream_rows_rega<DT, D, QB, kOcc == 1 ? 512 : 256>(qf, (const char*)a.vectors, row_bytes,
-                                                            r0, r1, vote, candidates);
+        stream_rows_rega<DT, D, QB, kOcc == 1 ? 512 : 256, true>(qf, (const char*)a.vfrag,
+                                                                  row_bytes, r0, r1, vote,
+                                                                  candidates);
         // The next tile's queries are staged after the stream, under the end
         // of this tile: an LDS-DMA load in flight during the stream makes the
         // compiler wait for every load there, not just the oldest ones.
@@ -454,8 +455,8 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
         itA = load_items(recA);
         recB = load_rec(tb);
       }
-      stream_rows<DT, D, 8, kNT == kScanThreads ? 80 : 150>(
-          buf, g, (const char*)a.vectors, row_bytes, r0, r1, qb_n, epi);
+      stream_rows<DT, D, 8, kNT == kScanThreads ? 80 : 150, (D > 0)>(
+          buf, g, (const char*)(D > 0 ? a.vfrag : a.vectors), row_bytes, r0, r1, qb_n, epi);
       if constexpr (kShallow) put_items(nset, recN, itN);  // staged at the next tile's start
     }
     if (lane == 0) s_wcnt[wv] = wcnt;
@@ -890,7 +891,8 @@ __global__ __launch_bounds__(64) void scan_heavy_kernel(HeavyArgs a) {
       for (int j = 0; j < nq; ++j)
         if (s_cnt[j] > kHeavyCap - 16) compact(j, false, 0);
     };
-    stream_rows_qb<DT, D, 1>(lds, g, (const char*)a.vectors, row_bytes, r0, r1, epi);
+    stream_rows_qb<DT, D, 1, decltype(epi), 0, (D > 0)>(
+        lds, g, (const char*)(D > 0 ? a.vfrag : a.vectors), row_bytes, r0, r1, epi);
 
     // each query's first k to the pool: one claim for the record
     int tot = 0;
@@ -1090,6 +1092,51 @@ int tile_rows(int dtype, int d) {
   int qb = (80 * 1024) / (16 * rb);
   qb = qb < 1 ? 1 : (qb > kQB ? kQB : qb);
   return 16 * qb;
+}
+
+namespace {
+// Fragment-order copy of the store (the layout FragStream reads): one thread
+// per 16-byte slot; slot (B nch + c) 64 + i + 16 s <- segment 4 c + s of row
+// 16 B + i, zeros past the last row or past the row's segments.
+__global__ __launch_bounds__(256) void vector_frag_kernel(const char* __restrict__ vectors,
+                                                          int64_t n, int32_t row_bytes,
+                                                          int32_t nch, u32x4* __restrict__ frag,
+                                                          int64_t nslots) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nslots;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int l = (int)(i & 63);
+    const int64_t bc = i >> 6;  // B nch + c
+    const int64_t blk = bc / nch;
+    const int c = (int)(bc - blk * nch);
+    const int64_t row = blk * 16 + (l & 15);
+    const int seg = 4 * c + (l >> 4);
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (row < n && seg * 16 < row_bytes)
+      v = *(const u32x4*)(vectors + row * row_bytes + (int64_t)seg * 16);
+    frag[i] = v;
+  }
+}
+}  // namespace
+
+size_t vector_frag_bytes(int dtype, int d, int64_t n) {
+  const bool fixed = dtype == SIEVE_F32 ? (d == 64 || d == 128)
+                                        : (d == 64 || d == 128 || d == 768);
+  if (!fixed || n <= 0) return 0;
+  const int64_t row_bytes = (int64_t)d * (dtype == SIEVE_F32 ? 4 : 2);
+  return (size_t)((n + 15) / 16) * (size_t)((row_bytes + 63) / 64) * 1024;
+}
+
+hipError_t launch_vector_frag(int dtype, int d, const void* vectors, int64_t n, void* frag,
+                              hipStream_t s) {
+  const size_t bytes = vector_frag_bytes(dtype, d, n);
+  if (bytes == 0) return hipSuccess;
+  const int32_t row_bytes = d * (dtype == SIEVE_F32 ? 4 : 2);
+  const int64_t nslots = (int64_t)(bytes / 16);
+  const int64_t blocks = (nslots + 255) / 256;
+  hipLaunchKernelGGL(vector_frag_kernel, dim3((unsigned)(blocks < (1 << 20) ? blocks : (1 << 20))),
+                     dim3(256), 0, s, (const char*)vectors, n, row_bytes,
+                     (int32_t)((row_bytes + 63) / 64), (u32x4*)frag, nslots);
+  return hipGetLastError();
 }
 
 hipError_t launch_scan(int dtype, const ScanArgs& a, int32_t grid, hipStream_t s) {
