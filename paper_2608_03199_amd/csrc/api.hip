@@ -99,6 +99,7 @@ struct sieve_index {
   void* centroids = nullptr;
   void* cfrag = nullptr;  // fragment-order centroids (ranking), or null
   void* vfrag = nullptr;  // fragment-order vectors (scan), or null
+  int64_t* foff = nullptr;  // [nlist + 1] partition starts in vfrag (rows)
   std::vector<int64_t> h_offsets;
   int64_t max_list = 0;
   double cmax = 0.0;
@@ -421,6 +422,7 @@ ScanArgs make_scan_args(sieve_index* ix, const void* queries, const int64_t* exc
   RoundCounters* rc = (RoundCounters*)ix->rc.p;
   a.vectors = ix->vectors;
   a.vfrag = ix->vfrag;
+  a.frag_offsets = ix->foff;
   a.list_offsets = ix->offsets;
   a.ids = ix->ids;
   a.queries = queries;
@@ -999,14 +1001,21 @@ SIEVE_API int sieve_load_index(const void* vectors, int32_t dtype, int64_t n, in
   };
   const size_t vbytes = (size_t)n * d * e, cbytes = (size_t)nlist * d * e;
   const size_t fbytes = centroid_frag_bytes(dtype, d, nlist);
-  const size_t vfbytes = vector_frag_bytes(dtype, d, n);
+  // partitions padded to whole 16-row blocks in the fragment-order copy
+  std::vector<int64_t> hfoff(nlist + 1, 0);
+  for (int l = 0; l < nlist; ++l) hfoff[l + 1] = hfoff[l] + (off[l + 1] - off[l] + 15) / 16 * 16;
+  const size_t vfbytes = vector_frag_bytes(dtype, d, hfoff[nlist]);
+  // the partition starts are read for every tile of a compile-time dimension,
+  // also when the store is empty (then no row is)
+  const bool vfixed = vector_frag_bytes(dtype, d, 16) > 0;
   hipError_t err;
   if ((err = hipMalloc(&ix->vectors, vbytes ? vbytes : 16)) != hipSuccess ||
       (err = hipMalloc((void**)&ix->offsets, sizeof(int64_t) * (nlist + 1))) != hipSuccess ||
       (err = hipMalloc((void**)&ix->ids, n > 0 ? sizeof(int64_t) * n : 16)) != hipSuccess ||
       (err = hipMalloc(&ix->centroids, cbytes)) != hipSuccess ||
       (fbytes && (err = hipMalloc(&ix->cfrag, fbytes)) != hipSuccess) ||
-      (vfbytes && (err = hipMalloc(&ix->vfrag, vfbytes)) != hipSuccess)) {
+      (vfbytes && (err = hipMalloc(&ix->vfrag, vfbytes)) != hipSuccess) ||
+      (vfixed && (err = hipMalloc((void**)&ix->foff, sizeof(int64_t) * (nlist + 1))) != hipSuccess)) {
     (void)hipGetLastError();
     return bail(fail(SIEVE_ENOMEM, "index allocation failed: %s", hipGetErrorString(err)));
   }
@@ -1015,7 +1024,10 @@ SIEVE_API int sieve_load_index(const void* vectors, int32_t dtype, int64_t n, in
       (n > 0 && (err = hipMemcpyAsync(ix->ids, ids, sizeof(int64_t) * n, hipMemcpyDeviceToDevice, s)) != hipSuccess) ||
       (err = hipMemcpyAsync(ix->centroids, centroids, cbytes, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
       (fbytes && (err = launch_centroid_frag(ix->centroids, nlist, ix->cfrag, s)) != hipSuccess) ||
-      (vfbytes && (err = launch_vector_frag(dtype, d, ix->vectors, n, ix->vfrag, s)) != hipSuccess))
+      (vfixed && (err = hipMemcpyAsync(ix->foff, hfoff.data(), sizeof(int64_t) * (nlist + 1),
+                                        hipMemcpyHostToDevice, s)) != hipSuccess) ||
+      (vfbytes && (err = launch_vector_frag(dtype, d, ix->vectors, ix->offsets, ix->foff, nlist,
+                                            hfoff[nlist], ix->vfrag, s)) != hipSuccess))
     return bail(fail(SIEVE_EDEVICE, "index copy failed: %s", hipGetErrorString(err)));
   std::vector<uint8_t> hc(cbytes);
   if ((err = hipMemcpyAsync(hc.data(), centroids, cbytes, hipMemcpyDeviceToHost, s)) != hipSuccess ||
@@ -1048,6 +1060,7 @@ SIEVE_API void sieve_free_index(sieve_index* ix) {
   if (ix->centroids) (void)hipFree(ix->centroids);
   if (ix->cfrag) (void)hipFree(ix->cfrag);
   if (ix->vfrag) (void)hipFree(ix->vfrag);
+  if (ix->foff) (void)hipFree(ix->foff);
   if (ix->rc_host) (void)hipHostFree(ix->rc_host);
   if (ix->rs_host) (void)hipHostFree(ix->rs_host);
   for (hipEvent_t e : ix->ev_pool) (void)hipEventDestroy(e);

@@ -286,20 +286,20 @@ struct RowStream {
   }
 };
 
-// The same rows read from a fragment-order copy of the whole store (rows
-// r0 .. r0 + nrows - 1 of it).  The copy keeps, for each 16-row block B of
-// the store (rows 16 B .. 16 B + 15, counted from the store's first row) and
-// each 64-byte chunk c of a row, the 64 16-byte segments that one fragment
-// load of that block takes, in lane order: segment 4 c + s of row 16 B + i
-// sits at 16-byte slot (B nch + c) 64 + i + 16 s.  A wave's fragment load of
-// a stream block then reads two runs of consecutive bytes per 16-lane group
-// (one when r0 is a multiple of 16) instead of 16 separate rows, so the
-// address unit coalesces it.  Rows past the store's end and segments past a
-// row's end hold zeros.
+// The same rows read from a fragment-order copy of the store.  The copy's
+// rows are the store's with padding rows (zeros) between partitions, so that
+// every partition starts a 16-row block; for each 16-row block B of the copy
+// and each 64-byte chunk c of a row it keeps the 64 16-byte segments that
+// one fragment load of that block takes, in lane order: segment 4 c + s of
+// copy row 16 B + i sits at 16-byte slot (B nch + c) 64 + i + 16 s.  A
+// wave's fragment load of a stream block that starts a copy block then reads
+// 1 KB of consecutive bytes (two runs per 16-lane group otherwise) instead of
+// 16 separate rows, so the address unit coalesces it.  Segments past a row's
+// end hold zeros.
 struct FragStream {
   static constexpr uint32_t kChunkStride = 1024;
   const char* frag;   // the copy
-  int64_t r0;         // stream row 0 = store row r0
+  int64_t r0;         // stream row 0 = copy row r0
   int nrows;
   uint32_t nch;       // 64-byte chunks per row
   __device__ __forceinline__ const char* seg_ptr(int blk) const {
@@ -311,11 +311,12 @@ struct FragStream {
 };
 
 // The stream type of a row source: the row-major store or its fragment copy.
+// fdelta: copy row minus store row of the stream's rows (fragment copy only).
 template <bool kFrag>
 __device__ __forceinline__ auto make_row_stream(const char* base, size_t row_bytes, int64_t r0,
-                                                int64_t r1) {
+                                                int64_t r1, int64_t fdelta) {
   if constexpr (kFrag)
-    return FragStream{base, r0, (int)(r1 - r0), (uint32_t)((row_bytes + 63) / 64)};
+    return FragStream{base, r0 + fdelta, (int)(r1 - r0), (uint32_t)((row_bytes + 63) / 64)};
   else
     return RowStream{base + (size_t)r0 * row_bytes, (int)(r1 - r0), (uint32_t)row_bytes};
 }
@@ -406,12 +407,13 @@ template <int DT, int D, int QB, typename Epi, int Reserve = 0, bool kFrag = fal
 __device__ __forceinline__ void stream_rows_qb(const u32x4* __restrict__ lds,
                                                const RowGeom<DT>& g,
                                                const char* __restrict__ base, size_t row_bytes,
-                                               int64_t r0, int64_t r1, Epi& epi) {
+                                               int64_t r0, int64_t r1, Epi& epi,
+                                               int64_t fdelta = 0) {
   const int wave = wave_id();
   const int nwaves = blockDim.x >> 6;
   const int r16 = threadIdx.x & 15;
   static_assert(!kFrag || D > 0, "the fragment copy serves compile-time dimensions");
-  const auto rs = make_row_stream<kFrag>(base, row_bytes, r0, r1);
+  const auto rs = make_row_stream<kFrag>(base, row_bytes, r0, r1, fdelta);
   using RS = decltype(rs);
   const int nrows = rs.nrows;
   constexpr int kNC = D / DTraits<DT>::kChunkDims;
@@ -512,13 +514,14 @@ constexpr int rega_ring() {
 template <int DT, int D, int QB, int kRegs, bool kFrag, typename Vote, typename Cand>
 __device__ __forceinline__ void stream_rows_rega(const u32x4 (&qf)[D / DTraits<DT>::kChunkDims][QB],
                                                  const char* __restrict__ base, size_t row_bytes,
-                                                 int64_t r0, int64_t r1, Vote& vote, Cand& cand) {
+                                                 int64_t r0, int64_t r1, Vote& vote, Cand& cand,
+                                                 int64_t fdelta = 0) {
   constexpr int kNC = D / DTraits<DT>::kChunkDims;
   constexpr int NB = rega_ring<DT, D, QB, kRegs>();
   const int wave = wave_id();
   const int nwaves = blockDim.x >> 6;
   const int r16 = threadIdx.x & 15;
-  const auto rs = make_row_stream<kFrag>(base, row_bytes, r0, r1);
+  const auto rs = make_row_stream<kFrag>(base, row_bytes, r0, r1, fdelta);
   using RS = decltype(rs);
   const int nrows = rs.nrows;
   auto load = [&](int blk, u32x4(&dst)[kNC]) {
@@ -586,28 +589,32 @@ template <int DT, int D, int QB, int kMax, bool kFrag, typename Epi>
 __device__ __forceinline__ void stream_rows_from(const u32x4* __restrict__ lds,
                                                  const RowGeom<DT>& g,
                                                  const char* __restrict__ base, size_t row_bytes,
-                                                 int64_t r0, int64_t r1, int qb_n, Epi& epi) {
+                                                 int64_t r0, int64_t r1, int qb_n, Epi& epi,
+                                                 int64_t fdelta) {
   if constexpr (QB >= kMax) {
-    stream_rows_qb<DT, D, kMax, Epi, 0, kFrag>(lds, g, base, row_bytes, r0, r1, epi);
+    stream_rows_qb<DT, D, kMax, Epi, 0, kFrag>(lds, g, base, row_bytes, r0, r1, epi, fdelta);
   } else {
     if (qb_n <= QB)
-      stream_rows_qb<DT, D, QB, Epi, 0, kFrag>(lds, g, base, row_bytes, r0, r1, epi);
+      stream_rows_qb<DT, D, QB, Epi, 0, kFrag>(lds, g, base, row_bytes, r0, r1, epi, fdelta);
     else
-      stream_rows_from<DT, D, QB + 1, kMax, kFrag>(lds, g, base, row_bytes, r0, r1, qb_n, epi);
+      stream_rows_from<DT, D, QB + 1, kMax, kFrag>(lds, g, base, row_bytes, r0, r1, qb_n, epi,
+                                                   fdelta);
   }
 }
 
 // Dispatch on the tile's number of 16-query blocks (uniform per tile).
 // QBLimit: the caller's largest tile, in 16-query blocks; kBudgetKB: the LDS
 // budget the caller's tile size follows; kFrag: base is the store's
-// fragment-order copy (FragStream), not the row-major store.
+// fragment-order copy (FragStream, its rows fdelta past the store's), not the
+// row-major store.
 template <int DT, int D, int QBLimit = 8, int kBudgetKB = 80, bool kFrag = false, typename Epi>
 __device__ __forceinline__ void stream_rows(const u32x4* __restrict__ lds, const RowGeom<DT>& g,
                                             const char* __restrict__ base, size_t row_bytes,
-                                            int64_t r0, int64_t r1, int qb_n, Epi&& epi) {
+                                            int64_t r0, int64_t r1, int qb_n, Epi&& epi,
+                                            int64_t fdelta = 0) {
   constexpr int kCap = qb_cap<DT, D, kBudgetKB>();
   constexpr int kMax = kCap < QBLimit ? kCap : QBLimit;
-  stream_rows_from<DT, D, 1, kMax, kFrag>(lds, g, base, row_bytes, r0, r1, qb_n, epi);
+  stream_rows_from<DT, D, 1, kMax, kFrag>(lds, g, base, row_bytes, r0, r1, qb_n, epi, fdelta);
 }
 
 }  // namespace sieve

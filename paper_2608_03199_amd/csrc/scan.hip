@@ -277,6 +277,9 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
     const int nq = recT.nq;
     const int qb_n = (nq + 15) >> 4;
     const int64_t r0 = recT.r0, r1 = recT.r0 + recT.nrows;
+    // copy row minus store row of the tile's partition (fragment-order copy)
+    const int64_t fd =
+        D > 0 ? a.frag_offsets[recT.list] - a.list_offsets[recT.list] : (int64_t)0;
     // the next tile's items go to the other set
     if constexpr (!kShallow) put_items(nset, recN, itN);
     BItem itA;
@@ -418,7 +421,7 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
         }
         stream_rows_rega<DT, D, QB, kOcc == 1 ? 512 : 256, true>(qf, (const char*)a.vfrag,
                                                                   row_bytes, r0, r1, vote,
-                                                                  candidates);
+                                                                  candidates, fd);
         // The next tile's queries are staged after the stream, under the end
         // of this tile: an LDS-DMA load in flight during the stream makes the
         // compiler wait for every load there, not just the oldest ones.
@@ -456,7 +459,7 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
         recB = load_rec(tb);
       }
       stream_rows<DT, D, 8, kNT == kScanThreads ? 80 : 150, (D > 0)>(
-          buf, g, (const char*)(D > 0 ? a.vfrag : a.vectors), row_bytes, r0, r1, qb_n, epi);
+          buf, g, (const char*)(D > 0 ? a.vfrag : a.vectors), row_bytes, r0, r1, qb_n, epi, fd);
       if constexpr (kShallow) put_items(nset, recN, itN);  // staged at the next tile's start
     }
     if (lane == 0) s_wcnt[wv] = wcnt;
@@ -593,6 +596,7 @@ __global__ __launch_bounds__(kNT, kOcc) void scan_kernel(ScanArgs a) {
           hr->ex[m] = sex[i];
           if (m == 0) {
             hr->r0 = r0;
+            hr->fd = fd;
             hr->nrows = (int32_t)(r1 - r0);
             hr->nq = min(kHeavyQ, over_n - gi * kHeavyQ);
           }
@@ -892,7 +896,7 @@ __global__ __launch_bounds__(64) void scan_heavy_kernel(HeavyArgs a) {
         if (s_cnt[j] > kHeavyCap - 16) compact(j, false, 0);
     };
     stream_rows_qb<DT, D, 1, decltype(epi), 0, (D > 0)>(
-        lds, g, (const char*)(D > 0 ? a.vfrag : a.vectors), row_bytes, r0, r1, epi);
+        lds, g, (const char*)(D > 0 ? a.vfrag : a.vectors), row_bytes, r0, r1, epi, hr->fd);
 
     // each query's first k to the pool: one claim for the record
     int tot = 0;
@@ -1096,46 +1100,56 @@ int tile_rows(int dtype, int d) {
 
 namespace {
 // Fragment-order copy of the store (the layout FragStream reads): one thread
-// per 16-byte slot; slot (B nch + c) 64 + i + 16 s <- segment 4 c + s of row
-// 16 B + i, zeros past the last row or past the row's segments.
-__global__ __launch_bounds__(256) void vector_frag_kernel(const char* __restrict__ vectors,
-                                                          int64_t n, int32_t row_bytes,
-                                                          int32_t nch, u32x4* __restrict__ frag,
-                                                          int64_t nslots) {
+// per 16-byte slot; slot (B nch + c) 64 + i + 16 s <- segment 4 c + s of copy
+// row p = 16 B + i, which is row off[L] + (p - foff[L]) of partition L
+// (foff[L] <= p < foff[L + 1]), or a padding row (zeros) past the
+// partition's last row; zeros past the row's segments too.
+__global__ __launch_bounds__(256) void vector_frag_kernel(
+    const char* __restrict__ vectors, const int64_t* __restrict__ off,
+    const int64_t* __restrict__ foff, int32_t nlist, int32_t row_bytes, int32_t nch,
+    u32x4* __restrict__ frag, int64_t nslots) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nslots;
        i += (int64_t)gridDim.x * blockDim.x) {
     const int l = (int)(i & 63);
     const int64_t bc = i >> 6;  // B nch + c
     const int64_t blk = bc / nch;
     const int c = (int)(bc - blk * nch);
-    const int64_t row = blk * 16 + (l & 15);
+    const int64_t p = blk * 16 + (l & 15);
+    // partition of copy row p: the last L with foff[L] <= p
+    int lo = 0, hi = nlist;  // foff[lo] <= p < foff[hi]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (foff[mid] <= p) lo = mid; else hi = mid;
+    }
+    const int64_t k = p - foff[lo];
     const int seg = 4 * c + (l >> 4);
     u32x4 v = {0u, 0u, 0u, 0u};
-    if (row < n && seg * 16 < row_bytes)
-      v = *(const u32x4*)(vectors + row * row_bytes + (int64_t)seg * 16);
+    if (k < off[lo + 1] - off[lo] && seg * 16 < row_bytes)
+      v = *(const u32x4*)(vectors + (off[lo] + k) * row_bytes + (int64_t)seg * 16);
     frag[i] = v;
   }
 }
 }  // namespace
 
-size_t vector_frag_bytes(int dtype, int d, int64_t n) {
+size_t vector_frag_bytes(int dtype, int d, int64_t frag_rows) {
   const bool fixed = dtype == SIEVE_F32 ? (d == 64 || d == 128)
                                         : (d == 64 || d == 128 || d == 768);
-  if (!fixed || n <= 0) return 0;
+  if (!fixed || frag_rows <= 0) return 0;
   const int64_t row_bytes = (int64_t)d * (dtype == SIEVE_F32 ? 4 : 2);
-  return (size_t)((n + 15) / 16) * (size_t)((row_bytes + 63) / 64) * 1024;
+  return (size_t)((frag_rows + 15) / 16) * (size_t)((row_bytes + 63) / 64) * 1024;
 }
 
-hipError_t launch_vector_frag(int dtype, int d, const void* vectors, int64_t n, void* frag,
-                              hipStream_t s) {
-  const size_t bytes = vector_frag_bytes(dtype, d, n);
-  if (bytes == 0) return hipSuccess;
+hipError_t launch_vector_frag(int dtype, int d, const void* vectors, const int64_t* offsets,
+                              const int64_t* frag_offsets, int32_t nlist, int64_t frag_rows,
+                              void* frag, hipStream_t s) {
+  const size_t bytes = vector_frag_bytes(dtype, d, frag_rows);
+  if (bytes == 0 || nlist < 1) return hipSuccess;
   const int32_t row_bytes = d * (dtype == SIEVE_F32 ? 4 : 2);
   const int64_t nslots = (int64_t)(bytes / 16);
   const int64_t blocks = (nslots + 255) / 256;
   hipLaunchKernelGGL(vector_frag_kernel, dim3((unsigned)(blocks < (1 << 20) ? blocks : (1 << 20))),
-                     dim3(256), 0, s, (const char*)vectors, n, row_bytes,
-                     (int32_t)((row_bytes + 63) / 64), (u32x4*)frag, nslots);
+                     dim3(256), 0, s, (const char*)vectors, offsets, frag_offsets, nlist,
+                     row_bytes, (int32_t)((row_bytes + 63) / 64), (u32x4*)frag, nslots);
   return hipGetLastError();
 }
 

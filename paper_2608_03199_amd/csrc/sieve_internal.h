@@ -120,6 +120,7 @@ struct TileCand {
 constexpr int kHeavyQ = 16;
 struct HeavyRec {
   int64_t r0;     // first stored row
+  int64_t fd;     // its row in the fragment-order copy, less r0
   int32_t nrows;  // rows
   int32_t nq;     // queries in the record (1..kHeavyQ)
   int32_t q[kHeavyQ];
@@ -146,6 +147,7 @@ __host__ __device__ inline size_t arena_block_entries(int spill_cap) {
 struct ScanArgs {
   const void* vectors;         // [n, d] partition-major
   const void* vfrag;           // its fragment-order copy (compile-time dimensions)
+  const int64_t* frag_offsets; // [nlist + 1] first row of each partition in the copy
   const int64_t* list_offsets; // [nlist + 1]
   const int64_t* ids;          // [n]
   const void* queries;         // [nq, d]
@@ -218,13 +220,16 @@ int rank_prefix_cap(int32_t R, int32_t nlist);
 size_t centroid_frag_bytes(int dtype, int d, int32_t nlist);
 hipError_t launch_centroid_frag(const void* centroids, int32_t nlist, void* frag, hipStream_t s);
 // Fragment-order copy of the stored vectors, read by the scan kernels of
-// compile-time dimensions: for each 16-row block and 64-byte chunk of a row,
-// the 64 16-byte segments one MFMA fragment load takes, in lane order (the
-// layout is given with the reader, FragStream).  vector_frag_bytes is 0 for
+// compile-time dimensions: each partition padded to whole 16-row blocks
+// (frag_offsets: its first copy row, a multiple of 16), and for each 16-row
+// block and 64-byte chunk of a row the 64 16-byte segments one MFMA fragment
+// load takes, in lane order (the layout is given with the reader,
+// FragStream).  frag_rows = frag_offsets[nlist].  vector_frag_bytes is 0 for
 // dimensions the scan handles at run time (no copy).
-size_t vector_frag_bytes(int dtype, int d, int64_t n);
-hipError_t launch_vector_frag(int dtype, int d, const void* vectors, int64_t n, void* frag,
-                              hipStream_t s);
+size_t vector_frag_bytes(int dtype, int d, int64_t frag_rows);
+hipError_t launch_vector_frag(int dtype, int d, const void* vectors, const int64_t* offsets,
+                              const int64_t* frag_offsets, int32_t nlist, int64_t frag_rows,
+                              void* frag, hipStream_t s);
 // cfrag: the index's fragment-order centroids (centroid_frag_bytes > 0), or
 // null where it has none.
 hipError_t launch_rank_prefix(int dtype, const void* queries, int64_t q0, int32_t nqc,
