@@ -1023,7 +1023,7 @@ SIEVE_API int sieve_load_index(const void* vectors, int32_t dtype, int64_t n, in
       (err = hipMemcpyAsync(ix->offsets, list_offsets, sizeof(int64_t) * (nlist + 1), hipMemcpyDeviceToDevice, s)) != hipSuccess ||
       (n > 0 && (err = hipMemcpyAsync(ix->ids, ids, sizeof(int64_t) * n, hipMemcpyDeviceToDevice, s)) != hipSuccess) ||
       (err = hipMemcpyAsync(ix->centroids, centroids, cbytes, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
-      (fbytes && (err = launch_centroid_frag(ix->centroids, nlist, ix->cfrag, s)) != hipSuccess) ||
+      (fbytes && (err = launch_centroid_frag(dtype, d, ix->centroids, nlist, ix->cfrag, s)) != hipSuccess) ||
       (vfixed && (err = hipMemcpyAsync(ix->foff, hfoff.data(), sizeof(int64_t) * (nlist + 1),
                                         hipMemcpyHostToDevice, s)) != hipSuccess) ||
       (vfbytes && (err = launch_vector_frag(dtype, d, ix->vectors, ix->offsets, ix->foff, nlist,

@@ -42,8 +42,12 @@ constexpr int prefix_keep() {
 template <int DT, int D, int QB, int kNT>
 __device__ __forceinline__ void prefix_body(
     u32x4* lds, const RowGeom<DT>& g, const void* __restrict__ queries, int64_t q0, int qt0,
-    int nq, const void* __restrict__ centroids, int32_t nlist, int d, int32_t R, double cmax,
-    int32_t cap, unsigned long long* __restrict__ cand, float* s_lo, int32_t* s_cnt) {
+    int nq, const void* __restrict__ centroids, const char* __restrict__ cfrag, int32_t nlist,
+    int d, int32_t R, double cmax, int32_t cap, unsigned long long* __restrict__ cand,
+    float* s_lo, int32_t* s_cnt) {
+  // compile-time dimensions read the fragment-order centroid copy
+  constexpr bool kFrag = D > 0;
+  const char* crows = kFrag ? cfrag : (const char*)centroids;
   constexpr int kKeep = prefix_keep<kNT>();
   constexpr int kWaves = kNT / 64;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -74,8 +78,8 @@ __device__ __forceinline__ void prefix_body(
       }
     }
   };
-  stream_rows_qb<DT, D, QB, decltype(top2), 8 * QB>(lds, g, (const char*)centroids, row_bytes, 0,
-                                                    nlist, top2);
+  stream_rows_qb<DT, D, QB, decltype(top2), 8 * QB, kFrag>(lds, g, crows, row_bytes, 0, nlist,
+                                                           top2);
   __syncthreads();  // the staged queries are dead until re-staged below
 
   float* keep = (float*)lds;  // [QB * 16][kKeep]
@@ -157,15 +161,16 @@ __device__ __forceinline__ void prefix_body(
       }
     }
   };
-  stream_rows_qb<DT, D, QB, decltype(collect), 4 * QB>(lds, g, (const char*)centroids, row_bytes,
-                                                       0, nlist, collect);
+  stream_rows_qb<DT, D, QB, decltype(collect), 4 * QB, kFrag>(lds, g, crows, row_bytes, 0,
+                                                              nlist, collect);
 }
 
 template <int DT, int D, int kNT>
 __global__ __launch_bounds__(kNT, kNT == 256 ? 2 : 1) void rank_prefix_kernel(
     const void* __restrict__ queries, int64_t q0, int32_t nqc, const void* __restrict__ centroids,
-    int32_t nlist, int32_t dd, int32_t R, int32_t rows, double cmax, int32_t cap,
-    unsigned long long* __restrict__ cand, int32_t* __restrict__ ccount) {
+    const char* __restrict__ cfrag, int32_t nlist, int32_t dd, int32_t R, int32_t rows,
+    double cmax, int32_t cap, unsigned long long* __restrict__ cand,
+    int32_t* __restrict__ ccount) {
   extern __shared__ u32x4 lds[];
   __shared__ float s_lo[kPrefixRowsMax];
   __shared__ int32_t s_cnt[kPrefixRowsMax];
@@ -187,8 +192,8 @@ __global__ __launch_bounds__(kNT, kNT == 256 ? 2 : 1) void rank_prefix_kernel(
   constexpr int kLim = kNT == 256 ? kPrefixQB : kPrefixQBWide;
   constexpr int kQBMax = kCap < kLim ? kCap : kLim;
 #define SIEVE_BODY(QB)                                                                       \
-  prefix_body<DT, D, QB, kNT>(lds, g, queries, q0, qt0, nq, centroids, nlist, d, R, cmax, cap, \
-                              cand, s_lo, s_cnt)
+  prefix_body<DT, D, QB, kNT>(lds, g, queries, q0, qt0, nq, centroids, cfrag, nlist, d, R, cmax, \
+                              cap, cand, s_lo, s_cnt)
   switch (qb_n) {
     case 1: SIEVE_BODY(1); break;
     case 2: if constexpr (kQBMax >= 2) SIEVE_BODY(2); break;
@@ -489,20 +494,25 @@ __global__ __launch_bounds__(256) void rank_prefix_finish_kernel(
                              cmax, P + ql * ldp);
 }
 
-// Fragment-order copy of fp16 128-dimension centroids: one thread per
-// 16-byte slot (4 b + c) 64 + l <- row 16 b + l % 16, bytes 64 c + 16 (l / 16)
-// of the row (zeros past the last row).
+// Fragment-order copy of the centroids (the layout FragStream reads, one
+// partition): one thread per 16-byte slot; slot (B nch + c) 64 + i + 16 s <-
+// segment 4 c + s of centroid 16 B + i (zeros past the last centroid or past
+// the row's segments).
 __global__ __launch_bounds__(256) void centroid_frag_kernel(const char* __restrict__ centroids,
-                                                           int32_t nlist, u32x4* __restrict__ frag,
+                                                           int32_t nlist, int32_t row_bytes,
+                                                           int32_t nch, u32x4* __restrict__ frag,
                                                            int64_t nslots) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= nslots) return;
   const int l = (int)(i & 63);
-  const int64_t bc = i >> 6;  // 4 b + c
-  const int c = (int)(bc & 3);
-  const int64_t row = (bc >> 2) * 16 + (l & 15);
+  const int64_t bc = i >> 6;  // B nch + c
+  const int64_t blk = bc / nch;
+  const int c = (int)(bc - blk * nch);
+  const int64_t row = blk * 16 + (l & 15);
+  const int seg = 4 * c + (l >> 4);
   u32x4 v = {0u, 0u, 0u, 0u};
-  if (row < nlist) v = *(const u32x4*)(centroids + row * 256 + 64 * c + 16 * (l >> 4));
+  if (row < nlist && seg * 16 < row_bytes)
+    v = *(const u32x4*)(centroids + row * row_bytes + (int64_t)seg * 16);
   frag[i] = v;
 }
 
@@ -522,8 +532,9 @@ int prefix_rows(int d, bool wide) {
 
 template <int DT, int D, int kNT>
 hipError_t launch_prefix_k(const void* queries, int64_t q0, int32_t nqc, const void* centroids,
-                           int32_t nlist, int32_t d, int32_t R, double cmax, int32_t cap,
-                           unsigned long long* cand, int32_t* ccount, hipStream_t s) {
+                           const void* cfrag, int32_t nlist, int32_t d, int32_t R, double cmax,
+                           int32_t cap, unsigned long long* cand, int32_t* ccount, hipStream_t s) {
+  if (D > 0 && !cfrag) return hipErrorInvalidValue;
   static const hipError_t attr =
       hipFuncSetAttribute((const void*)rank_prefix_kernel<DT, D, kNT>,
                           hipFuncAttributeMaxDynamicSharedMemorySize, kMaxDynLds);
@@ -534,8 +545,8 @@ hipError_t launch_prefix_k(const void* queries, int64_t q0, int32_t nqc, const v
   if (keep > lds) lds = keep;
   if (lds > (size_t)kMaxDynLds) return hipErrorInvalidValue;
   hipLaunchKernelGGL((rank_prefix_kernel<DT, D, kNT>), dim3((unsigned)((nqc + rows - 1) / rows)),
-                     dim3(kNT), lds, s, queries, q0, nqc, centroids, nlist, d, R, rows, cmax, cap,
-                     cand, ccount);
+                     dim3(kNT), lds, s, queries, q0, nqc, centroids, (const char*)cfrag, nlist, d,
+                     R, rows, cmax, cap, cand, ccount);
   return hipGetLastError();
 }
 
@@ -543,14 +554,14 @@ hipError_t launch_prefix_k(const void* queries, int64_t q0, int32_t nqc, const v
 // of the centroids instead of 48.
 template <int DT, int D>
 hipError_t launch_prefix_t(const void* queries, int64_t q0, int32_t nqc, const void* centroids,
-                           int32_t nlist, int32_t d, int32_t R, double cmax, int32_t cap,
-                           unsigned long long* cand, int32_t* ccount, hipStream_t s) {
+                           const void* cfrag, int32_t nlist, int32_t d, int32_t R, double cmax,
+                           int32_t cap, unsigned long long* cand, int32_t* ccount, hipStream_t s) {
   if constexpr (DT == SIEVE_F16 && D == 768)
-    return launch_prefix_k<DT, D, kPrefixThreadsWide>(queries, q0, nqc, centroids, nlist, d, R,
-                                                      cmax, cap, cand, ccount, s);
+    return launch_prefix_k<DT, D, kPrefixThreadsWide>(queries, q0, nqc, centroids, cfrag, nlist,
+                                                      d, R, cmax, cap, cand, ccount, s);
   else
-    return launch_prefix_k<DT, D, 256>(queries, q0, nqc, centroids, nlist, d, R, cmax, cap, cand,
-                                       ccount, s);
+    return launch_prefix_k<DT, D, 256>(queries, q0, nqc, centroids, cfrag, nlist, d, R, cmax, cap,
+                                       cand, ccount, s);
 }
 
 template <int DT>
@@ -572,15 +583,25 @@ hipError_t launch_finish_t(const void* queries, int64_t q0, int32_t nqc, const v
 
 }  // namespace
 
+// The ranking kernels of compile-time dimensions (the register-query kernel
+// for fp16 128, the LDS-staged one for fp16 768 and fp32 64 / 128) read the
+// copy; the others read the row-major centroids.
 size_t centroid_frag_bytes(int dtype, int d, int32_t nlist) {
-  return dtype == SIEVE_F16 && d == 128 && nlist > 0 ? (size_t)((nlist + 15) / 16) * 4096 : 0;
+  const bool fixed = dtype == SIEVE_F32 ? (d == 64 || d == 128) : (d == 128 || d == 768);
+  if (!fixed || nlist <= 0) return 0;
+  const int64_t row_bytes = (int64_t)d * (dtype == SIEVE_F32 ? 4 : 2);
+  return (size_t)((nlist + 15) / 16) * (size_t)((row_bytes + 63) / 64) * 1024;
 }
 
-hipError_t launch_centroid_frag(const void* centroids, int32_t nlist, void* frag, hipStream_t s) {
-  const int64_t nslots = (int64_t)((nlist + 15) / 16) * 256;
-  if (nslots <= 0) return hipSuccess;
+hipError_t launch_centroid_frag(int dtype, int d, const void* centroids, int32_t nlist, void* frag,
+                                hipStream_t s) {
+  const size_t bytes = centroid_frag_bytes(dtype, d, nlist);
+  if (bytes == 0) return hipSuccess;
+  const int32_t row_bytes = d * (dtype == SIEVE_F32 ? 4 : 2);
+  const int64_t nslots = (int64_t)(bytes / 16);
   hipLaunchKernelGGL(centroid_frag_kernel, dim3((unsigned)((nslots + 255) / 256)), dim3(256), 0,
-                     s, (const char*)centroids, nlist, (u32x4*)frag, nslots);
+                     s, (const char*)centroids, nlist, row_bytes, (int32_t)((row_bytes + 63) / 64),
+                     (u32x4*)frag, nslots);
   return hipGetLastError();
 }
 
@@ -617,7 +638,8 @@ hipError_t launch_rank_prefix(int dtype, const void* queries, int64_t q0, int32_
                                       P, ldp, rc, s);
   }
 #define SIEVE_PREFIX(DT, D)                                                                  \
-  launch_prefix_t<DT, D>(queries, q0, nqc, centroids, nlist, d, R, cmax, cap, cand, ccount, s)
+  launch_prefix_t<DT, D>(queries, q0, nqc, centroids, cfrag, nlist, d, R, cmax, cap, cand, ccount, \
+                         s)
   if (dtype == SIEVE_F32) {
     e = d == 64 ? SIEVE_PREFIX(SIEVE_F32, 64)
                 : d == 128 ? SIEVE_PREFIX(SIEVE_F32, 128) : SIEVE_PREFIX(SIEVE_F32, 0);

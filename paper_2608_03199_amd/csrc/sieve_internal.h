@@ -211,14 +211,15 @@ size_t scan_lds_bytes(int dtype, int d, int rows);
 // nqc * rank_prefix_cap(R, nlist) keys and ccount nqc counts.
 constexpr int kRankPrefixMax = 64;
 int rank_prefix_cap(int32_t R, int32_t nlist);
-// Centroids in MFMA fragment order, for the register-query ranking kernel
-// (fp16, 128 dimensions): 16-row block b, 32-dimension chunk c and lane l
-// hold the 16 bytes at slot (4 b + c) 64 + l, taken from row 16 b + l % 16,
-// dimensions 32 c + 8 (l / 16) .. + 8 (zeros past the last row), so that a
-// wave's fragment load reads 1 KB of consecutive bytes.  frag_bytes is 0
-// where the kernel does not apply.
+// Centroids in MFMA fragment order, for the ranking kernels of compile-time
+// dimensions: 16-row block b, 64-byte chunk c of a row and lane l hold the 16
+// bytes at slot (b nch + c) 64 + l, taken from row 16 b + l % 16, segment
+// 4 c + l / 16 (zeros past the last row), so that a wave's fragment load
+// reads 1 KB of consecutive bytes (nch = 64-byte chunks per row; the layout
+// FragStream reads).  centroid_frag_bytes is 0 where no kernel reads a copy.
 size_t centroid_frag_bytes(int dtype, int d, int32_t nlist);
-hipError_t launch_centroid_frag(const void* centroids, int32_t nlist, void* frag, hipStream_t s);
+hipError_t launch_centroid_frag(int dtype, int d, const void* centroids, int32_t nlist, void* frag,
+                                hipStream_t s);
 // Fragment-order copy of the stored vectors, read by the scan kernels of
 // compile-time dimensions: each partition padded to whole 16-row blocks
 // (frag_offsets: its first copy row, a multiple of 16), and for each 16-row
