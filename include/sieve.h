@@ -137,8 +137,9 @@ typedef struct sieve_stats {
  * Device memory: the row-major copy of the vectors, and for the dimensions the
  * scan handles at compile time (fp16 64/128/768, fp32 64/128) a second copy in
  * MFMA fragment order (each list padded to whole 16-row blocks), about twice
- * the vectors' bytes in all; fp16 128-dim centroids get a fragment-order copy
- * too.  An allocation failure returns SIEVE_ENOMEM.
+ * the vectors' bytes in all; the centroids get a fragment-order copy too for
+ * the ranking kernels' compile-time dimensions (fp16 128/768, fp32 64/128).
+ * An allocation failure returns SIEVE_ENOMEM.
  * Synchronous: returns once the copies are complete.
  */
 SIEVE_API int sieve_load_index(const void* vectors, int32_t dtype, int64_t n, int32_t d,

@@ -363,6 +363,53 @@ def test_empty_lists_and_unbalanced_index():
         assert_parity(rep)
 
 
+@pytest.mark.parametrize("d,dtype", [(64, np.float16), (128, np.float16), (768, np.float16),
+                                     (64, np.float32), (128, np.float32)])
+def test_fragment_copy_with_ragged_partitions(d, dtype):
+    """Dimensions whose scan and ranking read the fragment-order copies: partitions of 0, 1,
+    15, 16, 17, 33 ... rows, so that padding rows sit between most partitions of the vector
+    copy and the centroid copy ends in a partial block.  Search, fixed probing and, with the
+    arena off (every tile with candidates takes the exact top-k pass, which reads the copy
+    from its overflow records), the oracle's result every way."""
+    rng = np.random.default_rng(11 + d)
+    sizes = np.array([0, 1, 15, 16, 17, 33, 0, 300, 5, 31, 48, 64, 129, 0, 2, 47, 90])
+    n, nlist = int(sizes.sum()), len(sizes)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    X = rng.standard_normal((n, d))
+    X[1::4] = X[0::4][: len(X[1::4])] + 0.02 * rng.standard_normal((len(X[1::4]), d))
+    X /= np.linalg.norm(X, axis=1, keepdims=True)
+    C = rng.standard_normal((nlist, d))
+    C /= np.linalg.norm(C, axis=1, keepdims=True)
+    X, C = X.astype(dtype), C.astype(dtype)
+    ids = rng.permutation(n).astype(np.int64) + 1000
+    qrows = rng.choice(n, 200, replace=False)
+    Q, ex = X[qrows].copy(), ids[qrows]
+    Xo, Co, Qo = X.astype(np.float32), C.astype(np.float32), Q.astype(np.float32)
+    ps = _lib()
+    dev = "cuda"
+    t = lambda a: torch.from_numpy(a).to(dev)
+    for arena in ("1", "0"):
+        os.environ["SIEVE_ARENA"] = arena  # read when a search sizes its workspace
+        ix = ps.Index(t(X), t(off), t(ids), t(C))
+        try:
+            for W, fixed in ((2, False), (0x7FFFFFFF, False), (None, True)):
+                if fixed:
+                    g = ix.search_fixed(t(Q), t(ex), 10, 0.9, 9, with_stats=True)
+                else:
+                    g = ix.search(t(Q), t(ex), 10, 0.9, W, 9, with_stats=True)
+                o = oracle.search(Xo, off, ids, Co, Qo, ex, 10, 0.9,
+                                  oracle.W_INF if fixed else W, 9)
+                rep = compare(g[0].cpu().numpy(), g[1].cpu().numpy(), g[2].cpu().numpy(), o)
+                print(f"[gpu-test] d={d} {np.dtype(dtype).name} arena={arena} W={W} "
+                      f"fixed={fixed} heavy={g[3].heavy_records} -> {rep}", flush=True)
+                assert_parity(rep)
+                if arena == "0" and g[3].hits > 0:
+                    assert g[3].heavy_records > 0
+        finally:
+            del os.environ["SIEVE_ARENA"]
+            ix.close()
+
+
 def test_low_threshold_pool_and_overflow_records_grow():
     """tau = -1: every scanned row qualifies.  With k = 64 and 32 probes per query the
     pool, though bounded by k entries per (query, tile), needs about 2M entries for 1,000
