@@ -368,9 +368,10 @@ def test_empty_lists_and_unbalanced_index():
 def test_fragment_copy_with_ragged_partitions(d, dtype):
     """Dimensions whose scan and ranking read the fragment-order copies: partitions of 0, 1,
     15, 16, 17, 33 ... rows, so that padding rows sit between most partitions of the vector
-    copy and the centroid copy ends in a partial block.  Search, fixed probing and, with the
-    arena off (every tile with candidates takes the exact top-k pass, which reads the copy
-    from its overflow records), the oracle's result every way."""
+    copy, and 17 centroids, so that the centroid copy ends in a partial block (the fused
+    ranking path, which reads it, is forced on the second pass).  Search, fixed probing and,
+    with the arena off (every tile with candidates takes the exact top-k pass, which reads
+    the copy from its overflow records), the oracle's result every way."""
     rng = np.random.default_rng(11 + d)
     sizes = np.array([0, 1, 15, 16, 17, 33, 0, 300, 5, 31, 48, 64, 129, 0, 2, 47, 90])
     n, nlist = int(sizes.sum()), len(sizes)
@@ -388,8 +389,10 @@ def test_fragment_copy_with_ragged_partitions(d, dtype):
     ps = _lib()
     dev = "cuda"
     t = lambda a: torch.from_numpy(a).to(dev)
-    for arena in ("1", "0"):
+    for arena, rank_path in (("1", None), ("0", "2")):
         os.environ["SIEVE_ARENA"] = arena  # read when a search sizes its workspace
+        if rank_path is not None:
+            os.environ["SIEVE_RANK_PATH"] = rank_path
         ix = ps.Index(t(X), t(off), t(ids), t(C))
         try:
             for W, fixed in ((2, False), (0x7FFFFFFF, False), (None, True)):
@@ -400,13 +403,15 @@ def test_fragment_copy_with_ragged_partitions(d, dtype):
                 o = oracle.search(Xo, off, ids, Co, Qo, ex, 10, 0.9,
                                   oracle.W_INF if fixed else W, 9)
                 rep = compare(g[0].cpu().numpy(), g[1].cpu().numpy(), g[2].cpu().numpy(), o)
-                print(f"[gpu-test] d={d} {np.dtype(dtype).name} arena={arena} W={W} "
+                print(f"[gpu-test] d={d} {np.dtype(dtype).name} arena={arena} "
+                      f"rank_path={rank_path} W={W} "
                       f"fixed={fixed} heavy={g[3].heavy_records} -> {rep}", flush=True)
                 assert_parity(rep)
                 if arena == "0" and g[3].hits > 0:
                     assert g[3].heavy_records > 0
         finally:
             del os.environ["SIEVE_ARENA"]
+            os.environ.pop("SIEVE_RANK_PATH", None)
             ix.close()
 
 
